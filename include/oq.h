@@ -1,0 +1,258 @@
+/*
+ * oq.h -- C ABI of liboq.so, the MI355X (gfx950) implementation of
+ * OmniQuant's block-wise calibration step (arXiv 2308.13137).
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are caller-owned, contiguous, row-major DEVICE pointers,
+ *     16-byte aligned.  Nothing is retained after a call returns.
+ *   - Every call is asynchronous on the given stream (NULL = the default
+ *     stream) and is stateless; calls on different streams may overlap.
+ *   - Output buffers are overwritten, never accumulated into.
+ *   - Results are deterministic: no atomics, fixed reduction orders; two
+ *     identical calls produce identical bytes.
+ *   - Arguments are validated before anything is launched.  On error nothing
+ *     is launched, the status says why and oq_last_error() (thread-local)
+ *     holds a readable detail string.  A failed HIP launch returns OQ_ERR_HIP.
+ *   - Optional pointers may be NULL: s = NULL means ones, delta = NULL
+ *     zeros, B = NULL no bias, any optional output NULL means "not wanted".
+ *   - Supported quantisation: bits in [2, 8] (weights) and [2, 8] or 16
+ *     (activations, 16 = not quantised); group g divides C_in and is a
+ *     power of two in [8, 512] or equal to C_in (per output channel);
+ *     C_in, T and every leading dimension are multiples of 8.
+ *   - Entry points that need scratch memory take a caller workspace and a
+ *     matching *_workspace_size query.
+ *
+ * Numerics fixed for all kernels (identical integer codes to any
+ * implementation that follows the same order): every named quantity is one
+ * IEEE fp32 rounding, no fused multiply-add, round half to even, correctly
+ * rounded division and square root; clip strengths are the fp64 sigmoid of
+ * their logits rounded once to fp32.  Quantiser, per group of g weights w~:
+ *     gamma = sigmoid(gamma_logit), beta = sigmoid(beta_logit)
+ *     a = gamma*max, b = beta*min, h = max((a - b)/(2^N - 1), 1e-5)
+ *     r = 1/h, z = -rint(b*r), code = clamp(rint(w~*r) + z, 0, 2^N - 1)
+ *     w_hat = (code - z)*h
+ * max/min ties resolve to the lowest index.  Backward passes use the
+ * straight-through estimator: only rint has derivative 1; clamp, max/min and
+ * the 1e-5 guard are differentiated exactly.
+ */
+#ifndef OQ_H
+#define OQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OQ_OK = 0,
+  OQ_ERR_INVALID_ARG = 1,   /* NULL required pointer, bad shape or stride  */
+  OQ_ERR_UNSUPPORTED = 2,   /* valid request outside the supported set     */
+  OQ_ERR_WORKSPACE = 3,     /* workspace NULL or smaller than the query    */
+  OQ_ERR_HIP = 4            /* a HIP call or launch failed                 */
+} oq_status;
+
+typedef enum { OQ_F32 = 0, OQ_BF16 = 1 } oq_dtype;
+
+const char* oq_status_str(oq_status s);
+const char* oq_last_error(void);
+int oq_version(void);
+
+/* ---------------------------------------------------------------------------
+ * Learnable weight clipping, forward (Sec. 3.2, Eq. 2).
+ *   W            [c_out, c_in] (w_dt)      frozen full-precision weight
+ *   s            [c_in] fp32 | NULL        LET scale: quantises W~ = s (.) W (Eq. 3)
+ *   gamma_logit,
+ *   beta_logit   [c_out, c_in/group] fp32  clip-strength logits, one pair per group;
+ *                                          a group is `group` consecutive input
+ *                                          channels of one output row
+ *   W_dq         [c_out, c_in] (dq_dt) | NULL   dequantised weight (code - z)*h
+ *   codes        [c_out, c_in] uint8 | NULL     integer codes in [0, 2^bits - 1]
+ *   h, z         [c_out, c_in/group] fp32 | NULL   step and (integer-valued) zero point
+ */
+oq_status oq_lwc_fakequant_fwd(const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                               const float* s, const float* gamma_logit, const float* beta_logit,
+                               int bits, int64_t group, void* W_dq, oq_dtype dq_dt,
+                               uint8_t* codes, float* h, float* z, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Learnable weight clipping, straight-through backward (Sec. 3.2, Eq. 2).
+ *   dW_dq          [c_out, c_in] fp32   dL/d(dequantised weight)
+ *   d_gamma_logit,
+ *   d_beta_logit   [c_out, c_in/group] fp32 (required)
+ *   d_s            [c_in] fp32 | NULL   weight-path part of dL/ds: sum_o dL/dW~[o,c] * W[o,c]
+ *   dW_tilde       [c_out, c_in] fp32 | NULL   dL/dW~ per element
+ * Workspace: oq_lwc_fakequant_bwd_workspace_size (0 bytes when d_s is NULL).
+ */
+oq_status oq_lwc_fakequant_bwd(const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                               const float* s, const float* gamma_logit, const float* beta_logit,
+                               int bits, int64_t group, const float* dW_dq,
+                               float* d_gamma_logit, float* d_beta_logit, float* d_s,
+                               float* dW_tilde, void* ws, size_t ws_bytes, hipStream_t stream);
+oq_status oq_lwc_fakequant_bwd_workspace_size(int64_t c_out, int64_t c_in, int64_t group,
+                                              int want_d_s, size_t* bytes);
+
+/* ---------------------------------------------------------------------------
+ * LET fold for a linear layer (Sec. 3.3, Eq. 3): W~ = s (.) W, B~ = B + delta W.
+ *   W [c_out, c_in] (w_dt); B [c_out] fp32 | NULL; s, delta [c_in] fp32 | NULL
+ *   W_tilde [c_out, c_in] (wt_dt) | NULL;  B_tilde [c_out] fp32 | NULL
+ * B~ sums over input channels in fp64 and rounds once.
+ */
+oq_status oq_let_fold(const void* W, oq_dtype w_dt, const float* B, int64_t c_out, int64_t c_in,
+                      const float* s, const float* delta, void* W_tilde, oq_dtype wt_dt,
+                      float* B_tilde, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Per-token activation fake-quant with the LET input transform (Eq. 3-4;
+ * Sec. 4.1: per-token asymmetric MinMax, i.e. Eq. 2 with gamma = beta = 1 on
+ * each token row of X~ = (X - delta) / s, evaluated as (x - delta) * (1/s)).
+ *   X      [T, C] (x_dt);  bits in [2,8], or 16 = no quantisation (X_dq = X~)
+ *   X_dq   [T, C] (dq_dt) | NULL;  codes [T, C] uint8 | NULL;  h, z [T] fp32 | NULL
+ */
+oq_status oq_act_fakequant_fwd(const void* X, oq_dtype x_dt, int64_t T, int64_t C, int bits,
+                               const float* s, const float* delta, void* X_dq, oq_dtype dq_dt,
+                               uint8_t* codes, float* h, float* z, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Straight-through backward of oq_act_fakequant_fwd.
+ *   dX_dq    [T, C] fp32          dL/dX^ (summed over every linear reading X^)
+ *   dX_tilde [T, C] fp32 | NULL   dL/dX~
+ *   d_s      [C] fp32 | NULL      input-path part of dL/ds    = -sum_t dL/dX~ * X~ / s
+ *   d_delta  [C] fp32 | NULL      input-path part of dL/ddelta = -sum_t dL/dX~ / s
+ * Workspace: oq_act_fakequant_bwd_workspace_size (0 bytes when d_s and d_delta are NULL).
+ */
+oq_status oq_act_fakequant_bwd(const void* X, oq_dtype x_dt, int64_t T, int64_t C, int bits,
+                               const float* s, const float* delta, const float* dX_dq,
+                               float* dX_tilde, float* d_s, float* d_delta,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
+oq_status oq_act_fakequant_bwd_workspace_size(int64_t T, int64_t C, size_t* bytes);
+
+/* ---------------------------------------------------------------------------
+ * LET initialisation (Sec. 4.1: scale from SmoothQuant, shift from Outlier
+ * Suppression+):  s_c = sqrt(max_t |X[t,c]|) / sqrt(max over the site's
+ * linears and rows of |W[o,c]|), each max floored at 1e-5;  delta_c =
+ * mean_t X[t,c] (fp64 sum).
+ *   X [T, C] (x_dt); W_site: HOST array of n_site device pointers to
+ *   [c_out_site[i], C] (w_dt) weights; s, delta [C] fp32 (outputs).
+ */
+oq_status oq_let_init(const void* X, oq_dtype x_dt, int64_t T, int64_t C,
+                      const void* const* W_site, const int64_t* c_out_site, int n_site,
+                      oq_dtype w_dt, float* s, float* delta, void* ws, size_t ws_bytes,
+                      hipStream_t stream);
+oq_status oq_let_init_workspace_size(int64_t T, int64_t C, const int64_t* c_out_site, int n_site,
+                                     size_t* bytes);
+
+/* ---------------------------------------------------------------------------
+ * Full-precision target of one linear (Algorithm 1, the fp block output that
+ * the quantised block is trained to match):  Y_T = W X^T + B, stored
+ * channel-major [c_out, T] (the layout the calibration step consumes).
+ *   X [T, c_in], W [c_out, c_in] (dt);  B [c_out] fp32 | NULL;  Y_T [c_out, T] (dt)
+ * dt = OQ_BF16: bf16 matrix cores, fp32 accumulation, one bf16 rounding.
+ */
+oq_status oq_fp_target(const void* X, const void* W, oq_dtype dt, const float* B, int64_t T,
+                       int64_t c_in, int64_t c_out, void* Y_T, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Plain matrix product C[M,N] = A[M,K] B[N,K]^T (both operands K-contiguous),
+ * the building block of every linear in the step.  in_dt = OQ_BF16: matrix
+ * cores with fp32 accumulation; OQ_F32: fp32 throughout.  C is out_dt.
+ */
+oq_status oq_matmul_nt(const void* A, const void* B, oq_dtype in_dt, int64_t M, int64_t N,
+                       int64_t K, void* C, oq_dtype out_dt, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * AdamW update (Sec. 4.1: AdamW, zero weight decay; lr 5e-3 for the clipping
+ * logits, 1e-2 for s and delta).  fp32, in place on p, m, v; step counts from 1.
+ *   p = p*(1 - lr*wd);  m = b1*m + (1-b1)*g;  v = b2*v + (1-b2)*g*g
+ *   p -= lr * (m / (1 - b1^step)) / (sqrt(v / (1 - b2^step)) + eps)
+ */
+oq_status oq_adamw_step(float* p, const float* g, float* m, float* v, int64_t n, float lr,
+                        float beta1, float beta2, float eps, float wd, int step,
+                        hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * One block-wise calibration step (Sec. 3.1 Eq. 1; Algorithm 1's inner loop
+ * body: LET, LWC, forward of the quantised linears on x_q, squared error to
+ * x_fp, straight-through backward, optional AdamW update).
+ *
+ * The block is its linear sub-graph: n_sites input tensors ("sites") and
+ * n_linears linears; linear l reads site lin_site[l].  Linears of one site
+ * must be consecutive.  LET (s, delta) applies per site; per-token
+ * activation fake-quant applies to a site's input when site_act_bits < 16.
+ * Loss = sum over linears of mean((Y_l - Y_fp,l)^2), Y_l = Q_a(X~) Q_w(W~)^T + B~.
+ */
+#define OQ_MAX_SITES 8
+#define OQ_MAX_LINEARS 16
+
+typedef struct {
+  int64_t tokens;                          /* T                                    */
+  int n_sites, n_linears;
+  oq_dtype dtype;                          /* OQ_BF16: bf16 X, W, Y_fp, bf16 MFMA;
+                                              OQ_F32: fp32 everywhere             */
+  int64_t site_width[OQ_MAX_SITES];        /* C of each site                       */
+  int site_let[OQ_MAX_SITES];              /* 1 = LET on this site                 */
+  int site_act_bits[OQ_MAX_SITES];         /* 2..8, or 16 = no activation quant    */
+  int lin_site[OQ_MAX_LINEARS];
+  int64_t lin_c_out[OQ_MAX_LINEARS];
+  int lin_bits[OQ_MAX_LINEARS];
+  int64_t lin_group[OQ_MAX_LINEARS];       /* group size along C_in (C_in = per channel) */
+} oq_block_desc;
+
+typedef struct {                           /* device pointers                      */
+  const void* W[OQ_MAX_LINEARS];           /* [c_out, C_site]                      */
+  const float* B[OQ_MAX_LINEARS];          /* [c_out] | NULL                       */
+  float* gamma_logit[OQ_MAX_LINEARS];      /* [c_out, C_site/group]                */
+  float* beta_logit[OQ_MAX_LINEARS];
+  float* s[OQ_MAX_SITES];                  /* [C_site], LET sites only             */
+  float* delta[OQ_MAX_SITES];
+} oq_block_params;
+
+typedef struct {                           /* device pointers, outputs             */
+  float* d_gamma_logit[OQ_MAX_LINEARS];    /* required                             */
+  float* d_beta_logit[OQ_MAX_LINEARS];     /* required                             */
+  float* d_s[OQ_MAX_SITES];                /* required on LET sites                */
+  float* d_delta[OQ_MAX_SITES];            /* required on LET sites                */
+  float* row_loss[OQ_MAX_LINEARS];         /* [c_out] | NULL: sum_t (Y - Y_fp)^2   */
+} oq_block_grads;
+
+typedef struct {                           /* AdamW state; NULL pointer = no update */
+  float* m_gamma[OQ_MAX_LINEARS]; float* v_gamma[OQ_MAX_LINEARS];
+  float* m_beta[OQ_MAX_LINEARS];  float* v_beta[OQ_MAX_LINEARS];
+  float* m_s[OQ_MAX_SITES];       float* v_s[OQ_MAX_SITES];
+  float* m_delta[OQ_MAX_SITES];   float* v_delta[OQ_MAX_SITES];
+  int step;                                /* 1-based step number of this update   */
+  float lr_lwc, lr_let, beta1, beta2, eps, wd;
+} oq_block_optim;
+
+oq_status oq_block_workspace_size(const oq_block_desc* desc, size_t* bytes);
+
+/*   Y_fp_T : HOST array [n_linears] of device pointers, each [c_out, T] (Y_fp
+ *            channel-major, as oq_fp_target writes it)
+ *   X_q    : HOST array [n_sites] of device pointers, each [T, C_site]
+ *   loss   : device float scalar (output)
+ *   optim  : NULL = gradients only; else AdamW updates gamma/beta logits and s/delta in place
+ */
+oq_status oq_block_calib_step(const oq_block_desc* desc, const void* const* Y_fp_T,
+                              const void* const* X_q, const oq_block_params* params,
+                              const oq_block_grads* grads, const oq_block_optim* optim,
+                              float* loss, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Kernel timing on the launching stream (HIP events around each launch).
+ * Kinds: 0 forward GEMM, 1 weight-gradient GEMM, 2 input-gradient GEMM,
+ * 3 LWC forward, 4 LWC backward, 5 activation quant forward, 6 activation
+ * quant backward, 7 transposes, 8 other.  oq_profile_read synchronises the
+ * recorded events and returns launch count, total milliseconds and the
+ * algorithmic work (FLOP for GEMMs, bytes for the others) of that kind.
+ */
+#define OQ_PROF_KINDS 9
+oq_status oq_profile_enable(int on);
+oq_status oq_profile_reset(void);
+oq_status oq_profile_read(int kind, int64_t* launches, double* total_ms, double* work);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* OQ_H */

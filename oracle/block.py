@@ -130,3 +130,14 @@ def block_step(desc, X_q, Y_fp, params, ft=np.float32):
         S[k]["dxt"] = dxt
     return loss, dict(d_gamma_logit=d_gl, d_beta_logit=d_bl, d_s=d_s, d_delta=d_delta,
                       row_loss=row_loss, fwd=(S, L))
+
+
+def fp_target(X, W, B=None, bf16=True):
+    """Full-precision output of one linear (Algorithm 1: the fp block output
+    the quantised block is trained to match): X W^T + B, fp64 sum, rounded
+    once to the storage type (bf16 or fp32).  Layout [T, C_out]."""
+    acc = np.asarray(X, np.float64) @ np.asarray(W, np.float64).T
+    if B is not None:
+        acc = acc + np.asarray(B, np.float64)[None, :]
+    y = acc.astype(np.float32)
+    return bf16_round(y) if bf16 else y

@@ -1,0 +1,715 @@
+// C ABI of liboq: argument validation, workspace carving, the launch sequence
+// of one calibration step and the optional per-kernel event timing.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <algorithm>
+#include <cmath>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "oq.h"
+#include "oq_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+oq_status fail(oq_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+#define OQ_HIP(expr, what)                                                            \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess) return fail(OQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e_)); \
+  } while (0)
+
+#define OQ_REQ(cond, ...)                                    \
+  do {                                                       \
+    if (!(cond)) return fail(OQ_ERR_INVALID_ARG, __VA_ARGS__); \
+  } while (0)
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool dtype_ok(oq_dtype d) { return d == OQ_F32 || d == OQ_BF16; }
+size_t esize(oq_dtype d) { return d == OQ_BF16 ? 2 : 4; }
+
+// ------------------------------------------------------------------ profiling
+struct ProfRec {
+  int kind;
+  hipEvent_t e0, e1;
+  double work;
+};
+std::mutex g_pm;
+std::vector<ProfRec> g_pending;
+bool g_prof_on = false;
+struct ProfAcc {
+  int64_t n = 0;
+  double ms = 0, work = 0;
+} g_acc[OQ_PROF_KINDS];
+
+void drain_pending() {
+  for (auto& r : g_pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.e1) == hipSuccess && hipEventElapsedTime(&ms, r.e0, r.e1) == hipSuccess) {
+      g_acc[r.kind].n += 1;
+      g_acc[r.kind].ms += ms;
+      g_acc[r.kind].work += r.work;
+    }
+    (void)hipEventDestroy(r.e0);
+    (void)hipEventDestroy(r.e1);
+  }
+  g_pending.clear();
+}
+
+// ------------------------------------------------------------------ workspace carving
+struct Carver {
+  char* base;
+  size_t off = 0;
+  template <class T>
+  T* take(size_t count) {
+    off = (off + 255) & ~size_t(255);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+}  // namespace
+
+namespace oq {
+ProfScope::ProfScope(int k, hipStream_t s, double w) : kind(k), stream(s), work(w), on(g_prof_on) {
+  if (on) {
+    on = hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess &&
+         hipEventRecord(e0, s) == hipSuccess;
+  }
+}
+ProfScope::~ProfScope() {
+  if (!on) return;
+  (void)hipEventRecord(e1, stream);
+  std::lock_guard<std::mutex> lk(g_pm);
+  g_pending.push_back({kind, e0, e1, work});
+}
+}  // namespace oq
+
+using namespace oq;
+
+extern "C" {
+
+const char* oq_status_str(oq_status s) {
+  switch (s) {
+    case OQ_OK: return "OQ_OK";
+    case OQ_ERR_INVALID_ARG: return "OQ_ERR_INVALID_ARG";
+    case OQ_ERR_UNSUPPORTED: return "OQ_ERR_UNSUPPORTED";
+    case OQ_ERR_WORKSPACE: return "OQ_ERR_WORKSPACE";
+    case OQ_ERR_HIP: return "OQ_ERR_HIP";
+  }
+  return "OQ_ERR_UNKNOWN";
+}
+
+const char* oq_last_error(void) { return g_err.c_str(); }
+int oq_version(void) { return 1; }
+
+oq_status oq_profile_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_pm);
+  g_prof_on = on != 0;
+  return OQ_OK;
+}
+
+oq_status oq_profile_reset(void) {
+  std::lock_guard<std::mutex> lk(g_pm);
+  drain_pending();
+  for (auto& a : g_acc) a = ProfAcc{};
+  return OQ_OK;
+}
+
+oq_status oq_profile_read(int kind, int64_t* launches, double* total_ms, double* work) {
+  if (kind < 0 || kind >= OQ_PROF_KINDS) return fail(OQ_ERR_INVALID_ARG, "profile kind %d", kind);
+  std::lock_guard<std::mutex> lk(g_pm);
+  drain_pending();
+  if (launches) *launches = g_acc[kind].n;
+  if (total_ms) *total_ms = g_acc[kind].ms;
+  if (work) *work = g_acc[kind].work;
+  return OQ_OK;
+}
+
+// ------------------------------------------------------------------ quantisers
+static oq_status check_lwc(const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                           const float* gl, const float* bl, int bits, int64_t group) {
+  OQ_REQ(W && gl && bl, "W, gamma_logit and beta_logit are required");
+  OQ_REQ(dtype_ok(w_dt), "bad weight dtype %d", int(w_dt));
+  OQ_REQ(c_out >= 0 && c_in > 0, "bad shape c_out=%lld c_in=%lld", (long long)c_out, (long long)c_in);
+  OQ_REQ(c_in % 8 == 0, "c_in=%lld must be a multiple of 8", (long long)c_in);
+  OQ_REQ(aligned16(W), "W must be 16-byte aligned");
+  if (bits < 2 || bits > 8) return fail(OQ_ERR_UNSUPPORTED, "bits=%d outside [2, 8]", bits);
+  if (group <= 0 || c_in % group)
+    return fail(OQ_ERR_INVALID_ARG, "group=%lld must divide c_in=%lld", (long long)group, (long long)c_in);
+  if (!quant_shape_supported(c_in, group))
+    return fail(OQ_ERR_UNSUPPORTED,
+                "group=%lld with c_in=%lld: need a power of two in [8, 512] or group == c_in "
+                "(c_in <= 32768)",
+                (long long)group, (long long)c_in);
+  return OQ_OK;
+}
+
+oq_status oq_lwc_fakequant_fwd(const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                               const float* s, const float* gamma_logit, const float* beta_logit,
+                               int bits, int64_t group, void* W_dq, oq_dtype dq_dt,
+                               uint8_t* codes, float* h, float* z, hipStream_t stream) {
+  oq_status e = check_lwc(W, w_dt, c_out, c_in, gamma_logit, beta_logit, bits, group);
+  if (e != OQ_OK) return e;
+  OQ_REQ(!W_dq || dtype_ok(dq_dt), "bad W_dq dtype");
+  OQ_REQ(!W_dq || aligned16(W_dq), "W_dq must be 16-byte aligned");
+  OQ_REQ(!codes || (reinterpret_cast<uintptr_t>(codes) & 7u) == 0, "codes must be 8-byte aligned");
+  OQ_REQ(!s || aligned16(s), "s must be 16-byte aligned");
+  ProfScope ps(PK_LWC_FWD, stream,
+               double(c_out) * c_in * (esize(w_dt) + (W_dq ? esize(dq_dt) : 0) + (codes ? 1 : 0)));
+  OQ_HIP(lwc_fwd(W, w_dt == OQ_BF16, c_out, c_in, s, gamma_logit, beta_logit, bits, group, W_dq,
+                 dq_dt == OQ_BF16, codes, h, z, stream),
+         "lwc_fwd");
+  return OQ_OK;
+}
+
+oq_status oq_lwc_fakequant_bwd_workspace_size(int64_t c_out, int64_t c_in, int64_t group,
+                                              int want_d_s, size_t* bytes) {
+  (void)group;
+  OQ_REQ(bytes, "bytes is required");
+  *bytes = want_d_s ? size_t(lwc_bwd_nparts(c_out)) * size_t(c_in) * 4 + 256 : 0;
+  return OQ_OK;
+}
+
+oq_status oq_lwc_fakequant_bwd(const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                               const float* s, const float* gamma_logit, const float* beta_logit,
+                               int bits, int64_t group, const float* dW_dq,
+                               float* d_gamma_logit, float* d_beta_logit, float* d_s,
+                               float* dW_tilde, void* ws, size_t ws_bytes, hipStream_t stream) {
+  oq_status e = check_lwc(W, w_dt, c_out, c_in, gamma_logit, beta_logit, bits, group);
+  if (e != OQ_OK) return e;
+  OQ_REQ(dW_dq && d_gamma_logit && d_beta_logit, "dW_dq, d_gamma_logit, d_beta_logit are required");
+  OQ_REQ(aligned16(dW_dq) && (!dW_tilde || aligned16(dW_tilde)), "dW_dq/dW_tilde must be 16-byte aligned");
+  size_t need = 0;
+  oq_lwc_fakequant_bwd_workspace_size(c_out, c_in, group, d_s != nullptr, &need);
+  if (need && (!ws || ws_bytes < need))
+    return fail(OQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  Carver cv{static_cast<char*>(ws)};
+  float* parts = d_s ? cv.take<float>(size_t(lwc_bwd_nparts(c_out)) * c_in) : nullptr;
+  {
+    ProfScope ps(PK_LWC_BWD, stream, double(c_out) * c_in * (esize(w_dt) + 4 + (dW_tilde ? 4 : 0)));
+    OQ_HIP(lwc_bwd(W, w_dt == OQ_BF16, c_out, c_in, s, gamma_logit, beta_logit, bits, group, dW_dq,
+                   d_gamma_logit, d_beta_logit, dW_tilde, parts, stream),
+           "lwc_bwd");
+  }
+  if (d_s) {
+    ProfScope ps(PK_OTHER, stream, 0);
+    OQ_HIP(let_grad_finish(c_in, nullptr, parts, lwc_bwd_nparts(c_out), nullptr, nullptr, 0,
+                           nullptr, 0, d_s, nullptr, stream),
+           "ds finish");
+  }
+  return OQ_OK;
+}
+
+oq_status oq_let_fold(const void* W, oq_dtype w_dt, const float* B, int64_t c_out, int64_t c_in,
+                      const float* s, const float* delta, void* W_tilde, oq_dtype wt_dt,
+                      float* B_tilde, hipStream_t stream) {
+  OQ_REQ(W, "W is required");
+  OQ_REQ(dtype_ok(w_dt) && (!W_tilde || dtype_ok(wt_dt)), "bad dtype");
+  OQ_REQ(c_out >= 0 && c_in > 0 && c_in % 8 == 0, "bad shape");
+  OQ_REQ(aligned16(W) && (!W_tilde || aligned16(W_tilde)) && (!s || aligned16(s)) &&
+             (!delta || aligned16(delta)),
+         "pointers must be 16-byte aligned");
+  ProfScope ps(PK_OTHER, stream, double(c_out) * c_in * (esize(w_dt) + (W_tilde ? esize(wt_dt) : 0)));
+  OQ_HIP(let_fold(W, w_dt == OQ_BF16, B, c_out, c_in, s, delta, W_tilde, wt_dt == OQ_BF16, B_tilde,
+                  stream),
+         "let_fold");
+  return OQ_OK;
+}
+
+static oq_status check_act(const void* X, oq_dtype x_dt, int64_t T, int64_t C, int bits,
+                           const float* s, const float* delta) {
+  OQ_REQ(X, "X is required");
+  OQ_REQ(dtype_ok(x_dt), "bad dtype");
+  OQ_REQ(T >= 0 && C > 0 && C % 8 == 0, "bad shape T=%lld C=%lld", (long long)T, (long long)C);
+  OQ_REQ(aligned16(X) && (!s || aligned16(s)) && (!delta || aligned16(delta)),
+         "pointers must be 16-byte aligned");
+  if (!(bits == 16 || (bits >= 2 && bits <= 8)))
+    return fail(OQ_ERR_UNSUPPORTED, "activation bits=%d (need 2..8 or 16)", bits);
+  if (C > 32768) return fail(OQ_ERR_UNSUPPORTED, "C=%lld > 32768", (long long)C);
+  return OQ_OK;
+}
+
+oq_status oq_act_fakequant_fwd(const void* X, oq_dtype x_dt, int64_t T, int64_t C, int bits,
+                               const float* s, const float* delta, void* X_dq, oq_dtype dq_dt,
+                               uint8_t* codes, float* h, float* z, hipStream_t stream) {
+  oq_status e = check_act(X, x_dt, T, C, bits, s, delta);
+  if (e != OQ_OK) return e;
+  OQ_REQ(!X_dq || (dtype_ok(dq_dt) && aligned16(X_dq)), "bad X_dq");
+  OQ_REQ(!codes || (reinterpret_cast<uintptr_t>(codes) & 7u) == 0, "codes must be 8-byte aligned");
+  OQ_REQ(!codes || bits < 16, "codes need bits < 16");
+  ProfScope ps(PK_ACT_FWD, stream,
+               double(T) * C * (esize(x_dt) + (X_dq ? esize(dq_dt) : 0) + (codes ? 1 : 0)));
+  OQ_HIP(act_fwd(X, x_dt == OQ_BF16, T, C, bits, s, delta, X_dq, dq_dt == OQ_BF16, codes, h, z,
+                 stream),
+         "act_fwd");
+  return OQ_OK;
+}
+
+oq_status oq_act_fakequant_bwd_workspace_size(int64_t T, int64_t C, size_t* bytes) {
+  OQ_REQ(bytes, "bytes is required");
+  *bytes = 2 * (size_t(act_bwd_nparts(T)) * size_t(C) * 4 + 256);
+  return OQ_OK;
+}
+
+oq_status oq_act_fakequant_bwd(const void* X, oq_dtype x_dt, int64_t T, int64_t C, int bits,
+                               const float* s, const float* delta, const float* dX_dq,
+                               float* dX_tilde, float* d_s, float* d_delta, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  oq_status e = check_act(X, x_dt, T, C, bits, s, delta);
+  if (e != OQ_OK) return e;
+  OQ_REQ(dX_dq && aligned16(dX_dq), "dX_dq is required and 16-byte aligned");
+  OQ_REQ(!dX_tilde || aligned16(dX_tilde), "dX_tilde must be 16-byte aligned");
+  const bool parts = d_s || d_delta;
+  size_t need = 0;
+  if (parts) oq_act_fakequant_bwd_workspace_size(T, C, &need);
+  if (need && (!ws || ws_bytes < need))
+    return fail(OQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  Carver cv{static_cast<char*>(ws)};
+  const int64_t np = act_bwd_nparts(T);
+  float* psx = parts ? cv.take<float>(size_t(np) * C) : nullptr;
+  float* ps1 = parts ? cv.take<float>(size_t(np) * C) : nullptr;
+  {
+    ProfScope ps(PK_ACT_BWD, stream, double(T) * C * (esize(x_dt) + 4 + (dX_tilde ? 4 : 0)));
+    OQ_HIP(act_bwd(X, x_dt == OQ_BF16, T, C, bits, s, delta, dX_dq, dX_tilde, psx, ps1, stream),
+           "act_bwd");
+  }
+  if (parts) {
+    ProfScope ps(PK_OTHER, stream, 0);
+    OQ_HIP(let_grad_finish(C, s, nullptr, 0, psx, ps1, np, nullptr, 0, d_s, d_delta, stream),
+           "act finish");
+  }
+  return OQ_OK;
+}
+
+static size_t let_init_ws(int64_t T, int64_t C, const int64_t* c_out_site, int n_site) {
+  size_t naw = 0;
+  for (int i = 0; i < n_site; ++i) naw += size_t(colstat_nparts(c_out_site[i]));
+  return size_t(colstat_nparts(T)) * C * 12 + naw * C * 4 + 3 * 256;
+}
+
+oq_status oq_let_init_workspace_size(int64_t T, int64_t C, const int64_t* c_out_site, int n_site,
+                                     size_t* bytes) {
+  OQ_REQ(bytes && c_out_site, "bytes and c_out_site are required");
+  OQ_REQ(n_site >= 1 && n_site <= OQ_MAX_LINEARS, "n_site=%d", n_site);
+  *bytes = let_init_ws(T, C, c_out_site, n_site);
+  return OQ_OK;
+}
+
+oq_status oq_let_init(const void* X, oq_dtype x_dt, int64_t T, int64_t C,
+                      const void* const* W_site, const int64_t* c_out_site, int n_site,
+                      oq_dtype w_dt, float* s, float* delta, void* ws, size_t ws_bytes,
+                      hipStream_t stream) {
+  OQ_REQ(X && W_site && c_out_site && s && delta, "X, W_site, c_out_site, s, delta are required");
+  OQ_REQ(n_site >= 1 && n_site <= OQ_MAX_LINEARS, "n_site=%d", n_site);
+  OQ_REQ(dtype_ok(x_dt) && dtype_ok(w_dt), "bad dtype");
+  OQ_REQ(T > 0 && C > 0 && C % 8 == 0, "bad shape");
+  OQ_REQ(aligned16(X), "X must be 16-byte aligned");
+  int64_t naw = 0;
+  for (int i = 0; i < n_site; ++i) {
+    OQ_REQ(W_site[i] && aligned16(W_site[i]) && c_out_site[i] > 0, "bad site weight %d", i);
+    naw += colstat_nparts(c_out_site[i]);
+  }
+  const size_t need = let_init_ws(T, C, c_out_site, n_site);
+  if (!ws || ws_bytes < need)
+    return fail(OQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  Carver cv{static_cast<char*>(ws)};
+  const int64_t nax = colstat_nparts(T);
+  float* ax = cv.take<float>(size_t(nax) * C);
+  double* sm = cv.take<double>(size_t(nax) * C);
+  float* aw = cv.take<float>(size_t(naw) * C);
+  ProfScope ps(PK_OTHER, stream, double(T) * C * esize(x_dt));
+  OQ_HIP(colstat(X, x_dt == OQ_BF16, T, C, ax, sm, stream), "colstat X");
+  int64_t off = 0;
+  for (int i = 0; i < n_site; ++i) {
+    OQ_HIP(colstat(W_site[i], w_dt == OQ_BF16, c_out_site[i], C, aw + off * C, nullptr, stream),
+           "colstat W");
+    off += colstat_nparts(c_out_site[i]);
+  }
+  OQ_HIP(let_init_finish(C, T, ax, nax, sm, aw, naw, s, delta, stream), "let_init_finish");
+  return OQ_OK;
+}
+
+oq_status oq_fp_target(const void* X, const void* W, oq_dtype dt, const float* B, int64_t T,
+                       int64_t c_in, int64_t c_out, void* Y_T, hipStream_t stream) {
+  OQ_REQ(X && W && Y_T, "X, W, Y_T are required");
+  OQ_REQ(dtype_ok(dt), "bad dtype");
+  OQ_REQ(T >= 0 && c_out >= 0 && c_in > 0 && c_in % 8 == 0, "bad shape");
+  OQ_REQ(aligned16(X) && aligned16(W), "X and W must be 16-byte aligned");
+  ProfScope ps(PK_OTHER, stream, 2.0 * double(T) * c_in * c_out);
+  OQ_HIP(gemm_nt_store(W, X, dt == OQ_BF16, c_out, T, c_in, c_in, c_in, Y_T, dt == OQ_BF16, T, B,
+                       stream),
+         "fp_target");
+  return OQ_OK;
+}
+
+oq_status oq_matmul_nt(const void* A, const void* B, oq_dtype in_dt, int64_t M, int64_t N,
+                       int64_t K, void* C, oq_dtype out_dt, hipStream_t stream) {
+  OQ_REQ(A && B && C, "A, B, C are required");
+  OQ_REQ(dtype_ok(in_dt) && dtype_ok(out_dt), "bad dtype");
+  OQ_REQ(M >= 0 && N >= 0 && K >= 0 && K % 8 == 0, "bad shape (K must be a multiple of 8)");
+  OQ_REQ(aligned16(A) && aligned16(B), "A and B must be 16-byte aligned");
+  ProfScope ps(PK_OTHER, stream, 2.0 * double(M) * N * K);
+  if (out_dt == OQ_F32)
+    OQ_HIP(gemm_nt_f32out(A, B, in_dt == OQ_BF16, M, N, K, K, K, static_cast<float*>(C), N, stream),
+           "matmul");
+  else
+    OQ_HIP(gemm_nt_store(A, B, in_dt == OQ_BF16, M, N, K, K, K, C, true, N, nullptr, stream),
+           "matmul");
+  return OQ_OK;
+}
+
+oq_status oq_adamw_step(float* p, const float* g, float* m, float* v, int64_t n, float lr,
+                        float beta1, float beta2, float eps, float wd, int step,
+                        hipStream_t stream) {
+  OQ_REQ(p && g && m && v, "p, g, m, v are required");
+  OQ_REQ(n >= 0 && step >= 1, "bad n or step");
+  const float bc1 = float(1.0 - std::pow(double(beta1), step));
+  const float bc2 = float(1.0 - std::pow(double(beta2), step));
+  ProfScope ps(PK_OTHER, stream, double(n) * 28);
+  OQ_HIP(adamw(p, g, m, v, n, lr, beta1, beta2, eps, wd, bc1, bc2, stream), "adamw");
+  return OQ_OK;
+}
+
+// ------------------------------------------------------------------ block step
+namespace {
+
+struct SitePlan {
+  int k, l0, l1;
+  int64_t C, M;
+  bool let, act;
+};
+
+struct BlockWs {
+  void *what, *xhat, *xhatT, *dyT, *dy, *whatT;
+  float *dW, *dX, *psq, *pdy, *dbt, *bt, *pw, *psx, *ps1, *pb;
+  double* rl;
+};
+
+oq_status plan_block(const oq_block_desc* d, std::vector<SitePlan>& plan) {
+  OQ_REQ(d, "desc is required");
+  OQ_REQ(d->n_sites >= 1 && d->n_sites <= OQ_MAX_SITES, "n_sites=%d", d->n_sites);
+  OQ_REQ(d->n_linears >= 1 && d->n_linears <= OQ_MAX_LINEARS, "n_linears=%d", d->n_linears);
+  OQ_REQ(dtype_ok(d->dtype), "bad dtype");
+  OQ_REQ(d->tokens > 0 && d->tokens % 8 == 0, "tokens=%lld must be a positive multiple of 8",
+         (long long)d->tokens);
+  plan.clear();
+  int prev_site = -1;
+  for (int l = 0; l < d->n_linears; ++l) {
+    const int k = d->lin_site[l];
+    OQ_REQ(k >= 0 && k < d->n_sites, "linear %d: site %d out of range", l, k);
+    OQ_REQ(k >= prev_site, "linears of one site must be consecutive (linear %d)", l);
+    OQ_REQ(d->lin_c_out[l] > 0 && d->lin_c_out[l] % 8 == 0, "linear %d: c_out must be a positive multiple of 8", l);
+    if (k != prev_site) {
+      for (auto& p : plan) OQ_REQ(p.k != k, "linears of site %d are not consecutive", k);
+      const int64_t C = d->site_width[k];
+      OQ_REQ(C > 0 && C % 8 == 0, "site %d: width must be a positive multiple of 8", k);
+      const int ab = d->site_act_bits[k];
+      if (!(ab == 16 || (ab >= 2 && ab <= 8)))
+        return fail(OQ_ERR_UNSUPPORTED, "site %d: activation bits %d", k, ab);
+      if (C > 32768) return fail(OQ_ERR_UNSUPPORTED, "site %d: width %lld > 32768", k, (long long)C);
+      plan.push_back(SitePlan{k, l, l + 1, C, 0, d->site_let[k] != 0, ab < 16});
+      prev_site = k;
+    } else {
+      plan.back().l1 = l + 1;
+    }
+    SitePlan& sp = plan.back();
+    sp.M += d->lin_c_out[l];
+    if (sp.l1 - sp.l0 > MAX_SEG)
+      return fail(OQ_ERR_UNSUPPORTED, "site %d has more than %d linears", k, MAX_SEG);
+    if (d->lin_bits[l] < 2 || d->lin_bits[l] > 8)
+      return fail(OQ_ERR_UNSUPPORTED, "linear %d: bits %d", l, d->lin_bits[l]);
+    if (d->lin_group[l] <= 0 || sp.C % d->lin_group[l])
+      return fail(OQ_ERR_INVALID_ARG, "linear %d: group %lld does not divide %lld", l,
+                  (long long)d->lin_group[l], (long long)sp.C);
+    if (!quant_shape_supported(sp.C, d->lin_group[l]))
+      return fail(OQ_ERR_UNSUPPORTED, "linear %d: group %lld unsupported for width %lld", l,
+                  (long long)d->lin_group[l], (long long)sp.C);
+  }
+  return OQ_OK;
+}
+
+size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, char* base,
+                   BlockWs* w) {
+  const bool bf = d->dtype == OQ_BF16;
+  const size_t es = bf ? 2 : 4;
+  const int64_t T = d->tokens;
+  const int ptn = gemm_part_tile_n(bf);
+  const int64_t ntn = (T + ptn - 1) / ptn;
+  size_t what = 0, xhat = 0, xhatT = 0, dyT = 0, dy = 0, whatT = 0, dW = 0, dX = 0, parts = 0,
+         rows = 0, pw = 0, pa = 0, pb = 0;
+  int64_t mtot = 0;
+  for (const auto& p : plan) {
+    what = std::max(what, size_t(p.M * p.C));
+    xhatT = std::max(xhatT, size_t(T * p.C));
+    dyT = std::max(dyT, size_t(p.M * T));
+    dW = std::max(dW, size_t(p.M * p.C));
+    parts = std::max(parts, size_t(p.M * ntn));
+    rows = std::max(rows, size_t(p.M));
+    mtot += p.M;
+    if (p.let || p.act) xhat = std::max(xhat, size_t(T * p.C));
+    if (p.let) {
+      dy = std::max(dy, size_t(p.M * T));
+      whatT = std::max(whatT, size_t(p.M * p.C));
+      dX = std::max(dX, size_t(T * p.C));
+      pa = std::max(pa, size_t(act_bwd_nparts(T) * p.C));
+      size_t a = 0, b = 0;
+      for (int l = p.l0; l < p.l1; ++l) {
+        a += size_t(lwc_bwd_nparts(d->lin_c_out[l]));
+        b += size_t(wcolsum_nparts(d->lin_c_out[l]));
+      }
+      pw = std::max(pw, a * p.C);
+      pb = std::max(pb, b * p.C);
+    }
+  }
+  Carver cv{base};
+  BlockWs t{};
+  t.what = cv.take<char>(what * es);
+  t.xhat = xhat ? cv.take<char>(xhat * es) : nullptr;
+  t.xhatT = cv.take<char>(xhatT * es);
+  t.dyT = cv.take<char>(dyT * es);
+  t.dy = dy ? cv.take<char>(dy * es) : nullptr;
+  t.whatT = whatT ? cv.take<char>(whatT * es) : nullptr;
+  t.dW = cv.take<float>(dW);
+  t.dX = dX ? cv.take<float>(dX) : nullptr;
+  t.psq = cv.take<float>(parts);
+  t.pdy = cv.take<float>(parts);
+  t.dbt = cv.take<float>(rows);
+  t.bt = cv.take<float>(rows);
+  t.pw = pw ? cv.take<float>(pw) : nullptr;
+  t.psx = pa ? cv.take<float>(pa) : nullptr;
+  t.ps1 = pa ? cv.take<float>(pa) : nullptr;
+  t.pb = pb ? cv.take<float>(pb) : nullptr;
+  t.rl = cv.take<double>(size_t(mtot));
+  if (w) *w = t;
+  return cv.off + 256;
+}
+
+}  // namespace
+
+oq_status oq_block_workspace_size(const oq_block_desc* desc, size_t* bytes) {
+  OQ_REQ(bytes, "bytes is required");
+  std::vector<SitePlan> plan;
+  oq_status e = plan_block(desc, plan);
+  if (e != OQ_OK) return e;
+  *bytes = carve_block(desc, plan, nullptr, nullptr);
+  return OQ_OK;
+}
+
+oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
+                              const void* const* X_q, const oq_block_params* prm,
+                              const oq_block_grads* gr, const oq_block_optim* opt, float* loss,
+                              void* ws, size_t ws_bytes, hipStream_t st) {
+  std::vector<SitePlan> plan;
+  oq_status e = plan_block(d, plan);
+  if (e != OQ_OK) return e;
+  OQ_REQ(Y_fp_T && X_q && prm && gr && loss, "Y_fp_T, X_q, params, grads, loss are required");
+  for (const auto& p : plan) {
+    OQ_REQ(X_q[p.k] && aligned16(X_q[p.k]), "X_q[%d] missing or misaligned", p.k);
+    if (p.let) {
+      OQ_REQ(prm->s[p.k] && prm->delta[p.k] && aligned16(prm->s[p.k]) && aligned16(prm->delta[p.k]),
+             "site %d: LET needs 16-byte aligned s and delta", p.k);
+      OQ_REQ(gr->d_s[p.k] && gr->d_delta[p.k], "site %d: d_s and d_delta are required", p.k);
+    }
+  }
+  for (int l = 0; l < d->n_linears; ++l) {
+    OQ_REQ(prm->W[l] && aligned16(prm->W[l]), "W[%d] missing or misaligned", l);
+    OQ_REQ(prm->gamma_logit[l] && prm->beta_logit[l], "logits of linear %d missing", l);
+    OQ_REQ(gr->d_gamma_logit[l] && gr->d_beta_logit[l], "gradients of linear %d missing", l);
+    OQ_REQ(Y_fp_T[l], "Y_fp_T[%d] missing", l);
+  }
+  if (opt) {
+    OQ_REQ(opt->step >= 1, "optim step must be >= 1");
+    for (int l = 0; l < d->n_linears; ++l)
+      OQ_REQ(opt->m_gamma[l] && opt->v_gamma[l] && opt->m_beta[l] && opt->v_beta[l],
+             "AdamW state of linear %d missing", l);
+    for (const auto& p : plan)
+      if (p.let)
+        OQ_REQ(opt->m_s[p.k] && opt->v_s[p.k] && opt->m_delta[p.k] && opt->v_delta[p.k],
+               "AdamW state of site %d missing", p.k);
+  }
+  const size_t need = carve_block(d, plan, nullptr, nullptr);
+  if (!ws || ws_bytes < need)
+    return fail(OQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  BlockWs w;
+  carve_block(d, plan, static_cast<char*>(ws), &w);
+
+  const bool bf = d->dtype == OQ_BF16;
+  const size_t es = bf ? 2 : 4;
+  const int64_t T = d->tokens;
+  const int ptn = gemm_part_tile_n(bf);
+  const int ntn = int((T + ptn - 1) / ptn);
+  int64_t row_base = 0;
+  LossArgs la{};
+  la.nlin = d->n_linears;
+
+  for (const auto& p : plan) {
+    const int k = p.k;
+    const int64_t C = p.C, M = p.M;
+    const float* s = p.let ? prm->s[k] : nullptr;
+    const float* dl = p.let ? prm->delta[k] : nullptr;
+    bool any_bias = p.let;
+    for (int l = p.l0; l < p.l1; ++l) any_bias = any_bias || prm->B[l];
+
+    // 1. LWC forward of every linear of the site into the stacked W^ [M, C]
+    int64_t off = 0;
+    for (int l = p.l0; l < p.l1; ++l) {
+      const int64_t co = d->lin_c_out[l];
+      ProfScope ps(PK_LWC_FWD, st, double(co) * C * 2 * es);
+      OQ_HIP(lwc_fwd(prm->W[l], bf, co, C, s, prm->gamma_logit[l], prm->beta_logit[l],
+                     d->lin_bits[l], d->lin_group[l], static_cast<char*>(w.what) + off * C * es, bf,
+                     nullptr, nullptr, nullptr, st),
+             "lwc_fwd");
+      la.row_begin[l] = row_base + off;
+      la.row_end[l] = row_base + off + co;
+      la.inv_n[l] = 1.0 / (double(T) * double(co));
+      la.row_loss[l] = gr->row_loss[l];
+      off += co;
+    }
+    // 2. folded bias B~ = B + W delta
+    if (any_bias) {
+      ProfScope ps(PK_OTHER, st, double(M) * C * es);
+      off = 0;
+      for (int l = p.l0; l < p.l1; ++l) {
+        const int64_t co = d->lin_c_out[l];
+        OQ_HIP(let_fold(prm->W[l], bf, prm->B[l], co, C, nullptr, dl, nullptr, false, w.bt + off, st),
+               "let_fold");
+        off += co;
+      }
+    }
+    // 3. quantised-model input X^ = Q_a((X - delta)/s)
+    const void* xsrc = X_q[k];
+    if (p.let || p.act) {
+      ProfScope ps(PK_ACT_FWD, st, double(T) * C * 2 * es);
+      OQ_HIP(act_fwd(X_q[k], bf, T, C, p.act ? d->site_act_bits[k] : 16, s, dl, w.xhat, bf,
+                     nullptr, nullptr, nullptr, st),
+             "act_fwd");
+      xsrc = w.xhat;
+    }
+    // 4. token-contiguous copy of X^ for the weight gradient
+    {
+      ProfScope ps(PK_TRANSPOSE, st, double(T) * C * 2 * es);
+      OQ_HIP(transpose(xsrc, T, C, C, w.xhatT, T, int(es), st), "transpose X");
+    }
+    // 5. forward: Y^T = W^ X^T + B~, residual, dY^T, row partials
+    {
+      ResidArgs ra{};
+      ra.nseg = p.l1 - p.l0;
+      int64_t b = 0;
+      for (int i = 0; i < ra.nseg; ++i) {
+        const int l = p.l0 + i;
+        ra.seg_begin[i] = b;
+        b += d->lin_c_out[l];
+        ra.seg_end[i] = b;
+        ra.yfp[i] = Y_fp_T[l];
+        ra.scale[i] = 2.0f / float(T * d->lin_c_out[l]);
+      }
+      ra.ld_yfp = T;
+      ra.bias = any_bias ? w.bt : nullptr;
+      ra.dy = w.dyT;
+      ra.ld_dy = T;
+      ra.part_sq = w.psq;
+      ra.part_dy = p.let ? w.pdy : nullptr;
+      ProfScope ps(PK_GEMM_FWD, st, 2.0 * double(M) * T * C);
+      OQ_HIP(gemm_nt_resid(w.what, xsrc, bf, M, T, C, C, C, ra, st), "forward gemm");
+    }
+    {
+      ProfScope ps(PK_OTHER, st, double(M) * ntn * 8);
+      OQ_HIP(row_partials(w.psq, p.let ? w.pdy : nullptr, M, ntn, w.rl + row_base, w.dbt, st),
+             "row partials");
+    }
+    // 6. weight gradient dW^ = dY^T X^  [M, C]
+    {
+      ProfScope ps(PK_GEMM_WGRAD, st, 2.0 * double(M) * T * C);
+      OQ_HIP(gemm_nt_f32out(w.dyT, w.xhatT, bf, M, C, T, T, T, w.dW, C, st), "wgrad gemm");
+    }
+    // 7. LWC backward per linear (+ weight-path LET scale partials)
+    off = 0;
+    int64_t pwo = 0;
+    for (int l = p.l0; l < p.l1; ++l) {
+      const int64_t co = d->lin_c_out[l];
+      ProfScope ps(PK_LWC_BWD, st, double(co) * C * (es + 4));
+      OQ_HIP(lwc_bwd(prm->W[l], bf, co, C, s, prm->gamma_logit[l], prm->beta_logit[l],
+                     d->lin_bits[l], d->lin_group[l], w.dW + off * C, gr->d_gamma_logit[l],
+                     gr->d_beta_logit[l], nullptr, p.let ? w.pw + pwo * C : nullptr, st),
+             "lwc_bwd");
+      off += co;
+      pwo += lwc_bwd_nparts(co);
+    }
+    // 8. LET: input gradient through Q_a and (X - delta)/s, bias path, finish
+    if (p.let) {
+      {
+        ProfScope ps(PK_TRANSPOSE, st, double(M) * (T + C) * 2 * es);
+        OQ_HIP(transpose(w.dyT, M, T, T, w.dy, M, int(es), st), "transpose dY");
+        OQ_HIP(transpose(w.what, M, C, C, w.whatT, M, int(es), st), "transpose W^");
+      }
+      {
+        ProfScope ps(PK_GEMM_DGRAD, st, 2.0 * double(M) * T * C);
+        OQ_HIP(gemm_nt_f32out(w.dy, w.whatT, bf, T, C, M, M, M, w.dX, C, st), "dgrad gemm");
+      }
+      {
+        ProfScope ps(PK_ACT_BWD, st, double(T) * C * (es + 4));
+        OQ_HIP(act_bwd(X_q[k], bf, T, C, p.act ? d->site_act_bits[k] : 16, s, dl, w.dX, nullptr,
+                       w.psx, w.ps1, st),
+               "act_bwd");
+      }
+      ProfScope ps(PK_OTHER, st, double(M) * C * es);
+      off = 0;
+      int64_t pbo = 0;
+      for (int l = p.l0; l < p.l1; ++l) {
+        const int64_t co = d->lin_c_out[l];
+        OQ_HIP(wcolsum(prm->W[l], bf, co, C, w.dbt + off, w.pb + pbo * C, st), "bias path");
+        off += co;
+        pbo += wcolsum_nparts(co);
+      }
+      OQ_HIP(let_grad_finish(C, s, w.pw, pwo, w.psx, w.ps1, act_bwd_nparts(T), w.pb, pbo,
+                             gr->d_s[k], gr->d_delta[k], st),
+             "LET finish");
+    }
+    row_base += M;
+  }
+  {
+    ProfScope ps(PK_OTHER, st, double(row_base) * 8);
+    OQ_HIP(loss_finish(w.rl, la, loss, st), "loss");
+  }
+  if (opt) {
+    const float bc1 = float(1.0 - std::pow(double(opt->beta1), opt->step));
+    const float bc2 = float(1.0 - std::pow(double(opt->beta2), opt->step));
+    ProfScope ps(PK_OTHER, st, 0);
+    for (int l = 0; l < d->n_linears; ++l) {
+      const int64_t n = d->lin_c_out[l] * (d->site_width[d->lin_site[l]] / d->lin_group[l]);
+      OQ_HIP(adamw(prm->gamma_logit[l], gr->d_gamma_logit[l], opt->m_gamma[l], opt->v_gamma[l], n,
+                   opt->lr_lwc, opt->beta1, opt->beta2, opt->eps, opt->wd, bc1, bc2, st),
+             "adamw gamma");
+      OQ_HIP(adamw(prm->beta_logit[l], gr->d_beta_logit[l], opt->m_beta[l], opt->v_beta[l], n,
+                   opt->lr_lwc, opt->beta1, opt->beta2, opt->eps, opt->wd, bc1, bc2, st),
+             "adamw beta");
+    }
+    for (const auto& p : plan) {
+      if (!p.let) continue;
+      OQ_HIP(adamw(prm->s[p.k], gr->d_s[p.k], opt->m_s[p.k], opt->v_s[p.k], p.C, opt->lr_let,
+                   opt->beta1, opt->beta2, opt->eps, opt->wd, bc1, bc2, st),
+             "adamw s");
+      OQ_HIP(adamw(prm->delta[p.k], gr->d_delta[p.k], opt->m_delta[p.k], opt->v_delta[p.k], p.C,
+                   opt->lr_let, opt->beta1, opt->beta2, opt->eps, opt->wd, bc1, bc2, st),
+             "adamw delta");
+    }
+  }
+  return OQ_OK;
+}
+
+}  // extern "C"

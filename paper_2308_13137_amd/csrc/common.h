@@ -1,0 +1,171 @@
+// Device helpers shared by the liboq kernels (gfx950, wave64).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+// Every named quantity of the quantisers is one IEEE fp32 rounding: never
+// fuse a multiply with the following add.
+#pragma clang fp contract(off)
+
+#define OQ_DEV __device__ __forceinline__
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------------ bf16 <-> fp32
+OQ_DEV float bf2f(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
+
+// Round to nearest even; NaN stays NaN.
+OQ_DEV uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return uint16_t(u >> 16);
+}
+
+// ------------------------------------------------------------------ 8-wide element access
+// A "chunk" is 8 consecutive elements of a row: 16 bytes of bf16 or 32 bytes of fp32.
+OQ_DEV void load8(const uint16_t* p, float v[8]) {
+  uint4 q = *reinterpret_cast<const uint4*>(p);
+  uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[2 * e] = __uint_as_float(w[e] << 16);
+    v[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+  }
+}
+OQ_DEV void load8(const float* p, float v[8]) {
+  float4 a = *reinterpret_cast<const float4*>(p);
+  float4 b = *reinterpret_cast<const float4*>(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+OQ_DEV void store8(uint16_t* p, const float v[8]) {
+  uint4 q;
+  q.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
+  q.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
+  q.z = uint32_t(f2bf(v[4])) | (uint32_t(f2bf(v[5])) << 16);
+  q.w = uint32_t(f2bf(v[6])) | (uint32_t(f2bf(v[7])) << 16);
+  *reinterpret_cast<uint4*>(p) = q;
+}
+OQ_DEV void store8(float* p, const float v[8]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+OQ_DEV void store8_codes(uint8_t* p, const float q[8]) {
+  uint2 c;
+  c.x = uint32_t(q[0]) | (uint32_t(q[1]) << 8) | (uint32_t(q[2]) << 16) | (uint32_t(q[3]) << 24);
+  c.y = uint32_t(q[4]) | (uint32_t(q[5]) << 8) | (uint32_t(q[6]) << 16) | (uint32_t(q[7]) << 24);
+  *reinterpret_cast<uint2*>(p) = c;
+}
+
+OQ_DEV float load1(const uint16_t* p) { return bf2f(*p); }
+OQ_DEV float load1(const float* p) { return *p; }
+OQ_DEV void store1(uint16_t* p, float v) { *p = f2bf(v); }
+OQ_DEV void store1(float* p, float v) { *p = v; }
+
+// ------------------------------------------------------------------ reductions
+// (max, lowest index) and (min, lowest index) selections: associative and
+// commutative, so any reduction tree gives the same answer.
+OQ_DEV void sel_max(float& v, int& i, float ov, int oi) {
+  if (ov > v || (ov == v && oi < i)) { v = ov; i = oi; }
+}
+OQ_DEV void sel_min(float& v, int& i, float ov, int oi) {
+  if (ov < v || (ov == v && oi < i)) { v = ov; i = oi; }
+}
+
+// Butterfly over aligned groups of L lanes (L a power of two <= 64): every
+// lane of the group ends with the identical result.
+template <int L>
+OQ_DEV void group_minmax(float& mx, int& imx, float& mn, int& imn) {
+#pragma unroll
+  for (int off = 1; off < L; off <<= 1) {
+    float omx = __shfl_xor(mx, off);
+    int oimx = __shfl_xor(imx, off);
+    float omn = __shfl_xor(mn, off);
+    int oimn = __shfl_xor(imn, off);
+    sel_max(mx, imx, omx, oimx);
+    sel_min(mn, imn, omn, oimn);
+  }
+}
+template <int L>
+OQ_DEV float group_sum(float v) {
+#pragma unroll
+  for (int off = 1; off < L; off <<= 1) v += __shfl_xor(v, off);
+  return v;
+}
+OQ_DEV float dyn_group_sum(float v, int L) {
+  for (int off = 1; off < L; off <<= 1) v += __shfl_xor(v, off);
+  return v;
+}
+OQ_DEV void dyn_group_minmax(float& mx, int& imx, float& mn, int& imn, int L) {
+  for (int off = 1; off < L; off <<= 1) {
+    float omx = __shfl_xor(mx, off);
+    int oimx = __shfl_xor(imx, off);
+    float omn = __shfl_xor(mn, off);
+    int oimn = __shfl_xor(imn, off);
+    sel_max(mx, imx, omx, oimx);
+    sel_min(mn, imn, omn, oimn);
+  }
+}
+
+// ------------------------------------------------------------------ quantiser
+// Clip strength: the fp64 sigmoid of the logit, rounded once to fp32.
+OQ_DEV float clip_strength(float logit) {
+  double t = double(logit);
+  return float(1.0 / (1.0 + exp(-t)));
+}
+
+struct QParams {
+  float gamma, beta, a, b, h, r, z;
+  bool hclamp;
+};
+
+// Eq. 2 group parameters, fp32 in the fixed order
+//   a = gamma*max, b = beta*min, h = (a - b)/qmax, h >= 1e-5, r = 1/h, z = -rint(b*r)
+OQ_DEV QParams make_qparams(float mx, float mn, float gamma, float beta, float qmax) {
+  QParams p;
+  p.gamma = gamma;
+  p.beta = beta;
+  p.a = gamma * mx;
+  p.b = beta * mn;
+  float d = p.a - p.b;
+  float hr = d / qmax;
+  p.hclamp = hr < 1e-5f;
+  p.h = p.hclamp ? 1e-5f : hr;
+  p.r = 1.0f / p.h;
+  p.z = -rintf(p.b * p.r);
+  return p;
+}
+
+struct QElem {
+  float u, q;
+  bool m;
+};
+OQ_DEV QElem quant_elem(float wt, const QParams& p, float qmax) {
+  QElem e;
+  e.u = wt * p.r;
+  float c = rintf(e.u) + p.z;
+  e.m = (c >= 0.0f) && (c <= qmax);
+  e.q = fminf(fmaxf(c, 0.0f), qmax);
+  return e;
+}
+OQ_DEV float dequant(float q, const QParams& p) { return (q - p.z) * p.h; }
+
+// Straight-through group backward from the sums
+//   S_h = sum g*((q - z) - m*u),  S_z = sum g*(1 - m)
+struct QGrad {
+  float dmx, dmn, dgamma, dbeta;
+};
+OQ_DEV QGrad quant_group_grad(float s_h, float s_z, float mx, float mn, const QParams& p, float qmax) {
+  QGrad g;
+  float dh = s_h - s_z * (p.b / p.h);
+  if (p.hclamp) dh = 0.0f;
+  float da = dh / qmax;
+  float db = s_z - da;
+  g.dmx = da * p.gamma;
+  g.dmn = db * p.beta;
+  g.dgamma = da * mx;
+  g.dbeta = db * mn;
+  return g;
+}

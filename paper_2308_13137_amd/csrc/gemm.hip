@@ -1,0 +1,334 @@
+// Matrix products C[M,N] = A[M,K] B[N,K]^T for the calibration step.
+//
+// bf16 path (gfx950 matrix cores): 256x256 output tile per workgroup of four
+// wave64s, each wave owning a 128x128 quadrant as 8x8 fragments of
+// v_mfma_f32_16x16x32_bf16.  K advances 64 at a time through two LDS stages
+// (A and B tiles of 256 rows x 64 bf16 = 32 KiB each per stage); the global
+// loads of stage k+1 are issued before the matrix instructions of stage k.
+// Each LDS row is eight 16-byte chunks stored at chunk ^ (row & 7), so the
+// eight lanes of one 128-bit LDS access hit distinct banks both when a row is
+// written and when a fragment column is read.  Workgroups are numbered so that
+// the 32 tiles resident on one XCD (the hardware deals workgroups to the 8
+// XCDs round-robin) form an 8 x 4 block of the output, sharing A and B panels
+// in that XCD's L2.
+//
+// fp32 path: a plain LDS-tiled FMA kernel (64x64 tile, 4x4 per thread), used
+// by the fp32 workloads, whose matrices are small.
+//
+// Epilogues: plain fp32 store; bf16/fp32 store with a per-row bias; and the
+// calibration-step forward epilogue (residual against the full-precision
+// target, bf16 dL/dY, per-row partial sums of the squared residual and of dY).
+#include "common.h"
+#include "oq_internal.h"
+
+namespace oq {
+namespace {
+
+constexpr int BM = 256, BN = 256, BK = 64, NTHR = 256;
+constexpr int GROUP_M = 8;
+constexpr int F32_TILE = 64;
+
+// ------------------------------------------------------------------ epilogues
+struct EpiF32 {
+  float* C;
+  int64_t ldc;
+  static constexpr bool kRows = false;
+  struct Row { float* c; };
+  OQ_DEV Row row(int64_t m) const { return Row{C + m * ldc}; }
+  OQ_DEV float2 apply(const Row& r, int64_t n, float v) const {
+    r.c[n] = v;
+    return make_float2(0.f, 0.f);
+  }
+  OQ_DEV void finish(int64_t, int, float, float) const {}
+};
+
+template <typename TC>
+struct EpiStore {
+  TC* C;
+  int64_t ldc;
+  const float* bias;
+  static constexpr bool kRows = false;
+  struct Row { TC* c; float b; };
+  OQ_DEV Row row(int64_t m) const { return Row{C + m * ldc, bias ? bias[m] : 0.0f}; }
+  OQ_DEV float2 apply(const Row& r, int64_t n, float v) const {
+    store1(r.c + n, v + r.b);
+    return make_float2(0.f, 0.f);
+  }
+  OQ_DEV void finish(int64_t, int, float, float) const {}
+};
+
+// y = acc + B~[m]; r = y - y_fp; dY = r * 2/(T*c_out) stored in T;  row sums of r^2, dY.
+template <typename T>
+struct EpiResid {
+  ResidArgs a;
+  static constexpr bool kRows = true;
+  struct Row { const T* yfp; T* dy; float scale; float b; };
+  OQ_DEV Row row(int64_t m) const {
+    int s = 0;
+    while (s < a.nseg - 1 && m >= a.seg_end[s]) ++s;
+    Row r;
+    r.yfp = reinterpret_cast<const T*>(a.yfp[s]) + (m - a.seg_begin[s]) * a.ld_yfp;
+    r.dy = reinterpret_cast<T*>(a.dy) + m * a.ld_dy;
+    r.scale = a.scale[s];
+    r.b = a.bias ? a.bias[m] : 0.0f;
+    return r;
+  }
+  OQ_DEV float2 apply(const Row& r, int64_t n, float v) const {
+    float y = v + r.b;
+    float res = y - load1(r.yfp + n);
+    float d = res * r.scale;
+    store1(r.dy + n, d);
+    float dq = load1_rounded(d);
+    return make_float2(res * res, dq);
+  }
+  OQ_DEV static float load1_rounded(float d) {
+    if constexpr (sizeof(T) == 2) return bf2f(f2bf(d));
+    else return d;
+  }
+  OQ_DEV void finish(int64_t m, int tn, float sq, float dy) const {
+    a.part_sq[m * a.ntn + tn] = sq;
+    if (a.part_dy) a.part_dy[m * a.ntn + tn] = dy;
+  }
+};
+
+// ------------------------------------------------------------------ bf16 MFMA kernel
+OQ_DEV bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+template <class Epi>
+__global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
+    const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, int64_t M, int64_t N,
+    int64_t K, int64_t lda, int64_t ldb, int tiles_m, int tiles_n, Epi epi) {
+  __shared__ uint4 lds[2][2][BM * BK / 8];
+  __shared__ float2 rowbuf[2][BM];
+
+  const int tid = threadIdx.x;
+
+  // workgroup -> output tile: contiguous logical ranges per XCD, then
+  // GROUP_M tile-rows swept column by column.
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, local = bid >> 3, q = nblk >> 3, rem = nblk & 7;
+  const int L = xcd * q + min(xcd, rem) + local;
+  const int group_sz = GROUP_M * tiles_n;
+  const int g = L / group_sz;
+  const int first_m = g * GROUP_M;
+  const int gm = min(GROUP_M, tiles_m - first_m);
+  const int li = L - g * group_sz;
+  const int tm = first_m + li % gm, tn = li / gm;
+  const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+
+  // global -> LDS assignment: thread loads chunk (tid & 7) of rows (tid >> 3) + 32 i
+  const int lrow = tid >> 3, lch = tid & 7;
+  const int sw = lch ^ (lrow & 7);
+  const uint16_t* a_base = A + (m0 + lrow) * lda + lch * 8;
+  const uint16_t* b_base = B + (n0 + lrow) * ldb + lch * 8;
+  uint32_t amask = 0, bmask = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    if (m0 + lrow + 32 * i < M) amask |= 1u << i;
+    if (n0 + lrow + 32 * i < N) bmask |= 1u << i;
+  }
+
+  uint4 ra[8], rb[8];
+  const uint4 zero4 = make_uint4(0, 0, 0, 0);
+  auto gload = [&](int kt) {
+    const int64_t k = int64_t(kt) * BK;
+    const bool kv = k + lch * 8 < K;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      ra[i] = (kv && (amask >> i & 1u))
+                  ? *reinterpret_cast<const uint4*>(a_base + int64_t(32 * i) * lda + k)
+                  : zero4;
+      rb[i] = (kv && (bmask >> i & 1u))
+                  ? *reinterpret_cast<const uint4*>(b_base + int64_t(32 * i) * ldb + k)
+                  : zero4;
+    }
+  };
+  auto lstore = [&](int stage) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      lds[stage][0][(lrow + 32 * i) * 8 + sw] = ra[i];
+      lds[stage][1][(lrow + 32 * i) * 8 + sw] = rb[i];
+    }
+  };
+
+  const int wave = tid >> 6, lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int fr = lane & 15, fk = lane >> 4;
+
+  f32x4_t acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = int((K + BK - 1) / BK);
+  gload(0);
+  lstore(0);
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) gload(kt + 1);
+    const uint4* As = lds[kt & 1][0];
+    const uint4* Bs = lds[kt & 1][1];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int ch = (kk * 4 + fk) ^ (fr & 7);
+      bf16x8_t af[8], bfr[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) af[i] = as_bf16x8(As[(wm * 128 + 16 * i + fr) * 8 + ch]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) bfr[j] = as_bf16x8(Bs[(wn * 128 + 16 * j + fr) * 8 + ch]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) lstore((kt + 1) & 1);
+    __syncthreads();
+  }
+
+  // fragment (i, j) element r of lane (fr, fk) is C[16 i + 4 fk + r][16 j + fr] of the quadrant
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int trow = wm * 128 + 16 * i + 4 * fk + r;
+      const int64_t m = m0 + trow;
+      const bool mv = m < M;
+      float sq = 0.f, sdy = 0.f;
+      if (mv) {
+        auto rowc = epi.row(m);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int64_t n = n0 + wn * 128 + 16 * j + fr;
+          if (n < N) {
+            float2 c = epi.apply(rowc, n, acc[i][j][r]);
+            sq += c.x;
+            sdy += c.y;
+          }
+        }
+      }
+      if constexpr (Epi::kRows) {
+        sq = group_sum<16>(sq);
+        sdy = group_sum<16>(sdy);
+        if (fr == 0) rowbuf[wn][trow] = make_float2(sq, sdy);
+      }
+    }
+  }
+  if constexpr (Epi::kRows) {
+    __syncthreads();
+    const int64_t m = m0 + tid;
+    if (m < M) {
+      float2 p0 = rowbuf[0][tid], p1 = rowbuf[1][tid];
+      epi.finish(m, tn, p0.x + p1.x, p0.y + p1.y);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ fp32 kernel
+template <class Epi>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A,
+                                                       const float* __restrict__ B, int64_t M,
+                                                       int64_t N, int64_t K, int64_t lda,
+                                                       int64_t ldb, Epi epi) {
+  __shared__ float As[16][F32_TILE + 4];
+  __shared__ float Bs[16][F32_TILE + 4];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int64_t m0 = int64_t(blockIdx.y) * F32_TILE, n0 = int64_t(blockIdx.x) * F32_TILE;
+  const int lr = tid >> 2, lk = (tid & 3) * 4;
+  float acc[4][4] = {};
+  for (int64_t k0 = 0; k0 < K; k0 += 16) {
+    const int64_t k = k0 + lk;
+    float4 va = make_float4(0.f, 0.f, 0.f, 0.f), vb = va;
+    if (m0 + lr < M && k < K) va = *reinterpret_cast<const float4*>(A + (m0 + lr) * lda + k);
+    if (n0 + lr < N && k < K) vb = *reinterpret_cast<const float4*>(B + (n0 + lr) * ldb + k);
+    As[lk + 0][lr] = va.x; As[lk + 1][lr] = va.y; As[lk + 2][lr] = va.z; As[lk + 3][lr] = va.w;
+    Bs[lk + 0][lr] = vb.x; Bs[lk + 1][lr] = vb.y; Bs[lk + 2][lr] = vb.z; Bs[lk + 3][lr] = vb.w;
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t m = m0 + ty * 4 + i;
+    float sq = 0.f, sdy = 0.f;
+    if (m < M) {
+      auto rowc = epi.row(m);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int64_t n = n0 + tx * 4 + j;
+        if (n < N) {
+          float2 c = epi.apply(rowc, n, acc[i][j]);
+          sq += c.x;
+          sdy += c.y;
+        }
+      }
+    }
+    if constexpr (Epi::kRows) {
+      sq = group_sum<16>(sq);
+      sdy = group_sum<16>(sdy);
+      if (tx == 0 && m < M) epi.finish(m, int(blockIdx.x), sq, sdy);
+    }
+  }
+}
+
+template <class Epi>
+hipError_t launch(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
+                  int64_t lda, int64_t ldb, Epi epi, hipStream_t st) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (bf16) {
+    const int64_t tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
+    if (tm * tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(gemm_bf16_kernel<Epi>, dim3(unsigned(tm * tn)), dim3(NTHR), 0, st,
+                       static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N, K,
+                       lda, ldb, int(tm), int(tn), epi);
+  } else {
+    const int64_t tm = (M + F32_TILE - 1) / F32_TILE, tn = (N + F32_TILE - 1) / F32_TILE;
+    if (tm > 65535 || tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(gemm_f32_kernel<Epi>, dim3(unsigned(tn), unsigned(tm)), dim3(256), 0, st,
+                       static_cast<const float*>(A), static_cast<const float*>(B), M, N, K, lda,
+                       ldb, epi);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int gemm_part_tile_n(bool bf16) { return bf16 ? BN : F32_TILE; }
+
+hipError_t gemm_nt_f32out(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
+                          int64_t K, int64_t lda, int64_t ldb, float* C, int64_t ldc,
+                          hipStream_t st) {
+  return launch(A, B, bf16, M, N, K, lda, ldb, EpiF32{C, ldc}, st);
+}
+
+hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
+                         int64_t K, int64_t lda, int64_t ldb, void* C, bool c_bf16, int64_t ldc,
+                         const float* bias, hipStream_t st) {
+  if (c_bf16)
+    return launch(A, B, bf16, M, N, K, lda, ldb,
+                  EpiStore<uint16_t>{static_cast<uint16_t*>(C), ldc, bias}, st);
+  return launch(A, B, bf16, M, N, K, lda, ldb, EpiStore<float>{static_cast<float*>(C), ldc, bias},
+                st);
+}
+
+hipError_t gemm_nt_resid(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
+                         int64_t K, int64_t lda, int64_t ldb, ResidArgs ra, hipStream_t st) {
+  ra.ntn = int((N + gemm_part_tile_n(bf16) - 1) / gemm_part_tile_n(bf16));
+  if (bf16) return launch(A, B, true, M, N, K, lda, ldb, EpiResid<uint16_t>{ra}, st);
+  return launch(A, B, false, M, N, K, lda, ldb, EpiResid<float>{ra}, st);
+}
+
+}  // namespace oq

@@ -1,0 +1,337 @@
+// Bandwidth-bound helpers of the calibration step: tiled transposes, the LET
+// bias fold, column reductions with fixed-order finishing passes, the loss
+// reduction and the AdamW update.  Every reduction is a fixed tree (wave
+// butterflies, then ordered loops), never atomics, so results are bitwise
+// reproducible.
+#include <math.h>
+
+#include "common.h"
+#include "oq_internal.h"
+
+namespace oq {
+namespace {
+
+// ------------------------------------------------------------------ transpose
+// out[c][r] = in[r][c]; 64x64 tiles through LDS, 256 threads, 16 elements each.
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in, int64_t rows,
+                                                        int64_t cols, int64_t ld_in,
+                                                        T* __restrict__ out, int64_t ld_out) {
+  __shared__ T tile[64][65];
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int64_t r0 = int64_t(blockIdx.y) * 64, c0 = int64_t(blockIdx.x) * 64;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int r = ty + 4 * i;
+    if (r0 + r < rows && c0 + tx < cols) tile[r][tx] = in[(r0 + r) * ld_in + c0 + tx];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int c = ty + 4 * i;
+    if (c0 + c < cols && r0 + tx < rows) out[(c0 + c) * ld_out + r0 + tx] = tile[tx][c];
+  }
+}
+
+// ------------------------------------------------------------------ LET fold
+// One wave per output row: B~[o] = B[o] + sum_c W[o,c] delta[c] (fp64 sum),
+// W~[o,c] = W[o,c] * s[c].
+template <typename TW, typename TT>
+__global__ __launch_bounds__(256) void let_fold_kernel(const TW* __restrict__ W, const float* B,
+                                                       int64_t c_out, int64_t c_in,
+                                                       const float* s, const float* delta,
+                                                       TT* Wt, float* Bt) {
+  const int lane = threadIdx.x & 63;
+  const int64_t o = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (o >= c_out) return;
+  const int64_t cpr = c_in / 8;
+  double acc = 0.0;
+  for (int64_t j = lane; j < cpr; j += 64) {
+    float w[8];
+    load8(W + o * c_in + 8 * j, w);
+    if (delta) {
+      float d[8];
+      load8(delta + 8 * j, d);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc += double(w[e]) * double(d[e]);
+    }
+    if (Wt) {
+      float sv[8], t[8];
+      if (s) load8(s + 8 * j, sv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t[e] = s ? w[e] * sv[e] : w[e];
+      store8(Wt + o * c_in + 8 * j, t);
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0 && Bt) Bt[o] = float(acc + (B ? double(B[o]) : 0.0));
+}
+
+// ------------------------------------------------------------------ column reductions
+// Grid (column tiles of 2048, row blocks of R rows); thread owns 8 columns.
+template <typename TW>
+__global__ __launch_bounds__(256) void wcolsum_kernel(const TW* __restrict__ W, int64_t rows,
+                                                      int64_t cols, int R, const float* wt,
+                                                      float* out_parts) {
+  const int64_t c = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 8;
+  if (c >= cols) return;
+  const int64_t r0 = int64_t(blockIdx.y) * R, r1 = min(rows, r0 + R);
+  float acc[8] = {};
+  for (int64_t r = r0; r < r1; ++r) {
+    float w[8];
+    load8(W + r * cols + c, w);
+    const float f = wt[r];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += f * w[e];
+  }
+  store8(out_parts + int64_t(blockIdx.y) * cols + c, acc);
+}
+
+template <typename TX>
+__global__ __launch_bounds__(256) void colstat_kernel(const TX* __restrict__ X, int64_t rows,
+                                                      int64_t cols, int R, float* amax_parts,
+                                                      double* sum_parts) {
+  const int64_t c = (int64_t(blockIdx.x) * 256 + threadIdx.x) * 8;
+  if (c >= cols) return;
+  const int64_t r0 = int64_t(blockIdx.y) * R, r1 = min(rows, r0 + R);
+  float mx[8] = {};
+  double sm[8] = {};
+  for (int64_t r = r0; r < r1; ++r) {
+    float x[8];
+    load8(X + r * cols + c, x);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      mx[e] = fmaxf(mx[e], fabsf(x[e]));
+      sm[e] += double(x[e]);
+    }
+  }
+  store8(amax_parts + int64_t(blockIdx.y) * cols + c, mx);
+  if (sum_parts) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sum_parts[int64_t(blockIdx.y) * cols + c + e] = sm[e];
+  }
+}
+
+__global__ __launch_bounds__(256) void let_grad_finish_kernel(
+    int64_t C, const float* s, const float* pw, int64_t npw, const float* psx, const float* ps1,
+    int64_t npa, const float* pb, int64_t npb, float* d_s, float* d_delta) {
+  const int64_t c = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (c >= C) return;
+  double w = 0.0, sx = 0.0, s1 = 0.0, b = 0.0;
+  if (pw)
+    for (int64_t i = 0; i < npw; ++i) w += double(pw[i * C + c]);
+  if (psx)
+    for (int64_t i = 0; i < npa; ++i) sx += double(psx[i * C + c]);
+  if (ps1)
+    for (int64_t i = 0; i < npa; ++i) s1 += double(ps1[i * C + c]);
+  if (pb)
+    for (int64_t i = 0; i < npb; ++i) b += double(pb[i * C + c]);
+  const double sc = s ? double(s[c]) : 1.0;
+  if (d_s) d_s[c] = float(w - sx / sc);
+  if (d_delta) d_delta[c] = float(b - s1 / sc);
+}
+
+__global__ __launch_bounds__(256) void let_init_finish_kernel(int64_t C, int64_t T,
+                                                              const float* ax_parts, int64_t nax,
+                                                              const double* sum_parts,
+                                                              const float* aw_parts, int64_t naw,
+                                                              float* s, float* delta) {
+  const int64_t c = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (c >= C) return;
+  float ax = 0.f, aw = 0.f;
+  double sm = 0.0;
+  for (int64_t i = 0; i < nax; ++i) {
+    ax = fmaxf(ax, ax_parts[i * C + c]);
+    sm += sum_parts[i * C + c];
+  }
+  for (int64_t i = 0; i < naw; ++i) aw = fmaxf(aw, aw_parts[i * C + c]);
+  ax = fmaxf(ax, 1e-5f);
+  aw = fmaxf(aw, 1e-5f);
+  s[c] = __fsqrt_rn(ax) / __fsqrt_rn(aw);
+  delta[c] = float(sm / double(T));
+}
+
+// ------------------------------------------------------------------ loss
+// One wave per row: fp64 sums of the per-column-tile partials.
+__global__ __launch_bounds__(256) void row_partials_kernel(const float* __restrict__ psq,
+                                                           const float* __restrict__ pdy,
+                                                           int64_t M, int ntn, double* rl,
+                                                           float* dbt) {
+  const int lane = threadIdx.x & 63;
+  const int64_t m = int64_t(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (m >= M) return;
+  double a = 0.0, b = 0.0;
+  for (int j = lane; j < ntn; j += 64) {
+    a += double(psq[m * ntn + j]);
+    if (pdy) b += double(pdy[m * ntn + j]);
+  }
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    a += __shfl_xor(a, off);
+    b += __shfl_xor(b, off);
+  }
+  if (lane == 0) {
+    rl[m] = a;
+    if (pdy && dbt) dbt[m] = float(b);
+  }
+}
+
+__global__ __launch_bounds__(256) void loss_finish_kernel(const double* rl, LossArgs la,
+                                                          float* loss) {
+  __shared__ double sh[4];
+  const int tid = threadIdx.x;
+  double total = 0.0;
+  for (int l = 0; l < la.nlin; ++l) {
+    double a = 0.0;
+    for (int64_t m = la.row_begin[l] + tid; m < la.row_end[l]; m += 256) {
+      a += rl[m];
+      if (la.row_loss[l]) la.row_loss[l][m - la.row_begin[l]] = float(rl[m]);
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) a += __shfl_xor(a, off);
+    __syncthreads();
+    if ((tid & 63) == 0) sh[tid >> 6] = a;
+    __syncthreads();
+    total += ((sh[0] + sh[1]) + (sh[2] + sh[3])) * la.inv_n[l];
+  }
+  if (tid == 0) *loss = float(total);
+}
+
+// ------------------------------------------------------------------ AdamW
+__global__ __launch_bounds__(256) void adamw_kernel(float* p, const float* g, float* m, float* v,
+                                                    int64_t n, float lr, float b1, float b2,
+                                                    float eps, float wd, float bc1, float bc2) {
+  const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n) return;
+  const float gi = g[i];
+  const float mi = b1 * m[i] + (1.0f - b1) * gi;
+  const float vi = b2 * v[i] + (1.0f - b2) * (gi * gi);
+  m[i] = mi;
+  v[i] = vi;
+  float pi = p[i] * (1.0f - lr * wd);
+  const float mh = mi / bc1;
+  const float vh = vi / bc2;
+  pi = pi - lr * (mh / (__fsqrt_rn(vh) + eps));
+  p[i] = pi;
+}
+
+}  // namespace
+
+hipError_t transpose(const void* in, int64_t rows, int64_t cols, int64_t ld_in, void* out,
+                     int64_t ld_out, int elem_bytes, hipStream_t st) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  const int64_t gy = (rows + 63) / 64, gx = (cols + 63) / 64;
+  if (gy > 65535 || gx > 0x7fffffff) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(gx), static_cast<unsigned>(gy));
+  if (elem_bytes == 2)
+    hipLaunchKernelGGL(transpose_kernel<uint16_t>, grid, dim3(256), 0, st,
+                       static_cast<const uint16_t*>(in), rows, cols, ld_in,
+                       static_cast<uint16_t*>(out), ld_out);
+  else if (elem_bytes == 4)
+    hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(256), 0, st,
+                       static_cast<const float*>(in), rows, cols, ld_in, static_cast<float*>(out),
+                       ld_out);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t let_fold(const void* W, bool w_bf16, const float* B, int64_t c_out, int64_t c_in,
+                    const float* s, const float* delta, void* Wt, bool wt_bf16, float* Bt,
+                    hipStream_t st) {
+  if (c_out <= 0) return hipSuccess;
+  const dim3 grid(unsigned((c_out + 3) / 4));
+  auto go = [&](auto tw, auto tt) {
+    using TW = decltype(tw);
+    using TT = decltype(tt);
+    hipLaunchKernelGGL((let_fold_kernel<TW, TT>), grid, dim3(256), 0, st,
+                       static_cast<const TW*>(W), B, c_out, c_in, s, delta, static_cast<TT*>(Wt),
+                       Bt);
+  };
+  if (w_bf16) {
+    if (wt_bf16) go(uint16_t{}, uint16_t{}); else go(uint16_t{}, float{});
+  } else {
+    if (wt_bf16) go(float{}, uint16_t{}); else go(float{}, float{});
+  }
+  return hipGetLastError();
+}
+
+static int64_t colred_rows(int64_t rows) { return std::max<int64_t>(16, (rows + 511) / 512); }
+
+int64_t wcolsum_nparts(int64_t rows) {
+  if (rows <= 0) return 0;
+  const int64_t R = colred_rows(rows);
+  return (rows + R - 1) / R;
+}
+
+hipError_t wcolsum(const void* W, bool w_bf16, int64_t rows, int64_t cols, const float* wt,
+                   float* out_parts, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  const int64_t R = colred_rows(rows);
+  const dim3 grid(unsigned((cols / 8 + 255) / 256), unsigned((rows + R - 1) / R));
+  if (w_bf16)
+    hipLaunchKernelGGL(wcolsum_kernel<uint16_t>, grid, dim3(256), 0, st,
+                       static_cast<const uint16_t*>(W), rows, cols, int(R), wt, out_parts);
+  else
+    hipLaunchKernelGGL(wcolsum_kernel<float>, grid, dim3(256), 0, st,
+                       static_cast<const float*>(W), rows, cols, int(R), wt, out_parts);
+  return hipGetLastError();
+}
+
+int64_t colstat_nparts(int64_t rows) { return wcolsum_nparts(rows); }
+
+hipError_t colstat(const void* X, bool bf16, int64_t rows, int64_t cols, float* amax_parts,
+                   double* sum_parts, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  const int64_t R = colred_rows(rows);
+  const dim3 grid(unsigned((cols / 8 + 255) / 256), unsigned((rows + R - 1) / R));
+  if (bf16)
+    hipLaunchKernelGGL(colstat_kernel<uint16_t>, grid, dim3(256), 0, st,
+                       static_cast<const uint16_t*>(X), rows, cols, int(R), amax_parts, sum_parts);
+  else
+    hipLaunchKernelGGL(colstat_kernel<float>, grid, dim3(256), 0, st,
+                       static_cast<const float*>(X), rows, cols, int(R), amax_parts, sum_parts);
+  return hipGetLastError();
+}
+
+hipError_t let_grad_finish(int64_t C, const float* s, const float* pw, int64_t npw,
+                           const float* psx, const float* ps1, int64_t npa, const float* pb,
+                           int64_t npb, float* d_s, float* d_delta, hipStream_t st) {
+  if (C <= 0) return hipSuccess;
+  hipLaunchKernelGGL(let_grad_finish_kernel, dim3(unsigned((C + 255) / 256)), dim3(256), 0, st, C,
+                     s, pw, npw, psx, ps1, npa, pb, npb, d_s, d_delta);
+  return hipGetLastError();
+}
+
+hipError_t let_init_finish(int64_t C, int64_t T, const float* ax_parts, int64_t nax,
+                           const double* sum_parts, const float* aw_parts, int64_t naw, float* s,
+                           float* delta, hipStream_t st) {
+  if (C <= 0) return hipSuccess;
+  hipLaunchKernelGGL(let_init_finish_kernel, dim3(unsigned((C + 255) / 256)), dim3(256), 0, st, C,
+                     T, ax_parts, nax, sum_parts, aw_parts, naw, s, delta);
+  return hipGetLastError();
+}
+
+hipError_t row_partials(const float* psq, const float* pdy, int64_t M, int ntn, double* rl,
+                        float* dbt, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL(row_partials_kernel, dim3(unsigned((M + 3) / 4)), dim3(256), 0, st, psq, pdy,
+                     M, ntn, rl, dbt);
+  return hipGetLastError();
+}
+
+hipError_t loss_finish(const double* rl, LossArgs la, float* loss, hipStream_t st) {
+  hipLaunchKernelGGL(loss_finish_kernel, dim3(1), dim3(256), 0, st, rl, la, loss);
+  return hipGetLastError();
+}
+
+hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, float lr, float b1,
+                 float b2, float eps, float wd, float bc1, float bc2, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(adamw_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p, g, m, v,
+                     n, lr, b1, b2, eps, wd, bc1, bc2);
+  return hipGetLastError();
+}
+
+}  // namespace oq

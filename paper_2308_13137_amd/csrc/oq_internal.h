@@ -1,0 +1,119 @@
+// Host-side launchers shared between the kernel files and the C ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+namespace oq {
+
+enum ProfKind {
+  PK_GEMM_FWD = 0, PK_GEMM_WGRAD = 1, PK_GEMM_DGRAD = 2, PK_LWC_FWD = 3, PK_LWC_BWD = 4,
+  PK_ACT_FWD = 5, PK_ACT_BWD = 6, PK_TRANSPOSE = 7, PK_OTHER = 8
+};
+
+// Kernel timing: when enabled, brackets a launch with events on its stream.
+struct ProfScope {
+  ProfScope(int kind, hipStream_t s, double work);
+  ~ProfScope();
+  int kind;
+  hipStream_t stream;
+  double work;
+  hipEvent_t e0, e1;
+  bool on;
+};
+
+// ---------------------------------------------------------------- GEMM: C = A B^T
+// The forward epilogue of the calibration step: per output row m (an output
+// channel of one of up to MAX_SEG linears stacked along M) and column n (a token)
+//   y = acc + bias[m];  r = y - yfp[m][n];  dy = bf16(r * scale);  store dy
+// and per (row, column tile) the partial sums of r^2 and of dy.
+constexpr int MAX_SEG = 4;
+struct ResidArgs {
+  int nseg;
+  int64_t seg_end[MAX_SEG];        // exclusive row end of each linear
+  const void* yfp[MAX_SEG];        // [rows_l, ld_yfp], channel-major target
+  float scale[MAX_SEG];            // 2 / (T * c_out_l)
+  int64_t seg_begin[MAX_SEG];
+  int64_t ld_yfp;
+  const float* bias;               // [M] | nullptr
+  void* dy;                        // [M, ld_dy]
+  int64_t ld_dy;
+  float* part_sq;                  // [M, ntn]
+  float* part_dy;                  // [M, ntn] | nullptr
+  int ntn;                         // column tiles (set by the launcher)
+};
+
+// Column-tile width of the row partials written by the forward epilogue.
+int gemm_part_tile_n(bool bf16);
+
+hipError_t gemm_nt_f32out(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
+                          int64_t lda, int64_t ldb, float* C, int64_t ldc, hipStream_t st);
+hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
+                         int64_t lda, int64_t ldb, void* C, bool c_bf16, int64_t ldc,
+                         const float* bias, hipStream_t st);
+hipError_t gemm_nt_resid(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
+                         int64_t lda, int64_t ldb, ResidArgs ra, hipStream_t st);
+
+// ---------------------------------------------------------------- quantisers
+// LWC forward on rows [0, c_out) of one weight.  Returns hipErrorInvalidValue
+// when (c_in, group) is outside the supported set.
+hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
+                   const float* gl, const float* bl, int bits, int64_t group, void* W_dq,
+                   bool dq_bf16, uint8_t* codes, float* h, float* z, hipStream_t st);
+// LWC backward.  When ds_parts != nullptr each block writes one partial row
+// [c_in] of sum_o dW~[o,c]*W[o,c] into ds_parts; the number of rows written is
+// lwc_bwd_nparts(c_out).
+int64_t lwc_bwd_nparts(int64_t c_out);
+hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
+                   const float* gl, const float* bl, int bits, int64_t group, const float* dW,
+                   float* dgl, float* dbl, float* dW_tilde, float* ds_parts, hipStream_t st);
+bool quant_shape_supported(int64_t c_in, int64_t group);
+
+// Activation fake-quant (per token row), LET transform included.
+hipError_t act_fwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, const float* s,
+                   const float* delta, void* X_dq, bool dq_bf16, uint8_t* codes, float* h,
+                   float* z, hipStream_t st);
+int64_t act_bwd_nparts(int64_t T);
+hipError_t act_bwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, const float* s,
+                   const float* delta, const float* dXdq, float* dXt, float* p_sx, float* p_s1,
+                   hipStream_t st);
+
+// ---------------------------------------------------------------- elementwise / reductions
+hipError_t transpose(const void* in, int64_t rows, int64_t cols, int64_t ld_in, void* out,
+                     int64_t ld_out, int elem_bytes, hipStream_t st);
+hipError_t let_fold(const void* W, bool w_bf16, const float* B, int64_t c_out, int64_t c_in,
+                    const float* s, const float* delta, void* Wt, bool wt_bf16, float* Bt,
+                    hipStream_t st);
+// out_parts[b][c] = sum over rows o of block b of wt[o] * W[o,c]
+int64_t wcolsum_nparts(int64_t rows);
+hipError_t wcolsum(const void* W, bool w_bf16, int64_t rows, int64_t cols, const float* wt,
+                   float* out_parts, hipStream_t st);
+// LET gradient finish, per column c (fp64, fixed order):
+//   d_s[c]     = sum_b pw[b][c] - (sum_b psx[b][c]) / s[c]
+//   d_delta[c] = sum_b pb[b][c] - (sum_b ps1[b][c]) / s[c]
+hipError_t let_grad_finish(int64_t C, const float* s, const float* pw, int64_t npw,
+                           const float* psx, const float* ps1, int64_t npa, const float* pb,
+                           int64_t npb, float* d_s, float* d_delta, hipStream_t st);
+// Row sums of the forward partials: rl[m] = sum_j psq[m][j] (fp64), and
+// dbt[m] = sum_j pdy[m][j] when pdy != nullptr.
+hipError_t row_partials(const float* psq, const float* pdy, int64_t M, int ntn, double* rl,
+                        float* dbt, hipStream_t st);
+// loss = sum over linears l of sum_{m in l} rl[m] / n_l;  row_loss outputs optional.
+struct LossArgs {
+  int nlin;
+  int64_t row_begin[16], row_end[16];
+  double inv_n[16];
+  float* row_loss[16];
+};
+hipError_t loss_finish(const double* rl, LossArgs la, float* loss, hipStream_t st);
+hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, float lr, float b1,
+                 float b2, float eps, float wd, float bc1, float bc2, hipStream_t st);
+// LET initialisation pieces
+int64_t colstat_nparts(int64_t rows);
+hipError_t colstat(const void* X, bool bf16, int64_t rows, int64_t cols, float* amax_parts,
+                   double* sum_parts, hipStream_t st);
+hipError_t let_init_finish(int64_t C, int64_t T, const float* ax_parts, int64_t nax,
+                           const double* sum_parts, const float* aw_parts, int64_t naw, float* s,
+                           float* delta, hipStream_t st);
+
+}  // namespace oq

@@ -1,0 +1,683 @@
+// Quantiser kernels: learnable weight clipping (Eq. 2) and per-token MinMax
+// activation fake-quant with the LET input transform (Eq. 3-4), forward and
+// straight-through backward.
+//
+// Work layout: a workgroup of 256 threads walks R consecutive rows.  A row is
+// split into 8-element chunks (16-byte bf16 / 32-byte fp32 vectors); thread t
+// owns chunks t, t+256, t+512, ... of every row, so per-column running sums
+// (the LET scale gradient) stay in registers across the R rows and every
+// global access is a coalesced 16/32-byte vector.
+//  * small groups (g a power of two <= 512): a group is g/8 consecutive lanes
+//    of one wave; its max/min (with the lowest index) and its gradient sums
+//    are xor-butterflies over those lanes;
+//  * whole-row groups (per output channel / per token): wave butterflies,
+//    then the four wave results combined in a fixed order through LDS.
+// Every reduction has a fixed shape, so results are bitwise reproducible.
+#include <float.h>
+#include <limits.h>
+
+#include "common.h"
+#include "oq_internal.h"
+
+namespace oq {
+namespace {
+
+constexpr int NT = 256;
+
+struct MinMax {
+  float mx, mn;
+  int imx, imn;
+};
+
+OQ_DEV MinMax minmax_init() { return MinMax{-FLT_MAX, FLT_MAX, INT_MAX, INT_MAX}; }
+OQ_DEV void minmax_add(MinMax& s, float v, int idx) {
+  sel_max(s.mx, s.imx, v, idx);
+  sel_min(s.mn, s.imn, v, idx);
+}
+
+// Whole-workgroup (max, argmax, min, argmin); every thread gets the result.
+OQ_DEV MinMax block_minmax(MinMax v, MinMax* sh) {
+  group_minmax<64>(v.mx, v.imx, v.mn, v.imn);
+  const int wave = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[wave] = v;
+  __syncthreads();
+  MinMax r = sh[0];
+#pragma unroll
+  for (int w = 1; w < NT / 64; ++w) {
+    sel_max(r.mx, r.imx, sh[w].mx, sh[w].imx);
+    sel_min(r.mn, r.imn, sh[w].mn, sh[w].imn);
+  }
+  return r;
+}
+
+OQ_DEV float2 block_sum2(float2 v, float2* sh) {
+  v.x = group_sum<64>(v.x);
+  v.y = group_sum<64>(v.y);
+  const int wave = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh[wave] = v;
+  __syncthreads();
+  float2 r = sh[0];
+#pragma unroll
+  for (int w = 1; w < NT / 64; ++w) {
+    r.x += sh[w].x;
+    r.y += sh[w].y;
+  }
+  return r;
+}
+
+// ------------------------------------------------------------------ LWC forward
+template <typename TW, typename TQ, int KC, bool WHOLE_ROW>
+__global__ __launch_bounds__(NT) void lwc_fwd_kernel(
+    const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ s,
+    const float* __restrict__ gl, const float* __restrict__ bl, int bits, int group, int R,
+    TQ* __restrict__ wdq, uint8_t* __restrict__ codes, float* __restrict__ hout,
+    float* __restrict__ zout) {
+  __shared__ MinMax shm[NT / 64];
+  const int tid = threadIdx.x;
+  const int cpr = int(c_in / 8);
+  const int ng = int(c_in / group);
+  const int L = group / 8;
+  const float qmax = float((1 << bits) - 1);
+
+  float sv[KC][8];
+#pragma unroll
+  for (int k = 0; k < KC; ++k) {
+    const int j = tid + NT * k;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sv[k][e] = 1.0f;
+    if (s && j < cpr) load8(s + 8 * j, sv[k]);
+  }
+
+  const int64_t r0 = int64_t(blockIdx.x) * R;
+  const int64_t r1 = min(c_out, r0 + R);
+  for (int64_t row = r0; row < r1; ++row) {
+    const TW* wrow = W + row * c_in;
+    if constexpr (WHOLE_ROW) {
+      float v[KC][8];
+      MinMax st = minmax_init();
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        if (j < cpr) {
+          load8(wrow + 8 * j, v[k]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            if (s) v[k][e] = v[k][e] * sv[k][e];
+            minmax_add(st, v[k][e], 8 * j + e);
+          }
+        }
+      }
+      st = block_minmax(st, shm);
+      const QParams p = make_qparams(st.mx, st.mn, clip_strength(gl[row]), clip_strength(bl[row]), qmax);
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        if (j < cpr) {
+          float q[8], d[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            q[e] = quant_elem(v[k][e], p, qmax).q;
+            d[e] = dequant(q[e], p);
+          }
+          if (wdq) store8(wdq + row * c_in + 8 * j, d);
+          if (codes) store8_codes(codes + row * c_in + 8 * j, q);
+        }
+      }
+      if (tid == 0) {
+        if (hout) hout[row] = p.h;
+        if (zout) zout[row] = p.z;
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        const bool valid = j < cpr;
+        float v[8];
+        MinMax st = minmax_init();
+        if (valid) {
+          load8(wrow + 8 * j, v);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            if (s) v[e] = v[e] * sv[k][e];
+            minmax_add(st, v[e], 8 * j + e);
+          }
+        }
+        dyn_group_minmax(st.mx, st.imx, st.mn, st.imn, L);
+        if (valid) {
+          const int grp = j / L;
+          const QParams p = make_qparams(st.mx, st.mn, clip_strength(gl[row * ng + grp]),
+                                         clip_strength(bl[row * ng + grp]), qmax);
+          float q[8], d[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            q[e] = quant_elem(v[e], p, qmax).q;
+            d[e] = dequant(q[e], p);
+          }
+          if (wdq) store8(wdq + row * c_in + 8 * j, d);
+          if (codes) store8_codes(codes + row * c_in + 8 * j, q);
+          if (j % L == 0) {
+            if (hout) hout[row * ng + grp] = p.h;
+            if (zout) zout[row * ng + grp] = p.z;
+          }
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ LWC backward
+// Per group:  S_h = sum g*((q - z) - m*u),  S_z = sum g*(1 - m)  ->  dgamma, dbeta
+// per element: dW~ = g*m + [i = argmax] dmax + [i = argmin] dmin
+// per column (optional): partial sum over this block's rows of dW~ * W.
+template <typename TW, int KC, bool WHOLE_ROW>
+__global__ __launch_bounds__(NT) void lwc_bwd_kernel(
+    const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ s,
+    const float* __restrict__ gl, const float* __restrict__ bl, int bits, int group, int R,
+    const float* __restrict__ dW, float* __restrict__ dgl, float* __restrict__ dbl,
+    float* __restrict__ dWt, float* __restrict__ ds_parts) {
+  __shared__ MinMax shm[NT / 64];
+  __shared__ float2 shs[NT / 64];
+  const int tid = threadIdx.x;
+  const int cpr = int(c_in / 8);
+  const int ng = int(c_in / group);
+  const int L = group / 8;
+  const float qmax = float((1 << bits) - 1);
+
+  float sv[KC][8], dsacc[KC][8];
+#pragma unroll
+  for (int k = 0; k < KC; ++k) {
+    const int j = tid + NT * k;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      sv[k][e] = 1.0f;
+      dsacc[k][e] = 0.0f;
+    }
+    if (s && j < cpr) load8(s + 8 * j, sv[k]);
+  }
+
+  const int64_t r0 = int64_t(blockIdx.x) * R;
+  const int64_t r1 = min(c_out, r0 + R);
+  for (int64_t row = r0; row < r1; ++row) {
+    const TW* wrow = W + row * c_in;
+    const float* grow = dW + row * c_in;
+    if constexpr (WHOLE_ROW) {
+      float w[KC][8], wt[KC][8], g[KC][8];
+      MinMax st = minmax_init();
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        if (j < cpr) {
+          load8(wrow + 8 * j, w[k]);
+          load8(grow + 8 * j, g[k]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            wt[k][e] = s ? w[k][e] * sv[k][e] : w[k][e];
+            minmax_add(st, wt[k][e], 8 * j + e);
+          }
+        }
+      }
+      st = block_minmax(st, shm);
+      const QParams p = make_qparams(st.mx, st.mn, clip_strength(gl[row]), clip_strength(bl[row]), qmax);
+      float2 sums = make_float2(0.f, 0.f);
+      bool mk[KC][8];
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        if (j < cpr) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const QElem qe = quant_elem(wt[k][e], p, qmax);
+            mk[k][e] = qe.m;
+            const float t = qe.q - p.z;
+            const float th = qe.m ? t - qe.u : t;
+            sums.x += g[k][e] * th;
+            if (!qe.m) sums.y += g[k][e];
+          }
+        }
+      }
+      sums = block_sum2(sums, shs);
+      const QGrad qg = quant_group_grad(sums.x, sums.y, st.mx, st.mn, p, qmax);
+      if (tid == 0) {
+        dgl[row] = qg.dgamma * p.gamma * (1.0f - p.gamma);
+        dbl[row] = qg.dbeta * p.beta * (1.0f - p.beta);
+      }
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        if (j < cpr) {
+          float d[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int col = 8 * j + e;
+            float x = mk[k][e] ? g[k][e] : 0.0f;
+            if (col == st.imx) x += qg.dmx;
+            if (col == st.imn) x += qg.dmn;
+            d[e] = x;
+            dsacc[k][e] += x * w[k][e];
+          }
+          if (dWt) store8(dWt + row * c_in + 8 * j, d);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        const bool valid = j < cpr;
+        float w[8], wt[8], g[8];
+        MinMax st = minmax_init();
+        if (valid) {
+          load8(wrow + 8 * j, w);
+          load8(grow + 8 * j, g);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            wt[e] = s ? w[e] * sv[k][e] : w[e];
+            minmax_add(st, wt[e], 8 * j + e);
+          }
+        }
+        dyn_group_minmax(st.mx, st.imx, st.mn, st.imn, L);
+        const int grp = j / L;
+        QParams p{};
+        float sh = 0.f, sz = 0.f;
+        bool mk[8];
+        if (valid) {
+          p = make_qparams(st.mx, st.mn, clip_strength(gl[row * ng + grp]),
+                           clip_strength(bl[row * ng + grp]), qmax);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const QElem qe = quant_elem(wt[e], p, qmax);
+            mk[e] = qe.m;
+            const float t = qe.q - p.z;
+            const float th = qe.m ? t - qe.u : t;
+            sh += g[e] * th;
+            if (!qe.m) sz += g[e];
+          }
+        }
+        sh = dyn_group_sum(sh, L);
+        sz = dyn_group_sum(sz, L);
+        if (valid) {
+          const QGrad qg = quant_group_grad(sh, sz, st.mx, st.mn, p, qmax);
+          if (j % L == 0) {
+            dgl[row * ng + grp] = qg.dgamma * p.gamma * (1.0f - p.gamma);
+            dbl[row * ng + grp] = qg.dbeta * p.beta * (1.0f - p.beta);
+          }
+          float d[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int col = 8 * j + e;
+            float x = mk[e] ? g[e] : 0.0f;
+            if (col == st.imx) x += qg.dmx;
+            if (col == st.imn) x += qg.dmn;
+            d[e] = x;
+            dsacc[k][e] += x * w[e];
+          }
+          if (dWt) store8(dWt + row * c_in + 8 * j, d);
+        }
+      }
+    }
+  }
+  if (ds_parts) {
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      const int j = tid + NT * k;
+      if (j < cpr) store8(ds_parts + int64_t(blockIdx.x) * c_in + 8 * j, dsacc[k]);
+    }
+  }
+}
+
+// ------------------------------------------------------------------ activation forward
+// x~ = (x - delta) * (1/s); per token row Eq. 2 with gamma = beta = 1.
+template <typename TX, typename TQ, int KC>
+__global__ __launch_bounds__(NT) void act_fwd_kernel(
+    const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
+    const float* __restrict__ delta, int R, TQ* __restrict__ xdq, uint8_t* __restrict__ codes,
+    float* __restrict__ hout, float* __restrict__ zout) {
+  __shared__ MinMax shm[NT / 64];
+  const int tid = threadIdx.x;
+  const int cpr = int(C / 8);
+  const bool quant = bits < 16;
+  const float qmax = quant ? float((1 << bits) - 1) : 0.0f;
+  float rs[KC][8], dl[KC][8];
+#pragma unroll
+  for (int k = 0; k < KC; ++k) {
+    const int j = tid + NT * k;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      rs[k][e] = 1.0f;
+      dl[k][e] = 0.0f;
+    }
+    if (j < cpr) {
+      if (s) {
+        load8(s + 8 * j, rs[k]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) rs[k][e] = 1.0f / rs[k][e];
+      }
+      if (delta) load8(delta + 8 * j, dl[k]);
+    }
+  }
+  const bool let = s || delta;
+  const int64_t r0 = int64_t(blockIdx.x) * R;
+  const int64_t r1 = min(T, r0 + R);
+  for (int64_t row = r0; row < r1; ++row) {
+    float v[KC][8];
+    MinMax st = minmax_init();
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      const int j = tid + NT * k;
+      if (j < cpr) {
+        load8(X + row * C + 8 * j, v[k]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if (let) v[k][e] = (v[k][e] - dl[k][e]) * rs[k][e];
+          minmax_add(st, v[k][e], 8 * j + e);
+        }
+      }
+    }
+    if (!quant) {
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        if (j < cpr && xdq) store8(xdq + row * C + 8 * j, v[k]);
+      }
+      continue;
+    }
+    st = block_minmax(st, shm);
+    const QParams p = make_qparams(st.mx, st.mn, 1.0f, 1.0f, qmax);
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      const int j = tid + NT * k;
+      if (j < cpr) {
+        float q[8], d[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          q[e] = quant_elem(v[k][e], p, qmax).q;
+          d[e] = dequant(q[e], p);
+        }
+        if (xdq) store8(xdq + row * C + 8 * j, d);
+        if (codes) store8_codes(codes + row * C + 8 * j, q);
+      }
+    }
+    if (tid == 0) {
+      if (hout) hout[row] = p.h;
+      if (zout) zout[row] = p.z;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ activation backward
+// dx~ per element (straight-through with the row scale's gradient); per column
+// partial sums over this block's rows of dx~ * x~ and of dx~.
+template <typename TX, int KC>
+__global__ __launch_bounds__(NT) void act_bwd_kernel(
+    const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
+    const float* __restrict__ delta, int R, const float* __restrict__ dXdq,
+    float* __restrict__ dXt, float* __restrict__ p_sx, float* __restrict__ p_s1) {
+  __shared__ MinMax shm[NT / 64];
+  __shared__ float2 shs[NT / 64];
+  const int tid = threadIdx.x;
+  const int cpr = int(C / 8);
+  const bool quant = bits < 16;
+  const float qmax = quant ? float((1 << bits) - 1) : 0.0f;
+  float rs[KC][8], dl[KC][8], asx[KC][8], as1[KC][8];
+#pragma unroll
+  for (int k = 0; k < KC; ++k) {
+    const int j = tid + NT * k;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      rs[k][e] = 1.0f;
+      dl[k][e] = 0.0f;
+      asx[k][e] = 0.0f;
+      as1[k][e] = 0.0f;
+    }
+    if (j < cpr) {
+      if (s) {
+        load8(s + 8 * j, rs[k]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) rs[k][e] = 1.0f / rs[k][e];
+      }
+      if (delta) load8(delta + 8 * j, dl[k]);
+    }
+  }
+  const bool let = s || delta;
+  const int64_t r0 = int64_t(blockIdx.x) * R;
+  const int64_t r1 = min(T, r0 + R);
+  for (int64_t row = r0; row < r1; ++row) {
+    float v[KC][8], g[KC][8];
+    MinMax st = minmax_init();
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      const int j = tid + NT * k;
+      if (j < cpr) {
+        load8(X + row * C + 8 * j, v[k]);
+        load8(dXdq + row * C + 8 * j, g[k]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          if (let) v[k][e] = (v[k][e] - dl[k][e]) * rs[k][e];
+          minmax_add(st, v[k][e], 8 * j + e);
+        }
+      }
+    }
+    if (quant) {
+      st = block_minmax(st, shm);
+      const QParams p = make_qparams(st.mx, st.mn, 1.0f, 1.0f, qmax);
+      float2 sums = make_float2(0.f, 0.f);
+      bool mk[KC][8];
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        if (j < cpr) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const QElem qe = quant_elem(v[k][e], p, qmax);
+            mk[k][e] = qe.m;
+            const float t = qe.q - p.z;
+            const float th = qe.m ? t - qe.u : t;
+            sums.x += g[k][e] * th;
+            if (!qe.m) sums.y += g[k][e];
+          }
+        }
+      }
+      sums = block_sum2(sums, shs);
+      const QGrad qg = quant_group_grad(sums.x, sums.y, st.mx, st.mn, p, qmax);
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        if (j < cpr) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int col = 8 * j + e;
+            float x = mk[k][e] ? g[k][e] : 0.0f;
+            if (col == st.imx) x += qg.dmx;
+            if (col == st.imn) x += qg.dmn;
+            g[k][e] = x;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      const int j = tid + NT * k;
+      if (j < cpr) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          asx[k][e] += g[k][e] * v[k][e];
+          as1[k][e] += g[k][e];
+        }
+        if (dXt) store8(dXt + row * C + 8 * j, g[k]);
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < KC; ++k) {
+    const int j = tid + NT * k;
+    if (j < cpr) {
+      if (p_sx) store8(p_sx + int64_t(blockIdx.x) * C + 8 * j, asx[k]);
+      if (p_s1) store8(p_s1 + int64_t(blockIdx.x) * C + 8 * j, as1[k]);
+    }
+  }
+}
+
+int kc_for(int64_t cols) {
+  const int64_t need = (cols / 8 + NT - 1) / NT;
+  if (need <= 1) return 1;
+  if (need <= 2) return 2;
+  if (need <= 4) return 4;
+  if (need <= 8) return 8;
+  if (need <= 16) return 16;
+  return 0;
+}
+
+int rows_per_block(int64_t rows, int64_t target_blocks) {
+  return int(std::max<int64_t>(1, (rows + target_blocks - 1) / target_blocks));
+}
+
+constexpr int64_t LWC_BLOCKS = 1024;
+constexpr int64_t ACT_BLOCKS = 2048;
+
+#define OQ_KC_SWITCH(KCV, ...)                      \
+  switch (KCV) {                                    \
+    case 1: { constexpr int KC = 1; __VA_ARGS__; } break;  \
+    case 2: { constexpr int KC = 2; __VA_ARGS__; } break;  \
+    case 4: { constexpr int KC = 4; __VA_ARGS__; } break;  \
+    case 8: { constexpr int KC = 8; __VA_ARGS__; } break;  \
+    case 16: { constexpr int KC = 16; __VA_ARGS__; } break; \
+    default: return hipErrorInvalidValue;           \
+  }
+
+bool small_group(int64_t group) {
+  return group >= 8 && group <= 512 && (group & (group - 1)) == 0;
+}
+
+}  // namespace
+
+bool quant_shape_supported(int64_t c_in, int64_t group) {
+  if (c_in <= 0 || c_in % 8 || group <= 0 || c_in % group) return false;
+  if (kc_for(c_in) == 0) return false;
+  return small_group(group) || group == c_in;
+}
+
+hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
+                   const float* gl, const float* bl, int bits, int64_t group, void* W_dq,
+                   bool dq_bf16, uint8_t* codes, float* h, float* z, hipStream_t st) {
+  if (!quant_shape_supported(c_in, group)) return hipErrorInvalidValue;
+  if (c_out <= 0) return hipSuccess;
+  const int R = rows_per_block(c_out, LWC_BLOCKS);
+  const dim3 grid(unsigned((c_out + R - 1) / R));
+  const bool whole = !small_group(group);
+  const int kc = kc_for(c_in);
+  auto go = [&](auto tw, auto tq, auto kcc, auto wr) {
+    using TW = decltype(tw);
+    using TQ = decltype(tq);
+    constexpr int KCc = decltype(kcc)::value;
+    constexpr bool WR = decltype(wr)::value;
+    hipLaunchKernelGGL((lwc_fwd_kernel<TW, TQ, KCc, WR>), grid, dim3(NT), 0, st,
+                       static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits, int(group), R,
+                       static_cast<TQ*>(W_dq), codes, h, z);
+  };
+  auto by_kc = [&](auto tw, auto tq, auto wr) -> hipError_t {
+    OQ_KC_SWITCH(kc, go(tw, tq, std::integral_constant<int, KC>{}, wr))
+    return hipSuccess;
+  };
+  auto by_wr = [&](auto tw, auto tq) -> hipError_t {
+    return whole ? by_kc(tw, tq, std::true_type{}) : by_kc(tw, tq, std::false_type{});
+  };
+  hipError_t e;
+  if (w_bf16) e = dq_bf16 ? by_wr(uint16_t{}, uint16_t{}) : by_wr(uint16_t{}, float{});
+  else e = dq_bf16 ? by_wr(float{}, uint16_t{}) : by_wr(float{}, float{});
+  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+int64_t lwc_bwd_nparts(int64_t c_out) {
+  if (c_out <= 0) return 0;
+  const int R = rows_per_block(c_out, LWC_BLOCKS);
+  return (c_out + R - 1) / R;
+}
+
+hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
+                   const float* gl, const float* bl, int bits, int64_t group, const float* dW,
+                   float* dgl, float* dbl, float* dW_tilde, float* ds_parts, hipStream_t st) {
+  if (!quant_shape_supported(c_in, group)) return hipErrorInvalidValue;
+  if (c_out <= 0) return hipSuccess;
+  const int R = rows_per_block(c_out, LWC_BLOCKS);
+  const dim3 grid(unsigned((c_out + R - 1) / R));
+  const bool whole = !small_group(group);
+  const int kc = kc_for(c_in);
+  auto go = [&](auto tw, auto kcc, auto wr) {
+    using TW = decltype(tw);
+    constexpr int KCc = decltype(kcc)::value;
+    constexpr bool WR = decltype(wr)::value;
+    hipLaunchKernelGGL((lwc_bwd_kernel<TW, KCc, WR>), grid, dim3(NT), 0, st,
+                       static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits, int(group), R, dW,
+                       dgl, dbl, dW_tilde, ds_parts);
+  };
+  auto by_kc = [&](auto tw, auto wr) -> hipError_t {
+    OQ_KC_SWITCH(kc, go(tw, std::integral_constant<int, KC>{}, wr))
+    return hipSuccess;
+  };
+  auto by_wr = [&](auto tw) -> hipError_t {
+    return whole ? by_kc(tw, std::true_type{}) : by_kc(tw, std::false_type{});
+  };
+  hipError_t e = w_bf16 ? by_wr(uint16_t{}) : by_wr(float{});
+  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t act_fwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, const float* s,
+                   const float* delta, void* X_dq, bool dq_bf16, uint8_t* codes, float* h,
+                   float* z, hipStream_t st) {
+  const int kc = kc_for(C);
+  if (C <= 0 || C % 8 || kc == 0) return hipErrorInvalidValue;
+  if (T <= 0) return hipSuccess;
+  const int R = rows_per_block(T, ACT_BLOCKS);
+  const dim3 grid(unsigned((T + R - 1) / R));
+  auto go = [&](auto tx, auto tq, auto kcc) {
+    using TX = decltype(tx);
+    using TQ = decltype(tq);
+    constexpr int KCc = decltype(kcc)::value;
+    hipLaunchKernelGGL((act_fwd_kernel<TX, TQ, KCc>), grid, dim3(NT), 0, st,
+                       static_cast<const TX*>(X), T, C, bits, s, delta, R, static_cast<TQ*>(X_dq),
+                       codes, h, z);
+  };
+  auto by_kc = [&](auto tx, auto tq) -> hipError_t {
+    OQ_KC_SWITCH(kc, go(tx, tq, std::integral_constant<int, KC>{}))
+    return hipSuccess;
+  };
+  hipError_t e;
+  if (x_bf16) e = dq_bf16 ? by_kc(uint16_t{}, uint16_t{}) : by_kc(uint16_t{}, float{});
+  else e = dq_bf16 ? by_kc(float{}, uint16_t{}) : by_kc(float{}, float{});
+  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+int64_t act_bwd_nparts(int64_t T) {
+  if (T <= 0) return 0;
+  const int R = rows_per_block(T, ACT_BLOCKS);
+  return (T + R - 1) / R;
+}
+
+hipError_t act_bwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, const float* s,
+                   const float* delta, const float* dXdq, float* dXt, float* p_sx, float* p_s1,
+                   hipStream_t st) {
+  const int kc = kc_for(C);
+  if (C <= 0 || C % 8 || kc == 0) return hipErrorInvalidValue;
+  if (T <= 0) return hipSuccess;
+  const int R = rows_per_block(T, ACT_BLOCKS);
+  const dim3 grid(unsigned((T + R - 1) / R));
+  auto go = [&](auto tx, auto kcc) {
+    using TX = decltype(tx);
+    constexpr int KCc = decltype(kcc)::value;
+    hipLaunchKernelGGL((act_bwd_kernel<TX, KCc>), grid, dim3(NT), 0, st,
+                       static_cast<const TX*>(X), T, C, bits, s, delta, R, dXdq, dXt, p_sx, p_s1);
+  };
+  auto by_kc = [&](auto tx) -> hipError_t {
+    OQ_KC_SWITCH(kc, go(tx, std::integral_constant<int, KC>{}))
+    return hipSuccess;
+  };
+  hipError_t e = x_bf16 ? by_kc(uint16_t{}) : by_kc(float{});
+  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+}  // namespace oq

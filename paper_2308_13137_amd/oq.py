@@ -1,0 +1,376 @@
+"""Thin Python binding of liboq.so (declared in include/oq.h).
+
+Every function here only marshals arguments: it checks dtypes and devices,
+allocates output tensors with torch (device memory is torch's job) and calls
+the C entry point of the same name on the current HIP stream.  All arithmetic
+happens in the library's HIP kernels.  If ``liboq.so`` has not been built the
+first call raises :class:`OQError`; there is no fallback.
+"""
+import ctypes as C
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboq.so")
+
+OQ_F32, OQ_BF16 = 0, 1
+MAX_SITES, MAX_LINEARS = 8, 16
+PROF_KINDS = ["gemm_fwd", "gemm_wgrad", "gemm_dgrad", "lwc_fwd", "lwc_bwd", "act_fwd",
+              "act_bwd", "transpose", "other"]
+
+# name -> (restype, argtypes); the exported surface of include/oq.h
+_P, _I64, _I, _F, _SZ = C.c_void_p, C.c_int64, C.c_int, C.c_float, C.c_size_t
+_PSZ = C.POINTER(C.c_size_t)
+SIGNATURES = {
+    "oq_status_str": (C.c_char_p, [_I]),
+    "oq_last_error": (C.c_char_p, []),
+    "oq_version": (_I, []),
+    "oq_lwc_fakequant_fwd": (_I, [_P, _I, _I64, _I64, _P, _P, _P, _I, _I64, _P, _I, _P, _P, _P, _P]),
+    "oq_lwc_fakequant_bwd": (_I, [_P, _I, _I64, _I64, _P, _P, _P, _I, _I64, _P, _P, _P, _P, _P,
+                                  _P, _SZ, _P]),
+    "oq_lwc_fakequant_bwd_workspace_size": (_I, [_I64, _I64, _I64, _I, _PSZ]),
+    "oq_let_fold": (_I, [_P, _I, _P, _I64, _I64, _P, _P, _P, _I, _P, _P]),
+    "oq_act_fakequant_fwd": (_I, [_P, _I, _I64, _I64, _I, _P, _P, _P, _I, _P, _P, _P, _P]),
+    "oq_act_fakequant_bwd": (_I, [_P, _I, _I64, _I64, _I, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "oq_act_fakequant_bwd_workspace_size": (_I, [_I64, _I64, _PSZ]),
+    "oq_let_init": (_I, [_P, _I, _I64, _I64, _P, _P, _I, _I, _P, _P, _P, _SZ, _P]),
+    "oq_let_init_workspace_size": (_I, [_I64, _I64, _P, _I, _PSZ]),
+    "oq_fp_target": (_I, [_P, _P, _I, _P, _I64, _I64, _I64, _P, _P]),
+    "oq_matmul_nt": (_I, [_P, _P, _I, _I64, _I64, _I64, _P, _I, _P]),
+    "oq_adamw_step": (_I, [_P, _P, _P, _P, _I64, _F, _F, _F, _F, _F, _I, _P]),
+    "oq_block_workspace_size": (_I, [_P, _PSZ]),
+    "oq_block_calib_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "oq_profile_enable": (_I, [_I]),
+    "oq_profile_reset": (_I, []),
+    "oq_profile_read": (_I, [_I, C.POINTER(C.c_int64), C.POINTER(C.c_double),
+                             C.POINTER(C.c_double)]),
+}
+
+
+class OQError(RuntimeError):
+    pass
+
+
+class BlockDesc(C.Structure):
+    _fields_ = [("tokens", C.c_int64), ("n_sites", C.c_int), ("n_linears", C.c_int),
+                ("dtype", C.c_int),
+                ("site_width", C.c_int64 * MAX_SITES), ("site_let", C.c_int * MAX_SITES),
+                ("site_act_bits", C.c_int * MAX_SITES), ("lin_site", C.c_int * MAX_LINEARS),
+                ("lin_c_out", C.c_int64 * MAX_LINEARS), ("lin_bits", C.c_int * MAX_LINEARS),
+                ("lin_group", C.c_int64 * MAX_LINEARS)]
+
+
+class BlockParams(C.Structure):
+    _fields_ = [("W", C.c_void_p * MAX_LINEARS), ("B", C.c_void_p * MAX_LINEARS),
+                ("gamma_logit", C.c_void_p * MAX_LINEARS), ("beta_logit", C.c_void_p * MAX_LINEARS),
+                ("s", C.c_void_p * MAX_SITES), ("delta", C.c_void_p * MAX_SITES)]
+
+
+class BlockGrads(C.Structure):
+    _fields_ = [("d_gamma_logit", C.c_void_p * MAX_LINEARS),
+                ("d_beta_logit", C.c_void_p * MAX_LINEARS),
+                ("d_s", C.c_void_p * MAX_SITES), ("d_delta", C.c_void_p * MAX_SITES),
+                ("row_loss", C.c_void_p * MAX_LINEARS)]
+
+
+class BlockOptim(C.Structure):
+    _fields_ = [("m_gamma", C.c_void_p * MAX_LINEARS), ("v_gamma", C.c_void_p * MAX_LINEARS),
+                ("m_beta", C.c_void_p * MAX_LINEARS), ("v_beta", C.c_void_p * MAX_LINEARS),
+                ("m_s", C.c_void_p * MAX_SITES), ("v_s", C.c_void_p * MAX_SITES),
+                ("m_delta", C.c_void_p * MAX_SITES), ("v_delta", C.c_void_p * MAX_SITES),
+                ("step", C.c_int), ("lr_lwc", C.c_float), ("lr_let", C.c_float),
+                ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float), ("wd", C.c_float)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise OQError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2308_13137_amd.build`")
+        handle = C.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def _check(status):
+    if status != 0:
+        L = lib()
+        raise OQError(f"{L.oq_status_str(status).decode()}: {L.oq_last_error().decode()}")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise OQError("tensors must live on the GPU")
+    if not t.is_contiguous():
+        raise OQError("tensors must be contiguous")
+    return C.c_void_p(t.data_ptr())
+
+
+def _dt(t):
+    if t.dtype == torch.bfloat16:
+        return OQ_BF16
+    if t.dtype == torch.float32:
+        return OQ_F32
+    raise OQError(f"unsupported dtype {t.dtype}")
+
+
+def _tdt(code):
+    return torch.bfloat16 if code == OQ_BF16 else torch.float32
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _f32(t, name):
+    if t is not None and t.dtype != torch.float32:
+        raise OQError(f"{name} must be float32")
+    return t
+
+
+def lwc_fakequant_fwd(W, gamma_logit, beta_logit, bits, group, s=None, dq_dtype=None,
+                      codes=True, hz=True, stream=None):
+    """Eq. 2 forward.  Returns (W_dq, codes | None, h | None, z | None)."""
+    c_out, c_in = W.shape
+    ng = c_in // group
+    dq_dtype = dq_dtype or W.dtype
+    W_dq = torch.empty((c_out, c_in), dtype=dq_dtype, device=W.device)
+    cd = torch.empty((c_out, c_in), dtype=torch.uint8, device=W.device) if codes else None
+    h = torch.empty((c_out, ng), dtype=torch.float32, device=W.device) if hz else None
+    z = torch.empty((c_out, ng), dtype=torch.float32, device=W.device) if hz else None
+    _check(lib().oq_lwc_fakequant_fwd(_ptr(W), _dt(W), c_out, c_in, _ptr(_f32(s, "s")),
+                                      _ptr(_f32(gamma_logit, "gamma_logit")),
+                                      _ptr(_f32(beta_logit, "beta_logit")), bits, group,
+                                      _ptr(W_dq), _dt(W_dq), _ptr(cd), _ptr(h), _ptr(z),
+                                      _stream(stream)))
+    return W_dq, cd, h, z
+
+
+def lwc_fakequant_bwd(W, gamma_logit, beta_logit, bits, group, dW_dq, s=None, want_d_s=False,
+                      want_dW_tilde=False, stream=None):
+    """Straight-through backward.  Returns (d_gamma_logit, d_beta_logit, d_s | None, dW_tilde | None)."""
+    c_out, c_in = W.shape
+    ng = c_in // group
+    dev = W.device
+    dg = torch.empty((c_out, ng), dtype=torch.float32, device=dev)
+    db = torch.empty((c_out, ng), dtype=torch.float32, device=dev)
+    ds = torch.empty(c_in, dtype=torch.float32, device=dev) if want_d_s else None
+    dwt = torch.empty((c_out, c_in), dtype=torch.float32, device=dev) if want_dW_tilde else None
+    n = C.c_size_t(0)
+    _check(lib().oq_lwc_fakequant_bwd_workspace_size(c_out, c_in, group, int(want_d_s), C.byref(n)))
+    ws = torch.empty(max(n.value, 1), dtype=torch.uint8, device=dev)
+    _check(lib().oq_lwc_fakequant_bwd(_ptr(W), _dt(W), c_out, c_in, _ptr(_f32(s, "s")),
+                                      _ptr(gamma_logit), _ptr(beta_logit), bits, group,
+                                      _ptr(_f32(dW_dq, "dW_dq")), _ptr(dg), _ptr(db), _ptr(ds),
+                                      _ptr(dwt), _ptr(ws), n.value, _stream(stream)))
+    return dg, db, ds, dwt
+
+
+def let_fold(W, B=None, s=None, delta=None, wt_dtype=None, want_W_tilde=True, stream=None):
+    """Eq. 3 fold.  Returns (W_tilde | None, B_tilde)."""
+    c_out, c_in = W.shape
+    wt_dtype = wt_dtype or W.dtype
+    Wt = torch.empty((c_out, c_in), dtype=wt_dtype, device=W.device) if want_W_tilde else None
+    Bt = torch.empty(c_out, dtype=torch.float32, device=W.device)
+    _check(lib().oq_let_fold(_ptr(W), _dt(W), _ptr(_f32(B, "B")), c_out, c_in, _ptr(s), _ptr(delta),
+                             _ptr(Wt), OQ_BF16 if wt_dtype == torch.bfloat16 else OQ_F32,
+                             _ptr(Bt), _stream(stream)))
+    return Wt, Bt
+
+
+def act_fakequant_fwd(X, bits, s=None, delta=None, dq_dtype=None, codes=True, hz=True,
+                      stream=None):
+    """Per-token fake-quant of X~ = (X - delta)/s.  Returns (X_dq, codes | None, h | None, z | None)."""
+    T, Cw = X.shape
+    dq_dtype = dq_dtype or X.dtype
+    dev = X.device
+    Xq = torch.empty((T, Cw), dtype=dq_dtype, device=dev)
+    cd = torch.empty((T, Cw), dtype=torch.uint8, device=dev) if (codes and bits < 16) else None
+    h = torch.empty(T, dtype=torch.float32, device=dev) if (hz and bits < 16) else None
+    z = torch.empty(T, dtype=torch.float32, device=dev) if (hz and bits < 16) else None
+    _check(lib().oq_act_fakequant_fwd(_ptr(X), _dt(X), T, Cw, bits, _ptr(_f32(s, "s")),
+                                      _ptr(_f32(delta, "delta")), _ptr(Xq), _dt(Xq), _ptr(cd),
+                                      _ptr(h), _ptr(z), _stream(stream)))
+    return Xq, cd, h, z
+
+
+def act_fakequant_bwd(X, bits, dX_dq, s=None, delta=None, want_dX_tilde=True, stream=None):
+    """Returns (dX_tilde | None, d_s, d_delta) (input-path parts of the LET gradients)."""
+    T, Cw = X.shape
+    dev = X.device
+    dxt = torch.empty((T, Cw), dtype=torch.float32, device=dev) if want_dX_tilde else None
+    ds = torch.empty(Cw, dtype=torch.float32, device=dev)
+    dd = torch.empty(Cw, dtype=torch.float32, device=dev)
+    n = C.c_size_t(0)
+    _check(lib().oq_act_fakequant_bwd_workspace_size(T, Cw, C.byref(n)))
+    ws = torch.empty(max(n.value, 1), dtype=torch.uint8, device=dev)
+    _check(lib().oq_act_fakequant_bwd(_ptr(X), _dt(X), T, Cw, bits, _ptr(s), _ptr(delta),
+                                      _ptr(_f32(dX_dq, "dX_dq")), _ptr(dxt), _ptr(ds), _ptr(dd),
+                                      _ptr(ws), n.value, _stream(stream)))
+    return dxt, ds, dd
+
+
+def let_init(X, Ws, stream=None):
+    """SmoothQuant scale / OS+ shift initialisation.  Returns (s, delta)."""
+    T, Cw = X.shape
+    dev = X.device
+    s = torch.empty(Cw, dtype=torch.float32, device=dev)
+    d = torch.empty(Cw, dtype=torch.float32, device=dev)
+    ptrs = (C.c_void_p * len(Ws))(*[W.data_ptr() for W in Ws])
+    couts = (C.c_int64 * len(Ws))(*[int(W.shape[0]) for W in Ws])
+    n = C.c_size_t(0)
+    _check(lib().oq_let_init_workspace_size(T, Cw, couts, len(Ws), C.byref(n)))
+    ws = torch.empty(n.value, dtype=torch.uint8, device=dev)
+    _check(lib().oq_let_init(_ptr(X), _dt(X), T, Cw, ptrs, couts, len(Ws), _dt(Ws[0]), _ptr(s),
+                             _ptr(d), _ptr(ws), ws.numel(), _stream(stream)))
+    return s, d
+
+
+def fp_target(X, W, B=None, stream=None):
+    """Channel-major full-precision target Y_T = W X^T + B, [c_out, T]."""
+    T, c_in = X.shape
+    c_out = W.shape[0]
+    if X.dtype != W.dtype:
+        raise OQError("X and W must share a dtype")
+    Y = torch.empty((c_out, T), dtype=X.dtype, device=X.device)
+    _check(lib().oq_fp_target(_ptr(X), _ptr(W), _dt(X), _ptr(_f32(B, "B")), T, c_in, c_out,
+                              _ptr(Y), _stream(stream)))
+    return Y
+
+
+def matmul_nt(A, B, out_dtype=torch.float32, stream=None):
+    """C = A B^T with A [M, K], B [N, K]."""
+    M, K = A.shape
+    N = B.shape[0]
+    out = torch.empty((M, N), dtype=out_dtype, device=A.device)
+    _check(lib().oq_matmul_nt(_ptr(A), _ptr(B), _dt(A), M, N, K, _ptr(out),
+                              OQ_BF16 if out_dtype == torch.bfloat16 else OQ_F32, _stream(stream)))
+    return out
+
+
+def adamw_step(p, g, m, v, step, lr, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.0, stream=None):
+    """In-place AdamW on fp32 tensors p, m, v with gradient g."""
+    _check(lib().oq_adamw_step(_ptr(p), _ptr(g), _ptr(m), _ptr(v), p.numel(), lr, beta1, beta2,
+                               eps, wd, step, _stream(stream)))
+
+
+# ------------------------------------------------------------------ block step
+class Block:
+    """One block's calibration problem: description, parameters, gradient
+    buffers, AdamW state and workspace, all device tensors owned by torch.
+
+    ``sites``   list of (width, let, act_bits)
+    ``linears`` list of (site, c_out, bits, group); linears of a site consecutive
+    """
+
+    def __init__(self, T, sites, linears, dtype=torch.bfloat16, device="cuda"):
+        self.T, self.sites, self.linears = T, list(sites), list(linears)
+        self.dtype, self.device = dtype, device
+        d = BlockDesc()
+        d.tokens = T
+        d.n_sites, d.n_linears = len(sites), len(linears)
+        d.dtype = OQ_BF16 if dtype == torch.bfloat16 else OQ_F32
+        for k, (w, let, ab) in enumerate(sites):
+            d.site_width[k], d.site_let[k], d.site_act_bits[k] = w, int(bool(let)), ab
+        for l, (k, co, bits, g) in enumerate(linears):
+            d.lin_site[l], d.lin_c_out[l], d.lin_bits[l], d.lin_group[l] = k, co, bits, g
+        self.desc = d
+        n = C.c_size_t(0)
+        _check(lib().oq_block_workspace_size(C.byref(d), C.byref(n)))
+        self.ws_bytes = n.value
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        f32 = dict(dtype=torch.float32, device=device)
+        self.d_gamma = [torch.empty((co, sites[k][0] // g), **f32) for (k, co, _, g) in linears]
+        self.d_beta = [torch.empty_like(t) for t in self.d_gamma]
+        self.d_s = [torch.empty(w, **f32) if let else None for (w, let, _) in sites]
+        self.d_delta = [torch.empty(w, **f32) if let else None for (w, let, _) in sites]
+        self.row_loss = [torch.empty(co, **f32) for (_, co, _, _) in linears]
+        self.loss = torch.empty((), **f32)
+        self.opt_state = None
+        self.step_count = 0
+
+    def init_optimizer(self, lr_lwc=5e-3, lr_let=1e-2, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.0):
+        f32 = dict(dtype=torch.float32, device=self.device)
+        o = BlockOptim()
+        self._mv = []
+        for l, t in enumerate(self.d_gamma):
+            for name in ("m_gamma", "v_gamma", "m_beta", "v_beta"):
+                z = torch.zeros_like(t)
+                self._mv.append(z)
+                getattr(o, name)[l] = z.data_ptr()
+        for k, (w, let, _) in enumerate(self.sites):
+            if let:
+                for name in ("m_s", "v_s", "m_delta", "v_delta"):
+                    z = torch.zeros(w, **f32)
+                    self._mv.append(z)
+                    getattr(o, name)[k] = z.data_ptr()
+        o.lr_lwc, o.lr_let, o.beta1, o.beta2, o.eps, o.wd = lr_lwc, lr_let, beta1, beta2, eps, wd
+        self.opt_state = o
+
+    def step(self, X_q, Y_fp_T, W, gamma_logit, beta_logit, s=None, delta=None, B=None,
+             update=False, stream=None):
+        """One calibration step.  Tensors are lists per site (X_q, s, delta) or
+        per linear (Y_fp_T, W, logits, B).  With ``update`` the AdamW state of
+        :meth:`init_optimizer` updates the logits, s and delta in place."""
+        nl, ns = len(self.linears), len(self.sites)
+        prm = BlockParams()
+        grd = BlockGrads()
+        for l in range(nl):
+            prm.W[l] = _ptr(W[l]).value
+            prm.B[l] = B[l].data_ptr() if (B is not None and B[l] is not None) else None
+            prm.gamma_logit[l] = _ptr(gamma_logit[l]).value
+            prm.beta_logit[l] = _ptr(beta_logit[l]).value
+            grd.d_gamma_logit[l] = self.d_gamma[l].data_ptr()
+            grd.d_beta_logit[l] = self.d_beta[l].data_ptr()
+            grd.row_loss[l] = self.row_loss[l].data_ptr()
+        for k in range(ns):
+            if self.sites[k][1]:
+                prm.s[k] = _ptr(s[k]).value
+                prm.delta[k] = _ptr(delta[k]).value
+                grd.d_s[k] = self.d_s[k].data_ptr()
+                grd.d_delta[k] = self.d_delta[k].data_ptr()
+        yp = (C.c_void_p * nl)(*[_ptr(y).value for y in Y_fp_T])
+        xp = (C.c_void_p * ns)(*[_ptr(x).value if x is not None else None for x in X_q])
+        opt = None
+        if update:
+            if self.opt_state is None:
+                raise OQError("call init_optimizer() before update=True")
+            self.step_count += 1
+            self.opt_state.step = self.step_count
+            opt = C.byref(self.opt_state)
+        _check(lib().oq_block_calib_step(C.byref(self.desc), yp, xp, C.byref(prm), C.byref(grd),
+                                         opt, _ptr(self.loss), _ptr(self.ws), self.ws_bytes,
+                                         _stream(stream)))
+        return self.loss
+
+
+# ------------------------------------------------------------------ profiling
+def profile_enable(on=True):
+    _check(lib().oq_profile_enable(int(on)))
+
+
+def profile_reset():
+    _check(lib().oq_profile_reset())
+
+
+def profile_read():
+    """{kind: (launches, total_ms, work)} for every kernel kind."""
+    out = {}
+    for i, name in enumerate(PROF_KINDS):
+        n, ms, w = C.c_int64(0), C.c_double(0), C.c_double(0)
+        _check(lib().oq_profile_read(i, C.byref(n), C.byref(ms), C.byref(w)))
+        out[name] = (n.value, ms.value, w.value)
+    return out

@@ -1,0 +1,142 @@
+"""Host-only checks of the C ABI: the library loads, exports every entry point
+declared in include/oq.h, and rejects invalid arguments before it launches
+anything (no GPU needed: every call here fails validation or only sizes a
+workspace)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2308_13137_amd import configs, oq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "oq.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(oq.LIB_PATH), reason="liboq.so not built")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+FAKE = C.c_void_p(0x10000)      # aligned, never dereferenced: validation fails first
+MISALIGNED = C.c_void_p(0x10004)
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(oq_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    syms = declared_symbols()
+    assert len(syms) >= 20
+    L = oq.lib()
+    for s in syms:
+        assert hasattr(L, s), s
+    assert set(syms) == set(oq.SIGNATURES), set(syms) ^ set(oq.SIGNATURES)
+
+
+def test_status_strings():
+    L = oq.lib()
+    assert L.oq_status_str(0) == b"OQ_OK"
+    assert L.oq_status_str(3) == b"OQ_ERR_WORKSPACE"
+    assert L.oq_version() >= 1
+
+
+def lwc_fwd(**kw):
+    a = dict(W=FAKE, w_dt=oq.OQ_BF16, c_out=64, c_in=256, s=None, gl=FAKE, bl=FAKE, bits=4,
+             group=64, W_dq=FAKE, dq_dt=oq.OQ_BF16, codes=None, h=None, z=None, st=None)
+    a.update(kw)
+    return oq.lib().oq_lwc_fakequant_fwd(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(W=None), INVALID), (dict(gl=None), INVALID), (dict(bits=9), UNSUPPORTED),
+    (dict(bits=1), UNSUPPORTED), (dict(group=48, c_in=384), UNSUPPORTED), (dict(group=100), INVALID),
+    (dict(c_in=252, group=4), INVALID), (dict(W=MISALIGNED), INVALID), (dict(w_dt=7), INVALID),
+    (dict(group=1024, c_in=2048), UNSUPPORTED), (dict(c_out=-1), INVALID),
+])
+def test_lwc_fwd_rejects(kw, status):
+    assert lwc_fwd(**kw) == status
+    assert oq.lib().oq_last_error()
+
+
+def test_lwc_bwd_workspace_contract():
+    L = oq.lib()
+    n = C.c_size_t(0)
+    assert L.oq_lwc_fakequant_bwd_workspace_size(4096, 4096, 4096, 1, C.byref(n)) == OK
+    assert n.value >= 4096 * 4
+    assert L.oq_lwc_fakequant_bwd_workspace_size(4096, 4096, 128, 0, C.byref(n)) == OK
+    assert n.value == 0
+    # d_s wanted but no workspace: refused before launch
+    st = L.oq_lwc_fakequant_bwd(FAKE, oq.OQ_BF16, 64, 256, None, FAKE, FAKE, 4, 64, FAKE, FAKE,
+                                FAKE, FAKE, None, None, 0, None)
+    assert st == WORKSPACE
+
+
+def test_act_rejects():
+    L = oq.lib()
+    assert L.oq_act_fakequant_fwd(FAKE, oq.OQ_BF16, 16, 256, 9, None, None, FAKE, oq.OQ_BF16,
+                                  None, None, None, None) == UNSUPPORTED
+    assert L.oq_act_fakequant_fwd(FAKE, oq.OQ_BF16, 16, 250, 4, None, None, FAKE, oq.OQ_BF16,
+                                  None, None, None, None) == INVALID
+    assert L.oq_act_fakequant_bwd(FAKE, oq.OQ_BF16, 16, 256, 4, None, None, FAKE, None, FAKE,
+                                  FAKE, None, 0, None) == WORKSPACE
+
+
+def _desc(w):
+    d = oq.BlockDesc()
+    d.tokens = w.T
+    d.n_sites, d.n_linears = len(w.sites), len(w.linears)
+    d.dtype = oq.OQ_BF16 if w.bf16 else oq.OQ_F32
+    for k, s in enumerate(w.sites):
+        d.site_width[k], d.site_let[k], d.site_act_bits[k] = s.width, int(s.let), s.act_bits
+    for l, lin in enumerate(w.linears):
+        d.lin_site[l], d.lin_c_out[l], d.lin_bits[l], d.lin_group[l] = lin.site, lin.c_out, lin.bits, lin.group
+    return d
+
+
+@pytest.mark.parametrize("w", configs.CONFIGS, ids=[c.name for c in configs.CONFIGS])
+def test_block_workspace_sizes(w):
+    n = C.c_size_t(0)
+    assert oq.lib().oq_block_workspace_size(C.byref(_desc(w)), C.byref(n)) == OK
+    T = w.T
+    es = 2 if w.bf16 else 4
+    biggest = max(sum(l.c_out for l in w.linears if l.site == k) for k in range(len(w.sites)))
+    # at least the largest stacked dY^T of one site
+    assert n.value >= biggest * T * es
+    assert n.value < 200 * 2 ** 30
+
+
+def test_block_desc_validation():
+    L = oq.lib()
+    n = C.c_size_t(0)
+    d = _desc(configs.C2)
+    d.lin_site[3] = 3                     # o_proj moved after down_proj's site: not consecutive
+    d.lin_site[6] = 1
+    assert L.oq_block_workspace_size(C.byref(d), C.byref(n)) == INVALID
+    d = _desc(configs.C2)
+    d.tokens = 100
+    assert L.oq_block_workspace_size(C.byref(d), C.byref(n)) == INVALID
+    d = _desc(configs.C2)
+    d.lin_bits[0] = 1
+    assert L.oq_block_workspace_size(C.byref(d), C.byref(n)) == UNSUPPORTED
+    d = _desc(configs.C2)
+    d.site_act_bits[0] = 12
+    assert L.oq_block_workspace_size(C.byref(d), C.byref(n)) == UNSUPPORTED
+    # a step with too small a workspace is refused before any launch
+    prm, grd = oq.BlockParams(), oq.BlockGrads()
+    d = _desc(configs.C1)
+    prm.W[0] = prm.gamma_logit[0] = prm.beta_logit[0] = 0x10000
+    grd.d_gamma_logit[0] = grd.d_beta_logit[0] = 0x10000
+    yp = (C.c_void_p * 1)(0x10000)
+    xp = (C.c_void_p * 1)(0x10000)
+    st = L.oq_block_calib_step(C.byref(d), yp, xp, C.byref(prm), C.byref(grd), None, FAKE, FAKE,
+                               16, None)
+    assert st == WORKSPACE
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(oq, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(oq, "_lib", None)
+    with pytest.raises(oq.OQError):
+        oq.lib()

@@ -1,0 +1,128 @@
+"""GPU parity of oq_block_calib_step against the oracle's block step.
+
+Each workload keeps the shape structure of its full-size configuration
+(seven LLaMA linears on four sites, GQA k/v, LET on three sites, per-token
+activation quantisation, per-channel or grouped weights) at sizes the oracle
+finishes in seconds, with a token count that leaves a ragged last tile.
+Bar: loss, row losses and every gradient within 2e-2 normwise relative error
+(bf16 matrix-core products); the fp32 workload within 1e-4."""
+import numpy as np
+import pytest
+import torch
+
+from oracle.adamw import LR_LET, LR_LWC, adamw
+from oracle.block import block_step
+from oracle.quant import lwc_fwd
+from paper_2308_13137_amd import configs, oq
+from tests.cases import dev, make_problem, normwise, small_llama
+
+pytestmark = pytest.mark.gpu
+
+TOL_BF16 = 2e-2
+TOL_F32 = 1e-4
+
+WORKLOADS = [
+    configs.C1,
+    small_llama("c2_small", hidden=256, ffn=768, T=264, w_bits=3, group=128),
+    small_llama("c3_small", hidden=256, ffn=512, T=264, w_bits=4, let=True, act_bits=4),
+    small_llama("c4_small", hidden=320, ffn=832, T=136, w_bits=2, group=64),
+    small_llama("c5_small", hidden=512, ffn=1024, T=200, w_bits=4, group=128, kv=128, sigma=0.015),
+    small_llama("let_noact", hidden=256, ffn=512, T=128, w_bits=4, group=64, let=True),
+]
+
+
+def run_gpu(w, P, update=False, blk=None):
+    dt = torch.bfloat16 if w.bf16 else torch.float32
+    if blk is None:
+        blk = oq.Block(w.T, [(s.width, s.let, s.act_bits) for s in w.sites],
+                       [(l.site, l.c_out, l.bits, l.group) for l in w.linears], dtype=dt)
+    X = [dev(x, dt) for x in P["X"]]
+    Y = [dev(np.ascontiguousarray(y.T), dt) for y in P["Y"]]          # channel-major target
+    W = [dev(x, dt) for x in P["W"]]
+    gl = [dev(x) for x in P["gamma_logit"]]
+    bl = [dev(x) for x in P["beta_logit"]]
+    s = [None if x is None else dev(x) for x in P["s"]]
+    d = [None if x is None else dev(x) for x in P["delta"]]
+    B = [None if x is None else dev(x) for x in P["B"]]
+    loss = blk.step(X, Y, W, gl, bl, s=s, delta=d, B=B, update=update)
+    torch.cuda.synchronize()
+    return blk, float(loss.cpu()), gl, bl, s, d
+
+
+def oracle_step(w, P):
+    params = dict(W=P["W"], B=P["B"], gamma_logit=P["gamma_logit"], beta_logit=P["beta_logit"],
+                  s=P["s"], delta=P["delta"])
+    return block_step(w.oracle_desc(), P["X"], P["Y"], params)
+
+
+@pytest.mark.parametrize("w", WORKLOADS, ids=[w.name for w in WORKLOADS])
+@pytest.mark.parametrize("logit", ["init", "random"])
+def test_block_step_parity(w, logit):
+    print(f"block step {w.name} T={w.T} logits={logit}", flush=True)
+    P = make_problem(w, seed=3, logit=logit, bias=(w.name == "let_noact"))
+    blk, loss, *_ = run_gpu(w, P)
+    ref_loss, ref = oracle_step(w, P)
+    tol = TOL_BF16 if w.bf16 else TOL_F32
+    errs = {"loss": abs(loss - ref_loss) / abs(ref_loss)}
+    for l in range(len(w.linears)):
+        errs[f"dgl{l}"] = normwise(blk.d_gamma[l].cpu().numpy(), ref["d_gamma_logit"][l])
+        errs[f"dbl{l}"] = normwise(blk.d_beta[l].cpu().numpy(), ref["d_beta_logit"][l])
+        errs[f"row{l}"] = normwise(blk.row_loss[l].cpu().numpy(), ref["row_loss"][l])
+    for k, site in enumerate(w.sites):
+        if site.let:
+            errs[f"ds{k}"] = normwise(blk.d_s[k].cpu().numpy(), ref["d_s"][k])
+            errs[f"dd{k}"] = normwise(blk.d_delta[k].cpu().numpy(), ref["d_delta"][k])
+    worst = max(errs, key=errs.get)
+    print(f"  worst {worst} = {errs[worst]:.3e}", flush=True)
+    assert errs[worst] < tol, errs
+
+
+def test_block_step_is_deterministic():
+    w = WORKLOADS[2]
+    P = make_problem(w, seed=4)
+    blk, l1, *_ = run_gpu(w, P)
+    g1 = [t.clone() for t in blk.d_gamma + blk.d_beta] + [blk.d_s[0].clone(), blk.d_delta[0].clone()]
+    _, l2, *_ = run_gpu(w, P, blk=blk)
+    g2 = blk.d_gamma + blk.d_beta + [blk.d_s[0], blk.d_delta[0]]
+    assert l1 == l2
+    for a, b in zip(g1, g2):
+        assert torch.equal(a, b)
+
+
+def test_twenty_step_trajectory():
+    """Twenty AdamW steps on a fixed batch (the 13B-shaped W2A16 g64 workload,
+    scaled down): the GPU loss trajectory follows the oracle's."""
+    w = small_llama("c4_traj", hidden=256, ffn=512, T=128, w_bits=2, group=64)
+    P = make_problem(w, seed=5)
+    blk = None
+    st = {}
+    params = dict(W=P["W"], B=P["B"], gamma_logit=[g.copy() for g in P["gamma_logit"]],
+                  beta_logit=[b.copy() for b in P["beta_logit"]], s=P["s"], delta=P["delta"])
+    mv = {k: [np.zeros_like(g, np.float64) for g in params[k]] for k in ("gamma_logit", "beta_logit")}
+    vv = {k: [np.zeros_like(g, np.float64) for g in params[k]] for k in ("gamma_logit", "beta_logit")}
+    dt = torch.bfloat16
+    blk = oq.Block(w.T, [(s.width, s.let, s.act_bits) for s in w.sites],
+                   [(l.site, l.c_out, l.bits, l.group) for l in w.linears], dtype=dt)
+    blk.init_optimizer()
+    X = [dev(x, dt) for x in P["X"]]
+    Y = [dev(np.ascontiguousarray(y.T), dt) for y in P["Y"]]
+    W = [dev(x, dt) for x in P["W"]]
+    gl = [dev(x) for x in P["gamma_logit"]]
+    bl = [dev(x) for x in P["beta_logit"]]
+    ours, refs = [], []
+    for step in range(1, 21):
+        ours.append(float(blk.step(X, Y, W, gl, bl, update=True).cpu()))
+        rl, g = block_step(w.oracle_desc(), P["X"], P["Y"], params)
+        refs.append(rl)
+        for key, gk in (("gamma_logit", "d_gamma_logit"), ("beta_logit", "d_beta_logit")):
+            for l in range(len(w.linears)):
+                p, mv[key][l], vv[key][l] = adamw(params[key][l], g[gk][l], mv[key][l],
+                                                  vv[key][l], step, LR_LWC)
+                params[key][l] = p.astype(np.float32)
+    print("  loss gpu", ["%.4e" % x for x in ours[::5]], "oracle", ["%.4e" % x for x in refs[::5]])
+    assert refs[-1] < refs[0]
+    assert ours[-1] < ours[0]
+    for a, b in zip(ours, refs):
+        assert abs(a - b) / abs(b) < TOL_BF16
+    for l in range(len(w.linears)):
+        assert normwise(gl[l].cpu().numpy(), params["gamma_logit"][l]) < 1e-3
