@@ -165,11 +165,13 @@ oq_status oq_matmul_nt(const void* A, const void* B, oq_dtype in_dt, int64_t M, 
 /* ---------------------------------------------------------------------------
  * AdamW update (Sec. 4.1: AdamW, zero weight decay; lr 5e-3 for the clipping
  * logits, 1e-2 for s and delta).  fp32, in place on p, m, v; step counts from 1.
+ * Hyperparameters are doubles: the coefficients 1 - b1, 1 - b2 and the bias
+ * corrections are formed in fp64 and rounded once to fp32.
  *   p = p*(1 - lr*wd);  m = b1*m + (1-b1)*g;  v = b2*v + (1-b2)*g*g
  *   p -= lr * (m / (1 - b1^step)) / (sqrt(v / (1 - b2^step)) + eps)
  */
-oq_status oq_adamw_step(float* p, const float* g, float* m, float* v, int64_t n, float lr,
-                        float beta1, float beta2, float eps, float wd, int step,
+oq_status oq_adamw_step(float* p, const float* g, float* m, float* v, int64_t n, double lr,
+                        double beta1, double beta2, double eps, double wd, int step,
                         hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
@@ -223,7 +225,7 @@ typedef struct {                           /* AdamW state; NULL pointer = no upd
   float* m_s[OQ_MAX_SITES];       float* v_s[OQ_MAX_SITES];
   float* m_delta[OQ_MAX_SITES];   float* v_delta[OQ_MAX_SITES];
   int step;                                /* 1-based step number of this update   */
-  float lr_lwc, lr_let, beta1, beta2, eps, wd;
+  double lr_lwc, lr_let, beta1, beta2, eps, wd;
 } oq_block_optim;
 
 oq_status oq_block_workspace_size(const oq_block_desc* desc, size_t* bytes);

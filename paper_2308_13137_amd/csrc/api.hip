@@ -373,15 +373,13 @@ oq_status oq_matmul_nt(const void* A, const void* B, oq_dtype in_dt, int64_t M, 
   return OQ_OK;
 }
 
-oq_status oq_adamw_step(float* p, const float* g, float* m, float* v, int64_t n, float lr,
-                        float beta1, float beta2, float eps, float wd, int step,
+oq_status oq_adamw_step(float* p, const float* g, float* m, float* v, int64_t n, double lr,
+                        double beta1, double beta2, double eps, double wd, int step,
                         hipStream_t stream) {
   OQ_REQ(p && g && m && v, "p, g, m, v are required");
   OQ_REQ(n >= 0 && step >= 1, "bad n or step");
-  const float bc1 = float(1.0 - std::pow(double(beta1), step));
-  const float bc2 = float(1.0 - std::pow(double(beta2), step));
   ProfScope ps(PK_OTHER, stream, double(n) * 28);
-  OQ_HIP(adamw(p, g, m, v, n, lr, beta1, beta2, eps, wd, bc1, bc2, stream), "adamw");
+  OQ_HIP(adamw(p, g, m, v, n, adam_coef(lr, beta1, beta2, eps, wd, step), stream), "adamw");
   return OQ_OK;
 }
 
@@ -687,25 +685,24 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     OQ_HIP(loss_finish(w.rl, la, loss, st), "loss");
   }
   if (opt) {
-    const float bc1 = float(1.0 - std::pow(double(opt->beta1), opt->step));
-    const float bc2 = float(1.0 - std::pow(double(opt->beta2), opt->step));
+    const AdamCoef cl = adam_coef(opt->lr_lwc, opt->beta1, opt->beta2, opt->eps, opt->wd, opt->step);
+    const AdamCoef ce = adam_coef(opt->lr_let, opt->beta1, opt->beta2, opt->eps, opt->wd, opt->step);
     ProfScope ps(PK_OTHER, st, 0);
     for (int l = 0; l < d->n_linears; ++l) {
       const int64_t n = d->lin_c_out[l] * (d->site_width[d->lin_site[l]] / d->lin_group[l]);
       OQ_HIP(adamw(prm->gamma_logit[l], gr->d_gamma_logit[l], opt->m_gamma[l], opt->v_gamma[l], n,
-                   opt->lr_lwc, opt->beta1, opt->beta2, opt->eps, opt->wd, bc1, bc2, st),
+                   cl, st),
              "adamw gamma");
-      OQ_HIP(adamw(prm->beta_logit[l], gr->d_beta_logit[l], opt->m_beta[l], opt->v_beta[l], n,
-                   opt->lr_lwc, opt->beta1, opt->beta2, opt->eps, opt->wd, bc1, bc2, st),
+      OQ_HIP(adamw(prm->beta_logit[l], gr->d_beta_logit[l], opt->m_beta[l], opt->v_beta[l], n, cl,
+                   st),
              "adamw beta");
     }
     for (const auto& p : plan) {
       if (!p.let) continue;
-      OQ_HIP(adamw(prm->s[p.k], gr->d_s[p.k], opt->m_s[p.k], opt->v_s[p.k], p.C, opt->lr_let,
-                   opt->beta1, opt->beta2, opt->eps, opt->wd, bc1, bc2, st),
+      OQ_HIP(adamw(prm->s[p.k], gr->d_s[p.k], opt->m_s[p.k], opt->v_s[p.k], p.C, ce, st),
              "adamw s");
       OQ_HIP(adamw(prm->delta[p.k], gr->d_delta[p.k], opt->m_delta[p.k], opt->v_delta[p.k], p.C,
-                   opt->lr_let, opt->beta1, opt->beta2, opt->eps, opt->wd, bc1, bc2, st),
+                   ce, st),
              "adamw delta");
     }
   }

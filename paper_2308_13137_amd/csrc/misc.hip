@@ -5,6 +5,8 @@
 // reproducible.
 #include <math.h>
 
+#include <cmath>
+
 #include "common.h"
 #include "oq_internal.h"
 
@@ -200,20 +202,17 @@ __global__ __launch_bounds__(256) void loss_finish_kernel(const double* rl, Loss
 
 // ------------------------------------------------------------------ AdamW
 __global__ __launch_bounds__(256) void adamw_kernel(float* p, const float* g, float* m, float* v,
-                                                    int64_t n, float lr, float b1, float b2,
-                                                    float eps, float wd, float bc1, float bc2) {
+                                                    int64_t n, AdamCoef c) {
   const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
   if (i >= n) return;
   const float gi = g[i];
-  const float mi = b1 * m[i] + (1.0f - b1) * gi;
-  const float vi = b2 * v[i] + (1.0f - b2) * (gi * gi);
+  const float mi = c.b1 * m[i] + c.omb1 * gi;
+  const float vi = c.b2 * v[i] + c.omb2 * (gi * gi);
   m[i] = mi;
   v[i] = vi;
-  float pi = p[i] * (1.0f - lr * wd);
-  const float mh = mi / bc1;
-  const float vh = vi / bc2;
-  pi = pi - lr * (mh / (__fsqrt_rn(vh) + eps));
-  p[i] = pi;
+  const float mh = mi / c.bc1;
+  const float vh = vi / c.bc2;
+  p[i] = p[i] * c.decay - c.lr * (mh / (__fsqrt_rn(vh) + c.eps));
 }
 
 }  // namespace
@@ -326,11 +325,25 @@ hipError_t loss_finish(const double* rl, LossArgs la, float* loss, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, float lr, float b1,
-                 float b2, float eps, float wd, float bc1, float bc2, hipStream_t st) {
+AdamCoef adam_coef(double lr, double b1, double b2, double eps, double wd, int step) {
+  AdamCoef c;
+  c.lr = float(lr);
+  c.b1 = float(b1);
+  c.omb1 = float(1.0 - b1);
+  c.b2 = float(b2);
+  c.omb2 = float(1.0 - b2);
+  c.eps = float(eps);
+  c.decay = float(1.0 - lr * wd);
+  c.bc1 = float(1.0 - std::pow(b1, double(step)));
+  c.bc2 = float(1.0 - std::pow(b2, double(step)));
+  return c;
+}
+
+hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, AdamCoef c,
+                 hipStream_t st) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(adamw_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p, g, m, v,
-                     n, lr, b1, b2, eps, wd, bc1, bc2);
+                     n, c);
   return hipGetLastError();
 }
 

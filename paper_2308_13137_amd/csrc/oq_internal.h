@@ -106,8 +106,13 @@ struct LossArgs {
   float* row_loss[16];
 };
 hipError_t loss_finish(const double* rl, LossArgs la, float* loss, hipStream_t st);
-hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, float lr, float b1,
-                 float b2, float eps, float wd, float bc1, float bc2, hipStream_t st);
+// AdamW with its fp32 coefficients formed in fp64 on the host.
+struct AdamCoef {
+  float lr, b1, omb1, b2, omb2, eps, decay, bc1, bc2;
+};
+AdamCoef adam_coef(double lr, double b1, double b2, double eps, double wd, int step);
+hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, AdamCoef c,
+                 hipStream_t st);
 // LET initialisation pieces
 int64_t colstat_nparts(int64_t rows);
 hipError_t colstat(const void* X, bool bf16, int64_t rows, int64_t cols, float* amax_parts,

@@ -20,7 +20,7 @@ PROF_KINDS = ["gemm_fwd", "gemm_wgrad", "gemm_dgrad", "lwc_fwd", "lwc_bwd", "act
               "act_bwd", "transpose", "other"]
 
 # name -> (restype, argtypes); the exported surface of include/oq.h
-_P, _I64, _I, _F, _SZ = C.c_void_p, C.c_int64, C.c_int, C.c_float, C.c_size_t
+_P, _I64, _I, _D, _SZ = C.c_void_p, C.c_int64, C.c_int, C.c_double, C.c_size_t
 _PSZ = C.POINTER(C.c_size_t)
 SIGNATURES = {
     "oq_status_str": (C.c_char_p, [_I]),
@@ -38,7 +38,7 @@ SIGNATURES = {
     "oq_let_init_workspace_size": (_I, [_I64, _I64, _P, _I, _PSZ]),
     "oq_fp_target": (_I, [_P, _P, _I, _P, _I64, _I64, _I64, _P, _P]),
     "oq_matmul_nt": (_I, [_P, _P, _I, _I64, _I64, _I64, _P, _I, _P]),
-    "oq_adamw_step": (_I, [_P, _P, _P, _P, _I64, _F, _F, _F, _F, _F, _I, _P]),
+    "oq_adamw_step": (_I, [_P, _P, _P, _P, _I64, _D, _D, _D, _D, _D, _I, _P]),
     "oq_block_workspace_size": (_I, [_P, _PSZ]),
     "oq_block_calib_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "oq_profile_enable": (_I, [_I]),
@@ -79,8 +79,9 @@ class BlockOptim(C.Structure):
                 ("m_beta", C.c_void_p * MAX_LINEARS), ("v_beta", C.c_void_p * MAX_LINEARS),
                 ("m_s", C.c_void_p * MAX_SITES), ("v_s", C.c_void_p * MAX_SITES),
                 ("m_delta", C.c_void_p * MAX_SITES), ("v_delta", C.c_void_p * MAX_SITES),
-                ("step", C.c_int), ("lr_lwc", C.c_float), ("lr_let", C.c_float),
-                ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float), ("wd", C.c_float)]
+                ("step", C.c_int), ("lr_lwc", C.c_double), ("lr_let", C.c_double),
+                ("beta1", C.c_double), ("beta2", C.c_double), ("eps", C.c_double),
+                ("wd", C.c_double)]
 
 
 _lib = None

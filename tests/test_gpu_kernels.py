@@ -64,9 +64,10 @@ def test_fp_target(bf16):
     ref = fp_target_ref(X, W, B, bf16=bf16)                  # [T, c_out]
     got = host(oq.fp_target(dev(X, dt), dev(W, dt), dev(B)))  # [c_out, T]
     if bf16:
-        # one bf16 rounding on each side of an fp32-vs-fp64 sum: at most 1 ulp apart
-        ulp = np.abs(ref.T) * 2.0 ** -7 + 1e-30
-        assert np.all(np.abs(got - ref.T) <= ulp)
+        # one bf16 rounding of an fp32 sum vs of an fp64 sum: nearly all equal,
+        # the rest one bf16 step apart (relative to the output's scale)
+        assert np.mean(got == ref.T) > 0.98
+        assert normwise(got, ref.T) <= 2.0 ** -8
     else:
         assert normwise(got, ref.T) < TOL_GEMM
 
