@@ -64,12 +64,22 @@ struct EpiResid {
   static constexpr bool kRows = true;
   struct Row { const T* yfp; T* dy; float scale; float b; };
   OQ_DEV Row row(int64_t m) const {
-    int s = 0;
-    while (s < a.nseg - 1 && m >= a.seg_end[s]) ++s;
+    // constant indices only, so the argument block stays in scalar registers
+    const void* y = a.yfp[0];
+    float sc = a.scale[0];
+    int64_t b = a.seg_begin[0];
+#pragma unroll
+    for (int s = 1; s < MAX_SEG; ++s) {
+      if (s < a.nseg && m >= a.seg_begin[s]) {
+        y = a.yfp[s];
+        sc = a.scale[s];
+        b = a.seg_begin[s];
+      }
+    }
     Row r;
-    r.yfp = reinterpret_cast<const T*>(a.yfp[s]) + (m - a.seg_begin[s]) * a.ld_yfp;
+    r.yfp = reinterpret_cast<const T*>(y) + (m - b) * a.ld_yfp;
     r.dy = reinterpret_cast<T*>(a.dy) + m * a.ld_dy;
-    r.scale = a.scale[s];
+    r.scale = sc;
     r.b = a.bias ? a.bias[m] : 0.0f;
     return r;
   }
@@ -94,7 +104,19 @@ struct EpiResid {
 // ------------------------------------------------------------------ bf16 MFMA kernel
 OQ_DEV bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
 
-template <class Epi>
+typedef __attribute__((address_space(1))) void gvoid_t;
+typedef __attribute__((address_space(3))) void lvoid_t;
+
+OQ_DEV void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// DIRECT = true (K a multiple of 64): tiles go global -> LDS with
+// global_load_lds_dwordx4, which writes lane i's 16 bytes at LDS base + 16 i.
+// One such instruction fills 8 tile rows (64 slots); lane i fetches the global
+// chunk that belongs in its slot, (i & 7) ^ row, so the LDS image is the same
+// XOR-swizzled layout the fragment reads expect.  Rows past M (N) are clamped
+// to the last valid row: they only feed output rows that are never stored.
+// DIRECT = false: 16-byte loads through registers with zero fill past M, N, K.
+template <class Epi, bool DIRECT>
 __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, int64_t M, int64_t N,
     int64_t K, int64_t lda, int64_t ldb, int tiles_m, int tiles_n, Epi epi) {
@@ -102,6 +124,7 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
   __shared__ float2 rowbuf[2][BM];
 
   const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
 
   // workgroup -> output tile: contiguous logical ranges per XCD, then
   // GROUP_M tile-rows swept column by column.
@@ -116,42 +139,37 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
   const int tm = first_m + li % gm, tn = li / gm;
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
 
-  // global -> LDS assignment: thread loads chunk (tid & 7) of rows (tid >> 3) + 32 i
-  const int lrow = tid >> 3, lch = tid & 7;
-  const int sw = lch ^ (lrow & 7);
-  const uint16_t* a_base = A + (m0 + lrow) * lda + lch * 8;
-  const uint16_t* b_base = B + (n0 + lrow) * ldb + lch * 8;
+  const int nk = int((K + BK - 1) / BK);
+
+  // ---- per-thread load plan
+  // DIRECT: instruction i of wave w fills tile rows 8 (4 i + w) .. +7; lane
+  //   covers row 8 (4 i + w) + (lane >> 3), global chunk (lane & 7) ^ (lane >> 3).
+  // register path: thread loads chunk (tid & 7) of rows (tid >> 3) + 32 i.
+  int64_t aoff[8], boff[8];
   uint32_t amask = 0, bmask = 0;
+  if constexpr (DIRECT) {
+    const int r0 = 8 * wave + (lane >> 3);
+    const int ch = (lane & 7) ^ (lane >> 3);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    if (m0 + lrow + 32 * i < M) amask |= 1u << i;
-    if (n0 + lrow + 32 * i < N) bmask |= 1u << i;
+    for (int i = 0; i < 8; ++i) {
+      const int64_t ra = min(m0 + r0 + 32 * i, M - 1);
+      const int64_t rb = min(n0 + r0 + 32 * i, N - 1);
+      aoff[i] = ra * lda + 8 * ch;
+      boff[i] = rb * ldb + 8 * ch;
+    }
+  } else {
+    const int lrow = tid >> 3, lch = tid & 7;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int64_t ra = m0 + lrow + 32 * i, rb = n0 + lrow + 32 * i;
+      if (ra < M) amask |= 1u << i;
+      if (rb < N) bmask |= 1u << i;
+      aoff[i] = (ra < M ? ra : 0) * lda + 8 * lch;
+      boff[i] = (rb < N ? rb : 0) * ldb + 8 * lch;
+    }
   }
+  const int sw_store = (tid & 7) ^ ((tid >> 3) & 7);   // register path slot
 
-  uint4 ra[8], rb[8];
-  const uint4 zero4 = make_uint4(0, 0, 0, 0);
-  auto gload = [&](int kt) {
-    const int64_t k = int64_t(kt) * BK;
-    const bool kv = k + lch * 8 < K;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      ra[i] = (kv && (amask >> i & 1u))
-                  ? *reinterpret_cast<const uint4*>(a_base + int64_t(32 * i) * lda + k)
-                  : zero4;
-      rb[i] = (kv && (bmask >> i & 1u))
-                  ? *reinterpret_cast<const uint4*>(b_base + int64_t(32 * i) * ldb + k)
-                  : zero4;
-    }
-  };
-  auto lstore = [&](int stage) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      lds[stage][0][(lrow + 32 * i) * 8 + sw] = ra[i];
-      lds[stage][1][(lrow + 32 * i) * 8 + sw] = rb[i];
-    }
-  };
-
-  const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int fr = lane & 15, fk = lane >> 4;
 
@@ -161,30 +179,90 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = int((K + BK - 1) / BK);
-  gload(0);
-  lstore(0);
+  uint4 ra[8], rb[8];
+
+  // ---- stage 0
+  if constexpr (DIRECT) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_global_load_lds((gvoid_t*)(A + aoff[i]),
+                                       (lvoid_t*)(&lds[0][0][(4 * i + wave) * 64]), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((gvoid_t*)(B + boff[i]),
+                                       (lvoid_t*)(&lds[0][1][(4 * i + wave) * 64]), 16, 0, 0);
+    }
+    wait_vm0();
+  } else {
+    const bool kv = (tid & 7) * 8 < K;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      ra[i] = (kv && (amask >> i & 1u)) ? *reinterpret_cast<const uint4*>(A + aoff[i]) : make_uint4(0, 0, 0, 0);
+      rb[i] = (kv && (bmask >> i & 1u)) ? *reinterpret_cast<const uint4*>(B + boff[i]) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      lds[0][0][((tid >> 3) + 32 * i) * 8 + sw_store] = ra[i];
+      lds[0][1][((tid >> 3) + 32 * i) * 8 + sw_store] = rb[i];
+    }
+  }
   __syncthreads();
 
   for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload(kt + 1);
-    const uint4* As = lds[kt & 1][0];
-    const uint4* Bs = lds[kt & 1][1];
+    const int cur = kt & 1, nxt = cur ^ 1;
+    const bool more = kt + 1 < nk;
+    const int64_t knext = int64_t(kt + 1) * BK;
+    // 1. the whole K-slice of this wave's fragments into registers
+    const uint4* As = lds[cur][0];
+    const uint4* Bs = lds[cur][1];
+    bf16x8_t af[2][8], bfr[2][8];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       const int ch = (kk * 4 + fk) ^ (fr & 7);
-      bf16x8_t af[8], bfr[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) af[i] = as_bf16x8(As[(wm * 128 + 16 * i + fr) * 8 + ch]);
+      for (int i = 0; i < 8; ++i) af[kk][i] = as_bf16x8(As[(wm * 128 + 16 * i + fr) * 8 + ch]);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) bfr[j] = as_bf16x8(Bs[(wn * 128 + 16 * j + fr) * 8 + ch]);
+      for (int j = 0; j < 8; ++j) bfr[kk][j] = as_bf16x8(Bs[(wn * 128 + 16 * j + fr) * 8 + ch]);
+    }
+    // 2. next stage in flight (the other LDS buffer, free since the last barrier)
+    if (more) {
+      if constexpr (DIRECT) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          __builtin_amdgcn_global_load_lds((gvoid_t*)(A + aoff[i] + knext),
+                                           (lvoid_t*)(&lds[nxt][0][(4 * i + wave) * 64]), 16, 0, 0);
+          __builtin_amdgcn_global_load_lds((gvoid_t*)(B + boff[i] + knext),
+                                           (lvoid_t*)(&lds[nxt][1][(4 * i + wave) * 64]), 16, 0, 0);
+        }
+      } else {
+        const bool kv = knext + (tid & 7) * 8 < K;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          ra[i] = (kv && (amask >> i & 1u)) ? *reinterpret_cast<const uint4*>(A + aoff[i] + knext)
+                                            : make_uint4(0, 0, 0, 0);
+          rb[i] = (kv && (bmask >> i & 1u)) ? *reinterpret_cast<const uint4*>(B + boff[i] + knext)
+                                            : make_uint4(0, 0, 0, 0);
+        }
+      }
+    }
+    // 3. 128 matrix instructions on the registers
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[kk][i], bfr[kk][j], acc[i][j], 0, 0, 0);
+    // 4. next stage complete and visible to every wave
+    if (more) {
+      if constexpr (DIRECT) {
+        wait_vm0();
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          lds[nxt][0][((tid >> 3) + 32 * i) * 8 + sw_store] = ra[i];
+          lds[nxt][1][((tid >> 3) + 32 * i) * 8 + sw_store] = rb[i];
+        }
+      }
     }
-    if (kt + 1 < nk) lstore((kt + 1) & 1);
     __syncthreads();
   }
 
@@ -291,9 +369,15 @@ hipError_t launch(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
   if (bf16) {
     const int64_t tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
     if (tm * tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(gemm_bf16_kernel<Epi>, dim3(unsigned(tm * tn)), dim3(NTHR), 0, st,
-                       static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N, K,
-                       lda, ldb, int(tm), int(tn), epi);
+    const bool direct = K % BK == 0 && lda % 8 == 0 && ldb % 8 == 0 && K > 0;
+    if (direct)
+      hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true>), dim3(unsigned(tm * tn)), dim3(NTHR), 0, st,
+                         static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N, K,
+                         lda, ldb, int(tm), int(tn), epi);
+    else
+      hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false>), dim3(unsigned(tm * tn)), dim3(NTHR), 0,
+                         st, static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N,
+                         K, lda, ldb, int(tm), int(tn), epi);
   } else {
     const int64_t tm = (M + F32_TILE - 1) / F32_TILE, tn = (N + F32_TILE - 1) / F32_TILE;
     if (tm > 65535 || tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
