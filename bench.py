@@ -1,0 +1,214 @@
+#!/usr/bin/env python3
+"""Benchmark of one OmniQuant block-wise calibration step on one MI355X.
+
+A step is the whole hot path on one batch: LWC fake-quant of the block's
+seven linears, the forward matrix products with the residual epilogue, the
+loss, the weight-gradient products, the straight-through clipping gradients
+(plus, for LET workloads, the activation-side products and LET gradients) and
+the AdamW update.  Inputs are synthetic (seeded, drawn on the GPU), resident
+in HBM before the timed region; the full-precision targets are produced once
+before timing, as Algorithm 1 does once per block.
+
+    python bench.py [--steps K] [--warmup W] [--config NAME] [--tokens T]
+
+Prints one JSON line.  ``roofline`` describes the dominant kernel kind,
+timed with HIP events on the launching stream during the timed steps;
+``cpu_baseline`` times the CPU oracle on a bounded sample of the same
+workload (rank 0, one GPU only).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK = {"mfma_bf16_tflops": 2500.0, "fp32_tflops": 157.3, "hbm_gbs": 8000.0}
+GEMM_KINDS = ("gemm_fwd", "gemm_wgrad", "gemm_dgrad")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def make_inputs(w, device="cuda"):
+    import torch
+
+    from paper_2308_13137_amd import inputs, oq
+    dt = torch.bfloat16 if w.bf16 else torch.float32
+    gen = torch.Generator(device=device)
+    gen.manual_seed(inputs.SEED)
+    X = []
+    for s in w.sites:
+        if w.x_recipe == "small":
+            x = torch.randn((w.T, s.width), generator=gen, device=device)
+        else:
+            x = inputs.torch_activations(gen, w.T, s.width, dtype=dt, device=device)
+        X.append(x.to(dt).contiguous())
+    W = [inputs.torch_weights(gen, l.c_out, w.c_in(i), w.w_sigma, w.w_outlier, dtype=dt,
+                              device=device).contiguous() for i, l in enumerate(w.linears)]
+    Y = [oq.fp_target(X[l.site], W[i]) for i, l in enumerate(w.linears)]
+    gl = [torch.full((l.c_out, w.c_in(i) // l.group), 4.0, device=device)
+          for i, l in enumerate(w.linears)]
+    bl = [g.clone() for g in gl]
+    s, d = [], []
+    for k, site in enumerate(w.sites):
+        if site.let:
+            Ws = [W[i] for i, l in enumerate(w.linears) if l.site == k]
+            sk, dk = oq.let_init(X[k], Ws)
+            s.append(sk)
+            d.append(dk)
+        else:
+            s.append(None)
+            d.append(None)
+    return X, W, Y, gl, bl, s, d
+
+
+def cpu_baseline(w, tokens):
+    """Time the oracle's step on the same block at ``tokens`` tokens."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle.block import block_step, fp_target
+    from oracle.let import let_init
+    from paper_2308_13137_amd import inputs
+    import torch
+
+    ws = w.with_tokens(tokens)
+
+    def bf(a):
+        return torch.from_numpy(a).to(torch.bfloat16).float().numpy() if ws.bf16 else a
+    X = [bf(inputs.activations(inputs.rng_for(77, k), tokens, s.width)) for k, s in enumerate(ws.sites)]
+    W = [bf(inputs.weights(inputs.rng_for(78, i), l.c_out, ws.c_in(i), ws.w_sigma, ws.w_outlier))
+         for i, l in enumerate(ws.linears)]
+    Y = [fp_target(X[l.site], W[i], None, bf16=ws.bf16) for i, l in enumerate(ws.linears)]
+    gl = [np.full((l.c_out, ws.c_in(i) // l.group), 4.0, np.float32) for i, l in enumerate(ws.linears)]
+    s = [let_init(X[k], [W[i] for i, l in enumerate(ws.linears) if l.site == k])[0] if st.let else None
+         for k, st in enumerate(ws.sites)]
+    d = [let_init(X[k], [W[i] for i, l in enumerate(ws.linears) if l.site == k])[1] if st.let else None
+         for k, st in enumerate(ws.sites)]
+    params = dict(W=W, B=[None] * len(W), gamma_logit=gl, beta_logit=[g.copy() for g in gl], s=s, delta=d)
+    t0 = time.perf_counter()
+    block_step(ws.oracle_desc(), X, Y, params)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": round(tokens / dt, 3), "unit": "calibration tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"one full {w.name} block step (all {len(w.linears)} linears, LWC fwd/bwd on "
+                      f"every weight, fp64 products) at {tokens} tokens, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="llama7b_w3a16_g128")
+    ap.add_argument("--tokens", type=int, default=None, help="tokens per step (default: the workload's)")
+    ap.add_argument("--cpu-tokens", type=int, default=64)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures the calibration step on one GPU; --gpus {args.gpus} is not "
+              "supported (the step is single-GPU; sharding is described, not run).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2308_13137_amd import configs, oq
+
+    w = configs.BY_NAME[args.config]
+    if args.tokens:
+        w = w.with_tokens(args.tokens)
+    torch.cuda.set_device(0)
+    oq.lib()
+    log(f"[bench] {w.name}: T={w.T}, {len(w.linears)} linears, {w.n_params / 1e6:.1f} M weights")
+    X, W, Y, gl, bl, s, d = make_inputs(w)
+    dt = torch.bfloat16 if w.bf16 else torch.float32
+    blk = oq.Block(w.T, [(st.width, st.let, st.act_bits) for st in w.sites],
+                   [(l.site, l.c_out, l.bits, l.group) for l in w.linears], dtype=dt)
+    blk.init_optimizer()
+    torch.cuda.synchronize()
+    log(f"[bench] inputs resident, workspace {blk.ws_bytes / 2**30:.1f} GiB; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        blk.step(X, Y, W, gl, bl, s=s, delta=d, update=True)
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+
+    oq.profile_reset()
+    oq.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        blk.step(X, Y, W, gl, bl, s=s, delta=d, update=True)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    oq.profile_enable(False)
+    prof = oq.profile_read()
+    loss = float(blk.loss.cpu())
+
+    ms = (t1 - t0) * 1e3 / args.steps
+    value = w.T / (ms / 1e3)
+
+    kernels = {}
+    for kind, (n, kms, work) in prof.items():
+        if n == 0:
+            continue
+        ent = {"launches_per_step": n / args.steps, "ms_per_step": round(kms / args.steps, 4)}
+        if kind in GEMM_KINDS:
+            ent["tflops"] = round(work / (kms / 1e3) / 1e12, 1)
+        elif work > 0:
+            ent["gbs"] = round(work / (kms / 1e3) / 1e9, 1)
+        kernels[kind] = ent
+    dom = max(prof, key=lambda k: prof[k][1])
+    n, kms, work = prof[dom]
+    if dom in GEMM_KINDS:
+        achieved = work / n / (kms / n / 1e3) / 1e12
+        roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1),
+                "peak": PEAK["mfma_bf16_tflops"] if w.bf16 else PEAK["fp32_tflops"],
+                "unit": "TFLOP/s"}
+    else:
+        achieved = work / n / (kms / n / 1e3) / 1e9
+        roof = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
+                "peak": PEAK["hbm_gbs"], "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["avg_launch_ms"] = round(kms / n, 4)
+    roof["traffic"] = None
+
+    line = {
+        "metric": "calibration tokens/s per block fwd+bwd step",
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.bf16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "tokens_per_step": w.T, "linears": len(w.linears),
+                   "weights": w.n_params, "w_bits": w.linears[0].bits,
+                   "group": w.linears[0].group, "let": any(st.let for st in w.sites),
+                   "act_bits": w.sites[0].act_bits, "parallelism": "single GPU"},
+        "loss": loss,
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        del X, W, Y, blk
+        torch.cuda.empty_cache()
+        log(f"[bench] CPU oracle on a {args.cpu_tokens}-token sample")
+        line["cpu_baseline"] = cpu_baseline(w, args.cpu_tokens)
+    else:
+        line["cpu_baseline"] = None
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
