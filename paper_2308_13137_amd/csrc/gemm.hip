@@ -29,14 +29,25 @@ constexpr int GROUP_M = 8;
 constexpr int F32_TILE = 64;
 
 // ------------------------------------------------------------------ epilogues
+// An epilogue sees the accumulators of one output row m in chunks of up to
+// eight consecutive columns n .. n + cnt - 1: row(m) prepares the row,
+// apply8 stores the chunk (16/32-byte vectors when vec) and returns its
+// contributions to the row partials, finish writes one row's partials.
 struct EpiF32 {
   float* C;
   int64_t ldc;
+  bool vec;
   static constexpr bool kRows = false;
   struct Row { float* c; };
   OQ_DEV Row row(int64_t m) const { return Row{C + m * ldc}; }
-  OQ_DEV float2 apply(const Row& r, int64_t n, float v) const {
-    r.c[n] = v;
+  OQ_DEV float2 apply8(const Row& r, int64_t n, const float* v, int cnt) const {
+    if (vec && cnt == 8) {
+      store8(r.c + n, v);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (e < cnt) r.c[n + e] = v[e];
+    }
     return make_float2(0.f, 0.f);
   }
   OQ_DEV void finish(int64_t, int, float, float) const {}
@@ -47,11 +58,21 @@ struct EpiStore {
   TC* C;
   int64_t ldc;
   const float* bias;
+  bool vec;
   static constexpr bool kRows = false;
   struct Row { TC* c; float b; };
   OQ_DEV Row row(int64_t m) const { return Row{C + m * ldc, bias ? bias[m] : 0.0f}; }
-  OQ_DEV float2 apply(const Row& r, int64_t n, float v) const {
-    store1(r.c + n, v + r.b);
+  OQ_DEV float2 apply8(const Row& r, int64_t n, const float* v, int cnt) const {
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = v[e] + r.b;
+    if (vec && cnt == 8) {
+      store8(r.c + n, o);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (e < cnt) store1(r.c + n + e, o[e]);
+    }
     return make_float2(0.f, 0.f);
   }
   OQ_DEV void finish(int64_t, int, float, float) const {}
@@ -61,6 +82,7 @@ struct EpiStore {
 template <typename T>
 struct EpiResid {
   ResidArgs a;
+  bool vec;
   static constexpr bool kRows = true;
   struct Row { const T* yfp; T* dy; float scale; float b; };
   OQ_DEV Row row(int64_t m) const {
@@ -83,15 +105,36 @@ struct EpiResid {
     r.b = a.bias ? a.bias[m] : 0.0f;
     return r;
   }
-  OQ_DEV float2 apply(const Row& r, int64_t n, float v) const {
-    float y = v + r.b;
-    float res = y - load1(r.yfp + n);
-    float d = res * r.scale;
-    store1(r.dy + n, d);
-    float dq = load1_rounded(d);
-    return make_float2(res * res, dq);
+  OQ_DEV float2 apply8(const Row& r, int64_t n, const float* v, int cnt) const {
+    float yf[8], d[8];
+    const bool full = vec && cnt == 8;
+    if (full) {
+      load8(r.yfp + n, yf);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) yf[e] = e < cnt ? load1(r.yfp + n + e) : 0.0f;
+    }
+    float sq = 0.f, sdy = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float y = v[e] + r.b;
+      const float res = y - yf[e];
+      d[e] = res * r.scale;
+      if (e < cnt) {
+        sq += res * res;
+        sdy += rounded(d[e]);
+      }
+    }
+    if (full) {
+      store8(r.dy + n, d);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (e < cnt) store1(r.dy + n + e, d[e]);
+    }
+    return make_float2(sq, sdy);
   }
-  OQ_DEV static float load1_rounded(float d) {
+  OQ_DEV static float rounded(float d) {
     if constexpr (sizeof(T) == 2) return bf2f(f2bf(d));
     else return d;
   }
@@ -100,6 +143,69 @@ struct EpiResid {
     if (a.part_dy) a.part_dy[m * a.ntn + tn] = dy;
   }
 };
+
+// ------------------------------------------------------------------ bf16 epilogue
+// The 128x128 fp32 quadrant of each wave goes through LDS in four passes of 32
+// rows (row pitch 132 floats: the four row groups a fragment store touches
+// land 16 banks apart), then every lane takes 8 consecutive columns of one
+// row: global traffic is 16-byte vectors, 256 contiguous bytes per 16 lanes.
+// Row partials: 8 columns per lane, a butterfly over the 16 lanes of the row,
+// then the two waves of a tile row in a fixed order.
+constexpr int EPI_PITCH = 132;
+
+template <int P, class Epi>
+OQ_DEV void epilogue_pass(f32x4_t (&acc)[8][8], const Epi& epi, int64_t m0, int64_t M, int wm,
+                          int wn, int fr, int fk, int64_t nb, int cnt, float* reg,
+                          float2 (*rowbuf)[BM]) {
+#pragma unroll
+  for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        reg[(16 * ii + 4 * fk + r) * EPI_PITCH + 16 * j + fr] = acc[2 * P + ii][j][r];
+  for (int it = 0; it < 8; ++it) {
+    const int rloc = fk + 4 * it;
+    const int trow = wm * 128 + 32 * P + rloc;
+    const int64_t m = m0 + trow;
+    float v[8];
+    const float4 a = *reinterpret_cast<const float4*>(reg + rloc * EPI_PITCH + 8 * fr);
+    const float4 b = *reinterpret_cast<const float4*>(reg + rloc * EPI_PITCH + 8 * fr + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    float2 c = make_float2(0.f, 0.f);
+    if (m < M && cnt > 0) c = epi.apply8(epi.row(m), nb, v, cnt);
+    if constexpr (Epi::kRows) {
+      c.x = group_sum<16>(c.x);
+      c.y = group_sum<16>(c.y);
+      if (fr == 0) rowbuf[wn][trow] = c;
+    }
+  }
+}
+
+template <class Epi>
+OQ_DEV void epilogue_lds(f32x4_t (&acc)[8][8], const Epi& epi, int64_t m0, int64_t n0, int64_t M,
+                         int64_t N, int tn, int wave, int lane, float* scratch,
+                         float2 (*rowbuf)[BM]) {
+  const int wm = wave >> 1, wn = wave & 1;
+  const int fr = lane & 15, fk = lane >> 4;
+  float* reg = scratch + wave * (32 * EPI_PITCH);
+  const int64_t nb = n0 + wn * 128 + 8 * fr;
+  const int cnt = int(max<int64_t>(0, min<int64_t>(8, N - nb)));
+  epilogue_pass<0>(acc, epi, m0, M, wm, wn, fr, fk, nb, cnt, reg, rowbuf);
+  epilogue_pass<1>(acc, epi, m0, M, wm, wn, fr, fk, nb, cnt, reg, rowbuf);
+  epilogue_pass<2>(acc, epi, m0, M, wm, wn, fr, fk, nb, cnt, reg, rowbuf);
+  epilogue_pass<3>(acc, epi, m0, M, wm, wn, fr, fk, nb, cnt, reg, rowbuf);
+  if constexpr (Epi::kRows) {
+    __syncthreads();
+    const int tid = threadIdx.x;
+    const int64_t m = m0 + tid;
+    if (m < M) {
+      float2 p0 = rowbuf[0][tid], p1 = rowbuf[1][tid];
+      epi.finish(m, tn, p0.x + p1.x, p0.y + p1.y);
+    }
+  }
+}
 
 // ------------------------------------------------------------------ bf16 MFMA kernel
 OQ_DEV bf16x8_t as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8_t, v); }
@@ -266,42 +372,9 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
     __syncthreads();
   }
 
-  // fragment (i, j) element r of lane (fr, fk) is C[16 i + 4 fk + r][16 j + fr] of the quadrant
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int trow = wm * 128 + 16 * i + 4 * fk + r;
-      const int64_t m = m0 + trow;
-      const bool mv = m < M;
-      float sq = 0.f, sdy = 0.f;
-      if (mv) {
-        auto rowc = epi.row(m);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int64_t n = n0 + wn * 128 + 16 * j + fr;
-          if (n < N) {
-            float2 c = epi.apply(rowc, n, acc[i][j][r]);
-            sq += c.x;
-            sdy += c.y;
-          }
-        }
-      }
-      if constexpr (Epi::kRows) {
-        sq = group_sum<16>(sq);
-        sdy = group_sum<16>(sdy);
-        if (fr == 0) rowbuf[wn][trow] = make_float2(sq, sdy);
-      }
-    }
-  }
-  if constexpr (Epi::kRows) {
-    __syncthreads();
-    const int64_t m = m0 + tid;
-    if (m < M) {
-      float2 p0 = rowbuf[0][tid], p1 = rowbuf[1][tid];
-      epi.finish(m, tn, p0.x + p1.x, p0.y + p1.y);
-    }
-  }
+  // the loop ended with a barrier: every LDS read is done
+  epilogue_lds(acc, epi, m0, n0, M, N, tn, wave, lane, reinterpret_cast<float*>(&lds[0][0][0]),
+               rowbuf);
 }
 
 // ------------------------------------------------------------------ fp32 kernel
@@ -348,7 +421,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
       for (int j = 0; j < 4; ++j) {
         const int64_t n = n0 + tx * 4 + j;
         if (n < N) {
-          float2 c = epi.apply(rowc, n, acc[i][j]);
+          float v1[8] = {acc[i][j], 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+          float2 c = epi.apply8(rowc, n, v1, 1);
           sq += c.x;
           sdy += c.y;
         }
@@ -395,24 +469,29 @@ int gemm_part_tile_n(bool bf16) { return bf16 ? BN : F32_TILE; }
 hipError_t gemm_nt_f32out(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
                           int64_t K, int64_t lda, int64_t ldb, float* C, int64_t ldc,
                           hipStream_t st) {
-  return launch(A, B, bf16, M, N, K, lda, ldb, EpiF32{C, ldc}, st);
+  const bool vec = ldc % 8 == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
+  return launch(A, B, bf16, M, N, K, lda, ldb, EpiF32{C, ldc, vec}, st);
 }
 
 hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
                          int64_t K, int64_t lda, int64_t ldb, void* C, bool c_bf16, int64_t ldc,
                          const float* bias, hipStream_t st) {
+  const bool vec = ldc % 8 == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
   if (c_bf16)
     return launch(A, B, bf16, M, N, K, lda, ldb,
-                  EpiStore<uint16_t>{static_cast<uint16_t*>(C), ldc, bias}, st);
-  return launch(A, B, bf16, M, N, K, lda, ldb, EpiStore<float>{static_cast<float*>(C), ldc, bias},
-                st);
+                  EpiStore<uint16_t>{static_cast<uint16_t*>(C), ldc, bias, vec}, st);
+  return launch(A, B, bf16, M, N, K, lda, ldb,
+                EpiStore<float>{static_cast<float*>(C), ldc, bias, vec}, st);
 }
 
 hipError_t gemm_nt_resid(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
                          int64_t K, int64_t lda, int64_t ldb, ResidArgs ra, hipStream_t st) {
   ra.ntn = int((N + gemm_part_tile_n(bf16) - 1) / gemm_part_tile_n(bf16));
-  if (bf16) return launch(A, B, true, M, N, K, lda, ldb, EpiResid<uint16_t>{ra}, st);
-  return launch(A, B, false, M, N, K, lda, ldb, EpiResid<float>{ra}, st);
+  bool vec = ra.ld_yfp % 8 == 0 && ra.ld_dy % 8 == 0 &&
+             (reinterpret_cast<uintptr_t>(ra.dy) & 15) == 0;
+  for (int s = 0; s < ra.nseg; ++s) vec = vec && (reinterpret_cast<uintptr_t>(ra.yfp[s]) & 15) == 0;
+  if (bf16) return launch(A, B, true, M, N, K, lda, ldb, EpiResid<uint16_t>{ra, vec}, st);
+  return launch(A, B, false, M, N, K, lda, ldb, EpiResid<float>{ra, vec}, st);
 }
 
 }  // namespace oq
