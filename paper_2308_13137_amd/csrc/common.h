@@ -11,6 +11,7 @@
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // ------------------------------------------------------------------ bf16 <-> fp32
 OQ_DEV float bf2f(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }

@@ -215,6 +215,23 @@ typedef __attribute__((address_space(3))) void lvoid_t;
 
 OQ_DEV void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// 16-byte global -> LDS copy for every lane of the wave (lane i's bytes land
+// at LDS byte address lds_addr + 16 i).  Issued as inline assembly so the
+// compiler does not model it as an LDS write and adds no wait in front of
+// the reads of the other stage; the kernel waits for it (vmcnt) itself
+// before the barrier that publishes the stage.
+OQ_DEV void dma16(const void* g, uint32_t lds_addr) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_addr);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(m0v), "v"(g)
+               : "memory", "m0");
+}
+OQ_DEV uint32_t lds_addr_of(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
+      (__attribute__((address_space(3))) const char*)(p)));
+}
+
 // DIRECT = true (K a multiple of 64): tiles go global -> LDS with
 // global_load_lds_dwordx4, which writes lane i's 16 bytes at LDS base + 16 i.
 // One such instruction fills 8 tile rows (64 slots); lane i fetches the global
@@ -291,10 +308,8 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
   if constexpr (DIRECT) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_global_load_lds((gvoid_t*)(A + aoff[i]),
-                                       (lvoid_t*)(&lds[0][0][(4 * i + wave) * 64]), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds((gvoid_t*)(B + boff[i]),
-                                       (lvoid_t*)(&lds[0][1][(4 * i + wave) * 64]), 16, 0, 0);
+      dma16(A + aoff[i], lds_addr_of(&lds[0][0][(4 * i + wave) * 64]));
+      dma16(B + boff[i], lds_addr_of(&lds[0][1][(4 * i + wave) * 64]));
     }
     wait_vm0();
   } else {
@@ -316,27 +331,14 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
     const int cur = kt & 1, nxt = cur ^ 1;
     const bool more = kt + 1 < nk;
     const int64_t knext = int64_t(kt + 1) * BK;
-    // 1. the whole K-slice of this wave's fragments into registers
-    const uint4* As = lds[cur][0];
-    const uint4* Bs = lds[cur][1];
-    bf16x8_t af[2][8], bfr[2][8];
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int ch = (kk * 4 + fk) ^ (fr & 7);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) af[kk][i] = as_bf16x8(As[(wm * 128 + 16 * i + fr) * 8 + ch]);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) bfr[kk][j] = as_bf16x8(Bs[(wn * 128 + 16 * j + fr) * 8 + ch]);
-    }
-    // 2. next stage in flight (the other LDS buffer, free since the last barrier)
+    // 1. next stage in flight (the other LDS buffer, free since the last
+    //    barrier): it has this whole iteration to arrive
     if (more) {
       if constexpr (DIRECT) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          __builtin_amdgcn_global_load_lds((gvoid_t*)(A + aoff[i] + knext),
-                                           (lvoid_t*)(&lds[nxt][0][(4 * i + wave) * 64]), 16, 0, 0);
-          __builtin_amdgcn_global_load_lds((gvoid_t*)(B + boff[i] + knext),
-                                           (lvoid_t*)(&lds[nxt][1][(4 * i + wave) * 64]), 16, 0, 0);
+          dma16(A + aoff[i] + knext, lds_addr_of(&lds[nxt][0][(4 * i + wave) * 64]));
+          dma16(B + boff[i] + knext, lds_addr_of(&lds[nxt][1][(4 * i + wave) * 64]));
         }
       } else {
         const bool kv = knext + (tid & 7) * 8 < K;
@@ -348,6 +350,18 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
                                             : make_uint4(0, 0, 0, 0);
         }
       }
+    }
+    // 2. the whole K-slice of this wave's fragments into registers
+    const uint4* As = lds[cur][0];
+    const uint4* Bs = lds[cur][1];
+    bf16x8_t af[2][8], bfr[2][8];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int ch = (kk * 4 + fk) ^ (fr & 7);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) af[kk][i] = as_bf16x8(As[(wm * 128 + 16 * i + fr) * 8 + ch]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) bfr[kk][j] = as_bf16x8(Bs[(wn * 128 + 16 * j + fr) * 8 + ch]);
     }
     // 3. 128 matrix instructions on the registers
 #pragma unroll
@@ -375,6 +389,146 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
   // the loop ended with a barrier: every LDS read is done
   epilogue_lds(acc, epi, m0, n0, M, N, tn, wave, lane, reinterpret_cast<float*>(&lds[0][0][0]),
                rowbuf);
+}
+
+// ------------------------------------------------------------------ bf16 8-wave kernel
+// K % 64 == 0.  Same 256x256x64 tile, LDS stages and swizzle as above, but
+// eight waves (two per SIMD) each own a 128x64 block (2 x 4 waves).  While
+// one wave of a SIMD waits on its LDS reads the other issues matrix
+// instructions, so the hardware overlaps what a single wave serialises.
+// Per wave: 8 x 4 fragments of v_mfma_f32_16x16x32_bf16 (128 accumulators).
+constexpr int NTHR8 = 512;
+constexpr int EPI8_PITCH = 68;
+
+template <class Epi>
+__global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
+    const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, int64_t M, int64_t N,
+    int64_t K, int64_t lda, int64_t ldb, int tiles_m, int tiles_n, Epi epi) {
+  __shared__ uint4 lds[2][2][BM * BK / 8];
+  __shared__ float2 rowbuf[4][BM];
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int nblk = gridDim.x, bid = blockIdx.x;
+  const int xcd = bid & 7, local = bid >> 3, q = nblk >> 3, rem = nblk & 7;
+  const int L = xcd * q + min(xcd, rem) + local;
+  const int group_sz = GROUP_M * tiles_n;
+  const int g = L / group_sz;
+  const int first_m = g * GROUP_M;
+  const int gm = min(GROUP_M, tiles_m - first_m);
+  const int li = L - g * group_sz;
+  const int tm = first_m + li % gm, tn = li / gm;
+  const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
+  const int nk = int(K / BK);
+
+  // DMA plan: instruction i of wave w fills tile rows 8 (8 i + w) .. +7
+  int64_t aoff[4], boff[4];
+  {
+    const int ch = (lane & 7) ^ (lane >> 3);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 64 * i + 8 * wave + (lane >> 3);
+      aoff[i] = min(m0 + row, M - 1) * lda + 8 * ch;
+      boff[i] = min(n0 + row, N - 1) * ldb + 8 * ch;
+    }
+  }
+  const int wm = wave >> 2, wn = wave & 3;
+  const int fr = lane & 15, fk = lane >> 4;
+
+  f32x4_t acc[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    dma16(A + aoff[i], lds_addr_of(&lds[0][0][(8 * i + wave) * 64]));
+    dma16(B + boff[i], lds_addr_of(&lds[0][1][(8 * i + wave) * 64]));
+  }
+  wait_vm0();
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1, nxt = cur ^ 1;
+    if (kt + 1 < nk) {
+      const int64_t knext = int64_t(kt + 1) * BK;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        dma16(A + aoff[i] + knext, lds_addr_of(&lds[nxt][0][(8 * i + wave) * 64]));
+        dma16(B + boff[i] + knext, lds_addr_of(&lds[nxt][1][(8 * i + wave) * 64]));
+      }
+    }
+    const uint4* As = lds[cur][0];
+    const uint4* Bs = lds[cur][1];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int ch = (kk * 4 + fk) ^ (fr & 7);
+      bf16x8_t af[8], bfr[4];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) af[i] = as_bf16x8(As[(wm * 128 + 16 * i + fr) * 8 + ch]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bfr[j] = as_bf16x8(Bs[(wn * 64 + 16 * j + fr) * 8 + ch]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) wait_vm0();
+    __syncthreads();
+  }
+
+  // epilogue: each wave's 128x64 block through LDS in four passes of 32 rows;
+  // a lane then takes 8 consecutive columns of one row (8 lanes per row).
+  float* reg = reinterpret_cast<float*>(&lds[0][0][0]) + wave * (32 * EPI8_PITCH);
+  const int cl = lane & 7, rl = lane >> 3;
+  const int64_t nb = n0 + wn * 64 + 8 * cl;
+  const int cnt = int(max<int64_t>(0, min<int64_t>(8, N - nb)));
+#define OQ_EPI8_PASS(P)                                                                        \
+  do {                                                                                         \
+    _Pragma("unroll") for (int ii = 0; ii < 2; ++ii)                                           \
+      _Pragma("unroll") for (int j = 0; j < 4; ++j)                                            \
+        _Pragma("unroll") for (int r = 0; r < 4; ++r)                                          \
+          reg[(16 * ii + 4 * fk + r) * EPI8_PITCH + 16 * j + fr] = acc[2 * (P) + ii][j][r];    \
+    for (int it = 0; it < 4; ++it) {                                                           \
+      const int rloc = rl + 8 * it;                                                            \
+      const int trow = wm * 128 + 32 * (P) + rloc;                                             \
+      const int64_t m = m0 + trow;                                                             \
+      float v[8];                                                                              \
+      const float4 a_ = *reinterpret_cast<const float4*>(reg + rloc * EPI8_PITCH + 8 * cl);    \
+      const float4 b_ = *reinterpret_cast<const float4*>(reg + rloc * EPI8_PITCH + 8 * cl + 4); \
+      v[0] = a_.x; v[1] = a_.y; v[2] = a_.z; v[3] = a_.w;                                     \
+      v[4] = b_.x; v[5] = b_.y; v[6] = b_.z; v[7] = b_.w;                                     \
+      float2 c = make_float2(0.f, 0.f);                                                        \
+      if (m < M && cnt > 0) c = epi.apply8(epi.row(m), nb, v, cnt);                            \
+      if constexpr (Epi::kRows) {                                                              \
+        c.x = group_sum<8>(c.x);                                                               \
+        c.y = group_sum<8>(c.y);                                                               \
+        if (cl == 0) rowbuf[wn][trow] = c;                                                     \
+      }                                                                                        \
+    }                                                                                          \
+  } while (0)
+  OQ_EPI8_PASS(0);
+  OQ_EPI8_PASS(1);
+  OQ_EPI8_PASS(2);
+  OQ_EPI8_PASS(3);
+#undef OQ_EPI8_PASS
+  if constexpr (Epi::kRows) {
+    __syncthreads();
+    if (tid < BM) {
+      const int64_t m = m0 + tid;
+      if (m < M) {
+        float2 s = rowbuf[0][tid];
+#pragma unroll
+        for (int w = 1; w < 4; ++w) {
+          s.x += rowbuf[w][tid].x;
+          s.y += rowbuf[w][tid].y;
+        }
+        epi.finish(m, tn, s.x, s.y);
+      }
+    }
+  }
 }
 
 // ------------------------------------------------------------------ fp32 kernel
@@ -445,7 +599,7 @@ hipError_t launch(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
     if (tm * tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
     const bool direct = K % BK == 0 && lda % 8 == 0 && ldb % 8 == 0 && K > 0;
     if (direct)
-      hipLaunchKernelGGL((gemm_bf16_kernel<Epi, true>), dim3(unsigned(tm * tn)), dim3(NTHR), 0, st,
+      hipLaunchKernelGGL((gemm_bf16_w8_kernel<Epi>), dim3(unsigned(tm * tn)), dim3(NTHR8), 0, st,
                          static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N, K,
                          lda, ldb, int(tm), int(tn), epi);
     else
