@@ -18,6 +18,8 @@
 // Epilogues: plain fp32 store; bf16/fp32 store with a per-row bias; and the
 // calibration-step forward epilogue (residual against the full-precision
 // target, bf16 dL/dY, per-row partial sums of the squared residual and of dY).
+#include <type_traits>
+
 #include "common.h"
 #include "oq_internal.h"
 
@@ -25,6 +27,9 @@ namespace oq {
 namespace {
 
 constexpr int BM = 256, BN = 256, BK = 64, NTHR = 256;
+#ifndef OQ_GEMM_MF32
+#define OQ_GEMM_MF32 false
+#endif
 constexpr int GROUP_M = 8;
 constexpr int F32_TILE = 64;
 
@@ -219,13 +224,21 @@ OQ_DEV void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 // at LDS byte address lds_addr + 16 i).  Issued as inline assembly so the
 // compiler does not model it as an LDS write and adds no wait in front of
 // the reads of the other stage; the kernel waits for it (vmcnt) itself
-// before the barrier that publishes the stage.
+// before the barrier that publishes the stage.  m0 (the LDS base of the
+// copy) is saved and restored around it, and one wait state separates the
+// m0 write from the copy that reads it.
 OQ_DEV void dma16(const void* g, uint32_t lds_addr) {
   const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_addr);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-               :
-               : "s"(m0v), "v"(g)
-               : "memory", "m0");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(m0v), "v"(g)
+      : "memory");
 }
 OQ_DEV uint32_t lds_addr_of(const void* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
@@ -392,15 +405,21 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
 }
 
 // ------------------------------------------------------------------ bf16 8-wave kernel
-// K % 64 == 0.  Same 256x256x64 tile, LDS stages and swizzle as above, but
-// eight waves (two per SIMD) each own a 128x64 block (2 x 4 waves).  While
-// one wave of a SIMD waits on its LDS reads the other issues matrix
-// instructions, so the hardware overlaps what a single wave serialises.
-// Per wave: 8 x 4 fragments of v_mfma_f32_16x16x32_bf16 (128 accumulators).
+// K % 64 == 0.  Same 256x256x64 tile and LDS stages as above, but eight waves
+// (two per SIMD) each own a 128x64 block (2 x 4 waves): while one wave of a
+// SIMD waits on its LDS reads the other issues matrix instructions, so the
+// hardware overlaps what a single wave serialises.  MF32 selects
+// v_mfma_f32_32x32x16_bf16 (4 x 2 blocks per wave) over 16x16x32 (8 x 4);
+// both hold 128 accumulators per lane.
+// LDS slot of chunk c of row r: c ^ (r & 7) ^ ((r >> 4) & 1).  A 128-bit LDS
+// read serves lanes 0-7 together with 16-23 (and so on); in a 32x32x16
+// fragment those hold rows r and r + 16, which the row-bit-4 term separates.
 constexpr int NTHR8 = 512;
-constexpr int EPI8_PITCH = 68;
 
-template <class Epi>
+template <bool MF32>
+OQ_DEV constexpr int epi8_pitch() { return MF32 ? 72 : 68; }
+
+template <class Epi, bool MF32>
 __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, int64_t M, int64_t N,
     int64_t K, int64_t lda, int64_t ldb, int tiles_m, int tiles_n, Epi epi) {
@@ -421,10 +440,11 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int nk = int(K / BK);
 
-  // DMA plan: instruction i of wave w fills tile rows 8 (8 i + w) .. +7
+  // DMA plan: instruction i of wave w fills tile rows 8 (8 i + w) .. +7;
+  // lane l covers row 64 i + 8 w + (l >> 3), slot l & 7
   int64_t aoff[4], boff[4];
   {
-    const int ch = (lane & 7) ^ (lane >> 3);
+    const int ch = (lane & 7) ^ (lane >> 3) ^ ((wave >> 1) & 1);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = 64 * i + 8 * wave + (lane >> 3);
@@ -433,13 +453,16 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
     }
   }
   const int wm = wave >> 2, wn = wave & 3;
-  const int fr = lane & 15, fk = lane >> 4;
 
-  f32x4_t acc[8][4];
+  constexpr int BI = MF32 ? 4 : 8, BJ = MF32 ? 2 : 4;
+  using acc_t = typename std::conditional<MF32, f32x16_t, f32x4_t>::type;
+  acc_t acc[BI][BJ];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < BI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < BJ; ++j)
+#pragma unroll
+      for (int v = 0; v < (MF32 ? 16 : 4); ++v) acc[i][j][v] = 0.f;
 
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -461,19 +484,49 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
     }
     const uint4* As = lds[cur][0];
     const uint4* Bs = lds[cur][1];
+    if constexpr (MF32) {
+      // k-step ks: lane (f32, f2) holds row f32 of the block, chunk 2 ks + f2
+      const int f32 = lane & 31, f2 = lane >> 5;
+      const int sw = (f32 & 7) ^ ((f32 >> 4) & 1);
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int ch = (kk * 4 + fk) ^ (fr & 7);
-      bf16x8_t af[8], bfr[4];
+      for (int ks = 0; ks < 4; ++ks) {
+        const int ch = (2 * ks + f2) ^ sw;
+        bf16x8_t af[4], bfr[2];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) af[i] = as_bf16x8(As[(wm * 128 + 16 * i + fr) * 8 + ch]);
+        for (int i = 0; i < 4; ++i) af[i] = as_bf16x8(As[(wm * 128 + 32 * i + f32) * 8 + ch]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) bfr[j] = as_bf16x8(Bs[(wn * 64 + 16 * j + fr) * 8 + ch]);
+        for (int j = 0; j < 2; ++j) bfr[j] = as_bf16x8(Bs[(wn * 64 + 32 * j + f32) * 8 + ch]);
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      }
+    } else {
+      // k-half kk: lane (fr, fk) holds row fr of the 16-row block, chunk 4 kk + fk
+      const int fr = lane & 15, fk = lane >> 4;
+      const int sw = (fr & 7) ^ ((fr >> 4) & 1);
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int ch = (kk * 4 + fk) ^ sw;
+        bf16x8_t af[8], bfr[4];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int row = wm * 128 + 16 * i + fr;
+          af[i] = as_bf16x8(As[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int row = wn * 64 + 16 * j + fr;
+          bfr[j] = as_bf16x8(Bs[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
+        }
+        (void)ch;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      }
     }
     if (kt + 1 < nk) wait_vm0();
     __syncthreads();
@@ -481,23 +534,32 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
 
   // epilogue: each wave's 128x64 block through LDS in four passes of 32 rows;
   // a lane then takes 8 consecutive columns of one row (8 lanes per row).
-  float* reg = reinterpret_cast<float*>(&lds[0][0][0]) + wave * (32 * EPI8_PITCH);
+  constexpr int PITCH = epi8_pitch<MF32>();
+  float* reg = reinterpret_cast<float*>(&lds[0][0][0]) + wave * (32 * PITCH);
   const int cl = lane & 7, rl = lane >> 3;
   const int64_t nb = n0 + wn * 64 + 8 * cl;
   const int cnt = int(max<int64_t>(0, min<int64_t>(8, N - nb)));
 #define OQ_EPI8_PASS(P)                                                                        \
   do {                                                                                         \
-    _Pragma("unroll") for (int ii = 0; ii < 2; ++ii)                                           \
-      _Pragma("unroll") for (int j = 0; j < 4; ++j)                                            \
-        _Pragma("unroll") for (int r = 0; r < 4; ++r)                                          \
-          reg[(16 * ii + 4 * fk + r) * EPI8_PITCH + 16 * j + fr] = acc[2 * (P) + ii][j][r];    \
+    if constexpr (MF32) {                                                                      \
+      const int f32 = lane & 31, f2 = lane >> 5;                                               \
+      _Pragma("unroll") for (int j = 0; j < 2; ++j)                                            \
+        _Pragma("unroll") for (int v = 0; v < 16; ++v)                                         \
+          reg[(8 * (v >> 2) + 4 * f2 + (v & 3)) * PITCH + 32 * j + f32] = acc[(P)][j][v];      \
+    } else {                                                                                   \
+      const int fr = lane & 15, fk = lane >> 4;                                                \
+      _Pragma("unroll") for (int ii = 0; ii < 2; ++ii)                                         \
+        _Pragma("unroll") for (int j = 0; j < 4; ++j)                                          \
+          _Pragma("unroll") for (int r = 0; r < 4; ++r)                                        \
+            reg[(16 * ii + 4 * fk + r) * PITCH + 16 * j + fr] = acc[2 * (P) + ii][j][r];       \
+    }                                                                                          \
     for (int it = 0; it < 4; ++it) {                                                           \
       const int rloc = rl + 8 * it;                                                            \
       const int trow = wm * 128 + 32 * (P) + rloc;                                             \
       const int64_t m = m0 + trow;                                                             \
       float v[8];                                                                              \
-      const float4 a_ = *reinterpret_cast<const float4*>(reg + rloc * EPI8_PITCH + 8 * cl);    \
-      const float4 b_ = *reinterpret_cast<const float4*>(reg + rloc * EPI8_PITCH + 8 * cl + 4); \
+      const float4 a_ = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl);         \
+      const float4 b_ = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl + 4);     \
       v[0] = a_.x; v[1] = a_.y; v[2] = a_.z; v[3] = a_.w;                                     \
       v[4] = b_.x; v[5] = b_.y; v[6] = b_.z; v[7] = b_.w;                                     \
       float2 c = make_float2(0.f, 0.f);                                                        \
@@ -599,7 +661,7 @@ hipError_t launch(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
     if (tm * tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
     const bool direct = K % BK == 0 && lda % 8 == 0 && ldb % 8 == 0 && K > 0;
     if (direct)
-      hipLaunchKernelGGL((gemm_bf16_w8_kernel<Epi>), dim3(unsigned(tm * tn)), dim3(NTHR8), 0, st,
+      hipLaunchKernelGGL((gemm_bf16_w8_kernel<Epi, OQ_GEMM_MF32>), dim3(unsigned(tm * tn)), dim3(NTHR8), 0, st,
                          static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N, K,
                          lda, ldb, int(tm), int(tn), epi);
     else
