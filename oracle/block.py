@@ -6,15 +6,22 @@ Follows Algorithm 1's inner-loop body (apply LET, quantise with LWC, run the
 quantised block on x_q, squared error to x_fp, backward) with the block
 objective of Eq.1 and the quantised linear of Eq.4: Y = Q_a(X~) Q_w(W~) + B~.
 
+``mean_rows`` (default ``c_out``) is the output-channel count of the whole
+linear in the mean-squared-error normaliser.  Without LET each output row's
+loss and clipping gradients depend on that row alone, so a check may pass a
+subset of a linear's rows together with the whole linear's normaliser.
+
 "The block" here is its linear sub-graph: every linear l reads the input of
 its site k and is compared with its own full-precision target Y_fp,l.  The
-loss is the sum over linears of the mean squared error (the paper writes a
-squared norm; the mean per linear is the reading fixed in the design doc).
+loss is the sum over linears of the mean squared error (Eq.1 and Algorithm 1
+write a squared norm; a mean per linear fixes its scale, which sets the size
+of every gradient).
 
 Description (plain dicts):
   desc  = {"T": tokens, "bf16": bool,
            "sites":   [{"width": C, "let": bool, "act_bits": 16 | N}, ...],
-           "linears": [{"site": k, "c_out": C_out, "bits": N, "group": g}, ...]}
+           "linears": [{"site": k, "c_out": C_out, "bits": N, "group": g,
+                        "mean_rows": C_out_whole (optional)}, ...]}
   X_q   = [ [T, C_k] per site ]            (the quantised model's input x_q)
   Y_fp  = [ [T, C_out_l] per linear ]      (the full-precision target x_fp)
   params= {"W": [[C_out, C_in]], "B": [[C_out] | None],
@@ -76,7 +83,7 @@ def block_forward(desc, X_q, Y_fp, params, ft=np.float32):
         acc = S[k]["xop"] @ wop.T                       # [T, C_out], fp64 sum
         Y = (acc + np.asarray(Bt, np.float64)[None, :]).astype(ft)
         R = Y - np.asarray(Y_fp[l], dtype=ft)           # residual, one rounding
-        n = T * lin["c_out"]
+        n = T * lin.get("mean_rows", lin["c_out"])
         R64 = R.astype(np.float64)
         row_loss = np.sum(R64 * R64, axis=0)            # per output channel
         loss += float(np.sum(row_loss)) / n

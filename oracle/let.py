@@ -7,7 +7,7 @@ Layouts: X is [T, C_in] (tokens x channels); W is [C_out, C_in] (one row per
 output channel, the transpose of the paper's C_in x C_out matrix); s, delta
 are [C_in]; B is [C_out].
 
-Readings (listed in DESIGN.md):
+Readings of points the paper leaves open:
   * X~ = (X - delta) / s is evaluated as fl(fl(x - delta) * fl(1/s));
   * W~ = s (.) W is one fp32 product per element;
   * B~ = B + delta W uses the original W, summed in fp64, rounded once;

@@ -3,7 +3,7 @@ quantiser (Eq.4's Q_a), forward and straight-through backward.
 
 TEST INFRASTRUCTURE ONLY (see ``oracle/__init__``).
 
-Readings of points the paper leaves open (each is listed in the design doc):
+Readings of points the paper leaves open:
   * the round operation of Eq.2 rounds half to even (``np.rint``);
   * dequantisation, which Eq.2 does not write, is ``(W_q - z) * h``;
   * fp32 operation order: a = gamma*max, b = beta*min, h = (a - b)/qmax,

@@ -134,6 +134,12 @@ def test_row_decomposition_of_lwc_only_step():
     # d2's mean runs over 3 channels instead of 10: rescale
     np.testing.assert_allclose(out2["d_gamma_logit"][0] * 3 / 10, out["d_gamma_logit"][0][rows], rtol=1e-5)
     np.testing.assert_allclose(out2["row_loss"][0], out["row_loss"][0][rows], rtol=1e-12)
+    # with the whole linear's normaliser the subset reproduces the rows directly
+    d3 = _tiny_desc(T=12, c_in=32, c_out=3, g=8, bits=3)
+    d3["linears"][0]["mean_rows"] = 10
+    _, out3 = block_step(d3, X, [Y[0][:, rows]], p2)
+    np.testing.assert_allclose(out3["d_gamma_logit"][0], out["d_gamma_logit"][0][rows], rtol=1e-12)
+    np.testing.assert_allclose(out3["d_beta_logit"][0], out["d_beta_logit"][0][rows], rtol=1e-12)
 
 
 # ---------------------------------------------------------------- straight-through gradients
