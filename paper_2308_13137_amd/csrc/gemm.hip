@@ -1,16 +1,20 @@
 // Matrix products C[M,N] = A[M,K] B[N,K]^T for the calibration step.
 //
-// bf16 path (gfx950 matrix cores): 256x256 output tile per workgroup of four
-// wave64s, each wave owning a 128x128 quadrant as 8x8 fragments of
-// v_mfma_f32_16x16x32_bf16.  K advances 64 at a time through two LDS stages
-// (A and B tiles of 256 rows x 64 bf16 = 32 KiB each per stage); the global
-// loads of stage k+1 are issued before the matrix instructions of stage k.
-// Each LDS row is eight 16-byte chunks stored at chunk ^ (row & 7), so the
-// eight lanes of one 128-bit LDS access hit distinct banks both when a row is
-// written and when a fragment column is read.  Workgroups are numbered so that
-// the 32 tiles resident on one XCD (the hardware deals workgroups to the 8
-// XCDs round-robin) form an 8 x 4 block of the output, sharing A and B panels
-// in that XCD's L2.
+// bf16 path, K % 64 == 0 (gemm_bf16_w8_kernel): 256x256 output tile per
+// workgroup of eight wave64s (two per SIMD), each owning a 128x64 sub-tile as
+// 8 x 4 fragments of v_mfma_f32_16x16x32_bf16.  K advances 64 at a time
+// through two LDS stages (A and B tiles of 256 rows x 64 bf16 = 32 KiB each)
+// filled by global_load_lds_dwordx4 straight from global memory.  Fragments
+// are double-buffered in registers per 32-wide k-half, and the fragment reads
+// and stage copies are placed by hand between groups of four MFMAs.  Each LDS
+// row is eight 16-byte chunks at slot chunk ^ (row & 7) ^ ((row >> 4) & 1),
+// so the lanes of one 128-bit LDS access hit distinct banks.  Workgroups are
+// renumbered so that the tiles resident on one XCD (the hardware deals
+// workgroups to the 8 XCDs round-robin) form a contiguous block of the
+// output, grouped 8 tiles down M, sharing A and B panels in that XCD's L2.
+//
+// bf16 path, other K (gemm_bf16_kernel): four waves of 128x128, tiles staged
+// through registers with zero fill past M, N and K.
 //
 // fp32 path: a plain LDS-tiled FMA kernel (64x64 tile, 4x4 per thread), used
 // by the fp32 workloads, whose matrices are small.
@@ -27,9 +31,6 @@ namespace oq {
 namespace {
 
 constexpr int BM = 256, BN = 256, BK = 64, NTHR = 256;
-#ifndef OQ_GEMM_MF32
-#define OQ_GEMM_MF32 false
-#endif
 constexpr int GROUP_M = 8;
 constexpr int F32_TILE = 64;
 
@@ -240,6 +241,21 @@ OQ_DEV void dma16(const void* g, uint32_t lds_addr) {
       : "s"(m0v), "v"(g)
       : "memory");
 }
+// The same copy with a uniform 64-bit base in SGPRs and a 32-bit per-lane
+// byte offset (global address = base + offset).
+OQ_DEV void dma16_s(const void* base, uint32_t vofs, uint32_t lds_addr) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_addr);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, %3\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(m0v), "v"(vofs), "s"(base)
+      : "memory");
+}
 OQ_DEV uint32_t lds_addr_of(const void* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
       (__attribute__((address_space(3))) const char*)(p)));
@@ -407,19 +423,98 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
 // ------------------------------------------------------------------ bf16 8-wave kernel
 // K % 64 == 0.  Same 256x256x64 tile and LDS stages as above, but eight waves
 // (two per SIMD) each own a 128x64 block (2 x 4 waves): while one wave of a
-// SIMD waits on its LDS reads the other issues matrix instructions, so the
-// hardware overlaps what a single wave serialises.  MF32 selects
-// v_mfma_f32_32x32x16_bf16 (4 x 2 blocks per wave) over 16x16x32 (8 x 4);
-// both hold 128 accumulators per lane.
+// SIMD waits the other issues matrix instructions.
 // LDS slot of chunk c of row r: c ^ (r & 7) ^ ((r >> 4) & 1).  A 128-bit LDS
-// read serves lanes 0-7 together with 16-23 (and so on); in a 32x32x16
-// fragment those hold rows r and r + 16, which the row-bit-4 term separates.
+// read serves lanes 0-7 together with 16-23 (and so on); the row-bit-4 term
+// keeps rows r and r + 16 apart as well.
 constexpr int NTHR8 = 512;
+constexpr int EPI8_PITCH = 68;
 
-template <bool MF32>
-OQ_DEV constexpr int epi8_pitch() { return MF32 ? 72 : 68; }
+// Fragment reads of one k-half (32 of the stage's 64 k): lane (fr, fk) takes
+// row fr of each 16-row block, 16-byte chunk 4 kk + fk, at its swizzled slot.
+OQ_DEV void read_frags(const uint4* As, const uint4* Bs, int kk, int wm, int wn, int lane,
+                       bf16x8_t (&af)[8], bf16x8_t (&bq)[4]) {
+  const int fr = lane & 15, fk = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int row = wm * 128 + 16 * i + fr;
+    af[i] = as_bf16x8(As[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = wn * 64 + 16 * j + fr;
+    bq[j] = as_bf16x8(Bs[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
+  }
+}
 
-template <class Epi, bool MF32>
+// One LDS stage (A and B tiles, 256 rows x 64 k): Ab / Bb point at the
+// tiles' first row at the stage's first k, lds_stage is the stage's LDS byte
+// address (A tile, then B tile 32 KiB further).
+OQ_DEV void stage_dma(const uint16_t* Ab, const uint16_t* Bb, const uint32_t (&aoff)[4],
+                      const uint32_t (&boff)[4], uint32_t lds_stage, int wave) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    dma16_s(Ab, aoff[i], lds_stage + (8 * i + wave) * 1024);
+    dma16_s(Bb, boff[i], lds_stage + 32768 + (8 * i + wave) * 1024);
+  }
+}
+
+OQ_DEV void mfma_half(f32x4_t (&acc)[8][4], const bf16x8_t (&af)[8], const bf16x8_t (&bq)[4]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bq[j], acc[i][j], 0, 0, 0);
+}
+
+// One k-half of MFMAs (8 groups of 4, i-major) with the next fragment set's
+// 12 LDS reads (B first, then A, in the order the next half consumes them)
+// and, when DMA, one stage copy per group, each placed by hand between MFMA
+// groups; sched_barrier keeps the scheduler from bunching them again.
+template <bool READS, bool DMA>
+OQ_DEV void half_sched(f32x4_t (&acc)[8][4], const bf16x8_t (&au)[8], const bf16x8_t (&bu)[4],
+                       const uint4* As, const uint4* Bs, int kk, int wm, int wn, int lane,
+                       bf16x8_t (&ad)[8], bf16x8_t (&bd)[4], const uint16_t* Ab,
+                       const uint16_t* Bb, const uint32_t (&aoff)[4], const uint32_t (&boff)[4],
+                       uint32_t lds_stage, int wave) {
+  const int fr = lane & 15, fk = lane >> 4;
+#pragma unroll
+  for (int g = 0; g < 8; ++g) {
+    if constexpr (READS) {
+      // reads of group g: B0..B3 in groups 0,0,1,1 then A0..A7 in 2,2,3,3,4,5,6,7
+#pragma unroll
+      for (int r = 0; r < 12; ++r) {
+        const int grp = r < 4 ? r / 2 : (r < 8 ? 2 + (r - 4) / 2 : r - 4);
+        if (grp != g) continue;
+        if (r < 4) {
+          const int row = wn * 64 + 16 * r + fr;
+          bd[r] = as_bf16x8(Bs[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
+        } else {
+          const int i = r - 4;
+          const int row = wm * 128 + 16 * i + fr;
+          ad[i] = as_bf16x8(As[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
+        }
+      }
+    }
+    if constexpr (DMA) {
+      if (g & 1) dma16_s(Bb, boff[g >> 1], lds_stage + 32768 + (8 * (g >> 1) + wave) * 1024);
+      else       dma16_s(Ab, aoff[g >> 1], lds_stage + (8 * (g >> 1) + wave) * 1024);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      acc[g][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(au[g], bu[j], acc[g][j], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// 256x256 output tile, eight wave64s (two per SIMD) in a 2 x 4 grid, each
+// owning a 128x64 sub-tile as 8 x 4 fragments of v_mfma_f32_16x16x32_bf16.
+// K advances 64 per stage through two LDS stages filled by
+// global_load_lds_dwordx4.  The fragments of a stage's two k-halves live in
+// two register sets: the second half is read while the first half's MFMAs
+// run, and the next stage's first half is read (after the barrier that
+// publishes it) while the second half's MFMAs run.
+template <class Epi>
 __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, int64_t M, int64_t N,
     int64_t K, int64_t lda, int64_t ldb, int tiles_m, int tiles_n, Epi epi) {
@@ -442,117 +537,79 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
 
   // DMA plan: instruction i of wave w fills tile rows 8 (8 i + w) .. +7;
   // lane l covers row 64 i + 8 w + (l >> 3), slot l & 7
-  int64_t aoff[4], boff[4];
+  // 32-bit byte offsets from the tile's first row (a tile spans at most
+  // 256 rows; the launcher keeps 2 * 256 * ld below 2^32)
+  const uint16_t* At = A + m0 * lda;
+  const uint16_t* Bt = B + n0 * ldb;
+  uint32_t aoff[4], boff[4];                    // byte offsets
   {
     const int ch = (lane & 7) ^ (lane >> 3) ^ ((wave >> 1) & 1);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = 64 * i + 8 * wave + (lane >> 3);
-      aoff[i] = min(m0 + row, M - 1) * lda + 8 * ch;
-      boff[i] = min(n0 + row, N - 1) * ldb + 8 * ch;
+      aoff[i] = uint32_t(2 * (min<int64_t>(row, M - 1 - m0) * lda + 8 * ch));
+      boff[i] = uint32_t(2 * (min<int64_t>(row, N - 1 - n0) * ldb + 8 * ch));
     }
   }
+  const uint32_t lds0 = lds_addr_of(&lds[0][0][0]);
   const int wm = wave >> 2, wn = wave & 3;
 
-  constexpr int BI = MF32 ? 4 : 8, BJ = MF32 ? 2 : 4;
-  using acc_t = typename std::conditional<MF32, f32x16_t, f32x4_t>::type;
-  acc_t acc[BI][BJ];
+  f32x4_t acc[8][4];
 #pragma unroll
-  for (int i = 0; i < BI; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < BJ; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int v = 0; v < (MF32 ? 16 : 4); ++v) acc[i][j][v] = 0.f;
+      for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.f;
 
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    dma16(A + aoff[i], lds_addr_of(&lds[0][0][(8 * i + wave) * 64]));
-    dma16(B + boff[i], lds_addr_of(&lds[0][1][(8 * i + wave) * 64]));
-  }
+  stage_dma(At, Bt, aoff, boff, lds0, wave);
   wait_vm0();
   __syncthreads();
 
-  for (int kt = 0; kt < nk; ++kt) {
+  bf16x8_t a0[8], b0[4], a1[8], b1[4];
+  read_frags(lds[0][0], lds[0][1], 0, wm, wn, lane, a0, b0);
+  if (nk > 1) stage_dma(At + BK, Bt + BK, aoff, boff, lds0 + 65536, wave);
+
+  // Stage kt sits in buffer kt & 1.  A buffer's last fragment reads complete
+  // before the barrier in the middle of the iteration that uses it, so the
+  // copy of stage kt + 2 into it starts right after that barrier and has a
+  // whole iteration to land.
+  int kt = 0;
+  for (; kt + 2 < nk; ++kt) {
     const int cur = kt & 1, nxt = cur ^ 1;
-    if (kt + 1 < nk) {
-      const int64_t knext = int64_t(kt + 1) * BK;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        dma16(A + aoff[i] + knext, lds_addr_of(&lds[nxt][0][(8 * i + wave) * 64]));
-        dma16(B + boff[i] + knext, lds_addr_of(&lds[nxt][1][(8 * i + wave) * 64]));
-      }
-    }
-    const uint4* As = lds[cur][0];
-    const uint4* Bs = lds[cur][1];
-    if constexpr (MF32) {
-      // k-step ks: lane (f32, f2) holds row f32 of the block, chunk 2 ks + f2
-      const int f32 = lane & 31, f2 = lane >> 5;
-      const int sw = (f32 & 7) ^ ((f32 >> 4) & 1);
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int ch = (2 * ks + f2) ^ sw;
-        bf16x8_t af[4], bfr[2];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) af[i] = as_bf16x8(As[(wm * 128 + 32 * i + f32) * 8 + ch]);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) bfr[j] = as_bf16x8(Bs[(wn * 64 + 32 * j + f32) * 8 + ch]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-      }
-    } else {
-      // k-half kk: lane (fr, fk) holds row fr of the 16-row block, chunk 4 kk + fk
-      const int fr = lane & 15, fk = lane >> 4;
-      const int sw = (fr & 7) ^ ((fr >> 4) & 1);
-#pragma unroll
-      for (int kk = 0; kk < 2; ++kk) {
-        const int ch = (kk * 4 + fk) ^ sw;
-        bf16x8_t af[8], bfr[4];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int row = wm * 128 + 16 * i + fr;
-          af[i] = as_bf16x8(As[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int row = wn * 64 + 16 * j + fr;
-          bfr[j] = as_bf16x8(Bs[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
-        }
-        (void)ch;
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-      }
-    }
+    half_sched<true, false>(acc, a0, b0, lds[cur][0], lds[cur][1], 1, wm, wn, lane, a1, b1, At,
+                            Bt, aoff, boff, 0, wave);
+    wait_vm0();
+    __syncthreads();
+    half_sched<true, true>(acc, a1, b1, lds[nxt][0], lds[nxt][1], 0, wm, wn, lane, a0, b0,
+                           At + int64_t(kt + 2) * BK, Bt + int64_t(kt + 2) * BK, aoff, boff,
+                           lds0 + cur * 65536, wave);
+  }
+  for (; kt < nk; ++kt) {
+    const int cur = kt & 1, nxt = cur ^ 1;
+    read_frags(lds[cur][0], lds[cur][1], 1, wm, wn, lane, a1, b1);
+    mfma_half(acc, a0, b0);
     if (kt + 1 < nk) wait_vm0();
     __syncthreads();
+    if (kt + 1 < nk) read_frags(lds[nxt][0], lds[nxt][1], 0, wm, wn, lane, a0, b0);
+    mfma_half(acc, a1, b1);
   }
+  __syncthreads();
 
   // epilogue: each wave's 128x64 block through LDS in four passes of 32 rows;
   // a lane then takes 8 consecutive columns of one row (8 lanes per row).
-  constexpr int PITCH = epi8_pitch<MF32>();
+  constexpr int PITCH = EPI8_PITCH;
   float* reg = reinterpret_cast<float*>(&lds[0][0][0]) + wave * (32 * PITCH);
   const int cl = lane & 7, rl = lane >> 3;
   const int64_t nb = n0 + wn * 64 + 8 * cl;
   const int cnt = int(max<int64_t>(0, min<int64_t>(8, N - nb)));
 #define OQ_EPI8_PASS(P)                                                                        \
   do {                                                                                         \
-    if constexpr (MF32) {                                                                      \
-      const int f32 = lane & 31, f2 = lane >> 5;                                               \
-      _Pragma("unroll") for (int j = 0; j < 2; ++j)                                            \
-        _Pragma("unroll") for (int v = 0; v < 16; ++v)                                         \
-          reg[(8 * (v >> 2) + 4 * f2 + (v & 3)) * PITCH + 32 * j + f32] = acc[(P)][j][v];      \
-    } else {                                                                                   \
-      const int fr = lane & 15, fk = lane >> 4;                                                \
-      _Pragma("unroll") for (int ii = 0; ii < 2; ++ii)                                         \
-        _Pragma("unroll") for (int j = 0; j < 4; ++j)                                          \
-          _Pragma("unroll") for (int r = 0; r < 4; ++r)                                        \
-            reg[(16 * ii + 4 * fk + r) * PITCH + 16 * j + fr] = acc[2 * (P) + ii][j][r];       \
-    }                                                                                          \
+    const int fr = lane & 15, fk = lane >> 4;                                                  \
+    _Pragma("unroll") for (int ii = 0; ii < 2; ++ii)                                           \
+      _Pragma("unroll") for (int j = 0; j < 4; ++j)                                            \
+        _Pragma("unroll") for (int r = 0; r < 4; ++r)                                          \
+          reg[(16 * ii + 4 * fk + r) * PITCH + 16 * j + fr] = acc[2 * (P) + ii][j][r];         \
     for (int it = 0; it < 4; ++it) {                                                           \
       const int rloc = rl + 8 * it;                                                            \
       const int trow = wm * 128 + 32 * (P) + rloc;                                             \
@@ -659,9 +716,10 @@ hipError_t launch(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
   if (bf16) {
     const int64_t tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
     if (tm * tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
-    const bool direct = K % BK == 0 && lda % 8 == 0 && ldb % 8 == 0 && K > 0;
+    const bool direct = K % BK == 0 && lda % 8 == 0 && ldb % 8 == 0 && K > 0 &&
+                        lda < (int64_t(1) << 23) && ldb < (int64_t(1) << 23);
     if (direct)
-      hipLaunchKernelGGL((gemm_bf16_w8_kernel<Epi, OQ_GEMM_MF32>), dim3(unsigned(tm * tn)), dim3(NTHR8), 0, st,
+      hipLaunchKernelGGL((gemm_bf16_w8_kernel<Epi>), dim3(unsigned(tm * tn)), dim3(NTHR8), 0, st,
                          static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N, K,
                          lda, ldb, int(tm), int(tn), epi);
     else
