@@ -163,6 +163,19 @@ oq_status oq_matmul_nt(const void* A, const void* B, oq_dtype in_dt, int64_t M, 
                        int64_t K, void* C, oq_dtype out_dt, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * The same product with either operand stored the other way round, read as
+ * stored (the step's weight and input gradients use it on token-major X^ and
+ * on W^ without transposing them):
+ *   C[M,N] (fp32) = opA opB^T,  opA = A [M,K] (a_mn = 0) or A^T with A stored
+ *   [K,M] (a_mn = 1);  opB = B [N,K] (b_mn = 0) or B^T with B stored [K,N].
+ * bf16 only, dense row-major operands.  OQ_ERR_UNSUPPORTED when an operand
+ * is MN-major and K is not a multiple of 64 or the MN side is not a multiple
+ * of 8.
+ */
+oq_status oq_matmul(const void* A, int a_mn, const void* B, int b_mn, int64_t M, int64_t N,
+                    int64_t K, float* C, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * AdamW update (Sec. 4.1: AdamW, zero weight decay; lr 5e-3 for the clipping
  * logits, 1e-2 for s and delta).  fp32, in place on p, m, v; step counts from 1.
  * Hyperparameters are doubles: the coefficients 1 - b1, 1 - b2 and the bias

@@ -373,6 +373,25 @@ oq_status oq_matmul_nt(const void* A, const void* B, oq_dtype in_dt, int64_t M, 
   return OQ_OK;
 }
 
+oq_status oq_matmul(const void* A, int a_mn, const void* B, int b_mn, int64_t M, int64_t N,
+                    int64_t K, float* C, hipStream_t stream) {
+  OQ_REQ(A && B && C, "A, B, C are required");
+  OQ_REQ(M >= 0 && N >= 0 && K >= 0, "bad shape");
+  OQ_REQ(aligned16(A) && aligned16(B), "A and B must be 16-byte aligned");
+  const int64_t lda = a_mn ? M : K, ldb = b_mn ? N : K;
+  ProfScope ps(PK_OTHER, stream, 2.0 * double(M) * N * K);
+  if (!a_mn && !b_mn) {
+    OQ_REQ(K % 8 == 0, "K must be a multiple of 8");
+    OQ_HIP(gemm_nt_f32out(A, B, true, M, N, K, K, K, C, N, stream), "matmul");
+    return OQ_OK;
+  }
+  if (M == 0 || N == 0) return OQ_OK;
+  if (!gemm_mn_supported(a_mn != 0, b_mn != 0, M, N, K, lda, ldb))
+    return fail(OQ_ERR_UNSUPPORTED, "MN-major operand needs K %% 64 == 0 and M, N %% 8 == 0");
+  OQ_HIP(gemm_f32out_mn(A, a_mn != 0, B, b_mn != 0, M, N, K, lda, ldb, C, N, stream), "matmul");
+  return OQ_OK;
+}
+
 oq_status oq_adamw_step(float* p, const float* g, float* m, float* v, int64_t n, double lr,
                         double beta1, double beta2, double eps, double wd, int step,
                         hipStream_t stream) {
@@ -441,6 +460,17 @@ oq_status plan_block(const oq_block_desc* d, std::vector<SitePlan>& plan) {
   return OQ_OK;
 }
 
+// The weight gradient reads X^ token-major and the input gradient reads dY^T
+// and W^ as stored (no transposes) when the 8-wave kernel takes the shapes
+// with MN-major operands (bf16, T and the site's stacked rows multiples of 64).
+bool direct_grads(const oq_block_desc* d, const SitePlan& p) {
+  if (d->dtype != OQ_BF16) return false;
+  const int64_t T = d->tokens;
+  bool ok = gemm_mn_supported(false, true, p.M, p.C, T, T, p.C);
+  if (p.let) ok = ok && gemm_mn_supported(true, true, T, p.C, p.M, T, p.C);
+  return ok;
+}
+
 size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, char* base,
                    BlockWs* w) {
   const bool bf = d->dtype == OQ_BF16;
@@ -452,8 +482,9 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
          rows = 0, pw = 0, pa = 0, pb = 0;
   int64_t mtot = 0;
   for (const auto& p : plan) {
+    const bool direct = direct_grads(d, p);
     what = std::max(what, size_t(p.M * p.C));
-    xhatT = std::max(xhatT, size_t(T * p.C));
+    if (!direct) xhatT = std::max(xhatT, size_t(T * p.C));
     dyT = std::max(dyT, size_t(p.M * T));
     dW = std::max(dW, size_t(p.M * p.C));
     parts = std::max(parts, size_t(p.M * ntn));
@@ -461,8 +492,10 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
     mtot += p.M;
     if (p.let || p.act) xhat = std::max(xhat, size_t(T * p.C));
     if (p.let) {
-      dy = std::max(dy, size_t(p.M * T));
-      whatT = std::max(whatT, size_t(p.M * p.C));
+      if (!direct) {
+        dy = std::max(dy, size_t(p.M * T));
+        whatT = std::max(whatT, size_t(p.M * p.C));
+      }
       dX = std::max(dX, size_t(T * p.C));
       pa = std::max(pa, size_t(act_bwd_nparts(T) * p.C));
       size_t a = 0, b = 0;
@@ -478,7 +511,7 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
   BlockWs t{};
   t.what = cv.take<char>(what * es);
   t.xhat = xhat ? cv.take<char>(xhat * es) : nullptr;
-  t.xhatT = cv.take<char>(xhatT * es);
+  t.xhatT = xhatT ? cv.take<char>(xhatT * es) : nullptr;
   t.dyT = cv.take<char>(dyT * es);
   t.dy = dy ? cv.take<char>(dy * es) : nullptr;
   t.whatT = whatT ? cv.take<char>(whatT * es) : nullptr;
@@ -598,8 +631,10 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
              "act_fwd");
       xsrc = w.xhat;
     }
-    // 4. token-contiguous copy of X^ for the weight gradient
-    {
+    // 4. token-contiguous copy of X^ for the weight gradient (only where the
+    //    gradient products cannot read X^ as stored)
+    const bool direct = direct_grads(d, p);
+    if (!direct) {
       ProfScope ps(PK_TRANSPOSE, st, double(T) * C * 2 * es);
       OQ_HIP(transpose(xsrc, T, C, C, w.xhatT, T, int(es), st), "transpose X");
     }
@@ -633,7 +668,10 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     // 6. weight gradient dW^ = dY^T X^  [M, C]
     {
       ProfScope ps(PK_GEMM_WGRAD, st, 2.0 * double(M) * T * C);
-      OQ_HIP(gemm_nt_f32out(w.dyT, w.xhatT, bf, M, C, T, T, T, w.dW, C, st), "wgrad gemm");
+      if (direct)
+        OQ_HIP(gemm_f32out_mn(w.dyT, false, xsrc, true, M, C, T, T, C, w.dW, C, st), "wgrad gemm");
+      else
+        OQ_HIP(gemm_nt_f32out(w.dyT, w.xhatT, bf, M, C, T, T, T, w.dW, C, st), "wgrad gemm");
     }
     // 7. LWC backward per linear (+ weight-path LET scale partials)
     off = 0;
@@ -650,12 +688,17 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     }
     // 8. LET: input gradient through Q_a and (X - delta)/s, bias path, finish
     if (p.let) {
-      {
-        ProfScope ps(PK_TRANSPOSE, st, double(M) * (T + C) * 2 * es);
-        OQ_HIP(transpose(w.dyT, M, T, T, w.dy, M, int(es), st), "transpose dY");
-        OQ_HIP(transpose(w.what, M, C, C, w.whatT, M, int(es), st), "transpose W^");
-      }
-      {
+      if (direct) {
+        // dX^ [T, C] = dY W^ with dY read from dY^T [M, T] and W^ [M, C] as stored
+        ProfScope ps(PK_GEMM_DGRAD, st, 2.0 * double(M) * T * C);
+        OQ_HIP(gemm_f32out_mn(w.dyT, true, w.what, true, T, C, M, T, C, w.dX, C, st),
+               "dgrad gemm");
+      } else {
+        {
+          ProfScope ps(PK_TRANSPOSE, st, double(M) * (T + C) * 2 * es);
+          OQ_HIP(transpose(w.dyT, M, T, T, w.dy, M, int(es), st), "transpose dY");
+          OQ_HIP(transpose(w.what, M, C, C, w.whatT, M, int(es), st), "transpose W^");
+        }
         ProfScope ps(PK_GEMM_DGRAD, st, 2.0 * double(M) * T * C);
         OQ_HIP(gemm_nt_f32out(w.dy, w.whatT, bf, T, C, M, M, M, w.dX, C, st), "dgrad gemm");
       }

@@ -16,12 +16,13 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 // ------------------------------------------------------------------ bf16 <-> fp32
 OQ_DEV float bf2f(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
 
-// Round to nearest even; NaN stays NaN.
-OQ_DEV uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return uint16_t(u >> 16);
+// fp32 -> bf16, round to nearest even (gfx950's v_cvt_pk_bf16_f32).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+OQ_DEV uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f)); }
+// Two values packed low (a) and high (b) in one dword.
+OQ_DEV uint32_t f2bf2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
 }
 
 // ------------------------------------------------------------------ 8-wide element access
@@ -43,10 +44,10 @@ OQ_DEV void load8(const float* p, float v[8]) {
 }
 OQ_DEV void store8(uint16_t* p, const float v[8]) {
   uint4 q;
-  q.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
-  q.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
-  q.z = uint32_t(f2bf(v[4])) | (uint32_t(f2bf(v[5])) << 16);
-  q.w = uint32_t(f2bf(v[6])) | (uint32_t(f2bf(v[7])) << 16);
+  q.x = f2bf2(v[0], v[1]);
+  q.y = f2bf2(v[2], v[3]);
+  q.z = f2bf2(v[4], v[5]);
+  q.w = f2bf2(v[6], v[7]);
   *reinterpret_cast<uint4*>(p) = q;
 }
 OQ_DEV void store8(float* p, const float v[8]) {
@@ -110,6 +111,13 @@ OQ_DEV void dyn_group_minmax(float& mx, int& imx, float& mn, int& imn, int L) {
   }
 }
 
+// ------------------------------------------------------------------ rounding
+// Correctly rounded fp32 quotient and square root whatever the compiler's
+// fp32 division / sqrt expansion: one fp64 operation rounded again to fp32
+// is the correctly rounded fp32 result (53 >= 2 * 24 + 2 bits).
+OQ_DEV float div_rn(float a, float b) { return float(double(a) / double(b)); }
+OQ_DEV float sqrt_rn(float a) { return float(__builtin_sqrt(double(a))); }
+
 // ------------------------------------------------------------------ quantiser
 // Clip strength: the fp64 sigmoid of the logit, rounded once to fp32.
 OQ_DEV float clip_strength(float logit) {
@@ -131,10 +139,10 @@ OQ_DEV QParams make_qparams(float mx, float mn, float gamma, float beta, float q
   p.a = gamma * mx;
   p.b = beta * mn;
   float d = p.a - p.b;
-  float hr = d / qmax;
+  float hr = div_rn(d, qmax);
   p.hclamp = hr < 1e-5f;
   p.h = p.hclamp ? 1e-5f : hr;
-  p.r = 1.0f / p.h;
+  p.r = div_rn(1.0f, p.h);
   p.z = -rintf(p.b * p.r);
   return p;
 }
@@ -160,9 +168,9 @@ struct QGrad {
 };
 OQ_DEV QGrad quant_group_grad(float s_h, float s_z, float mx, float mn, const QParams& p, float qmax) {
   QGrad g;
-  float dh = s_h - s_z * (p.b / p.h);
+  float dh = s_h - s_z * div_rn(p.b, p.h);
   if (p.hclamp) dh = 0.0f;
-  float da = dh / qmax;
+  float da = div_rn(dh, qmax);
   float db = s_z - da;
   g.dmx = da * p.gamma;
   g.dmn = db * p.beta;

@@ -430,26 +430,82 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
 constexpr int NTHR8 = 512;
 constexpr int EPI8_PITCH = 68;
 
-// Fragment reads of one k-half (32 of the stage's 64 k): lane (fr, fk) takes
-// row fr of each 16-row block, 16-byte chunk 4 kk + fk, at its swizzled slot.
-OQ_DEV void read_frags(const uint4* As, const uint4* Bs, int kk, int wm, int wn, int lane,
-                       bf16x8_t (&af)[8], bf16x8_t (&bq)[4]) {
-  const int fr = lane & 15, fk = lane >> 4;
+// Operand tiles.  An operand is K-major (rows of the M or N side, k
+// contiguous: the A and B of C = A B^T) or MN-major (rows of k, the M or N
+// side contiguous).  Either way a stage's tile is 32 KiB:
+//  * K-major: 256 rows x 64 k, eight 16-byte chunks per row, chunk c of row r
+//    at slot c ^ (r & 7) ^ ((r >> 4) & 1);
+//  * MN-major: 64 k-rows x 256, 32 chunks per row, chunk c of k-row r at slot
+//    c ^ 2 h(r) with h(r) = (r & 3) | ((r >> 3) & 1) << 2.  A fragment takes
+//    two ds_read_b64_tr_b16 (4 k each); the swizzle puts the eight k-rows one
+//    such read touches in eight different 32-byte bank groups.
+// ds_read_b64_tr_b16: within each 16-lane group, with M[j] the four 16-bit
+// values at lane j's address, lane i receives M[4 e + i / 4][i % 4], e = 0..3.
+// Lane j = 4 e + i / 4 therefore points at k-row k0 + j / 4, column
+// 16 q + 4 (j % 4), and lane i receives k0 .. k0 + 3 of column 16 q + i.
+OQ_DEV int mn_swz(int r) { return (r & 3) | (((r >> 3) & 1) << 2); }
+
+// Per-lane byte offsets of a stage's four DMA instructions for one operand,
+// from the operand's tile origin (row mn0 for K-major, column mn0 for
+// MN-major).  Rows (K-major) or columns (MN-major) past the operand's extent
+// are clamped to the last valid one: they feed only outputs never stored.
+template <bool MN>
+OQ_DEV void dma_plan(uint32_t (&off)[4], int64_t mn0, int64_t extent, int64_t ld, int wave,
+                     int lane) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int row = wm * 128 + 16 * i + fr;
-    af[i] = as_bf16x8(As[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int row = wn * 64 + 16 * j + fr;
-    bq[j] = as_bf16x8(Bs[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
+  for (int i = 0; i < 4; ++i) {
+    if constexpr (MN) {
+      // instruction i of wave w fills k-rows 2 (8 i + w) and +1 (512 bytes each)
+      const int r = 16 * i + 2 * wave + (lane >> 5);
+      const int c = (lane & 31) ^ (2 * mn_swz(r));
+      const int64_t col = min<int64_t>(8 * c, extent - 8 - mn0);
+      off[i] = uint32_t(2 * (r * ld + col));
+    } else {
+      // instruction i of wave w fills rows 8 (8 i + w) .. +7 (128 bytes each)
+      const int row = 64 * i + 8 * wave + (lane >> 3);
+      const int c = (lane & 7) ^ (lane >> 3) ^ ((wave >> 1) & 1);
+      off[i] = uint32_t(2 * (min<int64_t>(row, extent - 1 - mn0) * ld + 8 * c));
+    }
   }
 }
 
-// One LDS stage (A and B tiles, 256 rows x 64 k): Ab / Bb point at the
-// tiles' first row at the stage's first k, lds_stage is the stage's LDS byte
-// address (A tile, then B tile 32 KiB further).
+typedef const __attribute__((address_space(3))) char lds_cchar;
+
+// One fragment (16 rows of the M/N side x 32 k, k-half kk) of the tile at
+// tile; q = first row / 16.
+template <bool MN>
+OQ_DEV bf16x8_t frag(lds_cchar* tile, int q, int kk, int lane) {
+  typedef short v4i16 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4i16 lds_v4;
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  typedef const __attribute__((address_space(3))) u32x4 lds_u4;
+  if constexpr (MN) {
+    const int g = lane >> 4, j = lane & 15;
+    lds_cchar* a = tile + kk * 16384 + g * 4096 + (j >> 2) * 512 + 8 * (j & 3) +
+                   32 * (q ^ mn_swz(8 * g + (j >> 2)));
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)a);
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(a + 2048));
+    return __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  } else {
+    const int row = 16 * q + (lane & 15);
+    const int slot = (kk * 4 + (lane >> 4)) ^ (row & 7) ^ ((row >> 4) & 1);
+    return __builtin_bit_cast(bf16x8_t, reinterpret_cast<lds_u4*>(tile)[row * 8 + slot]);
+  }
+}
+
+// Fragment reads of one k-half: A blocks q = 8 wm + i, B blocks q = 4 wn + j
+// of the stage at st (A tile, then B tile 32 KiB further).
+template <bool AMN, bool BMN>
+OQ_DEV void read_frags(lds_cchar* st, int kk, int wm, int wn, int lane, bf16x8_t (&af)[8],
+                       bf16x8_t (&bq)[4]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) af[i] = frag<AMN>(st, 8 * wm + i, kk, lane);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) bq[j] = frag<BMN>(st + 32768, 4 * wn + j, kk, lane);
+}
+
+// One LDS stage: Ab / Bb point at the operands' tile origins at the stage's
+// first k, lds_stage is the stage's LDS byte address.
 OQ_DEV void stage_dma(const uint16_t* Ab, const uint16_t* Bb, const uint32_t (&aoff)[4],
                       const uint32_t (&boff)[4], uint32_t lds_stage, int wave) {
 #pragma unroll
@@ -468,16 +524,16 @@ OQ_DEV void mfma_half(f32x4_t (&acc)[8][4], const bf16x8_t (&af)[8], const bf16x
 }
 
 // One k-half of MFMAs (8 groups of 4, i-major) with the next fragment set's
-// 12 LDS reads (B first, then A, in the order the next half consumes them)
-// and, when DMA, one stage copy per group, each placed by hand between MFMA
-// groups; sched_barrier keeps the scheduler from bunching them again.
-template <bool READS, bool DMA>
+// 12 reads (B first, then A, in the order the next half consumes them) from
+// the stage rd and, when DMA, one stage copy per group into the stage at LDS
+// byte address wr, each placed by hand between MFMA groups; sched_barrier
+// keeps the scheduler from bunching them again.
+template <bool AMN, bool BMN, bool READS, bool DMA>
 OQ_DEV void half_sched(f32x4_t (&acc)[8][4], const bf16x8_t (&au)[8], const bf16x8_t (&bu)[4],
-                       const uint4* As, const uint4* Bs, int kk, int wm, int wn, int lane,
-                       bf16x8_t (&ad)[8], bf16x8_t (&bd)[4], const uint16_t* Ab,
-                       const uint16_t* Bb, const uint32_t (&aoff)[4], const uint32_t (&boff)[4],
-                       uint32_t lds_stage, int wave) {
-  const int fr = lane & 15, fk = lane >> 4;
+                       lds_cchar* rd, int kk, int wm, int wn, int lane, bf16x8_t (&ad)[8],
+                       bf16x8_t (&bd)[4], const uint16_t* Ab, const uint16_t* Bb,
+                       const uint32_t (&aoff)[4], const uint32_t (&boff)[4], uint32_t wr,
+                       int wave) {
 #pragma unroll
   for (int g = 0; g < 8; ++g) {
     if constexpr (READS) {
@@ -486,19 +542,13 @@ OQ_DEV void half_sched(f32x4_t (&acc)[8][4], const bf16x8_t (&au)[8], const bf16
       for (int r = 0; r < 12; ++r) {
         const int grp = r < 4 ? r / 2 : (r < 8 ? 2 + (r - 4) / 2 : r - 4);
         if (grp != g) continue;
-        if (r < 4) {
-          const int row = wn * 64 + 16 * r + fr;
-          bd[r] = as_bf16x8(Bs[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
-        } else {
-          const int i = r - 4;
-          const int row = wm * 128 + 16 * i + fr;
-          ad[i] = as_bf16x8(As[row * 8 + ((kk * 4 + fk) ^ (row & 7) ^ ((row >> 4) & 1))]);
-        }
+        if (r < 4) bd[r] = frag<BMN>(rd + 32768, 4 * wn + r, kk, lane);
+        else ad[r - 4] = frag<AMN>(rd, 8 * wm + r - 4, kk, lane);
       }
     }
     if constexpr (DMA) {
-      if (g & 1) dma16_s(Bb, boff[g >> 1], lds_stage + 32768 + (8 * (g >> 1) + wave) * 1024);
-      else       dma16_s(Ab, aoff[g >> 1], lds_stage + (8 * (g >> 1) + wave) * 1024);
+      if (g & 1) dma16_s(Bb, boff[g >> 1], wr + 32768 + (8 * (g >> 1) + wave) * 1024);
+      else       dma16_s(Ab, aoff[g >> 1], wr + (8 * (g >> 1) + wave) * 1024);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -514,7 +564,7 @@ OQ_DEV void half_sched(f32x4_t (&acc)[8][4], const bf16x8_t (&au)[8], const bf16
 // two register sets: the second half is read while the first half's MFMAs
 // run, and the next stage's first half is read (after the barrier that
 // publishes it) while the second half's MFMAs run.
-template <class Epi>
+template <class Epi, bool AMN, bool BMN>
 __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, int64_t M, int64_t N,
     int64_t K, int64_t lda, int64_t ldb, int tiles_m, int tiles_n, Epi epi) {
@@ -535,22 +585,14 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int nk = int(K / BK);
 
-  // DMA plan: instruction i of wave w fills tile rows 8 (8 i + w) .. +7;
-  // lane l covers row 64 i + 8 w + (l >> 3), slot l & 7
-  // 32-bit byte offsets from the tile's first row (a tile spans at most
-  // 256 rows; the launcher keeps 2 * 256 * ld below 2^32)
-  const uint16_t* At = A + m0 * lda;
-  const uint16_t* Bt = B + n0 * ldb;
-  uint32_t aoff[4], boff[4];                    // byte offsets
-  {
-    const int ch = (lane & 7) ^ (lane >> 3) ^ ((wave >> 1) & 1);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = 64 * i + 8 * wave + (lane >> 3);
-      aoff[i] = uint32_t(2 * (min<int64_t>(row, M - 1 - m0) * lda + 8 * ch));
-      boff[i] = uint32_t(2 * (min<int64_t>(row, N - 1 - n0) * ldb + 8 * ch));
-    }
-  }
+  // DMA plans: 32-bit byte offsets from each operand's tile origin (the
+  // launcher keeps 2 * 256 * ld (K-major) and 2 * 64 * ld (MN-major) below 2^32)
+  const uint16_t* At = AMN ? A + m0 : A + m0 * lda;
+  const uint16_t* Bt = BMN ? B + n0 : B + n0 * ldb;
+  const int64_t astep = AMN ? BK * lda : BK, bstep = BMN ? BK * ldb : BK;
+  uint32_t aoff[4], boff[4];
+  dma_plan<AMN>(aoff, m0, M, lda, wave, lane);
+  dma_plan<BMN>(boff, n0, N, ldb, wave, lane);
   const uint32_t lds0 = lds_addr_of(&lds[0][0][0]);
   const int wm = wave >> 2, wn = wave & 3;
 
@@ -566,9 +608,10 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
   wait_vm0();
   __syncthreads();
 
+  lds_cchar* lbase = (lds_cchar*)(&lds[0][0][0]);
   bf16x8_t a0[8], b0[4], a1[8], b1[4];
-  read_frags(lds[0][0], lds[0][1], 0, wm, wn, lane, a0, b0);
-  if (nk > 1) stage_dma(At + BK, Bt + BK, aoff, boff, lds0 + 65536, wave);
+  read_frags<AMN, BMN>(lbase, 0, wm, wn, lane, a0, b0);
+  if (nk > 1) stage_dma(At + astep, Bt + bstep, aoff, boff, lds0 + 65536, wave);
 
   // Stage kt sits in buffer kt & 1.  A buffer's last fragment reads complete
   // before the barrier in the middle of the iteration that uses it, so the
@@ -577,21 +620,21 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
   int kt = 0;
   for (; kt + 2 < nk; ++kt) {
     const int cur = kt & 1, nxt = cur ^ 1;
-    half_sched<true, false>(acc, a0, b0, lds[cur][0], lds[cur][1], 1, wm, wn, lane, a1, b1, At,
-                            Bt, aoff, boff, 0, wave);
+    half_sched<AMN, BMN, true, false>(acc, a0, b0, lbase + cur * 65536, 1, wm, wn, lane, a1, b1,
+                                      At, Bt, aoff, boff, 0, wave);
     wait_vm0();
     __syncthreads();
-    half_sched<true, true>(acc, a1, b1, lds[nxt][0], lds[nxt][1], 0, wm, wn, lane, a0, b0,
-                           At + int64_t(kt + 2) * BK, Bt + int64_t(kt + 2) * BK, aoff, boff,
-                           lds0 + cur * 65536, wave);
+    half_sched<AMN, BMN, true, true>(acc, a1, b1, lbase + nxt * 65536, 0, wm, wn, lane, a0, b0,
+                                     At + (kt + 2) * astep, Bt + (kt + 2) * bstep, aoff, boff,
+                                     lds0 + cur * 65536, wave);
   }
   for (; kt < nk; ++kt) {
     const int cur = kt & 1, nxt = cur ^ 1;
-    read_frags(lds[cur][0], lds[cur][1], 1, wm, wn, lane, a1, b1);
+    read_frags<AMN, BMN>(lbase + cur * 65536, 1, wm, wn, lane, a1, b1);
     mfma_half(acc, a0, b0);
     if (kt + 1 < nk) wait_vm0();
     __syncthreads();
-    if (kt + 1 < nk) read_frags(lds[nxt][0], lds[nxt][1], 0, wm, wn, lane, a0, b0);
+    if (kt + 1 < nk) read_frags<AMN, BMN>(lbase + nxt * 65536, 0, wm, wn, lane, a0, b0);
     mfma_half(acc, a1, b1);
   }
   __syncthreads();
@@ -709,24 +752,54 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   }
 }
 
+// The 8-wave kernel applies when K is a multiple of 64 and every operand
+// offset of a tile fits the kernel's 32-bit byte offsets.
+bool w8_ok(bool amn, bool bmn, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb) {
+  if (K <= 0 || K % BK || lda % 8 || ldb % 8) return false;
+  auto fits = [](bool mn, int64_t extent, int64_t ld) {
+    return mn ? (extent >= 8 && extent % 8 == 0 && extent <= ld && ld < (int64_t(1) << 25))
+              : ld < (int64_t(1) << 23);
+  };
+  return fits(amn, M, lda) && fits(bmn, N, ldb);
+}
+
+template <class Epi, bool AMN, bool BMN>
+void launch_w8(const void* A, const void* B, int64_t M, int64_t N, int64_t K, int64_t lda,
+               int64_t ldb, int64_t tm, int64_t tn, Epi epi, hipStream_t st) {
+  hipLaunchKernelGGL((gemm_bf16_w8_kernel<Epi, AMN, BMN>), dim3(unsigned(tm * tn)), dim3(NTHR8), 0,
+                     st, static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N, K,
+                     lda, ldb, int(tm), int(tn), epi);
+}
+
+// amn / bmn: operand stored MN-major (A as [K, M], B as [K, N]); bf16 only,
+// fp32 output only, 8-wave kernel only.
 template <class Epi>
 hipError_t launch(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
-                  int64_t lda, int64_t ldb, Epi epi, hipStream_t st) {
+                  int64_t lda, int64_t ldb, Epi epi, hipStream_t st, bool amn = false,
+                  bool bmn = false) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (bf16) {
     const int64_t tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
     if (tm * tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
-    const bool direct = K % BK == 0 && lda % 8 == 0 && ldb % 8 == 0 && K > 0 &&
-                        lda < (int64_t(1) << 23) && ldb < (int64_t(1) << 23);
-    if (direct)
-      hipLaunchKernelGGL((gemm_bf16_w8_kernel<Epi>), dim3(unsigned(tm * tn)), dim3(NTHR8), 0, st,
-                         static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N, K,
-                         lda, ldb, int(tm), int(tn), epi);
-    else
+    if (w8_ok(amn, bmn, M, N, K, lda, ldb)) {
+      if (!amn && !bmn) {
+        launch_w8<Epi, false, false>(A, B, M, N, K, lda, ldb, tm, tn, epi, st);
+      } else if constexpr (std::is_same<Epi, EpiF32>::value) {
+        if (amn && bmn) launch_w8<Epi, true, true>(A, B, M, N, K, lda, ldb, tm, tn, epi, st);
+        else if (bmn) launch_w8<Epi, false, true>(A, B, M, N, K, lda, ldb, tm, tn, epi, st);
+        else launch_w8<Epi, true, false>(A, B, M, N, K, lda, ldb, tm, tn, epi, st);
+      } else {
+        return hipErrorInvalidValue;
+      }
+    } else if (!amn && !bmn) {
       hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false>), dim3(unsigned(tm * tn)), dim3(NTHR), 0,
                          st, static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N,
                          K, lda, ldb, int(tm), int(tn), epi);
+    } else {
+      return hipErrorInvalidValue;
+    }
   } else {
+    if (amn || bmn) return hipErrorInvalidValue;
     const int64_t tm = (M + F32_TILE - 1) / F32_TILE, tn = (N + F32_TILE - 1) / F32_TILE;
     if (tm > 65535 || tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
     hipLaunchKernelGGL(gemm_f32_kernel<Epi>, dim3(unsigned(tn), unsigned(tm)), dim3(256), 0, st,
@@ -745,6 +818,18 @@ hipError_t gemm_nt_f32out(const void* A, const void* B, bool bf16, int64_t M, in
                           hipStream_t st) {
   const bool vec = ldc % 8 == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
   return launch(A, B, bf16, M, N, K, lda, ldb, EpiF32{C, ldc, vec}, st);
+}
+
+bool gemm_mn_supported(bool a_mn, bool b_mn, int64_t M, int64_t N, int64_t K, int64_t lda,
+                       int64_t ldb) {
+  return w8_ok(a_mn, b_mn, M, N, K, lda, ldb);
+}
+
+hipError_t gemm_f32out_mn(const void* A, bool a_mn, const void* B, bool b_mn, int64_t M,
+                          int64_t N, int64_t K, int64_t lda, int64_t ldb, float* C, int64_t ldc,
+                          hipStream_t st) {
+  const bool vec = ldc % 8 == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
+  return launch(A, B, true, M, N, K, lda, ldb, EpiF32{C, ldc, vec}, st, a_mn, b_mn);
 }
 
 hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int64_t N,

@@ -115,43 +115,74 @@ __global__ __launch_bounds__(256) void colstat_kernel(const TX* __restrict__ X, 
   }
 }
 
-__global__ __launch_bounds__(256) void let_grad_finish_kernel(
-    int64_t C, const float* s, const float* pw, int64_t npw, const float* psx, const float* ps1,
-    int64_t npa, const float* pb, int64_t npb, float* d_s, float* d_delta) {
-  const int64_t c = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (c >= C) return;
-  double w = 0.0, sx = 0.0, s1 = 0.0, b = 0.0;
-  if (pw)
-    for (int64_t i = 0; i < npw; ++i) w += double(pw[i * C + c]);
-  if (psx)
-    for (int64_t i = 0; i < npa; ++i) sx += double(psx[i * C + c]);
-  if (ps1)
-    for (int64_t i = 0; i < npa; ++i) s1 += double(ps1[i * C + c]);
-  if (pb)
-    for (int64_t i = 0; i < npb; ++i) b += double(pb[i * C + c]);
-  const double sc = s ? double(s[c]) : 1.0;
-  if (d_s) d_s[c] = float(w - sx / sc);
-  if (d_delta) d_delta[c] = float(b - s1 / sc);
+// Column sums of [rows, C] partial arrays: a block of 16 waves covers 64
+// columns (lane = column); wave w adds rows w, w + 16, ... in fp64, and the 16
+// wave sums are combined through LDS in wave order (fixed, deterministic).
+constexpr int CS_WAVES = 16;
+
+OQ_DEV double strip_sum(const float* parts, int64_t rows, int64_t C, int64_t c, int w) {
+  double acc = 0.0;
+  if (parts && c < C)
+    for (int64_t i = w; i < rows; i += CS_WAVES) acc += double(parts[i * C + c]);
+  return acc;
 }
 
-__global__ __launch_bounds__(256) void let_init_finish_kernel(int64_t C, int64_t T,
-                                                              const float* ax_parts, int64_t nax,
-                                                              const double* sum_parts,
-                                                              const float* aw_parts, int64_t naw,
-                                                              float* s, float* delta) {
-  const int64_t c = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (c >= C) return;
-  float ax = 0.f, aw = 0.f;
-  double sm = 0.0;
-  for (int64_t i = 0; i < nax; ++i) {
-    ax = fmaxf(ax, ax_parts[i * C + c]);
-    sm += sum_parts[i * C + c];
+template <int NA>
+OQ_DEV void strip_combine(double (&v)[NA], double (*sh)[CS_WAVES][64], int w, int lane) {
+#pragma unroll
+  for (int a = 0; a < NA; ++a) sh[a][w][lane] = v[a];
+  __syncthreads();
+#pragma unroll
+  for (int a = 0; a < NA; ++a) {
+    double r = 0.0;
+    for (int k = 0; k < CS_WAVES; ++k) r += sh[a][k][lane];
+    v[a] = r;
   }
-  for (int64_t i = 0; i < naw; ++i) aw = fmaxf(aw, aw_parts[i * C + c]);
+}
+
+__global__ __launch_bounds__(64 * CS_WAVES) void let_grad_finish_kernel(
+    int64_t C, const float* s, const float* pw, int64_t npw, const float* psx, const float* ps1,
+    int64_t npa, const float* pb, int64_t npb, float* d_s, float* d_delta) {
+  __shared__ double sh[4][CS_WAVES][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t c = int64_t(blockIdx.x) * 64 + lane;
+  double v[4] = {strip_sum(pw, npw, C, c, w), strip_sum(psx, npa, C, c, w),
+                 strip_sum(ps1, npa, C, c, w), strip_sum(pb, npb, C, c, w)};
+  strip_combine<4>(v, sh, w, lane);
+  if (w != 0 || c >= C) return;
+  const double sc = s ? double(s[c]) : 1.0;
+  if (d_s) d_s[c] = float(v[0] - v[1] / sc);
+  if (d_delta) d_delta[c] = float(v[3] - v[2] / sc);
+}
+
+__global__ __launch_bounds__(64 * CS_WAVES) void let_init_finish_kernel(
+    int64_t C, int64_t T, const float* ax_parts, int64_t nax, const double* sum_parts,
+    const float* aw_parts, int64_t naw, float* s, float* delta) {
+  __shared__ double sh[1][CS_WAVES][64];
+  __shared__ float shm[2][CS_WAVES][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t c = int64_t(blockIdx.x) * 64 + lane;
+  float ax = 0.f, aw = 0.f;
+  double v[1] = {0.0};
+  if (c < C) {
+    for (int64_t i = w; i < nax; i += CS_WAVES) {
+      ax = fmaxf(ax, ax_parts[i * C + c]);
+      v[0] += sum_parts[i * C + c];
+    }
+    for (int64_t i = w; i < naw; i += CS_WAVES) aw = fmaxf(aw, aw_parts[i * C + c]);
+  }
+  shm[0][w][lane] = ax;
+  shm[1][w][lane] = aw;
+  strip_combine<1>(v, sh, w, lane);
+  if (w != 0 || c >= C) return;
+  for (int k = 0; k < CS_WAVES; ++k) {
+    ax = fmaxf(ax, shm[0][k][lane]);
+    aw = fmaxf(aw, shm[1][k][lane]);
+  }
   ax = fmaxf(ax, 1e-5f);
   aw = fmaxf(aw, 1e-5f);
-  s[c] = __fsqrt_rn(ax) / __fsqrt_rn(aw);
-  delta[c] = float(sm / double(T));
+  s[c] = div_rn(sqrt_rn(ax), sqrt_rn(aw));
+  delta[c] = float(v[0] / double(T));
 }
 
 // ------------------------------------------------------------------ loss
@@ -298,7 +329,7 @@ hipError_t let_grad_finish(int64_t C, const float* s, const float* pw, int64_t n
                            const float* psx, const float* ps1, int64_t npa, const float* pb,
                            int64_t npb, float* d_s, float* d_delta, hipStream_t st) {
   if (C <= 0) return hipSuccess;
-  hipLaunchKernelGGL(let_grad_finish_kernel, dim3(unsigned((C + 255) / 256)), dim3(256), 0, st, C,
+  hipLaunchKernelGGL(let_grad_finish_kernel, dim3(unsigned((C + 63) / 64)), dim3(64 * CS_WAVES), 0, st, C,
                      s, pw, npw, psx, ps1, npa, pb, npb, d_s, d_delta);
   return hipGetLastError();
 }
@@ -307,7 +338,7 @@ hipError_t let_init_finish(int64_t C, int64_t T, const float* ax_parts, int64_t 
                            const double* sum_parts, const float* aw_parts, int64_t naw, float* s,
                            float* delta, hipStream_t st) {
   if (C <= 0) return hipSuccess;
-  hipLaunchKernelGGL(let_init_finish_kernel, dim3(unsigned((C + 255) / 256)), dim3(256), 0, st, C,
+  hipLaunchKernelGGL(let_init_finish_kernel, dim3(unsigned((C + 63) / 64)), dim3(64 * CS_WAVES), 0, st, C,
                      T, ax_parts, nax, sum_parts, aw_parts, naw, s, delta);
   return hipGetLastError();
 }

@@ -48,6 +48,15 @@ int gemm_part_tile_n(bool bf16);
 
 hipError_t gemm_nt_f32out(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
                           int64_t lda, int64_t ldb, float* C, int64_t ldc, hipStream_t st);
+// bf16 C[M,N] = op(A) op(B)^T into fp32 with either operand stored MN-major
+// (a_mn: A as [K, M] with row stride lda; b_mn: B as [K, N] with row stride
+// ldb), read straight from that layout.  gemm_mn_supported tells whether the
+// shapes qualify (K a multiple of 64 and aligned strides).
+bool gemm_mn_supported(bool a_mn, bool b_mn, int64_t M, int64_t N, int64_t K, int64_t lda,
+                       int64_t ldb);
+hipError_t gemm_f32out_mn(const void* A, bool a_mn, const void* B, bool b_mn, int64_t M,
+                          int64_t N, int64_t K, int64_t lda, int64_t ldb, float* C, int64_t ldc,
+                          hipStream_t st);
 hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
                          int64_t lda, int64_t ldb, void* C, bool c_bf16, int64_t ldc,
                          const float* bias, hipStream_t st);

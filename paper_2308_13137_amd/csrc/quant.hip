@@ -14,6 +14,8 @@
 //    then the four wave results combined in a fixed order through LDS.
 // Every reduction has a fixed shape, so results are bitwise reproducible.
 #include <float.h>
+#include <algorithm>
+#include <type_traits>
 #include <limits.h>
 
 #include "common.h"
@@ -326,6 +328,201 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
   }
 }
 
+// ------------------------------------------------------------------ LWC, lane-owned runs
+// Groups of at most 512 weights without LET scaling: each lane owns a run of
+// E consecutive weights of one row (E / 8 independent 16-byte loads in
+// flight), takes the run's max / min (and, for the backward, the first index
+// holding each), and combines with the other group / E lanes of its group
+// (adjacent, aligned lanes) by butterflies.  The group parameters are
+// then computed once per E weights instead of once per 8, and the kernel has
+// no divergent branches.  A tail lane past the last run repeats the last run
+// without storing, so every butterfly sees whole groups.
+
+// Register image of a run of E elements as 16-byte vectors.
+template <typename TW, int E>
+struct Run {
+  static constexpr int NV = sizeof(TW) == 2 ? E / 8 : E / 4;
+  uint4 v[NV];
+  OQ_DEV void load(const TW* p) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = reinterpret_cast<const uint4*>(p)[i];
+  }
+  OQ_DEV static uint32_t word(const uint4& q, int k) {
+    return k == 0 ? q.x : (k == 1 ? q.y : (k == 2 ? q.z : q.w));
+  }
+  OQ_DEV float at(int i) const {
+    if constexpr (sizeof(TW) == 2) {
+      const uint32_t w = word(v[i >> 3], (i >> 1) & 3);
+      return __uint_as_float((i & 1) ? (w & 0xffff0000u) : (w << 16));
+    } else {
+      return __uint_as_float(word(v[i >> 2], i & 3));
+    }
+  }
+};
+
+// max / min of a run (values only: the forward parameters need no index)
+template <typename TW, int E>
+OQ_DEV void run_range(const Run<TW, E>& x, float& mx, float& mn) {
+  mx = x.at(0);
+  mn = mx;
+#pragma unroll
+  for (int i = 1; i < E; ++i) {
+    mx = fmaxf(mx, x.at(i));
+    mn = fminf(mn, x.at(i));
+  }
+}
+
+// Index (within the row) of the first element of the run equal to v.
+template <typename TW, int E>
+OQ_DEV int run_first(const Run<TW, E>& x, int col0, float v) {
+  int idx = E - 1;
+#pragma unroll
+  for (int i = E - 2; i >= 0; --i) idx = x.at(i) == v ? i : idx;
+  return col0 + idx;
+}
+
+// (max, min) over the L aligned lanes of a group, values only.
+OQ_DEV void dyn_group_range(float& mx, float& mn, int L) {
+  for (int off = 1; off < L; off <<= 1) {
+    mx = fmaxf(mx, __shfl_xor(mx, off));
+    mn = fminf(mn, __shfl_xor(mn, off));
+  }
+}
+
+template <typename TW, typename TQ, int E, bool CODES>
+__global__ __launch_bounds__(NT) void lwc_fwd_run_kernel(
+    const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ gl,
+    const float* __restrict__ bl, int bits, int group, TQ* __restrict__ wdq,
+    uint8_t* __restrict__ codes, float* __restrict__ hout, float* __restrict__ zout) {
+  const uint32_t runs = uint32_t(c_in / E), nrun = uint32_t(c_out) * runs;  // < 2^31 (host)
+  uint32_t t = blockIdx.x * NT + threadIdx.x;
+  const bool valid = t < nrun;
+  if (!valid) t = nrun - 1;
+  const uint32_t rq = t / runs;
+  const int64_t row = rq;
+  const int col0 = int(t - rq * runs) * E;
+  const float qmax = float((1 << bits) - 1);
+
+  Run<TW, E> x;
+  x.load(W + row * c_in + col0);
+  float mx, mn;
+  run_range(x, mx, mn);
+  if (group > E) dyn_group_range(mx, mn, group / E);
+  const int64_t gi = row * (c_in / group) + col0 / group;
+  const QParams p = make_qparams(mx, mn, clip_strength(gl[gi]), clip_strength(bl[gi]), qmax);
+  if (!valid) return;
+  // rint(u) and z are integers below 2^24, so clamp(rint(u) + z, 0, qmax) - z
+  // is exactly med3(rint(u), -z, qmax - z): one instruction for Eq. 2's clamp
+  const float lo = -p.z, hi = qmax - p.z;
+#pragma unroll
+  for (int c = 0; c < E / 8; ++c) {
+    float q[8], d[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float tq = __builtin_amdgcn_fmed3f(rintf(x.at(8 * c + e) * p.r), lo, hi);
+      d[e] = tq * p.h;
+      if constexpr (CODES) q[e] = tq + p.z;
+    }
+    if (wdq) store8(wdq + row * c_in + col0 + 8 * c, d);
+    if constexpr (CODES) store8_codes(codes + row * c_in + col0 + 8 * c, q);
+  }
+  if (col0 % group == 0) {
+    if (hout) hout[gi] = p.h;
+    if (zout) zout[gi] = p.z;
+  }
+}
+
+template <typename TW, int E, bool DWT>
+__global__ __launch_bounds__(NT) void lwc_bwd_run_kernel(
+    const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ gl,
+    const float* __restrict__ bl, int bits, int group, const float* __restrict__ dW,
+    float* __restrict__ dgl, float* __restrict__ dbl, float* __restrict__ dWt) {
+  const uint32_t runs = uint32_t(c_in / E), nrun = uint32_t(c_out) * runs;  // < 2^31 (host)
+  uint32_t t = blockIdx.x * NT + threadIdx.x;
+  const bool valid = t < nrun;
+  if (!valid) t = nrun - 1;
+  const uint32_t rq = t / runs;
+  const int64_t row = rq;
+  const int col0 = int(t - rq * runs) * E;
+  const float qmax = float((1 << bits) - 1);
+
+  Run<TW, E> x;
+  x.load(W + row * c_in + col0);
+  const float* grow = dW + row * c_in + col0;
+  Run<float, E> gr;                  // the run's dL/dW^, all loads in flight at once
+  gr.load(grow);
+  // max / min of the group; with DWT also the lowest index holding each
+  // (values first, then the first matching index in the run, then (max,
+  // index) across the group's lanes): only dW~ places the max/min gradient
+  float mx, mn;
+  run_range(x, mx, mn);
+  int imx = 0, imn = 0;
+  if constexpr (DWT) {
+    imx = run_first(x, col0, mx);
+    imn = run_first(x, col0, mn);
+    if (group > E) dyn_group_minmax(mx, imx, mn, imn, group / E);
+  } else {
+    if (group > E) dyn_group_range(mx, mn, group / E);
+  }
+  const int64_t gi = row * (c_in / group) + col0 / group;
+  const QParams p = make_qparams(mx, mn, clip_strength(gl[gi]), clip_strength(bl[gi]), qmax);
+  // S_h = sum g ((q - z) - m u), S_z = sum g (1 - m): per 8-element chunk, then a tree
+  // q - z = med3(rint(u), -z, qmax - z) exactly (integers below 2^24), and the
+  // element is inside the clamp (m = 1) exactly when med3 left rint(u) alone
+  const float lo = -p.z, hi = qmax - p.z;
+  float ph[E / 8], pz[E / 8];
+#pragma unroll
+  for (int c = 0; c < E / 8; ++c) {
+    float sh = 0.f, sz = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float g = gr.at(8 * c + e);
+      const float u = x.at(8 * c + e) * p.r;
+      const float ru = rintf(u);
+      const float tq = __builtin_amdgcn_fmed3f(ru, lo, hi);
+      const bool m = tq == ru;
+      sh += g * (m ? tq - u : tq);
+      sz += m ? 0.0f : g;
+    }
+    ph[c] = sh;
+    pz[c] = sz;
+  }
+#pragma unroll
+  for (int w = 1; w < E / 8; w <<= 1)
+#pragma unroll
+    for (int c = 0; c < E / 8; c += 2 * w) {
+      ph[c] += ph[c + w];
+      pz[c] += pz[c + w];
+    }
+  float sh = ph[0], sz = pz[0];
+  if (group > E) {
+    sh = dyn_group_sum(sh, group / E);
+    sz = dyn_group_sum(sz, group / E);
+  }
+  const QGrad qg = quant_group_grad(sh, sz, mx, mn, p, qmax);
+  if (!valid) return;
+  if (col0 % group == 0) {
+    dgl[gi] = qg.dgamma * p.gamma * (1.0f - p.gamma);
+    dbl[gi] = qg.dbeta * p.beta * (1.0f - p.beta);
+  }
+  if constexpr (DWT) {
+#pragma unroll
+    for (int c = 0; c < E / 8; ++c) {
+      float d[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int col = col0 + 8 * c + e;
+        const float ru = rintf(x.at(8 * c + e) * p.r);
+        float v = __builtin_amdgcn_fmed3f(ru, lo, hi) == ru ? gr.at(8 * c + e) : 0.0f;
+        if (col == imx) v += qg.dmx;
+        if (col == imn) v += qg.dmn;
+        d[e] = v;
+      }
+      store8(dWt + row * c_in + col0 + 8 * c, d);
+    }
+  }
+}
+
 // ------------------------------------------------------------------ activation forward
 // x~ = (x - delta) * (1/s); per token row Eq. 2 with gamma = beta = 1.
 template <typename TX, typename TQ, int KC>
@@ -351,7 +548,7 @@ __global__ __launch_bounds__(NT) void act_fwd_kernel(
       if (s) {
         load8(s + 8 * j, rs[k]);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) rs[k][e] = 1.0f / rs[k][e];
+        for (int e = 0; e < 8; ++e) rs[k][e] = div_rn(1.0f, rs[k][e]);
       }
       if (delta) load8(delta + 8 * j, dl[k]);
     }
@@ -434,7 +631,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
       if (s) {
         load8(s + 8 * j, rs[k]);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) rs[k][e] = 1.0f / rs[k][e];
+        for (int e = 0; e < 8; ++e) rs[k][e] = div_rn(1.0f, rs[k][e]);
       }
       if (delta) load8(delta + 8 * j, dl[k]);
     }
@@ -562,6 +759,36 @@ hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
                    bool dq_bf16, uint8_t* codes, float* h, float* z, hipStream_t st) {
   if (!quant_shape_supported(c_in, group)) return hipErrorInvalidValue;
   if (c_out <= 0) return hipSuccess;
+  if (small_group(group) && !s && c_out * c_in < (int64_t(1) << 34)) {
+    const int E = int(std::min<int64_t>(group, 128));
+    const int64_t nrun = c_out * (c_in / E);
+    const dim3 grid(unsigned((nrun + NT - 1) / NT));
+    auto run = [&](auto tw, auto tq, auto ec) {
+      using TW = decltype(tw);
+      using TQ = decltype(tq);
+      constexpr int Ec = decltype(ec)::value;
+      if (codes)
+        hipLaunchKernelGGL((lwc_fwd_run_kernel<TW, TQ, Ec, true>), grid, dim3(NT), 0, st,
+                           static_cast<const TW*>(W), c_out, c_in, gl, bl, bits, int(group),
+                           static_cast<TQ*>(W_dq), codes, h, z);
+      else
+        hipLaunchKernelGGL((lwc_fwd_run_kernel<TW, TQ, Ec, false>), grid, dim3(NT), 0, st,
+                           static_cast<const TW*>(W), c_out, c_in, gl, bl, bits, int(group),
+                           static_cast<TQ*>(W_dq), codes, h, z);
+    };
+    auto by_e = [&](auto tw, auto tq) {
+      switch (E) {
+        case 8: run(tw, tq, std::integral_constant<int, 8>{}); break;
+        case 16: run(tw, tq, std::integral_constant<int, 16>{}); break;
+        case 32: run(tw, tq, std::integral_constant<int, 32>{}); break;
+        case 64: run(tw, tq, std::integral_constant<int, 64>{}); break;
+        default: run(tw, tq, std::integral_constant<int, 128>{}); break;
+      }
+    };
+    if (w_bf16) dq_bf16 ? by_e(uint16_t{}, uint16_t{}) : by_e(uint16_t{}, float{});
+    else dq_bf16 ? by_e(float{}, uint16_t{}) : by_e(float{}, float{});
+    return hipGetLastError();
+  }
   const int R = rows_per_block(c_out, LWC_BLOCKS);
   const dim3 grid(unsigned((c_out + R - 1) / R));
   const bool whole = !small_group(group);
@@ -600,6 +827,34 @@ hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
                    float* dgl, float* dbl, float* dW_tilde, float* ds_parts, hipStream_t st) {
   if (!quant_shape_supported(c_in, group)) return hipErrorInvalidValue;
   if (c_out <= 0) return hipSuccess;
+  if (small_group(group) && !s && !ds_parts && c_out * c_in < (int64_t(1) << 34)) {
+    const int E = int(std::min<int64_t>(group, 32));
+    const int64_t nrun = c_out * (c_in / E);
+    const dim3 grid(unsigned((nrun + NT - 1) / NT));
+    auto run = [&](auto tw, auto ec) {
+      using TW = decltype(tw);
+      constexpr int Ec = decltype(ec)::value;
+      if (dW_tilde)
+        hipLaunchKernelGGL((lwc_bwd_run_kernel<TW, Ec, true>), grid, dim3(NT), 0, st,
+                           static_cast<const TW*>(W), c_out, c_in, gl, bl, bits, int(group), dW,
+                           dgl, dbl, dW_tilde);
+      else
+        hipLaunchKernelGGL((lwc_bwd_run_kernel<TW, Ec, false>), grid, dim3(NT), 0, st,
+                           static_cast<const TW*>(W), c_out, c_in, gl, bl, bits, int(group), dW,
+                           dgl, dbl, dW_tilde);
+    };
+    auto by_e = [&](auto tw) {
+      switch (E) {
+        case 8: run(tw, std::integral_constant<int, 8>{}); break;
+        case 16: run(tw, std::integral_constant<int, 16>{}); break;
+        case 32: run(tw, std::integral_constant<int, 32>{}); break;
+        default: run(tw, std::integral_constant<int, 64>{}); break;
+      }
+    };
+    if (w_bf16) by_e(uint16_t{});
+    else by_e(float{});
+    return hipGetLastError();
+  }
   const int R = rows_per_block(c_out, LWC_BLOCKS);
   const dim3 grid(unsigned((c_out + R - 1) / R));
   const bool whole = !small_group(group);

@@ -38,6 +38,7 @@ SIGNATURES = {
     "oq_let_init_workspace_size": (_I, [_I64, _I64, _P, _I, _PSZ]),
     "oq_fp_target": (_I, [_P, _P, _I, _P, _I64, _I64, _I64, _P, _P]),
     "oq_matmul_nt": (_I, [_P, _P, _I, _I64, _I64, _I64, _P, _I, _P]),
+    "oq_matmul": (_I, [_P, _I, _P, _I, _I64, _I64, _I64, _P, _P]),
     "oq_adamw_step": (_I, [_P, _P, _P, _P, _I64, _D, _D, _D, _D, _D, _I, _P]),
     "oq_block_workspace_size": (_I, [_P, _PSZ]),
     "oq_block_calib_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
@@ -260,6 +261,20 @@ def matmul_nt(A, B, out_dtype=torch.float32, stream=None):
     _check(lib().oq_matmul_nt(_ptr(A), _ptr(B), _dt(A), M, N, K, _ptr(out),
                               OQ_BF16 if out_dtype == torch.bfloat16 else OQ_F32, _stream(stream)))
     return out
+
+
+def matmul(A, B, a_mn=False, b_mn=False, stream=None):
+    """fp32 C = opA opB^T of bf16 operands, opA = A [M, K] or (a_mn) A^T with A
+    stored [K, M]; opB = B [N, K] or (b_mn) B^T with B stored [K, N]."""
+    M = A.shape[1] if a_mn else A.shape[0]
+    K = A.shape[0] if a_mn else A.shape[1]
+    N = B.shape[1] if b_mn else B.shape[0]
+    if (B.shape[0] if b_mn else B.shape[1]) != K:
+        raise OQError("inner dimensions differ")
+    Cm = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    _check(lib().oq_matmul(_ptr(A), int(a_mn), _ptr(B), int(b_mn), M, N, K, _ptr(Cm),
+                           _stream(stream)))
+    return Cm
 
 
 def adamw_step(p, g, m, v, step, lr, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.0, stream=None):

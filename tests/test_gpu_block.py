@@ -3,7 +3,9 @@
 Each workload keeps the shape structure of its full-size configuration
 (seven LLaMA linears on four sites, GQA k/v, LET on three sites, per-token
 activation quantisation, per-channel or grouped weights) at sizes the oracle
-finishes in seconds, with a token count that leaves a ragged last tile.
+finishes in seconds.  Most token counts leave a ragged last tile (the
+gradient products then use transposed copies); the multiples of 64 take the
+direct path that reads X^, dY^T and W^ as stored.
 Bar: loss, row losses and every gradient within 2e-2 normwise relative error
 (bf16 matrix-core products); the fp32 workload within 1e-4."""
 import numpy as np
@@ -28,6 +30,11 @@ WORKLOADS = [
     small_llama("c4_small", hidden=320, ffn=832, T=136, w_bits=2, group=64),
     small_llama("c5_small", hidden=512, ffn=1024, T=200, w_bits=4, group=128, kv=128, sigma=0.015),
     small_llama("let_noact", hidden=256, ffn=512, T=128, w_bits=4, group=64, let=True),
+    # token counts that are multiples of 64: the gradient products read X^, dY^T
+    # and W^ as stored instead of transposed copies
+    small_llama("c3_t256", hidden=256, ffn=512, T=256, w_bits=4, let=True, act_bits=4),
+    small_llama("c2_t320", hidden=256, ffn=768, T=320, w_bits=3, group=128),
+    small_llama("c5_t192", hidden=512, ffn=1024, T=192, w_bits=4, group=128, kv=128, sigma=0.015),
 ]
 
 

@@ -179,8 +179,9 @@ def test_bench_size_all_codes(c2_full):
 # ---------------------------------------------------------------- full width, fewer tokens
 def test_llama7b_let_act_full_width():
     """LLaMA-7B W4A4 LET+LWC, per-channel weights, per-token activations, at
-    full width and 2,000 tokens: every row and every LET gradient."""
-    w = configs.C3.with_tokens(2000)
+    full width and 2,048 tokens (gradient products read X^, dY^T, W^ as
+    stored): every row and every LET gradient."""
+    w = configs.C3.with_tokens(2048)
     X, W, gl, bl = draw(w, seed=12, logit_range=(2.0, 6.0))
     Xh = [host(x) for x in X]
     Wh = [host(x) for x in W]
@@ -219,9 +220,9 @@ def test_llama7b_let_act_full_width():
 
 
 def test_llama13b_twenty_steps_full_width():
-    """LLaMA-13B W2A16 g64 at full width, 1,000 tokens, twenty AdamW steps on
+    """LLaMA-13B W2A16 g64 at full width, 1,024 tokens, twenty AdamW steps on
     one batch: sampled rows' losses at every step and their logits after."""
-    w = configs.C4.with_tokens(1000)
+    w = configs.C4.with_tokens(1024)
     X, W, gl, bl = draw(w, seed=13, logit_range=(4.0, 4.0))
     rows = [sample_rows(l.c_out, 16, 200 + i) for i, l in enumerate(w.linears)]
     Xh = [host(x) for x in X]
@@ -255,7 +256,8 @@ def test_llama13b_twenty_steps_full_width():
 
 
 def test_llama2_70b_full_width():
-    """LLaMA-2-70B W4A16 g128 with GQA k/v at full width, 2,056 tokens:
+    """LLaMA-2-70B W4A16 g128 with GQA k/v at full width, 2,056 tokens (a
+    ragged token count: the weight gradient uses the transposed copy of X^):
     sampled rows of every linear and the loss identity."""
     w = configs.C5.with_tokens(2056)
     X, W, gl, bl = draw(w, seed=14)

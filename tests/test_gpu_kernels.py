@@ -40,6 +40,31 @@ def test_matmul_nt_bf16(M, N, K):
     assert np.max(np.abs(got16 - ref) / (np.abs(ref) + 1e-3 * np.max(np.abs(ref)))) < 2 ** -7
 
 
+@pytest.mark.parametrize("a_mn,b_mn", [(False, True), (True, True), (True, False), (False, False)])
+@pytest.mark.parametrize("M,N,K", [(256, 256, 64), (392, 1000, 640), (8, 264, 128),
+                                   (1024, 768, 4096), (520, 16, 192)])
+def test_matmul_operand_layouts(M, N, K, a_mn, b_mn):
+    """Operands stored MN-major ([K, M] / [K, N]) are read as stored (the
+    step's gradient products); M, N that are not tile multiples exercise the
+    clamped tile edges."""
+    print(f"matmul layouts a_mn={a_mn} b_mn={b_mn} M={M} N={N} K={K}", flush=True)
+    rng = np.random.default_rng(M * 3 + N * 5 + K + 2 * a_mn + b_mn)
+    A = bf16_exact(rng.standard_normal((M, K)))
+    B = bf16_exact(rng.standard_normal((N, K)))
+    ref = A.astype(np.float64) @ B.astype(np.float64).T
+    Ad = dev(np.ascontiguousarray(A.T) if a_mn else A, torch.bfloat16)
+    Bd = dev(np.ascontiguousarray(B.T) if b_mn else B, torch.bfloat16)
+    got = host(oq.matmul(Ad, Bd, a_mn=a_mn, b_mn=b_mn))
+    assert normwise(got, ref) < TOL_GEMM
+
+
+def test_matmul_operand_layout_unsupported():
+    A = torch.zeros((96, 64), dtype=torch.bfloat16, device="cuda")     # K = 96: not a multiple of 64
+    B = torch.zeros((96, 64), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(oq.OQError, match="UNSUPPORTED|MN-major"):
+        oq.matmul(A, B, a_mn=True, b_mn=True)
+
+
 @pytest.mark.parametrize("M,N,K", [(64, 64, 16), (130, 70, 264), (256, 256, 256)])
 def test_matmul_nt_f32(M, N, K):
     print(f"matmul f32 M={M} N={N} K={K}", flush=True)
