@@ -523,6 +523,116 @@ __global__ __launch_bounds__(NT) void lwc_bwd_run_kernel(
   }
 }
 
+// ------------------------------------------------------------------ activation forward, wave per row
+// Token rows of up to 512 * CH elements: each wave takes whole rows (grid
+// stride); lane l holds chunks l, l + 64, ... of its row, all loads in flight
+// at once.  The row's max / min is a wave butterfly (values only: the
+// forward parameters need no index); LET's 1/s and delta are staged in LDS
+// once per workgroup.  Same operation order as the per-block kernel below.
+template <typename TX>
+struct Chunk8 {
+  static constexpr int NV = sizeof(TX) == 2 ? 1 : 2;
+  uint4 v[NV];
+  OQ_DEV void load(const TX* p) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = reinterpret_cast<const uint4*>(p)[i];
+  }
+  OQ_DEV float at(int e) const {
+    const uint4& q = v[sizeof(TX) == 2 ? 0 : e >> 2];
+    if constexpr (sizeof(TX) == 2) {
+      const uint32_t w = Run<uint16_t, 8>::word(q, e >> 1);
+      return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+    } else {
+      return __uint_as_float(Run<float, 8>::word(q, e & 3));
+    }
+  }
+};
+
+template <typename TX, int CH>
+__global__ __launch_bounds__(NT) void act_fwd_row_kernel(
+    const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
+    const float* __restrict__ delta, TX* __restrict__ xdq, uint8_t* __restrict__ codes,
+    float* __restrict__ hout, float* __restrict__ zout) {
+  extern __shared__ float shl[];     // [C] 1/s, then [C] delta (LET only)
+  const bool let = s || delta;
+  const int nch = int(C / 8);
+  if (let) {
+    for (int c = threadIdx.x; c < C; c += NT) {
+      shl[c] = s ? div_rn(1.0f, s[c]) : 1.0f;
+      shl[C + c] = delta ? delta[c] : 0.0f;
+    }
+    __syncthreads();
+  }
+  const int lane = threadIdx.x & 63;
+  const int64_t nw = int64_t(gridDim.x) * (NT / 64);
+  const bool quant = bits < 16;
+  const float qmax = quant ? float((1 << bits) - 1) : 0.0f;
+  for (int64_t row = int64_t(blockIdx.x) * (NT / 64) + (threadIdx.x >> 6); row < T; row += nw) {
+    const TX* xr = X + row * C;
+    Chunk8<TX> raw[CH];
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      const int j = lane + 64 * k;
+      if (j < nch) raw[k].load(xr + 8 * j);
+    }
+    // x~ = (x - delta) (1/s), one rounding per operation
+    auto xt = [&](int k, int e) {
+      const float x = raw[k].at(e);
+      if (!let) return x;
+      const int c = 8 * (lane + 64 * k) + e;
+      return (x - shl[C + c]) * shl[c];
+    };
+    if (!quant) {
+#pragma unroll
+      for (int k = 0; k < CH; ++k) {
+        const int j = lane + 64 * k;
+        if (j >= nch) continue;
+        float d[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) d[e] = xt(k, e);
+        store8(xdq + row * C + 8 * j, d);
+      }
+      continue;
+    }
+    float mx = -FLT_MAX, mn = FLT_MAX;
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      if (lane + 64 * k >= nch) continue;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float v = xt(k, e);
+        mx = fmaxf(mx, v);
+        mn = fminf(mn, v);
+      }
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      mx = fmaxf(mx, __shfl_xor(mx, off));
+      mn = fminf(mn, __shfl_xor(mn, off));
+    }
+    const QParams p = make_qparams(mx, mn, 1.0f, 1.0f, qmax);
+    const float lo = -p.z, hi = qmax - p.z;     // clamp as one med3 (exact integers)
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      const int j = lane + 64 * k;
+      if (j >= nch) continue;
+      float q[8], d[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float tq = __builtin_amdgcn_fmed3f(rintf(xt(k, e) * p.r), lo, hi);
+        d[e] = tq * p.h;
+        q[e] = tq + p.z;
+      }
+      if (xdq) store8(xdq + row * C + 8 * j, d);
+      if (codes) store8_codes(codes + row * C + 8 * j, q);
+    }
+    if (lane == 0) {
+      if (hout) hout[row] = p.h;
+      if (zout) zout[row] = p.z;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ activation forward
 // x~ = (x - delta) * (1/s); per token row Eq. 2 with gamma = beta = 1.
 template <typename TX, typename TQ, int KC>
@@ -885,6 +995,34 @@ hipError_t act_fwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, c
   const int kc = kc_for(C);
   if (C <= 0 || C % 8 || kc == 0) return hipErrorInvalidValue;
   if (T <= 0) return hipSuccess;
+  const int64_t per_lane = (C / 8 + 63) / 64;
+  if (x_bf16 == dq_bf16 && per_lane <= 32 && (X_dq || bits < 16)) {
+    const int ch = per_lane <= 2 ? 2 : per_lane <= 4 ? 4 : per_lane <= 8 ? 8 : per_lane <= 12 ? 12
+                 : per_lane <= 16 ? 16 : per_lane <= 24 ? 24 : 32;
+    const unsigned lds = (s || delta) ? unsigned(2 * C * sizeof(float)) : 0u;
+    const dim3 grid(unsigned(std::min<int64_t>((T + NT / 64 - 1) / (NT / 64), 2048)));
+    auto run = [&](auto tx, auto chc) {
+      using TX = decltype(tx);
+      constexpr int CHc = decltype(chc)::value;
+      hipLaunchKernelGGL((act_fwd_row_kernel<TX, CHc>), grid, dim3(NT), lds, st,
+                         static_cast<const TX*>(X), T, C, bits, s, delta, static_cast<TX*>(X_dq),
+                         codes, h, z);
+    };
+    auto by_ch = [&](auto tx) {
+      switch (ch) {
+        case 2: run(tx, std::integral_constant<int, 2>{}); break;
+        case 4: run(tx, std::integral_constant<int, 4>{}); break;
+        case 8: run(tx, std::integral_constant<int, 8>{}); break;
+        case 12: run(tx, std::integral_constant<int, 12>{}); break;
+        case 16: run(tx, std::integral_constant<int, 16>{}); break;
+        case 24: run(tx, std::integral_constant<int, 24>{}); break;
+        default: run(tx, std::integral_constant<int, 32>{}); break;
+      }
+    };
+    if (x_bf16) by_ch(uint16_t{});
+    else by_ch(float{});
+    return hipGetLastError();
+  }
   const int R = rows_per_block(T, ACT_BLOCKS);
   const dim3 grid(unsigned((T + R - 1) / R));
   auto go = [&](auto tx, auto tq, auto kcc) {
