@@ -28,6 +28,99 @@ if ROOT not in sys.path:
 
 PEAK = {"mfma_bf16_tflops": 2500.0, "fp32_tflops": 157.3, "hbm_gbs": 8000.0}
 GEMM_KINDS = ("gemm_fwd", "gemm_wgrad", "gemm_dgrad")
+# sources whose text defines the forward-product kernel; a traffic summary
+# taken on other sources no longer describes it
+GEMM_SOURCES = ("paper_2308_13137_amd/csrc/gemm.hip", "paper_2308_13137_amd/csrc/common.h",
+                "paper_2308_13137_amd/csrc/oq_internal.h")
+COPY_BYTES = 1 << 30          # calibration copy: 1 GiB read, 1 GiB written
+
+
+def gemm_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in GEMM_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_file(workload):
+    return os.path.join(ROOT, "profiles", f"gemm_fwd_{workload}_hbm_traffic.md")
+
+
+def read_traffic(workload):
+    """HBM bytes per forward-product launch from the committed counter summary,
+    or None when there is none or it was taken on other kernel sources."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and line.startswith("- "):
+                k, v = line[2:].split(":", 1)
+                vals[k.strip()] = v.strip().strip("`")
+    if vals.get("gemm source hash") != gemm_source_hash():
+        return None
+    try:
+        return float(vals["HBM bytes per launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def summarize_traffic(fetch_dir, write_dir, workload, cmd_fetch, cmd_write):
+    """Counter passes (FETCH_SIZE, WRITE_SIZE, KiB per dispatch) -> summary:
+    the forward-product dispatches averaged, each counter scaled by what it
+    reads for the calibration copy of COPY_BYTES."""
+    import glob
+    import sqlite3
+
+    def per_kernel(d, counter):
+        out = {}
+        for db in glob.glob(os.path.join(d, "**", "*.db"), recursive=True):
+            con = sqlite3.connect(db)
+            for name, cn, v in con.execute(
+                    "select kernel_name, counter_name, value from counters_collection"):
+                if cn == counter:
+                    out.setdefault(name, []).append(v)
+        return out
+
+    def pick(d, pred):
+        return [v for n, vs in d.items() if pred(n) for v in vs]
+
+    fwd = lambda n: "gemm_bf16_w8_kernel" in n and "EpiResid" in n
+    copy = lambda n: "neg" in n
+    f = per_kernel(fetch_dir, "FETCH_SIZE")
+    w = per_kernel(write_dir, "WRITE_SIZE")
+    ff, ww, fc, wc = pick(f, fwd), pick(w, fwd), pick(f, copy), pick(w, copy)
+    if not (ff and ww and fc and wc):
+        raise SystemExit("counter databases lack the forward-product or copy dispatches")
+    k_fetch = COPY_BYTES / 1024 / (sum(fc) / len(fc))
+    k_write = COPY_BYTES / 1024 / (sum(wc) / len(wc))
+    fetch_kib = sum(ff) / len(ff)
+    write_kib = sum(ww) / len(ww)
+    total = (fetch_kib * k_fetch + write_kib * k_write) * 1024
+    lines = [
+        f"# HBM traffic of the forward product ({workload}), rocprofv3 counters",
+        "",
+        f"FETCH_SIZE pass: `{cmd_fetch}`",
+        "",
+        f"WRITE_SIZE pass: `{cmd_write}`",
+        "",
+        "Each counter is scaled by what it reads for a plain copy kernel of "
+        f"{COPY_BYTES >> 20} MiB read and {COPY_BYTES >> 20} MiB written (`--copy-calibration`).",
+        "",
+        f"- forward dispatches: {len(ff)}",
+        f"- FETCH_SIZE KiB per dispatch: {fetch_kib:.1f}",
+        f"- WRITE_SIZE KiB per dispatch: {write_kib:.1f}",
+        f"- copy FETCH_SIZE KiB: {sum(fc) / len(fc):.1f} (factor {k_fetch:.4f})",
+        f"- copy WRITE_SIZE KiB: {sum(wc) / len(wc):.1f} (factor {k_write:.4f})",
+        f"- HBM bytes per launch: {total:.6e}",
+        f"- gemm source hash: `{gemm_source_hash()}`",
+    ]
+    with open(traffic_file(workload), "w") as fo:
+        fo.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def log(*a):
@@ -110,7 +203,16 @@ def main():
     ap.add_argument("--tokens", type=int, default=None, help="tokens per step (default: the workload's)")
     ap.add_argument("--cpu-tokens", type=int, default=16384)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed steps, run a plain copy of known size (counter scale)")
+    ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CMD_FETCH",
+                                                             "CMD_WRITE"),
+                    help="write the HBM traffic summary from two rocprofv3 --pmc passes")
     args = ap.parse_args()
+    if args.summarize_traffic:
+        w = args.config if not args.tokens else f"{args.config}_t{args.tokens}"
+        summarize_traffic(*args.summarize_traffic[:2], w, *args.summarize_traffic[2:])
+        return
 
     if args.gpus != 1:
         print(f"bench.py measures the calibration step on one GPU; --gpus {args.gpus} is not "
@@ -178,6 +280,10 @@ def main():
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     roof["avg_launch_ms"] = round(kms / n, 4)
     roof["traffic"] = None
+    if dom == "gemm_fwd":
+        tb = read_traffic(args.config if not args.tokens else f"{args.config}_t{args.tokens}")
+        if tb is not None:
+            roof["traffic"] = tb          # HBM bytes per launch (counter passes, copy-scaled)
 
     line = {
         "metric": "calibration tokens/s per block fwd+bwd step",
@@ -200,6 +306,13 @@ def main():
         "roofline": roof,
         "kernels": kernels,
     }
+    if args.copy_calibration:
+        src = torch.ones(COPY_BYTES // 4, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         del X, W, Y, blk
         torch.cuda.empty_cache()
