@@ -203,6 +203,8 @@ def main():
     ap.add_argument("--tokens", type=int, default=None, help="tokens per step (default: the workload's)")
     ap.add_argument("--cpu-tokens", type=int, default=16384)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--step-times", action="store_true",
+                    help="also report each timed step's duration (events between steps)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, run a plain copy of known size (counter scale)")
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CMD_FETCH",
@@ -244,9 +246,15 @@ def main():
     oq.profile_reset()
     oq.profile_enable(True)
     torch.cuda.synchronize()
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)] \
+        if args.step_times else None
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for i in range(args.steps):
+        if marks:
+            marks[i].record()
         blk.step(X, Y, W, gl, bl, s=s, delta=d, update=True)
+    if marks:
+        marks[-1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     oq.profile_enable(False)
@@ -306,6 +314,8 @@ def main():
         "roofline": roof,
         "kernels": kernels,
     }
+    if marks:
+        line["step_ms"] = [round(marks[i].elapsed_time(marks[i + 1]), 3) for i in range(args.steps)]
     if args.copy_calibration:
         src = torch.ones(COPY_BYTES // 4, device="cuda")
         dst = torch.empty_like(src)

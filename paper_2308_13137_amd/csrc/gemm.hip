@@ -3,12 +3,13 @@
 // bf16 path, K % 64 == 0 (gemm_bf16_w8_kernel): 256x256 output tile per
 // workgroup of eight wave64s (two per SIMD), each owning a 128x64 sub-tile as
 // 8 x 4 fragments of v_mfma_f32_16x16x32_bf16.  K advances 64 at a time
-// through two LDS stages (A and B tiles of 256 rows x 64 bf16 = 32 KiB each)
-// filled by global_load_lds_dwordx4 straight from global memory.  Fragments
-// are double-buffered in registers per 32-wide k-half, and the fragment reads
-// and stage copies are placed by hand between groups of four MFMAs.  Each LDS
-// row is eight 16-byte chunks at slot chunk ^ (row & 7) ^ ((row >> 4) & 1),
-// so the lanes of one 128-bit LDS access hit distinct banks.  Workgroups are
+// through LDS stages (A and B tiles of 256 x 64 bf16 = 32 KiB each; three
+// for B and two for A, 160 KiB) filled by global_load_lds_dwordx4 straight
+// from global memory.  Fragments are double-buffered in registers per
+// 32-wide k-half, and the fragment reads and stage copies are placed by hand
+// between groups of four MFMAs: B's copies in one k-half, A's in the other.
+// LDS tiles are XOR-swizzled so the lanes of one LDS read hit distinct
+// banks; operands can be K-contiguous or M/N-contiguous.  Workgroups are
 // renumbered so that the tiles resident on one XCD (the hardware deals
 // workgroups to the 8 XCDs round-robin) form a contiguous block of the
 // output, grouped 8 tiles down M, sharing A and B panels in that XCD's L2.
@@ -421,12 +422,12 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_bf16_kernel(
 }
 
 // ------------------------------------------------------------------ bf16 8-wave kernel
-// K % 64 == 0.  Same 256x256x64 tile and LDS stages as above, but eight waves
-// (two per SIMD) each own a 128x64 block (2 x 4 waves): while one wave of a
-// SIMD waits the other issues matrix instructions.
-// LDS slot of chunk c of row r: c ^ (r & 7) ^ ((r >> 4) & 1).  A 128-bit LDS
-// read serves lanes 0-7 together with 16-23 (and so on); the row-bit-4 term
-// keeps rows r and r + 16 apart as well.
+// K % 64 == 0.  The same 256x256x64 tile as above, but eight waves (two per
+// SIMD) each own a 128x64 block (2 x 4 waves): while one wave of a SIMD waits
+// the other issues matrix instructions.
+// K-major LDS slot of chunk c of row r: c ^ (r & 7) ^ ((r >> 4) & 1).  A
+// 128-bit LDS read serves lanes 0-7 together with 16-23 (and so on); the
+// row-bit-4 term keeps rows r and r + 16 apart as well.
 constexpr int NTHR8 = 512;
 constexpr int EPI8_PITCH = 68;
 
@@ -493,28 +494,6 @@ OQ_DEV bf16x8_t frag(lds_cchar* tile, int q, int kk, int lane) {
   }
 }
 
-// Fragment reads of one k-half: A blocks q = 8 wm + i, B blocks q = 4 wn + j
-// of the stage at st (A tile, then B tile 32 KiB further).
-template <bool AMN, bool BMN>
-OQ_DEV void read_frags(lds_cchar* st, int kk, int wm, int wn, int lane, bf16x8_t (&af)[8],
-                       bf16x8_t (&bq)[4]) {
-#pragma unroll
-  for (int i = 0; i < 8; ++i) af[i] = frag<AMN>(st, 8 * wm + i, kk, lane);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) bq[j] = frag<BMN>(st + 32768, 4 * wn + j, kk, lane);
-}
-
-// One LDS stage: Ab / Bb point at the operands' tile origins at the stage's
-// first k, lds_stage is the stage's LDS byte address.
-OQ_DEV void stage_dma(const uint16_t* Ab, const uint16_t* Bb, const uint32_t (&aoff)[4],
-                      const uint32_t (&boff)[4], uint32_t lds_stage, int wave) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    dma16_s(Ab, aoff[i], lds_stage + (8 * i + wave) * 1024);
-    dma16_s(Bb, boff[i], lds_stage + 32768 + (8 * i + wave) * 1024);
-  }
-}
-
 OQ_DEV void mfma_half(f32x4_t (&acc)[8][4], const bf16x8_t (&af)[8], const bf16x8_t (&bq)[4]) {
 #pragma unroll
   for (int i = 0; i < 8; ++i)
@@ -523,32 +502,109 @@ OQ_DEV void mfma_half(f32x4_t (&acc)[8][4], const bf16x8_t (&af)[8], const bf16x
       acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bq[j], acc[i][j], 0, 0, 0);
 }
 
-// One k-half of MFMAs (8 groups of 4, i-major) with the next fragment set's
-// 12 reads (B first, then A, in the order the next half consumes them) from
-// the stage rd and, when DMA, one stage copy per group into the stage at LDS
-// byte address wr, each placed by hand between MFMA groups; sched_barrier
-// keeps the scheduler from bunching them again.
-template <bool AMN, bool BMN, bool READS, bool DMA>
-OQ_DEV void half_sched(f32x4_t (&acc)[8][4], const bf16x8_t (&au)[8], const bf16x8_t (&bu)[4],
-                       lds_cchar* rd, int kk, int wm, int wn, int lane, bf16x8_t (&ad)[8],
-                       bf16x8_t (&bd)[4], const uint16_t* Ab, const uint16_t* Bb,
-                       const uint32_t (&aoff)[4], const uint32_t (&boff)[4], uint32_t wr,
-                       int wave) {
+// Epilogue of the 8-wave kernels: each wave's 128x64 block goes through LDS
+// (scratch, 8 x 32 x EPI8_PITCH floats) in four passes of 32 rows; a lane
+// then takes 8 consecutive columns of one row (8 lanes per row).  Row
+// partials: 8 lanes per row, then the four column waves in a fixed order.
+template <int P, class Epi>
+OQ_DEV void epi8_pass(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, int64_t M, int wm,
+                      int wn, int lane, int64_t nb, int cnt, float* reg, float2 (*rowbuf)[BM]) {
+  constexpr int PITCH = EPI8_PITCH;
+  const int fr = lane & 15, fk = lane >> 4;
+  const int cl = lane & 7, rl = lane >> 3;
 #pragma unroll
-  for (int g = 0; g < 8; ++g) {
-    if constexpr (READS) {
-      // reads of group g: B0..B3 in groups 0,0,1,1 then A0..A7 in 2,2,3,3,4,5,6,7
+  for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-      for (int r = 0; r < 12; ++r) {
-        const int grp = r < 4 ? r / 2 : (r < 8 ? 2 + (r - 4) / 2 : r - 4);
-        if (grp != g) continue;
-        if (r < 4) bd[r] = frag<BMN>(rd + 32768, 4 * wn + r, kk, lane);
-        else ad[r - 4] = frag<AMN>(rd, 8 * wm + r - 4, kk, lane);
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        reg[(16 * ii + 4 * fk + r) * PITCH + 16 * j + fr] = acc[2 * P + ii][j][r];
+  for (int it = 0; it < 4; ++it) {
+    const int rloc = rl + 8 * it;
+    const int trow = wm * 128 + 32 * P + rloc;
+    const int64_t m = m0 + trow;
+    float v[8];
+    const float4 a_ = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl);
+    const float4 b_ = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl + 4);
+    v[0] = a_.x; v[1] = a_.y; v[2] = a_.z; v[3] = a_.w;
+    v[4] = b_.x; v[5] = b_.y; v[6] = b_.z; v[7] = b_.w;
+    float2 c = make_float2(0.f, 0.f);
+    if (m < M && cnt > 0) c = epi.apply8(epi.row(m), nb, v, cnt);
+    if constexpr (Epi::kRows) {
+      c.x = group_sum<8>(c.x);
+      c.y = group_sum<8>(c.y);
+      if (cl == 0) rowbuf[wn][trow] = c;
+    }
+  }
+}
+
+template <class Epi>
+OQ_DEV void epilogue8(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, int64_t n0,
+                      int64_t M, int64_t N, int tn, int wave, int lane, float* scratch,
+                      float2 (*rowbuf)[BM]) {
+  const int wm = wave >> 2, wn = wave & 3;
+  float* reg = scratch + wave * (32 * EPI8_PITCH);
+  const int64_t nb = n0 + wn * 64 + 8 * (lane & 7);
+  const int cnt = int(max<int64_t>(0, min<int64_t>(8, N - nb)));
+  epi8_pass<0>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf);
+  epi8_pass<1>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf);
+  epi8_pass<2>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf);
+  epi8_pass<3>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf);
+  if constexpr (Epi::kRows) {
+    __syncthreads();
+    const int tid = threadIdx.x;
+    if (tid < BM) {
+      const int64_t m = m0 + tid;
+      if (m < M) {
+        float2 s = rowbuf[0][tid];
+#pragma unroll
+        for (int w = 1; w < 4; ++w) {
+          s.x += rowbuf[w][tid].x;
+          s.y += rowbuf[w][tid].y;
+        }
+        epi.finish(m, tn, s.x, s.y);
       }
     }
+  }
+}
+
+// Stages: B's tile of stage s in one of three buffers (s % 3), A's in one of
+// two (s % 2), 160 KiB in all.  Iteration kt runs k-half 1 of stage kt, then
+// (after the middle barrier) k-half 0 of stage kt + 1.  B's buffer for stage
+// kt + 2 held stage kt - 1 and is free during the whole iteration, so its
+// copies go into the first k-half; A's held stage kt and is free after the
+// middle barrier, so its copies go into the second.  Each half then carries
+// 32 KiB of copies rather than one half carrying 64 (the per-CU copy path
+// moves about 64 bytes a clock), and B's copies have one and a half
+// iterations to land.
+template <bool AMN, bool BMN>
+OQ_DEV void read_frags(lds_cchar* at, lds_cchar* bt, int kk, int wm, int wn, int lane,
+                       bf16x8_t (&af)[8], bf16x8_t (&bq)[4]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) af[i] = frag<AMN>(at, 8 * wm + i, kk, lane);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) bq[j] = frag<BMN>(bt, 4 * wn + j, kk, lane);
+}
+
+// One k-half: 8 groups of four MFMAs; the next fragment set's 12 reads in
+// groups 0..5 (B first), and when DMA one copy of an operand tile (base Xb,
+// offsets xoff, LDS tile at wr) in each even group.
+template <bool AMN, bool BMN, bool DMA>
+OQ_DEV void half_sched(f32x4_t (&acc)[8][4], const bf16x8_t (&au)[8], const bf16x8_t (&bu)[4],
+                       lds_cchar* ra, lds_cchar* rb, int kk, int wm, int wn, int lane,
+                       bf16x8_t (&ad)[8], bf16x8_t (&bd)[4], const uint16_t* Xb,
+                       const uint32_t (&xoff)[4], uint32_t wr, int wave) {
+#pragma unroll
+  for (int g = 0; g < 8; ++g) {
+    if (g < 2) {
+      bd[2 * g] = frag<BMN>(rb, 4 * wn + 2 * g, kk, lane);
+      bd[2 * g + 1] = frag<BMN>(rb, 4 * wn + 2 * g + 1, kk, lane);
+    } else if (g < 6) {
+      ad[2 * g - 4] = frag<AMN>(ra, 8 * wm + 2 * g - 4, kk, lane);
+      ad[2 * g - 3] = frag<AMN>(ra, 8 * wm + 2 * g - 3, kk, lane);
+    }
     if constexpr (DMA) {
-      if (g & 1) dma16_s(Bb, boff[g >> 1], wr + 32768 + (8 * (g >> 1) + wave) * 1024);
-      else       dma16_s(Ab, aoff[g >> 1], wr + (8 * (g >> 1) + wave) * 1024);
+      if ((g & 1) == 0) dma16_s(Xb, xoff[g >> 1], wr + (8 * (g >> 1) + wave) * 1024);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -557,19 +613,14 @@ OQ_DEV void half_sched(f32x4_t (&acc)[8][4], const bf16x8_t (&au)[8], const bf16
   }
 }
 
-// 256x256 output tile, eight wave64s (two per SIMD) in a 2 x 4 grid, each
-// owning a 128x64 sub-tile as 8 x 4 fragments of v_mfma_f32_16x16x32_bf16.
-// K advances 64 per stage through two LDS stages filled by
-// global_load_lds_dwordx4.  The fragments of a stage's two k-halves live in
-// two register sets: the second half is read while the first half's MFMAs
-// run, and the next stage's first half is read (after the barrier that
-// publishes it) while the second half's MFMAs run.
+OQ_DEV void wait_vm4() { asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); }
+
 template <class Epi, bool AMN, bool BMN>
 __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, int64_t M, int64_t N,
     int64_t K, int64_t lda, int64_t ldb, int tiles_m, int tiles_n, Epi epi) {
-  __shared__ uint4 lds[2][2][BM * BK / 8];
-  __shared__ float2 rowbuf[4][BM];
+  // B stages at 0, 32 and 64 KiB, A stages at 96 and 128 KiB
+  __shared__ uint4 lds[5 * 32768 / 16];
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -585,16 +636,19 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int nk = int(K / BK);
 
-  // DMA plans: 32-bit byte offsets from each operand's tile origin (the
-  // launcher keeps 2 * 256 * ld (K-major) and 2 * 64 * ld (MN-major) below 2^32)
   const uint16_t* At = AMN ? A + m0 : A + m0 * lda;
   const uint16_t* Bt = BMN ? B + n0 : B + n0 * ldb;
   const int64_t astep = AMN ? BK * lda : BK, bstep = BMN ? BK * ldb : BK;
   uint32_t aoff[4], boff[4];
   dma_plan<AMN>(aoff, m0, M, lda, wave, lane);
   dma_plan<BMN>(boff, n0, N, ldb, wave, lane);
-  const uint32_t lds0 = lds_addr_of(&lds[0][0][0]);
+  const uint32_t lds0 = lds_addr_of(&lds[0]);
+  lds_cchar* lbase = (lds_cchar*)(&lds[0]);
   const int wm = wave >> 2, wn = wave & 3;
+  auto b_lds = [&](int s) { return lds0 + uint32_t(s % 3) * 32768u; };
+  auto a_lds = [&](int s) { return lds0 + 98304u + uint32_t(s & 1) * 32768u; };
+  auto b_tile = [&](int s) { return lbase + (s % 3) * 32768; };
+  auto a_tile = [&](int s) { return lbase + 98304 + (s & 1) * 32768; };
 
   f32x4_t acc[8][4];
 #pragma unroll
@@ -604,93 +658,47 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
 #pragma unroll
       for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.f;
 
-  stage_dma(At, Bt, aoff, boff, lds0, wave);
+  // stage 0 (A then B), then stage 1 in flight
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dma16_s(At, aoff[i], a_lds(0) + (8 * i + wave) * 1024);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dma16_s(Bt, boff[i], b_lds(0) + (8 * i + wave) * 1024);
   wait_vm0();
   __syncthreads();
-
-  lds_cchar* lbase = (lds_cchar*)(&lds[0][0][0]);
   bf16x8_t a0[8], b0[4], a1[8], b1[4];
-  read_frags<AMN, BMN>(lbase, 0, wm, wn, lane, a0, b0);
-  if (nk > 1) stage_dma(At + astep, Bt + bstep, aoff, boff, lds0 + 65536, wave);
+  read_frags<AMN, BMN>(a_tile(0), b_tile(0), 0, wm, wn, lane, a0, b0);
+  if (nk > 1) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16_s(At + astep, aoff[i], a_lds(1) + (8 * i + wave) * 1024);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16_s(Bt + bstep, boff[i], b_lds(1) + (8 * i + wave) * 1024);
+  }
 
-  // Stage kt sits in buffer kt & 1.  A buffer's last fragment reads complete
-  // before the barrier in the middle of the iteration that uses it, so the
-  // copy of stage kt + 2 into it starts right after that barrier and has a
-  // whole iteration to land.
+  // iteration kt: the first half copies B of stage kt + 2 (its buffer held
+  // stage kt - 1), the second half A of stage kt + 2 (its buffer held stage
+  // kt, whose last reads end at the middle barrier); the middle barrier
+  // waits for stage kt + 1 with B of stage kt + 2 still in flight.
   int kt = 0;
   for (; kt + 2 < nk; ++kt) {
-    const int cur = kt & 1, nxt = cur ^ 1;
-    half_sched<AMN, BMN, true, false>(acc, a0, b0, lbase + cur * 65536, 1, wm, wn, lane, a1, b1,
-                                      At, Bt, aoff, boff, 0, wave);
-    wait_vm0();
+    half_sched<AMN, BMN, true>(acc, a0, b0, a_tile(kt), b_tile(kt), 1, wm, wn, lane, a1, b1,
+                               Bt + (kt + 2) * bstep, boff, b_lds(kt + 2), wave);
+    wait_vm4();
     __syncthreads();
-    half_sched<AMN, BMN, true, true>(acc, a1, b1, lbase + nxt * 65536, 0, wm, wn, lane, a0, b0,
-                                     At + (kt + 2) * astep, Bt + (kt + 2) * bstep, aoff, boff,
-                                     lds0 + cur * 65536, wave);
+    half_sched<AMN, BMN, true>(acc, a1, b1, a_tile(kt + 1), b_tile(kt + 1), 0, wm, wn, lane, a0,
+                               b0, At + (kt + 2) * astep, aoff, a_lds(kt + 2), wave);
   }
   for (; kt < nk; ++kt) {
-    const int cur = kt & 1, nxt = cur ^ 1;
-    read_frags<AMN, BMN>(lbase + cur * 65536, 1, wm, wn, lane, a1, b1);
+    read_frags<AMN, BMN>(a_tile(kt), b_tile(kt), 1, wm, wn, lane, a1, b1);
     mfma_half(acc, a0, b0);
     if (kt + 1 < nk) wait_vm0();
     __syncthreads();
-    if (kt + 1 < nk) read_frags<AMN, BMN>(lbase + nxt * 65536, 0, wm, wn, lane, a0, b0);
+    if (kt + 1 < nk) read_frags<AMN, BMN>(a_tile(kt + 1), b_tile(kt + 1), 0, wm, wn, lane, a0, b0);
     mfma_half(acc, a1, b1);
   }
   __syncthreads();
-
-  // epilogue: each wave's 128x64 block through LDS in four passes of 32 rows;
-  // a lane then takes 8 consecutive columns of one row (8 lanes per row).
-  constexpr int PITCH = EPI8_PITCH;
-  float* reg = reinterpret_cast<float*>(&lds[0][0][0]) + wave * (32 * PITCH);
-  const int cl = lane & 7, rl = lane >> 3;
-  const int64_t nb = n0 + wn * 64 + 8 * cl;
-  const int cnt = int(max<int64_t>(0, min<int64_t>(8, N - nb)));
-#define OQ_EPI8_PASS(P)                                                                        \
-  do {                                                                                         \
-    const int fr = lane & 15, fk = lane >> 4;                                                  \
-    _Pragma("unroll") for (int ii = 0; ii < 2; ++ii)                                           \
-      _Pragma("unroll") for (int j = 0; j < 4; ++j)                                            \
-        _Pragma("unroll") for (int r = 0; r < 4; ++r)                                          \
-          reg[(16 * ii + 4 * fk + r) * PITCH + 16 * j + fr] = acc[2 * (P) + ii][j][r];         \
-    for (int it = 0; it < 4; ++it) {                                                           \
-      const int rloc = rl + 8 * it;                                                            \
-      const int trow = wm * 128 + 32 * (P) + rloc;                                             \
-      const int64_t m = m0 + trow;                                                             \
-      float v[8];                                                                              \
-      const float4 a_ = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl);         \
-      const float4 b_ = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl + 4);     \
-      v[0] = a_.x; v[1] = a_.y; v[2] = a_.z; v[3] = a_.w;                                     \
-      v[4] = b_.x; v[5] = b_.y; v[6] = b_.z; v[7] = b_.w;                                     \
-      float2 c = make_float2(0.f, 0.f);                                                        \
-      if (m < M && cnt > 0) c = epi.apply8(epi.row(m), nb, v, cnt);                            \
-      if constexpr (Epi::kRows) {                                                              \
-        c.x = group_sum<8>(c.x);                                                               \
-        c.y = group_sum<8>(c.y);                                                               \
-        if (cl == 0) rowbuf[wn][trow] = c;                                                     \
-      }                                                                                        \
-    }                                                                                          \
-  } while (0)
-  OQ_EPI8_PASS(0);
-  OQ_EPI8_PASS(1);
-  OQ_EPI8_PASS(2);
-  OQ_EPI8_PASS(3);
-#undef OQ_EPI8_PASS
-  if constexpr (Epi::kRows) {
-    __syncthreads();
-    if (tid < BM) {
-      const int64_t m = m0 + tid;
-      if (m < M) {
-        float2 s = rowbuf[0][tid];
-#pragma unroll
-        for (int w = 1; w < 4; ++w) {
-          s.x += rowbuf[w][tid].x;
-          s.y += rowbuf[w][tid].y;
-        }
-        epi.finish(m, tn, s.x, s.y);
-      }
-    }
-  }
+  // epilogue staging (68 KiB) and row partials (8 KiB at 96 KiB) reuse the stages
+  epilogue8(acc, epi, m0, n0, M, N, tn, wave, lane, reinterpret_cast<float*>(&lds[0]),
+            reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304));
 }
 
 // ------------------------------------------------------------------ fp32 kernel
