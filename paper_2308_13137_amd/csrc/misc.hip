@@ -116,15 +116,28 @@ __global__ __launch_bounds__(256) void colstat_kernel(const TX* __restrict__ X, 
 }
 
 // Column sums of [rows, C] partial arrays: a block of 16 waves covers 64
-// columns (lane = column); wave w adds rows w, w + 16, ... in fp64, and the 16
-// wave sums are combined through LDS in wave order (fixed, deterministic).
+// columns (lane = column); wave w adds rows w, w + 16, ... in fp64 into four
+// accumulators (four loads in flight; row w + 16 k goes to accumulator
+// k % 4), and the 16 wave sums are combined through LDS in wave order.  Every
+// order is fixed, so the result is deterministic.
 constexpr int CS_WAVES = 16;
 
 OQ_DEV double strip_sum(const float* parts, int64_t rows, int64_t C, int64_t c, int w) {
-  double acc = 0.0;
-  if (parts && c < C)
-    for (int64_t i = w; i < rows; i += CS_WAVES) acc += double(parts[i * C + c]);
-  return acc;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  if (parts && c < C) {
+    int64_t i = w;
+    for (; i + 3 * CS_WAVES < rows; i += 4 * CS_WAVES) {
+      float v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = parts[(i + u * CS_WAVES) * C + c];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] += double(v[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < 3; ++u)
+      if (i + u * CS_WAVES < rows) acc[u] += double(parts[(i + u * CS_WAVES) * C + c]);
+  }
+  return (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
 template <int NA>
