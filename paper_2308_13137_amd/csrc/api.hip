@@ -730,24 +730,24 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
   if (opt) {
     const AdamCoef cl = adam_coef(opt->lr_lwc, opt->beta1, opt->beta2, opt->eps, opt->wd, opt->step);
     const AdamCoef ce = adam_coef(opt->lr_let, opt->beta1, opt->beta2, opt->eps, opt->wd, opt->step);
+    // every parameter tensor of the block in one launch (set 0: LWC, set 1: LET)
     ProfScope ps(PK_OTHER, st, 0);
+    AdamList L{};
+    auto add = [&](float* pp, const float* g, float* m, float* v, int64_t n, int set) {
+      L.p[L.n] = pp; L.g[L.n] = g; L.m[L.n] = m; L.v[L.n] = v; L.len[L.n] = n; L.set[L.n] = set;
+      ++L.n;
+    };
     for (int l = 0; l < d->n_linears; ++l) {
       const int64_t n = d->lin_c_out[l] * (d->site_width[d->lin_site[l]] / d->lin_group[l]);
-      OQ_HIP(adamw(prm->gamma_logit[l], gr->d_gamma_logit[l], opt->m_gamma[l], opt->v_gamma[l], n,
-                   cl, st),
-             "adamw gamma");
-      OQ_HIP(adamw(prm->beta_logit[l], gr->d_beta_logit[l], opt->m_beta[l], opt->v_beta[l], n, cl,
-                   st),
-             "adamw beta");
+      add(prm->gamma_logit[l], gr->d_gamma_logit[l], opt->m_gamma[l], opt->v_gamma[l], n, 0);
+      add(prm->beta_logit[l], gr->d_beta_logit[l], opt->m_beta[l], opt->v_beta[l], n, 0);
     }
     for (const auto& p : plan) {
       if (!p.let) continue;
-      OQ_HIP(adamw(prm->s[p.k], gr->d_s[p.k], opt->m_s[p.k], opt->v_s[p.k], p.C, ce, st),
-             "adamw s");
-      OQ_HIP(adamw(prm->delta[p.k], gr->d_delta[p.k], opt->m_delta[p.k], opt->v_delta[p.k], p.C,
-                   ce, st),
-             "adamw delta");
+      add(prm->s[p.k], gr->d_s[p.k], opt->m_s[p.k], opt->v_s[p.k], p.C, 1);
+      add(prm->delta[p.k], gr->d_delta[p.k], opt->m_delta[p.k], opt->v_delta[p.k], p.C, 1);
     }
+    OQ_HIP(adamw_multi(L, cl, ce, st), "adamw");
   }
   return OQ_OK;
 }

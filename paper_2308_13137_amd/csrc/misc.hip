@@ -223,23 +223,47 @@ __global__ __launch_bounds__(256) void row_partials_kernel(const float* __restri
   }
 }
 
-__global__ __launch_bounds__(256) void loss_finish_kernel(const double* rl, LossArgs la,
-                                                          float* loss) {
-  __shared__ double sh[4];
+// One block of 16 waves; thread t adds rows t, t + 1024, ... of each linear
+// into four accumulators (row t + 1024 k goes to accumulator k % 4), then
+// the wave and the 16 waves combine in a fixed order.
+__global__ __launch_bounds__(1024) void loss_finish_kernel(const double* rl, LossArgs la,
+                                                           float* loss) {
+  __shared__ double sh[16];
   const int tid = threadIdx.x;
   double total = 0.0;
   for (int l = 0; l < la.nlin; ++l) {
-    double a = 0.0;
-    for (int64_t m = la.row_begin[l] + tid; m < la.row_end[l]; m += 256) {
-      a += rl[m];
-      if (la.row_loss[l]) la.row_loss[l][m - la.row_begin[l]] = float(rl[m]);
+    const int64_t b = la.row_begin[l], e = la.row_end[l];
+    float* out = la.row_loss[l];
+    double a[4] = {0.0, 0.0, 0.0, 0.0};
+    int64_t m = b + tid;
+    for (; m + 3 * 1024 < e; m += 4 * 1024) {
+      double v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = rl[m + u * 1024];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        a[u] += v[u];
+        if (out) out[m + u * 1024 - b] = float(v[u]);
+      }
     }
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) a += __shfl_xor(a, off);
+    for (int u = 0; u < 3; ++u) {
+      const int64_t mu = m + u * 1024;
+      if (mu < e) {
+        a[u] += rl[mu];
+        if (out) out[mu - b] = float(rl[mu]);
+      }
+    }
+    double s = (a[0] + a[1]) + (a[2] + a[3]);
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) s += __shfl_xor(s, off);
     __syncthreads();
-    if ((tid & 63) == 0) sh[tid >> 6] = a;
+    if ((tid & 63) == 0) sh[tid >> 6] = s;
     __syncthreads();
-    total += ((sh[0] + sh[1]) + (sh[2] + sh[3])) * la.inv_n[l];
+    double r = 0.0;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) r += sh[w];
+    total += r * la.inv_n[l];
   }
   if (tid == 0) *loss = float(total);
 }
@@ -250,6 +274,28 @@ __global__ __launch_bounds__(256) void adamw_kernel(float* p, const float* g, fl
   const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
   if (i >= n) return;
   const float gi = g[i];
+  const float mi = c.b1 * m[i] + c.omb1 * gi;
+  const float vi = c.b2 * v[i] + c.omb2 * (gi * gi);
+  m[i] = mi;
+  v[i] = vi;
+  const float mh = mi / c.bc1;
+  const float vh = vi / c.bc2;
+  p[i] = p[i] * c.decay - c.lr * (mh / (__fsqrt_rn(vh) + c.eps));
+}
+
+// Several tensors in one launch: block b belongs to the tensor whose block
+// range holds it (at most ADAM_MAX tensors, two coefficient sets).
+__global__ __launch_bounds__(256) void adamw_multi_kernel(AdamList L, AdamCoef c0, AdamCoef c1) {
+  int k = 0;
+#pragma unroll 1
+  while (k + 1 < L.n && int(blockIdx.x) >= L.block_begin[k + 1]) ++k;
+  const AdamCoef& c = L.set[k] ? c1 : c0;
+  const int64_t i = int64_t(blockIdx.x - L.block_begin[k]) * 256 + threadIdx.x;
+  if (i >= L.len[k]) return;
+  float* p = L.p[k];
+  float* m = L.m[k];
+  float* v = L.v[k];
+  const float gi = L.g[k][i];
   const float mi = c.b1 * m[i] + c.omb1 * gi;
   const float vi = c.b2 * v[i] + c.omb2 * (gi * gi);
   m[i] = mi;
@@ -365,7 +411,7 @@ hipError_t row_partials(const float* psq, const float* pdy, int64_t M, int ntn, 
 }
 
 hipError_t loss_finish(const double* rl, LossArgs la, float* loss, hipStream_t st) {
-  hipLaunchKernelGGL(loss_finish_kernel, dim3(1), dim3(256), 0, st, rl, la, loss);
+  hipLaunchKernelGGL(loss_finish_kernel, dim3(1), dim3(1024), 0, st, rl, la, loss);
   return hipGetLastError();
 }
 
@@ -381,6 +427,21 @@ AdamCoef adam_coef(double lr, double b1, double b2, double eps, double wd, int s
   c.bc1 = float(1.0 - std::pow(b1, double(step)));
   c.bc2 = float(1.0 - std::pow(b2, double(step)));
   return c;
+}
+
+hipError_t adamw_multi(const AdamList& L, AdamCoef c0, AdamCoef c1, hipStream_t st) {
+  if (L.n <= 0) return hipSuccess;
+  AdamList l = L;
+  int blocks = 0;
+  for (int k = 0; k < l.n; ++k) {
+    l.block_begin[k] = blocks;
+    const int64_t nb = (l.len[k] + 255) / 256;
+    if (blocks + nb > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
+    blocks += int(nb);
+  }
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(adamw_multi_kernel, dim3(unsigned(blocks)), dim3(256), 0, st, l, c0, c1);
+  return hipGetLastError();
 }
 
 hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, AdamCoef c,

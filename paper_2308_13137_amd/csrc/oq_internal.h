@@ -120,6 +120,20 @@ struct AdamCoef {
   float lr, b1, omb1, b2, omb2, eps, decay, bc1, bc2;
 };
 AdamCoef adam_coef(double lr, double b1, double b2, double eps, double wd, int step);
+// Up to ADAM_MAX tensors updated by one launch; set[k] picks coefficient set
+// 0 or 1; block_begin is filled in by adamw_multi.
+constexpr int ADAM_MAX = 48;
+struct AdamList {
+  int n;
+  float* p[ADAM_MAX];
+  const float* g[ADAM_MAX];
+  float* m[ADAM_MAX];
+  float* v[ADAM_MAX];
+  int64_t len[ADAM_MAX];
+  int set[ADAM_MAX];
+  int block_begin[ADAM_MAX];
+};
+hipError_t adamw_multi(const AdamList& L, AdamCoef c0, AdamCoef c1, hipStream_t st);
 hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, AdamCoef c,
                  hipStream_t st);
 // LET initialisation pieces
