@@ -328,15 +328,17 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
   }
 }
 
-// ------------------------------------------------------------------ LWC, lane-owned runs
+// ------------------------------------------------------------------ LWC backward, lane-owned runs
 // Groups of at most 512 weights without LET scaling: each lane owns a run of
 // E consecutive weights of one row (E / 8 independent 16-byte loads in
-// flight), takes the run's max / min (and, for the backward, the first index
-// holding each), and combines with the other group / E lanes of its group
-// (adjacent, aligned lanes) by butterflies.  The group parameters are
-// then computed once per E weights instead of once per 8, and the kernel has
-// no divergent branches.  A tail lane past the last run repeats the last run
-// without storing, so every butterfly sees whole groups.
+// flight, with the run's gradient), takes the run's max / min (and the first
+// index holding each where dW~ is wanted), and combines with the other
+// group / E lanes of its group (adjacent, aligned lanes) by butterflies.  The
+// group parameters are then computed once per E weights instead of once per
+// 8, and the kernel has no divergent branches.  A tail lane past the last run
+// repeats the last run without storing, so every butterfly sees whole groups.
+// (The same layout for the forward, with E = 128, left each 16-byte access of
+// a wave 256 bytes from the next; the forward below walks coalesced chunks.)
 
 // Register image of a run of E elements as 16-byte vectors.
 template <typename TW, int E>
@@ -389,46 +391,110 @@ OQ_DEV void dyn_group_range(float& mx, float& mn, int L) {
   }
 }
 
-template <typename TW, typename TQ, int E, bool CODES>
-__global__ __launch_bounds__(NT) void lwc_fwd_run_kernel(
-    const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ gl,
-    const float* __restrict__ bl, int bits, int group, TQ* __restrict__ wdq,
-    uint8_t* __restrict__ codes, float* __restrict__ hout, float* __restrict__ zout) {
-  const uint32_t runs = uint32_t(c_in / E), nrun = uint32_t(c_out) * runs;  // < 2^31 (host)
-  uint32_t t = blockIdx.x * NT + threadIdx.x;
-  const bool valid = t < nrun;
-  if (!valid) t = nrun - 1;
-  const uint32_t rq = t / runs;
-  const int64_t row = rq;
-  const int col0 = int(t - rq * runs) * E;
-  const float qmax = float((1 << bits) - 1);
-
-  Run<TW, E> x;
-  x.load(W + row * c_in + col0);
-  float mx, mn;
-  run_range(x, mx, mn);
-  if (group > E) dyn_group_range(mx, mn, group / E);
-  const int64_t gi = row * (c_in / group) + col0 / group;
-  const QParams p = make_qparams(mx, mn, clip_strength(gl[gi]), clip_strength(bl[gi]), qmax);
-  if (!valid) return;
-  // rint(u) and z are integers below 2^24, so clamp(rint(u) + z, 0, qmax) - z
-  // is exactly med3(rint(u), -z, qmax - z): one instruction for Eq. 2's clamp
-  const float lo = -p.z, hi = qmax - p.z;
+// ------------------------------------------------------------------ LWC forward, coalesced
+// Power-of-two groups of at most 512 weights without LET scaling.  The matrix
+// is walked as a flat sequence of 8-weight chunks (groups never straddle a
+// row); lane l of a wave takes chunk 64 u + l of each of its U slices, so
+// every load and store of a wave is 1 KiB of contiguous memory.  A group is
+// G = group / 8 adjacent lanes: their max / min combine by butterflies.  The
+// group parameters (sigmoids in fp64, Eq. 2's h, 1/h, z) are computed once
+// per group by an owner lane: the U * 64 / G groups of a wave step are owned
+// by lanes 0, 1, ... in order, which fetch their group's range and hand back
+// h, 1/h, z through cross-lane reads.  Lanes past the last chunk repeat it
+// without storing (whole groups, since a row holds whole groups).
+template <typename TW>
+OQ_DEV void load_chunk(const TW* p, float (&x)[8]) {
+  if constexpr (sizeof(TW) == 2) {
+    const uint4 q = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-  for (int c = 0; c < E / 8; ++c) {
-    float q[8], d[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float tq = __builtin_amdgcn_fmed3f(rintf(x.at(8 * c + e) * p.r), lo, hi);
-      d[e] = tq * p.h;
-      if constexpr (CODES) q[e] = tq + p.z;
-    }
-    if (wdq) store8(wdq + row * c_in + col0 + 8 * c, d);
-    if constexpr (CODES) store8_codes(codes + row * c_in + col0 + 8 * c, q);
+    for (int e = 0; e < 8; ++e)
+      x[e] = __uint_as_float((e & 1) ? (w[e >> 1] & 0xffff0000u) : (w[e >> 1] << 16));
+  } else {
+    const float4 a = reinterpret_cast<const float4*>(p)[0];
+    const float4 b = reinterpret_cast<const float4*>(p)[1];
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
   }
-  if (col0 % group == 0) {
-    if (hout) hout[gi] = p.h;
-    if (zout) zout[gi] = p.z;
+}
+
+template <typename TW, typename TQ, int G, bool CODES>
+__global__ __launch_bounds__(NT) void lwc_fwd_coal_kernel(
+    const TW* __restrict__ W, int64_t nchunk, const float* __restrict__ gl,
+    const float* __restrict__ bl, int bits, TQ* __restrict__ wdq, uint8_t* __restrict__ codes,
+    float* __restrict__ hout, float* __restrict__ zout) {
+  constexpr int U = G < 8 ? G : 8;           // slices per lane: the owners fit in a wave
+  constexpr int NGW = 64 / G;                // groups per slice
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t(blockIdx.x) * NT + threadIdx.x) >> 6;
+  const int64_t nwave = (int64_t(gridDim.x) * NT) >> 6;
+  const int64_t nstep = (nchunk + 64 * U - 1) / (64 * U);
+  const int64_t ngroup = nchunk / G;
+  const float qmax = float((1 << bits) - 1);
+  for (int64_t step = wave; step < nstep; step += nwave) {
+    const int64_t c0 = step * (64 * U) + lane;
+    float x[U][8], mx[U], mn[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) load_chunk(W + 8 * min(c0 + 64 * u, nchunk - 1), x[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      mx[u] = x[u][0];
+      mn[u] = x[u][0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) {
+        mx[u] = fmaxf(mx[u], x[u][e]);
+        mn[u] = fminf(mn[u], x[u][e]);
+      }
+#pragma unroll
+      for (int off = 1; off < G; off <<= 1) {
+        mx[u] = fmaxf(mx[u], __shfl_xor(mx[u], off));
+        mn[u] = fminf(mn[u], __shfl_xor(mn[u], off));
+      }
+    }
+    // owner lane o holds group step * U * NGW + o: slice o / NGW, lanes
+    // (o % NGW) * G .. + G - 1 of it
+    float gmx = 0.f, gmn = 0.f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float a = __shfl(mx[u], (lane % NGW) * G);
+      const float b = __shfl(mn[u], (lane % NGW) * G);
+      if (lane / NGW == u) {
+        gmx = a;
+        gmn = b;
+      }
+    }
+    const int64_t g = min(step * (U * NGW) + lane, ngroup - 1);
+    float h = 1.f, r = 1.f, z = 0.f;
+    if (lane < U * NGW) {
+      const QParams p = make_qparams(gmx, gmn, clip_strength(gl[g]), clip_strength(bl[g]), qmax);
+      h = p.h;
+      r = p.r;
+      z = p.z;
+      if (step * (U * NGW) + lane < ngroup) {
+        if (hout) hout[g] = p.h;
+        if (zout) zout[g] = p.z;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int own = u * NGW + lane / G;
+      const float hu = __shfl(h, own), ru = __shfl(r, own), zu = __shfl(z, own);
+      const int64_t c = c0 + 64 * u;
+      // rint(u) and z are integers below 2^24, so clamp(rint(u) + z, 0, qmax) - z
+      // is exactly med3(rint(u), -z, qmax - z): one instruction for Eq. 2's clamp
+      const float lo = -zu, hi = qmax - zu;
+      float d[8], q[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float tq = __builtin_amdgcn_fmed3f(rintf(x[u][e] * ru), lo, hi);
+        d[e] = tq * hu;
+        if constexpr (CODES) q[e] = tq + zu;
+      }
+      if (c < nchunk) {
+        if (wdq) store8(wdq + 8 * c, d);
+        if constexpr (CODES) store8_codes(codes + 8 * c, q);
+      }
+    }
   }
 }
 
@@ -869,34 +935,36 @@ hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
                    bool dq_bf16, uint8_t* codes, float* h, float* z, hipStream_t st) {
   if (!quant_shape_supported(c_in, group)) return hipErrorInvalidValue;
   if (c_out <= 0) return hipSuccess;
-  if (small_group(group) && !s && c_out * c_in < (int64_t(1) << 34)) {
-    const int E = int(std::min<int64_t>(group, 128));
-    const int64_t nrun = c_out * (c_in / E);
-    const dim3 grid(unsigned((nrun + NT - 1) / NT));
-    auto run = [&](auto tw, auto tq, auto ec) {
+  if (small_group(group) && !s) {
+    const int64_t nchunk = c_out * c_in / 8;
+    const int64_t waves = std::min<int64_t>((nchunk + 511) / 512, 256 * 32);
+    const dim3 grid(unsigned((waves * 64 + NT - 1) / NT));
+    auto go = [&](auto tw, auto tq, auto gc) {
       using TW = decltype(tw);
       using TQ = decltype(tq);
-      constexpr int Ec = decltype(ec)::value;
+      constexpr int Gc = decltype(gc)::value;
       if (codes)
-        hipLaunchKernelGGL((lwc_fwd_run_kernel<TW, TQ, Ec, true>), grid, dim3(NT), 0, st,
-                           static_cast<const TW*>(W), c_out, c_in, gl, bl, bits, int(group),
-                           static_cast<TQ*>(W_dq), codes, h, z);
+        hipLaunchKernelGGL((lwc_fwd_coal_kernel<TW, TQ, Gc, true>), grid, dim3(NT), 0, st,
+                           static_cast<const TW*>(W), nchunk, gl, bl, bits, static_cast<TQ*>(W_dq),
+                           codes, h, z);
       else
-        hipLaunchKernelGGL((lwc_fwd_run_kernel<TW, TQ, Ec, false>), grid, dim3(NT), 0, st,
-                           static_cast<const TW*>(W), c_out, c_in, gl, bl, bits, int(group),
-                           static_cast<TQ*>(W_dq), codes, h, z);
+        hipLaunchKernelGGL((lwc_fwd_coal_kernel<TW, TQ, Gc, false>), grid, dim3(NT), 0, st,
+                           static_cast<const TW*>(W), nchunk, gl, bl, bits, static_cast<TQ*>(W_dq),
+                           codes, h, z);
     };
-    auto by_e = [&](auto tw, auto tq) {
-      switch (E) {
-        case 8: run(tw, tq, std::integral_constant<int, 8>{}); break;
-        case 16: run(tw, tq, std::integral_constant<int, 16>{}); break;
-        case 32: run(tw, tq, std::integral_constant<int, 32>{}); break;
-        case 64: run(tw, tq, std::integral_constant<int, 64>{}); break;
-        default: run(tw, tq, std::integral_constant<int, 128>{}); break;
+    auto by_g = [&](auto tw, auto tq) {
+      switch (group / 8) {
+        case 1: go(tw, tq, std::integral_constant<int, 1>{}); break;
+        case 2: go(tw, tq, std::integral_constant<int, 2>{}); break;
+        case 4: go(tw, tq, std::integral_constant<int, 4>{}); break;
+        case 8: go(tw, tq, std::integral_constant<int, 8>{}); break;
+        case 16: go(tw, tq, std::integral_constant<int, 16>{}); break;
+        case 32: go(tw, tq, std::integral_constant<int, 32>{}); break;
+        default: go(tw, tq, std::integral_constant<int, 64>{}); break;
       }
     };
-    if (w_bf16) dq_bf16 ? by_e(uint16_t{}, uint16_t{}) : by_e(uint16_t{}, float{});
-    else dq_bf16 ? by_e(float{}, uint16_t{}) : by_e(float{}, float{});
+    if (w_bf16) dq_bf16 ? by_g(uint16_t{}, uint16_t{}) : by_g(uint16_t{}, float{});
+    else dq_bf16 ? by_g(float{}, uint16_t{}) : by_g(float{}, float{});
     return hipGetLastError();
   }
   const int R = rows_per_block(c_out, LWC_BLOCKS);

@@ -108,6 +108,11 @@ LWC_CASES = [
     dict(c_out=16, c_in=2048, group=512, bits=3, bf16=True),
     dict(c_out=12, c_in=4096, group=128, bits=4, bf16=True, let=True),
     dict(c_out=20, c_in=11008, group=11008, bits=4, bf16=True, let=True),
+    # the smallest and the remaining power-of-two groups, with a chunk count
+    # that leaves a partial wave step (13 x 17, 7 x 26, 9 x 96 chunks of 8)
+    dict(c_out=13, c_in=136, group=8, bits=2, bf16=True),
+    dict(c_out=7, c_in=208, group=16, bits=5, bf16=True),
+    dict(c_out=9, c_in=768, group=256, bits=6, bf16=False),
 ]
 
 
