@@ -471,6 +471,14 @@ bool direct_grads(const oq_block_desc* d, const SitePlan& p) {
   return ok;
 }
 
+// K-split count of the weight gradient (its K is the token count); only the
+// direct path splits.
+int wgrad_splits(const oq_block_desc* d, const SitePlan& p) {
+  if (!direct_grads(d, p)) return 1;
+  const int64_t T = d->tokens;
+  return gemm_mn_splits(false, true, p.M, p.C, T, T, p.C);
+}
+
 size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, char* base,
                    BlockWs* w) {
   const bool bf = d->dtype == OQ_BF16;
@@ -486,7 +494,7 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
     what = std::max(what, size_t(p.M * p.C));
     if (!direct) xhatT = std::max(xhatT, size_t(T * p.C));
     dyT = std::max(dyT, size_t(p.M * T));
-    dW = std::max(dW, size_t(p.M * p.C));
+    dW = std::max(dW, size_t(p.M * p.C) * size_t(wgrad_splits(d, p)));
     parts = std::max(parts, size_t(p.M * ntn));
     rows = std::max(rows, size_t(p.M));
     mtot += p.M;
@@ -665,12 +673,17 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
       OQ_HIP(row_partials(w.psq, p.let ? w.pdy : nullptr, M, ntn, w.rl + row_base, w.dbt, st),
              "row partials");
     }
-    // 6. weight gradient dW^ = dY^T X^  [M, C]
+    // 6. weight gradient dW^ = dY^T X^  [M, C]; over a K (token) split of S
+    //    parts when that fills the last wave of tiles better, the parts
+    //    summed in a fixed order
     {
       ProfScope ps(PK_GEMM_WGRAD, st, 2.0 * double(M) * T * C);
-      if (direct)
-        OQ_HIP(gemm_f32out_mn(w.dyT, false, xsrc, true, M, C, T, T, C, w.dW, C, st), "wgrad gemm");
-      else
+      if (direct) {
+        const int S = wgrad_splits(d, p);
+        OQ_HIP(gemm_f32out_mn(w.dyT, false, xsrc, true, M, C, T, T, C, w.dW, C, st, S, M * C),
+               "wgrad gemm");
+        if (S > 1) OQ_HIP(sum_partials(w.dW, M * C, S, M * C, st), "wgrad split sum");
+      } else
         OQ_HIP(gemm_nt_f32out(w.dyT, w.xhatT, bf, M, C, T, T, T, w.dW, C, st), "wgrad gemm");
     }
     // 7. LWC backward per linear (+ weight-path LET scale partials)

@@ -44,7 +44,9 @@ struct EpiF32 {
   float* C;
   int64_t ldc;
   bool vec;
+  int64_t split_stride;              // elements between the K-split partial outputs
   static constexpr bool kRows = false;
+  OQ_DEV void split(int s) { C += s * split_stride; }
   struct Row { float* c; };
   OQ_DEV Row row(int64_t m) const { return Row{C + m * ldc}; }
   OQ_DEV float2 apply8(const Row& r, int64_t n, const float* v, int cnt) const {
@@ -67,6 +69,7 @@ struct EpiStore {
   const float* bias;
   bool vec;
   static constexpr bool kRows = false;
+  OQ_DEV void split(int) {}
   struct Row { TC* c; float b; };
   OQ_DEV Row row(int64_t m) const { return Row{C + m * ldc, bias ? bias[m] : 0.0f}; }
   OQ_DEV float2 apply8(const Row& r, int64_t n, const float* v, int cnt) const {
@@ -91,6 +94,7 @@ struct EpiResid {
   ResidArgs a;
   bool vec;
   static constexpr bool kRows = true;
+  OQ_DEV void split(int) {}
   struct Row { const T* yfp; T* dy; float scale; float b; };
   OQ_DEV Row row(int64_t m) const {
     // constant indices only, so the argument block stays in scalar registers
@@ -619,6 +623,8 @@ template <class Epi, bool AMN, bool BMN>
 __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B, int64_t M, int64_t N,
     int64_t K, int64_t lda, int64_t ldb, int tiles_m, int tiles_n, Epi epi) {
+  // With a K split (grid = tiles x splits) each workgroup runs K of the
+  // whole and writes its own partial output (Epi::split).
   // B stages at 0, 32 and 64 KiB, A stages at 96 and 128 KiB
   __shared__ uint4 lds[5 * 32768 / 16];
 
@@ -626,7 +632,9 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
   const int wave = tid >> 6, lane = tid & 63;
   const int nblk = gridDim.x, bid = blockIdx.x;
   const int xcd = bid & 7, local = bid >> 3, q = nblk >> 3, rem = nblk & 7;
-  const int L = xcd * q + min(xcd, rem) + local;
+  const int Lall = xcd * q + min(xcd, rem) + local;
+  const int ks = Lall / (tiles_m * tiles_n);
+  const int L = Lall - ks * (tiles_m * tiles_n);
   const int group_sz = GROUP_M * tiles_n;
   const int g = L / group_sz;
   const int first_m = g * GROUP_M;
@@ -635,6 +643,11 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
   const int tm = first_m + li % gm, tn = li / gm;
   const int64_t m0 = int64_t(tm) * BM, n0 = int64_t(tn) * BN;
   const int nk = int(K / BK);
+  if (ks) {
+    A += AMN ? ks * K * lda : ks * K;
+    B += BMN ? ks * K * ldb : ks * K;
+    epi.split(ks);
+  }
 
   const uint16_t* At = AMN ? A + m0 : A + m0 * lda;
   const uint16_t* Bt = BMN ? B + n0 : B + n0 * ldb;
@@ -773,8 +786,9 @@ bool w8_ok(bool amn, bool bmn, int64_t M, int64_t N, int64_t K, int64_t lda, int
 
 template <class Epi, bool AMN, bool BMN>
 void launch_w8(const void* A, const void* B, int64_t M, int64_t N, int64_t K, int64_t lda,
-               int64_t ldb, int64_t tm, int64_t tn, Epi epi, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_bf16_w8_kernel<Epi, AMN, BMN>), dim3(unsigned(tm * tn)), dim3(NTHR8), 0,
+               int64_t ldb, int64_t tm, int64_t tn, Epi epi, hipStream_t st, int splits = 1) {
+  hipLaunchKernelGGL((gemm_bf16_w8_kernel<Epi, AMN, BMN>), dim3(unsigned(tm * tn * splits)),
+                     dim3(NTHR8), 0,
                      st, static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N, K,
                      lda, ldb, int(tm), int(tn), epi);
 }
@@ -784,21 +798,26 @@ void launch_w8(const void* A, const void* B, int64_t M, int64_t N, int64_t K, in
 template <class Epi>
 hipError_t launch(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
                   int64_t lda, int64_t ldb, Epi epi, hipStream_t st, bool amn = false,
-                  bool bmn = false) {
+                  bool bmn = false, int splits = 1) {
   if (M <= 0 || N <= 0) return hipSuccess;
   if (bf16) {
     const int64_t tm = (M + BM - 1) / BM, tn = (N + BN - 1) / BN;
-    if (tm * tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
+    if (tm * tn * splits > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
     if (w8_ok(amn, bmn, M, N, K, lda, ldb)) {
       if (!amn && !bmn) {
-        launch_w8<Epi, false, false>(A, B, M, N, K, lda, ldb, tm, tn, epi, st);
+        launch_w8<Epi, false, false>(A, B, M, N, K, lda, ldb, tm, tn, epi, st, splits);
       } else if constexpr (std::is_same<Epi, EpiF32>::value) {
-        if (amn && bmn) launch_w8<Epi, true, true>(A, B, M, N, K, lda, ldb, tm, tn, epi, st);
-        else if (bmn) launch_w8<Epi, false, true>(A, B, M, N, K, lda, ldb, tm, tn, epi, st);
-        else launch_w8<Epi, true, false>(A, B, M, N, K, lda, ldb, tm, tn, epi, st);
+        if (amn && bmn)
+          launch_w8<Epi, true, true>(A, B, M, N, K, lda, ldb, tm, tn, epi, st, splits);
+        else if (bmn)
+          launch_w8<Epi, false, true>(A, B, M, N, K, lda, ldb, tm, tn, epi, st, splits);
+        else
+          launch_w8<Epi, true, false>(A, B, M, N, K, lda, ldb, tm, tn, epi, st, splits);
       } else {
         return hipErrorInvalidValue;
       }
+    } else if (splits != 1) {
+      return hipErrorInvalidValue;
     } else if (!amn && !bmn) {
       hipLaunchKernelGGL((gemm_bf16_kernel<Epi, false>), dim3(unsigned(tm * tn)), dim3(NTHR), 0,
                          st, static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(B), M, N,
@@ -807,7 +826,7 @@ hipError_t launch(const void* A, const void* B, bool bf16, int64_t M, int64_t N,
       return hipErrorInvalidValue;
     }
   } else {
-    if (amn || bmn) return hipErrorInvalidValue;
+    if (amn || bmn || splits != 1) return hipErrorInvalidValue;
     const int64_t tm = (M + F32_TILE - 1) / F32_TILE, tn = (N + F32_TILE - 1) / F32_TILE;
     if (tm > 65535 || tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
     hipLaunchKernelGGL(gemm_f32_kernel<Epi>, dim3(unsigned(tn), unsigned(tm)), dim3(256), 0, st,
@@ -833,11 +852,42 @@ bool gemm_mn_supported(bool a_mn, bool b_mn, int64_t M, int64_t N, int64_t K, in
   return w8_ok(a_mn, b_mn, M, N, K, lda, ldb);
 }
 
+int gemm_mn_splits(bool a_mn, bool b_mn, int64_t M, int64_t N, int64_t K, int64_t lda,
+                   int64_t ldb) {
+  // Time in k-steps of one tile (a 256 x 256 x 64 MFMA step, ~1.65 us on a
+  // loaded CU): whole waves of units, each K/(64 S) steps plus an fp32
+  // epilogue worth ~16 steps, then the partial sum's (S + 1) M N 4 bytes at
+  // ~5 TB/s.
+  constexpr int kCUs = 256;
+  constexpr double kStep = 1.65e-6, kEpi = 16.0, kBw = 5.0e12;
+  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  int best = 1;
+  double best_t = 0.0;
+  for (int s = 1; s <= 8; s *= 2) {
+    if (K % (int64_t(BK) * s)) break;
+    const int64_t ks = K / s;
+    if (s > 1 && (ks < 16 * BK || !w8_ok(a_mn, b_mn, M, N, ks, lda, ldb))) break;
+    const int64_t waves = (tiles * s + kCUs - 1) / kCUs;
+    double t_s = double(waves) * (double(ks / BK) + kEpi) * kStep;
+    if (s > 1) t_s += double(s + 1) * double(M) * double(N) * 4.0 / kBw;
+    if (s == 1 || t_s < 0.99 * best_t) {
+      best = s;
+      best_t = t_s;
+    }
+  }
+  return best;
+}
+
 hipError_t gemm_f32out_mn(const void* A, bool a_mn, const void* B, bool b_mn, int64_t M,
                           int64_t N, int64_t K, int64_t lda, int64_t ldb, float* C, int64_t ldc,
-                          hipStream_t st) {
-  const bool vec = ldc % 8 == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
-  return launch(A, B, true, M, N, K, lda, ldb, EpiF32{C, ldc, vec}, st, a_mn, b_mn);
+                          hipStream_t st, int splits, int64_t split_stride) {
+  if (splits < 1 || K % splits) return hipErrorInvalidValue;
+  const int64_t ks = K / splits;
+  if (splits > 1 && !w8_ok(a_mn, b_mn, M, N, ks, lda, ldb)) return hipErrorInvalidValue;
+  const bool vec = ldc % 8 == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0 &&
+                   split_stride % 8 == 0;
+  return launch(A, B, true, M, N, ks, lda, ldb, EpiF32{C, ldc, vec, split_stride}, st, a_mn,
+                b_mn, splits);
 }
 
 hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int64_t N,

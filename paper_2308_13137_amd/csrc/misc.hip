@@ -305,6 +305,37 @@ __global__ __launch_bounds__(256) void adamw_multi_kernel(AdamList L, AdamCoef c
   p[i] = p[i] * c.decay - c.lr * (mh / (__fsqrt_rn(vh) + c.eps));
 }
 
+// ------------------------------------------------------------------ K-split partial sums
+// c[i] = ((c[i] + c[i + stride]) + c[i + 2 stride]) + ...  (fixed order), in
+// place over the first partial; grid stride, four elements per thread when
+// the layout allows.
+__global__ __launch_bounds__(256) void sum_partials4_kernel(float* c, int64_t n4, int parts,
+                                                            int64_t stride4) {
+  float4* c4 = reinterpret_cast<float4*>(c);
+  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n4;
+       i += int64_t(gridDim.x) * 256) {
+    float4 a = c4[i];
+    for (int s = 1; s < parts; ++s) {
+      const float4 b = c4[i + s * stride4];
+      a.x += b.x;
+      a.y += b.y;
+      a.z += b.z;
+      a.w += b.w;
+    }
+    c4[i] = a;
+  }
+}
+
+__global__ __launch_bounds__(256) void sum_partials1_kernel(float* c, int64_t n, int parts,
+                                                            int64_t stride) {
+  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n;
+       i += int64_t(gridDim.x) * 256) {
+    float a = c[i];
+    for (int s = 1; s < parts; ++s) a += c[i + s * stride];
+    c[i] = a;
+  }
+}
+
 }  // namespace
 
 hipError_t transpose(const void* in, int64_t rows, int64_t cols, int64_t ld_in, void* out,
@@ -441,6 +472,20 @@ hipError_t adamw_multi(const AdamList& L, AdamCoef c0, AdamCoef c1, hipStream_t 
   }
   if (blocks == 0) return hipSuccess;
   hipLaunchKernelGGL(adamw_multi_kernel, dim3(unsigned(blocks)), dim3(256), 0, st, l, c0, c1);
+  return hipGetLastError();
+}
+
+hipError_t sum_partials(float* c, int64_t n, int parts, int64_t stride, hipStream_t st) {
+  if (n <= 0 || parts <= 1) return hipSuccess;
+  if (stride < n) return hipErrorInvalidValue;
+  const bool v4 = n % 4 == 0 && stride % 4 == 0 && (reinterpret_cast<uintptr_t>(c) & 15) == 0;
+  const int64_t work = v4 ? n / 4 : n;
+  const unsigned grid = unsigned(std::min<int64_t>((work + 255) / 256, 8192));
+  if (v4)
+    hipLaunchKernelGGL(sum_partials4_kernel, dim3(grid), dim3(256), 0, st, c, n / 4, parts,
+                       stride / 4);
+  else
+    hipLaunchKernelGGL(sum_partials1_kernel, dim3(grid), dim3(256), 0, st, c, n, parts, stride);
   return hipGetLastError();
 }
 

@@ -51,12 +51,20 @@ hipError_t gemm_nt_f32out(const void* A, const void* B, bool bf16, int64_t M, in
 // bf16 C[M,N] = op(A) op(B)^T into fp32 with either operand stored MN-major
 // (a_mn: A as [K, M] with row stride lda; b_mn: B as [K, N] with row stride
 // ldb), read straight from that layout.  gemm_mn_supported tells whether the
-// shapes qualify (K a multiple of 64 and aligned strides).
+// shapes qualify (K a multiple of 64 and aligned strides).  With splits > 1
+// the K range is cut into that many equal parts (each a multiple of 64) and
+// part s writes its own partial product at C + s * split_stride; the caller
+// sums the parts (sum_partials).
 bool gemm_mn_supported(bool a_mn, bool b_mn, int64_t M, int64_t N, int64_t K, int64_t lda,
                        int64_t ldb);
+// K-split count (1, 2, 4 or 8) for gemm_f32out_mn on an M x N output: the one
+// whose whole waves of 256 x 256 tiles over 256 compute units, plus the
+// partial-sum pass, take the least modelled time.
+int gemm_mn_splits(bool a_mn, bool b_mn, int64_t M, int64_t N, int64_t K, int64_t lda,
+                   int64_t ldb);
 hipError_t gemm_f32out_mn(const void* A, bool a_mn, const void* B, bool b_mn, int64_t M,
                           int64_t N, int64_t K, int64_t lda, int64_t ldb, float* C, int64_t ldc,
-                          hipStream_t st);
+                          hipStream_t st, int splits = 1, int64_t split_stride = 0);
 hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
                          int64_t lda, int64_t ldb, void* C, bool c_bf16, int64_t ldc,
                          const float* bias, hipStream_t st);
@@ -134,6 +142,9 @@ struct AdamList {
   int block_begin[ADAM_MAX];
 };
 hipError_t adamw_multi(const AdamList& L, AdamCoef c0, AdamCoef c1, hipStream_t st);
+// In place over the first of `parts` fp32 partials spaced `stride` apart:
+// c[i] = ((c[i] + c[i + stride]) + ...) in that order, i < n.
+hipError_t sum_partials(float* c, int64_t n, int parts, int64_t stride, hipStream_t st);
 hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, AdamCoef c,
                  hipStream_t st);
 // LET initialisation pieces

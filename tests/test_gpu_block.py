@@ -35,6 +35,10 @@ WORKLOADS = [
     small_llama("c3_t256", hidden=256, ffn=512, T=256, w_bits=4, let=True, act_bits=4),
     small_llama("c2_t320", hidden=256, ffn=768, T=320, w_bits=3, group=128),
     small_llama("c5_t192", hidden=512, ffn=1024, T=192, w_bits=4, group=128, kv=128, sigma=0.015),
+    # long token runs over few output tiles: the weight gradient splits its
+    # token (K) range into 8 (T=8192) or 4 (T=4096) parts summed afterwards
+    small_llama("c2_t8192", hidden=256, ffn=768, T=8192, w_bits=3, group=128),
+    small_llama("c3_t4096", hidden=256, ffn=512, T=4096, w_bits=4, let=True, act_bits=4),
 ]
 
 
