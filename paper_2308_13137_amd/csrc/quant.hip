@@ -619,13 +619,24 @@ __global__ __launch_bounds__(NT) void act_fwd_row_kernel(
     const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
     const float* __restrict__ delta, TX* __restrict__ xdq, uint8_t* __restrict__ codes,
     float* __restrict__ hout, float* __restrict__ zout) {
-  extern __shared__ float shl[];     // [C] 1/s, then [C] delta (LET only)
+  // LET only: 1/s then delta, as float4 slots [k][half][lane] so that one
+  // 128-bit LDS read per (k, half) covers 1 KiB of consecutive LDS.
+  extern __shared__ float4 shl4[];
+  constexpr int SLOTS = CH * 128;
   const bool let = s || delta;
   const int nch = int(C / 8);
   if (let) {
-    for (int c = threadIdx.x; c < C; c += NT) {
-      shl[c] = s ? div_rn(1.0f, s[c]) : 1.0f;
-      shl[C + c] = delta ? delta[c] : 0.0f;
+    for (int i = threadIdx.x; i < SLOTS; i += NT) {
+      const int64_t c0 = 8 * int64_t((i & 63) + 64 * (i >> 7)) + 4 * ((i >> 6) & 1);
+      float a[4], b[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t c = c0 + q;
+        a[q] = (s && c < C) ? div_rn(1.0f, s[c]) : 1.0f;
+        b[q] = (delta && c < C) ? delta[c] : 0.0f;
+      }
+      shl4[i] = make_float4(a[0], a[1], a[2], a[3]);
+      shl4[SLOTS + i] = make_float4(b[0], b[1], b[2], b[3]);
     }
     __syncthreads();
   }
@@ -642,11 +653,19 @@ __global__ __launch_bounds__(NT) void act_fwd_row_kernel(
       if (j < nch) raw[k].load(xr + 8 * j);
     }
     // x~ = (x - delta) (1/s), one rounding per operation
-    auto xt = [&](int k, int e) {
-      const float x = raw[k].at(e);
-      if (!let) return x;
-      const int c = 8 * (lane + 64 * k) + e;
-      return (x - shl[C + c]) * shl[c];
+    auto xt8 = [&](int k, float (&o)[8]) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = raw[k].at(e);
+      if (!let) return;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float4 r = shl4[(2 * k + h) * 64 + lane];
+        const float4 d = shl4[SLOTS + (2 * k + h) * 64 + lane];
+        o[4 * h + 0] = (o[4 * h + 0] - d.x) * r.x;
+        o[4 * h + 1] = (o[4 * h + 1] - d.y) * r.y;
+        o[4 * h + 2] = (o[4 * h + 2] - d.z) * r.z;
+        o[4 * h + 3] = (o[4 * h + 3] - d.w) * r.w;
+      }
     };
     if (!quant) {
 #pragma unroll
@@ -654,8 +673,7 @@ __global__ __launch_bounds__(NT) void act_fwd_row_kernel(
         const int j = lane + 64 * k;
         if (j >= nch) continue;
         float d[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) d[e] = xt(k, e);
+        xt8(k, d);
         store8(xdq + row * C + 8 * j, d);
       }
       continue;
@@ -664,11 +682,12 @@ __global__ __launch_bounds__(NT) void act_fwd_row_kernel(
 #pragma unroll
     for (int k = 0; k < CH; ++k) {
       if (lane + 64 * k >= nch) continue;
+      float v[8];
+      xt8(k, v);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float v = xt(k, e);
-        mx = fmaxf(mx, v);
-        mn = fminf(mn, v);
+        mx = fmaxf(mx, v[e]);
+        mn = fminf(mn, v[e]);
       }
     }
 #pragma unroll
@@ -678,14 +697,25 @@ __global__ __launch_bounds__(NT) void act_fwd_row_kernel(
     }
     const QParams p = make_qparams(mx, mn, 1.0f, 1.0f, qmax);
     const float lo = -p.z, hi = qmax - p.z;     // clamp as one med3 (exact integers)
+    // x~ is recomputed from the packed row (and LDS) rather than kept as
+    // fp32 from the range pass: the opaque register and memory barrier
+    // stops the compiler from holding every converted value live
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int k = 0; k < CH; ++k)
+#pragma unroll
+      for (int i = 0; i < Chunk8<TX>::NV; ++i)
+        asm volatile("" : "+v"(raw[k].v[i].x), "+v"(raw[k].v[i].y), "+v"(raw[k].v[i].z),
+                     "+v"(raw[k].v[i].w));
 #pragma unroll
     for (int k = 0; k < CH; ++k) {
       const int j = lane + 64 * k;
       if (j >= nch) continue;
-      float q[8], d[8];
+      float v[8], q[8], d[8];
+      xt8(k, v);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float tq = __builtin_amdgcn_fmed3f(rintf(xt(k, e) * p.r), lo, hi);
+        const float tq = __builtin_amdgcn_fmed3f(rintf(v[e] * p.r), lo, hi);
         d[e] = tq * p.h;
         q[e] = tq + p.z;
       }
@@ -781,6 +811,16 @@ __global__ __launch_bounds__(NT) void act_fwd_kernel(
 // ------------------------------------------------------------------ activation backward
 // dx~ per element (straight-through with the row scale's gradient); per column
 // partial sums over this block's rows of dx~ * x~ and of dx~.
+// One barrier per block reduction: the LDS slots of the two reductions
+// alternate, and a wave reads each slot before it arrives at the other
+// reduction's barrier, so no second barrier guards the rewrite.  The barrier
+// waits for LDS only, so the next row's loads stay in flight across it.
+OQ_DEV void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 template <typename TX, int KC>
 __global__ __launch_bounds__(NT) void act_bwd_kernel(
     const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
@@ -789,6 +829,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
   __shared__ MinMax shm[NT / 64];
   __shared__ float2 shs[NT / 64];
   const int tid = threadIdx.x;
+  const int wave = tid >> 6;
   const int cpr = int(C / 8);
   const bool quant = bits < 16;
   const float qmax = quant ? float((1 << bits) - 1) : 0.0f;
@@ -815,15 +856,51 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
   const bool let = s || delta;
   const int64_t r0 = int64_t(blockIdx.x) * R;
   const int64_t r1 = min(T, r0 + R);
-  for (int64_t row = r0; row < r1; ++row) {
-    float v[KC][8], g[KC][8];
-    MinMax st = minmax_init();
+  // up to two chunks per thread, the next row's X and dX^ are loaded while
+  // this row is reduced (wider rows would spill)
+  constexpr bool PF = KC <= 2;
+  Chunk8<TX> xn[KC];
+  float gn[KC][8];
+  auto issue = [&](int64_t row) {
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
       const int j = tid + NT * k;
       if (j < cpr) {
-        load8(X + row * C + 8 * j, v[k]);
-        load8(dXdq + row * C + 8 * j, g[k]);
+        xn[k].load(X + row * C + 8 * j);
+        load8(dXdq + row * C + 8 * j, gn[k]);
+      }
+    }
+  };
+  if constexpr (PF) {
+    if (r0 < r1) issue(r0);
+  }
+  for (int64_t row = r0; row < r1; ++row) {
+    float v[KC][8], g[KC][8];
+    MinMax st = minmax_init();
+    if constexpr (PF) {
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          v[k][e] = xn[k].at(e);
+          g[k][e] = gn[k][e];
+        }
+      }
+      if (row + 1 < r1) issue(row + 1);
+    } else {
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const int j = tid + NT * k;
+        if (j < cpr) {
+          load8(X + row * C + 8 * j, v[k]);
+          load8(dXdq + row * C + 8 * j, g[k]);
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      const int j = tid + NT * k;
+      if (j < cpr) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           if (let) v[k][e] = (v[k][e] - dl[k][e]) * rs[k][e];
@@ -832,7 +909,15 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
       }
     }
     if (quant) {
-      st = block_minmax(st, shm);
+      group_minmax<64>(st.mx, st.imx, st.mn, st.imn);
+      if ((tid & 63) == 0) shm[wave] = st;
+      lds_barrier();
+      st = shm[0];
+#pragma unroll
+      for (int w = 1; w < NT / 64; ++w) {
+        sel_max(st.mx, st.imx, shm[w].mx, shm[w].imx);
+        sel_min(st.mn, st.imn, shm[w].mn, shm[w].imn);
+      }
       const QParams p = make_qparams(st.mx, st.mn, 1.0f, 1.0f, qmax);
       float2 sums = make_float2(0.f, 0.f);
       bool mk[KC][8];
@@ -851,7 +936,16 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
           }
         }
       }
-      sums = block_sum2(sums, shs);
+      sums.x = group_sum<64>(sums.x);
+      sums.y = group_sum<64>(sums.y);
+      if ((tid & 63) == 0) shs[wave] = sums;
+      lds_barrier();
+      sums = shs[0];
+#pragma unroll
+      for (int w = 1; w < NT / 64; ++w) {
+        sums.x += shs[w].x;
+        sums.y += shs[w].y;
+      }
       const QGrad qg = quant_group_grad(sums.x, sums.y, st.mx, st.mn, p, qmax);
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
@@ -1067,7 +1161,7 @@ hipError_t act_fwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, c
   if (x_bf16 == dq_bf16 && per_lane <= 32 && (X_dq || bits < 16)) {
     const int ch = per_lane <= 2 ? 2 : per_lane <= 4 ? 4 : per_lane <= 8 ? 8 : per_lane <= 12 ? 12
                  : per_lane <= 16 ? 16 : per_lane <= 24 ? 24 : 32;
-    const unsigned lds = (s || delta) ? unsigned(2 * C * sizeof(float)) : 0u;
+    const unsigned lds = (s || delta) ? unsigned(ch) * 128u * 2u * 16u : 0u;
     const dim3 grid(unsigned(std::min<int64_t>((T + NT / 64 - 1) / (NT / 64), 2048)));
     auto run = [&](auto tx, auto chc) {
       using TX = decltype(tx);
