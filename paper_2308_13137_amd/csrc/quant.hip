@@ -69,6 +69,37 @@ OQ_DEV float2 block_sum2(float2 v, float2* sh) {
   return r;
 }
 
+// Workgroup barrier that waits for LDS traffic only: global loads issued
+// before it (the next row's prefetch) stay in flight across it.
+OQ_DEV void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Register image of 8 consecutive elements as loaded (bf16 packed or fp32).
+template <typename TX>
+struct Chunk8 {
+  static constexpr int NV = sizeof(TX) == 2 ? 1 : 2;
+  uint4 v[NV];
+  OQ_DEV void load(const TX* p) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] = reinterpret_cast<const uint4*>(p)[i];
+  }
+  OQ_DEV static uint32_t word(const uint4& q, int k) {
+    return k == 0 ? q.x : (k == 1 ? q.y : (k == 2 ? q.z : q.w));
+  }
+  OQ_DEV float at(int e) const {
+    const uint4& q = v[sizeof(TX) == 2 ? 0 : e >> 2];
+    if constexpr (sizeof(TX) == 2) {
+      const uint32_t w = word(q, e >> 1);
+      return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+    } else {
+      return __uint_as_float(word(q, e & 3));
+    }
+  }
+};
+
 // ------------------------------------------------------------------ LWC forward
 template <typename TW, typename TQ, int KC, bool WHOLE_ROW>
 __global__ __launch_bounds__(NT) void lwc_fwd_kernel(
@@ -182,6 +213,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
   __shared__ MinMax shm[NT / 64];
   __shared__ float2 shs[NT / 64];
   const int tid = threadIdx.x;
+  const int wave = tid >> 6;
   const int cpr = int(c_in / 8);
   const int ng = int(c_in / group);
   const int L = group / 8;
@@ -201,18 +233,53 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
 
   const int64_t r0 = int64_t(blockIdx.x) * R;
   const int64_t r1 = min(c_out, r0 + R);
+  // whole rows of up to two chunks per thread: the next row's W and dW^ are
+  // loaded while this row is reduced (wider rows would spill)
+  constexpr bool PF = WHOLE_ROW && KC <= 2;
+  Chunk8<TW> wn[KC];
+  float gn[KC][8];
+  auto issue = [&](int64_t row) {
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      const int j = tid + NT * k;
+      if (j < cpr) {
+        wn[k].load(W + row * c_in + 8 * j);
+        load8(dW + row * c_in + 8 * j, gn[k]);
+      }
+    }
+  };
+  if constexpr (PF) {
+    if (r0 < r1) issue(r0);
+  }
   for (int64_t row = r0; row < r1; ++row) {
     const TW* wrow = W + row * c_in;
     const float* grow = dW + row * c_in;
     if constexpr (WHOLE_ROW) {
       float w[KC][8], wt[KC][8], g[KC][8];
       MinMax st = minmax_init();
+      if constexpr (PF) {
+#pragma unroll
+        for (int k = 0; k < KC; ++k)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            w[k][e] = wn[k].at(e);
+            g[k][e] = gn[k][e];
+          }
+        if (row + 1 < r1) issue(row + 1);
+      } else {
+#pragma unroll
+        for (int k = 0; k < KC; ++k) {
+          const int j = tid + NT * k;
+          if (j < cpr) {
+            load8(wrow + 8 * j, w[k]);
+            load8(grow + 8 * j, g[k]);
+          }
+        }
+      }
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
         const int j = tid + NT * k;
         if (j < cpr) {
-          load8(wrow + 8 * j, w[k]);
-          load8(grow + 8 * j, g[k]);
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             wt[k][e] = s ? w[k][e] * sv[k][e] : w[k][e];
@@ -220,7 +287,15 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
           }
         }
       }
-      st = block_minmax(st, shm);
+      group_minmax<64>(st.mx, st.imx, st.mn, st.imn);
+      if ((tid & 63) == 0) shm[wave] = st;
+      lds_barrier();
+      st = shm[0];
+#pragma unroll
+      for (int w8 = 1; w8 < NT / 64; ++w8) {
+        sel_max(st.mx, st.imx, shm[w8].mx, shm[w8].imx);
+        sel_min(st.mn, st.imn, shm[w8].mn, shm[w8].imn);
+      }
       const QParams p = make_qparams(st.mx, st.mn, clip_strength(gl[row]), clip_strength(bl[row]), qmax);
       float2 sums = make_float2(0.f, 0.f);
       bool mk[KC][8];
@@ -239,7 +314,16 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
           }
         }
       }
-      sums = block_sum2(sums, shs);
+      sums.x = group_sum<64>(sums.x);
+      sums.y = group_sum<64>(sums.y);
+      if ((tid & 63) == 0) shs[wave] = sums;
+      lds_barrier();
+      sums = shs[0];
+#pragma unroll
+      for (int w8 = 1; w8 < NT / 64; ++w8) {
+        sums.x += shs[w8].x;
+        sums.y += shs[w8].y;
+      }
       const QGrad qg = quant_group_grad(sums.x, sums.y, st.mx, st.mn, p, qmax);
       if (tid == 0) {
         dgl[row] = qg.dgamma * p.gamma * (1.0f - p.gamma);
@@ -595,25 +679,6 @@ __global__ __launch_bounds__(NT) void lwc_bwd_run_kernel(
 // at once.  The row's max / min is a wave butterfly (values only: the
 // forward parameters need no index); LET's 1/s and delta are staged in LDS
 // once per workgroup.  Same operation order as the per-block kernel below.
-template <typename TX>
-struct Chunk8 {
-  static constexpr int NV = sizeof(TX) == 2 ? 1 : 2;
-  uint4 v[NV];
-  OQ_DEV void load(const TX* p) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) v[i] = reinterpret_cast<const uint4*>(p)[i];
-  }
-  OQ_DEV float at(int e) const {
-    const uint4& q = v[sizeof(TX) == 2 ? 0 : e >> 2];
-    if constexpr (sizeof(TX) == 2) {
-      const uint32_t w = Run<uint16_t, 8>::word(q, e >> 1);
-      return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
-    } else {
-      return __uint_as_float(Run<float, 8>::word(q, e & 3));
-    }
-  }
-};
-
 template <typename TX, int CH>
 __global__ __launch_bounds__(NT) void act_fwd_row_kernel(
     const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
@@ -729,6 +794,105 @@ __global__ __launch_bounds__(NT) void act_fwd_row_kernel(
   }
 }
 
+// ------------------------------------------------------------------ LWC forward, wave per row
+// Whole-row groups (group = c_in, up to 512 * CH weights): each wave takes
+// whole rows (grid stride), lane l holding chunks l, l + 64, ... as loaded.
+// LET's s is staged in LDS once per workgroup as float4 slots [k][half][lane]
+// (conflict-free 128-bit reads).  Same Eq. 2 arithmetic as lwc_fwd_kernel:
+// the clamp is a median of three on rint(u) (q - z stays an exact integer).
+template <typename TW, typename TQ, int CH, bool CODES>
+__global__ __launch_bounds__(NT) void lwc_fwd_row_kernel(
+    const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ s,
+    const float* __restrict__ gl, const float* __restrict__ bl, int bits, TQ* __restrict__ wdq,
+    uint8_t* __restrict__ codes, float* __restrict__ hout, float* __restrict__ zout) {
+  extern __shared__ float4 shw4[];
+  constexpr int SLOTS = CH * 128;
+  const int nch = int(c_in / 8);
+  if (s) {
+    for (int i = threadIdx.x; i < SLOTS; i += NT) {
+      const int64_t c0 = 8 * int64_t((i & 63) + 64 * (i >> 7)) + 4 * ((i >> 6) & 1);
+      float a[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) a[q] = c0 + q < c_in ? s[c0 + q] : 1.0f;
+      shw4[i] = make_float4(a[0], a[1], a[2], a[3]);
+    }
+    __syncthreads();
+  }
+  const int lane = threadIdx.x & 63;
+  const int64_t nw = int64_t(gridDim.x) * (NT / 64);
+  const float qmax = float((1 << bits) - 1);
+  for (int64_t row = int64_t(blockIdx.x) * (NT / 64) + (threadIdx.x >> 6); row < c_out;
+       row += nw) {
+    const TW* wr = W + row * c_in;
+    Chunk8<TW> raw[CH];
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      const int j = lane + 64 * k;
+      if (j < nch) raw[k].load(wr + 8 * j);
+    }
+    // w~ = w * s, one rounding
+    auto wt8 = [&](int k, float (&o)[8]) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = raw[k].at(e);
+      if (!s) return;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float4 m = shw4[(2 * k + h) * 64 + lane];
+        o[4 * h + 0] *= m.x;
+        o[4 * h + 1] *= m.y;
+        o[4 * h + 2] *= m.z;
+        o[4 * h + 3] *= m.w;
+      }
+    };
+    float mx = -FLT_MAX, mn = FLT_MAX;
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      if (lane + 64 * k >= nch) continue;
+      float v[8];
+      wt8(k, v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        mx = fmaxf(mx, v[e]);
+        mn = fminf(mn, v[e]);
+      }
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      mx = fmaxf(mx, __shfl_xor(mx, off));
+      mn = fminf(mn, __shfl_xor(mn, off));
+    }
+    const QParams p = make_qparams(mx, mn, clip_strength(gl[row]), clip_strength(bl[row]), qmax);
+    const float lo = -p.z, hi = qmax - p.z;
+    // recompute w~ from the packed row rather than hold it in fp32
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int k = 0; k < CH; ++k)
+#pragma unroll
+      for (int i = 0; i < Chunk8<TW>::NV; ++i)
+        asm volatile("" : "+v"(raw[k].v[i].x), "+v"(raw[k].v[i].y), "+v"(raw[k].v[i].z),
+                     "+v"(raw[k].v[i].w));
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      const int j = lane + 64 * k;
+      if (j >= nch) continue;
+      float v[8], d[8], q[8];
+      wt8(k, v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float tq = __builtin_amdgcn_fmed3f(rintf(v[e] * p.r), lo, hi);
+        d[e] = tq * p.h;
+        q[e] = tq + p.z;
+      }
+      if (wdq) store8(wdq + row * c_in + 8 * j, d);
+      if constexpr (CODES) store8_codes(codes + row * c_in + 8 * j, q);
+    }
+    if (lane == 0) {
+      if (hout) hout[row] = p.h;
+      if (zout) zout[row] = p.z;
+    }
+  }
+}
+
 // ------------------------------------------------------------------ activation forward
 // x~ = (x - delta) * (1/s); per token row Eq. 2 with gamma = beta = 1.
 template <typename TX, typename TQ, int KC>
@@ -811,16 +975,9 @@ __global__ __launch_bounds__(NT) void act_fwd_kernel(
 // ------------------------------------------------------------------ activation backward
 // dx~ per element (straight-through with the row scale's gradient); per column
 // partial sums over this block's rows of dx~ * x~ and of dx~.
-// One barrier per block reduction: the LDS slots of the two reductions
-// alternate, and a wave reads each slot before it arrives at the other
-// reduction's barrier, so no second barrier guards the rewrite.  The barrier
-// waits for LDS only, so the next row's loads stay in flight across it.
-OQ_DEV void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
+// One barrier per block reduction (lds_barrier): the LDS slots of the two
+// reductions alternate, and a wave reads each slot before it arrives at the
+// other reduction's barrier, so no second barrier guards the rewrite.
 template <typename TX, int KC>
 __global__ __launch_bounds__(NT) void act_bwd_kernel(
     const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
@@ -999,7 +1156,7 @@ int rows_per_block(int64_t rows, int64_t target_blocks) {
   return int(std::max<int64_t>(1, (rows + target_blocks - 1) / target_blocks));
 }
 
-constexpr int64_t LWC_BLOCKS = 1024;
+constexpr int64_t LWC_BLOCKS = 768;
 constexpr int64_t ACT_BLOCKS = 2048;
 
 #define OQ_KC_SWITCH(KCV, ...)                      \
@@ -1059,6 +1216,40 @@ hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
     };
     if (w_bf16) dq_bf16 ? by_g(uint16_t{}, uint16_t{}) : by_g(uint16_t{}, float{});
     else dq_bf16 ? by_g(float{}, uint16_t{}) : by_g(float{}, float{});
+    return hipGetLastError();
+  }
+  const int64_t per_lane = (c_in / 8 + 63) / 64;
+  if (group == c_in && per_lane <= 32) {
+    const int ch = per_lane <= 2 ? 2 : per_lane <= 4 ? 4 : per_lane <= 8 ? 8 : per_lane <= 12 ? 12
+                 : per_lane <= 16 ? 16 : per_lane <= 24 ? 24 : 32;
+    const unsigned lds = s ? unsigned(ch) * 128u * 16u : 0u;
+    const dim3 grid(unsigned(std::min<int64_t>((c_out + NT / 64 - 1) / (NT / 64), 2048)));
+    auto run = [&](auto tw, auto tq, auto chc) {
+      using TW = decltype(tw);
+      using TQ = decltype(tq);
+      constexpr int CHc = decltype(chc)::value;
+      if (codes)
+        hipLaunchKernelGGL((lwc_fwd_row_kernel<TW, TQ, CHc, true>), grid, dim3(NT), lds, st,
+                           static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits,
+                           static_cast<TQ*>(W_dq), codes, h, z);
+      else
+        hipLaunchKernelGGL((lwc_fwd_row_kernel<TW, TQ, CHc, false>), grid, dim3(NT), lds, st,
+                           static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits,
+                           static_cast<TQ*>(W_dq), codes, h, z);
+    };
+    auto by_ch = [&](auto tw, auto tq) {
+      switch (ch) {
+        case 2: run(tw, tq, std::integral_constant<int, 2>{}); break;
+        case 4: run(tw, tq, std::integral_constant<int, 4>{}); break;
+        case 8: run(tw, tq, std::integral_constant<int, 8>{}); break;
+        case 12: run(tw, tq, std::integral_constant<int, 12>{}); break;
+        case 16: run(tw, tq, std::integral_constant<int, 16>{}); break;
+        case 24: run(tw, tq, std::integral_constant<int, 24>{}); break;
+        default: run(tw, tq, std::integral_constant<int, 32>{}); break;
+      }
+    };
+    if (w_bf16) dq_bf16 ? by_ch(uint16_t{}, uint16_t{}) : by_ch(uint16_t{}, float{});
+    else dq_bf16 ? by_ch(float{}, uint16_t{}) : by_ch(float{}, float{});
     return hipGetLastError();
   }
   const int R = rows_per_block(c_out, LWC_BLOCKS);

@@ -113,6 +113,10 @@ LWC_CASES = [
     dict(c_out=13, c_in=136, group=8, bits=2, bf16=True),
     dict(c_out=7, c_in=208, group=16, bits=5, bf16=True),
     dict(c_out=9, c_in=768, group=256, bits=6, bf16=False),
+    # whole-row groups on the wave-per-row kernels: fp32 rows with s, and
+    # two-chunk rows over more rows than one workgroup's waves
+    dict(c_out=33, c_in=2048, group=2048, bits=5, bf16=False, let=True),
+    dict(c_out=70, c_in=136, group=136, bits=3, bf16=True),
 ]
 
 
