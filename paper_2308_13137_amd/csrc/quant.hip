@@ -77,6 +77,62 @@ OQ_DEV void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Whole-wave reductions on the VALU: DPP exchanges within each 16-lane row
+// (quad xor 1, quad xor 2, half-row mirror, row mirror), then the four row
+// results read out (lanes 0, 16, 32, 48) and combined in that order.  Every
+// lane returns the same value; the order is fixed, so sums are reproducible.
+OQ_DEV float dpp_f(float v, int ctrl) {
+  switch (ctrl) {
+    case 0: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+    case 1: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+    case 2: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+    default: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
+  }
+}
+OQ_DEV int dpp_i(int v, int ctrl) {
+  switch (ctrl) {
+    case 0: return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+    case 1: return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+    case 2: return __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+    default: return __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
+  }
+}
+OQ_DEV float rl_f(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
+
+OQ_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v += dpp_f(v, c);
+  return ((rl_f(v, 0) + rl_f(v, 16)) + rl_f(v, 32)) + rl_f(v, 48);
+}
+OQ_DEV float wave_max(float v) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v = fmaxf(v, dpp_f(v, c));
+  return fmaxf(fmaxf(rl_f(v, 0), rl_f(v, 16)), fmaxf(rl_f(v, 32), rl_f(v, 48)));
+}
+OQ_DEV float wave_min(float v) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v = fminf(v, dpp_f(v, c));
+  return fminf(fminf(rl_f(v, 0), rl_f(v, 16)), fminf(rl_f(v, 32), rl_f(v, 48)));
+}
+// max / min with the lowest index among equal values (sel_max / sel_min)
+OQ_DEV void wave_minmax(float& mx, int& imx, float& mn, int& imn) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const float omx = dpp_f(mx, c), omn = dpp_f(mn, c);
+    const int oimx = dpp_i(imx, c), oimn = dpp_i(imn, c);
+    sel_max(mx, imx, omx, oimx);
+    sel_min(mn, imn, omn, oimn);
+  }
+  float rmx = rl_f(mx, 0), rmn = rl_f(mn, 0);
+  int rimx = __builtin_amdgcn_readlane(imx, 0), rimn = __builtin_amdgcn_readlane(imn, 0);
+#pragma unroll
+  for (int l = 16; l < 64; l += 16) {
+    sel_max(rmx, rimx, rl_f(mx, l), __builtin_amdgcn_readlane(imx, l));
+    sel_min(rmn, rimn, rl_f(mn, l), __builtin_amdgcn_readlane(imn, l));
+  }
+  mx = rmx; imx = rimx; mn = rmn; imn = rimn;
+}
+
 // Register image of 8 consecutive elements as loaded (bf16 packed or fp32).
 template <typename TX>
 struct Chunk8 {
@@ -287,7 +343,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
           }
         }
       }
-      group_minmax<64>(st.mx, st.imx, st.mn, st.imn);
+      wave_minmax(st.mx, st.imx, st.mn, st.imn);
       if ((tid & 63) == 0) shm[wave] = st;
       lds_barrier();
       st = shm[0];
@@ -314,8 +370,8 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
           }
         }
       }
-      sums.x = group_sum<64>(sums.x);
-      sums.y = group_sum<64>(sums.y);
+      sums.x = wave_sum(sums.x);
+      sums.y = wave_sum(sums.y);
       if ((tid & 63) == 0) shs[wave] = sums;
       lds_barrier();
       sums = shs[0];
@@ -755,11 +811,8 @@ __global__ __launch_bounds__(NT) void act_fwd_row_kernel(
         mn = fminf(mn, v[e]);
       }
     }
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      mx = fmaxf(mx, __shfl_xor(mx, off));
-      mn = fminf(mn, __shfl_xor(mn, off));
-    }
+    mx = wave_max(mx);
+    mn = wave_min(mn);
     const QParams p = make_qparams(mx, mn, 1.0f, 1.0f, qmax);
     const float lo = -p.z, hi = qmax - p.z;     // clamp as one med3 (exact integers)
     // x~ is recomputed from the packed row (and LDS) rather than kept as
@@ -856,11 +909,8 @@ __global__ __launch_bounds__(NT) void lwc_fwd_row_kernel(
         mn = fminf(mn, v[e]);
       }
     }
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      mx = fmaxf(mx, __shfl_xor(mx, off));
-      mn = fminf(mn, __shfl_xor(mn, off));
-    }
+    mx = wave_max(mx);
+    mn = wave_min(mn);
     const QParams p = make_qparams(mx, mn, clip_strength(gl[row]), clip_strength(bl[row]), qmax);
     const float lo = -p.z, hi = qmax - p.z;
     // recompute w~ from the packed row rather than hold it in fp32
@@ -1066,7 +1116,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
       }
     }
     if (quant) {
-      group_minmax<64>(st.mx, st.imx, st.mn, st.imn);
+      wave_minmax(st.mx, st.imx, st.mn, st.imn);
       if ((tid & 63) == 0) shm[wave] = st;
       lds_barrier();
       st = shm[0];
@@ -1093,8 +1143,8 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
           }
         }
       }
-      sums.x = group_sum<64>(sums.x);
-      sums.y = group_sum<64>(sums.y);
+      sums.x = wave_sum(sums.x);
+      sums.y = wave_sum(sums.y);
       if ((tid & 63) == 0) shs[wave] = sums;
       lds_barrier();
       sums = shs[0];

@@ -174,6 +174,9 @@ ACT_CASES = [
     dict(T=96, C=4096, bits=4, let=False), dict(T=77, C=4096, bits=4, let=True),
     dict(T=40, C=11008, bits=4, let=True), dict(T=64, C=1000, bits=8, let=True),
     dict(T=50, C=256, bits=6, let=False, bf16=False), dict(T=33, C=2048, bits=16, let=True),
+    # several rows per workgroup (T > 2048), so the backward's row pipeline
+    # runs; a ragged 257-chunk row and a plain 4096-channel one
+    dict(T=4100, C=2056, bits=4, let=True), dict(T=3000, C=4096, bits=3, let=False),
 ]
 
 
