@@ -260,7 +260,7 @@ __global__ __launch_bounds__(NT) void lwc_fwd_kernel(
 // Per group:  S_h = sum g*((q - z) - m*u),  S_z = sum g*(1 - m)  ->  dgamma, dbeta
 // per element: dW~ = g*m + [i = argmax] dmax + [i = argmin] dmin
 // per column (optional): partial sum over this block's rows of dW~ * W.
-template <typename TW, int KC, bool WHOLE_ROW>
+template <typename TW, int KC, bool WHOLE_ROW, bool LETW>
 __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
     const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ s,
     const float* __restrict__ gl, const float* __restrict__ bl, int bits, int group, int R,
@@ -275,16 +275,19 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
   const int L = group / 8;
   const float qmax = float((1 << bits) - 1);
 
-  float sv[KC][8], dsacc[KC][8];
+  // LETW: s is given or its partials are wanted (the weight-path LET scale,
+  // ones when s is absent, and the ds partials)
+  constexpr int KS = LETW ? KC : 1;
+  float sv[KS][8], dsacc[KS][8];
 #pragma unroll
-  for (int k = 0; k < KC; ++k) {
+  for (int k = 0; k < KS; ++k) {
     const int j = tid + NT * k;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       sv[k][e] = 1.0f;
       dsacc[k][e] = 0.0f;
     }
-    if (s && j < cpr) load8(s + 8 * j, sv[k]);
+    if (LETW && s && j < cpr) load8(s + 8 * j, sv[k]);
   }
 
   const int64_t r0 = int64_t(blockIdx.x) * R;
@@ -311,36 +314,39 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
     const TW* wrow = W + row * c_in;
     const float* grow = dW + row * c_in;
     if constexpr (WHOLE_ROW) {
-      float w[KC][8], wt[KC][8], g[KC][8];
+      // the row stays packed as loaded; w~ is recomputed in each pass
+      Chunk8<TW> wc[KC];
+      float g[KC][8];
       MinMax st = minmax_init();
       if constexpr (PF) {
 #pragma unroll
-        for (int k = 0; k < KC; ++k)
+        for (int k = 0; k < KC; ++k) {
+          wc[k] = wn[k];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            w[k][e] = wn[k].at(e);
-            g[k][e] = gn[k][e];
-          }
+          for (int e = 0; e < 8; ++e) g[k][e] = gn[k][e];
+        }
         if (row + 1 < r1) issue(row + 1);
       } else {
 #pragma unroll
         for (int k = 0; k < KC; ++k) {
           const int j = tid + NT * k;
           if (j < cpr) {
-            load8(wrow + 8 * j, w[k]);
+            wc[k].load(wrow + 8 * j);
             load8(grow + 8 * j, g[k]);
           }
         }
       }
+      auto wt_at = [&](int k, int e) {
+        const float w = wc[k].at(e);
+        if constexpr (LETW) return w * sv[k][e];
+        else return w;
+      };
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
         const int j = tid + NT * k;
         if (j < cpr) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            wt[k][e] = s ? w[k][e] * sv[k][e] : w[k][e];
-            minmax_add(st, wt[k][e], 8 * j + e);
-          }
+          for (int e = 0; e < 8; ++e) minmax_add(st, wt_at(k, e), 8 * j + e);
         }
       }
       wave_minmax(st.mx, st.imx, st.mn, st.imn);
@@ -354,15 +360,13 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
       }
       const QParams p = make_qparams(st.mx, st.mn, clip_strength(gl[row]), clip_strength(bl[row]), qmax);
       float2 sums = make_float2(0.f, 0.f);
-      bool mk[KC][8];
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
         const int j = tid + NT * k;
         if (j < cpr) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const QElem qe = quant_elem(wt[k][e], p, qmax);
-            mk[k][e] = qe.m;
+            const QElem qe = quant_elem(wt_at(k, e), p, qmax);
             const float t = qe.q - p.z;
             const float th = qe.m ? t - qe.u : t;
             sums.x += g[k][e] * th;
@@ -385,21 +389,31 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
         dgl[row] = qg.dgamma * p.gamma * (1.0f - p.gamma);
         dbl[row] = qg.dbeta * p.beta * (1.0f - p.beta);
       }
+      if (LETW || dWt) {
 #pragma unroll
-      for (int k = 0; k < KC; ++k) {
-        const int j = tid + NT * k;
-        if (j < cpr) {
-          float d[8];
+        for (int k = 0; k < KC; ++k) {
+          const int j = tid + NT * k;
+          if (j < cpr) {
+            // without LET only dW~ needs this pass: dW^ is read again rather
+            // than kept live through the reductions
+            float gg[8], d[8];
+            if constexpr (LETW) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int col = 8 * j + e;
-            float x = mk[k][e] ? g[k][e] : 0.0f;
-            if (col == st.imx) x += qg.dmx;
-            if (col == st.imn) x += qg.dmn;
-            d[e] = x;
-            dsacc[k][e] += x * w[k][e];
+              for (int e = 0; e < 8; ++e) gg[e] = g[k][e];
+            } else {
+              load8(grow + 8 * j, gg);
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int col = 8 * j + e;
+              float x = quant_elem(wt_at(k, e), p, qmax).m ? gg[e] : 0.0f;
+              if (col == st.imx) x += qg.dmx;
+              if (col == st.imn) x += qg.dmn;
+              d[e] = x;
+              if constexpr (LETW) dsacc[k][e] += x * wc[k].at(e);
+            }
+            if (dWt) store8(dWt + row * c_in + 8 * j, d);
           }
-          if (dWt) store8(dWt + row * c_in + 8 * j, d);
         }
       }
     } else {
@@ -414,7 +428,8 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
           load8(grow + 8 * j, g);
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            wt[e] = s ? w[e] * sv[k][e] : w[e];
+            if constexpr (LETW) wt[e] = w[e] * sv[k][e];
+            else wt[e] = w[e];
             minmax_add(st, wt[e], 8 * j + e);
           }
         }
@@ -452,16 +467,16 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
             if (col == st.imx) x += qg.dmx;
             if (col == st.imn) x += qg.dmn;
             d[e] = x;
-            dsacc[k][e] += x * w[e];
+            if constexpr (LETW) dsacc[k][e] += x * w[e];
           }
           if (dWt) store8(dWt + row * c_in + 8 * j, d);
         }
       }
     }
   }
-  if (ds_parts) {
+  if (LETW && ds_parts) {
 #pragma unroll
-    for (int k = 0; k < KC; ++k) {
+    for (int k = 0; k < KS; ++k) {
       const int j = tid + NT * k;
       if (j < cpr) store8(ds_parts + int64_t(blockIdx.x) * c_in + 8 * j, dsacc[k]);
     }
@@ -1202,12 +1217,31 @@ int kc_for(int64_t cols) {
   return 0;
 }
 
+// Blocks of NT threads that the current device keeps resident at once
+// (compute units times the kernel's occupancy), cached per kernel and device.
+template <typename Kern>
+int resident_blocks(Kern* kernel) {
+  static int cache[16] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+  int* slot = dev < 16 ? &cache[dev] : nullptr;
+  if (slot && *slot) return *slot;
+  int cus = 0, per = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, reinterpret_cast<const void*>(kernel), NT,
+                                                   0) != hipSuccess)
+    return 1024;
+  const int n = std::max(1, cus * per);
+  if (slot) *slot = n;
+  return n;
+}
+
 int rows_per_block(int64_t rows, int64_t target_blocks) {
   return int(std::max<int64_t>(1, (rows + target_blocks - 1) / target_blocks));
 }
 
 constexpr int64_t LWC_BLOCKS = 768;
-constexpr int64_t ACT_BLOCKS = 2048;
+constexpr int64_t ACT_BLOCKS = 768;
 
 #define OQ_KC_SWITCH(KCV, ...)                      \
   switch (KCV) {                                    \
@@ -1368,17 +1402,26 @@ hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
     else by_e(float{});
     return hipGetLastError();
   }
-  const int R = rows_per_block(c_out, LWC_BLOCKS);
-  const dim3 grid(unsigned((c_out + R - 1) / R));
   const bool whole = !small_group(group);
   const int kc = kc_for(c_in);
   auto go = [&](auto tw, auto kcc, auto wr) {
     using TW = decltype(tw);
     constexpr int KCc = decltype(kcc)::value;
     constexpr bool WR = decltype(wr)::value;
-    hipLaunchKernelGGL((lwc_bwd_kernel<TW, KCc, WR>), grid, dim3(NT), 0, st,
-                       static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits, int(group), R, dW,
-                       dgl, dbl, dW_tilde, ds_parts);
+    if (s || ds_parts) {
+      // the ds partials are one row per block: the block count is the fixed
+      // lwc_bwd_nparts(c_out) the workspace was sized for
+      const int R = rows_per_block(c_out, LWC_BLOCKS);
+      hipLaunchKernelGGL((lwc_bwd_kernel<TW, KCc, WR, true>), dim3(unsigned((c_out + R - 1) / R)),
+                         dim3(NT), 0, st, static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits,
+                         int(group), R, dW, dgl, dbl, dW_tilde, ds_parts);
+    } else {
+      // no partials: one round of resident blocks
+      const int R = rows_per_block(c_out, resident_blocks(lwc_bwd_kernel<TW, KCc, WR, false>));
+      hipLaunchKernelGGL((lwc_bwd_kernel<TW, KCc, WR, false>), dim3(unsigned((c_out + R - 1) / R)),
+                         dim3(NT), 0, st, static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits,
+                         int(group), R, dW, dgl, dbl, dW_tilde, ds_parts);
+    }
   };
   auto by_kc = [&](auto tw, auto wr) -> hipError_t {
     OQ_KC_SWITCH(kc, go(tw, std::integral_constant<int, KC>{}, wr))
