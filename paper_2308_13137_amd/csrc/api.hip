@@ -415,6 +415,7 @@ struct BlockWs {
   void *what, *xhat, *xhatT, *dyT, *dy, *whatT;
   float *dW, *dX, *psq, *pdy, *dbt, *bt, *pw, *psx, *ps1, *pb;
   double* rl;
+  float4* gstat;
 };
 
 oq_status plan_block(const oq_block_desc* d, std::vector<SitePlan>& plan) {
@@ -479,6 +480,17 @@ int wgrad_splits(const oq_block_desc* d, const SitePlan& p) {
   return gemm_mn_splits(false, true, p.M, p.C, T, T, p.C);
 }
 
+// The LWC straight-through backward runs in the weight gradient's epilogue
+// when that product is not split, the site has no LET, and every linear of it
+// shares one power-of-two group of at most 256 weights and one bit width.
+bool fused_lwc(const oq_block_desc* d, const SitePlan& p) {
+  if (p.let || !direct_grads(d, p) || wgrad_splits(d, p) != 1) return false;
+  const int64_t g = d->lin_group[p.l0];
+  for (int l = p.l0; l < p.l1; ++l)
+    if (d->lin_group[l] != g || d->lin_bits[l] != d->lin_bits[p.l0]) return false;
+  return p.l1 - p.l0 <= MAX_SEG && gemm_wgrad_lwc_supported(p.M, p.C, d->tokens, int(g));
+}
+
 size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, char* base,
                    BlockWs* w) {
   const bool bf = d->dtype == OQ_BF16;
@@ -487,7 +499,7 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
   const int ptn = gemm_part_tile_n(bf);
   const int64_t ntn = (T + ptn - 1) / ptn;
   size_t what = 0, xhat = 0, xhatT = 0, dyT = 0, dy = 0, whatT = 0, dW = 0, dX = 0, parts = 0,
-         rows = 0, pw = 0, pa = 0, pb = 0;
+         rows = 0, pw = 0, pa = 0, pb = 0, gs = 0;
   int64_t mtot = 0;
   for (const auto& p : plan) {
     const bool direct = direct_grads(d, p);
@@ -495,6 +507,7 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
     if (!direct) xhatT = std::max(xhatT, size_t(T * p.C));
     dyT = std::max(dyT, size_t(p.M * T));
     dW = std::max(dW, size_t(p.M * p.C) * size_t(wgrad_splits(d, p)));
+    if (fused_lwc(d, p)) gs = std::max(gs, size_t(p.M * (p.C / d->lin_group[p.l0])));
     parts = std::max(parts, size_t(p.M * ntn));
     rows = std::max(rows, size_t(p.M));
     mtot += p.M;
@@ -534,6 +547,7 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
   t.ps1 = pa ? cv.take<float>(pa) : nullptr;
   t.pb = pb ? cv.take<float>(pb) : nullptr;
   t.rl = cv.take<double>(size_t(mtot));
+  t.gstat = gs ? cv.take<float4>(gs) : nullptr;
   if (w) *w = t;
   return cv.off + 256;
 }
@@ -605,13 +619,16 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     for (int l = p.l0; l < p.l1; ++l) any_bias = any_bias || prm->B[l];
 
     // 1. LWC forward of every linear of the site into the stacked W^ [M, C]
+    //    (and, for the fused backward, each group's max, min, h and z)
+    const bool fused = fused_lwc(d, p);
+    const int64_t ngs = C / d->lin_group[p.l0];
     int64_t off = 0;
     for (int l = p.l0; l < p.l1; ++l) {
       const int64_t co = d->lin_c_out[l];
       ProfScope ps(PK_LWC_FWD, st, double(co) * C * 2 * es);
       OQ_HIP(lwc_fwd(prm->W[l], bf, co, C, s, prm->gamma_logit[l], prm->beta_logit[l],
                      d->lin_bits[l], d->lin_group[l], static_cast<char*>(w.what) + off * C * es, bf,
-                     nullptr, nullptr, nullptr, st),
+                     nullptr, nullptr, nullptr, st, fused ? w.gstat + off * ngs : nullptr),
              "lwc_fwd");
       la.row_begin[l] = row_base + off;
       la.row_end[l] = row_base + off + co;
@@ -678,7 +695,29 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     //    summed in a fixed order
     {
       ProfScope ps(PK_GEMM_WGRAD, st, 2.0 * double(M) * T * C);
-      if (direct) {
+      if (fused) {
+        // with the LWC straight-through backward in the epilogue (step 7)
+        LwcArgs la{};
+        la.nseg = p.l1 - p.l0;
+        int64_t b = 0;
+        for (int i = 0; i < la.nseg; ++i) {
+          const int l = p.l0 + i;
+          la.seg_begin[i] = b;
+          b += d->lin_c_out[l];
+          la.seg_end[i] = b;
+          la.W[i] = static_cast<const uint16_t*>(prm->W[l]);
+          la.gl[i] = prm->gamma_logit[l];
+          la.bl[i] = prm->beta_logit[l];
+          la.dgl[i] = gr->d_gamma_logit[l];
+          la.dbl[i] = gr->d_beta_logit[l];
+        }
+        la.gstat = w.gstat;
+        la.C = C;
+        la.group = int(d->lin_group[p.l0]);
+        la.ng = int(ngs);
+        la.qmax = float((1 << d->lin_bits[p.l0]) - 1);
+        OQ_HIP(gemm_wgrad_lwc(w.dyT, xsrc, M, C, T, T, C, la, st), "wgrad gemm with LWC backward");
+      } else if (direct) {
         const int S = wgrad_splits(d, p);
         OQ_HIP(gemm_f32out_mn(w.dyT, false, xsrc, true, M, C, T, T, C, w.dW, C, st, S, M * C),
                "wgrad gemm");
@@ -686,10 +725,11 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
       } else
         OQ_HIP(gemm_nt_f32out(w.dyT, w.xhatT, bf, M, C, T, T, T, w.dW, C, st), "wgrad gemm");
     }
-    // 7. LWC backward per linear (+ weight-path LET scale partials)
+    // 7. LWC backward per linear (+ weight-path LET scale partials), unless
+    //    the weight gradient's epilogue did it
     off = 0;
     int64_t pwo = 0;
-    for (int l = p.l0; l < p.l1; ++l) {
+    for (int l = p.l0; l < p.l1 && !fused; ++l) {
       const int64_t co = d->lin_c_out[l];
       ProfScope ps(PK_LWC_BWD, st, double(co) * C * (es + 4));
       OQ_HIP(lwc_bwd(prm->W[l], bf, co, C, s, prm->gamma_logit[l], prm->beta_logit[l],

@@ -572,6 +572,133 @@ OQ_DEV void epilogue8(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, in
   }
 }
 
+// Weight gradient with the LWC straight-through backward fused (no LET):
+// the accumulators are dW^ for rows m (output channels of the stacked
+// linears) and columns n (input channels).  G = group / 8 lanes of a row
+// cover one group; groups of 128 and 256 span two and four column waves and
+// meet in LDS.
+template <int G>
+struct EpiLwc {
+  LwcArgs a;
+  static constexpr bool kRows = false;
+  OQ_DEV void split(int) {}
+  // linear of stacked row m: constant indices only, so the argument block
+  // stays in scalar registers
+  struct Seg { const uint16_t* w; const float* gl; const float* bl; float* dgl; float* dbl; int64_t o; };
+  OQ_DEV Seg seg(int64_t m) const {
+    Seg s{a.W[0], a.gl[0], a.bl[0], a.dgl[0], a.dbl[0], m - a.seg_begin[0]};
+#pragma unroll
+    for (int i = 1; i < MAX_SEG; ++i) {
+      if (i < a.nseg && m >= a.seg_begin[i]) {
+        s = Seg{a.W[i], a.gl[i], a.bl[i], a.dgl[i], a.dbl[i], m - a.seg_begin[i]};
+      }
+    }
+    return s;
+  }
+  // S_h, S_z of one 8-column chunk of row m at column n
+  OQ_DEV float2 chunk(int64_t m, int64_t n, const float* g) const {
+    const Seg s = seg(m);
+    float w[8];
+    load8(s.w + s.o * a.C + n, w);
+    const float4 st = a.gstat[m * a.ng + n / a.group];
+    const float r = div_rn(1.0f, st.z);
+    const float lo = -st.w, hi = a.qmax - st.w;
+    float2 c = make_float2(0.f, 0.f);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      // q - z = med3(rint(u), -z, qmax - z); inside the clamp exactly when
+      // the median left rint(u) alone
+      const float u = w[e] * r;
+      const float ru = rintf(u);
+      const float tq = __builtin_amdgcn_fmed3f(ru, lo, hi);
+      const bool in = tq == ru;
+      c.x += g[e] * (in ? tq - u : tq);
+      c.y += in ? 0.0f : g[e];
+    }
+    return c;
+  }
+  // Eq. 2's parameters again from the group's max / min and the logits, then
+  // the logit gradients
+  OQ_DEV void finish(int64_t m, int gi, float sh, float sz) const {
+    const Seg s = seg(m);
+    const float4 st = a.gstat[m * a.ng + gi];
+    const int64_t k = s.o * a.ng + gi;
+    const QParams p = make_qparams(st.x, st.y, clip_strength(s.gl[k]), clip_strength(s.bl[k]), a.qmax);
+    const QGrad qg = quant_group_grad(sh, sz, st.x, st.y, p, a.qmax);
+    s.dgl[k] = qg.dgamma * p.gamma * (1.0f - p.gamma);
+    s.dbl[k] = qg.dbeta * p.beta * (1.0f - p.beta);
+  }
+};
+
+template <class E>
+struct IsLwc : std::false_type {};
+template <int G>
+struct IsLwc<EpiLwc<G>> : std::true_type {};
+
+template <int G>
+OQ_DEV void epilogue8_lwc(const f32x4_t (&acc)[8][4], const EpiLwc<G>& ep, int64_t m0,
+                          int64_t n0, int64_t M, int64_t N, int wave, int lane, float* scratch,
+                          float2 (*rowbuf)[BM]) {
+  constexpr int PITCH = EPI8_PITCH;
+  const int wm = wave >> 2, wn = wave & 3;
+  float* reg = scratch + wave * (32 * EPI8_PITCH);
+  const int fr = lane & 15, fk = lane >> 4;
+  const int cl = lane & 7, rl = lane >> 3;
+  const int64_t nb = n0 + wn * 64 + 8 * cl;
+  const bool colok = nb < N;                 // N % 8 == 0: a chunk is whole or absent
+#pragma unroll
+  for (int P = 0; P < 4; ++P) {
+#pragma unroll
+    for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          reg[(16 * ii + 4 * fk + r) * PITCH + 16 * j + fr] = acc[2 * P + ii][j][r];
+    for (int it = 0; it < 4; ++it) {
+      const int rloc = rl + 8 * it;
+      const int trow = wm * 128 + 32 * P + rloc;
+      const int64_t m = m0 + trow;
+      float2 c = make_float2(0.f, 0.f);
+      if (m < M && colok) {
+        float v[8];
+        const float4 a_ = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl);
+        const float4 b_ = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl + 4);
+        v[0] = a_.x; v[1] = a_.y; v[2] = a_.z; v[3] = a_.w;
+        v[4] = b_.x; v[5] = b_.y; v[6] = b_.z; v[7] = b_.w;
+        c = ep.chunk(m, nb, v);
+      }
+      if constexpr (G <= 8) {
+        c.x = group_sum<G>(c.x);
+        c.y = group_sum<G>(c.y);
+        if (m < M && colok && cl % G == 0) ep.finish(m, int(nb / ep.a.group), c.x, c.y);
+      } else {
+        c.x = group_sum<8>(c.x);
+        c.y = group_sum<8>(c.y);
+        if (cl == 0) rowbuf[wn][trow] = c;
+      }
+    }
+  }
+  if constexpr (G > 8) {
+    // a group covers WPG column waves; GPR groups per tile row
+    constexpr int WPG = G / 8, GPR = 4 / WPG;
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < BM * GPR; idx += NTHR8) {
+      const int trow = idx / GPR, gq = idx % GPR;
+      const int64_t m = m0 + trow, ng0 = n0 + int64_t(gq) * WPG * 64;
+      if (m < M && ng0 < N) {
+        float2 s = rowbuf[gq * WPG][trow];
+#pragma unroll
+        for (int w = 1; w < WPG; ++w) {
+          s.x += rowbuf[gq * WPG + w][trow].x;
+          s.y += rowbuf[gq * WPG + w][trow].y;
+        }
+        ep.finish(m, int(ng0 / ep.a.group), s.x, s.y);
+      }
+    }
+  }
+}
+
 // Stages: B's tile of stage s in one of three buffers (s % 3), A's in one of
 // two (s % 2), 160 KiB in all.  Iteration kt runs k-half 1 of stage kt, then
 // (after the middle barrier) k-half 0 of stage kt + 1.  B's buffer for stage
@@ -710,8 +837,12 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
   }
   __syncthreads();
   // epilogue staging (68 KiB) and row partials (8 KiB at 96 KiB) reuse the stages
-  epilogue8(acc, epi, m0, n0, M, N, tn, wave, lane, reinterpret_cast<float*>(&lds[0]),
-            reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304));
+  if constexpr (IsLwc<Epi>::value)
+    epilogue8_lwc(acc, epi, m0, n0, M, N, wave, lane, reinterpret_cast<float*>(&lds[0]),
+                  reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304));
+  else
+    epilogue8(acc, epi, m0, n0, M, N, tn, wave, lane, reinterpret_cast<float*>(&lds[0]),
+              reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304));
 }
 
 // ------------------------------------------------------------------ fp32 kernel
@@ -888,6 +1019,33 @@ hipError_t gemm_f32out_mn(const void* A, bool a_mn, const void* B, bool b_mn, in
                    split_stride % 8 == 0;
   return launch(A, B, true, M, N, ks, lda, ldb, EpiF32{C, ldc, vec, split_stride}, st, a_mn,
                 b_mn, splits);
+}
+
+bool gemm_wgrad_lwc_supported(int64_t M, int64_t C, int64_t K, int group) {
+  return group >= 8 && group <= BN && (group & (group - 1)) == 0 && C % group == 0 &&
+         w8_ok(false, true, M, C, K, K, C);
+}
+
+hipError_t gemm_wgrad_lwc(const void* dyT, const void* x, int64_t M, int64_t C, int64_t K,
+                          int64_t lda, int64_t ldb, const LwcArgs& la, hipStream_t st) {
+  if (!gemm_wgrad_lwc_supported(M, C, K, la.group) || lda != K || ldb != C || la.C != C ||
+      la.ng != C / la.group || la.nseg < 1 || la.nseg > MAX_SEG)
+    return hipErrorInvalidValue;
+  auto go = [&](auto gc) {
+    constexpr int Gc = decltype(gc)::value;
+    const int64_t tm = (M + BM - 1) / BM, tn = (C + BN - 1) / BN;
+    if (tm * tn > (int64_t(1) << 31) - 1) return hipErrorInvalidValue;
+    launch_w8<EpiLwc<Gc>, false, true>(dyT, x, M, C, K, lda, ldb, tm, tn, EpiLwc<Gc>{la}, st);
+    return hipGetLastError();
+  };
+  switch (la.group / 8) {
+    case 1: return go(std::integral_constant<int, 1>{});
+    case 2: return go(std::integral_constant<int, 2>{});
+    case 4: return go(std::integral_constant<int, 4>{});
+    case 8: return go(std::integral_constant<int, 8>{});
+    case 16: return go(std::integral_constant<int, 16>{});
+    default: return go(std::integral_constant<int, 32>{});
+  }
 }
 
 hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int64_t N,

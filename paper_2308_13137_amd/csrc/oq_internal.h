@@ -71,12 +71,38 @@ hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int
 hipError_t gemm_nt_resid(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
                          int64_t lda, int64_t ldb, ResidArgs ra, hipStream_t st);
 
+// The weight gradient with the LWC straight-through backward in its epilogue
+// (no LET, power-of-two groups of 8..256 weights).  The product dW^ = dY^T X^
+// over rows m of up to MAX_SEG linears stacked along M is never stored: per
+// (row, group) the epilogue forms S_h = sum g ((q - z) - m u) and
+// S_z = sum g (1 - m) from the accumulators, the bf16 weights and the group
+// statistics the forward wrote, and writes the logit gradients.
+struct LwcArgs {
+  int nseg;
+  int64_t seg_begin[MAX_SEG], seg_end[MAX_SEG];
+  const uint16_t* W[MAX_SEG];      // bf16 [rows_l, C]
+  const float* gl[MAX_SEG];        // [rows_l, ng] clip-strength logits
+  const float* bl[MAX_SEG];
+  float* dgl[MAX_SEG];             // [rows_l, ng] outputs
+  float* dbl[MAX_SEG];
+  const float4* gstat;             // [M, ng] {max, min, h, z} of each group
+  int64_t C;
+  int group, ng;
+  float qmax;
+};
+bool gemm_wgrad_lwc_supported(int64_t M, int64_t C, int64_t K, int group);
+// dY^T [M, K] K-contiguous (lda), X^ [K, C] read C-contiguous (ldb).
+hipError_t gemm_wgrad_lwc(const void* dyT, const void* x, int64_t M, int64_t C, int64_t K,
+                          int64_t lda, int64_t ldb, const LwcArgs& la, hipStream_t st);
+
 // ---------------------------------------------------------------- quantisers
 // LWC forward on rows [0, c_out) of one weight.  Returns hipErrorInvalidValue
 // when (c_in, group) is outside the supported set.
+// gstat (power-of-two groups without s only) receives {max, min, h, z} per group.
 hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
                    const float* gl, const float* bl, int bits, int64_t group, void* W_dq,
-                   bool dq_bf16, uint8_t* codes, float* h, float* z, hipStream_t st);
+                   bool dq_bf16, uint8_t* codes, float* h, float* z, hipStream_t st,
+                   float4* gstat = nullptr);
 // LWC backward.  When ds_parts != nullptr each block writes one partial row
 // [c_in] of sum_o dW~[o,c]*W[o,c] into ds_parts; the number of rows written is
 // lwc_bwd_nparts(c_out).

@@ -577,7 +577,7 @@ template <typename TW, typename TQ, int G, bool CODES>
 __global__ __launch_bounds__(NT) void lwc_fwd_coal_kernel(
     const TW* __restrict__ W, int64_t nchunk, const float* __restrict__ gl,
     const float* __restrict__ bl, int bits, TQ* __restrict__ wdq, uint8_t* __restrict__ codes,
-    float* __restrict__ hout, float* __restrict__ zout) {
+    float* __restrict__ hout, float* __restrict__ zout, float4* __restrict__ gstat) {
   constexpr int U = G < 8 ? G : 8;           // slices per lane: the owners fit in a wave
   constexpr int NGW = 64 / G;                // groups per slice
   const int lane = threadIdx.x & 63;
@@ -628,6 +628,7 @@ __global__ __launch_bounds__(NT) void lwc_fwd_coal_kernel(
       if (step * (U * NGW) + lane < ngroup) {
         if (hout) hout[g] = p.h;
         if (zout) zout[g] = p.z;
+        if (gstat) gstat[g] = make_float4(gmx, gmn, p.h, p.z);
       }
     }
 #pragma unroll
@@ -1267,9 +1268,11 @@ bool quant_shape_supported(int64_t c_in, int64_t group) {
 
 hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
                    const float* gl, const float* bl, int bits, int64_t group, void* W_dq,
-                   bool dq_bf16, uint8_t* codes, float* h, float* z, hipStream_t st) {
+                   bool dq_bf16, uint8_t* codes, float* h, float* z, hipStream_t st,
+                   float4* gstat) {
   if (!quant_shape_supported(c_in, group)) return hipErrorInvalidValue;
   if (c_out <= 0) return hipSuccess;
+  if (gstat && (s || !small_group(group))) return hipErrorInvalidValue;
   if (small_group(group) && !s) {
     const int64_t nchunk = c_out * c_in / 8;
     const int64_t waves = std::min<int64_t>((nchunk + 511) / 512, 256 * 32);
@@ -1281,11 +1284,11 @@ hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
       if (codes)
         hipLaunchKernelGGL((lwc_fwd_coal_kernel<TW, TQ, Gc, true>), grid, dim3(NT), 0, st,
                            static_cast<const TW*>(W), nchunk, gl, bl, bits, static_cast<TQ*>(W_dq),
-                           codes, h, z);
+                           codes, h, z, gstat);
       else
         hipLaunchKernelGGL((lwc_fwd_coal_kernel<TW, TQ, Gc, false>), grid, dim3(NT), 0, st,
                            static_cast<const TW*>(W), nchunk, gl, bl, bits, static_cast<TQ*>(W_dq),
-                           codes, h, z);
+                           codes, h, z, gstat);
     };
     auto by_g = [&](auto tw, auto tq) {
       switch (group / 8) {

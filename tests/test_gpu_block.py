@@ -39,6 +39,13 @@ WORKLOADS = [
     # token (K) range into 8 (T=8192) or 4 (T=4096) parts summed afterwards
     small_llama("c2_t8192", hidden=256, ffn=768, T=8192, w_bits=3, group=128),
     small_llama("c3_t4096", hidden=256, ffn=512, T=4096, w_bits=4, let=True, act_bits=4),
+    # without LET, unsplit weight gradients with power-of-two groups take the
+    # LWC backward in their epilogue: groups of 8 to 256 weights (one lane to
+    # four column waves per group), ragged row and column tiles
+    small_llama("g64_t256", hidden=320, ffn=832, T=256, w_bits=2, group=64),
+    small_llama("g256_t128", hidden=512, ffn=1024, T=128, w_bits=4, group=256),
+    small_llama("g32_t192", hidden=256, ffn=512, T=192, w_bits=3, group=32),
+    small_llama("g8_t128", hidden=256, ffn=512, T=128, w_bits=2, group=8),
 ]
 
 
