@@ -692,7 +692,12 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     }
     // 6. weight gradient dW^ = dY^T X^  [M, C]; over a K (token) split of S
     //    parts when that fills the last wave of tiles better, the parts
-    //    summed in a fixed order
+    //    summed in a fixed order (by the LWC backward's loads where it can)
+    const int S = direct && !fused ? wgrad_splits(d, p) : 1;
+    bool parts_in_bwd = S > 1;
+    for (int l = p.l0; l < p.l1; ++l)
+      parts_in_bwd = parts_in_bwd && lwc_bwd_sums_parts(d->lin_c_out[l], C, d->lin_group[l], s,
+                                                        p.let);
     {
       ProfScope ps(PK_GEMM_WGRAD, st, 2.0 * double(M) * T * C);
       if (fused) {
@@ -718,10 +723,9 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
         la.qmax = float((1 << d->lin_bits[p.l0]) - 1);
         OQ_HIP(gemm_wgrad_lwc(w.dyT, xsrc, M, C, T, T, C, la, st), "wgrad gemm with LWC backward");
       } else if (direct) {
-        const int S = wgrad_splits(d, p);
         OQ_HIP(gemm_f32out_mn(w.dyT, false, xsrc, true, M, C, T, T, C, w.dW, C, st, S, M * C),
                "wgrad gemm");
-        if (S > 1) OQ_HIP(sum_partials(w.dW, M * C, S, M * C, st), "wgrad split sum");
+        if (S > 1 && !parts_in_bwd) OQ_HIP(sum_partials(w.dW, M * C, S, M * C, st), "wgrad split sum");
       } else
         OQ_HIP(gemm_nt_f32out(w.dyT, w.xhatT, bf, M, C, T, T, T, w.dW, C, st), "wgrad gemm");
     }
@@ -734,7 +738,8 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
       ProfScope ps(PK_LWC_BWD, st, double(co) * C * (es + 4));
       OQ_HIP(lwc_bwd(prm->W[l], bf, co, C, s, prm->gamma_logit[l], prm->beta_logit[l],
                      d->lin_bits[l], d->lin_group[l], w.dW + off * C, gr->d_gamma_logit[l],
-                     gr->d_beta_logit[l], nullptr, p.let ? w.pw + pwo * C : nullptr, st),
+                     gr->d_beta_logit[l], nullptr, p.let ? w.pw + pwo * C : nullptr, st,
+                     parts_in_bwd ? S : 1, M * C),
              "lwc_bwd");
       off += co;
       pwo += lwc_bwd_nparts(co);

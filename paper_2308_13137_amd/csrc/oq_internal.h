@@ -107,9 +107,13 @@ hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
 // [c_in] of sum_o dW~[o,c]*W[o,c] into ds_parts; the number of rows written is
 // lwc_bwd_nparts(c_out).
 int64_t lwc_bwd_nparts(int64_t c_out);
+// With parts > 1 (only where lwc_bwd_sums_parts holds) dW holds `parts`
+// partial products spaced part_stride floats apart, summed in order on load.
+bool lwc_bwd_sums_parts(int64_t c_out, int64_t c_in, int64_t group, bool has_s, bool want_ds);
 hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
                    const float* gl, const float* bl, int bits, int64_t group, const float* dW,
-                   float* dgl, float* dbl, float* dW_tilde, float* ds_parts, hipStream_t st);
+                   float* dgl, float* dbl, float* dW_tilde, float* ds_parts, hipStream_t st,
+                   int parts = 1, int64_t part_stride = 0);
 bool quant_shape_supported(int64_t c_in, int64_t group);
 
 // Activation fake-quant (per token row), LET transform included.

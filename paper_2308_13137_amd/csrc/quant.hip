@@ -658,7 +658,8 @@ template <typename TW, int E, bool DWT>
 __global__ __launch_bounds__(NT) void lwc_bwd_run_kernel(
     const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ gl,
     const float* __restrict__ bl, int bits, int group, const float* __restrict__ dW,
-    float* __restrict__ dgl, float* __restrict__ dbl, float* __restrict__ dWt) {
+    float* __restrict__ dgl, float* __restrict__ dbl, float* __restrict__ dWt, int parts,
+    int64_t part_stride) {
   const uint32_t runs = uint32_t(c_in / E), nrun = uint32_t(c_out) * runs;  // < 2^31 (host)
   uint32_t t = blockIdx.x * NT + threadIdx.x;
   const bool valid = t < nrun;
@@ -673,6 +674,19 @@ __global__ __launch_bounds__(NT) void lwc_bwd_run_kernel(
   const float* grow = dW + row * c_in + col0;
   Run<float, E> gr;                  // the run's dL/dW^, all loads in flight at once
   gr.load(grow);
+  // a K-split product leaves `parts` partial dW^ spaced part_stride apart:
+  // summed here in order, ((p0 + p1) + p2) + ...
+  for (int q = 1; q < parts; ++q) {
+    Run<float, E> pq;
+    pq.load(grow + q * part_stride);
+#pragma unroll
+    for (int i = 0; i < Run<float, E>::NV; ++i) {
+      gr.v[i].x = __float_as_uint(__uint_as_float(gr.v[i].x) + __uint_as_float(pq.v[i].x));
+      gr.v[i].y = __float_as_uint(__uint_as_float(gr.v[i].y) + __uint_as_float(pq.v[i].y));
+      gr.v[i].z = __float_as_uint(__uint_as_float(gr.v[i].z) + __uint_as_float(pq.v[i].z));
+      gr.v[i].w = __float_as_uint(__uint_as_float(gr.v[i].w) + __uint_as_float(pq.v[i].w));
+    }
+  }
   // max / min of the group; with DWT also the lowest index holding each
   // (values first, then the first matching index in the run, then (max,
   // index) across the group's lanes): only dW~ places the max/min gradient
@@ -1372,12 +1386,21 @@ int64_t lwc_bwd_nparts(int64_t c_out) {
   return (c_out + R - 1) / R;
 }
 
+bool lwc_bwd_sums_parts(int64_t c_out, int64_t c_in, int64_t group, bool has_s, bool want_ds) {
+  return quant_shape_supported(c_in, group) && small_group(group) && !has_s && !want_ds &&
+         c_out * c_in < (int64_t(1) << 34);
+}
+
 hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
                    const float* gl, const float* bl, int bits, int64_t group, const float* dW,
-                   float* dgl, float* dbl, float* dW_tilde, float* ds_parts, hipStream_t st) {
+                   float* dgl, float* dbl, float* dW_tilde, float* ds_parts, hipStream_t st,
+                   int parts, int64_t part_stride) {
   if (!quant_shape_supported(c_in, group)) return hipErrorInvalidValue;
   if (c_out <= 0) return hipSuccess;
-  if (small_group(group) && !s && !ds_parts && c_out * c_in < (int64_t(1) << 34)) {
+  if (parts < 1 || (parts > 1 && (!lwc_bwd_sums_parts(c_out, c_in, group, s, ds_parts) ||
+                                  part_stride < c_out * c_in || part_stride % 4)))
+    return hipErrorInvalidValue;
+  if (lwc_bwd_sums_parts(c_out, c_in, group, s, ds_parts)) {
     const int E = int(std::min<int64_t>(group, 32));
     const int64_t nrun = c_out * (c_in / E);
     const dim3 grid(unsigned((nrun + NT - 1) / NT));
@@ -1387,11 +1410,11 @@ hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
       if (dW_tilde)
         hipLaunchKernelGGL((lwc_bwd_run_kernel<TW, Ec, true>), grid, dim3(NT), 0, st,
                            static_cast<const TW*>(W), c_out, c_in, gl, bl, bits, int(group), dW,
-                           dgl, dbl, dW_tilde);
+                           dgl, dbl, dW_tilde, parts, part_stride);
       else
         hipLaunchKernelGGL((lwc_bwd_run_kernel<TW, Ec, false>), grid, dim3(NT), 0, st,
                            static_cast<const TW*>(W), c_out, c_in, gl, bl, bits, int(group), dW,
-                           dgl, dbl, dW_tilde);
+                           dgl, dbl, dW_tilde, parts, part_stride);
     };
     auto by_e = [&](auto tw) {
       switch (E) {
