@@ -480,6 +480,13 @@ int wgrad_splits(const oq_block_desc* d, const SitePlan& p) {
   return gemm_mn_splits(false, true, p.M, p.C, T, T, p.C);
 }
 
+// K-split count of the forward product (bf16 only): few output tiles and a
+// long K, as at the paper's 2048-token step.
+int fwd_splits(const oq_block_desc* d, const SitePlan& p) {
+  if (d->dtype != OQ_BF16) return 1;
+  return gemm_resid_splits(p.M, d->tokens, p.C);
+}
+
 // The LWC straight-through backward runs in the weight gradient's epilogue
 // when that product is not split, the site has no LET, and every linear of it
 // shares one power-of-two group of at most 256 weights and one bit width.
@@ -507,6 +514,8 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
     if (!direct) xhatT = std::max(xhatT, size_t(T * p.C));
     dyT = std::max(dyT, size_t(p.M * T));
     dW = std::max(dW, size_t(p.M * p.C) * size_t(wgrad_splits(d, p)));
+    // the split forward's parts live there too (the weight gradient comes later)
+    dW = std::max(dW, size_t(p.M * T) * size_t(fwd_splits(d, p)));
     if (fused_lwc(d, p)) gs = std::max(gs, size_t(p.M * (p.C / d->lin_group[p.l0])));
     parts = std::max(parts, size_t(p.M * ntn));
     rows = std::max(rows, size_t(p.M));
@@ -683,7 +692,12 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
       ra.part_sq = w.psq;
       ra.part_dy = p.let ? w.pdy : nullptr;
       ProfScope ps(PK_GEMM_FWD, st, 2.0 * double(M) * T * C);
-      OQ_HIP(gemm_nt_resid(w.what, xsrc, bf, M, T, C, C, C, ra, st), "forward gemm");
+      const int SF = fwd_splits(d, p);
+      if (SF > 1)
+        OQ_HIP(gemm_nt_resid_split(w.what, xsrc, M, T, C, C, C, ra, w.dW, SF, st),
+               "forward gemm (K split)");
+      else
+        OQ_HIP(gemm_nt_resid(w.what, xsrc, bf, M, T, C, C, C, ra, st), "forward gemm");
     }
     {
       ProfScope ps(PK_OTHER, st, double(M) * ntn * 8);

@@ -76,6 +76,62 @@ OQ_DEV void sel_min(float& v, int& i, float ov, int oi) {
   if (ov < v || (ov == v && oi < i)) { v = ov; i = oi; }
 }
 
+// Whole-wave reductions on the VALU: DPP exchanges within each 16-lane row
+// (quad xor 1, quad xor 2, half-row mirror, row mirror), then the four row
+// results read out (lanes 0, 16, 32, 48) and combined in that order.  Every
+// lane returns the same value; the order is fixed, so sums are reproducible.
+OQ_DEV float dpp_f(float v, int ctrl) {
+  switch (ctrl) {
+    case 0: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+    case 1: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+    case 2: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+    default: return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
+  }
+}
+OQ_DEV int dpp_i(int v, int ctrl) {
+  switch (ctrl) {
+    case 0: return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+    case 1: return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+    case 2: return __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+    default: return __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
+  }
+}
+OQ_DEV float rl_f(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
+
+OQ_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v += dpp_f(v, c);
+  return ((rl_f(v, 0) + rl_f(v, 16)) + rl_f(v, 32)) + rl_f(v, 48);
+}
+OQ_DEV float wave_max(float v) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v = fmaxf(v, dpp_f(v, c));
+  return fmaxf(fmaxf(rl_f(v, 0), rl_f(v, 16)), fmaxf(rl_f(v, 32), rl_f(v, 48)));
+}
+OQ_DEV float wave_min(float v) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v = fminf(v, dpp_f(v, c));
+  return fminf(fminf(rl_f(v, 0), rl_f(v, 16)), fminf(rl_f(v, 32), rl_f(v, 48)));
+}
+// max / min with the lowest index among equal values (sel_max / sel_min)
+OQ_DEV void wave_minmax(float& mx, int& imx, float& mn, int& imn) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const float omx = dpp_f(mx, c), omn = dpp_f(mn, c);
+    const int oimx = dpp_i(imx, c), oimn = dpp_i(imn, c);
+    sel_max(mx, imx, omx, oimx);
+    sel_min(mn, imn, omn, oimn);
+  }
+  float rmx = rl_f(mx, 0), rmn = rl_f(mn, 0);
+  int rimx = __builtin_amdgcn_readlane(imx, 0), rimn = __builtin_amdgcn_readlane(imn, 0);
+#pragma unroll
+  for (int l = 16; l < 64; l += 16) {
+    sel_max(rmx, rimx, rl_f(mx, l), __builtin_amdgcn_readlane(imx, l));
+    sel_min(rmn, rimn, rl_f(mn, l), __builtin_amdgcn_readlane(imn, l));
+  }
+  mx = rmx; imx = rimx; mn = rmn; imn = rimn;
+}
+
 // Butterfly over aligned groups of L lanes (L a power of two <= 64): every
 // lane of the group ends with the identical result.
 template <int L>

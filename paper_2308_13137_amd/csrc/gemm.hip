@@ -845,6 +845,65 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
               reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304));
 }
 
+// ------------------------------------------------------------------ split forward's residual
+// The forward product split over K leaves `parts` fp32 partial products
+// [M, N] spaced part_stride apart.  One wave per (row m, 256-column tile):
+// y = ((p0 + p1) + ...) + bias[m], then the residual epilogue's arithmetic
+// (r = y - y_fp, dY = bf16(r * scale)) and the tile's sums of r^2 and of dY.
+__global__ __launch_bounds__(256) void resid_parts_kernel(const float* __restrict__ P, int parts,
+                                                          int64_t part_stride, int64_t M,
+                                                          int64_t N, ResidArgs a, bool vec4) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wid = (int64_t(blockIdx.x) * 256 + threadIdx.x) >> 6;
+  if (wid >= M * a.ntn) return;                  // whole waves leave together
+  const int64_t m = wid / a.ntn;
+  const int tn = int(wid - m * a.ntn);
+  const EpiResid<uint16_t> ep{a, false};
+  const auto r = ep.row(m);
+  const int64_t n0 = int64_t(tn) * BN + 4 * lane;
+  float sq = 0.f, sdy = 0.f;
+  if (vec4 && n0 + 4 <= N) {
+    float4 y = *reinterpret_cast<const float4*>(P + m * N + n0);
+    for (int q = 1; q < parts; ++q) {
+      const float4 t = *reinterpret_cast<const float4*>(P + q * part_stride + m * N + n0);
+      y.x += t.x;
+      y.y += t.y;
+      y.z += t.z;
+      y.w += t.w;
+    }
+    const uint2 f = *reinterpret_cast<const uint2*>(r.yfp + n0);
+    const float yv[4] = {y.x, y.y, y.z, y.w};
+    const float fv[4] = {__uint_as_float(f.x << 16), __uint_as_float(f.x & 0xffff0000u),
+                         __uint_as_float(f.y << 16), __uint_as_float(f.y & 0xffff0000u)};
+    float d[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float res = (yv[e] + r.b) - fv[e];
+      d[e] = res * r.scale;
+      sq += res * res;
+      sdy += EpiResid<uint16_t>::rounded(d[e]);
+    }
+    *reinterpret_cast<uint2*>(r.dy + n0) = make_uint2(f2bf2(d[0], d[1]), f2bf2(d[2], d[3]));
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t n = n0 + e;
+      if (n < N) {
+        float y = P[m * N + n];
+        for (int q = 1; q < parts; ++q) y += P[q * part_stride + m * N + n];
+        const float res = (y + r.b) - load1(r.yfp + n);
+        const float d = res * r.scale;
+        store1(r.dy + n, d);
+        sq += res * res;
+        sdy += EpiResid<uint16_t>::rounded(d);
+      }
+    }
+  }
+  sq = wave_sum(sq);
+  sdy = wave_sum(sdy);
+  if (lane == 0) ep.finish(m, tn, sq, sdy);
+}
+
 // ------------------------------------------------------------------ fp32 kernel
 template <class Epi>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A,
@@ -1057,6 +1116,52 @@ hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int
                   EpiStore<uint16_t>{static_cast<uint16_t*>(C), ldc, bias, vec}, st);
   return launch(A, B, bf16, M, N, K, lda, ldb,
                 EpiStore<float>{static_cast<float*>(C), ldc, bias, vec}, st);
+}
+
+int gemm_resid_splits(int64_t M, int64_t N, int64_t K) {
+  // Same step model as gemm_mn_splits; the parts cost 2 S M N 4 bytes more
+  // (written by the product, read by the residual pass).
+  constexpr int kCUs = 256;
+  constexpr double kStep = 1.45e-6, kEpi = 16.0, kBw = 5.0e12;
+  if (!w8_ok(false, false, M, N, K, K, K)) return 1;
+  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  int best = 1;
+  double best_t = 0.0;
+  for (int s = 1; s <= 4; s *= 2) {
+    if (K % (int64_t(BK) * s)) break;
+    const int64_t ks = K / s;
+    if (s > 1 && ks < 16 * BK) break;
+    const int64_t waves = (tiles * s + kCUs - 1) / kCUs;
+    double t_s = double(waves) * (double(ks / BK) + kEpi) * kStep;
+    if (s > 1) t_s += 2.0 * s * double(M) * double(N) * 4.0 / kBw + 5e-6;
+    if (s == 1 || t_s < 0.9 * best_t) {
+      best = s;
+      best_t = t_s;
+    }
+  }
+  return best;
+}
+
+hipError_t gemm_nt_resid_split(const void* A, const void* B, int64_t M, int64_t N, int64_t K,
+                               int64_t lda, int64_t ldb, ResidArgs ra, float* parts, int splits,
+                               hipStream_t st) {
+  if (splits < 2 || K % splits || M <= 0 || N <= 0) return hipErrorInvalidValue;
+  const int64_t ks = K / splits;
+  if (!w8_ok(false, false, M, N, ks, lda, ldb)) return hipErrorInvalidValue;
+  ra.ntn = int((N + BN - 1) / BN);
+  const int64_t stride = M * N;
+  const bool vec = N % 8 == 0 && (reinterpret_cast<uintptr_t>(parts) & 15) == 0;
+  hipError_t e = launch(A, B, true, M, N, ks, lda, ldb, EpiF32{parts, N, vec, stride}, st, false,
+                        false, splits);
+  if (e != hipSuccess) return e;
+  const int64_t waves = M * ra.ntn;
+  // 16-byte part loads, 8-byte target loads and dY stores when every row allows them
+  bool vec4 = N % 4 == 0 && ra.ld_yfp % 4 == 0 && ra.ld_dy % 4 == 0 &&
+              (reinterpret_cast<uintptr_t>(ra.dy) & 7) == 0;
+  for (int s = 0; s < ra.nseg; ++s) vec4 = vec4 && (reinterpret_cast<uintptr_t>(ra.yfp[s]) & 7) == 0;
+  hipLaunchKernelGGL(resid_parts_kernel, dim3(unsigned((waves + 3) / 4)), dim3(256), 0, st, parts,
+                     splits, stride, M, N, ra, vec4);
+  return hipGetLastError();
 }
 
 hipError_t gemm_nt_resid(const void* A, const void* B, bool bf16, int64_t M, int64_t N,

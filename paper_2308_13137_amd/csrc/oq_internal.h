@@ -70,6 +70,14 @@ hipError_t gemm_nt_store(const void* A, const void* B, bool bf16, int64_t M, int
                          const float* bias, hipStream_t st);
 hipError_t gemm_nt_resid(const void* A, const void* B, bool bf16, int64_t M, int64_t N, int64_t K,
                          int64_t lda, int64_t ldb, ResidArgs ra, hipStream_t st);
+// The same forward split over K (bf16): `splits` fp32 partial products go to
+// parts [splits, M, N], then one pass sums them in order and applies the
+// residual epilogue.  gemm_resid_splits picks the count (1 = do not split)
+// for 256 compute units: few output tiles and a long K.
+int gemm_resid_splits(int64_t M, int64_t N, int64_t K);
+hipError_t gemm_nt_resid_split(const void* A, const void* B, int64_t M, int64_t N, int64_t K,
+                               int64_t lda, int64_t ldb, ResidArgs ra, float* parts, int splits,
+                               hipStream_t st);
 
 // The weight gradient with the LWC straight-through backward in its epilogue
 // (no LET, power-of-two groups of 8..256 weights).  The product dW^ = dY^T X^

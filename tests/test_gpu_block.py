@@ -95,6 +95,16 @@ def test_block_step_parity(w, logit):
     assert errs[worst] < tol, errs
 
 
+# 2048-wide sites over 64 tokens: a handful of output tiles and K = 2048, so
+# the forward product splits its K range (2 parts, summed by the residual
+# pass) and the weight gradient takes the fused LWC backward
+FSPLIT = small_llama("fsplit_t64", hidden=2048, ffn=256, T=64, w_bits=4, group=128, kv=256)
+
+
+def test_block_step_parity_split_forward():
+    test_block_step_parity(FSPLIT, "random")
+
+
 def test_block_step_is_deterministic():
     w = WORKLOADS[2]
     P = make_problem(w, seed=4)
