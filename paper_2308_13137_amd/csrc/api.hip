@@ -747,7 +747,7 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     int64_t pwo = 0;
     for (int l = p.l0; l < p.l1 && !fused; ++l) {
       const int64_t co = d->lin_c_out[l];
-      ProfScope ps(PK_LWC_BWD, st, double(co) * C * (es + 4));
+      ProfScope ps(PK_LWC_BWD, st, double(co) * C * (es + 4.0 * (parts_in_bwd ? S : 1)));
       OQ_HIP(lwc_bwd(prm->W[l], bf, co, C, s, prm->gamma_logit[l], prm->beta_logit[l],
                      d->lin_bits[l], d->lin_group[l], w.dW + off * C, gr->d_gamma_logit[l],
                      gr->d_beta_logit[l], nullptr, p.let ? w.pw + pwo * C : nullptr, st,
