@@ -468,8 +468,15 @@ bool direct_grads(const oq_block_desc* d, const SitePlan& p) {
   if (d->dtype != OQ_BF16) return false;
   const int64_t T = d->tokens;
   bool ok = gemm_mn_supported(false, true, p.M, p.C, T, T, p.C);
-  if (p.let) ok = ok && gemm_mn_supported(true, false, T, p.C, p.M, T, p.M);
+  if (p.let) ok = ok && gemm_mn_supported(true, true, T, p.C, p.M, T, p.C);
   return ok;
+}
+
+// The direct input gradient reads W^ through a transposed copy when the
+// tokens are many enough for the faster product to repay the copy.
+bool direct_wt_copy(const oq_block_desc* d, const SitePlan& p) {
+  return p.let && d->tokens >= 65536 && direct_grads(d, p) &&
+         gemm_mn_supported(true, false, d->tokens, p.C, p.M, d->tokens, p.M);
 }
 
 // K-split count of the weight gradient (its K is the token count); only the
@@ -523,7 +530,7 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
     if (p.let || p.act) xhat = std::max(xhat, size_t(T * p.C));
     if (p.let) {
       if (!direct) dy = std::max(dy, size_t(p.M * T));
-      whatT = std::max(whatT, size_t(p.M * p.C));
+      if (!direct || direct_wt_copy(d, p)) whatT = std::max(whatT, size_t(p.M * p.C));
       dX = std::max(dX, size_t(T * p.C));
       pa = std::max(pa, size_t(act_bwd_nparts(T) * p.C));
       size_t a = 0, b = 0;
@@ -758,17 +765,23 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     }
     // 8. LET: input gradient through Q_a and (X - delta)/s, bias path, finish
     if (p.let) {
-      if (direct) {
+      const bool wt_copy = direct_wt_copy(d, p);
+      if (direct && wt_copy) {
         // dX^ [T, C] = dY W^ with dY read from dY^T [M, T] as stored and W^
         // from a K-contiguous copy W^T [C, M] (its fragments then load as
         // plain 128-bit LDS reads: 3-9% faster than reading W^ as stored, for
-        // a copy of M C bf16)
+        // a copy of M C bf16 that pays off only over many tokens)
         {
           ProfScope ps(PK_TRANSPOSE, st, double(M) * C * 2 * es);
           OQ_HIP(transpose(w.what, M, C, C, w.whatT, M, int(es), st), "transpose W^");
         }
         ProfScope ps(PK_GEMM_DGRAD, st, 2.0 * double(M) * T * C);
         OQ_HIP(gemm_f32out_mn(w.dyT, true, w.whatT, false, T, C, M, T, M, w.dX, C, st),
+               "dgrad gemm");
+      } else if (direct) {
+        // dX^ [T, C] = dY W^ with dY^T [M, T] and W^ [M, C] read as stored
+        ProfScope ps(PK_GEMM_DGRAD, st, 2.0 * double(M) * T * C);
+        OQ_HIP(gemm_f32out_mn(w.dyT, true, w.what, true, T, C, M, T, C, w.dX, C, st),
                "dgrad gemm");
       } else {
         {

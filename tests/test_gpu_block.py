@@ -77,7 +77,9 @@ def oracle_step(w, P):
 @pytest.mark.parametrize("logit", ["init", "random"])
 def test_block_step_parity(w, logit):
     print(f"block step {w.name} T={w.T} logits={logit}", flush=True)
-    P = make_problem(w, seed=3, logit=logit, bias=(w.name == "let_noact"))
+    # biases on a grouped LET workload (let_fold's kernel) and a per-channel
+    # one (the bias folded into the whole-row LWC forward)
+    P = make_problem(w, seed=3, logit=logit, bias=(w.name in ("let_noact", "c3_t256")))
     blk, loss, *_ = run_gpu(w, P)
     ref_loss, ref = oracle_step(w, P)
     tol = TOL_BF16 if w.bf16 else TOL_F32
@@ -103,6 +105,15 @@ FSPLIT = small_llama("fsplit_t64", hidden=2048, ffn=256, T=64, w_bits=4, group=1
 
 def test_block_step_parity_split_forward():
     test_block_step_parity(FSPLIT, "random")
+
+
+# LET + W4A4 over 65,536 tokens: the input gradient reads a transposed copy
+# of W^ (from 65,536 tokens on) and the weight gradients split K in 8
+LONG_LET = small_llama("c3_t65536", hidden=128, ffn=256, T=65536, w_bits=4, let=True, act_bits=4)
+
+
+def test_block_step_parity_long_let():
+    test_block_step_parity(LONG_LET, "init")
 
 
 def test_block_step_is_deterministic():
