@@ -505,64 +505,139 @@ bool fused_lwc(const oq_block_desc* d, const SitePlan& p) {
   return p.l1 - p.l0 <= MAX_SEG && gemm_wgrad_lwc_supported(p.M, p.C, d->tokens, int(g));
 }
 
-size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, char* base,
-                   BlockWs* w) {
+// Side streams (non-blocking, default priority) and fork / join events for
+// concurrent sites: created once per device and host thread, kept for the
+// life of the process.
+constexpr int MAX_SIDE = 3;
+struct SiteStreams {
+  hipStream_t s[MAX_SIDE];
+  hipEvent_t fork, join[MAX_SIDE];
+  bool ok;
+};
+
+hipError_t site_streams(SiteStreams** out) {
+  thread_local SiteStreams cache[16] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 16) return hipErrorInvalidDevice;
+  SiteStreams& c = cache[dev];
+  if (!c.ok) {
+    for (int i = 0; i < MAX_SIDE; ++i) {
+      if ((e = hipStreamCreateWithFlags(&c.s[i], hipStreamNonBlocking)) != hipSuccess) return e;
+      if ((e = hipEventCreateWithFlags(&c.join[i], hipEventDisableTiming)) != hipSuccess) return e;
+    }
+    if ((e = hipEventCreateWithFlags(&c.fork, hipEventDisableTiming)) != hipSuccess) return e;
+    c.ok = true;
+  }
+  *out = &c;
+  return hipSuccess;
+}
+
+// Sites run concurrently (one stream each) at small token counts, where a
+// site's products leave CUs idle in their last wave of tiles; each site then
+// has its own buffers.  At large token counts the sites share one set.
+bool concurrent_sites(const oq_block_desc* d, const std::vector<SitePlan>& plan) {
+  if (plan.size() < 2 || plan.size() > size_t(MAX_SIDE) + 1 || d->dtype != OQ_BF16 ||
+      d->tokens > 16384)
+    return false;
+  // only when every site's forward product is at most four waves of 256 x 256
+  // tiles over 256 CUs: larger concurrent products measured slower (the
+  // 70B block at 2048 tokens, 9%), smaller ones faster (the 7B and 13B, 5-14%)
+  for (const auto& p : plan)
+    if (((p.M + 255) / 256) * ((d->tokens + 255) / 256) > 4 * 256) return false;
+  return true;
+}
+
+// Buffer sizes (elements) one site needs.
+struct SiteSizes {
+  size_t what = 0, xhat = 0, xhatT = 0, dyT = 0, dy = 0, whatT = 0, dW = 0, dX = 0, parts = 0,
+         rows = 0, pw = 0, pa = 0, pb = 0, gs = 0;
+  void max_with(const SiteSizes& o) {
+    what = std::max(what, o.what); xhat = std::max(xhat, o.xhat); xhatT = std::max(xhatT, o.xhatT);
+    dyT = std::max(dyT, o.dyT); dy = std::max(dy, o.dy); whatT = std::max(whatT, o.whatT);
+    dW = std::max(dW, o.dW); dX = std::max(dX, o.dX); parts = std::max(parts, o.parts);
+    rows = std::max(rows, o.rows); pw = std::max(pw, o.pw); pa = std::max(pa, o.pa);
+    pb = std::max(pb, o.pb); gs = std::max(gs, o.gs);
+  }
+};
+
+SiteSizes site_sizes(const oq_block_desc* d, const SitePlan& p) {
   const bool bf = d->dtype == OQ_BF16;
-  const size_t es = bf ? 2 : 4;
   const int64_t T = d->tokens;
   const int ptn = gemm_part_tile_n(bf);
   const int64_t ntn = (T + ptn - 1) / ptn;
-  size_t what = 0, xhat = 0, xhatT = 0, dyT = 0, dy = 0, whatT = 0, dW = 0, dX = 0, parts = 0,
-         rows = 0, pw = 0, pa = 0, pb = 0, gs = 0;
-  int64_t mtot = 0;
-  for (const auto& p : plan) {
-    const bool direct = direct_grads(d, p);
-    what = std::max(what, size_t(p.M * p.C));
-    if (!direct) xhatT = std::max(xhatT, size_t(T * p.C));
-    dyT = std::max(dyT, size_t(p.M * T));
-    dW = std::max(dW, size_t(p.M * p.C) * size_t(wgrad_splits(d, p)));
-    // the split forward's parts live there too (the weight gradient comes later)
-    dW = std::max(dW, size_t(p.M * T) * size_t(fwd_splits(d, p)));
-    if (fused_lwc(d, p)) gs = std::max(gs, size_t(p.M * (p.C / d->lin_group[p.l0])));
-    parts = std::max(parts, size_t(p.M * ntn));
-    rows = std::max(rows, size_t(p.M));
-    mtot += p.M;
-    if (p.let || p.act) xhat = std::max(xhat, size_t(T * p.C));
-    if (p.let) {
-      if (!direct) dy = std::max(dy, size_t(p.M * T));
-      if (!direct || direct_wt_copy(d, p)) whatT = std::max(whatT, size_t(p.M * p.C));
-      dX = std::max(dX, size_t(T * p.C));
-      pa = std::max(pa, size_t(act_bwd_nparts(T) * p.C));
-      size_t a = 0, b = 0;
-      for (int l = p.l0; l < p.l1; ++l) {
-        a += size_t(lwc_bwd_nparts(d->lin_c_out[l]));
-        b += size_t(wcolsum_nparts(d->lin_c_out[l]));
-      }
-      pw = std::max(pw, a * p.C);
-      pb = std::max(pb, b * p.C);
+  const bool direct = direct_grads(d, p);
+  SiteSizes z;
+  z.what = size_t(p.M * p.C);
+  if (!direct) z.xhatT = size_t(T * p.C);
+  z.dyT = size_t(p.M * T);
+  z.dW = size_t(p.M * p.C) * size_t(wgrad_splits(d, p));
+  // the split forward's parts live there too (the weight gradient comes later)
+  z.dW = std::max(z.dW, size_t(p.M * T) * size_t(fwd_splits(d, p)));
+  if (fused_lwc(d, p)) z.gs = size_t(p.M * (p.C / d->lin_group[p.l0]));
+  z.parts = size_t(p.M * ntn);
+  z.rows = size_t(p.M);
+  if (p.let || p.act) z.xhat = size_t(T * p.C);
+  if (p.let) {
+    if (!direct) z.dy = size_t(p.M * T);
+    if (!direct || direct_wt_copy(d, p)) z.whatT = size_t(p.M * p.C);
+    z.dX = size_t(T * p.C);
+    z.pa = size_t(act_bwd_nparts(T) * p.C);
+    size_t a = 0, b = 0;
+    for (int l = p.l0; l < p.l1; ++l) {
+      a += size_t(lwc_bwd_nparts(d->lin_c_out[l]));
+      b += size_t(wcolsum_nparts(d->lin_c_out[l]));
     }
+    z.pw = a * p.C;
+    z.pb = b * p.C;
   }
-  Carver cv{base};
+  return z;
+}
+
+BlockWs carve_set(Carver& cv, const SiteSizes& z, size_t es) {
   BlockWs t{};
-  t.what = cv.take<char>(what * es);
-  t.xhat = xhat ? cv.take<char>(xhat * es) : nullptr;
-  t.xhatT = xhatT ? cv.take<char>(xhatT * es) : nullptr;
-  t.dyT = cv.take<char>(dyT * es);
-  t.dy = dy ? cv.take<char>(dy * es) : nullptr;
-  t.whatT = whatT ? cv.take<char>(whatT * es) : nullptr;
-  t.dW = cv.take<float>(dW);
-  t.dX = dX ? cv.take<float>(dX) : nullptr;
-  t.psq = cv.take<float>(parts);
-  t.pdy = cv.take<float>(parts);
-  t.dbt = cv.take<float>(rows);
-  t.bt = cv.take<float>(rows);
-  t.pw = pw ? cv.take<float>(pw) : nullptr;
-  t.psx = pa ? cv.take<float>(pa) : nullptr;
-  t.ps1 = pa ? cv.take<float>(pa) : nullptr;
-  t.pb = pb ? cv.take<float>(pb) : nullptr;
-  t.rl = cv.take<double>(size_t(mtot));
-  t.gstat = gs ? cv.take<float4>(gs) : nullptr;
-  if (w) *w = t;
+  t.what = cv.take<char>(z.what * es);
+  t.xhat = z.xhat ? cv.take<char>(z.xhat * es) : nullptr;
+  t.xhatT = z.xhatT ? cv.take<char>(z.xhatT * es) : nullptr;
+  t.dyT = cv.take<char>(z.dyT * es);
+  t.dy = z.dy ? cv.take<char>(z.dy * es) : nullptr;
+  t.whatT = z.whatT ? cv.take<char>(z.whatT * es) : nullptr;
+  t.dW = cv.take<float>(z.dW);
+  t.dX = z.dX ? cv.take<float>(z.dX) : nullptr;
+  t.psq = cv.take<float>(z.parts);
+  t.pdy = cv.take<float>(z.parts);
+  t.dbt = cv.take<float>(z.rows);
+  t.bt = cv.take<float>(z.rows);
+  t.pw = z.pw ? cv.take<float>(z.pw) : nullptr;
+  t.psx = z.pa ? cv.take<float>(z.pa) : nullptr;
+  t.ps1 = z.pa ? cv.take<float>(z.pa) : nullptr;
+  t.pb = z.pb ? cv.take<float>(z.pb) : nullptr;
+  t.gstat = z.gs ? cv.take<float4>(z.gs) : nullptr;
+  return t;
+}
+
+// Workspace layout: one buffer set per site when the sites run concurrently,
+// else one set sized for the largest site; the row losses (fp64, every row
+// of the block) after them.  w (one entry per site) may be null.
+size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, char* base,
+                   std::vector<BlockWs>* w) {
+  const size_t es = d->dtype == OQ_BF16 ? 2 : 4;
+  int64_t mtot = 0;
+  for (const auto& p : plan) mtot += p.M;
+  Carver cv{base};
+  std::vector<BlockWs> sets;
+  if (concurrent_sites(d, plan)) {
+    for (const auto& p : plan) sets.push_back(carve_set(cv, site_sizes(d, p), es));
+  } else {
+    SiteSizes z;
+    for (const auto& p : plan) z.max_with(site_sizes(d, p));
+    const BlockWs t = carve_set(cv, z, es);
+    sets.assign(plan.size(), t);
+  }
+  double* rl = cv.take<double>(size_t(mtot));
+  for (auto& t : sets) t.rl = rl;
+  if (w) *w = sets;
   return cv.off + 256;
 }
 
@@ -580,7 +655,7 @@ oq_status oq_block_workspace_size(const oq_block_desc* desc, size_t* bytes) {
 oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
                               const void* const* X_q, const oq_block_params* prm,
                               const oq_block_grads* gr, const oq_block_optim* opt, float* loss,
-                              void* ws, size_t ws_bytes, hipStream_t st) {
+                              void* ws, size_t ws_bytes, hipStream_t st0) {
   std::vector<SitePlan> plan;
   oq_status e = plan_block(d, plan);
   if (e != OQ_OK) return e;
@@ -612,8 +687,18 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
   const size_t need = carve_block(d, plan, nullptr, nullptr);
   if (!ws || ws_bytes < need)
     return fail(OQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
-  BlockWs w;
-  carve_block(d, plan, static_cast<char*>(ws), &w);
+  std::vector<BlockWs> wsets;
+  carve_block(d, plan, static_cast<char*>(ws), &wsets);
+  // concurrent sites: site 0 on the caller's stream, the others on side
+  // streams forked from it here and joined before the loss
+  const bool conc = concurrent_sites(d, plan);
+  SiteStreams* ss = nullptr;
+  if (conc) {
+    OQ_HIP(site_streams(&ss), "site streams");
+    OQ_HIP(hipEventRecord(ss->fork, st0), "fork");
+    for (size_t i = 1; i < plan.size(); ++i)
+      OQ_HIP(hipStreamWaitEvent(ss->s[i - 1], ss->fork, 0), "fork");
+  }
 
   const bool bf = d->dtype == OQ_BF16;
   const size_t es = bf ? 2 : 4;
@@ -624,7 +709,10 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
   LossArgs la{};
   la.nlin = d->n_linears;
 
-  for (const auto& p : plan) {
+  for (size_t si = 0; si < plan.size(); ++si) {
+    const SitePlan& p = plan[si];
+    hipStream_t st = conc && si > 0 ? ss->s[si - 1] : st0;
+    const BlockWs& w = wsets[si];
     const int k = p.k;
     const int64_t C = p.C, M = p.M;
     const float* s = p.let ? prm->s[k] : nullptr;
@@ -813,9 +901,16 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     }
     row_base += M;
   }
+  if (conc) {
+    for (size_t i = 1; i < plan.size(); ++i) {
+      OQ_HIP(hipEventRecord(ss->join[i - 1], ss->s[i - 1]), "join");
+      OQ_HIP(hipStreamWaitEvent(st0, ss->join[i - 1], 0), "join");
+    }
+  }
+  hipStream_t st = st0;
   {
     ProfScope ps(PK_OTHER, st, double(row_base) * 8);
-    OQ_HIP(loss_finish(w.rl, la, loss, st), "loss");
+    OQ_HIP(loss_finish(wsets[0].rl, la, loss, st), "loss");
   }
   if (opt) {
     const AdamCoef cl = adam_coef(opt->lr_lwc, opt->beta1, opt->beta2, opt->eps, opt->wd, opt->step);
