@@ -197,6 +197,15 @@ oq_status oq_adamw_step(float* p, const float* g, float* m, float* v, int64_t n,
  * must be consecutive.  LET (s, delta) applies per site; per-token
  * activation fake-quant applies to a site's input when site_act_bits < 16.
  * Loss = sum over linears of mean((Y_l - Y_fp,l)^2), Y_l = Q_a(X~) Q_w(W~)^T + B~.
+ *
+ * Ordering: the step is ordered on `stream` like a single launch.  At small
+ * token counts (bf16, T <= 16384, every site's forward product within four
+ * waves of 256 x 256 tiles, at most 4 sites) sites 1.. run on side streams
+ * forked from `stream` with an event and joined back to it before the loss.
+ * The side streams (non-blocking, default priority) and their events are
+ * created on first use, once per device and host thread, and kept; each site
+ * then has its own part of the workspace, so calls must not share one
+ * workspace concurrently.
  */
 #define OQ_MAX_SITES 8
 #define OQ_MAX_LINEARS 16
