@@ -573,8 +573,9 @@ SiteSizes site_sizes(const oq_block_desc* d, const SitePlan& p) {
   if (!direct) z.xhatT = size_t(T * p.C);
   z.dyT = size_t(p.M * T);
   z.dW = size_t(p.M * p.C) * size_t(wgrad_splits(d, p));
-  // the split forward's parts live there too (the weight gradient comes later)
-  z.dW = std::max(z.dW, size_t(p.M * T) * size_t(fwd_splits(d, p)));
+  // a split forward's parts live there too (the weight gradient comes later)
+  const int sf = fwd_splits(d, p);
+  if (sf > 1) z.dW = std::max(z.dW, size_t(p.M * T) * size_t(sf));
   if (fused_lwc(d, p)) z.gs = size_t(p.M * (p.C / d->lin_group[p.l0]));
   z.parts = size_t(p.M * ntn);
   z.rows = size_t(p.M);
