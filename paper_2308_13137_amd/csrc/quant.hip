@@ -741,13 +741,39 @@ __global__ __launch_bounds__(NT) void act_fwd_row_kernel(
   const int64_t nw = int64_t(gridDim.x) * (NT / 64);
   const bool quant = bits < 16;
   const float qmax = quant ? float((1 << bits) - 1) : 0.0f;
-  for (int64_t row = int64_t(blockIdx.x) * (NT / 64) + (threadIdx.x >> 6); row < T; row += nw) {
+  // rows of up to 8 chunks per lane: the wave's next row is loaded while this
+  // one is reduced and quantised
+  constexpr bool PF = CH <= 8;
+  Chunk8<TX> nxt[PF ? CH : 1];
+  const int64_t row0 = int64_t(blockIdx.x) * (NT / 64) + (threadIdx.x >> 6);
+  if constexpr (PF) {
+    if (row0 < T) {
+#pragma unroll
+      for (int k = 0; k < CH; ++k) {
+        const int j = lane + 64 * k;
+        if (j < nch) nxt[k].load(X + row0 * C + 8 * j);
+      }
+    }
+  }
+  for (int64_t row = row0; row < T; row += nw) {
     const TX* xr = X + row * C;
     Chunk8<TX> raw[CH];
+    if constexpr (PF) {
 #pragma unroll
-    for (int k = 0; k < CH; ++k) {
-      const int j = lane + 64 * k;
-      if (j < nch) raw[k].load(xr + 8 * j);
+      for (int k = 0; k < CH; ++k) raw[k] = nxt[k];
+      if (row + nw < T) {
+#pragma unroll
+        for (int k = 0; k < CH; ++k) {
+          const int j = lane + 64 * k;
+          if (j < nch) nxt[k].load(X + (row + nw) * C + 8 * j);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < CH; ++k) {
+        const int j = lane + 64 * k;
+        if (j < nch) raw[k].load(xr + 8 * j);
+      }
     }
     // x~ = (x - delta) (1/s), one rounding per operation
     auto xt8 = [&](int k, float (&o)[8]) {
