@@ -23,4 +23,6 @@ Modules
   block      one block step over the block's linear sub-graph (Eq.1, Eq.4, Alg.1)
   adamw      the AdamW update (Sec. 4.1 training settings)
   surrogate  fp64 frozen-selection surrogate of the step, for finite differences
+  packed     low-bit code storage and the weight-only quantised linear of
+             the deployed model (Sec. 4.5)
 """
