@@ -10,6 +10,7 @@ in HBM before the timed region; the full-precision targets are produced once
 before timing, as Algorithm 1 does once per block.
 
     python bench.py [--steps K] [--warmup W] [--config NAME] [--tokens T]
+    python bench.py --decode [--decode-bits B] [--decode-tokens N]   (deployment workload)
 
 Prints one JSON line.  ``roofline`` describes the dominant kernel kind,
 timed with HIP events on the launching stream during the timed steps;
@@ -194,6 +195,148 @@ def cpu_baseline(w, tokens):
                       f"every weight, fp64 products) at {tokens} tokens, {dt:.1f} s"}
 
 
+# The deployment workload (Sec. 4.5, Table "tab:speed"): one decoded token
+# through the linears of all 32 LLaMA-7B blocks, weights stored as packed
+# low-bit codes.  Linears that read the same input are stacked (q,k,v and
+# gate,up), as a deployment would: 4 launches per block.
+DECODE_BLOCKS = 32
+DECODE_LINEARS = (("qkv", 3 * 4096, 4096), ("o", 4096, 4096), ("gate_up", 2 * 11008, 4096),
+                  ("down", 4096, 11008))
+
+
+def decode_inputs(bits, group, n_blocks, n_tok, device="cuda"):
+    """Seeded random packed codes (every code value equally likely), step
+    sizes, zero points and activations, distinct for every block so that no
+    block's weights are cached when the next one is read."""
+    import torch
+
+    from paper_2308_13137_amd import inputs
+    gen = torch.Generator(device=device)
+    gen.manual_seed(inputs.SEED + 5)
+    lins = []
+    for _ in range(n_blocks):
+        for name, c_out, c_in in DECODE_LINEARS:
+            P = torch.randint(0, 256, (c_out, c_in * bits // 8), generator=gen, device=device,
+                              dtype=torch.uint8)
+            h = torch.rand((c_out, c_in // group), generator=gen, device=device) * 0.02 + 1e-3
+            z = torch.randint(0, 2 ** bits, (c_out, c_in // group), generator=gen,
+                              device=device).float()
+            lins.append((name, c_in, P, h, z))
+    X = {c_in: inputs.torch_activations(gen, n_tok, c_in, dtype=torch.bfloat16, device=device)
+         .contiguous() for c_in in {c for _, _, c in DECODE_LINEARS}}
+    return lins, X
+
+
+def decode_cpu_baseline(bits, group):
+    """The oracle's packed linear on the first eighth of the rows of one
+    block's four stacked linears, one token; rows are independent, so the
+    time scales by 8 to the block and by the block count to the model."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle.packed import packed_linear
+    rng = np.random.default_rng(5)
+    dt = 0.0
+    for name, c_out, c_in in DECODE_LINEARS:
+        rows = c_out // 8
+        P = rng.integers(0, 256, size=(rows, c_in * bits // 8), dtype=np.uint8)
+        h = rng.uniform(1e-3, 2.1e-2, size=(rows, c_in // group)).astype(np.float32)
+        z = rng.integers(0, 2 ** bits, size=(rows, c_in // group)).astype(np.float32)
+        x = rng.standard_normal((1, c_in))
+        t0 = time.perf_counter()
+        packed_linear(x, P, bits, group, h, z)
+        dt += time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": float(f"{1.0 / (8 * dt * DECODE_BLOCKS):.4g}"), "unit": "decoded tokens/s",
+            "cores": threads, "kind": "oracle",
+            "sample": f"one eighth of the rows of one block's four stacked linears, one token "
+                      f"({dt:.1f} s), scaled by 8 x {DECODE_BLOCKS} blocks"}
+
+
+def bench_decode(args):
+    import torch
+
+    from paper_2308_13137_amd import oq
+    bits, group, n_tok = args.decode_bits, args.decode_group, args.decode_tokens
+    torch.cuda.set_device(0)
+    oq.lib()
+    name = f"llama7b_w{bits}a16_g{group}_decode"
+    log(f"[bench] {name}: {DECODE_BLOCKS} blocks x {len(DECODE_LINEARS)} stacked linears, "
+        f"{n_tok} token(s) per step")
+    lins, X = decode_inputs(bits, group, DECODE_BLOCKS, n_tok)
+    outs = [torch.empty((n_tok, P.shape[0]), dtype=torch.float32, device="cuda")
+            for _, _, P, _, _ in lins]
+
+    def step():
+        for (nm, c_in, P, h, z), y in zip(lins, outs):
+            oq.packed_linear_into(X[c_in], P, bits, group, h, z, y)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    # kernel durations: eager steps, each launch bracketed by HIP events on its stream
+    oq.profile_reset()
+    oq.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    oq.profile_enable(False)
+    n, kms, work = oq.profile_read()["packed_linear"]
+    eager_ms = (t1 - t0) * 1e3 / args.steps
+    # step time: a decode loop launches the same kernels for every token, so
+    # the step is captured once in a HIP graph and replayed
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms = (t1 - t0) * 1e3 / args.steps
+    achieved = work / n / (kms / n / 1e3) / 1e9
+    weight_bytes = sum(P.numel() + 8 * h.numel() for _, _, P, h, _ in lins)
+    line = {
+        "metric": "decoded tokens/s through the block linears (packed weights)",
+        "value": round(n_tok / (ms / 1e3), 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "eager_ms_per_step": round(eager_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": name, "blocks": DECODE_BLOCKS, "tokens_per_step": n_tok,
+                   "w_bits": bits, "group": group, "weight_bytes": weight_bytes,
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "kernel": "packed_linear", "achieved": round(achieved, 1),
+                     "peak": PEAK["hbm_gbs"], "unit": "GB/s",
+                     "frac": round(achieved / PEAK["hbm_gbs"], 4),
+                     "avg_launch_ms": round(kms / n, 5), "traffic": None},
+        "kernels": {"packed_linear": {"launches_per_step": n / args.steps,
+                                      "ms_per_step": round(kms / args.steps, 4),
+                                      "gbs": round(achieved, 1)}},
+    }
+    del lins, X, outs
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log("[bench] CPU oracle on one block")
+        line["cpu_baseline"] = decode_cpu_baseline(bits, group)
+    else:
+        line["cpu_baseline"] = None
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -210,7 +353,16 @@ def main():
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CMD_FETCH",
                                                              "CMD_WRITE"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc passes")
+    ap.add_argument("--decode", action="store_true",
+                    help="time the deployment workload instead: packed-weight linears of "
+                         "all 32 LLaMA-7B blocks for one decoded token per step")
+    ap.add_argument("--decode-bits", type=int, default=4)
+    ap.add_argument("--decode-group", type=int, default=128)
+    ap.add_argument("--decode-tokens", type=int, default=1)
     args = ap.parse_args()
+    if args.decode and args.gpus == 1:
+        bench_decode(args)
+        return
     if args.summarize_traffic:
         w = args.config if not args.tokens else f"{args.config}_t{args.tokens}"
         summarize_traffic(*args.summarize_traffic[:2], w, *args.summarize_traffic[2:])

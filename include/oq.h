@@ -264,14 +264,50 @@ oq_status oq_block_calib_step(const oq_block_desc* desc, const void* const* Y_fp
                               float* loss, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * Deployment of the calibrated weights (Sec. 4.5 and Table "tab:speed":
+ * weight-only WxA16 models whose weights are stored as Eq.2's integer codes
+ * W_q with one step size h and zero point z per group).
+ *
+ * oq_pack_codes: codes [c_out, c_in] u8 -> packed [c_out, c_in * bits / 8] u8,
+ * both device memory owned by the caller.  Row o's codes form one
+ * little-endian bit string: code j occupies bits j*bits .. j*bits + bits - 1,
+ * and bit k of the string is bit (k mod 8) of byte k / 8; rows follow each
+ * other.  Only the low `bits` bits of each code are stored.
+ * Supported: bits 2..8 (else OQ_ERR_UNSUPPORTED); c_in % 32 == 0; both
+ * pointers 16-byte aligned (else OQ_ERR_INVALID_ARG).  c_out == 0 is a no-op
+ * that accepts NULL pointers.
+ */
+oq_status oq_pack_codes(const uint8_t* codes, int64_t c_out, int64_t c_in, int bits,
+                        uint8_t* packed, hipStream_t stream);
+
+/* oq_packed_linear: Y = X W^T + B with W[o, c] = (q[o, c] - z[o, g]) * h[o, g],
+ * g = c / group, the dequantisation of Eq.2, q read from `packed`.
+ *   X      : bf16 [n_tok, c_in] (x_dt must be OQ_BF16, else OQ_ERR_UNSUPPORTED)
+ *   packed : u8 [c_out, c_in * bits / 8] in the oq_pack_codes layout
+ *   h, z   : fp32 [c_out, c_in / group], as oq_lwc_fakequant_fwd writes them
+ *   B      : fp32 [c_out] | NULL
+ *   Y      : [n_tok, c_out] in y_dt (fp32 or bf16), overwritten
+ * Supported: bits 2..7 and c_in <= 65536 (else OQ_ERR_UNSUPPORTED); c_in % 32
+ * == 0; group % 32 == 0 dividing c_in; every pointer 16-byte aligned (else
+ * OQ_ERR_INVALID_ARG).  Any n_tok >= 0: the kernel is sized for decoding, one
+ * launch per 8 tokens, each reading the packed weights once; n_tok == 0 or
+ * c_out == 0 is a no-op that accepts NULL pointers.  Products and sums are
+ * fp32 in a fixed order, so results are reproducible.
+ */
+oq_status oq_packed_linear(const void* X, oq_dtype x_dt, int64_t n_tok, int64_t c_in,
+                           const uint8_t* packed, int bits, int64_t group, const float* h,
+                           const float* z, const float* B, int64_t c_out, void* Y,
+                           oq_dtype y_dt, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Kernel timing on the launching stream (HIP events around each launch).
  * Kinds: 0 forward GEMM, 1 weight-gradient GEMM, 2 input-gradient GEMM,
  * 3 LWC forward, 4 LWC backward, 5 activation quant forward, 6 activation
- * quant backward, 7 transposes, 8 other.  oq_profile_read synchronises the
+ * quant backward, 7 transposes, 8 other, 9 the packed linear.  oq_profile_read synchronises the
  * recorded events and returns launch count, total milliseconds and the
  * algorithmic work (FLOP for GEMMs, bytes for the others) of that kind.
  */
-#define OQ_PROF_KINDS 9
+#define OQ_PROF_KINDS 10
 oq_status oq_profile_enable(int on);
 oq_status oq_profile_reset(void);
 oq_status oq_profile_read(int kind, int64_t* launches, double* total_ms, double* work);

@@ -17,7 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "liboq.so")
-SOURCES = ["gemm.hip", "quant.hip", "misc.hip", "api.hip"]
+SOURCES = ["gemm.hip", "quant.hip", "misc.hip", "packed.hip", "api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

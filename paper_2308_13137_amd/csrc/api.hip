@@ -11,6 +11,7 @@
 
 #include "oq.h"
 #include "oq_internal.h"
+#include "packed.h"
 
 namespace {
 
@@ -389,6 +390,47 @@ oq_status oq_matmul(const void* A, int a_mn, const void* B, int b_mn, int64_t M,
   if (!gemm_mn_supported(a_mn != 0, b_mn != 0, M, N, K, lda, ldb))
     return fail(OQ_ERR_UNSUPPORTED, "MN-major operand needs K %% 64 == 0 and M, N %% 8 == 0");
   OQ_HIP(gemm_f32out_mn(A, a_mn != 0, B, b_mn != 0, M, N, K, lda, ldb, C, N, stream), "matmul");
+  return OQ_OK;
+}
+
+oq_status oq_pack_codes(const uint8_t* codes, int64_t c_out, int64_t c_in, int bits,
+                        uint8_t* packed, hipStream_t stream) {
+  OQ_REQ(c_out >= 0 && c_in > 0 && c_in % 32 == 0, "bad shape c_out=%lld c_in=%lld (need c_in %% 32 == 0)",
+         (long long)c_out, (long long)c_in);
+  if (bits < 2 || bits > 8) return fail(OQ_ERR_UNSUPPORTED, "bits=%d (need 2..8)", bits);
+  if (c_out == 0) return OQ_OK;                   // empty: pointers may be NULL
+  OQ_REQ(codes && packed, "codes and packed are required");
+  OQ_REQ(aligned16(codes) && aligned16(packed), "pointers must be 16-byte aligned");
+  ProfScope ps(PK_OTHER, stream, double(c_out) * c_in * (1.0 + bits / 8.0));
+  OQ_HIP(pack_codes(codes, c_out, c_in, bits, packed, stream), "pack_codes");
+  return OQ_OK;
+}
+
+oq_status oq_packed_linear(const void* X, oq_dtype x_dt, int64_t n_tok, int64_t c_in,
+                           const uint8_t* packed, int bits, int64_t group, const float* h,
+                           const float* z, const float* B, int64_t c_out, void* Y,
+                           oq_dtype y_dt, hipStream_t stream) {
+  if (x_dt != OQ_BF16) return fail(OQ_ERR_UNSUPPORTED, "the packed linear takes bf16 activations");
+  OQ_REQ(dtype_ok(y_dt), "bad Y dtype");
+  OQ_REQ(n_tok >= 0 && c_out >= 0 && c_in > 0 && c_in % 32 == 0,
+         "bad shape n_tok=%lld c_in=%lld c_out=%lld (need c_in %% 32 == 0)", (long long)n_tok,
+         (long long)c_in, (long long)c_out);
+  OQ_REQ(group > 0 && group % 32 == 0 && c_in % group == 0,
+         "group=%lld must be a multiple of 32 that divides c_in=%lld", (long long)group, (long long)c_in);
+  if (bits < 2 || bits > 7) return fail(OQ_ERR_UNSUPPORTED, "bits=%d (need 2..7)", bits);
+  if (c_in > PACKED_MAX_C_IN)
+    return fail(OQ_ERR_UNSUPPORTED, "c_in=%lld > %lld", (long long)c_in, (long long)PACKED_MAX_C_IN);
+  if (n_tok == 0 || c_out == 0) return OQ_OK;     // empty: pointers may be NULL
+  OQ_REQ(X && packed && h && z && Y, "X, packed, h, z and Y are required");
+  OQ_REQ(aligned16(X) && aligned16(packed) && aligned16(h) && aligned16(z) && (!B || aligned16(B)) &&
+             aligned16(Y),
+         "pointers must be 16-byte aligned");
+  const double bytes = double(c_out) * c_in * bits / 8.0 + double(c_out) * (c_in / group) * 8.0 +
+                       double(n_tok) * (2.0 * c_in + double(esize(y_dt)) * c_out) + (B ? 4.0 * c_out : 0.0);
+  ProfScope ps(PK_PACKED_LINEAR, stream, bytes);
+  OQ_HIP(packed_linear(static_cast<const uint16_t*>(X), n_tok, c_in, packed, bits, group, h, z, B, c_out,
+                       Y, y_dt == OQ_BF16, stream),
+         "packed_linear");
   return OQ_OK;
 }
 

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_HERE, "liboq.so")
 OQ_F32, OQ_BF16 = 0, 1
 MAX_SITES, MAX_LINEARS = 8, 16
 PROF_KINDS = ["gemm_fwd", "gemm_wgrad", "gemm_dgrad", "lwc_fwd", "lwc_bwd", "act_fwd",
-              "act_bwd", "transpose", "other"]
+              "act_bwd", "transpose", "other", "packed_linear"]
 
 # name -> (restype, argtypes); the exported surface of include/oq.h
 _P, _I64, _I, _D, _SZ = C.c_void_p, C.c_int64, C.c_int, C.c_double, C.c_size_t
@@ -42,6 +42,8 @@ SIGNATURES = {
     "oq_adamw_step": (_I, [_P, _P, _P, _P, _I64, _D, _D, _D, _D, _D, _I, _P]),
     "oq_block_workspace_size": (_I, [_P, _PSZ]),
     "oq_block_calib_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "oq_pack_codes": (_I, [_P, _I64, _I64, _I, _P, _P]),
+    "oq_packed_linear": (_I, [_P, _I, _I64, _I64, _P, _I, _I64, _P, _P, _P, _I64, _P, _I, _P]),
     "oq_profile_enable": (_I, [_I]),
     "oq_profile_reset": (_I, []),
     "oq_profile_read": (_I, [_I, C.POINTER(C.c_int64), C.POINTER(C.c_double),
@@ -239,6 +241,39 @@ def let_init(X, Ws, stream=None):
     _check(lib().oq_let_init(_ptr(X), _dt(X), T, Cw, ptrs, couts, len(Ws), _dt(Ws[0]), _ptr(s),
                              _ptr(d), _ptr(ws), ws.numel(), _stream(stream)))
     return s, d
+
+
+def pack_codes(codes, bits, stream=None):
+    """Row-wise low-bit strings of integer codes ([c_out, c_in] uint8).
+    Returns packed uint8 [c_out, c_in * bits // 8]."""
+    if codes.dtype != torch.uint8:
+        raise OQError("codes must be uint8")
+    c_out, c_in = codes.shape
+    packed = torch.empty((c_out, c_in * bits // 8), dtype=torch.uint8, device=codes.device)
+    _check(lib().oq_pack_codes(_ptr(codes), c_out, c_in, bits, _ptr(packed), _stream(stream)))
+    return packed
+
+
+def packed_linear(X, packed, bits, group, h, z, B=None, out_dtype=torch.float32, stream=None):
+    """Y = X W^T + B with W the dequantised weight of packed codes ([n_tok, c_out])."""
+    n_tok, c_in = X.shape
+    c_out = packed.shape[0]
+    if packed.dtype != torch.uint8 or packed.shape[1] * 8 != c_in * bits:
+        raise OQError("packed must be uint8 [c_out, c_in * bits / 8]")
+    Y = torch.empty((n_tok, c_out), dtype=out_dtype, device=X.device)
+    _check(lib().oq_packed_linear(_ptr(X), _dt(X), n_tok, c_in, _ptr(packed), bits, group,
+                                  _ptr(_f32(h, "h")), _ptr(_f32(z, "z")), _ptr(_f32(B, "B")),
+                                  c_out, _ptr(Y), _dt(Y), _stream(stream)))
+    return Y
+
+
+def packed_linear_into(X, packed, bits, group, h, z, Y, B=None, stream=None):
+    """:func:`packed_linear` writing into an existing ``Y`` [n_tok, c_out]."""
+    n_tok, c_in = X.shape
+    _check(lib().oq_packed_linear(_ptr(X), _dt(X), n_tok, c_in, _ptr(packed), bits, group,
+                                  _ptr(_f32(h, "h")), _ptr(_f32(z, "z")), _ptr(_f32(B, "B")),
+                                  packed.shape[0], _ptr(Y), _dt(Y), _stream(stream)))
+    return Y
 
 
 def fp_target(X, W, B=None, stream=None):

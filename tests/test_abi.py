@@ -83,6 +83,31 @@ def test_act_rejects():
                                   FAKE, None, 0, None) == WORKSPACE
 
 
+def test_packed_rejects():
+    L = oq.lib()
+    # pack: bits, shape, alignment
+    assert L.oq_pack_codes(FAKE, 4, 64, 9, FAKE, None) == UNSUPPORTED
+    assert L.oq_pack_codes(FAKE, 4, 48, 4, FAKE, None) == INVALID
+    assert L.oq_pack_codes(MISALIGNED, 4, 64, 4, FAKE, None) == INVALID
+    assert L.oq_pack_codes(None, 4, 64, 4, FAKE, None) == INVALID
+
+    def lin(**kw):
+        a = dict(X=FAKE, x_dt=oq.OQ_BF16, n_tok=1, c_in=256, P=FAKE, bits=4, group=128, h=FAKE,
+                 z=FAKE, B=None, c_out=64, Y=FAKE, y_dt=oq.OQ_F32, st=None)
+        a.update(kw)
+        return L.oq_packed_linear(*a.values())
+
+    assert lin(x_dt=oq.OQ_F32) == UNSUPPORTED
+    assert lin(bits=8) == UNSUPPORTED and lin(bits=1) == UNSUPPORTED
+    assert lin(c_in=131072, group=128) == UNSUPPORTED
+    assert lin(c_in=240, group=48) == INVALID          # c_in % 32
+    assert lin(group=96) == INVALID                     # does not divide 256
+    assert lin(group=16, c_in=256) == INVALID           # not a multiple of 32
+    assert lin(h=None) == INVALID and lin(z=MISALIGNED) == INVALID
+    assert lin(n_tok=-1) == INVALID and lin(y_dt=5) == INVALID
+    assert oq.lib().oq_last_error()
+
+
 def _desc(w):
     d = oq.BlockDesc()
     d.tokens = w.T

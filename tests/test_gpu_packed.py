@@ -1,0 +1,167 @@
+"""Parity of the deployment kernels (Sec. 4.5) with the oracle: the packed code
+layout bit for bit, and the weight-only quantised linear element by element
+within a bound derived from its fp32 arithmetic.
+
+Bound of the linear.  The kernel forms, per run of 32 codes, p = sum x (128 + q)
+with bf16 x and exact bf16 codes (every product exact in fp32), then
+h * (p - (128 + z) * xs) with xs = sum x, and sums runs and lanes in fp32.  Each
+of the at most ~40 roundings on the way contributes at most 2^-24 times a
+partial sum bounded by sum_c |x_c| (256 + q_c + |z_g|) h_g, so
+|Y - Y_oracle| <= 4e-6 * sum_c |x_c| (256 + q_c + |z_g|) h_g, plus half a bf16
+ulp of |Y| when Y is stored in bf16."""
+import numpy as np
+import pytest
+import torch
+
+from oracle.packed import pack_codes as o_pack
+from oracle.packed import packed_linear as o_linear
+from oracle.quant import bf16_round
+from paper_2308_13137_amd import oq
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def make_linear(seed, bits, n_tok, c_out, c_in, group, bias, z_spread=0):
+    rng = np.random.default_rng(seed)
+    q = rng.integers(0, 2 ** bits, size=(c_out, c_in), dtype=np.uint8)
+    ng = c_in // group
+    h = rng.uniform(1e-3, 2e-2, size=(c_out, ng)).astype(np.float32)
+    z = rng.integers(-z_spread, 2 ** bits + z_spread, size=(c_out, ng)).astype(np.float32)
+    X = rng.standard_normal((n_tok, c_in)).astype(np.float32)
+    heavy = rng.choice(c_in, size=max(1, c_in // 100), replace=False)
+    X[:, heavy] *= 10.0                               # a few outlier channels
+    X = bf16_round(X)
+    B = rng.standard_normal(c_out).astype(np.float32) if bias else None
+    return q, h, z, X, B
+
+
+def bound(q, h, z, X, group):
+    mag = (256.0 + q.astype(np.float64) + np.repeat(np.abs(z), group, axis=1)) * np.repeat(h, group, axis=1)
+    return 4e-6 * (np.abs(X).astype(np.float64) @ mag.T)
+
+
+def to_dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    return t if dtype is None else t.to(dtype)
+
+
+@pytest.mark.parametrize("bits,c_out,c_in", [
+    (2, 3, 32), (3, 5, 96), (4, 64, 4096), (5, 7, 160), (6, 33, 224), (7, 2, 32), (8, 17, 256),
+    (3, 129, 11008), (2, 0, 64),
+])
+def test_pack_codes_bit_exact(bits, c_out, c_in):
+    rng = np.random.default_rng(bits * 1000 + c_in)
+    codes = rng.integers(0, 2 ** bits, size=(c_out, c_in), dtype=np.uint8)
+    got = oq.pack_codes(to_dev(codes), bits).cpu().numpy()
+    assert got.shape == (c_out, c_in * bits // 8)
+    assert np.array_equal(got, o_pack(codes, bits))
+
+
+LINEAR = [
+    # bits, n_tok, c_out, c_in, group, bias, out dtype, z outside [0, qmax]
+    (4, 1, 4096, 4096, 128, False, torch.float32, 0),     # 7B q/k/v/o shape
+    (4, 1, 1000, 11008, 128, True, torch.float32, 0),     # down_proj width, ragged rows
+    (3, 1, 333, 4096, 128, False, torch.float32, 0),
+    (2, 1, 257, 4096, 64, False, torch.float32, 0),
+    (4, 3, 129, 512, 32, True, torch.bfloat16, 2),
+    (4, 8, 100, 4096, 128, False, torch.float32, 0),
+    (4, 13, 50, 1024, 1024, True, torch.float32, 0),      # 8 + 5 tokens, one group per row
+    (2, 8, 64, 11008, 128, False, torch.float32, 0),      # 8 tokens of 11008 exceed LDS: 4 + 4
+    (5, 2, 40, 96, 32, False, torch.float32, 3),
+    (6, 5, 40, 160, 32, True, torch.float32, 0),
+    (7, 4, 17, 224, 32, False, torch.bfloat16, 0),
+    (3, 6, 1, 32, 32, True, torch.float32, 1),
+]
+
+
+@pytest.mark.parametrize("case", LINEAR, ids=[f"b{c[0]}_t{c[1]}_{c[2]}x{c[3]}_g{c[4]}" for c in LINEAR])
+def test_packed_linear_matches_oracle(case):
+    bits, n_tok, c_out, c_in, group, bias, odt, zs = case
+    q, h, z, X, B = make_linear(100 + LINEAR.index(case), bits, n_tok, c_out, c_in, group, bias, zs)
+    P = o_pack(q, bits)
+    ref = o_linear(X, P, bits, group, h, z, B)
+    Y = oq.packed_linear(to_dev(X, torch.bfloat16), to_dev(P), bits, group, to_dev(h), to_dev(z),
+                         None if B is None else to_dev(B), out_dtype=odt)
+    torch.cuda.synchronize()
+    got = Y.float().cpu().numpy().astype(np.float64)
+    tol = bound(q, h, z, X, group)
+    if odt == torch.bfloat16:
+        tol = tol + np.abs(ref) * 2.0 ** -8
+    err = np.abs(got - ref)
+    assert np.all(err <= tol), (err.max(), (err / tol).max())
+
+
+def test_packed_linear_empty_and_reproducible():
+    q, h, z, X, _ = make_linear(9, 4, 5, 300, 4096, 128, False)
+    Xd, Pd, hd, zd = to_dev(X, torch.bfloat16), to_dev(o_pack(q, 4)), to_dev(h), to_dev(z)
+    assert oq.packed_linear(Xd[:0], Pd, 4, 128, hd, zd).shape == (0, 300)
+    a = oq.packed_linear(Xd, Pd, 4, 128, hd, zd)
+    b = oq.packed_linear(Xd, Pd, 4, 128, hd, zd)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    # one token at a time gives the same bits as the batch (fixed sum order)
+    for t in range(5):
+        assert torch.equal(oq.packed_linear(Xd[t:t + 1], Pd, 4, 128, hd, zd)[0], a[t])
+
+
+def test_gate_up_stack_full_size_sampled_rows():
+    # 7B gate and up projections stacked (22016 x 4096), 4-bit g128, one token:
+    # every row is independent, so sampled rows are checked against the oracle
+    bits, c_out, c_in, group = 4, 22016, 4096, 128
+    q, h, z, X, B = make_linear(21, bits, 1, c_out, c_in, group, True)
+    P = o_pack(q, bits)
+    Y = oq.packed_linear(to_dev(X, torch.bfloat16), to_dev(P), bits, group, to_dev(h), to_dev(z),
+                         to_dev(B)).cpu().numpy().astype(np.float64)
+    rows = np.random.default_rng(0).choice(c_out, size=64, replace=False)
+    rows = np.concatenate([rows, [0, c_out - 1]])
+    ref = o_linear(X, P[rows], bits, group, h[rows], z[rows], B[rows])
+    tol = bound(q[rows], h[rows], z[rows], X, group)
+    assert np.all(np.abs(Y[:, rows] - ref) <= tol)
+
+
+def test_pack_and_linear_agree_with_lwc_dequantised_weight():
+    # codes, h, z of the library's own Eq.2 forward, packed by the library: the
+    # packed linear reproduces X W_dq^T with W_dq that forward's fp32 output
+    rng = np.random.default_rng(4)
+    c_out, c_in, group, bits = 96, 1024, 128, 3
+    W = to_dev((0.02 * rng.standard_normal((c_out, c_in))).astype(np.float32), torch.bfloat16)
+    gl = torch.full((c_out, c_in // group), 2.0, device=DEV)
+    Wdq, codes, h, z = oq.lwc_fakequant_fwd(W, gl, gl, bits, group, dq_dtype=torch.float32)
+    X = to_dev(bf16_round(rng.standard_normal((2, c_in)).astype(np.float32)), torch.bfloat16)
+    Y = oq.packed_linear(X, oq.pack_codes(codes, bits), bits, group, h, z)
+    ref = X.double() @ Wdq.double().T
+    torch.cuda.synchronize()
+    zz = z.abs().repeat_interleave(group, 1).double()
+    hh = h.repeat_interleave(group, 1).double()
+    scale = X.double().abs() @ ((256 + codes.double() + zz) * hh).T
+    assert torch.all((Y.double() - ref).abs() <= 4e-6 * scale)
+
+
+def test_packed_linear_graph_replays_match_eager():
+    # a decode loop replays the same launches from a HIP graph: every replay,
+    # with eager work and new activations between replays, matches eager runs
+    q, h, z, X, B = make_linear(31, 4, 2, 700, 4096, 128, True)
+    Xd, Pd, hd, zd, Bd = (to_dev(X, torch.bfloat16), to_dev(o_pack(q, 4)), to_dev(h), to_dev(z),
+                          to_dev(B))
+    Y = torch.empty((2, 700), device=DEV)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        oq.packed_linear_into(Xd, Pd, 4, 128, hd, zd, Y, B=Bd)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        oq.packed_linear_into(Xd, Pd, 4, 128, hd, zd, Y, B=Bd)
+    rng = np.random.default_rng(32)
+    for i in range(4):
+        if i:
+            Xd.copy_(to_dev(bf16_round(rng.standard_normal((2, 4096)).astype(np.float32)),
+                            torch.bfloat16))
+        want = oq.packed_linear(Xd, Pd, 4, 128, hd, zd, Bd)
+        Y.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Y, want), i
