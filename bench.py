@@ -36,23 +36,40 @@ GEMM_SOURCES = ("paper_2308_13137_amd/csrc/gemm.hip", "paper_2308_13137_amd/csrc
 COPY_BYTES = 1 << 30          # calibration copy: 1 GiB read, 1 GiB written
 
 
-def gemm_source_hash():
+# sources whose text defines the packed linear's kernel
+PACKED_SOURCES = ("paper_2308_13137_amd/csrc/packed.hip", "paper_2308_13137_amd/csrc/packed.h",
+                  "paper_2308_13137_amd/csrc/common.h")
+# per dominant kernel: its sources, the key of their hash in the summary, the
+# dispatches the counters are read from, and what they are called
+TRAFFIC_KINDS = {
+    "gemm_fwd": (GEMM_SOURCES, "gemm source hash",
+                 lambda n: "gemm_bf16_w8_kernel" in n and "EpiResid" in n, "the forward product"),
+    "packed_linear": (PACKED_SOURCES, "packed source hash", lambda n: "packed_linear_kernel" in n,
+                      "the packed-weight linear"),
+}
+
+
+def source_hash(kind="gemm_fwd"):
     import hashlib
     h = hashlib.sha256()
-    for rel in GEMM_SOURCES:
+    for rel in TRAFFIC_KINDS[kind][0]:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def traffic_file(workload):
-    return os.path.join(ROOT, "profiles", f"gemm_fwd_{workload}_hbm_traffic.md")
+def gemm_source_hash():
+    return source_hash("gemm_fwd")
 
 
-def read_traffic(workload):
-    """HBM bytes per forward-product launch from the committed counter summary,
-    or None when there is none or it was taken on other kernel sources."""
-    path = traffic_file(workload)
+def traffic_file(workload, kind="gemm_fwd"):
+    return os.path.join(ROOT, "profiles", f"{kind}_{workload}_hbm_traffic.md")
+
+
+def read_traffic(workload, kind="gemm_fwd"):
+    """HBM bytes per launch of the kind's kernel from the committed counter
+    summary, or None when there is none or it was taken on other sources."""
+    path = traffic_file(workload, kind)
     if not os.path.exists(path):
         return None
     vals = {}
@@ -61,7 +78,7 @@ def read_traffic(workload):
             if ":" in line and line.startswith("- "):
                 k, v = line[2:].split(":", 1)
                 vals[k.strip()] = v.strip().strip("`")
-    if vals.get("gemm source hash") != gemm_source_hash():
+    if vals.get(TRAFFIC_KINDS[kind][1]) != source_hash(kind):
         return None
     try:
         return float(vals["HBM bytes per launch"])
@@ -69,10 +86,10 @@ def read_traffic(workload):
         return None
 
 
-def summarize_traffic(fetch_dir, write_dir, workload, cmd_fetch, cmd_write):
+def summarize_traffic(fetch_dir, write_dir, workload, cmd_fetch, cmd_write, kind="gemm_fwd"):
     """Counter passes (FETCH_SIZE, WRITE_SIZE, KiB per dispatch) -> summary:
-    the forward-product dispatches averaged, each counter scaled by what it
-    reads for the calibration copy of COPY_BYTES."""
+    the kind's dispatches averaged, each counter scaled by what it reads for
+    the calibration copy of COPY_BYTES."""
     import glob
     import sqlite3
 
@@ -89,20 +106,20 @@ def summarize_traffic(fetch_dir, write_dir, workload, cmd_fetch, cmd_write):
     def pick(d, pred):
         return [v for n, vs in d.items() if pred(n) for v in vs]
 
-    fwd = lambda n: "gemm_bf16_w8_kernel" in n and "EpiResid" in n
+    fwd = TRAFFIC_KINDS[kind][2]
     copy = lambda n: "neg" in n
     f = per_kernel(fetch_dir, "FETCH_SIZE")
     w = per_kernel(write_dir, "WRITE_SIZE")
     ff, ww, fc, wc = pick(f, fwd), pick(w, fwd), pick(f, copy), pick(w, copy)
     if not (ff and ww and fc and wc):
-        raise SystemExit("counter databases lack the forward-product or copy dispatches")
+        raise SystemExit(f"counter databases lack the {kind} or copy dispatches")
     k_fetch = COPY_BYTES / 1024 / (sum(fc) / len(fc))
     k_write = COPY_BYTES / 1024 / (sum(wc) / len(wc))
     fetch_kib = sum(ff) / len(ff)
     write_kib = sum(ww) / len(ww)
     total = (fetch_kib * k_fetch + write_kib * k_write) * 1024
     lines = [
-        f"# HBM traffic of the forward product ({workload}), rocprofv3 counters",
+        f"# HBM traffic of {TRAFFIC_KINDS[kind][3]} ({workload}), rocprofv3 counters",
         "",
         f"FETCH_SIZE pass: `{cmd_fetch}`",
         "",
@@ -111,15 +128,15 @@ def summarize_traffic(fetch_dir, write_dir, workload, cmd_fetch, cmd_write):
         "Each counter is scaled by what it reads for a plain copy kernel of "
         f"{COPY_BYTES >> 20} MiB read and {COPY_BYTES >> 20} MiB written (`--copy-calibration`).",
         "",
-        f"- forward dispatches: {len(ff)}",
+        f"- {'forward' if kind == 'gemm_fwd' else kind} dispatches: {len(ff)}",
         f"- FETCH_SIZE KiB per dispatch: {fetch_kib:.1f}",
         f"- WRITE_SIZE KiB per dispatch: {write_kib:.1f}",
         f"- copy FETCH_SIZE KiB: {sum(fc) / len(fc):.1f} (factor {k_fetch:.4f})",
         f"- copy WRITE_SIZE KiB: {sum(wc) / len(wc):.1f} (factor {k_write:.4f})",
         f"- HBM bytes per launch: {total:.6e}",
-        f"- gemm source hash: `{gemm_source_hash()}`",
+        f"- {TRAFFIC_KINDS[kind][1]}: `{source_hash(kind)}`",
     ]
-    with open(traffic_file(workload), "w") as fo:
+    with open(traffic_file(workload, kind), "w") as fo:
         fo.write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
@@ -227,30 +244,38 @@ def decode_inputs(bits, group, n_blocks, n_tok, device="cuda"):
     return lins, X
 
 
-def decode_cpu_baseline(bits, group):
+def decode_cpu_baseline(bits, group, min_seconds=10.0):
     """The oracle's packed linear on the first eighth of the rows of one
-    block's four stacked linears, one token; rows are independent, so the
-    time scales by 8 to the block and by the block count to the model."""
+    block's four stacked linears, one token, repeated on fresh inputs until
+    ``min_seconds`` have passed; rows are independent, so the time per pass
+    scales by 8 to the block and by the block count to the model."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle.packed import packed_linear
     rng = np.random.default_rng(5)
-    dt = 0.0
-    for name, c_out, c_in in DECODE_LINEARS:
-        rows = c_out // 8
-        P = rng.integers(0, 256, size=(rows, c_in * bits // 8), dtype=np.uint8)
-        h = rng.uniform(1e-3, 2.1e-2, size=(rows, c_in // group)).astype(np.float32)
-        z = rng.integers(0, 2 ** bits, size=(rows, c_in // group)).astype(np.float32)
-        x = rng.standard_normal((1, c_in))
-        t0 = time.perf_counter()
-        packed_linear(x, P, bits, group, h, z)
-        dt += time.perf_counter() - t0
+    dt, passes = 0.0, 0
+    while dt < min_seconds:
+        for name, c_out, c_in in DECODE_LINEARS:
+            rows = c_out // 8
+            P = rng.integers(0, 256, size=(rows, c_in * bits // 8), dtype=np.uint8)
+            h = rng.uniform(1e-3, 2.1e-2, size=(rows, c_in // group)).astype(np.float32)
+            z = rng.integers(0, 2 ** bits, size=(rows, c_in // group)).astype(np.float32)
+            x = rng.standard_normal((1, c_in))
+            t0 = time.perf_counter()
+            packed_linear(x, P, bits, group, h, z)
+            dt += time.perf_counter() - t0
+        passes += 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": float(f"{1.0 / (8 * dt * DECODE_BLOCKS):.4g}"), "unit": "decoded tokens/s",
+    return {"value": float(f"{passes / (8 * dt * DECODE_BLOCKS):.4g}"), "unit": "decoded tokens/s",
             "cores": threads, "kind": "oracle",
-            "sample": f"one eighth of the rows of one block's four stacked linears, one token "
-                      f"({dt:.1f} s), scaled by 8 x {DECODE_BLOCKS} blocks"}
+            "sample": f"{passes} pass(es) over one eighth of the rows of one block's four stacked "
+                      f"linears, one token ({dt:.1f} s), scaled by 8 x {DECODE_BLOCKS} blocks"}
+
+
+def decode_name(args):
+    name = f"llama7b_w{args.decode_bits}a16_g{args.decode_group}_decode"
+    return name if args.decode_tokens == 1 else f"{name}_t{args.decode_tokens}"
 
 
 def bench_decode(args):
@@ -260,7 +285,7 @@ def bench_decode(args):
     bits, group, n_tok = args.decode_bits, args.decode_group, args.decode_tokens
     torch.cuda.set_device(0)
     oq.lib()
-    name = f"llama7b_w{bits}a16_g{group}_decode"
+    name = decode_name(args)
     log(f"[bench] {name}: {DECODE_BLOCKS} blocks x {len(DECODE_LINEARS)} stacked linears, "
         f"{n_tok} token(s) per step")
     lins, X = decode_inputs(bits, group, DECODE_BLOCKS, n_tok)
@@ -294,13 +319,22 @@ def bench_decode(args):
     for _ in range(args.warmup):
         graph.replay()
     torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
+    e0.record()
     for _ in range(args.steps):
         graph.replay()
+    e1.record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms = (t1 - t0) * 1e3 / args.steps
-    achieved = work / n / (kms / n / 1e3) / 1e9
+    # every launch of the replayed step is the packed linear, back to back on
+    # the replay stream: the events around the replays over the launch count
+    # give its average duration (events around each eager launch add their
+    # own overhead to these few-microsecond kernels)
+    launches = n / args.steps
+    launch_ms = e0.elapsed_time(e1) / (args.steps * launches)
+    achieved = work / n / (launch_ms / 1e3) / 1e9
     weight_bytes = sum(P.numel() + 8 * h.numel() for _, _, P, h, _ in lins)
     line = {
         "metric": "decoded tokens/s through the block linears (packed weights)",
@@ -322,13 +356,58 @@ def bench_decode(args):
         "roofline": {"bound": "hbm", "kernel": "packed_linear", "achieved": round(achieved, 1),
                      "peak": PEAK["hbm_gbs"], "unit": "GB/s",
                      "frac": round(achieved / PEAK["hbm_gbs"], 4),
-                     "avg_launch_ms": round(kms / n, 5), "traffic": None},
-        "kernels": {"packed_linear": {"launches_per_step": n / args.steps,
-                                      "ms_per_step": round(kms / args.steps, 4),
-                                      "gbs": round(achieved, 1)}},
+                     "avg_launch_ms": round(launch_ms, 5),
+                     "traffic": read_traffic(name, "packed_linear")},
+        "kernels": {"packed_linear": {"launches_per_step": launches,
+                                      "bytes_per_launch": round(work / n),
+                                      "eager_event_bracketed_launch_ms": round(kms / n, 5)}},
     }
+    # per shape: its 32 launches replayed from a graph, against a torch copy
+    # of the same packed bytes (read + write): the practical streaming rate at
+    # these launch sizes
+    per_shape = {}
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for si, (nm, c_out, c_in) in enumerate(DECODE_LINEARS):
+        idx = [b * len(DECODE_LINEARS) + si for b in range(DECODE_BLOCKS)]
+        g_lin, g_cp = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_lin):
+            for i in idx:
+                _, _, P, h, z = lins[i]
+                oq.packed_linear_into(X[c_in], P, bits, group, h, z, outs[i])
+        dsts = [torch.empty_like(lins[i][2]) for i in idx]
+        with torch.cuda.graph(g_cp):
+            for i, d in zip(idx, dsts):
+                d.copy_(lins[i][2])
+        g_lin.replay()
+        g_cp.replay()
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(5):
+            g_lin.replay()
+        ev[1].record()
+        for _ in range(5):
+            g_cp.replay()
+        ev[2].record()
+        torch.cuda.synchronize()
+        lin_us = ev[0].elapsed_time(ev[1]) * 1e3 / (5 * len(idx))
+        cp_us = ev[1].elapsed_time(ev[2]) * 1e3 / (5 * len(idx))
+        _, _, P, h, _ = lins[idx[0]]
+        nbytes = P.numel() + 8 * h.numel()
+        per_shape[nm] = {"c_out": c_out, "c_in": c_in, "weight_bytes": nbytes,
+                         "linear_us": round(lin_us, 2), "linear_gbs": round(nbytes / lin_us / 1e3, 1),
+                         "copy_us": round(cp_us, 2),
+                         "copy_gbs": round(2 * P.numel() / cp_us / 1e3, 1)}
+        del g_lin, g_cp, dsts
+    line["per_shape"] = per_shape
     del lins, X, outs
     torch.cuda.empty_cache()
+    if args.copy_calibration:
+        src = torch.ones(COPY_BYTES // 4, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle on one block")
         line["cpu_baseline"] = decode_cpu_baseline(bits, group)
@@ -360,12 +439,16 @@ def main():
     ap.add_argument("--decode-group", type=int, default=128)
     ap.add_argument("--decode-tokens", type=int, default=1)
     args = ap.parse_args()
-    if args.decode and args.gpus == 1:
-        bench_decode(args)
-        return
     if args.summarize_traffic:
+        if args.decode:
+            summarize_traffic(*args.summarize_traffic[:2], decode_name(args),
+                              *args.summarize_traffic[2:], kind="packed_linear")
+            return
         w = args.config if not args.tokens else f"{args.config}_t{args.tokens}"
         summarize_traffic(*args.summarize_traffic[:2], w, *args.summarize_traffic[2:])
+        return
+    if args.decode and args.gpus == 1:
+        bench_decode(args)
         return
 
     if args.gpus != 1:
