@@ -432,6 +432,11 @@ def main():
     ap.add_argument("--summarize-traffic", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "CMD_FETCH",
                                                              "CMD_WRITE"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc passes")
+    ap.add_argument("--schedule", type=int, default=0, metavar="EPOCHS",
+                    help="time Algorithm 1's loop instead: EPOCHS passes over the workload's "
+                         "tokens as segments of --segment-tokens, one step per segment, in one "
+                         "oq_block_calibrate call")
+    ap.add_argument("--segment-tokens", type=int, default=2048)
     ap.add_argument("--decode", action="store_true",
                     help="time the deployment workload instead: packed-weight linears of "
                          "all 32 LLaMA-7B blocks for one decoded token per step")
@@ -468,7 +473,18 @@ def main():
     log(f"[bench] {w.name}: T={w.T}, {len(w.linears)} linears, {w.n_params / 1e6:.1f} M weights")
     X, W, Y, gl, bl, s, d = make_inputs(w)
     dt = torch.bfloat16 if w.bf16 else torch.float32
-    blk = oq.Block(w.T, [(st.width, st.let, st.act_bits) for st in w.sites],
+    T_step, n_seg = w.T, 1
+    if args.schedule:
+        # Algorithm 1's schedule: the same tokens as segments of T_step, one
+        # step per segment, LET initialised over all of them (make_inputs)
+        T_step = args.segment_tokens
+        n_seg = w.T // T_step
+        Xs = [[x[g * T_step:(g + 1) * T_step] for x in X] for g in range(n_seg)]
+        del Y
+        torch.cuda.empty_cache()
+        Ys = [[oq.fp_target(xs[l.site], W[i]) for i, l in enumerate(w.linears)] for xs in Xs]
+        X, Y = Xs[0], Ys[0]
+    blk = oq.Block(T_step, [(st.width, st.let, st.act_bits) for st in w.sites],
                    [(l.site, l.c_out, l.bits, l.group) for l in w.linears], dtype=dt)
     blk.init_optimizer()
     torch.cuda.synchronize()
@@ -476,7 +492,8 @@ def main():
     for _ in range(args.warmup):
         blk.step(X, Y, W, gl, bl, s=s, delta=d, update=True)
     torch.cuda.synchronize()
-    log(f"[bench] timing {args.steps} steps")
+    steps = args.schedule * n_seg if args.schedule else args.steps
+    log(f"[bench] timing {steps} steps")
 
     oq.profile_reset()
     oq.profile_enable(True)
@@ -484,26 +501,29 @@ def main():
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)] \
         if args.step_times else None
     t0 = time.perf_counter()
-    for i in range(args.steps):
+    if args.schedule:
+        losses = blk.calibrate(Xs, Ys, W, gl, bl, epochs=args.schedule, s=s, delta=d)
+    else:
+        for i in range(args.steps):
+            if marks:
+                marks[i].record()
+            blk.step(X, Y, W, gl, bl, s=s, delta=d, update=True)
         if marks:
-            marks[i].record()
-        blk.step(X, Y, W, gl, bl, s=s, delta=d, update=True)
-    if marks:
-        marks[-1].record()
+            marks[-1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     oq.profile_enable(False)
     prof = oq.profile_read()
-    loss = float(blk.loss.cpu())
+    loss = float(losses[-1].cpu()) if args.schedule else float(blk.loss.cpu())
 
-    ms = (t1 - t0) * 1e3 / args.steps
-    value = w.T / (ms / 1e3)
+    ms = (t1 - t0) * 1e3 / steps
+    value = T_step / (ms / 1e3)
 
     kernels = {}
     for kind, (n, kms, work) in prof.items():
         if n == 0:
             continue
-        ent = {"launches_per_step": n / args.steps, "ms_per_step": round(kms / args.steps, 4)}
+        ent = {"launches_per_step": n / steps, "ms_per_step": round(kms / steps, 4)}
         if kind in GEMM_KINDS:
             ent["tflops"] = round(work / (kms / 1e3) / 1e12, 1)
         elif work > 0:
@@ -523,17 +543,18 @@ def main():
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     roof["avg_launch_ms"] = round(kms / n, 4)
     roof["traffic"] = None
-    if dom == "gemm_fwd":
+    if dom == "gemm_fwd" and not args.schedule:
         tb = read_traffic(args.config if not args.tokens else f"{args.config}_t{args.tokens}")
         if tb is not None:
             roof["traffic"] = tb          # HBM bytes per launch (counter passes, copy-scaled)
 
     line = {
-        "metric": "calibration tokens/s per block fwd+bwd step",
+        "metric": ("calibration tokens/s, one step per calibration segment" if args.schedule
+                   else "calibration tokens/s per block fwd+bwd step"),
         "value": round(value, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 3),
         "higher_is_better": True,
@@ -541,7 +562,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if w.bf16 else "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "tokens_per_step": w.T, "linears": len(w.linears),
+        "config": {"workload": w.name, "tokens_per_step": T_step, "linears": len(w.linears),
                    "weights": w.n_params, "w_bits": w.linears[0].bits,
                    "group": w.linears[0].group, "let": any(st.let for st in w.sites),
                    "act_bits": w.sites[0].act_bits, "parallelism": "single GPU"},
@@ -549,6 +570,10 @@ def main():
         "roofline": roof,
         "kernels": kernels,
     }
+    if args.schedule:
+        line["config"].update(segments=n_seg, epochs=args.schedule)
+        line["block_seconds_at_20_epochs"] = round(20 * n_seg * ms / 1e3, 3)
+        line["first_last_loss"] = [float(losses[0].cpu()), loss]
     if marks:
         line["step_ms"] = [round(marks[i].elapsed_time(marks[i + 1]), 3) for i in range(args.steps)]
     if args.copy_calibration:

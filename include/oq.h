@@ -263,6 +263,27 @@ oq_status oq_block_calib_step(const oq_block_desc* desc, const void* const* Y_fp
                               const oq_block_grads* grads, const oq_block_optim* optim,
                               float* loss, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Algorithm 1's training loop for one block: `epochs` passes over
+ * `n_segments` calibration segments in order (the paper's bs = 1 schedule is
+ * 128 segments of 2048 tokens, 20 epochs), each one oq_block_calib_step with
+ * the AdamW update.
+ *   Y_fp_T : HOST array [n_segments * n_linears]; segment g's target of linear l
+ *            at [g * n_linears + l], each [c_out, desc->tokens] channel-major
+ *   X_q    : HOST array [n_segments * n_sites]; segment g's input of site k at
+ *            [g * n_sites + k], each [desc->tokens, C_site]
+ *   optim  : required; optim->step (>= 1) is the first step's count, the i-th
+ *            step uses optim->step + i; the struct is not written
+ *   losses : device float [epochs * n_segments]: the loss of every step, in order
+ * Parameters, gradients, AdamW state and workspace as oq_block_calib_step (the
+ * gradients hold the last step's).  Every pointer is validated before the first
+ * launch; steps are issued in order on `stream`.
+ */
+oq_status oq_block_calibrate(const oq_block_desc* desc, int n_segments, int epochs,
+                             const void* const* Y_fp_T, const void* const* X_q,
+                             const oq_block_params* params, const oq_block_grads* grads,
+                             const oq_block_optim* optim, float* losses, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Deployment of the calibrated weights (Sec. 4.5 and Table "tab:speed":
  * weight-only WxA16 models whose weights are stored as Eq.2's integer codes

@@ -4,6 +4,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <climits>
 #include <cmath>
 #include <mutex>
 #include <string>
@@ -977,6 +978,43 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     }
     OQ_HIP(adamw_multi(L, cl, ce, st), "adamw");
   }
+  return OQ_OK;
+}
+
+oq_status oq_block_calibrate(const oq_block_desc* d, int n_segments, int epochs,
+                             const void* const* Y_fp_T, const void* const* X_q,
+                             const oq_block_params* prm, const oq_block_grads* gr,
+                             const oq_block_optim* opt, float* losses, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  OQ_REQ(d && Y_fp_T && X_q && prm && gr && opt && losses,
+         "desc, Y_fp_T, X_q, params, grads, optim and losses are required");
+  OQ_REQ(n_segments >= 1 && epochs >= 1, "need n_segments >= 1 and epochs >= 1 (got %d, %d)",
+         n_segments, epochs);
+  OQ_REQ(opt->step >= 1 && int64_t(opt->step) + int64_t(epochs) * n_segments - 1 <= INT32_MAX,
+         "optim step %d out of range for %d steps", opt->step, epochs * n_segments);
+  size_t need = 0;
+  oq_status e = oq_block_workspace_size(d, &need);
+  if (e != OQ_OK) return e;
+  if (ws_bytes < need || !ws)
+    return fail(OQ_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  // every segment's pointers before the first launch; the first step checks the rest
+  for (int g = 0; g < n_segments; ++g) {
+    for (int l = 0; l < d->n_linears; ++l)
+      OQ_REQ(Y_fp_T[size_t(g) * d->n_linears + l], "segment %d: Y_fp_T[%d] missing", g, l);
+    for (int k = 0; k < d->n_sites; ++k) {
+      const void* x = X_q[size_t(g) * d->n_sites + k];
+      OQ_REQ(x && aligned16(x), "segment %d: X_q[%d] missing or misaligned", g, k);
+    }
+  }
+  oq_block_optim o = *opt;
+  for (int ep = 0; ep < epochs; ++ep)
+    for (int g = 0; g < n_segments; ++g) {
+      const int64_t i = int64_t(ep) * n_segments + g;
+      o.step = int(opt->step + i);
+      e = oq_block_calib_step(d, Y_fp_T + size_t(g) * d->n_linears, X_q + size_t(g) * d->n_sites,
+                              prm, gr, &o, losses + i, ws, ws_bytes, stream);
+      if (e != OQ_OK) return e;
+    }
   return OQ_OK;
 }
 

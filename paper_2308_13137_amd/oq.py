@@ -42,6 +42,7 @@ SIGNATURES = {
     "oq_adamw_step": (_I, [_P, _P, _P, _P, _I64, _D, _D, _D, _D, _D, _I, _P]),
     "oq_block_workspace_size": (_I, [_P, _PSZ]),
     "oq_block_calib_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "oq_block_calibrate": (_I, [_P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "oq_pack_codes": (_I, [_P, _I64, _I64, _I, _P, _P]),
     "oq_packed_linear": (_I, [_P, _I, _I64, _I64, _P, _I, _I64, _P, _P, _P, _I64, _P, _I, _P]),
     "oq_profile_enable": (_I, [_I]),
@@ -406,6 +407,45 @@ class Block:
                                          opt, _ptr(self.loss), _ptr(self.ws), self.ws_bytes,
                                          _stream(stream)))
         return self.loss
+
+    def _param_structs(self, W, gamma_logit, beta_logit, s, delta, B):
+        nl, ns = len(self.linears), len(self.sites)
+        prm, grd = BlockParams(), BlockGrads()
+        for l in range(nl):
+            prm.W[l] = _ptr(W[l]).value
+            prm.B[l] = B[l].data_ptr() if (B is not None and B[l] is not None) else None
+            prm.gamma_logit[l] = _ptr(gamma_logit[l]).value
+            prm.beta_logit[l] = _ptr(beta_logit[l]).value
+            grd.d_gamma_logit[l] = self.d_gamma[l].data_ptr()
+            grd.d_beta_logit[l] = self.d_beta[l].data_ptr()
+            grd.row_loss[l] = self.row_loss[l].data_ptr()
+        for k in range(ns):
+            if self.sites[k][1]:
+                prm.s[k] = _ptr(s[k]).value
+                prm.delta[k] = _ptr(delta[k]).value
+                grd.d_s[k] = self.d_s[k].data_ptr()
+                grd.d_delta[k] = self.d_delta[k].data_ptr()
+        return prm, grd
+
+    def calibrate(self, X_q_segs, Y_fp_T_segs, W, gamma_logit, beta_logit, epochs, s=None,
+                  delta=None, B=None, stream=None):
+        """Algorithm 1's loop: ``epochs`` passes over the segments in order,
+        AdamW after every step.  ``X_q_segs[g]`` / ``Y_fp_T_segs[g]`` are the
+        per-site / per-linear lists of segment g.  Returns the device tensor of
+        the epochs * segments step losses."""
+        if self.opt_state is None:
+            raise OQError("call init_optimizer() before calibrate()")
+        nl, ns, ng = len(self.linears), len(self.sites), len(X_q_segs)
+        prm, grd = self._param_structs(W, gamma_logit, beta_logit, s, delta, B)
+        yp = (C.c_void_p * (ng * nl))(*[_ptr(y).value for seg in Y_fp_T_segs for y in seg])
+        xp = (C.c_void_p * (ng * ns))(*[_ptr(x).value for seg in X_q_segs for x in seg])
+        losses = torch.empty(epochs * ng, dtype=torch.float32, device=self.device)
+        self.opt_state.step = self.step_count + 1
+        _check(lib().oq_block_calibrate(C.byref(self.desc), ng, epochs, yp, xp, C.byref(prm),
+                                        C.byref(grd), C.byref(self.opt_state), _ptr(losses),
+                                        _ptr(self.ws), self.ws_bytes, _stream(stream)))
+        self.step_count += epochs * ng
+        return losses
 
 
 # ------------------------------------------------------------------ profiling

@@ -162,6 +162,32 @@ def test_block_desc_validation():
     assert st == WORKSPACE
 
 
+def test_calibrate_validation():
+    L = oq.lib()
+    d = _desc(configs.C1)
+    n = C.c_size_t(0)
+    assert L.oq_block_workspace_size(C.byref(d), C.byref(n)) == OK
+    prm, grd, opt = oq.BlockParams(), oq.BlockGrads(), oq.BlockOptim()
+    opt.step = 1
+    yp = (C.c_void_p * 2)(0x10000, None)           # segment 1's target missing
+    xp = (C.c_void_p * 2)(0x10000, 0x10000)
+    args = lambda **kw: dict(dict(nseg=2, ep=2, yp=yp, xp=xp, losses=FAKE, ws=FAKE, nbytes=n.value),
+                             **kw)
+
+    def call(**kw):
+        a = args(**kw)
+        return L.oq_block_calibrate(C.byref(d), a["nseg"], a["ep"], a["yp"], a["xp"], C.byref(prm),
+                                    C.byref(grd), C.byref(opt), a["losses"], a["ws"], a["nbytes"],
+                                    None)
+
+    assert call() == INVALID                        # found before any launch
+    assert call(nseg=0) == INVALID and call(ep=0) == INVALID
+    assert call(losses=None) == INVALID
+    assert call(nbytes=n.value - 1) == WORKSPACE
+    opt.step = 0
+    assert call() == INVALID
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(oq, "LIB_PATH", str(tmp_path / "missing.so"))
     monkeypatch.setattr(oq, "_lib", None)

@@ -165,3 +165,90 @@ def test_twenty_step_trajectory():
         assert abs(a - b) / abs(b) < TOL_BF16
     for l in range(len(w.linears)):
         assert normwise(gl[l].cpu().numpy(), params["gamma_logit"][l]) < 1e-3
+
+
+def _segments(w, n_seg, seed):
+    """One problem of n_seg * T tokens cut into n_seg calibration segments of
+    T tokens (rows of X and of the token-major targets); LET is initialised
+    over all of them, once per block as Algorithm 1 does."""
+    P = make_problem(w.with_tokens(w.T * n_seg), seed=seed)
+    segs = []
+    for g in range(n_seg):
+        rows = slice(g * w.T, (g + 1) * w.T)
+        segs.append(dict(X=[x[rows] for x in P["X"]], Y=[y[rows] for y in P["Y"]]))
+    return P, segs
+
+
+def _device_segments(w, segs):
+    dt = torch.bfloat16 if w.bf16 else torch.float32
+    Xs = [[dev(np.ascontiguousarray(x), dt) for x in sg["X"]] for sg in segs]
+    Ys = [[dev(np.ascontiguousarray(y.T), dt) for y in sg["Y"]] for sg in segs]
+    return Xs, Ys
+
+
+def _new_block(w, P):
+    dt = torch.bfloat16 if w.bf16 else torch.float32
+    blk = oq.Block(w.T, [(s.width, s.let, s.act_bits) for s in w.sites],
+                   [(l.site, l.c_out, l.bits, l.group) for l in w.linears], dtype=dt)
+    blk.init_optimizer()
+    W = [dev(x, dt) for x in P["W"]]
+    gl = [dev(x) for x in P["gamma_logit"]]
+    bl = [dev(x) for x in P["beta_logit"]]
+    s = [None if x is None else dev(x) for x in P["s"]]
+    d = [None if x is None else dev(x) for x in P["delta"]]
+    return blk, W, gl, bl, s, d
+
+
+def test_calibrate_loop_equals_step_sequence():
+    """oq_block_calibrate (epochs x segments inside the library) gives bit for
+    bit what the same steps issued one by one give: losses, logits, s, delta."""
+    w = small_llama("c3_loop", hidden=256, ffn=512, T=128, w_bits=4, let=True, act_bits=4)
+    P, segs = _segments(w, 3, seed=7)
+    Xs, Ys = _device_segments(w, segs)
+    a = _new_block(w, P)
+    la = a[0].calibrate(Xs, Ys, a[1], a[2], a[3], epochs=2, s=a[4], delta=a[5])
+    b = _new_block(w, P)
+    lb = []
+    for _ in range(2):
+        for g in range(3):
+            lb.append(float(b[0].step(Xs[g], Ys[g], b[1], b[2], b[3], s=b[4], delta=b[5],
+                                      update=True).cpu()))
+    torch.cuda.synchronize()
+    assert la.cpu().tolist() == lb
+    for ta, tb in zip(a[2] + a[3] + [t for t in a[4] + a[5] if t is not None],
+                      b[2] + b[3] + [t for t in b[4] + b[5] if t is not None]):
+        assert torch.equal(ta, tb)
+    assert a[0].step_count == b[0].step_count == 6
+
+
+def test_calibrate_loop_follows_oracle():
+    """Two epochs over three segments (W3A16 g128, LLaMA-shaped, scaled down):
+    the step losses and the final clipping logits follow the oracle running
+    the same schedule with the same AdamW (Sec. 4.1 settings)."""
+    w = small_llama("c2_loop", hidden=256, ffn=768, T=128, w_bits=3, group=128)
+    n_seg, epochs = 3, 2
+    P, segs = _segments(w, n_seg, seed=11)
+    Xs, Ys = _device_segments(w, segs)
+    blk, W, gl, bl, s, d = _new_block(w, P)
+    ours = blk.calibrate(Xs, Ys, W, gl, bl, epochs=epochs).cpu().tolist()
+    params = dict(W=P["W"], B=P["B"], gamma_logit=[g.copy() for g in P["gamma_logit"]],
+                  beta_logit=[g.copy() for g in P["beta_logit"]], s=P["s"], delta=P["delta"])
+    mv = {k: [np.zeros_like(g, np.float64) for g in params[k]] for k in ("gamma_logit", "beta_logit")}
+    vv = {k: [np.zeros_like(g, np.float64) for g in params[k]] for k in ("gamma_logit", "beta_logit")}
+    refs, step = [], 0
+    for _ in range(epochs):
+        for sg in segs:
+            step += 1
+            rl, g = block_step(w.oracle_desc(), sg["X"], sg["Y"], params)
+            refs.append(rl)
+            for key, gk in (("gamma_logit", "d_gamma_logit"), ("beta_logit", "d_beta_logit")):
+                for l in range(len(w.linears)):
+                    p, mv[key][l], vv[key][l] = adamw(params[key][l], g[gk][l], mv[key][l],
+                                                      vv[key][l], step, LR_LWC)
+                    params[key][l] = p.astype(np.float32)
+    print("  loss gpu", ["%.4e" % x for x in ours], "oracle", ["%.4e" % x for x in refs])
+    for a, b in zip(ours, refs):
+        assert abs(a - b) / abs(b) < TOL_BF16
+    for l in range(len(w.linears)):
+        assert normwise(gl[l].cpu().numpy(), params["gamma_logit"][l]) < 1e-3
+        assert normwise(bl[l].cpu().numpy(), params["beta_logit"][l]) < 1e-3
