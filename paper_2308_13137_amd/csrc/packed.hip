@@ -92,7 +92,7 @@ OQ_DEV uint32_t field(const uint32_t* w, int pos) {
 // takes no literal, so they are passed in registers.
 OQ_DEV uint32_t and_or(uint32_t a, uint32_t mask, uint32_t magic) {
   uint32_t r;
-  asm volatile("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(mask), "v"(magic));
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(mask), "v"(magic));
   return r;
 }
 
