@@ -72,6 +72,11 @@ LINEAR = [
     (6, 5, 40, 160, 32, True, torch.float32, 0),
     (7, 4, 17, 224, 32, False, torch.bfloat16, 0),
     (3, 6, 1, 32, 32, True, torch.float32, 1),
+    # groups of a number of runs that is not a power of two (3 and 344 runs)
+    (4, 2, 70, 288, 96, True, torch.float32, 0),
+    (3, 1, 33, 11008, 11008, False, torch.float32, 0),
+    # the widest input: one token per launch fits LDS, so 3 tokens are 3 launches
+    (4, 3, 7, 65536, 128, False, torch.float32, 0),
 ]
 
 
