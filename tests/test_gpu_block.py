@@ -252,3 +252,26 @@ def test_calibrate_loop_follows_oracle():
     for l in range(len(w.linears)):
         assert normwise(gl[l].cpu().numpy(), params["gamma_logit"][l]) < 1e-3
         assert normwise(bl[l].cpu().numpy(), params["beta_logit"][l]) < 1e-3
+
+
+def test_iterative_schedule_freezes_one_parameter_set():
+    """The ablation's iterative training of LWC and LET alternates which set
+    learns: a calibrate call with one learning rate at zero leaves that set
+    bit for bit unchanged while the other set moves."""
+    w = small_llama("c3_iter", hidden=256, ffn=512, T=128, w_bits=4, let=True, act_bits=4)
+    P, segs = _segments(w, 2, seed=13)
+    Xs, Ys = _device_segments(w, segs)
+    blk, W, gl, bl, s, d = _new_block(w, P)
+    let0 = [t.clone() for t in s + d if t is not None]
+    lwc0 = [t.clone() for t in gl + bl]
+    blk.opt_state.lr_let = 0.0                      # LWC phase
+    blk.calibrate(Xs, Ys, W, gl, bl, epochs=1, s=s, delta=d)
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(let0, [t for t in s + d if t is not None]))
+    assert any(not torch.equal(a, b) for a, b in zip(lwc0, gl + bl))
+    lwc1 = [t.clone() for t in gl + bl]
+    blk.opt_state.lr_let, blk.opt_state.lr_lwc = 1e-2, 0.0   # LET phase
+    blk.calibrate(Xs, Ys, W, gl, bl, epochs=1, s=s, delta=d)
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(lwc1, gl + bl))
+    assert any(not torch.equal(a, b) for a, b in zip(let0, [t for t in s + d if t is not None]))
