@@ -213,15 +213,23 @@ def cpu_baseline(w, tokens):
 
 
 # The deployment workload (Sec. 4.5, Table "tab:speed"): one decoded token
-# through the linears of all 32 LLaMA-7B blocks, weights stored as packed
+# through the linears of all blocks of a LLaMA model (32 for 7B, 80 for
+# 65B), weights stored as packed
 # low-bit codes.  Linears that read the same input are stacked (q,k,v and
 # gate,up), as a deployment would: 4 launches per block.
-DECODE_BLOCKS = 32
-DECODE_LINEARS = (("qkv", 3 * 4096, 4096), ("o", 4096, 4096), ("gate_up", 2 * 11008, 4096),
-                  ("down", 4096, 11008))
+DECODE_MODELS = {
+    # name: (blocks, hidden, ffn); LLaMA-1 shapes of the paper's speed table
+    "llama7b": (32, 4096, 11008),
+    "llama65b": (80, 8192, 22016),
+}
 
 
-def decode_inputs(bits, group, n_blocks, n_tok, device="cuda"):
+def decode_linears(model):
+    _, hid, ffn = DECODE_MODELS[model]
+    return (("qkv", 3 * hid, hid), ("o", hid, hid), ("gate_up", 2 * ffn, hid), ("down", hid, ffn))
+
+
+def decode_inputs(bits, group, model, n_tok, device="cuda"):
     """Seeded random packed codes (every code value equally likely), step
     sizes, zero points and activations, distinct for every block so that no
     block's weights are cached when the next one is read."""
@@ -231,8 +239,8 @@ def decode_inputs(bits, group, n_blocks, n_tok, device="cuda"):
     gen = torch.Generator(device=device)
     gen.manual_seed(inputs.SEED + 5)
     lins = []
-    for _ in range(n_blocks):
-        for name, c_out, c_in in DECODE_LINEARS:
+    for _ in range(DECODE_MODELS[model][0]):
+        for name, c_out, c_in in decode_linears(model):
             P = torch.randint(0, 256, (c_out, c_in * bits // 8), generator=gen, device=device,
                               dtype=torch.uint8)
             h = torch.rand((c_out, c_in // group), generator=gen, device=device) * 0.02 + 1e-3
@@ -240,11 +248,11 @@ def decode_inputs(bits, group, n_blocks, n_tok, device="cuda"):
                               device=device).float()
             lins.append((name, c_in, P, h, z))
     X = {c_in: inputs.torch_activations(gen, n_tok, c_in, dtype=torch.bfloat16, device=device)
-         .contiguous() for c_in in {c for _, _, c in DECODE_LINEARS}}
+         .contiguous() for c_in in {c for _, _, c in decode_linears(model)}}
     return lins, X
 
 
-def decode_cpu_baseline(bits, group, min_seconds=10.0):
+def decode_cpu_baseline(bits, group, model, min_seconds=10.0):
     """The oracle's packed linear on the first eighth of the rows of one
     block's four stacked linears, one token, repeated on fresh inputs until
     ``min_seconds`` have passed; rows are independent, so the time per pass
@@ -256,7 +264,7 @@ def decode_cpu_baseline(bits, group, min_seconds=10.0):
     rng = np.random.default_rng(5)
     dt, passes = 0.0, 0
     while dt < min_seconds:
-        for name, c_out, c_in in DECODE_LINEARS:
+        for name, c_out, c_in in decode_linears(model):
             rows = c_out // 8
             P = rng.integers(0, 256, size=(rows, c_in * bits // 8), dtype=np.uint8)
             h = rng.uniform(1e-3, 2.1e-2, size=(rows, c_in // group)).astype(np.float32)
@@ -267,14 +275,15 @@ def decode_cpu_baseline(bits, group, min_seconds=10.0):
             dt += time.perf_counter() - t0
         passes += 1
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": float(f"{passes / (8 * dt * DECODE_BLOCKS):.4g}"), "unit": "decoded tokens/s",
+    blocks = DECODE_MODELS[model][0]
+    return {"value": float(f"{passes / (8 * dt * blocks):.4g}"), "unit": "decoded tokens/s",
             "cores": threads, "kind": "oracle",
             "sample": f"{passes} pass(es) over one eighth of the rows of one block's four stacked "
-                      f"linears, one token ({dt:.1f} s), scaled by 8 x {DECODE_BLOCKS} blocks"}
+                      f"linears, one token ({dt:.1f} s), scaled by 8 x {blocks} blocks"}
 
 
 def decode_name(args):
-    name = f"llama7b_w{args.decode_bits}a16_g{args.decode_group}_decode"
+    name = f"{args.decode_model}_w{args.decode_bits}a16_g{args.decode_group}_decode"
     return name if args.decode_tokens == 1 else f"{name}_t{args.decode_tokens}"
 
 
@@ -286,9 +295,11 @@ def bench_decode(args):
     torch.cuda.set_device(0)
     oq.lib()
     name = decode_name(args)
-    log(f"[bench] {name}: {DECODE_BLOCKS} blocks x {len(DECODE_LINEARS)} stacked linears, "
+    n_blocks = DECODE_MODELS[args.decode_model][0]
+    shapes = decode_linears(args.decode_model)
+    log(f"[bench] {name}: {n_blocks} blocks x {len(shapes)} stacked linears, "
         f"{n_tok} token(s) per step")
-    lins, X = decode_inputs(bits, group, DECODE_BLOCKS, n_tok)
+    lins, X = decode_inputs(bits, group, args.decode_model, n_tok)
     outs = [torch.empty((n_tok, P.shape[0]), dtype=torch.float32, device="cuda")
             for _, _, P, _, _ in lins]
 
@@ -350,7 +361,7 @@ def bench_decode(args):
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": name, "blocks": DECODE_BLOCKS, "tokens_per_step": n_tok,
+        "config": {"workload": name, "blocks": n_blocks, "tokens_per_step": n_tok,
                    "w_bits": bits, "group": group, "weight_bytes": weight_bytes,
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "packed_linear", "achieved": round(achieved, 1),
@@ -367,8 +378,8 @@ def bench_decode(args):
     # these launch sizes
     per_shape = {}
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-    for si, (nm, c_out, c_in) in enumerate(DECODE_LINEARS):
-        idx = [b * len(DECODE_LINEARS) + si for b in range(DECODE_BLOCKS)]
+    for si, (nm, c_out, c_in) in enumerate(shapes):
+        idx = [b * len(shapes) + si for b in range(n_blocks)]
         g_lin, g_cp = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
         with torch.cuda.graph(g_lin):
             for i in idx:
@@ -410,7 +421,7 @@ def bench_decode(args):
         del src, dst
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle on one block")
-        line["cpu_baseline"] = decode_cpu_baseline(bits, group)
+        line["cpu_baseline"] = decode_cpu_baseline(bits, group, args.decode_model)
     else:
         line["cpu_baseline"] = None
     print(json.dumps(line), flush=True)
@@ -439,7 +450,8 @@ def main():
     ap.add_argument("--segment-tokens", type=int, default=2048)
     ap.add_argument("--decode", action="store_true",
                     help="time the deployment workload instead: packed-weight linears of "
-                         "all 32 LLaMA-7B blocks for one decoded token per step")
+                         "all blocks of --decode-model for one decoded token per step")
+    ap.add_argument("--decode-model", default="llama7b", choices=sorted(DECODE_MODELS))
     ap.add_argument("--decode-bits", type=int, default=4)
     ap.add_argument("--decode-group", type=int, default=128)
     ap.add_argument("--decode-tokens", type=int, default=1)
