@@ -284,6 +284,24 @@ oq_status oq_block_calibrate(const oq_block_desc* desc, int n_segments, int epoc
                              const oq_block_optim* optim, float* losses, void* ws,
                              size_t ws_bytes, hipStream_t stream);
 
+/* Algorithm 1's last step for one block ("obtain the quantised block"), on
+ * its linear sub-graph: with the learned clipping logits and LET parameters,
+ * each linear's weight is transformed (Eq. 3: s (.) W on LET sites) and
+ * quantised by LWC (Eq. 2); its codes are written packed in the
+ * oq_pack_codes layout with their h and z, ready for oq_packed_linear.
+ *   packed  : HOST [n_linears] device pointers, each [c_out, C_site * bits / 8] u8
+ *   h, z    : HOST [n_linears] device pointers, each [c_out, C_site / group] fp32
+ *   B_tilde : HOST [n_linears] device pointers [c_out] fp32, or NULL (array or
+ *             entry): the folded bias B + delta W on LET sites, else B (0 without B)
+ * The deployed linear then reads X~ = (X - delta) / s on LET sites (Eq. 3).
+ * C_site % 32 == 0.  Workspace: oq_block_export_workspace_size bytes, 16-byte
+ * aligned (the largest linear's u8 codes).  Errors as oq_block_calib_step.
+ */
+oq_status oq_block_export_workspace_size(const oq_block_desc* desc, size_t* bytes);
+oq_status oq_block_export(const oq_block_desc* desc, const oq_block_params* params,
+                          uint8_t* const* packed, float* const* h, float* const* z,
+                          float* const* B_tilde, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Deployment of the calibrated weights (Sec. 4.5 and Table "tab:speed":
  * weight-only WxA16 models whose weights are stored as Eq.2's integer codes

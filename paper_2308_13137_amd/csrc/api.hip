@@ -981,6 +981,59 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
   return OQ_OK;
 }
 
+oq_status oq_block_export_workspace_size(const oq_block_desc* d, size_t* bytes) {
+  OQ_REQ(bytes, "bytes is required");
+  std::vector<SitePlan> plan;
+  oq_status e = plan_block(d, plan);
+  if (e != OQ_OK) return e;
+  size_t mx = 0;
+  for (int l = 0; l < d->n_linears; ++l)
+    mx = std::max(mx, size_t(d->lin_c_out[l]) * size_t(d->site_width[d->lin_site[l]]));
+  *bytes = (mx + 255) & ~size_t(255);
+  return OQ_OK;
+}
+
+oq_status oq_block_export(const oq_block_desc* d, const oq_block_params* prm,
+                          uint8_t* const* packed, float* const* h, float* const* z,
+                          float* const* B_tilde, void* ws, size_t ws_bytes, hipStream_t st) {
+  size_t need = 0;
+  oq_status e = oq_block_export_workspace_size(d, &need);
+  if (e != OQ_OK) return e;
+  OQ_REQ(prm && packed && h && z, "params, packed, h and z are required");
+  if (!ws || ws_bytes < need || !aligned16(ws))
+    return fail(OQ_ERR_WORKSPACE, "workspace of %zu bytes (16-byte aligned) needed, %zu given", need,
+                ws_bytes);
+  for (int l = 0; l < d->n_linears; ++l) {
+    const int k = d->lin_site[l];
+    OQ_REQ(d->site_width[k] % 32 == 0, "linear %d: C_in=%lld is not a multiple of 32", l,
+           (long long)d->site_width[k]);
+    OQ_REQ(prm->W[l] && aligned16(prm->W[l]), "W[%d] missing or misaligned", l);
+    OQ_REQ(prm->gamma_logit[l] && prm->beta_logit[l], "logits of linear %d missing", l);
+    OQ_REQ(packed[l] && aligned16(packed[l]) && h[l] && z[l], "outputs of linear %d missing or misaligned", l);
+    if (d->site_let[k])
+      OQ_REQ(prm->s[k] && prm->delta[k] && aligned16(prm->s[k]) && aligned16(prm->delta[k]),
+             "site %d: LET needs 16-byte aligned s and delta", k);
+  }
+  const bool bf = d->dtype == OQ_BF16;
+  uint8_t* codes = static_cast<uint8_t*>(ws);
+  for (int l = 0; l < d->n_linears; ++l) {
+    const int k = d->lin_site[l];
+    const int64_t c_out = d->lin_c_out[l], c_in = d->site_width[k];
+    const bool let = d->site_let[k] != 0;
+    ProfScope ps(PK_OTHER, st, double(c_out) * c_in * (esize(d->dtype) + 1.0 + d->lin_bits[l] / 8.0));
+    OQ_HIP(lwc_fwd(prm->W[l], bf, c_out, c_in, let ? prm->s[k] : nullptr, prm->gamma_logit[l],
+                   prm->beta_logit[l], d->lin_bits[l], d->lin_group[l], nullptr, false, codes, h[l],
+                   z[l], st),
+           "export lwc_fwd");
+    OQ_HIP(pack_codes(codes, c_out, c_in, d->lin_bits[l], packed[l], st), "export pack_codes");
+    if (B_tilde && B_tilde[l])
+      OQ_HIP(let_fold(prm->W[l], bf, prm->B[l], c_out, c_in, let ? prm->s[k] : nullptr,
+                      let ? prm->delta[k] : nullptr, nullptr, false, B_tilde[l], st),
+             "export let_fold");
+  }
+  return OQ_OK;
+}
+
 oq_status oq_block_calibrate(const oq_block_desc* d, int n_segments, int epochs,
                              const void* const* Y_fp_T, const void* const* X_q,
                              const oq_block_params* prm, const oq_block_grads* gr,

@@ -43,6 +43,8 @@ SIGNATURES = {
     "oq_block_workspace_size": (_I, [_P, _PSZ]),
     "oq_block_calib_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "oq_block_calibrate": (_I, [_P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "oq_block_export_workspace_size": (_I, [_P, _PSZ]),
+    "oq_block_export": (_I, [_P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "oq_pack_codes": (_I, [_P, _I64, _I64, _I, _P, _P]),
     "oq_packed_linear": (_I, [_P, _I, _I64, _I64, _P, _I, _I64, _P, _P, _P, _I64, _P, _I, _P]),
     "oq_profile_enable": (_I, [_I]),
@@ -426,6 +428,25 @@ class Block:
                 grd.d_s[k] = self.d_s[k].data_ptr()
                 grd.d_delta[k] = self.d_delta[k].data_ptr()
         return prm, grd
+
+    def export(self, W, gamma_logit, beta_logit, s=None, delta=None, B=None, stream=None):
+        """Algorithm 1's quantised block: per linear (packed codes, h, z, B~)."""
+        nl = len(self.linears)
+        prm, _ = self._param_structs(W, gamma_logit, beta_logit, s, delta, B)
+        outs = []
+        for l, (k, c_out, bits, group) in enumerate(self.linears):
+            c_in = self.sites[k][0]
+            f32 = dict(dtype=torch.float32, device=self.device)
+            outs.append((torch.empty((c_out, c_in * bits // 8), dtype=torch.uint8, device=self.device),
+                         torch.empty((c_out, c_in // group), **f32),
+                         torch.empty((c_out, c_in // group), **f32), torch.empty(c_out, **f32)))
+        n = C.c_size_t(0)
+        _check(lib().oq_block_export_workspace_size(C.byref(self.desc), C.byref(n)))
+        ws = torch.empty(max(n.value, 1), dtype=torch.uint8, device=self.device)
+        arr = lambda i: (C.c_void_p * nl)(*[o[i].data_ptr() for o in outs])
+        _check(lib().oq_block_export(C.byref(self.desc), C.byref(prm), arr(0), arr(1), arr(2), arr(3),
+                                     _ptr(ws), n.value, _stream(stream)))
+        return outs
 
     def calibrate(self, X_q_segs, Y_fp_T_segs, W, gamma_logit, beta_logit, epochs, s=None,
                   delta=None, B=None, stream=None):

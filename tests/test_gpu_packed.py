@@ -170,3 +170,35 @@ def test_packed_linear_graph_replays_match_eager():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(Y, want), i
+
+
+@pytest.mark.parametrize("let", [False, True], ids=["w3_g64", "w4_let"])
+def test_block_export_matches_oracle(let):
+    """Algorithm 1's quantised block: every linear's packed codes, h and z equal
+    the oracle's Eq. 2 quantisation of s (.) W bit for bit, and the folded bias
+    is the oracle's B + delta W."""
+    from oracle.let import let_bias
+    from oracle.quant import lwc_fwd as o_lwc
+    from tests.cases import make_problem, small_llama
+    if let:
+        w = small_llama("export_let", hidden=256, ffn=512, T=128, w_bits=4, let=True, act_bits=4)
+    else:
+        w = small_llama("export", hidden=256, ffn=512, T=128, w_bits=3, group=64)
+    P = make_problem(w, seed=3, logit="random", bias=True)
+    blk = oq.Block(w.T, [(s.width, s.let, s.act_bits) for s in w.sites],
+                   [(l.site, l.c_out, l.bits, l.group) for l in w.linears], dtype=torch.bfloat16)
+    opt = lambda xs: [None if x is None else to_dev(x) for x in xs]
+    outs = blk.export([to_dev(x, torch.bfloat16) for x in P["W"]], opt(P["gamma_logit"]),
+                      opt(P["beta_logit"]), s=opt(P["s"]), delta=opt(P["delta"]), B=opt(P["B"]))
+    torch.cuda.synchronize()
+    for l, lin in enumerate(w.linears):
+        site = w.sites[lin.site]
+        st = o_lwc(P["W"][l], P["gamma_logit"][l], P["beta_logit"][l], lin.bits, lin.group,
+                   s=P["s"][lin.site] if site.let else None)
+        packed, h, z, bt = (t.cpu().numpy() for t in outs[l])
+        assert np.array_equal(packed, o_pack(st["codes"], lin.bits)), l
+        assert np.array_equal(h, st["h_g"]) and np.array_equal(z, st["z_g"]), l
+        want = let_bias(P["W"][l], P["B"][l], P["delta"][lin.site]) if site.let else P["B"][l]
+        scale = np.abs(P["W"][l]).astype(np.float64) @ (np.abs(P["delta"][lin.site]) if site.let
+                                                        else np.zeros(site.width)) + np.abs(want)
+        assert np.all(np.abs(bt - want) <= 1e-5 * scale + 1e-30), l
