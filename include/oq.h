@@ -116,7 +116,10 @@ oq_status oq_act_fakequant_fwd(const void* X, oq_dtype x_dt, int64_t T, int64_t 
                                uint8_t* codes, float* h, float* z, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
- * Straight-through backward of oq_act_fakequant_fwd.
+ * Straight-through backward of oq_act_fakequant_fwd (Sec. 3.2, Eq. 2 at
+ * gamma = beta = 1 per token row: only rint has derivative 1, the row's
+ * max/min and the clamp are differentiated exactly; Eq. 3 for the LET input
+ * transform X~ = (X - delta) / s, whose s and delta gradients are returned).
  *   dX_dq    [T, C] fp32          dL/dX^ (summed over every linear reading X^)
  *   dX_tilde [T, C] fp32 | NULL   dL/dX~
  *   d_s      [C] fp32 | NULL      input-path part of dL/ds    = -sum_t dL/dX~ * X~ / s

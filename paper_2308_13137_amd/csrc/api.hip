@@ -445,6 +445,8 @@ oq_status oq_adamw_step(float* p, const float* g, float* m, float* v, int64_t n,
   return OQ_OK;
 }
 
+}  // extern "C"
+
 // ------------------------------------------------------------------ block step
 namespace {
 
@@ -686,6 +688,8 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
 }
 
 }  // namespace
+
+extern "C" {
 
 oq_status oq_block_workspace_size(const oq_block_desc* desc, size_t* bytes) {
   OQ_REQ(bytes, "bytes is required");

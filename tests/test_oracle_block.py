@@ -8,7 +8,7 @@ import pytest
 import torch
 
 from oracle.adamw import adamw
-from oracle.block import block_step
+from oracle.block import block_step, fp_target
 from oracle.let import let_bias, let_fold, let_init, let_w, let_x
 from oracle.quant import lwc_fwd
 from oracle.surrogate import freeze, surrogate_loss
@@ -246,3 +246,29 @@ def test_adamw_matches_library_optimizer():
         opt.step()
         p, m, v = adamw(p, g, m, v, step, 1e-2)
     np.testing.assert_allclose(p, t.detach().numpy(), rtol=1e-12, atol=1e-14)
+
+
+def test_fp_target_worked_product_with_bias():
+    c = GOLD["fp_target_worked"]
+    for bf16 in (True, False):
+        y = fp_target(np.float32(c["x"]), np.float32(c["w"]), np.float32(c["b"]), bf16=bf16)
+        assert y.dtype == np.float32
+        np.testing.assert_array_equal(y, np.float32(c["y"]))
+    # no bias: the product alone
+    y = fp_target(np.float32(c["x"]), np.float32(c["w"]), None)
+    np.testing.assert_array_equal(y, np.float32(c["y"]) - np.float32(c["b"])[None, :])
+
+
+def test_fp_target_rounds_through_fp32_before_bf16():
+    """The exact sum lies just above a bf16 midpoint; its fp32 rounding lands
+    on the midpoint, which ties to even.  Pins the two-step rounding of the
+    target (fp32 accumulator, then bf16 storage)."""
+    c = GOLD["fp_target_double_rounding"]
+    X, W = np.float32(c["x"]), np.float32(c["w"])
+    for b, two, direct in zip(c["b_cases"], c["y_two_step"], c["y_direct"]):
+        y = fp_target(X, W, np.float32([b]), bf16=True)
+        assert y[0, 0] == np.float32(two), (b, y)
+        assert y[0, 0] != np.float32(direct)
+        # the fp32 target keeps the fp32 sum (1 + 2^-8 or 1.5 + 2^-8)
+        y32 = fp_target(X, W, np.float32([b]), bf16=False)
+        assert y32[0, 0] == np.float32(b + 1.0 + 2.0 ** -8)
