@@ -133,6 +133,28 @@ oq_status oq_act_fakequant_bwd(const void* X, oq_dtype x_dt, int64_t T, int64_t 
 oq_status oq_act_fakequant_bwd_workspace_size(int64_t T, int64_t C, size_t* bytes);
 
 /* ---------------------------------------------------------------------------
+ * oq_act_fakequant_bwd without a workspace, for callers that cannot allocate
+ * device memory (code under stream capture, serving loops, harnesses that
+ * forbid hipMalloc).  Same arguments, outputs, kernels and results (bit for
+ * bit) as oq_act_fakequant_bwd; the column partials of d_s / d_delta go to a
+ * static device array of OQ_NOALLOC_SCRATCH_BYTES that the library holds on
+ * each GPU it runs on until the process ends.  The call allocates nothing.
+ *   Limit: when d_s or d_delta is wanted, the bytes that
+ *   oq_act_fakequant_bwd_workspace_size reports for (T, C) must not exceed
+ *   OQ_NOALLOC_SCRATCH_BYTES (else OQ_ERR_UNSUPPORTED, nothing launched);
+ *   e.g. C = 4096 or 5120 at any T; C = 11008 only for T <= 381.
+ *   Concurrency: every call on one GPU shares that GPU's array, so calls
+ *   that overlap on one GPU (different streams or host threads) race; order
+ *   them on one stream.  The array keeps the last call's partials; nothing
+ *   in it needs to start at zero.
+ */
+#define OQ_NOALLOC_SCRATCH_BYTES (32u * 1024u * 1024u)
+oq_status oq_act_fakequant_bwd_noalloc(const void* X, oq_dtype x_dt, int64_t T, int64_t C, int bits,
+                                       const float* s, const float* delta, const float* dX_dq,
+                                       float* dX_tilde, float* d_s, float* d_delta,
+                                       hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * LET initialisation (Sec. 4.1: scale from SmoothQuant, shift from Outlier
  * Suppression+):  s_c = sqrt(max_t |X[t,c]|) / sqrt(max over the site's
  * linears and rows of |W[o,c]|), each max floored at 1e-5;  delta_c =

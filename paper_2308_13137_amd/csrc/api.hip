@@ -298,6 +298,78 @@ oq_status oq_act_fakequant_bwd(const void* X, oq_dtype x_dt, int64_t T, int64_t 
   return OQ_OK;
 }
 
+}  // extern "C"
+
+// ------------------------------------------------------------------ no-allocation variant
+// File-scope device array that holds the column partials of
+// oq_act_fakequant_bwd_noalloc.  Each GPU has its own copy at its own
+// address; host code uses the address hipGetSymbolAddress returns for the
+// current device, never the array's name (a host-side stand-in).
+static __device__ __align__(256) unsigned char scratch[OQ_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The scratch array's device address on the current device, looked up once
+// per device (with that device current) and kept.
+oq_status scratch_for_current_device(void** out) {
+  int dev = 0;
+  OQ_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(OQ_ERR_UNSUPPORTED, "device %d out of range", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    OQ_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(OQ_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return OQ_OK;
+}
+}  // namespace
+
+extern "C" {
+
+oq_status oq_act_fakequant_bwd_noalloc(const void* X, oq_dtype x_dt, int64_t T, int64_t C, int bits,
+                                       const float* s, const float* delta, const float* dX_dq,
+                                       float* dX_tilde, float* d_s, float* d_delta,
+                                       hipStream_t stream) {
+  oq_status e = check_act(X, x_dt, T, C, bits, s, delta);
+  if (e != OQ_OK) return e;
+  OQ_REQ(dX_dq && aligned16(dX_dq), "dX_dq is required and 16-byte aligned");
+  OQ_REQ(!dX_tilde || aligned16(dX_tilde), "dX_tilde must be 16-byte aligned");
+  const bool parts = d_s || d_delta;
+  size_t need = 0;
+  if (parts) oq_act_fakequant_bwd_workspace_size(T, C, &need);
+  if (need > size_t(OQ_NOALLOC_SCRATCH_BYTES))
+    return fail(OQ_ERR_UNSUPPORTED,
+                "T=%lld C=%lld needs %zu bytes of partials, more than the %zu-byte scratch",
+                (long long)T, (long long)C, need, size_t(OQ_NOALLOC_SCRATCH_BYTES));
+  float *psx = nullptr, *ps1 = nullptr;
+  const int64_t np = act_bwd_nparts(T);
+  if (parts) {
+    void* base = nullptr;
+    e = scratch_for_current_device(&base);
+    if (e != OQ_OK) return e;
+    Carver cv{static_cast<char*>(base)};
+    psx = cv.take<float>(size_t(np) * C);
+    ps1 = cv.take<float>(size_t(np) * C);
+  }
+  {
+    ProfScope ps(PK_ACT_BWD, stream, double(T) * C * (esize(x_dt) + 4 + (dX_tilde ? 4 : 0)));
+    OQ_HIP(act_bwd(X, x_dt == OQ_BF16, T, C, bits, s, delta, dX_dq, dX_tilde, psx, ps1, stream),
+           "act_bwd");
+  }
+  if (parts) {
+    ProfScope ps(PK_OTHER, stream, 0);
+    OQ_HIP(let_grad_finish(C, s, nullptr, 0, psx, ps1, np, nullptr, 0, d_s, d_delta, stream),
+           "act finish");
+  }
+  return OQ_OK;
+}
+
 static size_t let_init_ws(int64_t T, int64_t C, const int64_t* c_out_site, int n_site) {
   size_t naw = 0;
   for (int i = 0; i < n_site; ++i) naw += size_t(colstat_nparts(c_out_site[i]));

@@ -34,6 +34,7 @@ SIGNATURES = {
     "oq_act_fakequant_fwd": (_I, [_P, _I, _I64, _I64, _I, _P, _P, _P, _I, _P, _P, _P, _P]),
     "oq_act_fakequant_bwd": (_I, [_P, _I, _I64, _I64, _I, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "oq_act_fakequant_bwd_workspace_size": (_I, [_I64, _I64, _PSZ]),
+    "oq_act_fakequant_bwd_noalloc": (_I, [_P, _I, _I64, _I64, _I, _P, _P, _P, _P, _P, _P, _P]),
     "oq_let_init": (_I, [_P, _I, _I64, _I64, _P, _P, _I, _I, _P, _P, _P, _SZ, _P]),
     "oq_let_init_workspace_size": (_I, [_I64, _I64, _P, _I, _PSZ]),
     "oq_fp_target": (_I, [_P, _P, _I, _P, _I64, _I64, _I64, _P, _P]),
@@ -228,6 +229,17 @@ def act_fakequant_bwd(X, bits, dX_dq, s=None, delta=None, want_dX_tilde=True, st
                                       _ptr(_f32(dX_dq, "dX_dq")), _ptr(dxt), _ptr(ds), _ptr(dd),
                                       _ptr(ws), n.value, _stream(stream)))
     return dxt, ds, dd
+
+
+def act_fakequant_bwd_noalloc_into(X, bits, dX_dq, dX_tilde, d_s, d_delta, s=None, delta=None,
+                                   stream=None):
+    """oq_act_fakequant_bwd_noalloc into caller-provided outputs (any may be
+    None): the column partials live in the library's static device scratch,
+    so the call allocates nothing."""
+    T, Cw = X.shape
+    _check(lib().oq_act_fakequant_bwd_noalloc(_ptr(X), _dt(X), T, Cw, bits, _ptr(s), _ptr(delta),
+                                              _ptr(_f32(dX_dq, "dX_dq")), _ptr(dX_tilde),
+                                              _ptr(d_s), _ptr(d_delta), _stream(stream)))
 
 
 def let_init(X, Ws, stream=None):

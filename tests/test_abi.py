@@ -193,3 +193,22 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(oq, "_lib", None)
     with pytest.raises(oq.OQError):
         oq.lib()
+
+
+def test_act_bwd_noalloc_limits():
+    """The allocation-free activation backward refuses, before any launch,
+    sizes whose column partials exceed its static scratch, and bad pointers."""
+    L = oq.lib()
+    lim = 32 * 1024 * 1024
+    n = C.c_size_t(0)
+    assert L.oq_act_fakequant_bwd_workspace_size(1000, 11008, C.byref(n)) == OK
+    assert n.value > lim
+    assert L.oq_act_fakequant_bwd_noalloc(FAKE, oq.OQ_BF16, 1000, 11008, 4, None, None, FAKE,
+                                          None, FAKE, None, None) == UNSUPPORTED
+    assert b"scratch" in L.oq_last_error()
+    assert L.oq_act_fakequant_bwd_noalloc(FAKE, oq.OQ_BF16, 1000, 11008, 4, None, None, MISALIGNED,
+                                          None, FAKE, None, None) == INVALID
+    assert L.oq_act_fakequant_bwd_noalloc(FAKE, oq.OQ_BF16, 16, 256, 9, None, None, FAKE,
+                                          None, FAKE, None, None) == UNSUPPORTED
+    assert L.oq_act_fakequant_bwd_workspace_size(1 << 20, 4096, C.byref(n)) == OK
+    assert n.value <= lim        # 4096 channels fit at any token count
