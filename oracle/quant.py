@@ -34,10 +34,15 @@ def clip_strength(logit, ft=np.float32):
 
 def bf16_round(x):
     """Round fp32 values to the nearest bfloat16 (ties to even); fp32 result."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    lsb = (u >> np.uint64(16)) & np.uint64(1)
-    r = ((u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)) << np.uint64(16)
-    return r.astype(np.uint32).view(np.float32).reshape(np.shape(x))
+    # add 0x7FFF plus the lowest kept bit, then clear the 16 dropped bits: a
+    # tie rounds to the even neighbour.  Finite inputs never carry past bit
+    # 31 (the largest finite magnitude is 0x7F7FFFFF), so uint32 suffices.
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (u >> np.uint32(16)) & np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r &= np.uint32(0xFFFF0000)
+    return r.view(np.float32).reshape(np.shape(x))
 
 
 def minmax_quant_rows(wt, gamma, beta, bits, ft=np.float32):

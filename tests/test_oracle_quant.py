@@ -53,6 +53,12 @@ def test_bf16_round_matches_library_conversion():
     ours = bf16_round(x)
     lib = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).float().numpy()
     assert np.array_equal(ours.view(np.uint32), lib.view(np.uint32))
+    # random bit patterns over the whole finite fp32 range (normals, subnormals)
+    u = rng.integers(0, 2 ** 32, 2_000_000, dtype=np.uint64).astype(np.uint32)
+    xf = u.view(np.float32)
+    xf = xf[np.isfinite(xf)]
+    lib = torch.from_numpy(xf.copy()).to(torch.bfloat16).float().numpy()
+    assert np.array_equal(bf16_round(xf).view(np.uint32), lib.view(np.uint32))
     assert bf16_round(np.float32([1 + 2 ** -8]))[0] == 1.0                 # tie to even (down)
     assert bf16_round(np.float32([1 + 3 * 2 ** -8]))[0] == np.float32(1 + 2 ** -6)  # tie to even (up)
 
