@@ -70,3 +70,82 @@ def normwise(got, ref):
     ref = np.asarray(ref, np.float64)
     den = np.max(np.abs(ref))
     return float(np.max(np.abs(got - ref)) / den) if den > 0 else float(np.max(np.abs(got)))
+
+
+def elemwise(got, ref, floor=1e-3):
+    """Per-element relative error max_i |g_i - r_i| / max(|r_i|, floor * max|r|):
+    each entry is held to its own size, except that the denominator never
+    drops below ``floor`` of the tensor's largest entry (entries near zero
+    after cancellation carry only absolute rounding)."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if ref.size == 0:
+        return 0.0
+    top = np.max(np.abs(ref))
+    if top == 0:
+        return float(np.max(np.abs(got)))
+    den = np.maximum(np.abs(ref), floor * top)
+    return float(np.max(np.abs(got - ref) / den))
+
+
+U32 = 2.0 ** -24      # unit roundoff of fp32
+
+
+def quant_grad_bounds(st, G):
+    """Per-element bounds on the fp32 straight-through backward of Eq. 2 (one
+    group or token row per row of the oracle's forward record ``st``) against
+    the oracle's fp64 result, derived from the arithmetic: each group sum
+    S_h = sum g((q - z) - m u), S_z = sum g (1 - m) over n terms carries at
+    most (n + 8) u times the sum of its terms' magnitudes (any summation
+    order), and each later fp32 operation one more rounding u of its result.
+    Returns (dx_bound [rows, n], dgamma_bound [rows], dbeta_bound [rows]);
+    the last two bound the logit gradients (sigmoid chain included).
+
+    Only the elements that receive the max/min gradient carry more than the
+    exact g*m, so an error at any other element, or a max/min gradient sent
+    to a tied copy instead of the lowest index, exceeds the bound."""
+    g = np.asarray(G, np.float64).reshape(st["q"].shape)
+    q, u, m = (st[k].astype(np.float64) for k in ("q", "u", "m"))
+    z = st["z"].astype(np.float64)[:, None]
+    h = st["h"].astype(np.float64)
+    b = st["b"].astype(np.float64)
+    mx, mn = st["mx"].astype(np.float64), st["mn"].astype(np.float64)
+    gam, bet = st["gamma"].astype(np.float64), st["beta"].astype(np.float64)
+    qmax = float(st["qmax"])
+    n = g.shape[1]
+    eps = (n + 8) * U32
+    a_h = np.sum(np.abs(g * ((q - z) - m * u)), axis=1)
+    a_z = np.sum(np.abs(g * (1.0 - m)), axis=1)
+    s_h = np.sum(g * ((q - z) - m * u), axis=1)
+    s_z = np.sum(g * (1.0 - m), axis=1)
+    boh = np.abs(b / h)
+    dh = s_h - s_z * b / h
+    e_dh = eps * (a_h + a_z * boh) + 4 * U32 * (np.abs(s_h) + np.abs(s_z) * boh)
+    e_dh = np.where(st["hclamp"], 0.0, e_dh)
+    da = np.where(st["hclamp"], 0.0, dh) / qmax
+    db = s_z - da
+    e_da = e_dh / qmax + 2 * U32 * np.abs(da)
+    e_db = eps * a_z + e_da + 2 * U32 * np.abs(db)
+    e_dmx = gam * e_da + 2 * U32 * np.abs(da * gam)
+    e_dmn = bet * e_db + 2 * U32 * np.abs(db * bet)
+    ref = g * m
+    dx_b = 2 * U32 * np.abs(ref)
+    rows = np.arange(g.shape[0])
+    dx_b[rows, st["i_mx"]] += e_dmx + 2 * U32 * np.abs(da * gam)
+    dx_b[rows, st["i_mn"]] += e_dmn + 2 * U32 * np.abs(db * bet)
+    sig_g, sig_b = gam * (1 - gam), bet * (1 - bet)
+    dg_b = np.abs(mx) * sig_g * e_da + 4 * U32 * np.abs(da * mx * sig_g)
+    db_b = np.abs(mn) * sig_b * e_db + 4 * U32 * np.abs(db * mn * sig_b)
+    return dx_b, dg_b, db_b
+
+
+def within(got, ref, bound, name):
+    """Assert |got - ref| <= bound elementwise; report the worst ratio."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    bound = np.broadcast_to(np.asarray(bound, np.float64), ref.shape)
+    err = np.abs(got - ref)
+    ratio = float(np.max(err / np.maximum(bound, 1e-300))) if err.size else 0.0
+    bad = err > bound
+    assert not np.any(bad), (name, int(np.sum(bad)), ratio, np.argwhere(bad)[:5].tolist())
+    return ratio

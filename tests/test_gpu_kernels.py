@@ -13,7 +13,7 @@ from oracle.block import fp_target as fp_target_ref
 from oracle.let import let_bias, let_init as let_init_ref, let_w, let_x
 from oracle.quant import act_bwd, act_fwd, bf16_round, lwc_bwd, lwc_fwd
 from paper_2308_13137_amd import inputs, oq
-from tests.cases import bf16_exact, dev, normwise
+from tests.cases import U32, bf16_exact, dev, normwise, quant_grad_bounds, within
 
 pytestmark = pytest.mark.gpu
 
@@ -36,6 +36,9 @@ def test_matmul_nt_bf16(M, N, K):
     ref = A.astype(np.float64) @ B.astype(np.float64).T
     got = host(oq.matmul_nt(dev(A, torch.bfloat16), dev(B, torch.bfloat16)))
     assert normwise(got, ref) < TOL_GEMM
+    # bf16 x bf16 products are exact in fp32: only the K-term fp32 sum rounds
+    within(got, ref, (K + 2) * U32 * (np.abs(A).astype(np.float64) @ np.abs(B).T.astype(np.float64)),
+           "C")
     got16 = host(oq.matmul_nt(dev(A, torch.bfloat16), dev(B, torch.bfloat16), torch.bfloat16))
     assert np.max(np.abs(got16 - ref) / (np.abs(ref) + 1e-3 * np.max(np.abs(ref)))) < 2 ** -7
 
@@ -56,6 +59,8 @@ def test_matmul_operand_layouts(M, N, K, a_mn, b_mn):
     Bd = dev(np.ascontiguousarray(B.T) if b_mn else B, torch.bfloat16)
     got = host(oq.matmul(Ad, Bd, a_mn=a_mn, b_mn=b_mn))
     assert normwise(got, ref) < TOL_GEMM
+    within(got, ref, (K + 2) * U32 * (np.abs(A).astype(np.float64) @ np.abs(B).T.astype(np.float64)),
+           "C")
 
 
 def test_matmul_operand_layout_unsupported():
@@ -95,6 +100,15 @@ def test_fp_target(bf16):
         assert normwise(got, ref.T) <= 2.0 ** -8
     else:
         assert normwise(got, ref.T) < TOL_GEMM
+    # per element: the fp32 accumulator's error bound, then (bf16 target) at
+    # most one bf16 step more than the oracle's single rounding
+    acc = (np.abs(X).astype(np.float64) @ np.abs(W).T.astype(np.float64) + np.abs(B)[None, :]).T
+    bound = (c_in + 3) * U32 * acc
+    if bf16:
+        # two roundings to bf16 of values that close can land one bf16 step
+        # (at most 2^-7 relative) apart
+        bound = bound * (1 + 2.0 ** -7) + 2.0 ** -7 * np.abs(ref.T)
+    within(got, ref.T, bound, "Y_fp")
 
 
 # ---------------------------------------------------------------- LWC
@@ -167,6 +181,11 @@ def test_lwc_bwd(case):
     assert normwise(host(db), ref["d_beta_logit"]) < TOL_FP32
     assert normwise(host(dwt), ref["dW_tilde"]) < TOL_FP32
     assert normwise(host(ds), ref["d_s"]) < TOL_FP32
+    # per element, within the bound the fp32 arithmetic allows
+    bx, bg, bb = quant_grad_bounds(st, G)
+    within(host(dwt), ref["dW_tilde"], bx.reshape(G.shape), "dW~")
+    within(host(dg), ref["d_gamma_logit"], bg.reshape(dg.shape), "d_gamma_logit")
+    within(host(db), ref["d_beta_logit"], bb.reshape(db.shape), "d_beta_logit")
 
 
 # ---------------------------------------------------------------- activations
@@ -219,8 +238,11 @@ def test_act_bwd(case):
     rng = np.random.default_rng(case["T"])
     G = rng.standard_normal(X.shape).astype(np.float32)
     xt = let_x(X, s, d) if case["let"] else X
+    bx = None
     if case["bits"] < 16:
-        dxt = act_bwd(act_fwd(xt, case["bits"]), G)
+        st = act_fwd(xt, case["bits"])
+        dxt = act_bwd(st, G)
+        bx, _, _ = quant_grad_bounds(st, G)
     else:
         dxt = G.astype(np.float64)
     sv = np.ones(X.shape[1]) if s is None else s.astype(np.float64)
@@ -230,6 +252,10 @@ def test_act_bwd(case):
                                       s=None if s is None else dev(s),
                                       delta=None if d is None else dev(d))
     assert normwise(host(gx), dxt) < TOL_FP32
+    if bx is not None:
+        within(host(gx), dxt, bx, "dX~")
+    else:
+        assert np.array_equal(host(gx), G)
     assert normwise(host(ds), ref_ds) < TOL_FP32
     assert normwise(host(dd), ref_dd) < TOL_FP32
 

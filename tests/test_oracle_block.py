@@ -142,6 +142,44 @@ def test_row_decomposition_of_lwc_only_step():
     np.testing.assert_allclose(out3["d_beta_logit"][0], out["d_beta_logit"][0][rows], rtol=1e-12)
 
 
+@pytest.mark.parametrize("let,act,bf16", [(False, 16, True), (False, 16, False), (True, 4, True)])
+def test_token_decomposition_of_the_step(let, act, bf16):
+    """Every term of the step is a sum over tokens for fixed parameters (the
+    per-token quantiser reads only its own row), so the step over token
+    chunks, each normalised by the whole token count, adds up to the step
+    over all tokens: loss, row losses and every parameter gradient.  This is
+    what lets the full-size checks run the oracle chunk by chunk."""
+    rng = np.random.default_rng(5 + int(let) + 2 * int(bf16))
+    T, n_chunks = 24, 3
+    desc = _tiny_desc(T=T, c_in=32, c_out=10, g=8, bits=3, let=let, act=act, n_lin=2, bf16=bf16)
+    X, Y, p = _tiny_params(desc, rng, bias=let)
+    loss, out = block_step(desc, X, Y, p)
+    step = T // n_chunks
+    tot_loss = 0.0
+    acc = None
+    for c in range(n_chunks):
+        dc = _tiny_desc(T=step, c_in=32, c_out=10, g=8, bits=3, let=let, act=act, n_lin=2, bf16=bf16)
+        for lin in dc["linears"]:
+            lin["mean_rows"] = lin["c_out"] * n_chunks
+        sl = slice(c * step, (c + 1) * step)
+        lc, oc = block_step(dc, [x[sl] for x in X], [y[sl] for y in Y], p)
+        tot_loss += lc
+        part = {k: [None if a is None else np.asarray(a, np.float64) for a in oc[k]]
+                for k in ("d_gamma_logit", "d_beta_logit", "d_s", "d_delta", "row_loss")}
+        if acc is None:
+            acc = part
+        else:
+            for k in acc:
+                acc[k] = [None if a is None else a + b for a, b in zip(acc[k], part[k])]
+    np.testing.assert_allclose(tot_loss, loss, rtol=1e-12)
+    for k in acc:
+        for a, b in zip(acc[k], out[k]):
+            if b is None:
+                assert a is None
+            else:
+                np.testing.assert_allclose(a, b, rtol=1e-9, atol=1e-12 * np.max(np.abs(b)))
+
+
 # ---------------------------------------------------------------- straight-through gradients
 FD_CASES = [
     dict(bits=2, g=8), dict(bits=3, g=8), dict(bits=4, g=8),
