@@ -19,13 +19,17 @@ of every gradient).
 
 Description (plain dicts):
   desc  = {"T": tokens, "bf16": bool,
-           "sites":   [{"width": C, "let": bool, "act_bits": 16 | N}, ...],
+           "sites":   [{"width": C, "let": bool, "act_bits": 16 | N,
+                        "act_sym": bool (optional: symmetric absmax Q_a)}, ...],
            "linears": [{"site": k, "c_out": C_out, "bits": N, "group": g,
+                        "quant": "lwc" | "pact" | "lsq" (optional, default LWC),
                         "mean_rows": C_out_whole (optional)}, ...]}
   X_q   = [ [T, C_k] per site ]            (the quantised model's input x_q)
   Y_fp  = [ [T, C_out_l] per linear ]      (the full-precision target x_fp)
   params= {"W": [[C_out, C_in]], "B": [[C_out] | None],
            "gamma_logit": [[C_out, C_in/g]], "beta_logit": [...],
+                (for PACT these hold the thresholds hi, lo; for LSQ the step h
+                 and zero point z of each group)
            "s": [[C_k] | None per site], "delta": [...]}
 
 With ``bf16`` the matrix-product operands (X^, W^, dY) are rounded to bf16,
@@ -33,7 +37,8 @@ as the kernels feed them to the matrix cores; sums are fp64 throughout.
 """
 import numpy as np
 
-from .quant import act_bwd, act_fwd, bf16_round, lwc_bwd, lwc_fwd
+from .quant import (act_bwd, act_fwd, act_sym_bwd, act_sym_fwd, bf16_round, lsq_bwd, lsq_fwd,
+                    lwc_bwd, lwc_fwd, pact_bwd, pact_fwd)
 from .let import let_bias, let_x
 
 
@@ -56,7 +61,8 @@ def block_forward(desc, X_q, Y_fp, params, ft=np.float32):
         else:
             rec["xt"] = x
         if site["act_bits"] < 16:
-            rec["act"] = act_fwd(rec["xt"], site["act_bits"], ft)
+            fwd = act_sym_fwd if site.get("act_sym") else act_fwd
+            rec["act"] = fwd(rec["xt"], site["act_bits"], ft)
             rec["xhat"] = rec["act"]["X_dq"]
         else:
             rec["xhat"] = rec["xt"]
@@ -70,8 +76,9 @@ def block_forward(desc, X_q, Y_fp, params, ft=np.float32):
         site = sites[k]
         W = np.asarray(params["W"][l], dtype=ft)
         s = params["s"][k] if site["let"] else None
-        st = lwc_fwd(W, params["gamma_logit"][l], params["beta_logit"][l],
-                     lin["bits"], lin["group"], s=s, ft=ft)
+        fwd = {"lwc": lwc_fwd, "pact": pact_fwd, "lsq": lsq_fwd}[lin.get("quant", "lwc")]
+        st = fwd(W, params["gamma_logit"][l], params["beta_logit"][l],
+                 lin["bits"], lin["group"], s=s, ft=ft)
         B = params["B"][l] if params.get("B") is not None else None
         if site["let"]:
             Bt = let_bias(W, B, params["delta"][k], ft)
@@ -110,9 +117,16 @@ def block_step(desc, X_q, Y_fp, params, ft=np.float32):
         k = lin["site"]
         rec = L[l]
         dWdq = rec["dY"].T @ S[k]["xop"]                # [C_out, C_in], fp64 sum over tokens
-        g = lwc_bwd(rec["st"], dWdq, W=rec["W"], with_s=sites[k]["let"])
-        d_gl.append(g["d_gamma_logit"])
-        d_bl.append(g["d_beta_logit"])
+        quant = lin.get("quant", "lwc")
+        if quant == "lwc":
+            g = lwc_bwd(rec["st"], dWdq, W=rec["W"], with_s=sites[k]["let"])
+            d_gl.append(g["d_gamma_logit"])
+            d_bl.append(g["d_beta_logit"])
+        else:
+            bwd = pact_bwd if quant == "pact" else lsq_bwd
+            g = bwd(rec["st"], dWdq, W=rec["W"], with_s=sites[k]["let"])
+            d_gl.append(g["d_p1"])
+            d_bl.append(g["d_p2"])
         row_loss.append(rec["row_loss"])
         if sites[k]["let"]:
             ds_w[k] += g["d_s"]                          # W~ = s (.) W
@@ -126,7 +140,8 @@ def block_step(desc, X_q, Y_fp, params, ft=np.float32):
             d_delta.append(None)
             continue
         if site["act_bits"] < 16:
-            dxt = act_bwd(S[k]["act"], dXhat[k])        # through Q_a (straight-through)
+            bwd = act_sym_bwd if site.get("act_sym") else act_bwd
+            dxt = bwd(S[k]["act"], dXhat[k])            # through Q_a (straight-through)
         else:
             dxt = dXhat[k]                              # X^ = X~
         s = np.asarray(params["s"][k], np.float64)

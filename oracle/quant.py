@@ -184,3 +184,174 @@ def act_bwd(st, dX_dq):
     """Straight-through backward of :func:`act_fwd`: dL/dX~ (no learnable
     parameters inside Q_a; its scale still carries gradient)."""
     return minmax_quant_rows_bwd(st, dX_dq, need_ratio_grads=False)["dx"]
+
+
+# ---------------------------------------------------------------- quantiser variants
+# The paper's appendix compares LWC with PACT and LSQ "by replacing LWC in our
+# pipeline" (weight clipping only), and names symmetric uniform quantisation
+# as the other format of the field.  Their readings here:
+#   * PACT learns the clipping thresholds themselves, one upper (hi) and one
+#     lower (lo) per group, initialised to the group's max and min; the grid
+#     spans [lo, hi] exactly as Eq. 2 spans [beta*min, gamma*max]; PACT's own
+#     straight-through rule treats the quantiser as the identity on the
+#     clipped weight, so dL/dhi sums the gradient of the elements whose code
+#     saturates at qmax, dL/dlo of those at 0, and dL/dw = g*m.
+#   * LSQ learns the step size h and the zero point z directly (initialised
+#     to MinMax's), with z rounded in the forward; its straight-through rule
+#     gives rint derivative 1 (codes and zero point), and its gradient scale
+#     1/sqrt(n * qmax) (n = group size) multiplies dL/dh and dL/dz.
+#   * Symmetric per-token activation quantisation: h = max|x| / (2^(N-1) - 1)
+#     (floored at 1e-5), zero point fixed at 2^(N-1), so codes span
+#     [1, 2^N - 1] around it; the gradient of the row's absolute maximum goes
+#     to the lowest index holding it, with that element's sign.
+
+
+def _grid_rows(wt, a, b, h_direct, z_direct, bits, ft):
+    """Eq. 2's grid with given bounds (a, b) or a given step / zero point."""
+    qmax = ft(2 ** bits - 1)
+    if h_direct is None:
+        h_raw = (a - b) / qmax
+    else:
+        h_raw = np.asarray(h_direct, ft)
+    hclamp = h_raw < ft(H_MIN)
+    h = np.where(hclamp, ft(H_MIN), h_raw).astype(ft)
+    r = ft(1.0) / h
+    if z_direct is None:
+        z = -np.rint(b * r)
+    else:
+        z = np.rint(np.asarray(z_direct, ft))
+    u = wt * r[:, None]
+    c = np.rint(u) + z[:, None]
+    m = (c >= 0) & (c <= qmax)
+    q = np.clip(c, ft(0), qmax).astype(ft)
+    wdq = (q - z[:, None]) * h[:, None]
+    return dict(h=h, hclamp=hclamp, r=r, z=z, u=u, c=c, m=m, q=q, wdq=wdq, qmax=qmax, bits=bits)
+
+
+def _as_layer(st, wt, c_out, c_in, group):
+    ng = c_in // group
+    st["wt"] = wt
+    st["shape"] = (c_out, c_in, group)
+    st["codes"] = st["q"].reshape(c_out, c_in).astype(np.uint8)
+    st["W_dq"] = st["wdq"].reshape(c_out, c_in)
+    st["h_g"] = st["h"].reshape(c_out, ng)
+    st["z_g"] = st["z"].reshape(c_out, ng)
+    return st
+
+
+def pact_fwd(W, hi, lo, bits, group, s=None, ft=np.float32):
+    """PACT weight clipping in LWC's place: learned thresholds hi, lo
+    [C_out, C_in/g] bound the grid directly (a = hi, b = lo)."""
+    W = np.asarray(W, dtype=ft)
+    c_out, c_in = W.shape
+    wt = W * np.asarray(s, dtype=ft)[None, :] if s is not None else W
+    a = np.asarray(hi, ft).reshape(-1)
+    b = np.asarray(lo, ft).reshape(-1)
+    st = _grid_rows(wt.reshape(-1, group), a, b, None, None, bits, ft)
+    st.update(a=a, b=b, quant="pact")
+    return _as_layer(st, wt, c_out, c_in, group)
+
+
+def pact_bwd(st, dW_dq, W=None, with_s=False):
+    """PACT's straight-through rule: dhi = sum g [code above qmax],
+    dlo = sum g [code below 0], dW~ = g*m."""
+    c_out, c_in, group = st["shape"]
+    ng = c_in // group
+    g = np.asarray(dW_dq, np.float64).reshape(-1, group)
+    c = st["c"].astype(np.float64)
+    m = st["m"].astype(np.float64)
+    out = dict(d_p1=np.sum(g * (c > float(st["qmax"])), axis=1).reshape(c_out, ng),
+               d_p2=np.sum(g * (c < 0), axis=1).reshape(c_out, ng),
+               dW_tilde=(g * m).reshape(c_out, c_in))
+    if with_s:
+        out["d_s"] = np.sum(out["dW_tilde"] * np.asarray(W, np.float64), axis=0)
+    return out
+
+
+def lsq_fwd(W, step, zero, bits, group, s=None, ft=np.float32):
+    """LSQ in LWC's place: learned step h and zero point z [C_out, C_in/g]
+    (the zero point is rounded in the forward; the step floored at 1e-5)."""
+    W = np.asarray(W, dtype=ft)
+    c_out, c_in = W.shape
+    wt = W * np.asarray(s, dtype=ft)[None, :] if s is not None else W
+    st = _grid_rows(wt.reshape(-1, group), None, None, np.asarray(step, ft).reshape(-1),
+                    np.asarray(zero, ft).reshape(-1), bits, ft)
+    st.update(quant="lsq", group=group)
+    return _as_layer(st, wt, c_out, c_in, group)
+
+
+def lsq_grad_scale(group, bits):
+    """LSQ's gradient scale 1/sqrt(n * Q_P), n = weights per step size."""
+    return 1.0 / np.sqrt(float(group) * float(2 ** bits - 1))
+
+
+def lsq_bwd(st, dW_dq, W=None, with_s=False):
+    """LSQ's straight-through rule (rint derivative 1 on the codes and the
+    zero point), times the gradient scale:
+      dh = gs * sum g ((q - z) - m u)   (0 where the 1e-5 floor is active)
+      dz = -gs * h * sum g (1 - m),     dW~ = g*m."""
+    c_out, c_in, group = st["shape"]
+    ng = c_in // group
+    g = np.asarray(dW_dq, np.float64).reshape(-1, group)
+    q, u, m = (st[k].astype(np.float64) for k in ("q", "u", "m"))
+    z = st["z"].astype(np.float64)[:, None]
+    h = st["h"].astype(np.float64)
+    gs = lsq_grad_scale(group, st["bits"])
+    s_h = np.sum(g * ((q - z) - m * u), axis=1)
+    s_z = np.sum(g * (1.0 - m), axis=1)
+    out = dict(d_p1=(gs * np.where(st["hclamp"], 0.0, s_h)).reshape(c_out, ng),
+               d_p2=(-gs * h * s_z).reshape(c_out, ng),
+               dW_tilde=(g * m).reshape(c_out, c_in))
+    if with_s:
+        out["d_s"] = np.sum(out["dW_tilde"] * np.asarray(W, np.float64), axis=0)
+    return out
+
+
+def wquant_init(W, bits, group, quant, s=None, ft=np.float32):
+    """MinMax initial parameters of a quantiser variant, per group:
+    PACT (hi, lo) = (max, min); LSQ (h, z) = MinMax's h and z (Eq. 2 at
+    gamma = beta = 1); LWC (gamma_logit, beta_logit) = (4, 4)."""
+    W = np.asarray(W, dtype=ft)
+    c_out, c_in = W.shape
+    ng = c_in // group
+    wt = W * np.asarray(s, dtype=ft)[None, :] if s is not None else W
+    rows = wt.reshape(-1, group)
+    if quant == "lwc":
+        return np.full((c_out, ng), 4.0, ft), np.full((c_out, ng), 4.0, ft)
+    if quant == "pact":
+        return rows.max(axis=1).reshape(c_out, ng), rows.min(axis=1).reshape(c_out, ng)
+    ones = np.ones(rows.shape[0], ft)
+    st = minmax_quant_rows(rows, ones, ones, bits, ft)
+    return st["h"].reshape(c_out, ng), st["z"].reshape(c_out, ng).astype(ft)
+
+
+def act_sym_fwd(Xt, bits, ft=np.float32):
+    """Symmetric per-token absmax fake-quant: h = max(absmax/(2^(N-1)-1), 1e-5),
+    z = 2^(N-1), codes clamp(rint(x/h) + z, 0, 2^N - 1)."""
+    Xt = np.asarray(Xt, dtype=ft)
+    qs = ft(2 ** (bits - 1) - 1)
+    ax = np.abs(Xt)
+    i_ab = np.argmax(ax, axis=1)                     # lowest index of the largest |x|
+    rows = np.arange(Xt.shape[0])
+    amax = ax[rows, i_ab]
+    sgn = np.where(Xt[rows, i_ab] < 0, -1.0, 1.0)
+    st = _grid_rows(Xt, None, None, amax / qs, np.full(Xt.shape[0], ft(2 ** (bits - 1))), bits, ft)
+    st.update(i_ab=i_ab, amax=amax, sgn=sgn, qs=qs, sym=True)
+    st["codes"] = st["q"].astype(np.uint8)
+    st["X_dq"] = st["wdq"]
+    return st
+
+
+def act_sym_bwd(st, dX_dq):
+    """Straight-through backward of :func:`act_sym_fwd`: dx = g*m plus, at
+    the row's absmax element, sign * dh / (2^(N-1) - 1) with
+    dh = sum g ((q - z) - m u) (0 under the floor)."""
+    g = np.asarray(dX_dq, np.float64)
+    q, u, m = (st[k].astype(np.float64) for k in ("q", "u", "m"))
+    z = st["z"].astype(np.float64)[:, None]
+    s_h = np.sum(g * ((q - z) - m * u), axis=1)
+    dh = np.where(st["hclamp"], 0.0, s_h)
+    dx = g * m
+    rows = np.arange(g.shape[0])
+    np.add.at(dx, (rows, st["i_ab"]), st["sgn"] * dh / float(st["qs"]))
+    return dx
