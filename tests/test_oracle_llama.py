@@ -1,0 +1,248 @@
+"""Pins for the whole-block oracle (oracle/llama_block.py) against things
+other than itself: closed forms of RMSNorm, RoPE and SiLU, the library's
+scaled-dot-product attention and a torch rebuild of the full-precision block,
+the LET equivalences of Eq. 3 and Eq. 5 through the whole block, and central
+finite differences of the frozen-choice surrogate for every trained
+parameter (clipping logits of all seven linears, s and delta of three sites,
+the [Q, K] scale s_a)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import llama_block as lb
+
+
+def tiny_desc(act_bits=4, let=True, H=2, Hkv=1, D=16, F=24, S=6, bits=(3, 4, 4, 3, 4, 3, 4)):
+    return dict(hidden=D, heads=H, kv_heads=Hkv, ffn=F, seq_len=S, norm_eps=1e-6,
+                rope_base=10000.0, w_bits=list(bits), w_group=[8, 8, 16, 8, 8, 16, 8],
+                act_bits=act_bits, let=let)
+
+
+def tiny_params(desc, rng, T):
+    D, H, Hkv, F = desc["hidden"], desc["heads"], desc["kv_heads"], desc["ffn"]
+    d = D // H
+    shapes = [(H * d, D), (Hkv * d, D), (Hkv * d, D), (D, H * d), (F, D), (F, D), (D, F)]
+    W = [rng.standard_normal(sh) * 0.3 for sh in shapes]
+    gl = [rng.uniform(1.0, 4.0, (sh[0], sh[1] // g)) for sh, g in zip(shapes, desc["w_group"])]
+    bl = [rng.uniform(1.0, 4.0, a.shape) for a in gl]
+    p = dict(W=W, gamma_logit=gl, beta_logit=bl, g1=rng.uniform(0.5, 1.5, D),
+             g2=rng.uniform(0.5, 1.5, D),
+             s=[rng.uniform(0.5, 2.0, D), rng.uniform(0.5, 2.0, H * d), rng.uniform(0.5, 2.0, D)],
+             delta=[rng.standard_normal(D) * 0.2, rng.standard_normal(H * d) * 0.2,
+                    rng.standard_normal(D) * 0.2],
+             s_a=rng.uniform(0.5, 2.0, Hkv * d))
+    h0 = rng.standard_normal((T, D))
+    target = lb.fp_block(desc, h0, p) + rng.standard_normal((T, D)) * 0.05
+    return h0, target, p
+
+
+# ---------------------------------------------------------------- smooth pieces
+def test_rmsnorm_closed_form():
+    y, rstd = lb.rmsnorm(np.array([[3.0, 4.0]]), np.array([1.0, 2.0]), 0.0)
+    r = 1.0 / np.sqrt(12.5)
+    np.testing.assert_allclose(y[0], [3 * r, 8 * r], rtol=1e-15)
+    np.testing.assert_allclose(rstd[0], r, rtol=1e-15)
+
+
+def test_rmsnorm_backward_is_its_jacobian():
+    rng = np.random.default_rng(1)
+    h, g, dy = rng.standard_normal((3, 8)), rng.uniform(0.5, 2, 8), rng.standard_normal((3, 8))
+    _, rstd = lb.rmsnorm(h, g, 1e-6)
+    an = lb.rmsnorm_bwd(h, g, rstd, dy)
+    fd = np.zeros_like(h)
+    for i in range(3):
+        for j in range(8):
+            e = np.zeros_like(h)
+            e[i, j] = 1e-6
+            fd[i, j] = np.sum(dy * (lb.rmsnorm(h + e, g, 1e-6)[0] - lb.rmsnorm(h - e, g, 1e-6)[0])) / 2e-6
+    np.testing.assert_allclose(an, fd, rtol=1e-7, atol=1e-9)
+
+
+def test_rope_closed_forms():
+    # d = 2, base irrelevant: the pair (x0, x1) turns by the position angle
+    cos, sin = lb.rope_angles(4, 4, 2, 10000.0)
+    y = lb.rope(np.tile([[1.0, 0.0]], (4, 1)), 1, 2, cos, sin)
+    np.testing.assert_allclose(y, np.stack([np.cos(np.arange(4)), np.sin(np.arange(4))], 1), atol=1e-15)
+    rng = np.random.default_rng(2)
+    d, S = 8, 7
+    cos, sin = lb.rope_angles(2 * S, S, d, 10000.0)
+    x = rng.standard_normal((2 * S, 2 * d))
+    y = lb.rope(x, 2, d, cos, sin)
+    np.testing.assert_allclose(y[0], x[0], atol=0)                  # position 0: identity
+    np.testing.assert_allclose(y[S], x[S], atol=0)                  # each sample restarts
+    # norms of the pairs (i, i + d/2) are kept; the inverse undoes it
+    pr = lambda z: z.reshape(-1, 2, 2, d // 2)
+    np.testing.assert_allclose(np.hypot(pr(y)[:, :, 0], pr(y)[:, :, 1]),
+                               np.hypot(pr(x)[:, :, 0], pr(x)[:, :, 1]), rtol=1e-13)
+    np.testing.assert_allclose(lb.rope(y, 2, d, cos, sin, inverse=True), x, atol=1e-14)
+    # <R_m q, R_n k> depends on m - n only
+    q, k = rng.standard_normal(d), rng.standard_normal(d)
+    cos, sin = lb.rope_angles(S, S, d, 10000.0)
+    Rq = lb.rope(np.tile(q, (S, 1)), 1, d, cos, sin)
+    Rk = lb.rope(np.tile(k, (S, 1)), 1, d, cos, sin)
+    np.testing.assert_allclose(Rq[5] @ Rk[3], Rq[2] @ Rk[0], rtol=1e-12)
+
+
+def test_silu_closed_form():
+    np.testing.assert_allclose(lb.silu(np.array([0.0, 1.0])), [0.0, 1 / (1 + np.exp(-1.0))])
+    x = np.linspace(-4, 4, 9)
+    fd = (lb.silu(x + 1e-7) - lb.silu(x - 1e-7)) / 2e-7
+    np.testing.assert_allclose(lb.silu_grad(x), fd, rtol=1e-7)
+
+
+@pytest.mark.parametrize("H,Hkv", [(2, 2), (4, 2), (4, 1)])
+def test_attention_matches_library_sdpa(H, Hkv):
+    rng = np.random.default_rng(3)
+    d, S, ns = 8, 7, 2
+    q = rng.standard_normal((ns * S, H * d))
+    k = rng.standard_normal((ns * S, Hkv * d))
+    v = rng.standard_normal((ns * S, Hkv * d))
+    out, P = lb.attention(q, k, v, H, Hkv, d, S)
+    tq = torch.from_numpy(q).reshape(ns, S, H, d).transpose(1, 2)
+    tk = torch.from_numpy(k).reshape(ns, S, Hkv, d).transpose(1, 2).repeat_interleave(H // Hkv, 1)
+    tv = torch.from_numpy(v).reshape(ns, S, Hkv, d).transpose(1, 2).repeat_interleave(H // Hkv, 1)
+    ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, is_causal=True)
+    np.testing.assert_allclose(out, ref.transpose(1, 2).reshape(ns * S, H * d).numpy(), rtol=1e-12,
+                               atol=1e-12)
+    # the backward against torch's autograd of the same library routine
+    do = rng.standard_normal(out.shape)
+    dq, dk, dv = lb.attention_bwd(q, k, v, P, do, H, Hkv, d, S)
+    tq2 = torch.from_numpy(q).requires_grad_()
+    tk2 = torch.from_numpy(k).requires_grad_()
+    tv2 = torch.from_numpy(v).requires_grad_()
+    o = torch.nn.functional.scaled_dot_product_attention(
+        tq2.reshape(ns, S, H, d).transpose(1, 2),
+        tk2.reshape(ns, S, Hkv, d).transpose(1, 2).repeat_interleave(H // Hkv, 1),
+        tv2.reshape(ns, S, Hkv, d).transpose(1, 2).repeat_interleave(H // Hkv, 1), is_causal=True)
+    o.transpose(1, 2).reshape(ns * S, H * d).backward(torch.from_numpy(do))
+    for a, b in ((dq, tq2), (dk, tk2), (dv, tv2)):
+        np.testing.assert_allclose(a, b.grad.numpy(), rtol=1e-10, atol=1e-12)
+
+
+def test_fp_block_matches_a_torch_llama_block():
+    """The full-precision block against the same block written with torch's
+    own ops (RMSNorm by formula, RoPE by complex multiplication, the
+    library's causal attention, SiLU)."""
+    rng = np.random.default_rng(4)
+    desc = tiny_desc(H=4, Hkv=2)
+    T = 12
+    h0, _, p = tiny_params(desc, rng, T)
+    ours = lb.fp_block(desc, h0, p)
+    D, H, Hkv, S = 16, 4, 2, 6
+    d = D // H
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    h = t(h0)
+
+    def norm(x, g):
+        return x * torch.rsqrt(x.pow(2).mean(-1, keepdim=True) + 1e-6) * t(g)
+
+    pos = torch.arange(T) % S
+    freq = 10000.0 ** (-torch.arange(0, d // 2, dtype=torch.float64) * 2 / d)
+    rot = torch.polar(torch.ones(T, d // 2, dtype=torch.float64), pos[:, None] * freq[None, :])
+
+    def rope(x, nh):
+        x = x.reshape(T, nh, d)
+        z = torch.complex(x[..., : d // 2], x[..., d // 2:]) * rot[:, None, :]
+        return torch.cat([z.real, z.imag], -1)
+
+    W = [t(w) for w in p["W"]]
+    x1 = norm(h, p["g1"])
+    q = rope(x1 @ W[0].T, H).reshape(T // S, S, H, d).transpose(1, 2)
+    k = rope(x1 @ W[1].T, Hkv).reshape(T // S, S, Hkv, d).transpose(1, 2).repeat_interleave(H // Hkv, 1)
+    v = (x1 @ W[2].T).reshape(T // S, S, Hkv, d).transpose(1, 2).repeat_interleave(H // Hkv, 1)
+    a = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True)
+    h1 = h + a.transpose(1, 2).reshape(T, D) @ W[3].T
+    x3 = norm(h1, p["g2"])
+    ref = h1 + (torch.nn.functional.silu(x3 @ W[4].T) * (x3 @ W[5].T)) @ W[6].T
+    np.testing.assert_allclose(ours, ref.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_let_is_an_equivalence_through_the_whole_block():
+    """Eq. 3 (s, delta on three sites, folded into the weights and biases) and
+    Eq. 5 (s_a on Q and K) change nothing without quantisation: the block's
+    loss equals that of the full-precision block for any s, delta, s_a."""
+    rng = np.random.default_rng(5)
+    desc = dict(tiny_desc(act_bits=16, let=True), w_quant=False)
+    T = 12
+    h0, target, p = tiny_params(desc, rng, T)
+    fp = lb.fp_block(desc, h0, p)
+    ref = float(np.mean((fp - target) ** 2))
+    loss, c = lb.block_forward(desc, h0, target, p, ft=np.float64)
+    np.testing.assert_allclose(loss, ref, rtol=1e-12)
+    np.testing.assert_allclose(c["h2"], fp, rtol=1e-11, atol=1e-12)
+    # a wrong sign in the [Q, K] scale (s_a on both sides) breaks it
+    p2 = dict(p, s_a=p["s_a"] * 1.7)
+    loss2, _ = lb.block_forward(desc, h0, target, p2, ft=np.float64)
+    np.testing.assert_allclose(loss2, ref, rtol=1e-12)
+
+
+# ---------------------------------------------------------------- finite differences
+FD_CASES = [dict(act_bits=4, let=True), dict(act_bits=16, let=True), dict(act_bits=16, let=False),
+            dict(act_bits=3, let=True, H=4, Hkv=2)]
+
+
+@pytest.mark.parametrize("case", FD_CASES, ids=[str(c) for c in FD_CASES])
+def test_block_gradients_match_finite_differences(case):
+    rng = np.random.default_rng(6)
+    desc = tiny_desc(**case)
+    T = 12
+    h0, target, p = tiny_params(desc, rng, T)
+    loss, g = lb.block_step(desc, h0, target, p, ft=np.float64)
+    frz = lb.freeze(desc, h0, target, p)
+    np.testing.assert_allclose(lb.surrogate_loss(desc, h0, target, p, frz), loss, rtol=1e-12)
+    names = [("gamma_logit", "d_gamma_logit"), ("beta_logit", "d_beta_logit")]
+    if desc["let"]:
+        names += [("s", "d_s"), ("delta", "d_delta")]
+    checks = [(n, gn, i) for n, gn in names for i in range(len(p[n]))]
+    if desc["let"]:
+        checks.append(("s_a", "d_s_a", None))
+    rs = np.random.default_rng(7)
+    for name, gname, i in checks:
+        base = p[name] if i is None else p[name][i]
+        an = np.asarray(g[gname] if i is None else g[gname][i]).reshape(-1)
+        idx = rs.choice(base.size, size=min(6, base.size), replace=False)
+        for j in idx:
+            eps = 1e-6 * max(1.0, abs(base.flat[j]))
+            fd = 0.0
+            for sgn in (1, -1):
+                arr = np.array(base, np.float64, copy=True)
+                arr.flat[j] += sgn * eps
+                q = dict(p)
+                if i is None:
+                    q[name] = arr
+                else:
+                    q[name] = list(p[name])
+                    q[name][i] = arr
+                fd += sgn * lb.surrogate_loss(desc, h0, target, q, frz) / (2 * eps)
+            scale = max(np.max(np.abs(an)), 1e-30)
+            # (without activation quantisation s_a cancels exactly: its gradient is 0
+            # and the difference quotient is rounding noise of the loss)
+            assert abs(an[j] - fd) <= 1e-6 * scale + 1e-9 * max(1.0, loss), (name, i, j, an[j], fd)
+
+
+def test_fd_detects_a_planted_error_in_the_attention_backward():
+    """A 1% error planted in the attention backward's dQ makes the
+    finite-difference check of s_a fail (with activation quantisation on, s_a
+    carries a gradient)."""
+    rng = np.random.default_rng(8)
+    desc = tiny_desc(act_bits=4, let=True)
+    h0, target, p = tiny_params(desc, rng, 12)
+    frz = lb.freeze(desc, h0, target, p)
+    j = 3
+    fd = 0.0
+    for sgn in (1, -1):
+        q = dict(p, s_a=p["s_a"].copy())
+        q["s_a"][j] += sgn * 1e-6
+        fd += sgn * lb.surrogate_loss(desc, h0, target, q, frz) / 2e-6
+    _, g_ok = lb.block_step(desc, h0, target, p, ft=np.float64)
+    good = lb.attention_bwd
+    try:
+        def bad(*a):
+            dq, dk, dv = good(*a)
+            return dq * 1.01, dk, dv
+        lb.attention_bwd = bad
+        _, g_bad = lb.block_step(desc, h0, target, p, ft=np.float64)
+    finally:
+        lb.attention_bwd = good
+    assert abs(g_ok["d_s_a"][j] - fd) <= 1e-6 * abs(fd)
+    assert abs(g_bad["d_s_a"][j] - fd) > 1e-4 * abs(fd)
