@@ -56,6 +56,30 @@ typedef enum {
 
 typedef enum { OQ_F32 = 0, OQ_BF16 = 1 } oq_dtype;
 
+/* Weight quantisers (the appendix compares LWC with PACT and LSQ run in its
+ * place inside the same pipeline, weight clipping only).  Each has two
+ * parameters per group, p1 and p2:
+ *   OQ_WQ_LWC   clip-strength logits (gamma_logit, beta_logit), Eq. 2
+ *   OQ_WQ_PACT  the grid's upper and lower thresholds (hi, lo) learned
+ *               directly: a = hi, b = lo in Eq. 2's order; PACT's
+ *               straight-through rule (identity on the clipped weight):
+ *               d hi = sum of dW^ over codes saturated at 2^N - 1,
+ *               d lo = over codes saturated at 0, dW~ = dW^ * [in range]
+ *   OQ_WQ_LSQ   step h and zero point z learned directly (h floored at
+ *               1e-5, z rounded in the forward); rint has derivative 1 on
+ *               codes and zero point; LSQ's gradient scale 1/sqrt(g (2^N-1))
+ *               multiplies both: d h = gs * sum dW^((q - z) - m w~/h),
+ *               d z = -gs * h * sum dW^(1 - m), dW~ = dW^ * m
+ * Activation quantisation by default is per-token asymmetric MinMax; OR-ing
+ * OQ_ACT_SYM into an activation bit width (2..8) selects symmetric absmax:
+ * h = max(max|x~| / (2^(N-1) - 1), 1e-5), zero point 2^(N-1), codes
+ * clamp(rint(x~/h) + 2^(N-1), 0, 2^N - 1); the gradient of max|x~| goes to
+ * the lowest index holding it, with that element's sign. */
+#define OQ_WQ_LWC 0
+#define OQ_WQ_PACT 1
+#define OQ_WQ_LSQ 2
+#define OQ_ACT_SYM 0x100
+
 const char* oq_status_str(oq_status s);
 const char* oq_last_error(void);
 int oq_version(void);
@@ -93,6 +117,30 @@ oq_status oq_lwc_fakequant_bwd(const void* W, oq_dtype w_dt, int64_t c_out, int6
                                float* dW_tilde, void* ws, size_t ws_bytes, hipStream_t stream);
 oq_status oq_lwc_fakequant_bwd_workspace_size(int64_t c_out, int64_t c_in, int64_t group,
                                               int want_d_s, size_t* bytes);
+
+/* ---------------------------------------------------------------------------
+ * Any weight quantiser (OQ_WQ_*), forward and straight-through backward, with
+ * the arguments and outputs of oq_lwc_fakequant_fwd / _bwd (which are the
+ * OQ_WQ_LWC case); p1, p2 and d_p1, d_p2 are the quantiser's two parameters
+ * per group and their gradients.  Workspace of the backward:
+ * oq_lwc_fakequant_bwd_workspace_size.
+ */
+oq_status oq_wquant_fakequant_fwd(int quantizer, const void* W, oq_dtype w_dt, int64_t c_out,
+                                  int64_t c_in, const float* s, const float* p1, const float* p2,
+                                  int bits, int64_t group, void* W_dq, oq_dtype dq_dt,
+                                  uint8_t* codes, float* h, float* z, hipStream_t stream);
+oq_status oq_wquant_fakequant_bwd(int quantizer, const void* W, oq_dtype w_dt, int64_t c_out,
+                                  int64_t c_in, const float* s, const float* p1, const float* p2,
+                                  int bits, int64_t group, const float* dW_dq, float* d_p1,
+                                  float* d_p2, float* d_s, float* dW_tilde, void* ws,
+                                  size_t ws_bytes, hipStream_t stream);
+/* MinMax starting parameters of a quantiser per group of W~ = s (.) W:
+ * PACT (hi, lo) = (max, min); LSQ (h, z) = Eq. 2's step and zero point at
+ * clip strength 1; LWC logits 4.0 (Sec. 4.1 / the configurations' init).
+ * p1, p2 [c_out, c_in/group] fp32 (outputs). */
+oq_status oq_wquant_init(int quantizer, const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                         const float* s, int bits, int64_t group, float* p1, float* p2,
+                         hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * LET fold for a linear layer (Sec. 3.3, Eq. 3): W~ = s (.) W, B~ = B + delta W.
@@ -242,11 +290,15 @@ typedef struct {
                                               OQ_F32: fp32 everywhere             */
   int64_t site_width[OQ_MAX_SITES];        /* C of each site                       */
   int site_let[OQ_MAX_SITES];              /* 1 = LET on this site                 */
-  int site_act_bits[OQ_MAX_SITES];         /* 2..8, or 16 = no activation quant    */
+  int site_act_bits[OQ_MAX_SITES];         /* 2..8 (| OQ_ACT_SYM), or 16 = none     */
   int lin_site[OQ_MAX_LINEARS];
   int64_t lin_c_out[OQ_MAX_LINEARS];
   int lin_bits[OQ_MAX_LINEARS];
   int64_t lin_group[OQ_MAX_LINEARS];       /* group size along C_in (C_in = per channel) */
+  int lin_quant[OQ_MAX_LINEARS];           /* weight quantiser: OQ_WQ_LWC (0, the default),
+                                              OQ_WQ_PACT or OQ_WQ_LSQ; the params' and
+                                              grads' gamma/beta slots then hold that
+                                              quantiser's two parameters             */
 } oq_block_desc;
 
 typedef struct {                           /* device pointers                      */
@@ -273,9 +325,29 @@ typedef struct {                           /* AdamW state; NULL pointer = no upd
   float* m_delta[OQ_MAX_SITES];   float* v_delta[OQ_MAX_SITES];
   int step;                                /* 1-based step number of this update   */
   double lr_lwc, lr_let, beta1, beta2, eps, wd;
+  /* Iterative LWC/LET training (the ablation on training LWC and LET in
+   * turn): OQ_FREEZE_LWC keeps the clipping logits fixed, OQ_FREEZE_LET keeps
+   * s and delta fixed.  A frozen set is not updated and its AdamW m, v are
+   * not touched; gradient work that only the frozen set needs is skipped
+   * (a frozen LET skips the input-gradient path; a frozen LWC skips the
+   * weight gradient of every site whose LET is absent or frozen), and the
+   * frozen set's gradient outputs are then left unwritten.  0 = train both. */
+  int frozen;
 } oq_block_optim;
+#define OQ_FREEZE_LWC 1
+#define OQ_FREEZE_LET 2
 
 oq_status oq_block_workspace_size(const oq_block_desc* desc, size_t* bytes);
+
+/* The launch plan oq_block_calib_step takes for `desc` (a host query, nothing
+ * launched), OQ_PLAN_FIELDS ints per site k at info[OQ_PLAN_FIELDS * k + i]:
+ *   0  sites run concurrently on side streams      1  gradient products read
+ *   X^ and dY^T as stored (no transposed copies)   2  K-split count of the
+ *   weight gradient   3  K-split count of the forward product   4  LWC
+ *   backward fused into the weight gradient's epilogue   5  input gradient
+ *   reads a transposed copy of W^.   n_info >= OQ_PLAN_FIELDS * n_sites.  */
+#define OQ_PLAN_FIELDS 6
+oq_status oq_block_plan(const oq_block_desc* desc, int* info, int n_info);
 
 /*   Y_fp_T : HOST array [n_linears] of device pointers, each [c_out, T] (Y_fp
  *            channel-major, as oq_fp_target writes it)
@@ -309,6 +381,38 @@ oq_status oq_block_calibrate(const oq_block_desc* desc, int n_segments, int epoc
                              const oq_block_optim* optim, float* losses, void* ws,
                              size_t ws_bytes, hipStream_t stream);
 
+/* Checkpoint / resume of one block's calibration (Algorithm 1 trains each
+ * block for many epochs; a run that stops can continue from its last saved
+ * state).  The state is the learnable set Theta -- clipping logits per
+ * linear, s and delta per LET site -- plus, with `opt`, the AdamW moments m,
+ * v, the hyperparameters and the number of completed updates.
+ *
+ * oq_block_state_save copies the state to host memory and writes `path`
+ * (first to path + ".tmp", then renamed over `path`, so an interrupted save
+ * leaves the previous file intact).  File layout, little-endian: 8-byte
+ * magic "OQCKPT\0\1"; int32 version (1), size of the shape record,
+ * completed_steps, has-AdamW flag; the block's shape record (site widths,
+ * LET flags, activation bits, linear sites, c_out, bits, groups,
+ * quantisers); uint64
+ * tensor count; with AdamW six doubles (lr_lwc, lr_let, beta1, beta2, eps,
+ * wd); then per tensor uint32 kind, uint32 linear/site index, uint64
+ * element count, uint64 FNV-1a hash of its bytes and the fp32 data.
+ *
+ * oq_block_state_load reads and verifies the whole file (magic, version,
+ * shape equal to `desc`'s apart from the token count and dtype, every hash,
+ * every size) before it writes any device buffer, then restores params (and
+ * opt's m, v, hyperparameters, and opt->step = completed_steps + 1, the
+ * number of the next update).  Both synchronise `stream`.  A failed load
+ * changes nothing on the device.  Errors: OQ_ERR_INVALID_ARG (I/O, format,
+ * mismatch), OQ_ERR_HIP.
+ */
+oq_status oq_block_state_save(const oq_block_desc* desc, const oq_block_params* params,
+                              const oq_block_optim* opt, int completed_steps, const char* path,
+                              hipStream_t stream);
+oq_status oq_block_state_load(const oq_block_desc* desc, const oq_block_params* params,
+                              oq_block_optim* opt, int* completed_steps, const char* path,
+                              hipStream_t stream);
+
 /* Algorithm 1's last step for one block ("obtain the quantised block"), on
  * its linear sub-graph: with the learned clipping logits and LET parameters,
  * each linear's weight is transformed (Eq. 3: s (.) W on LET sites) and
@@ -319,13 +423,32 @@ oq_status oq_block_calibrate(const oq_block_desc* desc, int n_segments, int epoc
  *   B_tilde : HOST [n_linears] device pointers [c_out] fp32, or NULL (array or
  *             entry): the folded bias B + delta W on LET sites, else B (0 without B)
  * The deployed linear then reads X~ = (X - delta) / s on LET sites (Eq. 3).
- * C_site % 32 == 0.  Workspace: oq_block_export_workspace_size bytes, 16-byte
- * aligned (the largest linear's u8 codes).  Errors as oq_block_calib_step.
+ * C_site % 32 == 0 (else OQ_ERR_INVALID_ARG); every linear's bits <= 7 and
+ * group % 32 == 0, what oq_packed_linear accepts (else OQ_ERR_UNSUPPORTED).
+ * Workspace: oq_block_export_workspace_size bytes, 16-byte aligned (the
+ * largest linear's u8 codes).  Other errors as oq_block_calib_step.
  */
 oq_status oq_block_export_workspace_size(const oq_block_desc* desc, size_t* bytes);
 oq_status oq_block_export(const oq_block_desc* desc, const oq_block_params* params,
                           uint8_t* const* packed, float* const* h, float* const* z,
                           float* const* B_tilde, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * LET absorbed into the operation that produces a site's input (Sec. 3.3:
+ * after calibration s and delta fold into the preceding normalisation or
+ * linear layer, so the deployed block runs no extra transform; on the
+ * [v, o] pair the attention probabilities sum to 1 over keys, so a shift of
+ * V passes through them).  Row c of P [C, n] in p_dt (a normalisation's
+ * gain is n = 1; a previous linear's weight [C, c_in_prev] has the site's
+ * channels as its output rows) becomes P[c, :] * (1/s[c]), and its bias
+ * b [C] fp32 | NULL (0) becomes (b[c] - delta[c]) * (1/s[c]) in b_out [C]
+ * fp32 -- the same fp32 order as the activation transform (x - delta)*(1/s),
+ * so the absorbed producer emits X~ = (X - delta)/s.  s, delta [C] fp32 |
+ * NULL (ones / zeros).  P_out may be NULL (bias only); P_out may equal P.
+ */
+oq_status oq_let_absorb(const void* P, oq_dtype p_dt, const float* b, int64_t C, int64_t n,
+                        const float* s, const float* delta, void* P_out, float* b_out,
+                        hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Deployment of the calibrated weights (Sec. 4.5 and Table "tab:speed":

@@ -2,6 +2,7 @@
 // of one calibration step and the optional per-kernel event timing.
 #include <stdarg.h>
 #include <stdio.h>
+#include <string.h>
 
 #include <algorithm>
 #include <climits>
@@ -161,10 +162,37 @@ static oq_status check_lwc(const void* W, oq_dtype w_dt, int64_t c_out, int64_t 
   return OQ_OK;
 }
 
+static oq_status wquant_fwd(int quant, const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                            const float* s, const float* gamma_logit, const float* beta_logit,
+                            int bits, int64_t group, void* W_dq, oq_dtype dq_dt, uint8_t* codes,
+                            float* h, float* z, hipStream_t stream);
+static oq_status wquant_bwd(int quant, const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                            const float* s, const float* gamma_logit, const float* beta_logit,
+                            int bits, int64_t group, const float* dW_dq, float* d_gamma_logit,
+                            float* d_beta_logit, float* d_s, float* dW_tilde, void* ws,
+                            size_t ws_bytes, hipStream_t stream);
+
 oq_status oq_lwc_fakequant_fwd(const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
                                const float* s, const float* gamma_logit, const float* beta_logit,
                                int bits, int64_t group, void* W_dq, oq_dtype dq_dt,
                                uint8_t* codes, float* h, float* z, hipStream_t stream) {
+  return wquant_fwd(OQ_WQ_LWC, W, w_dt, c_out, c_in, s, gamma_logit, beta_logit, bits, group, W_dq,
+                    dq_dt, codes, h, z, stream);
+}
+
+oq_status oq_wquant_fakequant_fwd(int quantizer, const void* W, oq_dtype w_dt, int64_t c_out,
+                                  int64_t c_in, const float* s, const float* p1, const float* p2,
+                                  int bits, int64_t group, void* W_dq, oq_dtype dq_dt,
+                                  uint8_t* codes, float* h, float* z, hipStream_t stream) {
+  return wquant_fwd(quantizer, W, w_dt, c_out, c_in, s, p1, p2, bits, group, W_dq, dq_dt, codes, h,
+                    z, stream);
+}
+
+static oq_status wquant_fwd(int quant, const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                            const float* s, const float* gamma_logit, const float* beta_logit,
+                            int bits, int64_t group, void* W_dq, oq_dtype dq_dt, uint8_t* codes,
+                            float* h, float* z, hipStream_t stream) {
+  OQ_REQ(quant >= OQ_WQ_LWC && quant <= OQ_WQ_LSQ, "quantizer=%d", quant);
   oq_status e = check_lwc(W, w_dt, c_out, c_in, gamma_logit, beta_logit, bits, group);
   if (e != OQ_OK) return e;
   OQ_REQ(!W_dq || dtype_ok(dq_dt), "bad W_dq dtype");
@@ -174,7 +202,7 @@ oq_status oq_lwc_fakequant_fwd(const void* W, oq_dtype w_dt, int64_t c_out, int6
   ProfScope ps(PK_LWC_FWD, stream,
                double(c_out) * c_in * (esize(w_dt) + (W_dq ? esize(dq_dt) : 0) + (codes ? 1 : 0)));
   OQ_HIP(lwc_fwd(W, w_dt == OQ_BF16, c_out, c_in, s, gamma_logit, beta_logit, bits, group, W_dq,
-                 dq_dt == OQ_BF16, codes, h, z, stream),
+                 dq_dt == OQ_BF16, codes, h, z, stream, nullptr, quant),
          "lwc_fwd");
   return OQ_OK;
 }
@@ -192,6 +220,39 @@ oq_status oq_lwc_fakequant_bwd(const void* W, oq_dtype w_dt, int64_t c_out, int6
                                int bits, int64_t group, const float* dW_dq,
                                float* d_gamma_logit, float* d_beta_logit, float* d_s,
                                float* dW_tilde, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return wquant_bwd(OQ_WQ_LWC, W, w_dt, c_out, c_in, s, gamma_logit, beta_logit, bits, group, dW_dq,
+                    d_gamma_logit, d_beta_logit, d_s, dW_tilde, ws, ws_bytes, stream);
+}
+
+oq_status oq_wquant_fakequant_bwd(int quantizer, const void* W, oq_dtype w_dt, int64_t c_out,
+                                  int64_t c_in, const float* s, const float* p1, const float* p2,
+                                  int bits, int64_t group, const float* dW_dq, float* d_p1,
+                                  float* d_p2, float* d_s, float* dW_tilde, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  return wquant_bwd(quantizer, W, w_dt, c_out, c_in, s, p1, p2, bits, group, dW_dq, d_p1, d_p2,
+                    d_s, dW_tilde, ws, ws_bytes, stream);
+}
+
+oq_status oq_wquant_init(int quantizer, const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                         const float* s, int bits, int64_t group, float* p1, float* p2,
+                         hipStream_t stream) {
+  OQ_REQ(quantizer >= OQ_WQ_LWC && quantizer <= OQ_WQ_LSQ, "quantizer=%d", quantizer);
+  OQ_REQ(p1 && p2, "p1 and p2 are required");
+  oq_status e = check_lwc(W, w_dt, c_out, c_in, p1, p2, bits, group);
+  if (e != OQ_OK) return e;
+  OQ_REQ(!s || aligned16(s), "s must be 16-byte aligned");
+  ProfScope ps(PK_OTHER, stream, double(c_out) * c_in * esize(w_dt));
+  OQ_HIP(wquant_init(W, w_dt == OQ_BF16, c_out, c_in, s, bits, group, quantizer, p1, p2, stream),
+         "wquant_init");
+  return OQ_OK;
+}
+
+static oq_status wquant_bwd(int quant, const void* W, oq_dtype w_dt, int64_t c_out, int64_t c_in,
+                            const float* s, const float* gamma_logit, const float* beta_logit,
+                            int bits, int64_t group, const float* dW_dq, float* d_gamma_logit,
+                            float* d_beta_logit, float* d_s, float* dW_tilde, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+  OQ_REQ(quant >= OQ_WQ_LWC && quant <= OQ_WQ_LSQ, "quantizer=%d", quant);
   oq_status e = check_lwc(W, w_dt, c_out, c_in, gamma_logit, beta_logit, bits, group);
   if (e != OQ_OK) return e;
   OQ_REQ(dW_dq && d_gamma_logit && d_beta_logit, "dW_dq, d_gamma_logit, d_beta_logit are required");
@@ -205,7 +266,7 @@ oq_status oq_lwc_fakequant_bwd(const void* W, oq_dtype w_dt, int64_t c_out, int6
   {
     ProfScope ps(PK_LWC_BWD, stream, double(c_out) * c_in * (esize(w_dt) + 4 + (dW_tilde ? 4 : 0)));
     OQ_HIP(lwc_bwd(W, w_dt == OQ_BF16, c_out, c_in, s, gamma_logit, beta_logit, bits, group, dW_dq,
-                   d_gamma_logit, d_beta_logit, dW_tilde, parts, stream),
+                   d_gamma_logit, d_beta_logit, dW_tilde, parts, stream, 1, 0, quant),
            "lwc_bwd");
   }
   if (d_s) {
@@ -233,8 +294,18 @@ oq_status oq_let_fold(const void* W, oq_dtype w_dt, const float* B, int64_t c_ou
   return OQ_OK;
 }
 
-static oq_status check_act(const void* X, oq_dtype x_dt, int64_t T, int64_t C, int bits,
+// Splits the activation bits argument: the bit width and OQ_ACT_SYM.
+static void act_mode(int bits_arg, int* bits, bool* sym) {
+  *sym = (bits_arg & OQ_ACT_SYM) != 0;
+  *bits = bits_arg & ~OQ_ACT_SYM;
+}
+
+static oq_status check_act(const void* X, oq_dtype x_dt, int64_t T, int64_t C, int bits_arg,
                            const float* s, const float* delta) {
+  int bits;
+  bool sym;
+  act_mode(bits_arg, &bits, &sym);
+  if (sym && bits == 16) return fail(OQ_ERR_UNSUPPORTED, "OQ_ACT_SYM needs bits in [2, 8]");
   OQ_REQ(X, "X is required");
   OQ_REQ(dtype_ok(x_dt), "bad dtype");
   OQ_REQ(T >= 0 && C > 0 && C % 8 == 0, "bad shape T=%lld C=%lld", (long long)T, (long long)C);
@@ -253,11 +324,14 @@ oq_status oq_act_fakequant_fwd(const void* X, oq_dtype x_dt, int64_t T, int64_t 
   if (e != OQ_OK) return e;
   OQ_REQ(!X_dq || (dtype_ok(dq_dt) && aligned16(X_dq)), "bad X_dq");
   OQ_REQ(!codes || (reinterpret_cast<uintptr_t>(codes) & 7u) == 0, "codes must be 8-byte aligned");
-  OQ_REQ(!codes || bits < 16, "codes need bits < 16");
+  int nb;
+  bool sym;
+  act_mode(bits, &nb, &sym);
+  OQ_REQ(!codes || nb < 16, "codes need bits < 16");
   ProfScope ps(PK_ACT_FWD, stream,
                double(T) * C * (esize(x_dt) + (X_dq ? esize(dq_dt) : 0) + (codes ? 1 : 0)));
-  OQ_HIP(act_fwd(X, x_dt == OQ_BF16, T, C, bits, s, delta, X_dq, dq_dt == OQ_BF16, codes, h, z,
-                 stream),
+  OQ_HIP(act_fwd(X, x_dt == OQ_BF16, T, C, nb, s, delta, X_dq, dq_dt == OQ_BF16, codes, h, z,
+                 stream, sym),
          "act_fwd");
   return OQ_OK;
 }
@@ -286,8 +360,11 @@ oq_status oq_act_fakequant_bwd(const void* X, oq_dtype x_dt, int64_t T, int64_t 
   float* psx = parts ? cv.take<float>(size_t(np) * C) : nullptr;
   float* ps1 = parts ? cv.take<float>(size_t(np) * C) : nullptr;
   {
+    int nb;
+    bool sym;
+    act_mode(bits, &nb, &sym);
     ProfScope ps(PK_ACT_BWD, stream, double(T) * C * (esize(x_dt) + 4 + (dX_tilde ? 4 : 0)));
-    OQ_HIP(act_bwd(X, x_dt == OQ_BF16, T, C, bits, s, delta, dX_dq, dX_tilde, psx, ps1, stream),
+    OQ_HIP(act_bwd(X, x_dt == OQ_BF16, T, C, nb, s, delta, dX_dq, dX_tilde, psx, ps1, stream, sym),
            "act_bwd");
   }
   if (parts) {
@@ -358,8 +435,11 @@ oq_status oq_act_fakequant_bwd_noalloc(const void* X, oq_dtype x_dt, int64_t T, 
     ps1 = cv.take<float>(size_t(np) * C);
   }
   {
+    int nb;
+    bool sym;
+    act_mode(bits, &nb, &sym);
     ProfScope ps(PK_ACT_BWD, stream, double(T) * C * (esize(x_dt) + 4 + (dX_tilde ? 4 : 0)));
-    OQ_HIP(act_bwd(X, x_dt == OQ_BF16, T, C, bits, s, delta, dX_dq, dX_tilde, psx, ps1, stream),
+    OQ_HIP(act_bwd(X, x_dt == OQ_BF16, T, C, nb, s, delta, dX_dq, dX_tilde, psx, ps1, stream, sym),
            "act_bwd");
   }
   if (parts) {
@@ -525,7 +605,9 @@ namespace {
 struct SitePlan {
   int k, l0, l1;
   int64_t C, M;
-  bool let, act;
+  bool let, act, sym;   // sym: symmetric absmax activation quantiser
+  int act_bits;         // 2..8, or 16 = no activation quantisation
+  bool lwc_only;        // every linear of the site quantised by LWC
 };
 
 struct BlockWs {
@@ -553,11 +635,13 @@ oq_status plan_block(const oq_block_desc* d, std::vector<SitePlan>& plan) {
       for (auto& p : plan) OQ_REQ(p.k != k, "linears of site %d are not consecutive", k);
       const int64_t C = d->site_width[k];
       OQ_REQ(C > 0 && C % 8 == 0, "site %d: width must be a positive multiple of 8", k);
-      const int ab = d->site_act_bits[k];
+      const int ab = d->site_act_bits[k] & ~OQ_ACT_SYM;
+      const bool sym = (d->site_act_bits[k] & OQ_ACT_SYM) != 0;
+      if (sym && ab == 16) return fail(OQ_ERR_UNSUPPORTED, "site %d: OQ_ACT_SYM needs bits 2..8", k);
       if (!(ab == 16 || (ab >= 2 && ab <= 8)))
         return fail(OQ_ERR_UNSUPPORTED, "site %d: activation bits %d", k, ab);
       if (C > 32768) return fail(OQ_ERR_UNSUPPORTED, "site %d: width %lld > 32768", k, (long long)C);
-      plan.push_back(SitePlan{k, l, l + 1, C, 0, d->site_let[k] != 0, ab < 16});
+      plan.push_back(SitePlan{k, l, l + 1, C, 0, d->site_let[k] != 0, ab < 16, sym, ab, true});
       prev_site = k;
     } else {
       plan.back().l1 = l + 1;
@@ -568,6 +652,9 @@ oq_status plan_block(const oq_block_desc* d, std::vector<SitePlan>& plan) {
       return fail(OQ_ERR_UNSUPPORTED, "site %d has more than %d linears", k, MAX_SEG);
     if (d->lin_bits[l] < 2 || d->lin_bits[l] > 8)
       return fail(OQ_ERR_UNSUPPORTED, "linear %d: bits %d", l, d->lin_bits[l]);
+    if (d->lin_quant[l] < OQ_WQ_LWC || d->lin_quant[l] > OQ_WQ_LSQ)
+      return fail(OQ_ERR_UNSUPPORTED, "linear %d: quantizer %d", l, d->lin_quant[l]);
+    sp.lwc_only = sp.lwc_only && d->lin_quant[l] == OQ_WQ_LWC;
     if (d->lin_group[l] <= 0 || sp.C % d->lin_group[l])
       return fail(OQ_ERR_INVALID_ARG, "linear %d: group %lld does not divide %lld", l,
                   (long long)d->lin_group[l], (long long)sp.C);
@@ -615,7 +702,7 @@ int fwd_splits(const oq_block_desc* d, const SitePlan& p) {
 // when that product is not split, the site has no LET, and every linear of it
 // shares one power-of-two group of at most 256 weights and one bit width.
 bool fused_lwc(const oq_block_desc* d, const SitePlan& p) {
-  if (p.let || !direct_grads(d, p) || wgrad_splits(d, p) != 1) return false;
+  if (p.let || !p.lwc_only || !direct_grads(d, p) || wgrad_splits(d, p) != 1) return false;
   const int64_t g = d->lin_group[p.l0];
   for (int l = p.l0; l < p.l1; ++l)
     if (d->lin_group[l] != g || d->lin_bits[l] != d->lin_bits[p.l0]) return false;
@@ -763,6 +850,27 @@ size_t carve_block(const oq_block_desc* d, const std::vector<SitePlan>& plan, ch
 
 extern "C" {
 
+oq_status oq_block_plan(const oq_block_desc* desc, int* info, int n_info) {
+  OQ_REQ(info, "info is required");
+  std::vector<SitePlan> plan;
+  oq_status e = plan_block(desc, plan);
+  if (e != OQ_OK) return e;
+  OQ_REQ(n_info >= OQ_PLAN_FIELDS * desc->n_sites, "info holds %d ints, %d needed", n_info,
+         OQ_PLAN_FIELDS * desc->n_sites);
+  const bool conc = concurrent_sites(desc, plan);
+  for (const auto& p : plan) {
+    int* r = info + OQ_PLAN_FIELDS * p.k;
+    const bool direct = direct_grads(desc, p);
+    r[0] = conc;
+    r[1] = direct;
+    r[2] = direct && !fused_lwc(desc, p) ? wgrad_splits(desc, p) : 1;
+    r[3] = fwd_splits(desc, p);
+    r[4] = fused_lwc(desc, p);
+    r[5] = p.let && direct_wt_copy(desc, p);
+  }
+  return OQ_OK;
+}
+
 oq_status oq_block_workspace_size(const oq_block_desc* desc, size_t* bytes) {
   OQ_REQ(bytes, "bytes is required");
   std::vector<SitePlan> plan;
@@ -780,12 +888,16 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
   oq_status e = plan_block(d, plan);
   if (e != OQ_OK) return e;
   OQ_REQ(Y_fp_T && X_q && prm && gr && loss, "Y_fp_T, X_q, params, grads, loss are required");
+  const int frozen = opt ? opt->frozen : 0;
+  OQ_REQ(frozen >= 0 && frozen <= (OQ_FREEZE_LWC | OQ_FREEZE_LET), "optim frozen=%d", frozen);
+  const bool lwc_train = !(frozen & OQ_FREEZE_LWC), let_train = !(frozen & OQ_FREEZE_LET);
   for (const auto& p : plan) {
     OQ_REQ(X_q[p.k] && aligned16(X_q[p.k]), "X_q[%d] missing or misaligned", p.k);
     if (p.let) {
       OQ_REQ(prm->s[p.k] && prm->delta[p.k] && aligned16(prm->s[p.k]) && aligned16(prm->delta[p.k]),
              "site %d: LET needs 16-byte aligned s and delta", p.k);
-      OQ_REQ(gr->d_s[p.k] && gr->d_delta[p.k], "site %d: d_s and d_delta are required", p.k);
+      if (let_train)
+        OQ_REQ(gr->d_s[p.k] && gr->d_delta[p.k], "site %d: d_s and d_delta are required", p.k);
     }
   }
   for (int l = 0; l < d->n_linears; ++l) {
@@ -796,11 +908,11 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
   }
   if (opt) {
     OQ_REQ(opt->step >= 1, "optim step must be >= 1");
-    for (int l = 0; l < d->n_linears; ++l)
+    for (int l = 0; l < d->n_linears && lwc_train; ++l)
       OQ_REQ(opt->m_gamma[l] && opt->v_gamma[l] && opt->m_beta[l] && opt->v_beta[l],
              "AdamW state of linear %d missing", l);
     for (const auto& p : plan)
-      if (p.let)
+      if (p.let && let_train)
         OQ_REQ(opt->m_s[p.k] && opt->v_s[p.k] && opt->m_delta[p.k] && opt->v_delta[p.k],
                "AdamW state of site %d missing", p.k);
   }
@@ -837,6 +949,10 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     const int64_t C = p.C, M = p.M;
     const float* s = p.let ? prm->s[k] : nullptr;
     const float* dl = p.let ? prm->delta[k] : nullptr;
+    // LET gradients (the input-gradient path) only for a trained LET; the
+    // weight gradient only when some trained parameter needs it
+    const bool let_grads = p.let && let_train;
+    const bool wgrad = lwc_train || let_grads;
     bool any_bias = p.let;
     for (int l = p.l0; l < p.l1; ++l) any_bias = any_bias || prm->B[l];
 
@@ -850,7 +966,8 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
       ProfScope ps(PK_LWC_FWD, st, double(co) * C * 2 * es);
       OQ_HIP(lwc_fwd(prm->W[l], bf, co, C, s, prm->gamma_logit[l], prm->beta_logit[l],
                      d->lin_bits[l], d->lin_group[l], static_cast<char*>(w.what) + off * C * es, bf,
-                     nullptr, nullptr, nullptr, st, fused ? w.gstat + off * ngs : nullptr),
+                     nullptr, nullptr, nullptr, st, fused ? w.gstat + off * ngs : nullptr,
+                     d->lin_quant[l]),
              "lwc_fwd");
       la.row_begin[l] = row_base + off;
       la.row_end[l] = row_base + off + co;
@@ -873,8 +990,8 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     const void* xsrc = X_q[k];
     if (p.let || p.act) {
       ProfScope ps(PK_ACT_FWD, st, double(T) * C * 2 * es);
-      OQ_HIP(act_fwd(X_q[k], bf, T, C, p.act ? d->site_act_bits[k] : 16, s, dl, w.xhat, bf,
-                     nullptr, nullptr, nullptr, st),
+      OQ_HIP(act_fwd(X_q[k], bf, T, C, p.act ? p.act_bits : 16, s, dl, w.xhat, bf,
+                     nullptr, nullptr, nullptr, st, p.sym),
              "act_fwd");
       xsrc = w.xhat;
     }
@@ -903,7 +1020,7 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
       ra.dy = w.dyT;
       ra.ld_dy = T;
       ra.part_sq = w.psq;
-      ra.part_dy = p.let ? w.pdy : nullptr;
+      ra.part_dy = let_grads ? w.pdy : nullptr;
       ProfScope ps(PK_GEMM_FWD, st, 2.0 * double(M) * T * C);
       const int SF = fwd_splits(d, p);
       if (SF > 1)
@@ -914,14 +1031,18 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
     }
     {
       ProfScope ps(PK_OTHER, st, double(M) * ntn * 8);
-      OQ_HIP(row_partials(w.psq, p.let ? w.pdy : nullptr, M, ntn, w.rl + row_base, w.dbt, st),
+      OQ_HIP(row_partials(w.psq, let_grads ? w.pdy : nullptr, M, ntn, w.rl + row_base, w.dbt, st),
              "row partials");
+    }
+    if (!wgrad) {            // every parameter this site feeds is frozen
+      row_base += M;
+      continue;
     }
     // 6. weight gradient dW^ = dY^T X^  [M, C]; over a K (token) split of S
     //    parts when that fills the last wave of tiles better, the parts
     //    summed in a fixed order (by the LWC backward's loads where it can)
     const int S = direct && !fused ? wgrad_splits(d, p) : 1;
-    bool parts_in_bwd = S > 1;
+    bool parts_in_bwd = S > 1 && p.lwc_only;
     for (int l = p.l0; l < p.l1; ++l)
       parts_in_bwd = parts_in_bwd && lwc_bwd_sums_parts(d->lin_c_out[l], C, d->lin_group[l], s,
                                                         p.let);
@@ -965,14 +1086,14 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
       ProfScope ps(PK_LWC_BWD, st, double(co) * C * (es + 4.0 * (parts_in_bwd ? S : 1)));
       OQ_HIP(lwc_bwd(prm->W[l], bf, co, C, s, prm->gamma_logit[l], prm->beta_logit[l],
                      d->lin_bits[l], d->lin_group[l], w.dW + off * C, gr->d_gamma_logit[l],
-                     gr->d_beta_logit[l], nullptr, p.let ? w.pw + pwo * C : nullptr, st,
-                     parts_in_bwd ? S : 1, M * C),
+                     gr->d_beta_logit[l], nullptr, let_grads ? w.pw + pwo * C : nullptr, st,
+                     parts_in_bwd ? S : 1, M * C, d->lin_quant[l]),
              "lwc_bwd");
       off += co;
       pwo += lwc_bwd_nparts(co);
     }
     // 8. LET: input gradient through Q_a and (X - delta)/s, bias path, finish
-    if (p.let) {
+    if (let_grads) {
       const bool wt_copy = direct_wt_copy(d, p);
       if (direct && wt_copy) {
         // dX^ [T, C] = dY W^ with dY read from dY^T [M, T] as stored and W^
@@ -1002,8 +1123,8 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
       }
       {
         ProfScope ps(PK_ACT_BWD, st, double(T) * C * (es + 4));
-        OQ_HIP(act_bwd(X_q[k], bf, T, C, p.act ? d->site_act_bits[k] : 16, s, dl, w.dX, nullptr,
-                       w.psx, w.ps1, st),
+        OQ_HIP(act_bwd(X_q[k], bf, T, C, p.act ? p.act_bits : 16, s, dl, w.dX, nullptr,
+                       w.psx, w.ps1, st, p.sym),
                "act_bwd");
       }
       ProfScope ps(PK_OTHER, st, double(M) * C * es);
@@ -1042,13 +1163,13 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
       L.p[L.n] = pp; L.g[L.n] = g; L.m[L.n] = m; L.v[L.n] = v; L.len[L.n] = n; L.set[L.n] = set;
       ++L.n;
     };
-    for (int l = 0; l < d->n_linears; ++l) {
+    for (int l = 0; l < d->n_linears && lwc_train; ++l) {
       const int64_t n = d->lin_c_out[l] * (d->site_width[d->lin_site[l]] / d->lin_group[l]);
       add(prm->gamma_logit[l], gr->d_gamma_logit[l], opt->m_gamma[l], opt->v_gamma[l], n, 0);
       add(prm->beta_logit[l], gr->d_beta_logit[l], opt->m_beta[l], opt->v_beta[l], n, 0);
     }
     for (const auto& p : plan) {
-      if (!p.let) continue;
+      if (!p.let || !let_train) continue;
       add(prm->s[p.k], gr->d_s[p.k], opt->m_s[p.k], opt->v_s[p.k], p.C, 1);
       add(prm->delta[p.k], gr->d_delta[p.k], opt->m_delta[p.k], opt->v_delta[p.k], p.C, 1);
     }
@@ -1083,6 +1204,13 @@ oq_status oq_block_export(const oq_block_desc* d, const oq_block_params* prm,
     const int k = d->lin_site[l];
     OQ_REQ(d->site_width[k] % 32 == 0, "linear %d: C_in=%lld is not a multiple of 32", l,
            (long long)d->site_width[k]);
+    // the packed linear consumes the export: codes of 2..7 bits, groups of
+    // whole 32-code runs
+    if (d->lin_bits[l] > 7 || d->lin_group[l] % 32 != 0)
+      return fail(OQ_ERR_UNSUPPORTED,
+                  "linear %d: bits %d / group %lld cannot be deployed by oq_packed_linear "
+                  "(bits 2..7, group a multiple of 32)",
+                  l, d->lin_bits[l], (long long)d->lin_group[l]);
     OQ_REQ(prm->W[l] && aligned16(prm->W[l]), "W[%d] missing or misaligned", l);
     OQ_REQ(prm->gamma_logit[l] && prm->beta_logit[l], "logits of linear %d missing", l);
     OQ_REQ(packed[l] && aligned16(packed[l]) && h[l] && z[l], "outputs of linear %d missing or misaligned", l);
@@ -1099,13 +1227,249 @@ oq_status oq_block_export(const oq_block_desc* d, const oq_block_params* prm,
     ProfScope ps(PK_OTHER, st, double(c_out) * c_in * (esize(d->dtype) + 1.0 + d->lin_bits[l] / 8.0));
     OQ_HIP(lwc_fwd(prm->W[l], bf, c_out, c_in, let ? prm->s[k] : nullptr, prm->gamma_logit[l],
                    prm->beta_logit[l], d->lin_bits[l], d->lin_group[l], nullptr, false, codes, h[l],
-                   z[l], st),
+                   z[l], st, nullptr, d->lin_quant[l]),
            "export lwc_fwd");
     OQ_HIP(pack_codes(codes, c_out, c_in, d->lin_bits[l], packed[l], st), "export pack_codes");
     if (B_tilde && B_tilde[l])
       OQ_HIP(let_fold(prm->W[l], bf, prm->B[l], c_out, c_in, let ? prm->s[k] : nullptr,
                       let ? prm->delta[k] : nullptr, nullptr, false, B_tilde[l], st),
              "export let_fold");
+  }
+  return OQ_OK;
+}
+
+oq_status oq_let_absorb(const void* P, oq_dtype p_dt, const float* b, int64_t C, int64_t n,
+                        const float* s, const float* delta, void* P_out, float* b_out,
+                        hipStream_t stream) {
+  OQ_REQ(dtype_ok(p_dt), "bad dtype");
+  OQ_REQ(C >= 0 && n >= 0, "bad shape C=%lld n=%lld", (long long)C, (long long)n);
+  OQ_REQ(!P_out || P, "P_out needs P");
+  OQ_REQ(P_out || b_out, "nothing to write: P_out and b_out are both NULL");
+  ProfScope ps(PK_OTHER, stream, double(C) * n * 2 * esize(p_dt));
+  OQ_HIP(let_absorb(P, p_dt == OQ_BF16, b, C, n, s, delta, P_out, b_out, stream), "let_absorb");
+  return OQ_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ checkpoint / resume
+namespace {
+
+constexpr char kCkptMagic[8] = {'O', 'Q', 'C', 'K', 'P', 'T', '\0', '\1'};
+constexpr uint32_t kCkptVersion = 1;
+
+uint64_t fnv1a64(const void* data, size_t n) {
+  const unsigned char* p = static_cast<const unsigned char*>(data);
+  uint64_t h = 1469598103934665603ull;
+  for (size_t i = 0; i < n; ++i) {
+    h ^= p[i];
+    h *= 1099511628211ull;
+  }
+  return h;
+}
+
+// One calibrated tensor of the block: kind (0 gamma_logit, 1 beta_logit,
+// 2 s, 3 delta, 4 m_gamma, 5 v_gamma, 6 m_beta, 7 v_beta, 8 m_s, 9 v_s,
+// 10 m_delta, 11 v_delta), the linear or site it belongs to, its device
+// pointer and element count.
+struct CkptTensor {
+  uint32_t kind, index;
+  float* ptr;
+  uint64_t count;
+};
+
+std::vector<CkptTensor> ckpt_tensors(const oq_block_desc* d, const std::vector<SitePlan>& plan,
+                                     const oq_block_params* prm, const oq_block_optim* opt) {
+  std::vector<CkptTensor> t;
+  for (int l = 0; l < d->n_linears; ++l) {
+    const uint64_t n = uint64_t(d->lin_c_out[l]) * uint64_t(d->site_width[d->lin_site[l]] / d->lin_group[l]);
+    t.push_back({0, uint32_t(l), prm->gamma_logit[l], n});
+    t.push_back({1, uint32_t(l), prm->beta_logit[l], n});
+    if (opt) {
+      t.push_back({4, uint32_t(l), opt->m_gamma[l], n});
+      t.push_back({5, uint32_t(l), opt->v_gamma[l], n});
+      t.push_back({6, uint32_t(l), opt->m_beta[l], n});
+      t.push_back({7, uint32_t(l), opt->v_beta[l], n});
+    }
+  }
+  for (const auto& p : plan) {
+    if (!p.let) continue;
+    const uint64_t n = uint64_t(p.C);
+    t.push_back({2, uint32_t(p.k), prm->s[p.k], n});
+    t.push_back({3, uint32_t(p.k), prm->delta[p.k], n});
+    if (opt) {
+      t.push_back({8, uint32_t(p.k), opt->m_s[p.k], n});
+      t.push_back({9, uint32_t(p.k), opt->v_s[p.k], n});
+      t.push_back({10, uint32_t(p.k), opt->m_delta[p.k], n});
+      t.push_back({11, uint32_t(p.k), opt->v_delta[p.k], n});
+    }
+  }
+  return t;
+}
+
+// The descriptor fields a checkpoint must agree on (the token count and the
+// data type of X and W may differ between the saving and the resuming run).
+struct CkptShape {
+  int32_t n_sites, n_linears;
+  int64_t site_width[OQ_MAX_SITES];
+  int32_t site_let[OQ_MAX_SITES], site_act_bits[OQ_MAX_SITES];
+  int32_t lin_site[OQ_MAX_LINEARS];
+  int64_t lin_c_out[OQ_MAX_LINEARS];
+  int32_t lin_bits[OQ_MAX_LINEARS];
+  int64_t lin_group[OQ_MAX_LINEARS];
+  int32_t lin_quant[OQ_MAX_LINEARS];
+};
+
+CkptShape ckpt_shape(const oq_block_desc* d) {
+  CkptShape c;
+  memset(&c, 0, sizeof c);
+  c.n_sites = d->n_sites;
+  c.n_linears = d->n_linears;
+  for (int k = 0; k < d->n_sites; ++k) {
+    c.site_width[k] = d->site_width[k];
+    c.site_let[k] = d->site_let[k];
+    c.site_act_bits[k] = d->site_act_bits[k];
+  }
+  for (int l = 0; l < d->n_linears; ++l) {
+    c.lin_site[l] = d->lin_site[l];
+    c.lin_c_out[l] = d->lin_c_out[l];
+    c.lin_bits[l] = d->lin_bits[l];
+    c.lin_quant[l] = d->lin_quant[l];
+    c.lin_group[l] = d->lin_group[l];
+  }
+  return c;
+}
+
+struct FileCloser {
+  FILE* f;
+  ~FileCloser() {
+    if (f) fclose(f);
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+oq_status oq_block_state_save(const oq_block_desc* d, const oq_block_params* prm,
+                              const oq_block_optim* opt, int completed_steps, const char* path,
+                              hipStream_t stream) {
+  std::vector<SitePlan> plan;
+  oq_status e = plan_block(d, plan);
+  if (e != OQ_OK) return e;
+  OQ_REQ(prm && path, "params and path are required");
+  OQ_REQ(completed_steps >= 0, "completed_steps=%d", completed_steps);
+  const auto ts = ckpt_tensors(d, plan, prm, opt);
+  for (const auto& t : ts) OQ_REQ(t.ptr, "tensor kind %u of %u is missing", t.kind, t.index);
+  OQ_HIP(hipStreamSynchronize(stream), "synchronise before saving");
+  const std::string tmp = std::string(path) + ".tmp";
+  {
+    FileCloser fc{fopen(tmp.c_str(), "wb")};
+    if (!fc.f) return fail(OQ_ERR_INVALID_ARG, "cannot open %s for writing", tmp.c_str());
+    const CkptShape shape = ckpt_shape(d);
+    const int32_t head[4] = {int32_t(kCkptVersion), int32_t(sizeof(CkptShape)), completed_steps,
+                             opt ? 1 : 0};
+    const uint64_t nt = ts.size();
+    bool ok = fwrite(kCkptMagic, 1, 8, fc.f) == 8 && fwrite(head, sizeof head, 1, fc.f) == 1 &&
+              fwrite(&shape, sizeof shape, 1, fc.f) == 1 && fwrite(&nt, 8, 1, fc.f) == 1;
+    if (opt) {
+      const double hp[6] = {opt->lr_lwc, opt->lr_let, opt->beta1, opt->beta2, opt->eps, opt->wd};
+      ok = ok && fwrite(hp, sizeof hp, 1, fc.f) == 1;
+    }
+    std::vector<float> buf;
+    for (const auto& t : ts) {
+      if (!ok) break;
+      buf.resize(t.count);
+      OQ_HIP(hipMemcpy(buf.data(), t.ptr, t.count * 4, hipMemcpyDeviceToHost), "copy to host");
+      const uint64_t sum = fnv1a64(buf.data(), t.count * 4);
+      const uint32_t ki[2] = {t.kind, t.index};
+      ok = fwrite(ki, sizeof ki, 1, fc.f) == 1 && fwrite(&t.count, 8, 1, fc.f) == 1 &&
+           fwrite(&sum, 8, 1, fc.f) == 1 &&
+           (t.count == 0 || fwrite(buf.data(), 4, t.count, fc.f) == t.count);
+    }
+    if (!ok) return fail(OQ_ERR_INVALID_ARG, "write to %s failed", tmp.c_str());
+    if (fflush(fc.f) != 0) return fail(OQ_ERR_INVALID_ARG, "flush of %s failed", tmp.c_str());
+  }
+  if (rename(tmp.c_str(), path) != 0)
+    return fail(OQ_ERR_INVALID_ARG, "cannot rename %s to %s", tmp.c_str(), path);
+  return OQ_OK;
+}
+
+oq_status oq_block_state_load(const oq_block_desc* d, const oq_block_params* prm,
+                              oq_block_optim* opt, int* completed_steps, const char* path,
+                              hipStream_t stream) {
+  std::vector<SitePlan> plan;
+  oq_status e = plan_block(d, plan);
+  if (e != OQ_OK) return e;
+  OQ_REQ(prm && path && completed_steps, "params, path and completed_steps are required");
+  FileCloser fc{fopen(path, "rb")};
+  if (!fc.f) return fail(OQ_ERR_INVALID_ARG, "cannot open %s", path);
+  char magic[8];
+  int32_t head[4];
+  CkptShape shape;
+  uint64_t nt = 0;
+  if (fread(magic, 1, 8, fc.f) != 8 || memcmp(magic, kCkptMagic, 8) != 0)
+    return fail(OQ_ERR_INVALID_ARG, "%s is not a block checkpoint", path);
+  if (fread(head, sizeof head, 1, fc.f) != 1 || head[0] != int32_t(kCkptVersion) ||
+      head[1] != int32_t(sizeof(CkptShape)))
+    return fail(OQ_ERR_INVALID_ARG, "%s: unsupported checkpoint version", path);
+  if (fread(&shape, sizeof shape, 1, fc.f) != 1 || fread(&nt, 8, 1, fc.f) != 1)
+    return fail(OQ_ERR_INVALID_ARG, "%s: truncated header", path);
+  const CkptShape want = ckpt_shape(d);
+  if (memcmp(&shape, &want, sizeof shape) != 0)
+    return fail(OQ_ERR_INVALID_ARG, "%s: the checkpoint's block shape differs from desc", path);
+  const bool has_opt = head[3] != 0;
+  if (opt && !has_opt) return fail(OQ_ERR_INVALID_ARG, "%s holds no AdamW state", path);
+  double hp[6];
+  if (has_opt && fread(hp, sizeof hp, 1, fc.f) != 1)
+    return fail(OQ_ERR_INVALID_ARG, "%s: truncated header", path);
+  const auto ts = ckpt_tensors(d, plan, prm, has_opt ? opt : nullptr);
+  for (const auto& t : ts) OQ_REQ(t.ptr, "tensor kind %u of %u is missing", t.kind, t.index);
+  // read and verify everything before any device buffer is written
+  std::vector<std::vector<float>> data;
+  std::vector<const CkptTensor*> dst;
+  for (uint64_t i = 0; i < nt; ++i) {
+    uint32_t ki[2];
+    uint64_t cnt = 0, sum = 0;
+    if (fread(ki, sizeof ki, 1, fc.f) != 1 || fread(&cnt, 8, 1, fc.f) != 1 ||
+        fread(&sum, 8, 1, fc.f) != 1)
+      return fail(OQ_ERR_INVALID_ARG, "%s: truncated at tensor %llu", path, (unsigned long long)i);
+    const CkptTensor* match = nullptr;
+    for (const auto& t : ts)
+      if (t.kind == ki[0] && t.index == ki[1]) match = &t;
+    if (cnt > (uint64_t(1) << 40))
+      return fail(OQ_ERR_INVALID_ARG, "%s: tensor %llu has an implausible size", path,
+                  (unsigned long long)i);
+    std::vector<float> v(cnt);
+    if (cnt && fread(v.data(), 4, cnt, fc.f) != cnt)
+      return fail(OQ_ERR_INVALID_ARG, "%s: truncated in tensor %llu", path, (unsigned long long)i);
+    if (fnv1a64(v.data(), cnt * 4) != sum)
+      return fail(OQ_ERR_INVALID_ARG, "%s: checksum mismatch in tensor kind %u of %u", path, ki[0],
+                  ki[1]);
+    if (!match) continue;               // AdamW state the caller does not restore
+    if (match->count != cnt)
+      return fail(OQ_ERR_INVALID_ARG, "%s: tensor kind %u of %u has %llu elements, %llu expected",
+                  path, ki[0], ki[1], (unsigned long long)cnt, (unsigned long long)match->count);
+    data.push_back(std::move(v));
+    dst.push_back(match);
+  }
+  if (data.size() != ts.size())
+    return fail(OQ_ERR_INVALID_ARG, "%s holds %zu of the %zu tensors needed", path, data.size(),
+                ts.size());
+  for (size_t i = 0; i < data.size(); ++i)
+    OQ_HIP(hipMemcpyAsync(dst[i]->ptr, data[i].data(), dst[i]->count * 4, hipMemcpyHostToDevice,
+                          stream),
+           "copy to device");
+  OQ_HIP(hipStreamSynchronize(stream), "synchronise after loading");
+  *completed_steps = head[2];
+  if (opt) {
+    opt->step = head[2] + 1;
+    opt->lr_lwc = hp[0];
+    opt->lr_let = hp[1];
+    opt->beta1 = hp[2];
+    opt->beta2 = hp[3];
+    opt->eps = hp[4];
+    opt->wd = hp[5];
   }
   return OQ_OK;
 }

@@ -234,3 +234,98 @@ OQ_DEV QGrad quant_group_grad(float s_h, float s_z, float mx, float mn, const QP
   g.dbeta = db * mn;
   return g;
 }
+
+// ------------------------------------------------------------------ quantiser variants
+// Which weight quantiser fills a group's two parameters p1, p2: LWC's
+// clip-strength logits (Eq. 2), PACT's grid thresholds (upper, lower), or
+// LSQ's step and zero point (the zero point rounded in the forward).
+enum WQuant { WQ_LWC = 0, WQ_PACT = 1, WQ_LSQ = 2 };
+
+OQ_DEV QParams make_group_qparams(int quant, float mx, float mn, float p1, float p2, float qmax) {
+  if (quant == WQ_PACT) return make_qparams(p1, p2, 1.0f, 1.0f, qmax);
+  if (quant == WQ_LSQ) {
+    QParams p;
+    p.gamma = p.beta = 1.0f;
+    p.a = p.b = 0.0f;
+    p.hclamp = p1 < 1e-5f;
+    p.h = p.hclamp ? 1e-5f : p1;
+    p.r = div_rn(1.0f, p.h);
+    p.z = rintf(p2);
+    return p;
+  }
+  return make_qparams(mx, mn, clip_strength(p1), clip_strength(p2), qmax);
+}
+
+// One element's share of its group's two backward sums: LWC and LSQ sum
+// (S_h, S_z) = (g((q - z) - m u), g(1 - m)); PACT sums the gradient of the
+// codes saturated above qmax and below 0.
+OQ_DEV void group_terms(int quant, float g, const QElem& qe, const QParams& p, float qmax,
+                        float& s1, float& s2) {
+  if (quant == WQ_PACT) {
+    if (!qe.m) {
+      if (qe.q == qmax) s1 += g;
+      else s2 += g;
+    }
+    return;
+  }
+  const float t = qe.q - p.z;
+  const float th = qe.m ? t - qe.u : t;
+  s1 += g * th;
+  if (!qe.m) s2 += g;
+}
+
+// A group's parameter gradients from its two sums, and the max/min
+// gradients to route (LWC only: PACT's thresholds and LSQ's step do not
+// depend on the weights).  gs is LSQ's gradient scale 1/sqrt(n * qmax).
+struct GroupGrad {
+  float d1, d2, dmx, dmn;
+};
+OQ_DEV GroupGrad group_param_grads(int quant, float s1, float s2, float mx, float mn,
+                                   const QParams& p, float qmax, float gs) {
+  GroupGrad r;
+  if (quant == WQ_PACT) {
+    r.d1 = s1;
+    r.d2 = s2;
+    r.dmx = r.dmn = 0.0f;
+  } else if (quant == WQ_LSQ) {
+    r.d1 = p.hclamp ? 0.0f : gs * s1;
+    r.d2 = -(gs * (p.h * s2));
+    r.dmx = r.dmn = 0.0f;
+  } else {
+    const QGrad qg = quant_group_grad(s1, s2, mx, mn, p, qmax);
+    r.d1 = qg.dgamma * p.gamma * (1.0f - p.gamma);
+    r.d2 = qg.dbeta * p.beta * (1.0f - p.beta);
+    r.dmx = qg.dmx;
+    r.dmn = qg.dmn;
+  }
+  return r;
+}
+
+// Symmetric per-token absmax quantiser: h = max(|x|max / qs, 1e-5), qs =
+// 2^(N-1) - 1, zero point qs + 1.  The absmax element is the lowest index
+// holding the largest |x|: from a row's (max, argmax, min, argmin).
+OQ_DEV QParams make_sym_qparams(float mx, int imx, float mn, int imn, float qs, int& iab,
+                                float& sgn) {
+  const float amx = mx, amn = -mn;
+  float a;
+  if (amx > amn || (amx == amn && imx < imn)) {
+    a = amx;
+    iab = imx;
+    sgn = 1.0f;
+  } else {
+    a = amn;
+    iab = imn;
+    sgn = -1.0f;
+  }
+  QParams p;
+  p.gamma = p.beta = 1.0f;
+  p.a = a;
+  p.b = -a;
+  const float hr = div_rn(a, qs);
+  p.hclamp = hr < 1e-5f;
+  p.h = p.hclamp ? 1e-5f : hr;
+  p.r = div_rn(1.0f, p.h);
+  p.z = qs + 1.0f;
+  return p;
+}
+

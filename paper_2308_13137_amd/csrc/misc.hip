@@ -5,6 +5,7 @@
 // reproducible.
 #include <math.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "common.h"
@@ -68,6 +69,31 @@ __global__ __launch_bounds__(256) void let_fold_kernel(const TW* __restrict__ W,
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) acc += __shfl_xor(acc, off);
   if (lane == 0 && Bt) Bt[o] = float(acc + (B ? double(B[o]) : 0.0));
+}
+
+// ------------------------------------------------------------------ LET absorption
+// Folds a site's LET into the op that produces its input: row c of P [C, n]
+// (a normalisation's gain is n = 1, a previous linear's weight has its output
+// channels as rows) becomes P[c, :] * (1/s[c]) and its bias (b[c] - delta[c])
+// * (1/s[c]), the same fp32 order as the activation transform (x - delta)*(1/s).
+template <typename TP>
+__global__ __launch_bounds__(256) void let_absorb_kernel(const TP* __restrict__ P,
+                                                         const float* __restrict__ b, int64_t C,
+                                                         int64_t n, const float* __restrict__ s,
+                                                         const float* __restrict__ delta,
+                                                         TP* __restrict__ Pout,
+                                                         float* __restrict__ bout) {
+  const int64_t total = C * n;
+  for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < total;
+       i += int64_t(gridDim.x) * 256) {
+    const int64_t c = i / n;
+    const float r = s ? div_rn(1.0f, s[c]) : 1.0f;
+    if (Pout) store1(Pout + i, load1(P + i) * r);
+    if (bout && i % n == 0) {
+      const float bb = b ? b[c] : 0.0f;
+      bout[c] = (delta ? bb - delta[c] : bb) * r;
+    }
+  }
 }
 
 // ------------------------------------------------------------------ column reductions
@@ -374,6 +400,22 @@ hipError_t let_fold(const void* W, bool w_bf16, const float* B, int64_t c_out, i
   } else {
     if (wt_bf16) go(float{}, uint16_t{}); else go(float{}, float{});
   }
+  return hipGetLastError();
+}
+
+hipError_t let_absorb(const void* P, bool p_bf16, const float* b, int64_t C, int64_t n,
+                      const float* s, const float* delta, void* Pout, float* bout,
+                      hipStream_t st) {
+  if (C <= 0 || n <= 0) return hipSuccess;
+  const dim3 grid(unsigned(std::min<int64_t>((C * n + 255) / 256, 4096)));
+  if (p_bf16)
+    hipLaunchKernelGGL((let_absorb_kernel<uint16_t>), grid, dim3(256), 0, st,
+                       static_cast<const uint16_t*>(P), b, C, n, s, delta,
+                       static_cast<uint16_t*>(Pout), bout);
+  else
+    hipLaunchKernelGGL((let_absorb_kernel<float>), grid, dim3(256), 0, st,
+                       static_cast<const float*>(P), b, C, n, s, delta, static_cast<float*>(Pout),
+                       bout);
   return hipGetLastError();
 }
 

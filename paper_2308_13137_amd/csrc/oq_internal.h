@@ -107,10 +107,12 @@ hipError_t gemm_wgrad_lwc(const void* dyT, const void* x, int64_t M, int64_t C, 
 // LWC forward on rows [0, c_out) of one weight.  Returns hipErrorInvalidValue
 // when (c_in, group) is outside the supported set.
 // gstat (power-of-two groups without s only) receives {max, min, h, z} per group.
+// quant: WQ_LWC (gl, bl = clip-strength logits), WQ_PACT (gl, bl = upper and
+// lower thresholds), WQ_LSQ (gl, bl = step and zero point); see common.h.
 hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
                    const float* gl, const float* bl, int bits, int64_t group, void* W_dq,
                    bool dq_bf16, uint8_t* codes, float* h, float* z, hipStream_t st,
-                   float4* gstat = nullptr);
+                   float4* gstat = nullptr, int quant = 0);
 // LWC backward.  When ds_parts != nullptr each block writes one partial row
 // [c_in] of sum_o dW~[o,c]*W[o,c] into ds_parts; the number of rows written is
 // lwc_bwd_nparts(c_out).
@@ -121,17 +123,21 @@ bool lwc_bwd_sums_parts(int64_t c_out, int64_t c_in, int64_t group, bool has_s, 
 hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
                    const float* gl, const float* bl, int bits, int64_t group, const float* dW,
                    float* dgl, float* dbl, float* dW_tilde, float* ds_parts, hipStream_t st,
-                   int parts = 1, int64_t part_stride = 0);
+                   int parts = 1, int64_t part_stride = 0, int quant = 0);
 bool quant_shape_supported(int64_t c_in, int64_t group);
+// MinMax starting parameters of a weight quantiser variant, per group.
+hipError_t wquant_init(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
+                       int bits, int64_t group, int quant, float* p1, float* p2, hipStream_t st);
 
 // Activation fake-quant (per token row), LET transform included.
+// sym: symmetric absmax quantiser (zero point 2^(bits-1)) in place of MinMax.
 hipError_t act_fwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, const float* s,
                    const float* delta, void* X_dq, bool dq_bf16, uint8_t* codes, float* h,
-                   float* z, hipStream_t st);
+                   float* z, hipStream_t st, bool sym = false);
 int64_t act_bwd_nparts(int64_t T);
 hipError_t act_bwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, const float* s,
                    const float* delta, const float* dXdq, float* dXt, float* p_sx, float* p_s1,
-                   hipStream_t st);
+                   hipStream_t st, bool sym = false);
 
 // ---------------------------------------------------------------- elementwise / reductions
 hipError_t transpose(const void* in, int64_t rows, int64_t cols, int64_t ld_in, void* out,
@@ -139,6 +145,11 @@ hipError_t transpose(const void* in, int64_t rows, int64_t cols, int64_t ld_in, 
 hipError_t let_fold(const void* W, bool w_bf16, const float* B, int64_t c_out, int64_t c_in,
                     const float* s, const float* delta, void* Wt, bool wt_bf16, float* Bt,
                     hipStream_t st);
+// LET absorbed into the producer of a site's input: Pout[c,:] = P[c,:]*(1/s[c]),
+// bout[c] = (b[c] - delta[c])*(1/s[c]); P is [C, n] (n = 1 for a norm gain).
+hipError_t let_absorb(const void* P, bool p_bf16, const float* b, int64_t C, int64_t n,
+                      const float* s, const float* delta, void* Pout, float* bout,
+                      hipStream_t st);
 // out_parts[b][c] = sum over rows o of block b of wt[o] * W[o,c]
 int64_t wcolsum_nparts(int64_t rows);
 hipError_t wcolsum(const void* W, bool w_bf16, int64_t rows, int64_t cols, const float* wt,

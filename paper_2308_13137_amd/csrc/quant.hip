@@ -108,7 +108,7 @@ __global__ __launch_bounds__(NT) void lwc_fwd_kernel(
     const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ s,
     const float* __restrict__ gl, const float* __restrict__ bl, int bits, int group, int R,
     TQ* __restrict__ wdq, uint8_t* __restrict__ codes, float* __restrict__ hout,
-    float* __restrict__ zout) {
+    float* __restrict__ zout, int quant) {
   __shared__ MinMax shm[NT / 64];
   const int tid = threadIdx.x;
   const int cpr = int(c_in / 8);
@@ -145,7 +145,7 @@ __global__ __launch_bounds__(NT) void lwc_fwd_kernel(
         }
       }
       st = block_minmax(st, shm);
-      const QParams p = make_qparams(st.mx, st.mn, clip_strength(gl[row]), clip_strength(bl[row]), qmax);
+      const QParams p = make_group_qparams(quant, st.mx, st.mn, gl[row], bl[row], qmax);
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
         const int j = tid + NT * k;
@@ -182,8 +182,8 @@ __global__ __launch_bounds__(NT) void lwc_fwd_kernel(
         dyn_group_minmax(st.mx, st.imx, st.mn, st.imn, L);
         if (valid) {
           const int grp = j / L;
-          const QParams p = make_qparams(st.mx, st.mn, clip_strength(gl[row * ng + grp]),
-                                         clip_strength(bl[row * ng + grp]), qmax);
+          const QParams p = make_group_qparams(quant, st.mx, st.mn, gl[row * ng + grp],
+                                               bl[row * ng + grp], qmax);
           float q[8], d[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
     const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ s,
     const float* __restrict__ gl, const float* __restrict__ bl, int bits, int group, int R,
     const float* __restrict__ dW, float* __restrict__ dgl, float* __restrict__ dbl,
-    float* __restrict__ dWt, float* __restrict__ ds_parts) {
+    float* __restrict__ dWt, float* __restrict__ ds_parts, int quant, float gs) {
   __shared__ MinMax shm[NT / 64];
   __shared__ float2 shs[NT / 64];
   const int tid = threadIdx.x;
@@ -304,20 +304,15 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
         sel_max(st.mx, st.imx, shm[w8].mx, shm[w8].imx);
         sel_min(st.mn, st.imn, shm[w8].mn, shm[w8].imn);
       }
-      const QParams p = make_qparams(st.mx, st.mn, clip_strength(gl[row]), clip_strength(bl[row]), qmax);
+      const QParams p = make_group_qparams(quant, st.mx, st.mn, gl[row], bl[row], qmax);
       float2 sums = make_float2(0.f, 0.f);
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
         const int j = tid + NT * k;
         if (j < cpr) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const QElem qe = quant_elem(wt_at(k, e), p, qmax);
-            const float t = qe.q - p.z;
-            const float th = qe.m ? t - qe.u : t;
-            sums.x += g[k][e] * th;
-            if (!qe.m) sums.y += g[k][e];
-          }
+          for (int e = 0; e < 8; ++e)
+            group_terms(quant, g[k][e], quant_elem(wt_at(k, e), p, qmax), p, qmax, sums.x, sums.y);
         }
       }
       sums.x = wave_sum(sums.x);
@@ -330,10 +325,10 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
         sums.x += shs[w8].x;
         sums.y += shs[w8].y;
       }
-      const QGrad qg = quant_group_grad(sums.x, sums.y, st.mx, st.mn, p, qmax);
+      const GroupGrad qg = group_param_grads(quant, sums.x, sums.y, st.mx, st.mn, p, qmax, gs);
       if (tid == 0) {
-        dgl[row] = qg.dgamma * p.gamma * (1.0f - p.gamma);
-        dbl[row] = qg.dbeta * p.beta * (1.0f - p.beta);
+        dgl[row] = qg.d1;
+        dbl[row] = qg.d2;
       }
       if (LETW || dWt) {
 #pragma unroll
@@ -353,8 +348,10 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
             for (int e = 0; e < 8; ++e) {
               const int col = 8 * j + e;
               float x = quant_elem(wt_at(k, e), p, qmax).m ? gg[e] : 0.0f;
-              if (col == st.imx) x += qg.dmx;
-              if (col == st.imn) x += qg.dmn;
+              if (quant == WQ_LWC) {
+                if (col == st.imx) x += qg.dmx;
+                if (col == st.imn) x += qg.dmn;
+              }
               d[e] = x;
               if constexpr (LETW) dsacc[k][e] += x * wc[k].at(e);
             }
@@ -385,33 +382,31 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
         float sh = 0.f, sz = 0.f;
         bool mk[8];
         if (valid) {
-          p = make_qparams(st.mx, st.mn, clip_strength(gl[row * ng + grp]),
-                           clip_strength(bl[row * ng + grp]), qmax);
+          p = make_group_qparams(quant, st.mx, st.mn, gl[row * ng + grp], bl[row * ng + grp], qmax);
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const QElem qe = quant_elem(wt[e], p, qmax);
             mk[e] = qe.m;
-            const float t = qe.q - p.z;
-            const float th = qe.m ? t - qe.u : t;
-            sh += g[e] * th;
-            if (!qe.m) sz += g[e];
+            group_terms(quant, g[e], qe, p, qmax, sh, sz);
           }
         }
         sh = dyn_group_sum(sh, L);
         sz = dyn_group_sum(sz, L);
         if (valid) {
-          const QGrad qg = quant_group_grad(sh, sz, st.mx, st.mn, p, qmax);
+          const GroupGrad qg = group_param_grads(quant, sh, sz, st.mx, st.mn, p, qmax, gs);
           if (j % L == 0) {
-            dgl[row * ng + grp] = qg.dgamma * p.gamma * (1.0f - p.gamma);
-            dbl[row * ng + grp] = qg.dbeta * p.beta * (1.0f - p.beta);
+            dgl[row * ng + grp] = qg.d1;
+            dbl[row * ng + grp] = qg.d2;
           }
           float d[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int col = 8 * j + e;
             float x = mk[e] ? g[e] : 0.0f;
-            if (col == st.imx) x += qg.dmx;
-            if (col == st.imn) x += qg.dmn;
+            if (quant == WQ_LWC) {
+              if (col == st.imx) x += qg.dmx;
+              if (col == st.imn) x += qg.dmn;
+            }
             d[e] = x;
             if constexpr (LETW) dsacc[k][e] += x * w[e];
           }
@@ -951,12 +946,13 @@ template <typename TX, typename TQ, int KC>
 __global__ __launch_bounds__(NT) void act_fwd_kernel(
     const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
     const float* __restrict__ delta, int R, TQ* __restrict__ xdq, uint8_t* __restrict__ codes,
-    float* __restrict__ hout, float* __restrict__ zout) {
+    float* __restrict__ hout, float* __restrict__ zout, bool sym) {
   __shared__ MinMax shm[NT / 64];
   const int tid = threadIdx.x;
   const int cpr = int(C / 8);
   const bool quant = bits < 16;
   const float qmax = quant ? float((1 << bits) - 1) : 0.0f;
+  const float qs = quant ? float((1 << (bits - 1)) - 1) : 0.0f;
   float rs[KC][8], dl[KC][8];
 #pragma unroll
   for (int k = 0; k < KC; ++k) {
@@ -1002,7 +998,10 @@ __global__ __launch_bounds__(NT) void act_fwd_kernel(
       continue;
     }
     st = block_minmax(st, shm);
-    const QParams p = make_qparams(st.mx, st.mn, 1.0f, 1.0f, qmax);
+    int iab;
+    float sgn;
+    const QParams p = sym ? make_sym_qparams(st.mx, st.imx, st.mn, st.imn, qs, iab, sgn)
+                          : make_qparams(st.mx, st.mn, 1.0f, 1.0f, qmax);
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
       const int j = tid + NT * k;
@@ -1034,7 +1033,7 @@ template <typename TX, int KC>
 __global__ __launch_bounds__(NT) void act_bwd_kernel(
     const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
     const float* __restrict__ delta, int R, const float* __restrict__ dXdq,
-    float* __restrict__ dXt, float* __restrict__ p_sx, float* __restrict__ p_s1) {
+    float* __restrict__ dXt, float* __restrict__ p_sx, float* __restrict__ p_s1, bool sym) {
   __shared__ MinMax shm[NT / 64];
   __shared__ float2 shs[NT / 64];
   const int tid = threadIdx.x;
@@ -1042,6 +1041,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
   const int cpr = int(C / 8);
   const bool quant = bits < 16;
   const float qmax = quant ? float((1 << bits) - 1) : 0.0f;
+  const float qs = quant ? float((1 << (bits - 1)) - 1) : 0.0f;
   float rs[KC][8], dl[KC][8], asx[KC][8], as1[KC][8];
 #pragma unroll
   for (int k = 0; k < KC; ++k) {
@@ -1127,7 +1127,10 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
         sel_max(st.mx, st.imx, shm[w].mx, shm[w].imx);
         sel_min(st.mn, st.imn, shm[w].mn, shm[w].imn);
       }
-      const QParams p = make_qparams(st.mx, st.mn, 1.0f, 1.0f, qmax);
+      int iab = -1;
+      float sgn = 1.0f;
+      const QParams p = sym ? make_sym_qparams(st.mx, st.imx, st.mn, st.imn, qs, iab, sgn)
+                            : make_qparams(st.mx, st.mn, 1.0f, 1.0f, qmax);
       float2 sums = make_float2(0.f, 0.f);
       bool mk[KC][8];
 #pragma unroll
@@ -1156,6 +1159,9 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
         sums.y += shs[w].y;
       }
       const QGrad qg = quant_group_grad(sums.x, sums.y, st.mx, st.mn, p, qmax);
+      // symmetric: the zero point is fixed, dh = S_h goes to the absmax
+      // element through |x|max = qs * h, with that element's sign
+      const float dab = sym ? (p.hclamp ? 0.0f : sgn * div_rn(sums.x, qs)) : 0.0f;
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
         const int j = tid + NT * k;
@@ -1164,8 +1170,12 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
           for (int e = 0; e < 8; ++e) {
             const int col = 8 * j + e;
             float x = mk[k][e] ? g[k][e] : 0.0f;
-            if (col == st.imx) x += qg.dmx;
-            if (col == st.imn) x += qg.dmn;
+            if (sym) {
+              if (col == iab) x += dab;
+            } else {
+              if (col == st.imx) x += qg.dmx;
+              if (col == st.imn) x += qg.dmn;
+            }
             g[k][e] = x;
           }
         }
@@ -1191,6 +1201,46 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
       if (p_sx) store8(p_sx + int64_t(blockIdx.x) * C + 8 * j, asx[k]);
       if (p_s1) store8(p_s1 + int64_t(blockIdx.x) * C + 8 * j, as1[k]);
     }
+  }
+}
+
+// ------------------------------------------------------------------ quantiser initialisation
+// One wave per group: the group's (max, min) of w~ = s (.) w, and from them
+// the MinMax starting point of a quantiser variant: PACT (hi, lo) = (max,
+// min); LSQ (h, z) = Eq. 2's step and zero point at clip strength 1; LWC
+// keeps its logits at 4 (clip strength sigmoid(4)).
+template <typename TW>
+__global__ __launch_bounds__(NT) void wquant_init_kernel(const TW* __restrict__ W, int64_t n_groups,
+                                                         int64_t c_in, int group,
+                                                         const float* __restrict__ s, int bits,
+                                                         int quant, float* __restrict__ p1,
+                                                         float* __restrict__ p2) {
+  const int lane = threadIdx.x & 63;
+  const int64_t gi = int64_t(blockIdx.x) * (NT / 64) + (threadIdx.x >> 6);
+  if (gi >= n_groups) return;
+  const int64_t ng = c_in / group;
+  const int64_t row = gi / ng, c0 = (gi % ng) * group;
+  float mx = -FLT_MAX, mn = FLT_MAX;
+  int imx = INT_MAX, imn = INT_MAX;
+  for (int i = lane; i < group; i += 64) {
+    float w = load1(W + row * c_in + c0 + i);
+    if (s) w = w * s[c0 + i];
+    sel_max(mx, imx, w, i);
+    sel_min(mn, imn, w, i);
+  }
+  wave_minmax(mx, imx, mn, imn);
+  if (lane != 0) return;
+  const float qmax = float((1 << bits) - 1);
+  if (quant == WQ_PACT) {
+    p1[gi] = mx;
+    p2[gi] = mn;
+  } else if (quant == WQ_LSQ) {
+    const QParams p = make_qparams(mx, mn, 1.0f, 1.0f, qmax);
+    p1[gi] = p.h;
+    p2[gi] = p.z;
+  } else {
+    p1[gi] = 4.0f;
+    p2[gi] = 4.0f;
   }
 }
 
@@ -1260,11 +1310,12 @@ bool quant_shape_supported(int64_t c_in, int64_t group) {
 hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
                    const float* gl, const float* bl, int bits, int64_t group, void* W_dq,
                    bool dq_bf16, uint8_t* codes, float* h, float* z, hipStream_t st,
-                   float4* gstat) {
+                   float4* gstat, int quant) {
   if (!quant_shape_supported(c_in, group)) return hipErrorInvalidValue;
   if (c_out <= 0) return hipSuccess;
-  if (gstat && (s || !small_group(group))) return hipErrorInvalidValue;
-  if (small_group(group) && !s) {
+  if (gstat && (s || !small_group(group) || quant != WQ_LWC)) return hipErrorInvalidValue;
+  if (quant < WQ_LWC || quant > WQ_LSQ) return hipErrorInvalidValue;
+  if (small_group(group) && !s && quant == WQ_LWC) {
     const int64_t nchunk = c_out * c_in / 8;
     const int64_t waves = std::min<int64_t>((nchunk + 511) / 512, 256 * 32);
     const dim3 grid(unsigned((waves * 64 + NT - 1) / NT));
@@ -1297,7 +1348,7 @@ hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
     return hipGetLastError();
   }
   const int64_t per_lane = (c_in / 8 + 63) / 64;
-  if (group == c_in && per_lane <= 32) {
+  if (group == c_in && per_lane <= 32 && quant == WQ_LWC) {
     const int ch = per_lane <= 2 ? 2 : per_lane <= 4 ? 4 : per_lane <= 8 ? 8 : per_lane <= 12 ? 12
                  : per_lane <= 16 ? 16 : per_lane <= 24 ? 24 : 32;
     const unsigned lds = s ? unsigned(ch) * 128u * 16u : 0u;
@@ -1345,7 +1396,7 @@ hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
     constexpr bool WR = decltype(wr)::value;
     hipLaunchKernelGGL((lwc_fwd_kernel<TW, TQ, KCc, WR>), grid, dim3(NT), 0, st,
                        static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits, int(group), R,
-                       static_cast<TQ*>(W_dq), codes, h, z);
+                       static_cast<TQ*>(W_dq), codes, h, z, quant);
   };
   auto by_kc = [&](auto tw, auto tq, auto wr) -> hipError_t {
     OQ_KC_SWITCH(kc, go(tw, tq, std::integral_constant<int, KC>{}, wr))
@@ -1358,6 +1409,21 @@ hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
   if (w_bf16) e = dq_bf16 ? by_wr(uint16_t{}, uint16_t{}) : by_wr(uint16_t{}, float{});
   else e = dq_bf16 ? by_wr(float{}, uint16_t{}) : by_wr(float{}, float{});
   if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t wquant_init(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
+                       int bits, int64_t group, int quant, float* p1, float* p2, hipStream_t st) {
+  if (group <= 0 || c_in % group || quant < WQ_LWC || quant > WQ_LSQ) return hipErrorInvalidValue;
+  const int64_t n = c_out * (c_in / group);
+  if (n <= 0) return hipSuccess;
+  const dim3 grid(unsigned((n + NT / 64 - 1) / (NT / 64)));
+  if (w_bf16)
+    hipLaunchKernelGGL(wquant_init_kernel<uint16_t>, grid, dim3(NT), 0, st,
+                       static_cast<const uint16_t*>(W), n, c_in, int(group), s, bits, quant, p1, p2);
+  else
+    hipLaunchKernelGGL(wquant_init_kernel<float>, grid, dim3(NT), 0, st,
+                       static_cast<const float*>(W), n, c_in, int(group), s, bits, quant, p1, p2);
   return hipGetLastError();
 }
 
@@ -1375,13 +1441,17 @@ bool lwc_bwd_sums_parts(int64_t c_out, int64_t c_in, int64_t group, bool has_s, 
 hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,
                    const float* gl, const float* bl, int bits, int64_t group, const float* dW,
                    float* dgl, float* dbl, float* dW_tilde, float* ds_parts, hipStream_t st,
-                   int parts, int64_t part_stride) {
+                   int parts, int64_t part_stride, int quant) {
   if (!quant_shape_supported(c_in, group)) return hipErrorInvalidValue;
   if (c_out <= 0) return hipSuccess;
+  if (quant < WQ_LWC || quant > WQ_LSQ || (quant != WQ_LWC && parts != 1))
+    return hipErrorInvalidValue;
   if (parts < 1 || (parts > 1 && (!lwc_bwd_sums_parts(c_out, c_in, group, s, ds_parts) ||
                                   part_stride < c_out * c_in || part_stride % 4)))
     return hipErrorInvalidValue;
-  if (lwc_bwd_sums_parts(c_out, c_in, group, s, ds_parts)) {
+  // LSQ's gradient scale 1/sqrt(n * Q_P), n = weights per step size
+  const float gs = float(1.0 / std::sqrt(double(group) * double((1 << bits) - 1)));
+  if (quant == WQ_LWC && lwc_bwd_sums_parts(c_out, c_in, group, s, ds_parts)) {
     const int E = int(std::min<int64_t>(group, 32));
     const int64_t nrun = c_out * (c_in / E);
     const dim3 grid(unsigned((nrun + NT - 1) / NT));
@@ -1421,14 +1491,14 @@ hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
       const int R = rows_per_block(c_out, LWC_BLOCKS);
       hipLaunchKernelGGL((lwc_bwd_kernel<TW, KCc, WR, true>), dim3(unsigned((c_out + R - 1) / R)),
                          dim3(NT), 0, st, static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits,
-                         int(group), R, dW, dgl, dbl, dW_tilde, ds_parts);
+                         int(group), R, dW, dgl, dbl, dW_tilde, ds_parts, quant, gs);
     } else {
       // no partials: one round of resident blocks
       const int R = rows_per_block(
           c_out, resident_blocks(reinterpret_cast<const void*>(lwc_bwd_kernel<TW, KCc, WR, false>)));
       hipLaunchKernelGGL((lwc_bwd_kernel<TW, KCc, WR, false>), dim3(unsigned((c_out + R - 1) / R)),
                          dim3(NT), 0, st, static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits,
-                         int(group), R, dW, dgl, dbl, dW_tilde, ds_parts);
+                         int(group), R, dW, dgl, dbl, dW_tilde, ds_parts, quant, gs);
     }
   };
   auto by_kc = [&](auto tw, auto wr) -> hipError_t {
@@ -1445,12 +1515,13 @@ hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
 
 hipError_t act_fwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, const float* s,
                    const float* delta, void* X_dq, bool dq_bf16, uint8_t* codes, float* h,
-                   float* z, hipStream_t st) {
+                   float* z, hipStream_t st, bool sym) {
   const int kc = kc_for(C);
   if (C <= 0 || C % 8 || kc == 0) return hipErrorInvalidValue;
   if (T <= 0) return hipSuccess;
+  if (sym && bits >= 16) sym = false;
   const int64_t per_lane = (C / 8 + 63) / 64;
-  if (x_bf16 == dq_bf16 && per_lane <= 32 && (X_dq || bits < 16)) {
+  if (x_bf16 == dq_bf16 && per_lane <= 32 && (X_dq || bits < 16) && !sym) {
     const int ch = per_lane <= 2 ? 2 : per_lane <= 4 ? 4 : per_lane <= 8 ? 8 : per_lane <= 12 ? 12
                  : per_lane <= 16 ? 16 : per_lane <= 24 ? 24 : 32;
     const unsigned lds = (s || delta) ? unsigned(ch) * 128u * 2u * 16u : 0u;
@@ -1487,7 +1558,7 @@ hipError_t act_fwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, c
     constexpr int KCc = decltype(kcc)::value;
     hipLaunchKernelGGL((act_fwd_kernel<TX, TQ, KCc>), grid, dim3(NT), 0, st,
                        static_cast<const TX*>(X), T, C, bits, s, delta, R, static_cast<TQ*>(X_dq),
-                       codes, h, z);
+                       codes, h, z, sym);
   };
   auto by_kc = [&](auto tx, auto tq) -> hipError_t {
     OQ_KC_SWITCH(kc, go(tx, tq, std::integral_constant<int, KC>{}))
@@ -1508,7 +1579,7 @@ int64_t act_bwd_nparts(int64_t T) {
 
 hipError_t act_bwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, const float* s,
                    const float* delta, const float* dXdq, float* dXt, float* p_sx, float* p_s1,
-                   hipStream_t st) {
+                   hipStream_t st, bool sym) {
   const int kc = kc_for(C);
   if (C <= 0 || C % 8 || kc == 0) return hipErrorInvalidValue;
   if (T <= 0) return hipSuccess;
@@ -1518,7 +1589,8 @@ hipError_t act_bwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, c
     using TX = decltype(tx);
     constexpr int KCc = decltype(kcc)::value;
     hipLaunchKernelGGL((act_bwd_kernel<TX, KCc>), grid, dim3(NT), 0, st,
-                       static_cast<const TX*>(X), T, C, bits, s, delta, R, dXdq, dXt, p_sx, p_s1);
+                       static_cast<const TX*>(X), T, C, bits, s, delta, R, dXdq, dXt, p_sx, p_s1,
+                       sym && bits < 16);
   };
   auto by_kc = [&](auto tx) -> hipError_t {
     OQ_KC_SWITCH(kc, go(tx, std::integral_constant<int, KC>{}))

@@ -15,6 +15,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liboq.so")
 
 OQ_F32, OQ_BF16 = 0, 1
+WQ_LWC, WQ_PACT, WQ_LSQ = 0, 1, 2          # weight quantisers (lin_quant)
+ACT_SYM = 0x100                            # OR into activation bits: symmetric absmax
 MAX_SITES, MAX_LINEARS = 8, 16
 PROF_KINDS = ["gemm_fwd", "gemm_wgrad", "gemm_dgrad", "lwc_fwd", "lwc_bwd", "act_fwd",
               "act_bwd", "transpose", "other", "packed_linear"]
@@ -30,6 +32,11 @@ SIGNATURES = {
     "oq_lwc_fakequant_bwd": (_I, [_P, _I, _I64, _I64, _P, _P, _P, _I, _I64, _P, _P, _P, _P, _P,
                                   _P, _SZ, _P]),
     "oq_lwc_fakequant_bwd_workspace_size": (_I, [_I64, _I64, _I64, _I, _PSZ]),
+    "oq_wquant_fakequant_fwd": (_I, [_I, _P, _I, _I64, _I64, _P, _P, _P, _I, _I64, _P, _I, _P, _P,
+                                     _P, _P]),
+    "oq_wquant_fakequant_bwd": (_I, [_I, _P, _I, _I64, _I64, _P, _P, _P, _I, _I64, _P, _P, _P, _P,
+                                     _P, _P, _SZ, _P]),
+    "oq_wquant_init": (_I, [_I, _P, _I, _I64, _I64, _P, _I, _I64, _P, _P, _P]),
     "oq_let_fold": (_I, [_P, _I, _P, _I64, _I64, _P, _P, _P, _I, _P, _P]),
     "oq_act_fakequant_fwd": (_I, [_P, _I, _I64, _I64, _I, _P, _P, _P, _I, _P, _P, _P, _P]),
     "oq_act_fakequant_bwd": (_I, [_P, _I, _I64, _I64, _I, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
@@ -42,10 +49,14 @@ SIGNATURES = {
     "oq_matmul": (_I, [_P, _I, _P, _I, _I64, _I64, _I64, _P, _P]),
     "oq_adamw_step": (_I, [_P, _P, _P, _P, _I64, _D, _D, _D, _D, _D, _I, _P]),
     "oq_block_workspace_size": (_I, [_P, _PSZ]),
+    "oq_block_plan": (_I, [_P, _P, _I]),
     "oq_block_calib_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "oq_block_calibrate": (_I, [_P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "oq_block_export_workspace_size": (_I, [_P, _PSZ]),
     "oq_block_export": (_I, [_P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "oq_let_absorb": (_I, [_P, _I, _P, _I64, _I64, _P, _P, _P, _P, _P]),
+    "oq_block_state_save": (_I, [_P, _P, _P, _I, C.c_char_p, _P]),
+    "oq_block_state_load": (_I, [_P, _P, _P, C.POINTER(C.c_int), C.c_char_p, _P]),
     "oq_pack_codes": (_I, [_P, _I64, _I64, _I, _P, _P]),
     "oq_packed_linear": (_I, [_P, _I, _I64, _I64, _P, _I, _I64, _P, _P, _P, _I64, _P, _I, _P]),
     "oq_profile_enable": (_I, [_I]),
@@ -65,7 +76,7 @@ class BlockDesc(C.Structure):
                 ("site_width", C.c_int64 * MAX_SITES), ("site_let", C.c_int * MAX_SITES),
                 ("site_act_bits", C.c_int * MAX_SITES), ("lin_site", C.c_int * MAX_LINEARS),
                 ("lin_c_out", C.c_int64 * MAX_LINEARS), ("lin_bits", C.c_int * MAX_LINEARS),
-                ("lin_group", C.c_int64 * MAX_LINEARS)]
+                ("lin_group", C.c_int64 * MAX_LINEARS), ("lin_quant", C.c_int * MAX_LINEARS)]
 
 
 class BlockParams(C.Structure):
@@ -88,7 +99,10 @@ class BlockOptim(C.Structure):
                 ("m_delta", C.c_void_p * MAX_SITES), ("v_delta", C.c_void_p * MAX_SITES),
                 ("step", C.c_int), ("lr_lwc", C.c_double), ("lr_let", C.c_double),
                 ("beta1", C.c_double), ("beta2", C.c_double), ("eps", C.c_double),
-                ("wd", C.c_double)]
+                ("wd", C.c_double), ("frozen", C.c_int)]
+
+
+FREEZE_LWC, FREEZE_LET = 1, 2
 
 
 _lib = None
@@ -187,6 +201,55 @@ def lwc_fakequant_bwd(W, gamma_logit, beta_logit, bits, group, dW_dq, s=None, wa
     return dg, db, ds, dwt
 
 
+def wquant_fakequant_fwd(quantizer, W, p1, p2, bits, group, s=None, dq_dtype=None, codes=True,
+                         hz=True, stream=None):
+    """Any weight quantiser's forward (WQ_LWC / WQ_PACT / WQ_LSQ).
+    Returns (W_dq, codes | None, h | None, z | None)."""
+    c_out, c_in = W.shape
+    dev = W.device
+    dq_dt = _dt(W) if dq_dtype is None else (OQ_BF16 if dq_dtype == torch.bfloat16 else OQ_F32)
+    W_dq = torch.empty((c_out, c_in), dtype=_tdt(dq_dt), device=dev)
+    cd = torch.empty((c_out, c_in), dtype=torch.uint8, device=dev) if codes else None
+    ng = c_in // group
+    h = torch.empty((c_out, ng), dtype=torch.float32, device=dev) if hz else None
+    z = torch.empty((c_out, ng), dtype=torch.float32, device=dev) if hz else None
+    _check(lib().oq_wquant_fakequant_fwd(quantizer, _ptr(W), _dt(W), c_out, c_in, _ptr(s),
+                                         _ptr(_f32(p1, "p1")), _ptr(_f32(p2, "p2")), bits, group,
+                                         _ptr(W_dq), dq_dt, _ptr(cd), _ptr(h), _ptr(z),
+                                         _stream(stream)))
+    return W_dq, cd, h, z
+
+
+def wquant_fakequant_bwd(quantizer, W, p1, p2, bits, group, dW_dq, s=None, want_d_s=False,
+                         want_dW_tilde=False, stream=None):
+    """Returns (d_p1, d_p2, d_s | None, dW_tilde | None)."""
+    c_out, c_in = W.shape
+    dev = W.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    d1 = torch.empty_like(p1)
+    d2 = torch.empty_like(p2)
+    ds = torch.empty(c_in, **f32) if want_d_s else None
+    dwt = torch.empty((c_out, c_in), **f32) if want_dW_tilde else None
+    n = C.c_size_t(0)
+    _check(lib().oq_lwc_fakequant_bwd_workspace_size(c_out, c_in, group, int(want_d_s), C.byref(n)))
+    ws = torch.empty(max(n.value, 1), dtype=torch.uint8, device=dev)
+    _check(lib().oq_wquant_fakequant_bwd(quantizer, _ptr(W), _dt(W), c_out, c_in, _ptr(s),
+                                         _ptr(p1), _ptr(p2), bits, group,
+                                         _ptr(_f32(dW_dq, "dW_dq")), _ptr(d1), _ptr(d2), _ptr(ds),
+                                         _ptr(dwt), _ptr(ws), n.value, _stream(stream)))
+    return d1, d2, ds, dwt
+
+
+def wquant_init(quantizer, W, bits, group, s=None, stream=None):
+    """MinMax starting parameters (p1, p2) of a weight quantiser per group."""
+    c_out, c_in = W.shape
+    p1 = torch.empty((c_out, c_in // group), dtype=torch.float32, device=W.device)
+    p2 = torch.empty_like(p1)
+    _check(lib().oq_wquant_init(quantizer, _ptr(W), _dt(W), c_out, c_in, _ptr(s), bits, group,
+                                _ptr(p1), _ptr(p2), _stream(stream)))
+    return p1, p2
+
+
 def let_fold(W, B=None, s=None, delta=None, wt_dtype=None, want_W_tilde=True, stream=None):
     """Eq. 3 fold.  Returns (W_tilde | None, B_tilde)."""
     c_out, c_in = W.shape
@@ -206,9 +269,10 @@ def act_fakequant_fwd(X, bits, s=None, delta=None, dq_dtype=None, codes=True, hz
     dq_dtype = dq_dtype or X.dtype
     dev = X.device
     Xq = torch.empty((T, Cw), dtype=dq_dtype, device=dev)
-    cd = torch.empty((T, Cw), dtype=torch.uint8, device=dev) if (codes and bits < 16) else None
-    h = torch.empty(T, dtype=torch.float32, device=dev) if (hz and bits < 16) else None
-    z = torch.empty(T, dtype=torch.float32, device=dev) if (hz and bits < 16) else None
+    quant = (bits & ~ACT_SYM) < 16
+    cd = torch.empty((T, Cw), dtype=torch.uint8, device=dev) if (codes and quant) else None
+    h = torch.empty(T, dtype=torch.float32, device=dev) if (hz and quant) else None
+    z = torch.empty(T, dtype=torch.float32, device=dev) if (hz and quant) else None
     _check(lib().oq_act_fakequant_fwd(_ptr(X), _dt(X), T, Cw, bits, _ptr(_f32(s, "s")),
                                       _ptr(_f32(delta, "delta")), _ptr(Xq), _dt(Xq), _ptr(cd),
                                       _ptr(h), _ptr(z), _stream(stream)))
@@ -240,6 +304,19 @@ def act_fakequant_bwd_noalloc_into(X, bits, dX_dq, dX_tilde, d_s, d_delta, s=Non
     _check(lib().oq_act_fakequant_bwd_noalloc(_ptr(X), _dt(X), T, Cw, bits, _ptr(s), _ptr(delta),
                                               _ptr(_f32(dX_dq, "dX_dq")), _ptr(dX_tilde),
                                               _ptr(d_s), _ptr(d_delta), _stream(stream)))
+
+
+def let_absorb(P, s, delta, b=None, stream=None):
+    """LET absorbed into the producer of a site's input: P [C] (a norm gain)
+    or [C, n] (a previous linear's weight, output channels as rows).
+    Returns (P / s row-wise, (b - delta) / s)."""
+    Cn = P.shape[0]
+    n = P.numel() // Cn if Cn else 0
+    P_out = torch.empty_like(P)
+    b_out = torch.empty(Cn, dtype=torch.float32, device=P.device)
+    _check(lib().oq_let_absorb(_ptr(P), _dt(P), _ptr(b), Cn, n, _ptr(s), _ptr(delta), _ptr(P_out),
+                               _ptr(b_out), _stream(stream)))
+    return P_out, b_out
 
 
 def let_init(X, Ws, stream=None):
@@ -338,8 +415,10 @@ class Block:
     """One block's calibration problem: description, parameters, gradient
     buffers, AdamW state and workspace, all device tensors owned by torch.
 
-    ``sites``   list of (width, let, act_bits)
-    ``linears`` list of (site, c_out, bits, group); linears of a site consecutive
+    ``sites``   list of (width, let, act_bits); act_bits may carry ACT_SYM
+    ``linears`` list of (site, c_out, bits, group[, quantizer]); linears of a
+                site consecutive; quantizer WQ_LWC (default), WQ_PACT or WQ_LSQ
+                (the gamma/beta tensors then hold that quantizer's parameters)
     """
 
     def __init__(self, T, sites, linears, dtype=torch.bfloat16, device="cuda"):
@@ -351,22 +430,34 @@ class Block:
         d.dtype = OQ_BF16 if dtype == torch.bfloat16 else OQ_F32
         for k, (w, let, ab) in enumerate(sites):
             d.site_width[k], d.site_let[k], d.site_act_bits[k] = w, int(bool(let)), ab
-        for l, (k, co, bits, g) in enumerate(linears):
+        for l, lin in enumerate(linears):
+            k, co, bits, g = lin[:4]
             d.lin_site[l], d.lin_c_out[l], d.lin_bits[l], d.lin_group[l] = k, co, bits, g
+            d.lin_quant[l] = lin[4] if len(lin) > 4 else WQ_LWC
         self.desc = d
         n = C.c_size_t(0)
         _check(lib().oq_block_workspace_size(C.byref(d), C.byref(n)))
         self.ws_bytes = n.value
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
         f32 = dict(dtype=torch.float32, device=device)
-        self.d_gamma = [torch.empty((co, sites[k][0] // g), **f32) for (k, co, _, g) in linears]
+        self.d_gamma = [torch.empty((lin[1], sites[lin[0]][0] // lin[3]), **f32) for lin in linears]
         self.d_beta = [torch.empty_like(t) for t in self.d_gamma]
         self.d_s = [torch.empty(w, **f32) if let else None for (w, let, _) in sites]
         self.d_delta = [torch.empty(w, **f32) if let else None for (w, let, _) in sites]
-        self.row_loss = [torch.empty(co, **f32) for (_, co, _, _) in linears]
+        self.row_loss = [torch.empty(lin[1], **f32) for lin in linears]
         self.loss = torch.empty((), **f32)
         self.opt_state = None
         self.step_count = 0
+
+    PLAN_FIELDS = ("concurrent", "direct", "wgrad_splits", "fwd_splits", "fused_lwc", "wt_copy")
+
+    def plan(self):
+        """The step's launch plan per site: a list of dicts of PLAN_FIELDS."""
+        n = len(self.PLAN_FIELDS) * len(self.sites)
+        buf = (C.c_int * n)()
+        _check(lib().oq_block_plan(C.byref(self.desc), buf, n))
+        k = len(self.PLAN_FIELDS)
+        return [dict(zip(self.PLAN_FIELDS, buf[i * k:(i + 1) * k])) for i in range(len(self.sites))]
 
     def init_optimizer(self, lr_lwc=5e-3, lr_let=1e-2, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.0):
         f32 = dict(dtype=torch.float32, device=self.device)
@@ -387,7 +478,7 @@ class Block:
         self.opt_state = o
 
     def step(self, X_q, Y_fp_T, W, gamma_logit, beta_logit, s=None, delta=None, B=None,
-             update=False, stream=None):
+             update=False, frozen=0, stream=None):
         """One calibration step.  Tensors are lists per site (X_q, s, delta) or
         per linear (Y_fp_T, W, logits, B).  With ``update`` the AdamW state of
         :meth:`init_optimizer` updates the logits, s and delta in place."""
@@ -416,6 +507,7 @@ class Block:
                 raise OQError("call init_optimizer() before update=True")
             self.step_count += 1
             self.opt_state.step = self.step_count
+            self.opt_state.frozen = frozen
             opt = C.byref(self.opt_state)
         _check(lib().oq_block_calib_step(C.byref(self.desc), yp, xp, C.byref(prm), C.byref(grd),
                                          opt, _ptr(self.loss), _ptr(self.ws), self.ws_bytes,
@@ -441,12 +533,30 @@ class Block:
                 grd.d_delta[k] = self.d_delta[k].data_ptr()
         return prm, grd
 
+    def save_state(self, path, W, gamma_logit, beta_logit, s=None, delta=None, stream=None):
+        """Write Theta (and the AdamW state, when initialised) to ``path``."""
+        prm, _ = self._param_structs(W, gamma_logit, beta_logit, s, delta, None)
+        opt = C.byref(self.opt_state) if self.opt_state is not None else None
+        _check(lib().oq_block_state_save(C.byref(self.desc), C.byref(prm), opt, self.step_count,
+                                         os.fsencode(path), _stream(stream)))
+
+    def load_state(self, path, W, gamma_logit, beta_logit, s=None, delta=None, stream=None):
+        """Restore Theta (and the AdamW state, when initialised) from ``path``
+        into the given tensors; the step count continues from the file."""
+        prm, _ = self._param_structs(W, gamma_logit, beta_logit, s, delta, None)
+        opt = C.byref(self.opt_state) if self.opt_state is not None else None
+        done = C.c_int(0)
+        _check(lib().oq_block_state_load(C.byref(self.desc), C.byref(prm), opt, C.byref(done),
+                                         os.fsencode(path), _stream(stream)))
+        self.step_count = done.value
+
     def export(self, W, gamma_logit, beta_logit, s=None, delta=None, B=None, stream=None):
         """Algorithm 1's quantised block: per linear (packed codes, h, z, B~)."""
         nl = len(self.linears)
         prm, _ = self._param_structs(W, gamma_logit, beta_logit, s, delta, B)
         outs = []
-        for l, (k, c_out, bits, group) in enumerate(self.linears):
+        for l, lin in enumerate(self.linears):
+            k, c_out, bits, group = lin[:4]
             c_in = self.sites[k][0]
             f32 = dict(dtype=torch.float32, device=self.device)
             outs.append((torch.empty((c_out, c_in * bits // 8), dtype=torch.uint8, device=self.device),
@@ -461,11 +571,12 @@ class Block:
         return outs
 
     def calibrate(self, X_q_segs, Y_fp_T_segs, W, gamma_logit, beta_logit, epochs, s=None,
-                  delta=None, B=None, stream=None):
+                  delta=None, B=None, frozen=0, stream=None):
         """Algorithm 1's loop: ``epochs`` passes over the segments in order,
         AdamW after every step.  ``X_q_segs[g]`` / ``Y_fp_T_segs[g]`` are the
         per-site / per-linear lists of segment g.  Returns the device tensor of
-        the epochs * segments step losses."""
+        the epochs * segments step losses.  ``frozen`` (FREEZE_LWC | FREEZE_LET)
+        keeps a parameter set and its AdamW state fixed (iterative training)."""
         if self.opt_state is None:
             raise OQError("call init_optimizer() before calibrate()")
         nl, ns, ng = len(self.linears), len(self.sites), len(X_q_segs)
@@ -474,6 +585,7 @@ class Block:
         xp = (C.c_void_p * (ng * ns))(*[_ptr(x).value for seg in X_q_segs for x in seg])
         losses = torch.empty(epochs * ng, dtype=torch.float32, device=self.device)
         self.opt_state.step = self.step_count + 1
+        self.opt_state.frozen = frozen
         _check(lib().oq_block_calibrate(C.byref(self.desc), ng, epochs, yp, xp, C.byref(prm),
                                         C.byref(grd), C.byref(self.opt_state), _ptr(losses),
                                         _ptr(self.ws), self.ws_bytes, _stream(stream)))

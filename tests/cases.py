@@ -149,3 +149,38 @@ def within(got, ref, bound, name):
     bad = err > bound
     assert not np.any(bad), (name, int(np.sum(bad)), ratio, np.argwhere(bad)[:5].tolist())
     return ratio
+
+
+def variant_grad_bounds(st, G, quant):
+    """Per-element bounds like :func:`quant_grad_bounds` for PACT / LSQ weight
+    quantisers and the symmetric activation quantiser (``quant`` "pact",
+    "lsq" or "sym"): each group sum of n terms within (n + 8) u of its terms'
+    magnitudes, a few roundings of the results.  Returns (dx_bound, d1_bound,
+    d2_bound); d1/d2 are None for "sym"."""
+    g = np.asarray(G, np.float64).reshape(st["q"].shape)
+    q, u, m = (st[k].astype(np.float64) for k in ("q", "u", "m"))
+    z = st["z"].astype(np.float64)[:, None]
+    n = g.shape[1]
+    eps = (n + 8) * U32
+    dx_b = 2 * U32 * np.abs(g * m)
+    if quant == "pact":
+        c = st["c"].astype(np.float64)
+        qmax = float(st["qmax"])
+        a1 = np.sum(np.abs(g) * (c > qmax), axis=1)
+        a2 = np.sum(np.abs(g) * (c < 0), axis=1)
+        return dx_b, eps * a1, eps * a2
+    a_h = np.sum(np.abs(g * ((q - z) - m * u)), axis=1)
+    s_h = np.sum(g * ((q - z) - m * u), axis=1)
+    if quant == "lsq":
+        gs = 1.0 / np.sqrt(float(n) * float(st["qmax"]))
+        h = st["h"].astype(np.float64)
+        a_z = np.sum(np.abs(g * (1.0 - m)), axis=1)
+        s_z = np.sum(g * (1.0 - m), axis=1)
+        d1 = np.where(st["hclamp"], 0.0, gs * (eps * a_h + 2 * U32 * np.abs(s_h)))
+        d2 = gs * h * (eps * a_z + 3 * U32 * np.abs(s_z))
+        return dx_b, d1, d2
+    # symmetric activations: sign * S_h / qs added at the absmax element
+    qs = float(st["qs"])
+    e = np.where(st["hclamp"], 0.0, (eps * a_h + 2 * U32 * np.abs(s_h)) / qs)
+    dx_b[np.arange(g.shape[0]), st["i_ab"]] += e + 2 * U32 * np.abs(s_h) / qs
+    return dx_b, None, None

@@ -162,6 +162,74 @@ def test_block_desc_validation():
     assert st == WORKSPACE
 
 
+def _export_call(d, prm=None, packed=None, h=None, z=None, ws=FAKE, nbytes=None):
+    L = oq.lib()
+    n = C.c_size_t(0)
+    L.oq_block_export_workspace_size(C.byref(d), C.byref(n))
+    nl = d.n_linears
+    arr = lambda v: (C.c_void_p * nl)(*([v] * nl))
+    if prm is None:
+        prm = oq.BlockParams()
+        for l in range(nl):
+            prm.W[l] = prm.gamma_logit[l] = prm.beta_logit[l] = 0x10000
+        for k in range(d.n_sites):
+            prm.s[k] = prm.delta[k] = 0x10000
+    return L.oq_block_export(C.byref(d), C.byref(prm), packed or arr(0x10000), h or arr(0x10000),
+                             z or arr(0x10000), None, ws, n.value if nbytes is None else nbytes,
+                             None)
+
+
+def test_export_validation():
+    """oq_block_export checks everything before its first launch: workspace
+    size and alignment, C_in % 32, outputs, and that the packed linear can
+    consume what it writes (bits 2..7, groups of whole 32-code runs)."""
+    L = oq.lib()
+    assert _export_call(_desc(configs.C2), nbytes=16) == WORKSPACE
+    assert _export_call(_desc(configs.C2), ws=MISALIGNED) == WORKSPACE
+    assert _export_call(_desc(configs.C2), ws=None) == WORKSPACE
+    d = _desc(configs.C2)
+    d.lin_bits[2] = 8
+    assert _export_call(d) == UNSUPPORTED and b"packed_linear" in L.oq_last_error()
+    d = _desc(configs.C2)
+    for l in range(d.n_linears):
+        d.lin_group[l] = 16
+    assert _export_call(d) == UNSUPPORTED
+    d = _desc(configs.C1)
+    d.site_width[0] = d.lin_c_out[0] = 264          # C_in % 32 != 0 (groups of 8 divide it)
+    d.lin_group[0] = 8
+    assert _export_call(d) == INVALID
+    nl = configs.C2.linears
+    missing = (C.c_void_p * len(nl))(*([0x10000] * (len(nl) - 1) + [None]))
+    assert _export_call(_desc(configs.C2), packed=missing) == INVALID
+    assert _export_call(_desc(configs.C2), z=missing) == INVALID
+    misaligned = (C.c_void_p * len(nl))(*([0x10004] * len(nl)))
+    assert _export_call(_desc(configs.C2), packed=misaligned) == INVALID
+
+
+def test_block_plan_of_benchmark_workloads():
+    """The launch plan is a host-side function of the descriptor: at the
+    benchmark's 262,144 tokens every site runs in sequence and the gradient
+    products read their operands as stored; the plans the full-size GPU tests
+    assert are the ones fixed here."""
+    L = oq.lib()
+    expect = {  # per site: concurrent, direct, wgrad splits, fwd splits, fused LWC bwd, W^T copy
+        "llama7b_w3a16_g128": [[0, 1, 1, 1, 1, 0], [0, 1, 1, 1, 1, 0], [0, 1, 2, 1, 0, 0], [0, 1, 4, 1, 0, 0]],
+        "llama7b_w4a4_let_lwc": [[0, 1, 1, 1, 0, 1], [0, 1, 1, 1, 0, 1], [0, 1, 2, 1, 0, 1], [0, 1, 4, 1, 0, 0]],
+        "llama13b_w2a16_g64": [[0, 1, 4, 1, 0, 0], [0, 1, 8, 1, 0, 0], [0, 1, 2, 1, 0, 0], [0, 1, 4, 1, 0, 0]],
+        "llama2_70b_w4a16_g128": [[0, 1, 1, 1, 1, 0]] * 4,
+    }
+    for w in configs.CONFIGS[1:]:
+        n = 6 * len(w.sites)
+        buf = (C.c_int * n)()
+        assert L.oq_block_plan(C.byref(_desc(w)), buf, n) == OK
+        assert [list(buf[i * 6:(i + 1) * 6]) for i in range(len(w.sites))] == expect[w.name], w.name
+    # the paper's 2048-token segment runs the sites concurrently
+    buf = (C.c_int * 24)()
+    assert L.oq_block_plan(C.byref(_desc(configs.C2.with_tokens(2048))), buf, 24) == OK
+    assert all(buf[6 * k] == 1 for k in range(4))
+    assert L.oq_block_plan(C.byref(_desc(configs.C2)), buf, 5) == INVALID
+
+
 def test_calibrate_validation():
     L = oq.lib()
     d = _desc(configs.C1)
@@ -212,3 +280,65 @@ def test_act_bwd_noalloc_limits():
                                           None, FAKE, None, None) == UNSUPPORTED
     assert L.oq_act_fakequant_bwd_workspace_size(1 << 20, 4096, C.byref(n)) == OK
     assert n.value <= lim        # 4096 channels fit at any token count
+
+
+def _ckpt_bytes(w, completed=3, c_out_override=None, bad_hash=False, truncate=0):
+    """A checkpoint file written by hand from the layout include/oq.h states
+    (no AdamW state): header, shape record, then each clipping-logit tensor."""
+    import struct
+    import numpy as np
+    nl, ns = len(w.linears), len(w.sites)
+    pad = lambda xs, n: list(xs) + [0] * (n - len(xs))
+    c_outs = [l.c_out for l in w.linears]
+    if c_out_override is not None:
+        c_outs[0] = c_out_override
+    shape = struct.pack("<ii8q8i8i16i16q16i16q16i", ns, nl,
+                        *pad([s.width for s in w.sites], 8), *pad([int(s.let) for s in w.sites], 8),
+                        *pad([s.act_bits for s in w.sites], 8), *pad([l.site for l in w.linears], 16),
+                        *pad(c_outs, 16), *pad([l.bits for l in w.linears], 16),
+                        *pad([l.group for l in w.linears], 16), *pad([0] * nl, 16))
+    assert len(shape) == 584
+    tensors = []
+    for i, l in enumerate(w.linears):
+        n = l.c_out * (w.sites[l.site].width // l.group)
+        for kind in (0, 1):
+            data = np.full(n, 4.0, np.float32).tobytes()
+            h = 1469598103934665603
+            for byte in data:
+                h = ((h ^ byte) * 1099511628211) & (2 ** 64 - 1)
+            if bad_hash:
+                h ^= 1
+            tensors.append(struct.pack("<IIQQ", kind, i, n, h) + data)
+    head = b"OQCKPT\0\1" + struct.pack("<iiii", 1, 584, completed, 0) + shape + \
+        struct.pack("<Q", len(tensors))
+    blob = head + b"".join(tensors)
+    return blob[:len(blob) - truncate] if truncate else blob
+
+
+def test_checkpoint_load_validation(tmp_path):
+    """A block checkpoint is verified completely before any device buffer is
+    written: magic, shape, sizes and every hash (the file is written here
+    from the documented layout)."""
+    L = oq.lib()
+    w = configs.C1
+    d = _desc(w)
+    prm = oq.BlockParams()
+    prm.W[0] = prm.gamma_logit[0] = prm.beta_logit[0] = 0x10000
+    done = C.c_int(-1)
+
+    def load(blob):
+        p = tmp_path / "ck.bin"
+        p.write_bytes(blob)
+        return L.oq_block_state_load(C.byref(d), C.byref(prm), None, C.byref(done),
+                                     str(p).encode(), None)
+    assert load(b"NOTACKPT" + _ckpt_bytes(w)[8:]) == INVALID
+    assert b"not a block checkpoint" in L.oq_last_error()
+    assert load(_ckpt_bytes(w, c_out_override=128)) == INVALID
+    assert b"shape" in L.oq_last_error()
+    assert load(_ckpt_bytes(w, bad_hash=True)) == INVALID
+    assert b"checksum" in L.oq_last_error()
+    assert load(_ckpt_bytes(w, truncate=100)) == INVALID
+    assert b"truncated" in L.oq_last_error()
+    assert L.oq_block_state_load(C.byref(d), C.byref(prm), None, C.byref(done),
+                                 str(tmp_path / "missing.bin").encode(), None) == INVALID
+    assert done.value == -1                      # nothing reported on failure

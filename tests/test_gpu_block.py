@@ -6,8 +6,11 @@ activation quantisation, per-channel or grouped weights) at sizes the oracle
 finishes in seconds.  Most token counts leave a ragged last tile (the
 gradient products then use transposed copies); the multiples of 64 take the
 direct path that reads X^, dY^T and W^ as stored.
-Bar: loss, row losses and every gradient within 2e-2 normwise relative error
-(bf16 matrix-core products); the fp32 workload within 1e-4."""
+Bars (bf16 matrix-core products): loss, row losses and every gradient within
+1e-3 normwise relative error (max |g - r| / max |r|) and 1e-2 per element
+(|g_i - r_i| / max(|r_i|, 1e-2 max |r|)); the fp32 workload within 1e-4 and
+1e-3.  The LET gradients are sums of two terms that can nearly cancel, so
+they are measured against their terms' magnitude instead of their own."""
 import numpy as np
 import pytest
 import torch
@@ -16,12 +19,13 @@ from oracle.adamw import LR_LET, LR_LWC, adamw
 from oracle.block import block_step
 from oracle.quant import lwc_fwd
 from paper_2308_13137_amd import configs, oq
-from tests.cases import dev, make_problem, normwise, small_llama
+from tests.cases import bf16_exact, dev, elemwise, make_problem, normwise, small_llama
 
 pytestmark = pytest.mark.gpu
 
-TOL_BF16 = 2e-2
-TOL_F32 = 1e-4
+TOL_BF16 = 2e-2      # normwise bar of the multi-step trajectories
+# bf16: (normwise, per element), about ten times the largest errors measured
+BARS = {True: (1e-3, 1e-2), False: (1e-4, 1e-3)}
 
 WORKLOADS = [
     configs.C1,
@@ -82,19 +86,41 @@ def test_block_step_parity(w, logit):
     P = make_problem(w, seed=3, logit=logit, bias=(w.name in ("let_noact", "c3_t256")))
     blk, loss, *_ = run_gpu(w, P)
     ref_loss, ref = oracle_step(w, P)
-    tol = TOL_BF16 if w.bf16 else TOL_F32
-    errs = {"loss": abs(loss - ref_loss) / abs(ref_loss)}
+    bar_n, bar_e = BARS[w.bf16]
+    errs = {"loss.norm": abs(loss - ref_loss) / abs(ref_loss)}
+
+    def both(name, got, want):
+        errs[f"{name}.norm"] = normwise(got, want)
+        errs[f"{name}.elem"] = elemwise(got, want, floor=1e-2)
     for l in range(len(w.linears)):
-        errs[f"dgl{l}"] = normwise(blk.d_gamma[l].cpu().numpy(), ref["d_gamma_logit"][l])
-        errs[f"dbl{l}"] = normwise(blk.d_beta[l].cpu().numpy(), ref["d_beta_logit"][l])
-        errs[f"row{l}"] = normwise(blk.row_loss[l].cpu().numpy(), ref["row_loss"][l])
+        both(f"dgl{l}", blk.d_gamma[l].cpu().numpy(), ref["d_gamma_logit"][l])
+        both(f"dbl{l}", blk.d_beta[l].cpu().numpy(), ref["d_beta_logit"][l])
+        both(f"row{l}", blk.row_loss[l].cpu().numpy(), ref["row_loss"][l])
+    S, _ = ref["fwd"]
     for k, site in enumerate(w.sites):
         if site.let:
-            errs[f"ds{k}"] = normwise(blk.d_s[k].cpu().numpy(), ref["d_s"][k])
-            errs[f"dd{k}"] = normwise(blk.d_delta[k].cpu().numpy(), ref["d_delta"][k])
-    worst = max(errs, key=errs.get)
-    print(f"  worst {worst} = {errs[worst]:.3e}", flush=True)
-    assert errs[worst] < tol, errs
+            # d_s and d_delta are each the sum of a weight/bias-path term A and
+            # an input-path term B (Eq. 3); where they nearly cancel (no
+            # activation quantisation: B ~ -A up to the weight quantisation
+            # error) the rounding of the terms is what remains, so each
+            # element is held to its terms' magnitude |A| + |B|
+            sv = np.asarray(P["s"][k], np.float64)
+            dxt, xt = S[k]["dxt"], S[k]["xt"].astype(np.float64)
+            for name, got, want, b_in in (
+                    (f"ds{k}", blk.d_s[k].cpu().numpy(), ref["d_s"][k], -np.sum(dxt * xt, axis=0) / sv),
+                    (f"dd{k}", blk.d_delta[k].cpu().numpy(), ref["d_delta"][k], -np.sum(dxt, axis=0) / sv)):
+                scale = np.abs(want - b_in) + np.abs(b_in)
+                err = np.abs(got.astype(np.float64) - want)
+                errs[f"{name}.norm"] = float(np.max(err) / np.max(scale))
+                errs[f"{name}.elem"] = float(np.max(err / np.maximum(scale, 1e-2 * np.max(scale))))
+    wn = max((k for k in errs if k.endswith(".norm")), key=errs.get)
+    we = max((k for k in errs if k.endswith(".elem")), key=errs.get)
+    print(f"  worst {wn} = {errs[wn]:.3e}, {we} = {errs[we]:.3e}", flush=True)
+    # per element the LET gradients (against their terms' magnitude) keep the
+    # 2e-2 bar of bf16 products
+    bad = {k: v for k, v in errs.items()
+           if v >= ((2 * bar_e if k[:2] in ("ds", "dd") else bar_e) if k.endswith(".elem") else bar_n)}
+    assert not bad, errs
 
 
 # 2048-wide sites over 64 tokens: a handful of output tiles and K = 2048, so
@@ -254,24 +280,151 @@ def test_calibrate_loop_follows_oracle():
         assert normwise(bl[l].cpu().numpy(), params["beta_logit"][l]) < 1e-3
 
 
-def test_iterative_schedule_freezes_one_parameter_set():
-    """The ablation's iterative training of LWC and LET alternates which set
-    learns: a calibrate call with one learning rate at zero leaves that set
-    bit for bit unchanged while the other set moves."""
+def test_iterative_schedule_follows_oracle():
+    """The ablation's iterative training of LWC and LET: epochs alternate which
+    set learns (OQ_FREEZE_LET, then OQ_FREEZE_LWC, twice).  The frozen set,
+    its AdamW m and v stay bit for bit unchanged through its frozen epoch; the
+    step losses and all parameters follow the oracle running the same
+    schedule (full gradients, AdamW on the learning set only)."""
     w = small_llama("c3_iter", hidden=256, ffn=512, T=128, w_bits=4, let=True, act_bits=4)
-    P, segs = _segments(w, 2, seed=13)
+    n_seg = 2
+    P, segs = _segments(w, n_seg, seed=13)
     Xs, Ys = _device_segments(w, segs)
     blk, W, gl, bl, s, d = _new_block(w, P)
-    let0 = [t.clone() for t in s + d if t is not None]
-    lwc0 = [t.clone() for t in gl + bl]
-    blk.opt_state.lr_let = 0.0                      # LWC phase
-    blk.calibrate(Xs, Ys, W, gl, bl, epochs=1, s=s, delta=d)
+    lwc_t = gl + bl
+    let_t = [t for t in s + d if t is not None]
+    nl = len(w.linears)
+    mv_lwc = blk._mv[:4 * nl]                         # m/v of the logits, then of s and delta
+    mv_let = blk._mv[4 * nl:]
+    schedule = [oq.FREEZE_LET, oq.FREEZE_LWC, oq.FREEZE_LET, oq.FREEZE_LWC]
+    ours = []
+    for fz in schedule:
+        frozen_t = (let_t + mv_let) if fz == oq.FREEZE_LET else (lwc_t + mv_lwc)
+        moving_t = (lwc_t if fz == oq.FREEZE_LET else let_t)
+        before = [t.clone() for t in frozen_t]
+        before_moving = [t.clone() for t in moving_t]
+        ours += blk.calibrate(Xs, Ys, W, gl, bl, epochs=1, s=s, delta=d, frozen=fz).cpu().tolist()
+        torch.cuda.synchronize()
+        assert all(torch.equal(a, b) for a, b in zip(before, frozen_t)), fz
+        assert any(not torch.equal(a, b) for a, b in zip(before_moving, moving_t)), fz
+    # the oracle on the same schedule
+    params = dict(W=P["W"], B=P["B"], gamma_logit=[g.copy() for g in P["gamma_logit"]],
+                  beta_logit=[g.copy() for g in P["beta_logit"]],
+                  s=[None if x is None else x.copy() for x in P["s"]],
+                  delta=[None if x is None else x.copy() for x in P["delta"]])
+    keys = (("gamma_logit", "d_gamma_logit", LR_LWC, oq.FREEZE_LWC),
+            ("beta_logit", "d_beta_logit", LR_LWC, oq.FREEZE_LWC),
+            ("s", "d_s", LR_LET, oq.FREEZE_LET), ("delta", "d_delta", LR_LET, oq.FREEZE_LET))
+    mom = {k: [None if a is None else (np.zeros_like(a, np.float64), np.zeros_like(a, np.float64))
+               for a in params[k]] for k, *_ in keys}
+    refs, step = [], 0
+    for fz in schedule:
+        for sg in segs:
+            step += 1
+            rl, g = block_step(w.oracle_desc(), sg["X"], sg["Y"], params)
+            refs.append(rl)
+            for key, gk, lr, bit in keys:
+                if fz == bit:
+                    continue
+                for i, a in enumerate(params[key]):
+                    if a is None:
+                        continue
+                    m, v = mom[key][i]
+                    pnew, m, v = adamw(a, g[gk][i], m, v, step, lr)
+                    mom[key][i] = (m, v)
+                    params[key][i] = pnew.astype(np.float32)
+    print("  loss gpu", ["%.4e" % x for x in ours], "oracle", ["%.4e" % x for x in refs])
+    for a, b in zip(ours, refs):
+        assert abs(a - b) / abs(b) < TOL_BF16
+    for l in range(nl):
+        assert normwise(gl[l].cpu().numpy(), params["gamma_logit"][l]) < 1e-3
+        assert normwise(bl[l].cpu().numpy(), params["beta_logit"][l]) < 1e-3
+    for k, site in enumerate(w.sites):
+        if site.let:
+            assert normwise(s[k].cpu().numpy(), params["s"][k]) < 1e-3
+            assert normwise(d[k].cpu().numpy(), params["delta"][k]) < 1e-3
+
+
+def test_frozen_lwc_without_let_skips_the_backward():
+    """With the clipping logits frozen and no LET, no parameter needs the
+    weight gradient: the step computes the loss only, and every logit, m, v
+    and gradient output stays untouched."""
+    w = small_llama("c2_frozen", hidden=256, ffn=768, T=128, w_bits=3, group=128)
+    P, segs = _segments(w, 1, seed=17)
+    Xs, Ys = _device_segments(w, segs)
+    blk, W, gl, bl, s, d = _new_block(w, P)
+    for t in blk.d_gamma + blk.d_beta:
+        t.fill_(123.0)
+    before = [t.clone() for t in gl + bl + blk._mv]
+    loss = float(blk.step(Xs[0], Ys[0], W, gl, bl, update=True, frozen=oq.FREEZE_LWC).cpu())
     torch.cuda.synchronize()
-    assert all(torch.equal(a, b) for a, b in zip(let0, [t for t in s + d if t is not None]))
-    assert any(not torch.equal(a, b) for a, b in zip(lwc0, gl + bl))
-    lwc1 = [t.clone() for t in gl + bl]
-    blk.opt_state.lr_let, blk.opt_state.lr_lwc = 1e-2, 0.0   # LET phase
-    blk.calibrate(Xs, Ys, W, gl, bl, epochs=1, s=s, delta=d)
+    assert all(torch.equal(a, b) for a, b in zip(before, gl + bl + blk._mv))
+    assert all(bool(torch.all(t == 123.0)) for t in blk.d_gamma + blk.d_beta)
+    ref_loss, _ = oracle_step(w, P)
+    assert abs(loss - ref_loss) / ref_loss < TOL_BF16
+
+
+def test_checkpoint_resume_is_bitwise(tmp_path):
+    """Algorithm 1's training of one block stopped after three steps, saved,
+    and resumed in a fresh Block (new tensors) gives bit for bit the run that
+    never stopped: losses of the later steps, logits, s, delta, AdamW m, v."""
+    w = small_llama("c3_ckpt", hidden=256, ffn=512, T=128, w_bits=4, let=True, act_bits=4)
+    P, segs = _segments(w, 3, seed=19)
+    Xs, Ys = _device_segments(w, segs)
+    a = _new_block(w, P)
+    la = a[0].calibrate(Xs, Ys, a[1], a[2], a[3], epochs=2, s=a[4], delta=a[5]).cpu().tolist()
+    b = _new_block(w, P)
+    lb = b[0].calibrate(Xs, Ys, b[1], b[2], b[3], epochs=1, s=b[4], delta=b[5]).cpu().tolist()
+    path = tmp_path / "block.ckpt"
+    b[0].save_state(path, b[1], b[2], b[3], s=b[4], delta=b[5])
+    c = _new_block(w, P)                         # fresh parameters, zero moments
+    for t in c[2] + c[3]:
+        t.fill_(0.25)
+    c[0].load_state(path, c[1], c[2], c[3], s=c[4], delta=c[5])
+    assert c[0].step_count == 3 and c[0].opt_state.step == 4
+    lc = c[0].calibrate(Xs, Ys, c[1], c[2], c[3], epochs=1, s=c[4], delta=c[5]).cpu().tolist()
     torch.cuda.synchronize()
-    assert all(torch.equal(a, b) for a, b in zip(lwc1, gl + bl))
-    assert any(not torch.equal(a, b) for a, b in zip(let0, [t for t in s + d if t is not None]))
+    assert lb + lc == la
+    ta = a[2] + a[3] + [t for t in a[4] + a[5] if t is not None] + a[0]._mv
+    tc = c[2] + c[3] + [t for t in c[4] + c[5] if t is not None] + c[0]._mv
+    for x, y in zip(ta, tc):
+        assert torch.equal(x, y)
+
+
+def test_let_absorbed_into_norm_reproduces_the_calibrated_linear():
+    """After calibration LET folds into the previous normalisation (Sec. 3.3):
+    the norm with gain g/s and bias -delta/s, feeding the exported packed
+    linear, gives the calibrated quantised linear's output on the same
+    normalised input (weight-only deployment)."""
+    rng = np.random.default_rng(23)
+    T, Cw, co, bits, group = 64, 512, 384, 4, 128
+    n_tok = rng.standard_normal((T, Cw)).astype(np.float32)
+    n_tok /= np.sqrt(np.mean(n_tok ** 2, axis=1, keepdims=True))        # RMS-normalised rows
+    gain = rng.uniform(0.5, 1.5, Cw).astype(np.float32)
+    X = (n_tok * gain).astype(np.float32)                                # the site's input
+    W = bf16_exact((rng.standard_normal((co, Cw)) * 0.02).astype(np.float32))
+    s = rng.uniform(0.5, 2.0, Cw).astype(np.float32)
+    d = (rng.standard_normal(Cw) * 0.1).astype(np.float32)
+    gl = rng.uniform(2.0, 5.0, (co, Cw // group)).astype(np.float32)
+    bl = rng.uniform(2.0, 5.0, (co, Cw // group)).astype(np.float32)
+    # the calibrated linear (oracle): Q_w(s W) applied to X~ = (X - delta)/s, plus B~
+    from oracle.let import let_bias, let_x
+    from oracle.quant import lwc_fwd as lwc_fwd_ref
+    st = lwc_fwd_ref(W, gl, bl, bits, group, s=s)
+    Y_cal = let_x(X, s, d).astype(np.float64) @ st["W_dq"].T.astype(np.float64) + \
+        let_bias(W, None, d).astype(np.float64)[None, :]
+    # deployment: absorb LET into the norm, export the linear, run the packed product
+    g2, b2 = oq.let_absorb(dev(gain), dev(s), dev(d))
+    g2h, b2h = g2.cpu().numpy(), b2.cpu().numpy()
+    np.testing.assert_allclose(g2h, gain / s, rtol=2e-7)
+    np.testing.assert_allclose(b2h, -d / s, rtol=2e-7, atol=1e-12)
+    Xdep = (n_tok * g2h + b2h).astype(np.float32)                       # the absorbed norm's output
+    blk = oq.Block(T, [(Cw, True, 16)], [(0, co, bits, group)])
+    (packed, h, z, Bt), = blk.export([dev(W, torch.bfloat16)], [dev(gl)], [dev(bl)],
+                                     s=[dev(s)], delta=[dev(d)])
+    Y_dep = oq.packed_linear(dev(Xdep, torch.bfloat16), packed, bits, group, h, z, B=Bt)
+    got = Y_dep.cpu().numpy().astype(np.float64)
+    # bf16 rounding of the deployed activations (2^-9 relative per element)
+    bound = 2.0 ** -8 * (np.abs(Xdep).astype(np.float64) @ np.abs(st["W_dq"]).T.astype(np.float64)) \
+        + 1e-5 * np.max(np.abs(Y_cal))
+    assert np.all(np.abs(got - Y_cal) <= bound), float(np.max(np.abs(got - Y_cal) / bound))
