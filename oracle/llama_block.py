@@ -44,8 +44,9 @@ functions of their inputs and parameters (the frozen-selection surrogate of
 """
 import numpy as np
 
-from .quant import act_bwd, act_fwd, bf16_round, clip_strength, lwc_bwd, lwc_fwd
-from .surrogate import _frozen_choices, _quant_frozen
+from .quant import (act_bwd, act_fwd, act_sym_bwd, act_sym_fwd, bf16_round, clip_strength, lwc_bwd,
+                    lwc_fwd)
+from .surrogate import _frozen_choices, _frozen_variant, _quant_frozen, _sym_frozen
 
 LINEARS = ("q", "k", "v", "o", "gate", "up", "down")
 SITE_OF = (0, 0, 0, 1, 2, 2, 3)          # input site of each linear
@@ -94,9 +95,17 @@ def rope(x, n_heads, d, cos, sin, inverse=False):
     return out.reshape(T, n_heads * d)
 
 
-def attention(q, k, v, H, Hkv, d, seq_len):
+def attention(q, k, v, H, Hkv, d, seq_len, bf16=False):
     """Causal softmax(q k^T / sqrt(d)) v per sample and query head; query
-    head h reads key/value head h // (H / Hkv).  Returns (out, probs)."""
+    head h reads key/value head h // (H / Hkv).  Returns (out, probs), probs
+    the exact softmax.
+
+    ``bf16``: the weights enter the product with v as bf16 matrix-core
+    operands.  Reading: a row's weights are 2^(t - M) with t the logit in
+    base 2 (s log2(e)) and M = ceil(max t) (an integral reference, so that
+    the rounded weights do not depend on how the maximum was found), each
+    rounded to bf16, and the output is divided by the sum of those rounded
+    weights (a weighted mean of v rows)."""
     T = q.shape[0]
     ns = T // seq_len
     grp = H // Hkv
@@ -111,16 +120,22 @@ def attention(q, k, v, H, Hkv, d, seq_len):
             kv = h // grp
             s = q[b, :, h, :] @ k[b, :, kv, :].T / np.sqrt(d)
             s[mask] = -np.inf
+            if bf16:
+                t = s * np.log2(np.e)
+                w = _op(np.exp2(t - np.ceil(np.max(t, axis=1, keepdims=True))), True)
+                out[b, :, h, :] = (w @ v[b, :, kv, :]) / np.sum(w, axis=1, keepdims=True)
             s = s - np.max(s, axis=1, keepdims=True)
             p = np.exp(s)
             p /= np.sum(p, axis=1, keepdims=True)
             P[b, h] = p
-            out[b, :, h, :] = p @ v[b, :, kv, :]
+            if not bf16:
+                out[b, :, h, :] = p @ v[b, :, kv, :]
     return out.reshape(T, H * d), P
 
 
-def attention_bwd(q, k, v, P, dout, H, Hkv, d, seq_len):
-    """Gradients of :func:`attention` with respect to q, k, v."""
+def attention_bwd(q, k, v, P, dout, H, Hkv, d, seq_len, bf16=False):
+    """Gradients of :func:`attention` with respect to q, k, v (from the exact
+    softmax ``P``).  ``bf16``: P enters the dV product as a bf16 operand."""
     T = q.shape[0]
     ns = T // seq_len
     grp = H // Hkv
@@ -135,7 +150,7 @@ def attention_bwd(q, k, v, P, dout, H, Hkv, d, seq_len):
         for h in range(H):
             kv = h // grp
             p = P[b, h]
-            dv[b, :, kv, :] += p.T @ do[b, :, h, :]
+            dv[b, :, kv, :] += _op(p, bf16).T @ do[b, :, h, :]
             dp = do[b, :, h, :] @ v[b, :, kv, :].T
             ds = p * (dp - np.sum(dp * p, axis=1, keepdims=True)) / np.sqrt(d)
             dq[b, :, h, :] = ds @ k[b, :, kv, :]
@@ -153,15 +168,17 @@ def silu_grad(x):
 
 
 # ---------------------------------------------------------------- quantiser wrappers
-def _act(x, bits, frozen, key, rec, ft):
+def _act(x, bits, frozen, key, rec, ft, sym=False):
     """Q_a on token rows (in ``ft``: fp32 spec or fp64; or the frozen fp64
-    surrogate)."""
+    surrogate): per-token MinMax, or symmetric absmax when ``sym``."""
     if bits >= 16:
         return np.asarray(x, np.float64)
     if frozen is not None:
+        if sym:
+            return _sym_frozen(np.asarray(x, np.float64), frozen[key])
         ones = np.ones(x.shape[0])
         return _quant_frozen(np.asarray(x, np.float64), ones, ones, frozen[key])
-    st = act_fwd(np.asarray(x, ft), bits, ft=ft)
+    st = (act_sym_fwd if sym else act_fwd)(np.asarray(x, ft), bits, ft=ft)
     rec[key] = st
     return st["X_dq"].astype(np.float64)
 
@@ -169,7 +186,8 @@ def _act(x, bits, frozen, key, rec, ft):
 def _act_bwd(g, bits, key, rec):
     if bits >= 16:
         return g
-    return act_bwd(rec[key], g)
+    st = rec[key]
+    return act_sym_bwd(st, g) if st.get("sym") else act_bwd(st, g)
 
 
 def _lwc(W, gl, bl, bits, group, s, frozen, key, rec, ft, quantise=True):
@@ -210,6 +228,7 @@ def block_forward(desc, h0, target, params, frozen=None, ft=np.float32):
     S = desc["seq_len"]
     T = h0.shape[0]
     ab = desc["act_bits"]
+    sym = bool(desc.get("act_sym", False))
     let = desc["let"]
     bf16 = desc.get("bf16", True) and frozen is None and ft == np.float32
     wq = desc.get("w_quant", True)
@@ -224,7 +243,7 @@ def block_forward(desc, h0, target, params, frozen=None, ft=np.float32):
         s = P["s"][k] if let and k < 3 else None
         dl = P["delta"][k] if let and k < 3 else None
         xt = _let_x(x, s, dl, frozen, ft)
-        xh = _act(xt, ab, frozen, f"act{k}", rec, ft)
+        xh = _act(xt, ab, frozen, f"act{k}", rec, ft, sym)
         c[f"xt{k}"] = xt
         return _op(xh, bf16)
 
@@ -254,10 +273,10 @@ def block_forward(desc, h0, target, params, frozen=None, ft=np.float32):
     sa_q = np.tile(sa.reshape(Hkv, 1, d), (1, H // Hkv, 1)).reshape(H * d)
     qt = q / sa_q[None, :]
     kt = kk * sa[None, :]
-    qh = _op(_act(qt, ab, frozen, "actq", rec, ft), bf16)
-    kh = _op(_act(kt, ab, frozen, "actk", rec, ft), bf16)
-    vh = _op(_act(v, ab, frozen, "actv", rec, ft), bf16)
-    att, probs = attention(qh, kh, vh, H, Hkv, d, S)
+    qh = _op(_act(qt, ab, frozen, "actq", rec, ft, sym), bf16)
+    kh = _op(_act(kt, ab, frozen, "actk", rec, ft, sym), bf16)
+    vh = _op(_act(v, ab, frozen, "actv", rec, ft, sym), bf16)
+    att, probs = attention(qh, kh, vh, H, Hkv, d, S, bf16)
     c.update(qt=qt, kt=kt, v=v, qh=qh, kh=kh, vh=vh, probs=probs, sa=sa, sa_q=sa_q)
     x2op = site_input(att, 1)
     c.update(x2=att, xop1=x2op)
@@ -334,11 +353,14 @@ def block_step(desc, h0, target, params, ft=np.float32):
     dh1 = dh2 + rmsnorm_bwd(c["h1"], P["g2"], c["rstd2"], dx3)
     # attention half
     datt = site_bwd(1, linear_bwd(3, dh1))
-    dqh, dkh, dvh = attention_bwd(c["qh"], c["kh"], c["vh"], c["probs"], datt, H, Hkv, d, S)
+    # dO enters the attention backward's products (dP = dO V^T, dV = P^T dO)
+    dqh, dkh, dvh = attention_bwd(c["qh"], c["kh"], c["vh"], c["probs"], _op(datt, bf16), H, Hkv,
+                                  d, S, bf16)
     dqt = _act_bwd(dqh, ab, "actq", rec)
     dkt = _act_bwd(dkh, ab, "actk", rec)
     dv = _act_bwd(dvh, ab, "actv", rec)
     sa, sa_q = c["sa"], c["sa_q"]
+    c.update(dqt=dqt, dkt=dkt)
     dsa = None
     if let:
         # Q~ = q / s_a: dQ~/ds_a = -Q~ / s_a;  K~ = k s_a: dK~/ds_a = K~ / s_a
@@ -359,7 +381,8 @@ def freeze(desc, h0, target, params):
     fp64 forward (the frozen-selection surrogate of the straight-through
     gradients)."""
     _, c = block_forward(desc, h0, target, params, ft=np.float64)
-    return {k: _frozen_choices(st) for k, st in c["rec"].items()}
+    return {k: _frozen_variant(st, None) if st.get("sym") else _frozen_choices(st)
+            for k, st in c["rec"].items()}
 
 
 def surrogate_loss(desc, h0, target, params, frozen):

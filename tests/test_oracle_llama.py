@@ -5,6 +5,9 @@ the LET equivalences of Eq. 3 and Eq. 5 through the whole block, and central
 finite differences of the frozen-choice surrogate for every trained
 parameter (clipping logits of all seven linears, s and delta of three sites,
 the [Q, K] scale s_a)."""
+import math
+import struct
+
 import numpy as np
 import pytest
 import torch
@@ -12,10 +15,11 @@ import torch
 from oracle import llama_block as lb
 
 
-def tiny_desc(act_bits=4, let=True, H=2, Hkv=1, D=16, F=24, S=6, bits=(3, 4, 4, 3, 4, 3, 4)):
+def tiny_desc(act_bits=4, let=True, H=2, Hkv=1, D=16, F=24, S=6, bits=(3, 4, 4, 3, 4, 3, 4),
+              act_sym=False):
     return dict(hidden=D, heads=H, kv_heads=Hkv, ffn=F, seq_len=S, norm_eps=1e-6,
                 rope_base=10000.0, w_bits=list(bits), w_group=[8, 8, 16, 8, 8, 16, 8],
-                act_bits=act_bits, let=let)
+                act_bits=act_bits, let=let, act_sym=act_sym)
 
 
 def tiny_params(desc, rng, T):
@@ -119,6 +123,62 @@ def test_attention_matches_library_sdpa(H, Hkv):
         np.testing.assert_allclose(a, b.grad.numpy(), rtol=1e-10, atol=1e-12)
 
 
+def _bf16_py(x):
+    """Round-to-nearest-even to bf16 through the float32 bit pattern (struct)."""
+    b = struct.unpack("<I", struct.pack("<f", x))[0]
+    b = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000
+    return struct.unpack("<f", struct.pack("<I", b))[0]
+
+
+def test_attention_bf16_weights_brute_force():
+    """The bf16 reading of the softmax weights, written out per query with
+    math/struct on a tiny case: w_j = bf16(2^(t_j - ceil(max t))), out = sum w v
+    / sum w (t = q.k log2(e) / sqrt(d), causal)."""
+    rng = np.random.default_rng(11)
+    H, Hkv, d, S = 2, 1, 4, 5
+    q = rng.standard_normal((S, H * d)) * 2
+    k = rng.standard_normal((S, Hkv * d))
+    v = rng.standard_normal((S, Hkv * d))
+    out, _ = lb.attention(q, k, v, H, Hkv, d, S, bf16=True)
+    for h in range(H):
+        for i in range(S):
+            t = [sum(q[i, h * d + e] * k[j, e] for e in range(d)) / math.sqrt(d) / math.log(2)
+                 for j in range(i + 1)]
+            M = math.ceil(max(t))
+            w = [_bf16_py(float(np.float32(2.0 ** (tj - M)))) for tj in t]
+            for e in range(d):
+                ref = sum(w[j] * v[j, e] for j in range(i + 1)) / sum(w)
+                assert abs(out[i, h * d + e] - ref) <= 1e-12 * max(1.0, abs(ref))
+
+
+def test_attention_bf16_weights_properties():
+    """A V component shared by every key passes the bf16-weighted mean
+    unchanged, and the reading stays within 2^-8 of the exact attention
+    relative to the spread of V; P enters dV rounded (within 2^-8)."""
+    rng = np.random.default_rng(12)
+    H, Hkv, d, S = 2, 2, 8, 16
+    q = rng.standard_normal((2 * S, H * d)) * 2
+    k = rng.standard_normal((2 * S, Hkv * d))
+    u = rng.standard_normal(Hkv * d) * 50
+    out_u, _ = lb.attention(q, k, np.tile(u, (2 * S, 1)), H, Hkv, d, S, bf16=True)
+    np.testing.assert_allclose(out_u, np.tile(u, (2 * S, H // Hkv)), rtol=1e-13)
+    v = rng.standard_normal((2 * S, Hkv * d)) + u
+    out_b, P = lb.attention(q, k, v, H, Hkv, d, S, bf16=True)
+    out_x, _ = lb.attention(q, k, v, H, Hkv, d, S)
+    spread = np.max(np.abs(v - v.mean(axis=0)))
+    assert np.max(np.abs(out_b - out_x)) <= 2.0 ** -8 * spread
+    do = rng.standard_normal(out_b.shape)
+    _, _, dv_b = lb.attention_bwd(q, k, v, P, do, H, Hkv, d, S, bf16=True)
+    _, _, dv_x = lb.attention_bwd(q, k, v, P, do, H, Hkv, d, S)
+    Pb = np.abs(P).transpose(0, 1, 3, 2)          # [ns, H, key, query]
+    bound = np.zeros_like(dv_x)
+    for b in range(2):
+        for h in range(H):
+            bound[b * S:(b + 1) * S, h * d:(h + 1) * d] = 2.0 ** -8 * Pb[b, h] @ np.abs(
+                do[b * S:(b + 1) * S, h * d:(h + 1) * d])
+    assert np.all(np.abs(dv_b - dv_x) <= bound + 1e-15)
+
+
 def test_fp_block_matches_a_torch_llama_block():
     """The full-precision block against the same block written with torch's
     own ops (RMSNorm by formula, RoPE by complex multiplication, the
@@ -178,7 +238,7 @@ def test_let_is_an_equivalence_through_the_whole_block():
 
 # ---------------------------------------------------------------- finite differences
 FD_CASES = [dict(act_bits=4, let=True), dict(act_bits=16, let=True), dict(act_bits=16, let=False),
-            dict(act_bits=3, let=True, H=4, Hkv=2)]
+            dict(act_bits=3, let=True, H=4, Hkv=2), dict(act_bits=4, let=True, act_sym=True)]
 
 
 @pytest.mark.parametrize("case", FD_CASES, ids=[str(c) for c in FD_CASES])
