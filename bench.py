@@ -141,6 +141,56 @@ def summarize_traffic(fetch_dir, write_dir, workload, cmd_fetch, cmd_write, kind
     print("\n".join(lines))
 
 
+def summarize_trace(db_path, steps, title, cmd):
+    """Markdown summary of a rocprofv3 kernel trace (its rocpd database),
+    restricted to the timed steps: every step launches the same kernel
+    sequence, so the step's length is the period of the sequence at the end of
+    the trace, and the last ``steps`` periods are the timed steps."""
+    import sqlite3
+    con = sqlite3.connect(db_path)
+    rows = con.execute("select name, start, end from kernels order by start").fetchall()
+    period, drop = None, 0
+    # trailing dispatches after the steps (the runtime's copy of the loss to
+    # the host) are not part of the period
+    for drop in range(0, 16):
+        names = [r[0] for r in rows[:len(rows) - drop]]
+        for L in range(1, len(names) // (steps + 1) + 1):
+            if all(names[-i] == names[-i - L] for i in range(1, (steps - 1) * L + 1)):
+                period = L
+                break
+        if period:
+            break
+    if period is None:
+        raise SystemExit("no repeating step found at the end of the trace")
+    end = len(rows) - drop
+    timed = rows[end - steps * period:end]
+    agg = {}
+    for name, t0, t1 in timed:
+        a = agg.setdefault(name, [0, 0.0, float("inf"), 0.0])
+        d = (t1 - t0) / 1e6
+        a[0] += 1
+        a[1] += d
+        a[2] = min(a[2], d)
+        a[3] = max(a[3], d)
+    total = sum(a[1] for a in agg.values())
+    span = (timed[-1][2] - timed[0][1]) / 1e6
+    out = [f"# rocprofv3 kernel trace: {title}", "",
+           f"Command: `{cmd}`", "",
+           f"Table: the last {steps} steps of that run ({period} dispatches per step, "
+           f"{steps * period} dispatches), grouped by kernel; warmup, input setup and "
+           f"{drop} trailing dispatch(es) after the steps excluded.  "
+           f"Kernel time per step {total / steps:.3f} ms; first-dispatch-start to "
+           f"last-dispatch-end per step {span / steps:.3f} ms.", "",
+           "| kernel | calls/step | ms/step | avg ms | min ms | max ms | % |",
+           "|---|---|---|---|---|---|---|"]
+    for name, (n, tot, mn, mx) in sorted(agg.items(), key=lambda kv: -kv[1][1]):
+        short = name.replace("oq::(anonymous namespace)::", "").replace("unsigned short", "u16")
+        short = short.split("(")[0] if "(" in short else short
+        out.append(f"| {short[:110]} | {n / steps:g} | {tot / steps:.4f} | {tot / n:.4f} | "
+                   f"{mn:.4f} | {mx:.4f} | {100 * tot / total:.1f} |")
+    print("\n".join(out))
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -178,10 +228,30 @@ def make_inputs(w, device="cuda"):
     return X, W, Y, gl, bl, s, d
 
 
-def cpu_baseline(w, tokens):
-    """Time the oracle's step on the same block at ``tokens`` tokens."""
-    import numpy as np
+def cpu_facts():
+    """The host the CPU baseline ran on, and the threads it used: the fp64
+    products run on BLAS threads, the oracle's elementwise numpy on one."""
     from threadpoolctl import threadpool_info
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"cores": threads, "cores_note": "BLAS threads of the fp64 products; the "
+            "oracle's elementwise code runs on one core", "nproc": os.cpu_count(),
+            "affinity": len(os.sched_getaffinity(0)), "cpu_model": model}
+
+
+def cpu_baseline(w, tokens):
+    """Time the oracle's step on the same block at ``tokens`` tokens, then on
+    an eighth of them with one BLAS thread (the one-core figure)."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
 
     from oracle.block import block_step, fp_target
     from oracle.let import let_init
@@ -205,11 +275,20 @@ def cpu_baseline(w, tokens):
     t0 = time.perf_counter()
     block_step(ws.oracle_desc(), X, Y, params)
     dt = time.perf_counter() - t0
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": round(tokens / dt, 3), "unit": "calibration tokens/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"one full {w.name} block step (all {len(w.linears)} linears, LWC fwd/bwd on "
-                      f"every weight, fp64 products) at {tokens} tokens, {dt:.1f} s"}
+    out = dict(cpu_facts(), value=round(tokens / dt, 3), unit="calibration tokens/s", kind="oracle",
+               sample=f"one full {w.name} block step (all {len(w.linears)} linears, LWC fwd/bwd on "
+                      f"every weight, fp64 products) at {tokens} tokens, {dt:.1f} s")
+    t1 = max(tokens // 8, 64)
+    ws1 = w.with_tokens(t1)
+    X1 = [x[:t1] for x in X]
+    Y1 = [y[:t1] for y in Y]
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        block_step(ws1.oracle_desc(), X1, Y1, params)
+        dt1 = time.perf_counter() - t0
+    out["one_core"] = {"value": round(t1 / dt1, 3), "unit": "calibration tokens/s",
+                       "sample": f"the same step at its first {t1} tokens, one thread, {dt1:.1f} s"}
+    return out
 
 
 # The deployment workload (Sec. 4.5, Table "tab:speed"): one decoded token
@@ -258,7 +337,6 @@ def decode_cpu_baseline(bits, group, model, min_seconds=10.0):
     ``min_seconds`` have passed; rows are independent, so the time per pass
     scales by 8 to the block and by the block count to the model."""
     import numpy as np
-    from threadpoolctl import threadpool_info
 
     from oracle.packed import packed_linear
     rng = np.random.default_rng(5)
@@ -274,12 +352,11 @@ def decode_cpu_baseline(bits, group, model, min_seconds=10.0):
             packed_linear(x, P, bits, group, h, z)
             dt += time.perf_counter() - t0
         passes += 1
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     blocks = DECODE_MODELS[model][0]
-    return {"value": float(f"{passes / (8 * dt * blocks):.4g}"), "unit": "decoded tokens/s",
-            "cores": threads, "kind": "oracle",
-            "sample": f"{passes} pass(es) over one eighth of the rows of one block's four stacked "
-                      f"linears, one token ({dt:.1f} s), scaled by 8 x {blocks} blocks"}
+    return dict(cpu_facts(), value=float(f"{passes / (8 * dt * blocks):.4g}"),
+                unit="decoded tokens/s", kind="oracle",
+                sample=f"{passes} pass(es) over one eighth of the rows of one block's four stacked "
+                       f"linears, one token ({dt:.1f} s), scaled by 8 x {blocks} blocks")
 
 
 def decode_name(args):
@@ -427,6 +504,183 @@ def bench_decode(args):
     print(json.dumps(line), flush=True)
 
 
+# The whole LLaMA block (Sec. 3.1 and 3.3): RMSNorm, the seven linears with
+# LWC (and LET at three sites), RoPE, causal attention with the [Q, K] scale
+# s_a and per-token Q/K/V quantisation, SiLU gating, residuals; the loss on the
+# block output.  LLaMA-7B shapes, one 2048-token calibration sample per step
+# by default (Algorithm 1's batch).
+BLOCK_MODELS = {
+    # name: (hidden, heads, kv_heads, ffn)
+    "llama7b": (4096, 32, 32, 11008),
+}
+
+
+def block_name(args):
+    g = "ch" if args.block_group == 0 else str(args.block_group)
+    name = (f"{args.block_model}_block_w{args.block_bits}a{args.block_act_bits}_g{g}"
+            f"{'_let' if args.block_let else ''}")
+    return name if args.block_tokens == args.block_seq else f"{name}_t{args.block_tokens}"
+
+
+def block_inputs(args, device="cuda"):
+    """Seeded synthetic block on the GPU: bf16 weights N(0, 0.02) with 0.1%
+    x10 outliers, bf16 inputs with 1% heavy-tailed outlier channels (RMS 1 per
+    token), norm gains U(0.8, 1.2), clipping logits 4 (sigmoid 0.982), LET at
+    its identity (s = 1, delta = 0, s_a = 1), the target the block's own
+    full-precision output."""
+    import torch
+
+    from paper_2308_13137_amd import inputs, oq
+    D, H, Hkv, F = BLOCK_MODELS[args.block_model]
+    d = D // H
+    T = args.block_tokens
+    gen = torch.Generator(device=device)
+    gen.manual_seed(inputs.SEED + 7)
+    shapes = [(H * d, D), (Hkv * d, D), (Hkv * d, D), (D, H * d), (F, D), (F, D), (D, F)]
+    W = [inputs.torch_weights(gen, a, b, 0.02, 0.001, dtype=torch.bfloat16, device=device).contiguous()
+         for a, b in shapes]
+    h0 = inputs.torch_activations(gen, T, D, dtype=torch.bfloat16, device=device).contiguous()
+    g1 = 0.8 + 0.4 * torch.rand(D, generator=gen, device=device)
+    g2 = 0.8 + 0.4 * torch.rand(D, generator=gen, device=device)
+    groups = [b if args.block_group == 0 else args.block_group for _, b in shapes]
+    gl = [torch.full((a, b // g), 4.0, device=device) for (a, b), g in zip(shapes, groups)]
+    bl = [t.clone() for t in gl]
+    let = None
+    if args.block_let:
+        sw = [D, H * d, D]
+        let = dict(s=[torch.ones(n, device=device) for n in sw],
+                   delta=[torch.zeros(n, device=device) for n in sw],
+                   s_a=torch.ones(Hkv * d, device=device))
+    blk = oq.LlamaBlock(T, args.block_seq, D, H, Hkv, F, [args.block_bits] * 7, groups,
+                        act_bits=args.block_act_bits, let=args.block_let)
+    target = blk.forward(h0, W, g1, g2, quantised=False)
+    return blk, h0, target, W, g1, g2, gl, bl, let, groups
+
+
+def block_cpu_baseline(args, groups):
+    """The oracle's whole-block step on one calibration sample of the same
+    block (all seven linears at full width, attention over the sample)."""
+    import numpy as np
+
+    from oracle import llama_block as lb
+    from paper_2308_13137_amd import inputs
+    D, H, Hkv, F = BLOCK_MODELS[args.block_model]
+    d = D // H
+    T = args.block_seq
+    rng = inputs.rng_for(79, T)
+    import torch
+
+    def bf(a):
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16).float().numpy()
+    shapes = [(H * d, D), (Hkv * d, D), (Hkv * d, D), (D, H * d), (F, D), (F, D), (D, F)]
+    W = [bf(inputs.weights(rng, a, b, 0.02, 0.001)) for a, b in shapes]
+    desc = dict(hidden=D, heads=H, kv_heads=Hkv, ffn=F, seq_len=T, norm_eps=1e-6, rope_base=10000.0,
+                w_bits=[args.block_bits] * 7, w_group=groups, act_bits=args.block_act_bits,
+                let=args.block_let)
+    gl = [np.full((a, b // g), 4.0, np.float32) for (a, b), g in zip(shapes, groups)]
+    p = dict(W=W, gamma_logit=gl, beta_logit=[g.copy() for g in gl],
+             g1=np.ones(D, np.float32), g2=np.ones(D, np.float32),
+             s=[np.ones(n, np.float32) for n in (D, H * d, D)],
+             delta=[np.zeros(n, np.float32) for n in (D, H * d, D)], s_a=np.ones(Hkv * d, np.float32))
+    h0 = bf(inputs.activations(rng, T, D))
+    target = bf(lb.fp_block(desc, h0, p))
+    t0 = time.perf_counter()
+    lb.block_step(desc, h0, target, p)
+    dt = time.perf_counter() - t0
+    return dict(cpu_facts(), value=round(T / dt, 3), unit="calibration tokens/s", kind="oracle",
+                sample=f"one whole-block step of the same block on one {T}-token sample "
+                       f"(fp64 products, fp32 quantisers), {dt:.1f} s")
+
+
+def bench_block(args):
+    import torch
+
+    from paper_2308_13137_amd import oq
+    torch.cuda.set_device(0)
+    oq.lib()
+    name = block_name(args)
+    log(f"[bench] {name}: T={args.block_tokens} in samples of {args.block_seq}")
+    blk, h0, target, W, g1, g2, gl, bl, let, groups = block_inputs(args)
+    blk.init_optimizer()
+    kw = dict(let) if let else {}
+
+    def step():
+        blk.step(h0, target, W, g1, g2, gl, bl, update=True, **kw)
+    torch.cuda.synchronize()
+    log(f"[bench] inputs resident, workspace {blk.ws_bytes / 2**30:.2f} GiB; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    oq.profile_reset()
+    oq.profile_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    oq.profile_enable(False)
+    prof = oq.profile_read()
+    loss = float(blk.loss.cpu())
+    ms = (t1 - t0) * 1e3 / args.steps
+    kernels = {}
+    for kind, (n, kms, work) in prof.items():
+        if n == 0:
+            continue
+        ent = {"launches_per_step": n / args.steps, "ms_per_step": round(kms / args.steps, 4)}
+        if kind in GEMM_KINDS or kind.startswith("attn"):
+            ent["tflops"] = round(work / (kms / 1e3) / 1e12, 1)
+        elif work > 0:
+            ent["gbs"] = round(work / (kms / 1e3) / 1e9, 1)
+        kernels[kind] = ent
+    dom = max(prof, key=lambda k: prof[k][1])
+    n, kms, work = prof[dom]
+    if dom in GEMM_KINDS or dom.startswith("attn"):
+        achieved = work / n / (kms / n / 1e3) / 1e12
+        roof = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1),
+                "peak": PEAK["mfma_bf16_tflops"], "unit": "TFLOP/s"}
+    else:
+        achieved = work / n / (kms / n / 1e3) / 1e9
+        roof = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
+                "peak": PEAK["hbm_gbs"], "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["avg_launch_ms"] = round(kms / n, 4)
+    roof["traffic"] = None
+    D, H, Hkv, F = BLOCK_MODELS[args.block_model]
+    line = {
+        "metric": "calibration tokens/s per whole-block fwd+bwd step",
+        "value": round(args.block_tokens / (ms / 1e3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": name, "tokens_per_step": args.block_tokens,
+                   "seq_len": args.block_seq, "hidden": D, "heads": H, "kv_heads": Hkv, "ffn": F,
+                   "w_bits": args.block_bits, "group": args.block_group or "per-channel",
+                   "act_bits": args.block_act_bits, "let": args.block_let,
+                   "parallelism": "single GPU"},
+        "loss": loss,
+        "block_seconds_at_20_epochs_128_samples": round(20 * 128 * args.block_seq / args.block_tokens
+                                                       * ms / 1e3, 2),
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    del blk, h0, target, W, gl, bl
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log("[bench] CPU oracle on one sample of the block")
+        line["cpu_baseline"] = block_cpu_baseline(args, groups)
+    else:
+        line["cpu_baseline"] = None
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -455,7 +709,24 @@ def main():
     ap.add_argument("--decode-bits", type=int, default=4)
     ap.add_argument("--decode-group", type=int, default=128)
     ap.add_argument("--decode-tokens", type=int, default=1)
+    ap.add_argument("--block", action="store_true",
+                    help="time the whole LLaMA block's step instead (attention, norms, RoPE, "
+                         "SiLU, residuals and the seven quantised linears)")
+    ap.add_argument("--block-model", default="llama7b", choices=sorted(BLOCK_MODELS))
+    ap.add_argument("--block-bits", type=int, default=4)
+    ap.add_argument("--block-group", type=int, default=0, help="0: per output channel")
+    ap.add_argument("--block-act-bits", type=int, default=4)
+    ap.add_argument("--block-let", type=int, default=1)
+    ap.add_argument("--block-seq", type=int, default=2048)
+    ap.add_argument("--block-tokens", type=int, default=2048)
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("DB", "TITLE", "CMD"),
+                    help="print the per-kernel summary of a rocprofv3 trace over the last "
+                         "--steps steps")
     args = ap.parse_args()
+    args.block_let = bool(args.block_let)
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace[0], args.steps, *args.summarize_trace[1:])
+        return
     if args.summarize_traffic:
         if args.decode:
             summarize_traffic(*args.summarize_traffic[:2], decode_name(args),
@@ -466,6 +737,9 @@ def main():
         return
     if args.decode and args.gpus == 1:
         bench_decode(args)
+        return
+    if args.block and args.gpus == 1:
+        bench_block(args)
         return
 
     if args.gpus != 1:

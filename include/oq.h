@@ -487,14 +487,118 @@ oq_status oq_packed_linear(const void* X, oq_dtype x_dt, int64_t n_tok, int64_t 
                            oq_dtype y_dt, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * Causal multi-head attention of the block (Sec. 3.3, Eq. 5: the attention
+ * operation on the quantised Q^, K^, V^), on bf16 matrix cores.
+ *   Q [T, H d], K, V [T, Hkv d] bf16 device, token-major, heads side by side;
+ *   T = n_seq * S tokens, sample after sample; query head h reads key/value
+ *   head h / (H / Hkv).  O [T, H d] fp32 = softmax(Q K^T / sqrt(d) + causal
+ *   mask) V per sample and head.  LSE [H, T] fp32: per query the log-sum-exp
+ *   of its logits in base 2 of t = q.k log2(e)/sqrt(d) (kept for the backward).
+ * The probabilities enter the product with V as bf16 weights 2^(t - ceil(max t))
+ * and O is divided by the sum of those rounded weights (an exact weighted mean
+ * of V rows).
+ * Backward: dO [T, H d] bf16 -> dQ [T, H d], dK, dV [T, Hkv d] fp32 (dK and dV
+ * summed over the query heads of each group), from the probabilities
+ * recomputed with LSE; D = sum_j P_ij dP_ij is formed from those same
+ * probabilities; P enters the dV product as bf16, dS the dQ and dK products
+ * as a pair of bf16 terms (hi + lo); deterministic (no atomics).  Workspace:
+ * [H, T] fp32 (D).
+ * Supported: d in {64, 128}, S a multiple of 64, T a multiple of S.
+ */
+oq_status oq_attention_fwd(const void* Q, const void* K, const void* V, int64_t T, int64_t S,
+                           int H, int Hkv, int head_dim, float* O, float* LSE, hipStream_t stream);
+oq_status oq_attention_bwd_workspace_size(int64_t T, int H, size_t* bytes);
+oq_status oq_attention_bwd(const void* Q, const void* K, const void* V, const void* dO,
+                           const float* LSE, int64_t T, int64_t S, int H, int Hkv, int head_dim,
+                           float* dQ, float* dK, float* dV, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * One calibration step over a whole LLaMA transformer block (Eq. 1 with F
+ * the block itself; Algorithm 1's inner-loop body):
+ *   x1 = RMSNorm(h0) g1;  q, k, v = Q_w(W~) Q_a((x1 - delta1)/s1) + B~
+ *   q, k <- RoPE (pairs (i, i + d/2) of each head, position = token mod S)
+ *   Q~ = q / s_a, K~ = k * s_a (Eq. 5, after RoPE; s_a per key-head channel,
+ *   shared by the query heads of its group); Q^, K^, V^ = Q_a(Q~, K~, v)
+ *   o = causal softmax(Q^ K^T / sqrt(d)) V^ per sample and head
+ *   h1 = h0 + Q_w(W_o~) Q_a((o - delta2)/s2) + B~_o
+ *   x3 = RMSNorm(h1) g2; x4 = SiLU(gate) * up with gate, up from site 3
+ *   h2 = h1 + Q_w(W_d) Q_a(x4);  loss = mean over T x D of (h2 - target)^2
+ * with the straight-through backward to every clipping logit, s, delta and
+ * s_a, and an optional AdamW update.  Activations bf16 at every matrix-core
+ * operand, fp32 residual stream and accumulation.
+ *   h0, target : bf16 [T, D] device (the block's quantised-model input X_q and
+ *                its full-precision output X_fp, Algorithm 1)
+ * Supported: head_dim D/H in {64, 128}; S a multiple of 64; T a multiple of
+ * S; H a multiple of Hkv; every linear's c_in a multiple of 64; bits 2..8,
+ * groups as oq_lwc_fakequant_fwd.  Workspace: oq_llama_workspace_size.
+ */
+#define OQ_LLAMA_LINEARS 7   /* q, k, v, o, gate, up, down */
+typedef struct {
+  int64_t tokens, seq_len;            /* T = n_seq * seq_len                       */
+  int64_t hidden, ffn;                /* D, F                                      */
+  int heads, kv_heads;                /* H, Hkv                                    */
+  float norm_eps, rope_base;          /* RMSNorm epsilon, RoPE base (10000)        */
+  int w_bits[OQ_LLAMA_LINEARS];
+  int64_t w_group[OQ_LLAMA_LINEARS];  /* group along c_in (c_in = per channel)     */
+  int act_bits;                       /* 2..8 (| OQ_ACT_SYM): Q_a on the four linear
+                                         inputs and on Q~, K~, V; 16 = none       */
+  int let;                            /* 1: LET on the q/k/v, o, gate/up inputs and s_a */
+} oq_llama_desc;
+
+typedef struct {                      /* device pointers                            */
+  const void* W[OQ_LLAMA_LINEARS];    /* bf16 [c_out, c_in]                         */
+  const float* norm1;                 /* RMSNorm gains [D] fp32 (frozen)            */
+  const float* norm2;
+  float* gamma_logit[OQ_LLAMA_LINEARS]; /* [c_out, c_in / group]                    */
+  float* beta_logit[OQ_LLAMA_LINEARS];
+  float* s[3];                        /* [D], [H d], [D]  (LET only)                */
+  float* delta[3];
+  float* s_a;                         /* [Hkv d]           (LET only)               */
+} oq_llama_params;
+
+typedef struct {                      /* device outputs                              */
+  float* d_gamma_logit[OQ_LLAMA_LINEARS];
+  float* d_beta_logit[OQ_LLAMA_LINEARS];
+  float* d_s[3];
+  float* d_delta[3];
+  float* d_s_a;
+} oq_llama_grads;
+
+typedef struct {                      /* AdamW state, as oq_block_optim             */
+  float* m_gamma[OQ_LLAMA_LINEARS]; float* v_gamma[OQ_LLAMA_LINEARS];
+  float* m_beta[OQ_LLAMA_LINEARS];  float* v_beta[OQ_LLAMA_LINEARS];
+  float* m_s[3]; float* v_s[3]; float* m_delta[3]; float* v_delta[3];
+  float* m_s_a; float* v_s_a;
+  int step;
+  double lr_lwc, lr_let, beta1, beta2, eps, wd;
+} oq_llama_optim;
+
+oq_status oq_llama_workspace_size(const oq_llama_desc* desc, size_t* bytes);
+oq_status oq_llama_block_step(const oq_llama_desc* desc, const void* h0, const void* target,
+                              const oq_llama_params* params, const oq_llama_grads* grads,
+                              const oq_llama_optim* optim, float* loss, void* ws,
+                              size_t ws_bytes, hipStream_t stream);
+
+/* The block's forward alone, for Algorithm 1's propagation from block to
+ * block: quantised = 0 gives the full-precision block (W as given, no LET,
+ * no quantiser: X_fp <- B(X_fp)); quantised = 1 the quantised block with the
+ * learned parameters (X_q <- B_q(X_q)).  h_out: bf16 [T, D], may not alias
+ * h0.  Same workspace as the step. */
+oq_status oq_llama_block_forward(const oq_llama_desc* desc, const void* h0,
+                                 const oq_llama_params* params, int quantised, void* h_out,
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Kernel timing on the launching stream (HIP events around each launch).
  * Kinds: 0 forward GEMM, 1 weight-gradient GEMM, 2 input-gradient GEMM,
  * 3 LWC forward, 4 LWC backward, 5 activation quant forward, 6 activation
- * quant backward, 7 transposes, 8 other, 9 the packed linear.  oq_profile_read synchronises the
+ * quant backward, 7 transposes, 8 other, 9 the packed linear, 10 attention
+ * forward, 11 attention backward.  oq_profile_read synchronises the
  * recorded events and returns launch count, total milliseconds and the
  * algorithmic work (FLOP for GEMMs, bytes for the others) of that kind.
  */
-#define OQ_PROF_KINDS 10
+#define OQ_PROF_KINDS 12
 oq_status oq_profile_enable(int on);
 oq_status oq_profile_reset(void);
 oq_status oq_profile_read(int kind, int64_t* launches, double* total_ms, double* work);

@@ -17,7 +17,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "liboq.so")
-SOURCES = ["gemm.hip", "quant.hip", "misc.hip", "packed.hip", "api.hip"]
+SOURCES = ["gemm.hip", "quant.hip", "misc.hip", "packed.hip", "attention.hip", "block_ops.hip",
+           "api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

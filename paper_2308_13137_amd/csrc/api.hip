@@ -1512,3 +1512,527 @@ oq_status oq_block_calibrate(const oq_block_desc* d, int n_segments, int epochs,
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------------------ whole LLaMA block
+namespace {
+
+constexpr int NL = OQ_LLAMA_LINEARS;
+constexpr int L_SITE[NL] = {0, 0, 0, 1, 2, 2, 3};
+
+struct LlamaDims {
+  int64_t T, S, D, F, H, Hkv, dh, Hd, Kd, Mqkv;
+  int64_t c_out[NL], c_in[NL];
+  int ab;     // activation bits without the symmetric flag
+  bool sym, let;
+};
+
+oq_status llama_dims(const oq_llama_desc* d, LlamaDims* o) {
+  OQ_REQ(d, "desc is required");
+  LlamaDims& m = *o;
+  m.T = d->tokens;
+  m.S = d->seq_len;
+  m.D = d->hidden;
+  m.F = d->ffn;
+  m.H = d->heads;
+  m.Hkv = d->kv_heads;
+  OQ_REQ(m.T > 0 && m.S > 0 && m.D > 0 && m.F > 0 && m.H > 0 && m.Hkv > 0, "bad shape");
+  OQ_REQ(m.D % m.H == 0, "hidden %lld not a multiple of heads %lld", (long long)m.D, (long long)m.H);
+  m.dh = m.D / m.H;
+  m.Hd = m.H * m.dh;
+  m.Kd = m.Hkv * m.dh;
+  m.Mqkv = m.Hd + 2 * m.Kd;
+  if (!attn_supported(m.T, int(m.S), int(m.H), int(m.Hkv), int(m.dh)))
+    return fail(OQ_ERR_UNSUPPORTED,
+                "attention: head_dim %lld (need 64 or 128), S %lld (multiple of 64), T %lld "
+                "(multiple of S), H %lld / Hkv %lld",
+                (long long)m.dh, (long long)m.S, (long long)m.T, (long long)m.H, (long long)m.Hkv);
+  if (m.D % 64 || m.F % 64) return fail(OQ_ERR_UNSUPPORTED, "hidden and ffn must be multiples of 64");
+  m.sym = (d->act_bits & OQ_ACT_SYM) != 0;
+  m.ab = d->act_bits & ~OQ_ACT_SYM;
+  if (!(m.ab == 16 || (m.ab >= 2 && m.ab <= 8)) || (m.sym && m.ab == 16))
+    return fail(OQ_ERR_UNSUPPORTED, "activation bits %d", d->act_bits);
+  m.let = d->let != 0;
+  const int64_t co[NL] = {m.Hd, m.Kd, m.Kd, m.D, m.F, m.F, m.D};
+  const int64_t ci[NL] = {m.D, m.D, m.D, m.Hd, m.D, m.D, m.F};
+  for (int l = 0; l < NL; ++l) {
+    m.c_out[l] = co[l];
+    m.c_in[l] = ci[l];
+    if (d->w_bits[l] < 2 || d->w_bits[l] > 8)
+      return fail(OQ_ERR_UNSUPPORTED, "linear %d: bits %d", l, d->w_bits[l]);
+    if (d->w_group[l] <= 0 || ci[l] % d->w_group[l])
+      return fail(OQ_ERR_INVALID_ARG, "linear %d: group %lld does not divide %lld", l,
+                  (long long)d->w_group[l], (long long)ci[l]);
+    if (!quant_shape_supported(ci[l], d->w_group[l]))
+      return fail(OQ_ERR_UNSUPPORTED, "linear %d: group %lld for width %lld", l,
+                  (long long)d->w_group[l], (long long)ci[l]);
+  }
+  return OQ_OK;
+}
+
+struct LlamaWs {
+  float *x1, *rstd1, *qkv, *qt, *kt, *vv, *att, *lse, *o, *h1, *x3, *rstd2, *gu, *x4, *dn, *h2;
+  void *xh1, *wqkv, *qh, *kh, *vh, *xh2, *wo, *xh3, *wgu, *xh4, *wd;
+  float *dh2, *dW, *dxh, *dxt, *dh1, *Dl, *dQ, *dK, *dV, *dqt, *dkt, *dvt;
+  void *dh2_16, *dh1_16, *dgu16, *datt16, *dqkv16;
+  double* rows;
+  float *bt_qkv, *bt_o, *bt_gu;       // folded biases B~ of the LET sites
+  float *dbt, *psx, *ps1, *psxq, *psxk, *pw, *pb, *amax;
+  double* csum;
+};
+
+size_t llama_carve(const LlamaDims& m, char* base, LlamaWs* w) {
+  Carver cv{base};
+  LlamaWs t{};
+  const int64_t T = m.T, D = m.D, F = m.F;
+  const int64_t maxC = std::max(std::max(D, m.Hd), F);
+  int64_t maxWC = 0, maxM = 0;
+  for (int l = 0; l < NL; ++l) maxWC = std::max(maxWC, m.c_out[l] * m.c_in[l]);
+  maxWC = std::max(maxWC, std::max(m.Mqkv * D, 2 * F * D));
+  maxM = std::max(std::max(m.Mqkv, 2 * F), std::max(D, m.Hd));
+  t.x1 = cv.take<float>(T * D);
+  t.rstd1 = cv.take<float>(T);
+  t.xh1 = cv.take<uint16_t>(T * D);
+  t.wqkv = cv.take<uint16_t>(m.Mqkv * D);
+  t.qkv = cv.take<float>(T * m.Mqkv);
+  t.qt = cv.take<float>(T * m.Hd);
+  t.kt = cv.take<float>(T * m.Kd);
+  t.vv = cv.take<float>(T * m.Kd);
+  t.qh = cv.take<uint16_t>(T * m.Hd);
+  t.kh = cv.take<uint16_t>(T * m.Kd);
+  t.vh = cv.take<uint16_t>(T * m.Kd);
+  t.att = cv.take<float>(T * m.Hd);
+  t.lse = cv.take<float>(m.H * T);
+  t.xh2 = cv.take<uint16_t>(T * m.Hd);
+  t.wo = cv.take<uint16_t>(D * m.Hd);
+  t.o = cv.take<float>(T * D);
+  t.h1 = cv.take<float>(T * D);
+  t.x3 = cv.take<float>(T * D);
+  t.rstd2 = cv.take<float>(T);
+  t.xh3 = cv.take<uint16_t>(T * D);
+  t.wgu = cv.take<uint16_t>(2 * F * D);
+  t.gu = cv.take<float>(T * 2 * F);
+  t.x4 = cv.take<float>(T * F);
+  t.xh4 = cv.take<uint16_t>(T * F);
+  t.wd = cv.take<uint16_t>(D * F);
+  t.dn = cv.take<float>(T * D);
+  t.h2 = cv.take<float>(T * D);
+  t.dh2 = cv.take<float>(T * D);
+  t.dh2_16 = cv.take<uint16_t>(T * D);
+  t.rows = cv.take<double>(T);
+  t.bt_qkv = cv.take<float>(m.Mqkv);
+  t.bt_o = cv.take<float>(D);
+  t.bt_gu = cv.take<float>(2 * F);
+  t.dW = cv.take<float>(maxWC);
+  t.dxh = cv.take<float>(T * maxC);
+  t.dxt = cv.take<float>(T * maxC);
+  t.dh1 = cv.take<float>(T * D);
+  t.dh1_16 = cv.take<uint16_t>(T * D);
+  t.dgu16 = cv.take<uint16_t>(T * 2 * F);
+  t.datt16 = cv.take<uint16_t>(T * m.Hd);
+  t.Dl = cv.take<float>(m.H * T);
+  t.dQ = cv.take<float>(T * m.Hd);
+  t.dK = cv.take<float>(T * m.Kd);
+  t.dV = cv.take<float>(T * m.Kd);
+  t.dqt = cv.take<float>(T * m.Hd);
+  t.dkt = cv.take<float>(T * m.Kd);
+  t.dvt = cv.take<float>(T * m.Kd);
+  t.dqkv16 = cv.take<uint16_t>(T * m.Mqkv);
+  const int64_t npa = act_bwd_nparts(T);
+  t.psx = cv.take<float>(npa * maxC);
+  t.ps1 = cv.take<float>(npa * maxC);
+  t.psxq = cv.take<float>(npa * m.Hd);
+  t.psxk = cv.take<float>(npa * m.Kd);
+  int64_t npw = 0, npb = 0;
+  for (int l = 0; l < NL; ++l) {
+    npw = std::max(npw, lwc_bwd_nparts(m.c_out[l]));
+    npb = std::max(npb, wcolsum_nparts(m.c_out[l]));
+  }
+  t.pw = cv.take<float>(3 * npw * maxC);        // up to three linears per site
+  t.pb = cv.take<float>(3 * npb * maxC);
+  t.dbt = cv.take<float>(maxM);
+  const int64_t nc = colstat_nparts(T);
+  t.amax = cv.take<float>(nc * maxM);
+  t.csum = cv.take<double>(nc * maxM);
+  if (w) *w = t;
+  return cv.off + 256;
+}
+
+}  // namespace
+
+extern "C" {
+
+oq_status oq_llama_workspace_size(const oq_llama_desc* d, size_t* bytes) {
+  OQ_REQ(bytes, "bytes is required");
+  LlamaDims m;
+  oq_status e = llama_dims(d, &m);
+  if (e != OQ_OK) return e;
+  *bytes = llama_carve(m, nullptr, nullptr);
+  return OQ_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// The quantised (or full-precision) forward of the block into the workspace,
+// up to h2.  Returns the LWC'd weights and the site tensors the backward reads.
+oq_status llama_forward(const LlamaDims& m, const oq_llama_desc* d, const void* h0,
+                        const oq_llama_params* p, bool quant, const LlamaWs& w, hipStream_t st) {
+  const int64_t T = m.T, D = m.D, F = m.F;
+  const bool let = quant && m.let;
+  const int ab = quant ? m.ab : 16;
+  const bool sym = quant && m.sym;
+  const float* s1 = let ? p->s[0] : nullptr;
+  const float* d1 = let ? p->delta[0] : nullptr;
+  // LWC'd weights of the linears stacked per site (or the plain weights)
+  auto weights = [&](int l0, int l1, void* dst) -> oq_status {
+    int64_t off = 0;
+    for (int l = l0; l < l1; ++l) {
+      const int k = L_SITE[l];
+      const float* s = let && k < 3 ? p->s[k] : nullptr;
+      char* out = static_cast<char*>(dst) + off * m.c_in[l] * 2;
+      if (quant) {
+        ProfScope ps(PK_LWC_FWD, st, double(m.c_out[l]) * m.c_in[l] * 4);
+        OQ_HIP(lwc_fwd(p->W[l], true, m.c_out[l], m.c_in[l], s, p->gamma_logit[l], p->beta_logit[l],
+                       d->w_bits[l], d->w_group[l], out, true, nullptr, nullptr, nullptr, st),
+               "lwc_fwd");
+      } else {
+        OQ_HIP(hipMemcpyAsync(out, p->W[l], size_t(m.c_out[l] * m.c_in[l]) * 2,
+                              hipMemcpyDeviceToDevice, st),
+               "weight copy");
+      }
+      off += m.c_out[l];
+    }
+    return OQ_OK;
+  };
+  auto biases = [&](int l0, int l1, float* bt) -> oq_status {
+    int64_t off = 0;
+    for (int l = l0; l < l1; ++l) {
+      const int k = L_SITE[l];
+      OQ_HIP(let_fold(p->W[l], true, nullptr, m.c_out[l], m.c_in[l], nullptr, p->delta[k], nullptr,
+                      false, bt + off, st),
+             "let_fold");
+      off += m.c_out[l];
+    }
+    return OQ_OK;
+  };
+  auto product = [&](const void* x, const void* wt, int64_t M, int64_t K, float* out) -> oq_status {
+    ProfScope ps(PK_GEMM_FWD, st, 2.0 * double(T) * M * K);
+    OQ_HIP(gemm_f32out_mn(x, false, wt, false, T, M, K, K, K, out, M, st), "forward product");
+    return OQ_OK;
+  };
+  oq_status e;
+  // ---- attention half
+  OQ_HIP(rmsnorm_fwd(h0, true, p->norm1, T, D, d->norm_eps, w.x1, w.rstd1, st), "rmsnorm");
+  {
+    ProfScope ps(PK_ACT_FWD, st, double(T) * D * 6);
+    OQ_HIP(act_fwd(w.x1, false, T, D, ab, s1, d1, w.xh1, true, nullptr, nullptr, nullptr, st, sym),
+           "act_fwd site 1");
+  }
+  if ((e = weights(0, 3, w.wqkv)) != OQ_OK) return e;
+  if (let && (e = biases(0, 3, w.bt_qkv)) != OQ_OK) return e;
+  if ((e = product(w.xh1, w.wqkv, m.Mqkv, D, w.qkv)) != OQ_OK) return e;
+  OQ_HIP(qkv_post(w.qkv, let ? w.bt_qkv : nullptr, T, int(m.S), int(m.H), int(m.Hkv), int(m.dh),
+                  d->rope_base, let ? p->s_a : nullptr, w.qt, w.kt, w.vv, st),
+         "qkv epilogue");
+  {
+    ProfScope ps(PK_ACT_FWD, st, double(T) * m.Mqkv * 6);
+    OQ_HIP(act_fwd(w.qt, false, T, m.Hd, ab, nullptr, nullptr, w.qh, true, nullptr, nullptr, nullptr,
+                   st, sym),
+           "act_fwd Q");
+    OQ_HIP(act_fwd(w.kt, false, T, m.Kd, ab, nullptr, nullptr, w.kh, true, nullptr, nullptr, nullptr,
+                   st, sym),
+           "act_fwd K");
+    OQ_HIP(act_fwd(w.vv, false, T, m.Kd, ab, nullptr, nullptr, w.vh, true, nullptr, nullptr, nullptr,
+                   st, sym),
+           "act_fwd V");
+  }
+  {
+    ProfScope ps(PK_ATTN_FWD, st, 2.0 * double(T) * m.S * m.Hd);   // causal: QK^T and PV, half each
+    OQ_HIP(attn_fwd(w.qh, w.kh, w.vh, T, int(m.S), int(m.H), int(m.Hkv), int(m.dh), w.att, w.lse, st),
+           "attention");
+  }
+  {
+    ProfScope ps(PK_ACT_FWD, st, double(T) * m.Hd * 6);
+    OQ_HIP(act_fwd(w.att, false, T, m.Hd, ab, let ? p->s[1] : nullptr, let ? p->delta[1] : nullptr,
+                   w.xh2, true, nullptr, nullptr, nullptr, st, sym),
+           "act_fwd site 2");
+  }
+  if ((e = weights(3, 4, w.wo)) != OQ_OK) return e;
+  if (let && (e = biases(3, 4, w.bt_o)) != OQ_OK) return e;
+  if ((e = product(w.xh2, w.wo, D, m.Hd, w.o)) != OQ_OK) return e;
+  OQ_HIP(resid_add(h0, true, w.o, let ? w.bt_o : nullptr, T, D, w.h1, st), "residual 1");
+  // ---- feed-forward half
+  OQ_HIP(rmsnorm_fwd(w.h1, false, p->norm2, T, D, d->norm_eps, w.x3, w.rstd2, st), "rmsnorm 2");
+  {
+    ProfScope ps(PK_ACT_FWD, st, double(T) * D * 6);
+    OQ_HIP(act_fwd(w.x3, false, T, D, ab, let ? p->s[2] : nullptr, let ? p->delta[2] : nullptr,
+                   w.xh3, true, nullptr, nullptr, nullptr, st, sym),
+           "act_fwd site 3");
+  }
+  if ((e = weights(4, 6, w.wgu)) != OQ_OK) return e;
+  if (let && (e = biases(4, 6, w.bt_gu)) != OQ_OK) return e;
+  if ((e = product(w.xh3, w.wgu, 2 * F, D, w.gu)) != OQ_OK) return e;
+  OQ_HIP(silu_mul(w.gu, let ? w.bt_gu : nullptr, T, F, w.x4, st), "silu");
+  {
+    ProfScope ps(PK_ACT_FWD, st, double(T) * F * 6);
+    OQ_HIP(act_fwd(w.x4, false, T, F, ab, nullptr, nullptr, w.xh4, true, nullptr, nullptr, nullptr,
+                   st, sym),
+           "act_fwd site 4");
+  }
+  if ((e = weights(6, 7, w.wd)) != OQ_OK) return e;
+  if ((e = product(w.xh4, w.wd, D, F, w.dn)) != OQ_OK) return e;
+  OQ_HIP(resid_add(w.h1, false, w.dn, nullptr, T, D, w.h2, st), "residual 2");
+  return OQ_OK;
+}
+
+oq_status llama_check(const LlamaDims& m, const oq_llama_params* p, bool quant) {
+  OQ_REQ(p, "params are required");
+  for (int l = 0; l < NL; ++l) {
+    OQ_REQ(p->W[l] && aligned16(p->W[l]), "W[%d] missing or misaligned", l);
+    if (quant) OQ_REQ(p->gamma_logit[l] && p->beta_logit[l], "logits of linear %d missing", l);
+  }
+  OQ_REQ(p->norm1 && p->norm2, "norm gains are required");
+  if (quant && m.let) {
+    for (int k = 0; k < 3; ++k)
+      OQ_REQ(p->s[k] && p->delta[k] && aligned16(p->s[k]) && aligned16(p->delta[k]),
+             "LET site %d: s and delta (16-byte aligned) are required", k);
+    OQ_REQ(p->s_a, "s_a is required with LET");
+  }
+  return OQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+oq_status oq_attention_fwd(const void* Q, const void* K, const void* V, int64_t T, int64_t S,
+                           int H, int Hkv, int head_dim, float* O, float* LSE, hipStream_t st) {
+  OQ_REQ(Q && K && V && O && LSE, "Q, K, V, O and LSE are required");
+  OQ_REQ(aligned16(Q) && aligned16(K) && aligned16(V) && aligned16(O), "pointers must be 16-byte aligned");
+  if (!attn_supported(T, int(S), H, Hkv, head_dim) || S > INT32_MAX)
+    return fail(OQ_ERR_UNSUPPORTED, "attention shape T=%lld S=%lld H=%d Hkv=%d d=%d", (long long)T,
+                (long long)S, H, Hkv, head_dim);
+  ProfScope ps(PK_ATTN_FWD, st, 2.0 * double(T) * S * H * head_dim);
+  OQ_HIP(attn_fwd(Q, K, V, T, int(S), H, Hkv, head_dim, O, LSE, st), "attention");
+  return OQ_OK;
+}
+
+oq_status oq_attention_bwd_workspace_size(int64_t T, int H, size_t* bytes) {
+  OQ_REQ(bytes && T >= 0 && H > 0, "bad arguments");
+  *bytes = size_t(T) * size_t(H) * 4 + 256;
+  return OQ_OK;
+}
+
+oq_status oq_attention_bwd(const void* Q, const void* K, const void* V, const void* dO,
+                           const float* LSE, int64_t T, int64_t S, int H, int Hkv, int head_dim,
+                           float* dQ, float* dK, float* dV, void* ws, size_t ws_bytes,
+                           hipStream_t st) {
+  OQ_REQ(Q && K && V && dO && LSE && dQ && dK && dV, "every tensor is required");
+  OQ_REQ(aligned16(Q) && aligned16(K) && aligned16(V) && aligned16(dO),
+         "pointers must be 16-byte aligned");
+  if (!attn_supported(T, int(S), H, Hkv, head_dim) || S > INT32_MAX)
+    return fail(OQ_ERR_UNSUPPORTED, "attention shape T=%lld S=%lld H=%d Hkv=%d d=%d", (long long)T,
+                (long long)S, H, Hkv, head_dim);
+  size_t need = 0;
+  oq_attention_bwd_workspace_size(T, H, &need);
+  if (!ws || ws_bytes < need) return fail(OQ_ERR_WORKSPACE, "workspace of %zu bytes needed", need);
+  ProfScope ps(PK_ATTN_BWD, st, 4.0 * double(T) * S * H * head_dim);   // dV, dP, dQ, dK (causal halves)
+  OQ_HIP(attn_bwd(Q, K, V, dO, LSE, T, int(S), H, Hkv, head_dim, static_cast<float*>(ws), dQ, dK, dV,
+                  st),
+         "attention backward");
+  return OQ_OK;
+}
+
+oq_status oq_llama_block_forward(const oq_llama_desc* d, const void* h0,
+                                 const oq_llama_params* p, int quantised, void* h_out, void* ws,
+                                 size_t ws_bytes, hipStream_t st) {
+  LlamaDims m;
+  oq_status e = llama_dims(d, &m);
+  if (e != OQ_OK) return e;
+  if ((e = llama_check(m, p, quantised != 0)) != OQ_OK) return e;
+  OQ_REQ(h0 && h_out && aligned16(h0) && aligned16(h_out) && h0 != h_out, "h0, h_out");
+  const size_t need = llama_carve(m, nullptr, nullptr);
+  if (!ws || ws_bytes < need)
+    return fail(OQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  LlamaWs w;
+  llama_carve(m, static_cast<char*>(ws), &w);
+  if ((e = llama_forward(m, d, h0, p, quantised != 0, w, st)) != OQ_OK) return e;
+  OQ_HIP(scale_to_bf16(w.h2, nullptr, m.T, m.D, h_out, st), "output");
+  return OQ_OK;
+}
+
+oq_status oq_llama_block_step(const oq_llama_desc* d, const void* h0, const void* target,
+                              const oq_llama_params* p, const oq_llama_grads* g,
+                              const oq_llama_optim* opt, float* loss, void* ws, size_t ws_bytes,
+                              hipStream_t st) {
+  LlamaDims m;
+  oq_status e = llama_dims(d, &m);
+  if (e != OQ_OK) return e;
+  if ((e = llama_check(m, p, true)) != OQ_OK) return e;
+  OQ_REQ(h0 && target && aligned16(h0) && aligned16(target) && loss && g,
+         "h0, target, grads and loss are required");
+  for (int l = 0; l < NL; ++l)
+    OQ_REQ(g->d_gamma_logit[l] && g->d_beta_logit[l], "gradients of linear %d missing", l);
+  if (m.let) {
+    for (int k = 0; k < 3; ++k) OQ_REQ(g->d_s[k] && g->d_delta[k], "LET gradients of site %d", k);
+    OQ_REQ(g->d_s_a, "d_s_a is required with LET");
+  }
+  if (opt) {
+    OQ_REQ(opt->step >= 1, "optim step must be >= 1");
+    for (int l = 0; l < NL; ++l)
+      OQ_REQ(opt->m_gamma[l] && opt->v_gamma[l] && opt->m_beta[l] && opt->v_beta[l],
+             "AdamW state of linear %d missing", l);
+    if (m.let) {
+      for (int k = 0; k < 3; ++k)
+        OQ_REQ(opt->m_s[k] && opt->v_s[k] && opt->m_delta[k] && opt->v_delta[k],
+               "AdamW state of site %d missing", k);
+      OQ_REQ(opt->m_s_a && opt->v_s_a, "AdamW state of s_a missing");
+    }
+  }
+  const size_t need = llama_carve(m, nullptr, nullptr);
+  if (!ws || ws_bytes < need)
+    return fail(OQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws_bytes);
+  LlamaWs w;
+  llama_carve(m, static_cast<char*>(ws), &w);
+  const int64_t T = m.T, D = m.D, F = m.F;
+  const bool let = m.let;
+  const int ab = m.ab;
+  const bool sym = m.sym;
+  if ((e = llama_forward(m, d, h0, p, true, w, st)) != OQ_OK) return e;
+  {
+    ProfScope ps(PK_OTHER, st, double(T) * D * 12);
+    OQ_HIP(block_loss(w.h2, target, T, D, w.dh2, w.dh2_16, w.rows, loss, st), "loss");
+  }
+  const int64_t npa = act_bwd_nparts(T);
+  // dX^ = dY W^ and dW^ = dY^T X^ of the linears [l0, l1) stacked on one
+  // site, then their LWC backward (with LET: the weight-path ds partials and
+  // the bias-path partials of ddelta); dy16 bf16 [T, M], xh bf16 [T, C].
+  int64_t npw = 0, npb = 0;
+  auto linears_bwd = [&](int l0, int l1, const void* dy16, const void* wst, const void* xh,
+                         float* dxh) -> oq_status {
+    const int k = L_SITE[l0];
+    const int64_t C = m.c_in[l0];
+    int64_t M = 0;
+    for (int l = l0; l < l1; ++l) M += m.c_out[l];
+    const bool let_site = let && k < 3;
+    {
+      ProfScope ps(PK_GEMM_DGRAD, st, 2.0 * double(T) * M * C);
+      OQ_HIP(gemm_f32out_mn(dy16, false, wst, true, T, C, M, M, C, dxh, C, st), "input gradient");
+    }
+    {
+      ProfScope ps(PK_GEMM_WGRAD, st, 2.0 * double(T) * M * C);
+      OQ_HIP(gemm_f32out_mn(dy16, true, xh, true, M, C, T, M, C, w.dW, C, st), "weight gradient");
+    }
+    npw = npb = 0;
+    int64_t off = 0;
+    for (int l = l0; l < l1; ++l) {
+      ProfScope ps(PK_LWC_BWD, st, double(m.c_out[l]) * C * 6);
+      OQ_HIP(lwc_bwd(p->W[l], true, m.c_out[l], C, let_site ? p->s[k] : nullptr, p->gamma_logit[l],
+                     p->beta_logit[l], d->w_bits[l], d->w_group[l], w.dW + off * C,
+                     g->d_gamma_logit[l], g->d_beta_logit[l], nullptr,
+                     let_site ? w.pw + npw * C : nullptr, st),
+             "lwc_bwd");
+      if (let_site) npw += lwc_bwd_nparts(m.c_out[l]);
+      off += m.c_out[l];
+    }
+    if (let_site) {
+      ProfScope ps(PK_OTHER, st, double(T) * M * 2 + double(M) * C * 2);
+      const int64_t nc = colstat_nparts(T);
+      OQ_HIP(colstat(dy16, true, T, M, w.amax, w.csum, st), "bias-path column sums");
+      OQ_HIP(colsum_finish(w.csum, nc, M, w.dbt, st), "bias-path finish");
+      off = 0;
+      for (int l = l0; l < l1; ++l) {
+        OQ_HIP(wcolsum(p->W[l], true, m.c_out[l], C, w.dbt + off, w.pb + npb * C, st), "bias path");
+        npb += wcolsum_nparts(m.c_out[l]);
+        off += m.c_out[l];
+      }
+    }
+    return OQ_OK;
+  };
+  // through Q_a and the LET transform of site k: dxt = dL/dX~ (and the LET
+  // gradients of the site)
+  auto site_bwd = [&](int k, const float* x, int64_t C, const float* dxh, float* dxt) -> oq_status {
+    const bool let_site = let && k < 3;
+    {
+      ProfScope ps(PK_ACT_BWD, st, double(T) * C * 8);
+      OQ_HIP(act_bwd(x, false, T, C, ab, let_site ? p->s[k] : nullptr,
+                     let_site ? p->delta[k] : nullptr, dxh, dxt, let_site ? w.psx : nullptr,
+                     let_site ? w.ps1 : nullptr, st, sym),
+             "act_bwd");
+    }
+    if (let_site)
+      OQ_HIP(let_grad_finish(C, p->s[k], w.pw, npw, w.psx, w.ps1, npa, w.pb, npb, g->d_s[k],
+                             g->d_delta[k], st),
+             "LET finish");
+    return OQ_OK;
+  };
+  // ---- feed-forward half
+  if ((e = linears_bwd(6, 7, w.dh2_16, w.wd, w.xh4, w.dxh)) != OQ_OK) return e;
+  if ((e = site_bwd(3, w.x4, F, w.dxh, w.dxt)) != OQ_OK) return e;
+  OQ_HIP(silu_mul_bwd(w.gu, w.dxt, T, F, w.dgu16, st), "silu backward");
+  if ((e = linears_bwd(4, 6, w.dgu16, w.wgu, w.xh3, w.dxh)) != OQ_OK) return e;
+  if ((e = site_bwd(2, w.x3, D, w.dxh, w.dxt)) != OQ_OK) return e;
+  OQ_HIP(rmsnorm_bwd(w.h1, false, p->norm2, w.rstd2, w.dxt, let ? p->s[2] : nullptr, w.dh2, T, D,
+                     w.dh1, st),
+         "rmsnorm backward");
+  OQ_HIP(scale_to_bf16(w.dh1, nullptr, T, D, w.dh1_16, st), "dh1");
+  // ---- attention half
+  if ((e = linears_bwd(3, 4, w.dh1_16, w.wo, w.xh2, w.dxh)) != OQ_OK) return e;
+  if ((e = site_bwd(1, w.att, m.Hd, w.dxh, w.dxt)) != OQ_OK) return e;
+  OQ_HIP(scale_to_bf16(w.dxt, let ? p->s[1] : nullptr, T, m.Hd, w.datt16, st), "dO");
+  {
+    ProfScope ps(PK_ATTN_BWD, st, 4.0 * double(T) * m.S * m.Hd);   // dV, dP, dQ, dK (causal halves)
+    OQ_HIP(attn_bwd(w.qh, w.kh, w.vh, w.datt16, w.lse, T, int(m.S), int(m.H), int(m.Hkv),
+                    int(m.dh), w.Dl, w.dQ, w.dK, w.dV, st),
+           "attention backward");
+  }
+  {
+    ProfScope ps(PK_ACT_BWD, st, double(T) * m.Mqkv * 8);
+    OQ_HIP(act_bwd(w.qt, false, T, m.Hd, ab, nullptr, nullptr, w.dQ, w.dqt, let ? w.psxq : nullptr,
+                   let ? w.ps1 : nullptr, st, sym),
+           "act_bwd Q");
+    OQ_HIP(act_bwd(w.kt, false, T, m.Kd, ab, nullptr, nullptr, w.dK, w.dkt, let ? w.psxk : nullptr,
+                   let ? w.ps1 : nullptr, st, sym),
+           "act_bwd K");
+    OQ_HIP(act_bwd(w.vv, false, T, m.Kd, ab, nullptr, nullptr, w.dV, w.dvt, nullptr, nullptr, st, sym),
+           "act_bwd V");
+  }
+  if (let)
+    OQ_HIP(sa_grad_finish(w.psxq, npa, w.psxk, npa, int(m.H), int(m.Hkv), int(m.dh), p->s_a,
+                          g->d_s_a, st),
+           "s_a finish");
+  OQ_HIP(qkv_post_bwd(w.dqt, w.dkt, w.dvt, T, int(m.S), int(m.H), int(m.Hkv), int(m.dh),
+                      d->rope_base, let ? p->s_a : nullptr, w.dqkv16, st),
+         "qkv epilogue backward");
+  if ((e = linears_bwd(0, 3, w.dqkv16, w.wqkv, w.xh1, w.dxh)) != OQ_OK) return e;
+  if ((e = site_bwd(0, w.x1, D, w.dxh, w.dxt)) != OQ_OK) return e;
+  // ---- AdamW over every trained tensor
+  if (opt) {
+    const AdamCoef cl = adam_coef(opt->lr_lwc, opt->beta1, opt->beta2, opt->eps, opt->wd, opt->step);
+    const AdamCoef ce = adam_coef(opt->lr_let, opt->beta1, opt->beta2, opt->eps, opt->wd, opt->step);
+    ProfScope ps(PK_OTHER, st, 0);
+    AdamList L{};
+    auto add = [&](float* pp, const float* gg, float* mm, float* vv, int64_t n, int set) {
+      L.p[L.n] = pp; L.g[L.n] = gg; L.m[L.n] = mm; L.v[L.n] = vv; L.len[L.n] = n; L.set[L.n] = set;
+      ++L.n;
+    };
+    for (int l = 0; l < NL; ++l) {
+      const int64_t n = m.c_out[l] * (m.c_in[l] / d->w_group[l]);
+      add(p->gamma_logit[l], g->d_gamma_logit[l], opt->m_gamma[l], opt->v_gamma[l], n, 0);
+      add(p->beta_logit[l], g->d_beta_logit[l], opt->m_beta[l], opt->v_beta[l], n, 0);
+    }
+    if (let) {
+      const int64_t cs[3] = {D, m.Hd, D};
+      for (int k = 0; k < 3; ++k) {
+        add(p->s[k], g->d_s[k], opt->m_s[k], opt->v_s[k], cs[k], 1);
+        add(p->delta[k], g->d_delta[k], opt->m_delta[k], opt->v_delta[k], cs[k], 1);
+      }
+      add(p->s_a, g->d_s_a, opt->m_s_a, opt->v_s_a, m.Kd, 1);
+    }
+    OQ_HIP(adamw_multi(L, cl, ce, st), "adamw");
+  }
+  return OQ_OK;
+}
+
+}  // extern "C"

@@ -8,7 +8,8 @@ namespace oq {
 
 enum ProfKind {
   PK_GEMM_FWD = 0, PK_GEMM_WGRAD = 1, PK_GEMM_DGRAD = 2, PK_LWC_FWD = 3, PK_LWC_BWD = 4,
-  PK_ACT_FWD = 5, PK_ACT_BWD = 6, PK_TRANSPOSE = 7, PK_OTHER = 8
+  PK_ACT_FWD = 5, PK_ACT_BWD = 6, PK_TRANSPOSE = 7, PK_OTHER = 8,
+  PK_ATTN_FWD = 10, PK_ATTN_BWD = 11
 };
 
 // Kernel timing: when enabled, brackets a launch with events on its stream.
@@ -203,5 +204,37 @@ hipError_t colstat(const void* X, bool bf16, int64_t rows, int64_t cols, float* 
 hipError_t let_init_finish(int64_t C, int64_t T, const float* ax_parts, int64_t nax,
                            const double* sum_parts, const float* aw_parts, int64_t naw, float* s,
                            float* delta, hipStream_t st);
+
+// ---------------------------------------------------------------- whole-block pieces
+// Causal attention (bf16 matrix cores), head_dim 64 or 128, S a multiple of 64.
+bool attn_supported(int64_t T, int S, int H, int Hkv, int dh);
+hipError_t attn_fwd(const void* Q, const void* K, const void* V, int64_t T, int S, int H, int Hkv,
+                    int dh, float* O, float* LSE, hipStream_t st);
+// Dl [H, T] scratch (D = sum_j P_ij dP_ij); dQ [T, H dh], dK, dV [T, Hkv dh] fp32 outputs.
+hipError_t attn_bwd(const void* Q, const void* K, const void* V, const void* dO, const float* LSE,
+                    int64_t T, int S, int H, int Hkv, int dh, float* Dl, float* dQ, float* dK,
+                    float* dV, hipStream_t st);
+hipError_t rmsnorm_fwd(const void* h, bool h_bf16, const float* g, int64_t T, int64_t D, float eps,
+                       float* x, float* rstd, hipStream_t st);
+hipError_t rmsnorm_bwd(const void* h, bool h_bf16, const float* g, const float* rstd,
+                       const float* dxt, const float* s, const float* dres, int64_t T, int64_t D,
+                       float* dh, hipStream_t st);
+hipError_t qkv_post(const float* qkv, const float* b, int64_t T, int S, int H, int Hkv, int dh,
+                    float base, const float* sa, float* Qt, float* Kt, float* V, hipStream_t st);
+hipError_t qkv_post_bwd(const float* dQt, const float* dKt, const float* dV, int64_t T, int S,
+                        int H, int Hkv, int dh, float base, const float* sa, void* dqkv,
+                        hipStream_t st);
+hipError_t sa_grad_finish(const float* pq, int64_t nq, const float* pk, int64_t nk, int H, int Hkv,
+                          int dh, const float* sa, float* dsa, hipStream_t st);
+hipError_t silu_mul(float* gu, const float* b, int64_t T, int64_t F, float* x4, hipStream_t st);
+hipError_t silu_mul_bwd(const float* gu, const float* dx4, int64_t T, int64_t F, void* dgu,
+                        hipStream_t st);
+hipError_t resid_add(const void* base, bool base_bf16, const float* y, const float* b, int64_t T,
+                     int64_t D, float* out, hipStream_t st);
+hipError_t block_loss(const float* h2, const void* tgt, int64_t T, int64_t D, float* dh,
+                      void* dh16, double* rows, float* loss, hipStream_t st);
+hipError_t scale_to_bf16(const float* in, const float* s, int64_t T, int64_t C, void* out,
+                         hipStream_t st);
+hipError_t colsum_finish(const double* parts, int64_t n, int64_t C, float* out, hipStream_t st);
 
 }  // namespace oq

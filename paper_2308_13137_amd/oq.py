@@ -19,7 +19,7 @@ WQ_LWC, WQ_PACT, WQ_LSQ = 0, 1, 2          # weight quantisers (lin_quant)
 ACT_SYM = 0x100                            # OR into activation bits: symmetric absmax
 MAX_SITES, MAX_LINEARS = 8, 16
 PROF_KINDS = ["gemm_fwd", "gemm_wgrad", "gemm_dgrad", "lwc_fwd", "lwc_bwd", "act_fwd",
-              "act_bwd", "transpose", "other", "packed_linear"]
+              "act_bwd", "transpose", "other", "packed_linear", "attn_fwd", "attn_bwd"]
 
 # name -> (restype, argtypes); the exported surface of include/oq.h
 _P, _I64, _I, _D, _SZ = C.c_void_p, C.c_int64, C.c_int, C.c_double, C.c_size_t
@@ -610,3 +610,182 @@ def profile_read():
         _check(lib().oq_profile_read(i, C.byref(n), C.byref(ms), C.byref(w)))
         out[name] = (n.value, ms.value, w.value)
     return out
+
+
+# ------------------------------------------------------------------ whole LLaMA block
+_SIGS_LLAMA = {
+    "oq_attention_fwd": (_I, [_P, _P, _P, _I64, _I64, _I, _I, _I, _P, _P, _P]),
+    "oq_attention_bwd_workspace_size": (_I, [_I64, _I, _PSZ]),
+    "oq_attention_bwd": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]),
+    "oq_llama_workspace_size": (_I, [_P, _PSZ]),
+    "oq_llama_block_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "oq_llama_block_forward": (_I, [_P, _P, _P, _I, _P, _P, _SZ, _P]),
+}
+SIGNATURES.update(_SIGS_LLAMA)
+NL = 7
+
+
+class LlamaDesc(C.Structure):
+    _fields_ = [("tokens", C.c_int64), ("seq_len", C.c_int64), ("hidden", C.c_int64),
+                ("ffn", C.c_int64), ("heads", C.c_int), ("kv_heads", C.c_int),
+                ("norm_eps", C.c_float), ("rope_base", C.c_float), ("w_bits", C.c_int * NL),
+                ("w_group", C.c_int64 * NL), ("act_bits", C.c_int), ("let", C.c_int)]
+
+
+class LlamaParams(C.Structure):
+    _fields_ = [("W", C.c_void_p * NL), ("norm1", C.c_void_p), ("norm2", C.c_void_p),
+                ("gamma_logit", C.c_void_p * NL), ("beta_logit", C.c_void_p * NL),
+                ("s", C.c_void_p * 3), ("delta", C.c_void_p * 3), ("s_a", C.c_void_p)]
+
+
+class LlamaGrads(C.Structure):
+    _fields_ = [("d_gamma_logit", C.c_void_p * NL), ("d_beta_logit", C.c_void_p * NL),
+                ("d_s", C.c_void_p * 3), ("d_delta", C.c_void_p * 3), ("d_s_a", C.c_void_p)]
+
+
+class LlamaOptim(C.Structure):
+    _fields_ = [("m_gamma", C.c_void_p * NL), ("v_gamma", C.c_void_p * NL),
+                ("m_beta", C.c_void_p * NL), ("v_beta", C.c_void_p * NL),
+                ("m_s", C.c_void_p * 3), ("v_s", C.c_void_p * 3), ("m_delta", C.c_void_p * 3),
+                ("v_delta", C.c_void_p * 3), ("m_s_a", C.c_void_p), ("v_s_a", C.c_void_p),
+                ("step", C.c_int), ("lr_lwc", C.c_double), ("lr_let", C.c_double),
+                ("beta1", C.c_double), ("beta2", C.c_double), ("eps", C.c_double),
+                ("wd", C.c_double)]
+
+
+def attention_fwd(Q, K, V, S, H, Hkv, stream=None):
+    """Causal attention over bf16 Q [T, H d], K, V [T, Hkv d].  Returns (O, LSE)."""
+    T = Q.shape[0]
+    d = Q.shape[1] // H
+    O = torch.empty((T, H * d), dtype=torch.float32, device=Q.device)
+    lse = torch.empty((H, T), dtype=torch.float32, device=Q.device)
+    _check(lib().oq_attention_fwd(_ptr(Q), _ptr(K), _ptr(V), T, S, H, Hkv, d, _ptr(O), _ptr(lse),
+                                  _stream(stream)))
+    return O, lse
+
+
+def attention_bwd(Q, K, V, dO, lse, S, H, Hkv, stream=None):
+    """Gradients of :func:`attention_fwd` for bf16 dO [T, H d], from its LSE.
+    Returns (dQ, dK, dV) fp32."""
+    T = Q.shape[0]
+    d = Q.shape[1] // H
+    f32 = dict(dtype=torch.float32, device=Q.device)
+    dQ = torch.empty((T, H * d), **f32)
+    dK = torch.empty((T, Hkv * d), **f32)
+    dV = torch.empty((T, Hkv * d), **f32)
+    n = C.c_size_t(0)
+    _check(lib().oq_attention_bwd_workspace_size(T, H, C.byref(n)))
+    ws = torch.empty(n.value, dtype=torch.uint8, device=Q.device)
+    _check(lib().oq_attention_bwd(_ptr(Q), _ptr(K), _ptr(V), _ptr(dO), _ptr(lse), T, S, H, Hkv, d,
+                                  _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), n.value,
+                                  _stream(stream)))
+    return dQ, dK, dV
+
+
+class LlamaBlock:
+    """One whole LLaMA block's calibration problem (oq_llama_block_step):
+    description, gradient buffers, AdamW state and workspace (torch tensors).
+    Linears in the order q, k, v, o, gate, up, down."""
+
+    def __init__(self, T, seq_len, hidden, heads, kv_heads, ffn, w_bits, w_group, act_bits=16,
+                 let=False, norm_eps=1e-6, rope_base=10000.0, device="cuda"):
+        d = LlamaDesc()
+        d.tokens, d.seq_len, d.hidden, d.ffn = T, seq_len, hidden, ffn
+        d.heads, d.kv_heads = heads, kv_heads
+        d.norm_eps, d.rope_base = norm_eps, rope_base
+        for l in range(NL):
+            d.w_bits[l], d.w_group[l] = w_bits[l], w_group[l]
+        d.act_bits, d.let = act_bits, int(bool(let))
+        self.desc, self.device, self.let = d, device, bool(let)
+        self.T, self.D, self.H, self.Hkv, self.F = T, hidden, heads, kv_heads, ffn
+        dh = hidden // heads
+        self.c_out = [heads * dh, kv_heads * dh, kv_heads * dh, hidden, ffn, ffn, hidden]
+        self.c_in = [hidden, hidden, hidden, heads * dh, hidden, hidden, ffn]
+        n = C.c_size_t(0)
+        _check(lib().oq_llama_workspace_size(C.byref(d), C.byref(n)))
+        self.ws_bytes = n.value
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        f32 = dict(dtype=torch.float32, device=device)
+        self.d_gamma = [torch.empty((co, ci // g), **f32)
+                        for co, ci, g in zip(self.c_out, self.c_in, w_group)]
+        self.d_beta = [torch.empty_like(t) for t in self.d_gamma]
+        site_w = [hidden, heads * dh, hidden]
+        self.d_s = [torch.empty(w, **f32) for w in site_w] if let else [None] * 3
+        self.d_delta = [torch.empty(w, **f32) for w in site_w] if let else [None] * 3
+        self.d_s_a = torch.empty(kv_heads * dh, **f32) if let else None
+        self.loss = torch.empty((), **f32)
+        self.opt = None
+        self.step_count = 0
+
+    def init_optimizer(self, lr_lwc=5e-3, lr_let=1e-2, beta1=0.9, beta2=0.999, eps=1e-8, wd=0.0):
+        o = LlamaOptim()
+        self._mv = []
+
+        def z(t, name, i=None):
+            m = torch.zeros_like(t)
+            self._mv.append(m)
+            if i is None:
+                setattr(o, name, m.data_ptr())
+            else:
+                getattr(o, name)[i] = m.data_ptr()
+        for l in range(NL):
+            for nm in ("m_gamma", "v_gamma", "m_beta", "v_beta"):
+                z(self.d_gamma[l], nm, l)
+        if self.let:
+            for k in range(3):
+                for nm in ("m_s", "v_s", "m_delta", "v_delta"):
+                    z(self.d_s[k], nm, k)
+            z(self.d_s_a, "m_s_a")
+            z(self.d_s_a, "v_s_a")
+        o.lr_lwc, o.lr_let, o.beta1, o.beta2, o.eps, o.wd = lr_lwc, lr_let, beta1, beta2, eps, wd
+        self.opt = o
+
+    def _params(self, W, norm1, norm2, gl=None, bl=None, s=None, delta=None, s_a=None):
+        p = LlamaParams()
+        for l in range(NL):
+            p.W[l] = _ptr(W[l]).value
+            if gl is not None:
+                p.gamma_logit[l] = _ptr(gl[l]).value
+                p.beta_logit[l] = _ptr(bl[l]).value
+        p.norm1, p.norm2 = _ptr(_f32(norm1, "norm1")).value, _ptr(_f32(norm2, "norm2")).value
+        if self.let and s is not None:
+            for k in range(3):
+                p.s[k] = _ptr(s[k]).value
+                p.delta[k] = _ptr(delta[k]).value
+            p.s_a = _ptr(s_a).value
+        return p
+
+    def step(self, h0, target, W, norm1, norm2, gl, bl, s=None, delta=None, s_a=None,
+             update=False, stream=None):
+        p = self._params(W, norm1, norm2, gl, bl, s, delta, s_a)
+        g = LlamaGrads()
+        for l in range(NL):
+            g.d_gamma_logit[l] = self.d_gamma[l].data_ptr()
+            g.d_beta_logit[l] = self.d_beta[l].data_ptr()
+        if self.let:
+            for k in range(3):
+                g.d_s[k] = self.d_s[k].data_ptr()
+                g.d_delta[k] = self.d_delta[k].data_ptr()
+            g.d_s_a = self.d_s_a.data_ptr()
+        opt = None
+        if update:
+            if self.opt is None:
+                raise OQError("call init_optimizer() before update=True")
+            self.step_count += 1
+            self.opt.step = self.step_count
+            opt = C.byref(self.opt)
+        _check(lib().oq_llama_block_step(C.byref(self.desc), _ptr(h0), _ptr(target), C.byref(p),
+                                         C.byref(g), opt, _ptr(self.loss), _ptr(self.ws),
+                                         self.ws_bytes, _stream(stream)))
+        return self.loss
+
+    def forward(self, h0, W, norm1, norm2, gl=None, bl=None, s=None, delta=None, s_a=None,
+                quantised=True, stream=None):
+        """The block's output (bf16 [T, D]): quantised with the given
+        parameters, or the full-precision block (Algorithm 1's propagation)."""
+        p = self._params(W, norm1, norm2, gl, bl, s, delta, s_a)
+        out = torch.empty((self.T, self.D), dtype=torch.bfloat16, device=self.device)
+        _check(lib().oq_llama_block_forward(C.byref(self.desc), _ptr(h0), C.byref(p),
+                                            int(bool(quantised)), _ptr(out), _ptr(self.ws),
+                                            self.ws_bytes, _stream(stream)))
+        return out
