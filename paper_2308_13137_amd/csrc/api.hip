@@ -1575,6 +1575,7 @@ struct LlamaWs {
   float *dh2, *dW, *dxh, *dxt, *dh1, *Dl, *dQ, *dK, *dV, *dqt, *dkt, *dvt;
   void *dh2_16, *dh1_16, *dgu16, *datt16, *dqkv16;
   double* rows;
+  float* rope;                        // RoPE table [S, dh/2] (cos, sin)
   float *bt_qkv, *bt_o, *bt_gu;       // folded biases B~ of the LET sites
   float *dbt, *psx, *ps1, *psxq, *psxk, *pw, *pb, *amax;
   double* csum;
@@ -1619,6 +1620,7 @@ size_t llama_carve(const LlamaDims& m, char* base, LlamaWs* w) {
   t.dh2 = cv.take<float>(T * D);
   t.dh2_16 = cv.take<uint16_t>(T * D);
   t.rows = cv.take<double>(T);
+  t.rope = cv.take<float>(m.S * m.dh);
   t.bt_qkv = cv.take<float>(m.Mqkv);
   t.bt_o = cv.take<float>(D);
   t.bt_gu = cv.take<float>(2 * F);
@@ -1732,8 +1734,9 @@ oq_status llama_forward(const LlamaDims& m, const oq_llama_desc* d, const void* 
   if ((e = weights(0, 3, w.wqkv)) != OQ_OK) return e;
   if (let && (e = biases(0, 3, w.bt_qkv)) != OQ_OK) return e;
   if ((e = product(w.xh1, w.wqkv, m.Mqkv, D, w.qkv)) != OQ_OK) return e;
+  OQ_HIP(rope_table(int(m.S), int(m.dh), d->rope_base, w.rope, st), "RoPE table");
   OQ_HIP(qkv_post(w.qkv, let ? w.bt_qkv : nullptr, T, int(m.S), int(m.H), int(m.Hkv), int(m.dh),
-                  d->rope_base, let ? p->s_a : nullptr, w.qt, w.kt, w.vv, st),
+                  w.rope, let ? p->s_a : nullptr, w.qt, w.kt, w.vv, st),
          "qkv epilogue");
   {
     ProfScope ps(PK_ACT_FWD, st, double(T) * m.Mqkv * 6);
@@ -2002,8 +2005,8 @@ oq_status oq_llama_block_step(const oq_llama_desc* d, const void* h0, const void
     OQ_HIP(sa_grad_finish(w.psxq, npa, w.psxk, npa, int(m.H), int(m.Hkv), int(m.dh), p->s_a,
                           g->d_s_a, st),
            "s_a finish");
-  OQ_HIP(qkv_post_bwd(w.dqt, w.dkt, w.dvt, T, int(m.S), int(m.H), int(m.Hkv), int(m.dh),
-                      d->rope_base, let ? p->s_a : nullptr, w.dqkv16, st),
+  OQ_HIP(qkv_post_bwd(w.dqt, w.dkt, w.dvt, T, int(m.S), int(m.H), int(m.Hkv), int(m.dh), w.rope,
+                      let ? p->s_a : nullptr, w.dqkv16, st),
          "qkv epilogue backward");
   if ((e = linears_bwd(0, 3, w.dqkv16, w.wqkv, w.xh1, w.dxh)) != OQ_OK) return e;
   if ((e = site_bwd(0, w.x1, D, w.dxh, w.dxt)) != OQ_OK) return e;

@@ -43,7 +43,6 @@ namespace {
 
 constexpr int AT = 64;          // queries / keys per tile
 constexpr int ANT = 256;        // threads per workgroup (4 waves)
-constexpr int TP = 72;          // bf16 pitch of a transposed [d][64] or [16][64] LDS row (144 B)
 
 typedef uint16_t bf16raw;
 
@@ -53,53 +52,76 @@ OQ_DEV f32x4_t mfma(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 }
 OQ_DEV uint32_t pack2(float a, float b) { return f2bf2(a, b); }
 
-// Row-major [64][DH] bf16 tile, 16-byte chunk c of row r at slot c ^ (r & (NCH-1)).
-template <int DH>
-OQ_DEV void load_tile_rm(uint4* lds, const bf16raw* g, int64_t ld, int tid) {
-  constexpr int NCH = DH / 8;
-#pragma unroll
-  for (int i = 0; i < AT * NCH / ANT; ++i) {
-    const int idx = tid + ANT * i;
-    const int r = idx / NCH, c = idx % NCH;
-    lds[r * NCH + (c ^ (r & (NCH - 1)))] = *reinterpret_cast<const uint4*>(g + r * ld + 8 * c);
-  }
-}
+// Row-major [64][DH] bf16 tile ("K layout"), 16-byte chunk c of row r at
+// slot c ^ (r & (NCH-1)).
 template <int DH>
 OQ_DEV bf16x8_t read_rm(const uint4* lds, int r, int c) {
   constexpr int NCH = DH / 8;
   return bits_as_bf16x8(lds[r * NCH + (c ^ (r & (NCH - 1)))]);
 }
-// Transposed [DH][64] bf16 tile with row pitch TP (the 64 tile rows become columns).
+
+// ------------------------------------------------------------------ forward
+// Row-major [64][DH] bf16 tile in 32-byte blocks, block b of row r at
+// b ^ vswz(r): the four rows one transposed read of a 16-lane group touches
+// (and the next group's four) fall in distinct banks.
 template <int DH>
-OQ_DEV void load_tile_tr(bf16raw* lds, const bf16raw* g, int64_t ld, int tid) {
+OQ_DEV int vswz(int r) {
+  return (r + 4 * (r >> 3)) & (DH / 16 - 1);
+}
+// Global -> registers: this thread's chunks of a 64-row tile (NCH 16-byte
+// chunks per row), chunk idx = tid + ANT * i.
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+template <int DH>
+OQ_DEV void tile_to_regs(u32x4_t (&v)[AT * DH / 8 / ANT], const bf16raw* g, int64_t ld, int tid) {
   constexpr int NCH = DH / 8;
 #pragma unroll
   for (int i = 0; i < AT * NCH / ANT; ++i) {
     const int idx = tid + ANT * i;
-    const int r = idx % AT, c = idx / AT;        // consecutive lanes: consecutive rows
-    const uint4 v = *reinterpret_cast<const uint4*>(g + r * ld + 8 * c);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      lds[(8 * c + 2 * e) * TP + r] = bf16raw(w[e] & 0xffffu);
-      lds[(8 * c + 2 * e + 1) * TP + r] = bf16raw(w[e] >> 16);
-    }
+    v[i] = *reinterpret_cast<const u32x4_t*>(g + (idx / NCH) * ld + 8 * (idx % NCH));
   }
 }
-// 8 consecutive bf16 of row `row` at column `col` (a multiple of 8) of a
-// pitch-TP tile.
-OQ_DEV bf16x8_t read_tr8(const bf16raw* lds, int row, int col) {
-  return bits_as_bf16x8(*reinterpret_cast<const uint4*>(lds + row * TP + col));
+// registers -> LDS, K layout (16-byte chunk c of row r at c ^ (r & (NCH-1)))
+template <int DH>
+OQ_DEV void regs_to_k(uint4* lds, const u32x4_t (&v)[AT * DH / 8 / ANT], int tid) {
+  constexpr int NCH = DH / 8;
+#pragma unroll
+  for (int i = 0; i < AT * NCH / ANT; ++i) {
+    const int idx = tid + ANT * i;
+    const int r = idx / NCH, c = idx % NCH;
+    reinterpret_cast<u32x4_t*>(lds)[r * NCH + (c ^ (r & (NCH - 1)))] = v[i];
+  }
 }
-// columns col .. col+3 and col+16 .. col+19 of row `row` (the permuted
-// k-order that matches a C-layout operand, see the forward)
-OQ_DEV bf16x8_t read_tr_perm(const bf16raw* lds, int row, int col) {
-  const uint2 a = *reinterpret_cast<const uint2*>(lds + row * TP + col);
-  const uint2 b = *reinterpret_cast<const uint2*>(lds + row * TP + col + 16);
-  return bits_as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
+// registers -> LDS, V layout (32-byte block b of row r at b ^ vswz(r))
+template <int DH>
+OQ_DEV void regs_to_v(uint4* lds, const u32x4_t (&v)[AT * DH / 8 / ANT], int tid) {
+  constexpr int NCH = DH / 8;
+#pragma unroll
+  for (int i = 0; i < AT * NCH / ANT; ++i) {
+    const int idx = tid + ANT * i;
+    const int r = idx / NCH, c = idx % NCH;
+    reinterpret_cast<u32x4_t*>(lds)[r * NCH + 2 * ((c >> 1) ^ vswz<DH>(r)) + (c & 1)] = v[i];
+  }
+}
+// A operand of O^T = V^T P for rows d = 16 j .. 16 j + 15 and the k-chunk k2,
+// in the k order of the P operand: lane (fk, i) needs keys 32 k2 + 4 fk + 0..3
+// and 32 k2 + 16 + 4 fk + 0..3 of column d = 16 j + i.  ds_read_b64_tr_b16
+// gives lane i of a 16-lane group four consecutive rows k0..k0+3 of column
+// 16 j + i when lane j' of the group points at row k0 + j'/4, columns
+// 16 j + 4 (j' % 4) .. + 3.
+template <int DH>
+OQ_DEV bf16x8_t v_frag(const uint4* sV, int j, int k2, int lane) {
+  typedef short v4i16 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4i16 lds_v4;
+  const int fk = lane >> 4, jj = lane & 15;
+  const int r0 = 32 * k2 + 4 * fk + (jj >> 2), r1 = r0 + 16;
+  const char* base = reinterpret_cast<const char*>(sV);
+  const char* a0 = base + r0 * (2 * DH) + 32 * (j ^ vswz<DH>(r0)) + 8 * (jj & 3);
+  const char* a1 = base + r1 * (2 * DH) + 32 * (j ^ vswz<DH>(r1)) + 8 * (jj & 3);
+  const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(a0));
+  const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(a1));
+  return __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-// ------------------------------------------------------------------ forward
 template <int DH>
 __global__ __launch_bounds__(ANT) void attn_fwd_kernel(const bf16raw* __restrict__ Q,
                                                        const bf16raw* __restrict__ K,
@@ -108,8 +130,10 @@ __global__ __launch_bounds__(ANT) void attn_fwd_kernel(const bf16raw* __restrict
                                                        float* __restrict__ LSE, int64_t T) {
   constexpr int KS = DH / 32;        // k-steps of the S product
   constexpr int JD = DH / 16;        // 16-row tiles of O^T
+  constexpr int NR = AT * DH / 8 / ANT;
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
   __shared__ uint4 sK[AT * DH / 8];
-  __shared__ __attribute__((aligned(16))) bf16raw sVt[DH * TP];
+  __shared__ uint4 sV[AT * DH / 8];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int fr = lane & 15, fk = lane >> 4;
   const int ntile = S / AT;
@@ -120,6 +144,7 @@ __global__ __launch_bounds__(ANT) void attn_fwd_kernel(const bf16raw* __restrict
   const int64_t row0 = int64_t(b) * S;
   const int qrow = qt * AT + 16 * wave + fr;            // this lane's query within the sample
   const float sc = 1.4426950408889634f / sqrtf(float(DH));
+  const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
 
   bf16x8_t qf[KS];
   {
@@ -132,14 +157,21 @@ __global__ __launch_bounds__(ANT) void attn_fwd_kernel(const bf16raw* __restrict
 #pragma unroll
   for (int j = 0; j < JD; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m = -INFINITY, l = 0.f, l_b = 0.f;
+  u32x4_t kr[NR], vr[NR];
+  tile_to_regs<DH>(kr, K + row0 * ldk + int64_t(g) * DH, ldk, tid);
+  tile_to_regs<DH>(vr, V + row0 * ldk + int64_t(g) * DH, ldk, tid);
 
   for (int kt = 0; kt <= qt; ++kt) {
     __syncthreads();
-    const int64_t krow = row0 + int64_t(kt) * AT;
-    load_tile_rm<DH>(sK, K + krow * ldk + int64_t(g) * DH, ldk, tid);
-    load_tile_tr<DH>(sVt, V + krow * ldk + int64_t(g) * DH, ldk, tid);
+    regs_to_k<DH>(sK, kr, tid);
+    regs_to_v<DH>(sV, vr, tid);
     __syncthreads();
-    // S^T [64 keys x 16 queries of this wave]
+    {                                                    // the next tile, in flight meanwhile
+      const int64_t krow = row0 + int64_t(kt < qt ? kt + 1 : kt) * AT;
+      tile_to_regs<DH>(kr, K + krow * ldk + int64_t(g) * DH, ldk, tid);
+      tile_to_regs<DH>(vr, V + krow * ldk + int64_t(g) * DH, ldk, tid);
+    }
+    // S^T [64 keys x 16 queries of this wave]: lane holds key 16 i + 4 fk + r, query fr
     f32x4_t st[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -148,67 +180,59 @@ __global__ __launch_bounds__(ANT) void attn_fwd_kernel(const bf16raw* __restrict
       for (int ks = 0; ks < KS; ++ks)
         st[i] = mfma(read_rm<DH>(sK, 16 * i + fr, 4 * ks + fk), qf[ks], st[i]);
     }
+    if (kt == qt) {                                      // the diagonal tile: causal mask
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (kt * AT + 16 * i + 4 * fk + r > qrow) st[i][r] = -INFINITY;
+    }
     float mt = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = kt * AT + 16 * i + 4 * fk + r;
-        float t = st[i][r] * sc;
-        if (key > qrow) t = -INFINITY;
-        st[i][r] = t;
-        mt = fmaxf(mt, t);
-      }
+    for (int i = 0; i < 4; ++i) mt = fmaxf(fmaxf(mt, fmaxf(st[i][0], st[i][1])), fmaxf(st[i][2], st[i][3]));
     mt = fmaxf(mt, __shfl_xor(mt, 16));
     mt = fmaxf(mt, __shfl_xor(mt, 32));
-    // the running maximum stays an integer, so every rescaling below is an
-    // exact power of two: each weight that reaches the PV product equals
-    // bf16(2^(t - M)) times a power of two, M the row's final maximum,
-    // whatever the tile order
-    const float mn = fmaxf(m, ceilf(mt));
-    const float alpha = m == -INFINITY ? 0.0f : ldexpf(1.0f, int(m - mn));
-    float ls = 0.f;
+    // the running maximum stays an integer, so every rescaling is an exact
+    // power of two: each weight reaching the PV product is bf16(2^(t - M))
+    // times a power of two, M the row's final maximum, whatever the tile order
+    const float mn = fmaxf(m, ceilf(mt * sc));
+    float ls = 0.f, lr = 0.f;
     bf16x8_t pb[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float p = exp2f(st[i][r] - mn);
-        st[i][r] = p;
-        ls += p;
-      }
-#pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2)
-      pb[k2] = bits_as_bf16x8(make_uint4(pack2(st[2 * k2][0], st[2 * k2][1]),
-                                         pack2(st[2 * k2][2], st[2 * k2][3]),
-                                         pack2(st[2 * k2 + 1][0], st[2 * k2 + 1][1]),
-                                         pack2(st[2 * k2 + 1][2], st[2 * k2 + 1][3])));
-    // the weights the PV product sees are the bf16 values: their own sum
-    // normalises O, so O stays an exact weighted mean of V rows (a component
-    // shared by every V row passes through unchanged); l (unrounded) gives LSE
-    float lr = 0.f;
-#pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
-      const uint4 u = __builtin_bit_cast(uint4, pb[k2]);
-      const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+      uint32_t w[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        lr += __uint_as_float(w4[e] << 16) + __uint_as_float(w4[e] & 0xffff0000u);
+      for (int e = 0; e < 4; ++e) {
+        const int i = 2 * k2 + (e >> 1), r0 = 2 * (e & 1);
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(st[i][r0], sc, -mn));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(st[i][r0 + 1], sc, -mn));
+        ls += p0 + p1;
+        w[e] = pack2(p0, p1);
+        // the weights the PV product sees are these bf16 values: their own
+        // sum normalises O (an exact weighted mean of V rows); l (unrounded)
+        // gives LSE
+        lr = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w[e]), ones, lr, false);
+      }
+      pb[k2] = bits_as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
     }
     ls += __shfl_xor(ls, 16);
     ls += __shfl_xor(ls, 32);
     lr += __shfl_xor(lr, 16);
     lr += __shfl_xor(lr, 32);
-    l = l * alpha + ls;
-    l_b = l_b * alpha + lr;
+    if (__any(mn != m)) {
+      const float alpha = m == -INFINITY ? 0.0f : ldexpf(1.0f, int(m - mn));
+      l *= alpha;
+      l_b *= alpha;
+#pragma unroll
+      for (int j = 0; j < JD; ++j) acc[j] = acc[j] * alpha;
+    }
+    l += ls;
+    l_b += lr;
     m = mn;
 #pragma unroll
-    for (int j = 0; j < JD; ++j) {
-      acc[j] = acc[j] * alpha;
+    for (int j = 0; j < JD; ++j)
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2)
-        acc[j] = mfma(read_tr_perm(sVt, 16 * j + fr, 32 * k2 + 4 * fk), pb[k2], acc[j]);
-    }
+      for (int k2 = 0; k2 < 2; ++k2) acc[j] = mfma(v_frag<DH>(sV, j, k2, lane), pb[k2], acc[j]);
   }
   const float inv = 1.0f / l_b;
   float* op = O + (row0 + qrow) * ldq + int64_t(h) * DH;
@@ -219,25 +243,69 @@ __global__ __launch_bounds__(ANT) void attn_fwd_kernel(const bf16raw* __restrict
   if (fk == 0) LSE[int64_t(h) * T + row0 + qrow] = m + log2f(l);
 }
 
-// ------------------------------------------------------------------ backward: dK, dV
+// ------------------------------------------------------------------ backward
+// Operands the backward needs transposed are read from the row-major tiles
+// with ds_read_b64_tr_b16: lane i of a 16-lane group receives rows
+// k0 .. k0+3 of column c0 + i when lane j of the group points at row
+// k0 + j/4, columns c0 + 4 (j % 4) .. + 3.
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+OQ_DEV v4i16_t tr4(const void* p) {
+  typedef __attribute__((address_space(3))) v4i16_t lds_v4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(p));
+}
+OQ_DEV bf16x8_t join(v4i16_t lo, v4i16_t hi) {
+  return __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+// Operand fragment from a [64][DH] tile in the K layout: lane (fk, i) gets
+// rows kb + 8 fk + 0..7 of column cb + i (cb a multiple of 16).
 template <int DH>
-__global__ __launch_bounds__(ANT) void attn_bwd_dkv_kernel(
+OQ_DEV bf16x8_t col_frag(const uint4* tile, int kb, int cb, int lane) {
+  constexpr int NCH = DH / 8;
+  const int fk = lane >> 4, jj = lane & 15;
+  const int cc = cb + 4 * (jj & 3);
+  const int r0 = kb + 8 * fk + (jj >> 2), r1 = r0 + 4;
+  const char* base = reinterpret_cast<const char*>(tile);
+  const char* a0 = base + r0 * (2 * DH) + 16 * ((cc >> 3) ^ (r0 & (NCH - 1))) + 2 * (cc & 7);
+  const char* a1 = base + r1 * (2 * DH) + 16 * ((cc >> 3) ^ (r1 & (NCH - 1))) + 2 * (cc & 7);
+  return join(tr4(a0), tr4(a1));
+}
+// A wave's [64][16] bf16 staging tile (row pitch TS): a lane of the product's
+// C layout writes four consecutive columns of one row in one 8-byte store;
+// t16_frag gives lane (fk, i) rows kb + 8 fk + 0..7 of column i.
+constexpr int TS = 20;
+OQ_DEV void t16_put4(bf16raw* t, int row, int col, float a, float b, float c, float d) {
+  *reinterpret_cast<uint2*>(t + row * TS + col) = make_uint2(pack2(a, b), pack2(c, d));
+}
+OQ_DEV bf16x8_t t16_frag(const bf16raw* t, int kb, int lane) {
+  const int fk = lane >> 4, jj = lane & 15;
+  const int r0 = kb + 8 * fk + (jj >> 2);
+  const bf16raw* a0 = t + r0 * TS + 4 * (jj & 3);
+  return join(tr4(a0), tr4(a0 + 4 * TS));
+}
+
+// dK, dV: one workgroup per 64-key tile and key head; each wave owns 16 keys
+// and accumulates over every query tile and query head of its group (S^T and
+// dP^T recomputed from LSE and D).  P^T and dS^T pass through the wave's
+// staging tiles, query-major, to become A operands.
+template <int DH>
+__global__ __launch_bounds__(ANT, 2) void attn_bwd_dkv_kernel(
     const bf16raw* __restrict__ Q, const bf16raw* __restrict__ K, const bf16raw* __restrict__ V,
     const bf16raw* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ Dl,
     int S, int H, int Hkv, int64_t T, float* __restrict__ dK, float* __restrict__ dV) {
-  constexpr int KS = DH / 32, JD = DH / 16;
+  constexpr int KS = DH / 32, JD = DH / 16, NR = AT * DH / 8 / ANT;
   __shared__ uint4 sQ[AT * DH / 8];
   __shared__ uint4 sdO[AT * DH / 8];
-  __shared__ __attribute__((aligned(16))) bf16raw sQt[DH * TP];
-  __shared__ __attribute__((aligned(16))) bf16raw sdOt[DH * TP];
-  __shared__ __attribute__((aligned(16))) bf16raw sP[4][16 * TP];
-  __shared__ __attribute__((aligned(16))) bf16raw sPl[4][16 * TP];
+  __shared__ __attribute__((aligned(16))) bf16raw sP[4][AT * TS];
+  __shared__ __attribute__((aligned(16))) bf16raw sH[4][AT * TS];
+  __shared__ __attribute__((aligned(16))) bf16raw sLo[4][AT * TS];
   __shared__ float sL[AT], sD[AT];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int fr = lane & 15, fk = lane >> 4;
   const int ntile = S / AT;
   const int kt = int(blockIdx.x), g = blockIdx.y, b = blockIdx.z;
   const int grp = H / Hkv;
+  const int nq = ntile - kt;                           // query tiles at or after this key tile
+  const int n_it = grp * nq;
   const int64_t ldq = int64_t(H) * DH, ldk = int64_t(Hkv) * DH;
   const int64_t row0 = int64_t(b) * S;
   const int key_w = kt * AT + 16 * wave;                // this wave's first key
@@ -258,74 +326,80 @@ __global__ __launch_bounds__(ANT) void attn_bwd_dkv_kernel(
 #pragma unroll
   for (int j = 0; j < JD; ++j) adk[j] = adv[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  for (int hq = g * grp; hq < (g + 1) * grp; ++hq) {
-    for (int qt = kt; qt < ntile; ++qt) {
-      __syncthreads();
-      const int64_t qrow0 = row0 + int64_t(qt) * AT;
-      load_tile_rm<DH>(sQ, Q + qrow0 * ldq + int64_t(hq) * DH, ldq, tid);
-      load_tile_rm<DH>(sdO, dO + qrow0 * ldq + int64_t(hq) * DH, ldq, tid);
-      load_tile_tr<DH>(sQt, Q + qrow0 * ldq + int64_t(hq) * DH, ldq, tid);
-      load_tile_tr<DH>(sdOt, dO + qrow0 * ldq + int64_t(hq) * DH, ldq, tid);
-      if (tid < AT) {
-        sL[tid] = LSE[int64_t(hq) * T + qrow0 + tid];
-        sD[tid] = Dl[int64_t(hq) * T + qrow0 + tid];
+  // registers holding the next (query head, query tile)'s Q, dO, LSE and D
+  u32x4_t qr[NR], dr[NR];
+  float lr = 0.f, dlr = 0.f;
+  auto fetch = [&](int it) {
+    const int hq = g * grp + it / nq, qt = kt + it % nq;
+    const int64_t qrow0 = row0 + int64_t(qt) * AT;
+    tile_to_regs<DH>(qr, Q + qrow0 * ldq + int64_t(hq) * DH, ldq, tid);
+    tile_to_regs<DH>(dr, dO + qrow0 * ldq + int64_t(hq) * DH, ldq, tid);
+    if (tid < AT) {
+      lr = LSE[int64_t(hq) * T + qrow0 + tid];
+      dlr = Dl[int64_t(hq) * T + qrow0 + tid];
+    }
+  };
+  fetch(0);
+  bf16raw* tp = sP[wave];
+  bf16raw* th = sH[wave];
+  bf16raw* tl = sLo[wave];
+  for (int it = 0; it < n_it; ++it) {
+    const int qt = kt + it % nq;
+    __syncthreads();
+    regs_to_k<DH>(sQ, qr, tid);
+    regs_to_k<DH>(sdO, dr, tid);
+    if (tid < AT) {
+      sL[tid] = lr;
+      sD[tid] = dlr;
+    }
+    __syncthreads();
+    fetch(it + 1 < n_it ? it + 1 : it);                 // in flight meanwhile
+    // S^T and dP^T [16 keys x 64 queries]: lane holds key 4 fk + r, query 16 jn + fr
+    f32x4_t st[4], dp[4];
+#pragma unroll
+    for (int jn = 0; jn < 4; ++jn) {
+      st[jn] = dp[jn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        st[jn] = mfma(kf[ks], read_rm<DH>(sQ, 16 * jn + fr, 4 * ks + fk), st[jn]);
+        dp[jn] = mfma(vf[ks], read_rm<DH>(sdO, 16 * jn + fr, 4 * ks + fk), dp[jn]);
       }
-      __syncthreads();
-      // S^T and dP^T [16 keys x 64 queries]: lane holds key 4 fk + r, query 16 jn + fr
-      f32x4_t st[4], dp[4];
+    }
+    const bool diag = qt == kt;
 #pragma unroll
-      for (int jn = 0; jn < 4; ++jn) {
-        st[jn] = dp[jn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int jn = 0; jn < 4; ++jn) {
+      const int ql = 16 * jn + fr;
+      const float L = sL[ql], D = sD[ql];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          st[jn] = mfma(kf[ks], read_rm<DH>(sQ, 16 * jn + fr, 4 * ks + fk), st[jn]);
-          dp[jn] = mfma(vf[ks], read_rm<DH>(sdO, 16 * jn + fr, 4 * ks + fk), dp[jn]);
-        }
+      for (int r = 0; r < 4; ++r) {
+        float p = __builtin_amdgcn_exp2f(fmaf(st[jn][r], sc, -L));
+        if (diag && 16 * wave + 4 * fk + r > ql) p = 0.0f;
+        st[jn][r] = p;
+        dp[jn][r] = p * (dp[jn][r] - D) * rs;           // dS^T (with the 1/sqrt(d) of the logits)
       }
-      bf16raw* pw = sP[wave];
-      // P^T into this wave's LDS rows; then dS^T into the same rows (after dV)
+      // P^T query-major: row = query, four consecutive keys
+      t16_put4(tp, ql, 4 * fk, st[jn][0], st[jn][1], st[jn][2], st[jn][3]);
+      // dS^T as two bf16 terms (hi + lo, 16 significant bits): a component
+      // shared by all queries' Q rows would otherwise meet the rounding of dS
+      float hi[4];
 #pragma unroll
-      for (int jn = 0; jn < 4; ++jn) {
-        const int ql = 16 * jn + fr;
-        const int q = qt * AT + ql;
+      for (int r = 0; r < 4; ++r) hi[r] = bf2f(f2bf(dp[jn][r]));
+      t16_put4(th, ql, 4 * fk, hi[0], hi[1], hi[2], hi[3]);
+      t16_put4(tl, ql, 4 * fk, dp[jn][0] - hi[0], dp[jn][1] - hi[1], dp[jn][2] - hi[2],
+               dp[jn][3] - hi[3]);
+    }
+    // dV += P^T dO and dK += dS^T Q: A = rows of keys, k = queries; B = dO^T
+    // and Q^T (rows of d), read transposed from the row-major tiles
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int key = key_w + 4 * fk + r;
-          float p = key > q ? 0.0f : exp2f(st[jn][r] * sc - sL[ql]);
-          st[jn][r] = p;
-          dp[jn][r] = p * (dp[jn][r] - sD[ql]) * rs;     // dS^T (with the 1/sqrt(d) of the logits)
-          pw[(4 * fk + r) * TP + ql] = f2bf(p);
-        }
-      }
-      // dV += P^T dO: A = P^T rows (keys), B = dO^T rows (d); k = queries
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const bf16x8_t ap = t16_frag(tp, 32 * k2, lane);
+      const bf16x8_t ah = t16_frag(th, 32 * k2, lane);
+      const bf16x8_t al = t16_frag(tl, 32 * k2, lane);
 #pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        const bf16x8_t a = read_tr8(pw, fr, 32 * k2 + 8 * fk);
-#pragma unroll
-        for (int j = 0; j < JD; ++j) adv[j] = mfma(a, read_tr8(sdOt, 16 * j + fr, 32 * k2 + 8 * fk), adv[j]);
-      }
-      // dK += dS^T Q with dS split into two bf16 terms (hi + lo, 16 significant
-      // bits): a component shared by all queries' Q rows would otherwise meet
-      // the rounding of dS unreduced.  The wave rewrites only its own rows,
-      // after its own reads of them.
-      bf16raw* pwl = sPl[wave];
-#pragma unroll
-      for (int jn = 0; jn < 4; ++jn)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const bf16raw hi = f2bf(dp[jn][r]);
-          pw[(4 * fk + r) * TP + 16 * jn + fr] = hi;
-          pwl[(4 * fk + r) * TP + 16 * jn + fr] = f2bf(dp[jn][r] - bf2f(hi));
-        }
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        const bf16x8_t a = read_tr8(pw, fr, 32 * k2 + 8 * fk);
-        const bf16x8_t al = read_tr8(pwl, fr, 32 * k2 + 8 * fk);
-#pragma unroll
-        for (int j = 0; j < JD; ++j) {
-          const bf16x8_t bq = read_tr8(sQt, 16 * j + fr, 32 * k2 + 8 * fk);
-          adk[j] = mfma(al, bq, mfma(a, bq, adk[j]));
-        }
+      for (int j = 0; j < JD; ++j) {
+        adv[j] = mfma(ap, col_frag<DH>(sdO, 32 * k2, 16 * j, lane), adv[j]);
+        const bf16x8_t bq = col_frag<DH>(sQ, 32 * k2, 16 * j, lane);
+        adk[j] = mfma(al, bq, mfma(ah, bq, adk[j]));
       }
     }
   }
@@ -340,18 +414,21 @@ __global__ __launch_bounds__(ANT) void attn_bwd_dkv_kernel(
     }
 }
 
-// ------------------------------------------------------------------ backward: dQ
+// dQ: one workgroup per 64-query tile and head, four waves of 16 queries.  A
+// first sweep over the key tiles forms D = sum_j P_ij dP_ij from the very
+// probabilities the gradients use (so every row of dS sums to zero to fp32
+// rounding) and writes it for the dK/dV kernel; the second sweep accumulates
+// dQ = dS K, dS staged key-major as two bf16 terms.
 template <int DH>
-__global__ __launch_bounds__(ANT) void attn_bwd_dq_kernel(
+__global__ __launch_bounds__(ANT, 2) void attn_bwd_dq_kernel(
     const bf16raw* __restrict__ Q, const bf16raw* __restrict__ K, const bf16raw* __restrict__ V,
     const bf16raw* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ Dl,
     int S, int H, int Hkv, int64_t T, float* __restrict__ dQ) {
-  constexpr int KS = DH / 32, JD = DH / 16;
+  constexpr int KS = DH / 32, JD = DH / 16, NR = AT * DH / 8 / ANT;
   __shared__ uint4 sK[AT * DH / 8];
   __shared__ uint4 sV[AT * DH / 8];
-  __shared__ __attribute__((aligned(16))) bf16raw sKt[DH * TP];
-  __shared__ __attribute__((aligned(16))) bf16raw sS[4][16 * TP];
-  __shared__ __attribute__((aligned(16))) bf16raw sSl[4][16 * TP];
+  __shared__ __attribute__((aligned(16))) bf16raw sH[4][AT * TS];
+  __shared__ __attribute__((aligned(16))) bf16raw sLo[4][AT * TS];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int fr = lane & 15, fk = lane >> 4;
   const int ntile = S / AT;
@@ -381,49 +458,26 @@ __global__ __launch_bounds__(ANT) void attn_bwd_dq_kernel(
     lse[r] = LSE[int64_t(h) * T + row0 + q_w + 4 * fk + r];
     dl[r] = 0.f;
   }
-  // sweep 1: D = sum_j P_ij dP_ij from the very probabilities the gradients
-  // use, so that every row of dS sums to zero to fp32 rounding
-  for (int kt = 0; kt <= qt; ++kt) {
-    __syncthreads();
-    const int64_t krow = row0 + int64_t(kt) * AT;
-    load_tile_rm<DH>(sK, K + krow * ldk + int64_t(g) * DH, ldk, tid);
-    load_tile_rm<DH>(sV, V + krow * ldk + int64_t(g) * DH, ldk, tid);
-    __syncthreads();
-#pragma unroll
-    for (int jn = 0; jn < 4; ++jn) {
-      f32x4_t st = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = st;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        st = mfma(qf[ks], read_rm<DH>(sK, 16 * jn + fr, 4 * ks + fk), st);
-        dp = mfma(df[ks], read_rm<DH>(sV, 16 * jn + fr, 4 * ks + fk), dp);
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = kt * AT + 16 * jn + fr;
-        if (key <= q_w + 4 * fk + r) dl[r] += exp2f(st[r] * sc - lse[r]) * dp[r];
-      }
-    }
-  }
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) dl[r] += __shfl_xor(dl[r], o);
-  }
-  if (fr == 0) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) Dl[int64_t(h) * T + row0 + q_w + 4 * fk + r] = dl[r];
-  }
   f32x4_t adq[JD];
 #pragma unroll
   for (int j = 0; j < JD; ++j) adq[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  for (int kt = 0; kt <= qt; ++kt) {
+  u32x4_t kr[NR], vr[NR];
+  const int nk = qt + 1;
+  auto fetch = [&](int t) {
+    const int64_t krow = row0 + int64_t(t) * AT;
+    tile_to_regs<DH>(kr, K + krow * ldk + int64_t(g) * DH, ldk, tid);
+    tile_to_regs<DH>(vr, V + krow * ldk + int64_t(g) * DH, ldk, tid);
+  };
+  fetch(0);
+  bf16raw* th = sH[wave];
+  bf16raw* tl = sLo[wave];
+  for (int it = 0; it < 2 * nk; ++it) {
+    const int kt = it < nk ? it : it - nk;
     __syncthreads();
-    const int64_t krow = row0 + int64_t(kt) * AT;
-    load_tile_rm<DH>(sK, K + krow * ldk + int64_t(g) * DH, ldk, tid);
-    load_tile_rm<DH>(sV, V + krow * ldk + int64_t(g) * DH, ldk, tid);
-    load_tile_tr<DH>(sKt, K + krow * ldk + int64_t(g) * DH, ldk, tid);
+    regs_to_k<DH>(sK, kr, tid);
+    regs_to_k<DH>(sV, vr, tid);
     __syncthreads();
+    fetch(kt + 1 < nk ? kt + 1 : 0);                    // in flight meanwhile
     // S and dP [16 queries x 64 keys]: lane holds query 4 fk + r, key 16 jn + fr
     f32x4_t st[4], dp[4];
 #pragma unroll
@@ -435,37 +489,57 @@ __global__ __launch_bounds__(ANT) void attn_bwd_dq_kernel(
         dp[jn] = mfma(df[ks], read_rm<DH>(sV, 16 * jn + fr, 4 * ks + fk), dp[jn]);
       }
     }
-    bf16raw* sw = sS[wave];
+    const bool diag = kt == qt;
 #pragma unroll
     for (int jn = 0; jn < 4; ++jn)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int q = q_w + 4 * fk + r;
-        const int key = kt * AT + 16 * jn + fr;
-        const float p = key > q ? 0.0f : exp2f(st[jn][r] * sc - lse[r]);
-        dp[jn][r] = p * (dp[jn][r] - dl[r]) * rs;
+        float p = __builtin_amdgcn_exp2f(fmaf(st[jn][r], sc, -lse[r]));
+        if (diag && 16 * jn + fr > 16 * wave + 4 * fk + r) p = 0.0f;
+        st[jn][r] = p;
       }
-    // dQ += dS K: A = dS rows (queries), B = K^T rows (d); k = keys.  dS as
-    // hi + lo bf16 terms: each row of dS sums to zero, so a component shared
-    // by all K rows cancels in the exact product and must not survive the
-    // rounding of dS.  Wave-private rows, rewritten after their reads.
-    bf16raw* swl = sSl[wave];
+    if (it < nk) {
+      // sweep 1: D
 #pragma unroll
-    for (int jn = 0; jn < 4; ++jn)
+      for (int jn = 0; jn < 4; ++jn)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dl[r] += st[jn][r] * dp[jn][r];
+      if (it == nk - 1) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+#pragma unroll
+          for (int o = 1; o < 16; o <<= 1) dl[r] += __shfl_xor(dl[r], o);
+        }
+        if (fr == 0) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) Dl[int64_t(h) * T + row0 + q_w + 4 * fk + r] = dl[r];
+        }
+      }
+      continue;
+    }
+    // sweep 2: dS = P (dP - D) / sqrt(d), key-major as hi + lo bf16 terms: each
+    // row of dS sums to zero, so a component shared by all K rows cancels in
+    // the exact product and must not survive the rounding of dS
+#pragma unroll
+    for (int jn = 0; jn < 4; ++jn) {
+      float v[4], hi[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const bf16raw hi = f2bf(dp[jn][r]);
-        sw[(4 * fk + r) * TP + 16 * jn + fr] = hi;
-        swl[(4 * fk + r) * TP + 16 * jn + fr] = f2bf(dp[jn][r] - bf2f(hi));
+        v[r] = st[jn][r] * (dp[jn][r] - dl[r]) * rs;
+        hi[r] = bf2f(f2bf(v[r]));
       }
+      t16_put4(th, 16 * jn + fr, 4 * fk, hi[0], hi[1], hi[2], hi[3]);
+      t16_put4(tl, 16 * jn + fr, 4 * fk, v[0] - hi[0], v[1] - hi[1], v[2] - hi[2], v[3] - hi[3]);
+    }
+    // dQ += dS K: A = dS rows (queries), k = keys; B = K^T rows (d)
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
-      const bf16x8_t a = read_tr8(sw, fr, 32 * k2 + 8 * fk);
-      const bf16x8_t al = read_tr8(swl, fr, 32 * k2 + 8 * fk);
+      const bf16x8_t ah = t16_frag(th, 32 * k2, lane);
+      const bf16x8_t al = t16_frag(tl, 32 * k2, lane);
 #pragma unroll
       for (int j = 0; j < JD; ++j) {
-        const bf16x8_t bk = read_tr8(sKt, 16 * j + fr, 32 * k2 + 8 * fk);
-        adq[j] = mfma(al, bk, mfma(a, bk, adq[j]));
+        const bf16x8_t bk = col_frag<DH>(sK, 32 * k2, 16 * j, lane);
+        adq[j] = mfma(al, bk, mfma(ah, bk, adq[j]));
       }
     }
   }

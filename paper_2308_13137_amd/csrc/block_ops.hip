@@ -77,10 +77,24 @@ __global__ __launch_bounds__(BT) void rmsnorm_bwd_kernel(const TH* __restrict__ 
 // head's key group), K~ = RoPE(k + b) * s_a, V = v + b.  RoPE turns the pair
 // (i, i + d/2) of each head by pos * base^(-2i/d), pos = token mod S.
 // One thread per (token, pair) of q and k heads and per v element pair.
+// RoPE angles of one sample: tab[pos * (d/2) + p] = (cos, sin) of
+// pos * base^(-2p/d), evaluated in fp64 and rounded to fp32 (computed once per
+// step; the rotation kernels read it from L2).
+__global__ __launch_bounds__(BT) void rope_table_kernel(int S, int dh, float base,
+                                                        float2* __restrict__ tab) {
+  const int half = dh / 2;
+  const int64_t i = int64_t(blockIdx.x) * BT + threadIdx.x;
+  if (i >= int64_t(S) * half) return;
+  const int pos = int(i / half), p = int(i % half);
+  const double ang = double(pos) * pow(double(base), -2.0 * p / dh);
+  tab[i] = make_float2(float(cos(ang)), float(sin(ang)));
+}
+
 __global__ __launch_bounds__(BT) void qkv_post_kernel(const float* __restrict__ qkv,
                                                       const float* __restrict__ b, int64_t T,
-                                                      int S, int H, int Hkv, int dh, float base,
+                                                      int S, int H, int Hkv, int dh,
                                                       const float* __restrict__ sa,
+                                                      const float2* __restrict__ tab,
                                                       float* __restrict__ Qt, float* __restrict__ Kt,
                                                       float* __restrict__ Vv) {
   const int half = dh / 2;
@@ -100,8 +114,8 @@ __global__ __launch_bounds__(BT) void qkv_post_kernel(const float* __restrict__ 
       a += b[c0];
       bb += b[c1];
     }
-    const double ang = double(t % S) * pow(double(base), -2.0 * p / dh);
-    const float cs = float(cos(ang)), sn = float(sin(ang));
+    const float2 cssn = tab[(t % S) * half + p];
+    const float cs = cssn.x, sn = cssn.y;
     const float ra = a * cs - bb * sn, rb = bb * cs + a * sn;
     if (isq) {
       const int g = head / (H / Hkv);
@@ -130,8 +144,9 @@ __global__ __launch_bounds__(BT) void qkv_post_kernel(const float* __restrict__ 
 __global__ __launch_bounds__(BT) void qkv_post_bwd_kernel(const float* __restrict__ dQt,
                                                           const float* __restrict__ dKt,
                                                           const float* __restrict__ dV, int64_t T,
-                                                          int S, int H, int Hkv, int dh, float base,
+                                                          int S, int H, int Hkv, int dh,
                                                           const float* __restrict__ sa,
+                                                          const float2* __restrict__ tab,
                                                           uint16_t* __restrict__ dqkv) {
   const int half = dh / 2;
   const int64_t W = int64_t(H + 2 * Hkv) * dh;
@@ -158,8 +173,8 @@ __global__ __launch_bounds__(BT) void qkv_post_bwd_kernel(const float* __restric
       ga = dKt[k0] * s0;
       gb = dKt[k0 + half] * s1;
     }
-    const double ang = double(t % S) * pow(double(base), -2.0 * p / dh);
-    const float cs = float(cos(ang)), sn = float(sin(ang));
+    const float2 cssn = tab[(t % S) * half + p];
+    const float cs = cssn.x, sn = cssn.y;
     // the transpose of the rotation [[c, -s], [s, c]]
     const int64_t c0 = int64_t(head) * dh + p;
     row[c0] = f2bf(ga * cs + gb * sn);
@@ -176,21 +191,31 @@ __global__ __launch_bounds__(BT) void qkv_post_bwd_kernel(const float* __restric
 // ds_a[g d + c] = (sum_t dK~ K~ [.., g d + c] - sum over the group's query
 // heads h of sum_t dQ~ Q~ [.., h d + c]) / s_a, from the column partials the
 // activation backward wrote ([nq, H d] and [nk, Hkv d]), in fixed order.
-__global__ __launch_bounds__(BT) void sa_grad_finish_kernel(const float* __restrict__ pq, int64_t nq,
-                                                            const float* __restrict__ pk, int64_t nk,
-                                                            int H, int Hkv, int dh,
-                                                            const float* __restrict__ sa,
-                                                            float* __restrict__ dsa) {
-  const int64_t c = int64_t(blockIdx.x) * BT + threadIdx.x;
+// Workgroup: 64 channels x 16 row slices; each thread sums its slice's rows in
+// order (fp64), the slices combine in a fixed tree: deterministic.
+constexpr int SA_COLS = 64, SA_SLICES = 16;
+__global__ __launch_bounds__(SA_COLS * SA_SLICES) void sa_grad_finish_kernel(
+    const float* __restrict__ pq, int64_t nq, const float* __restrict__ pk, int64_t nk, int H,
+    int Hkv, int dh, const float* __restrict__ sa, float* __restrict__ dsa) {
+  __shared__ double red[SA_SLICES][SA_COLS];
+  const int tc = threadIdx.x % SA_COLS, ts = threadIdx.x / SA_COLS;
+  const int64_t c = int64_t(blockIdx.x) * SA_COLS + tc;
   const int64_t Ck = int64_t(Hkv) * dh, Cq = int64_t(H) * dh;
-  if (c >= Ck) return;
-  const int g = int(c / dh), e = int(c % dh);
   double acc = 0.0;
-  for (int64_t i = 0; i < nk; ++i) acc += double(pk[i * Ck + c]);
-  const int grp = H / Hkv;
-  for (int hq = g * grp; hq < (g + 1) * grp; ++hq)
-    for (int64_t i = 0; i < nq; ++i) acc -= double(pq[i * Cq + int64_t(hq) * dh + e]);
-  dsa[c] = float(acc / double(sa[c]));
+  if (c < Ck) {
+    const int g = int(c / dh), e = int(c % dh);
+    for (int64_t i = ts; i < nk; i += SA_SLICES) acc += double(pk[i * Ck + c]);
+    const int grp = H / Hkv;
+    for (int hq = g * grp; hq < (g + 1) * grp; ++hq)
+      for (int64_t i = ts; i < nq; i += SA_SLICES) acc -= double(pq[i * Cq + int64_t(hq) * dh + e]);
+  }
+  red[ts][tc] = acc;
+  __syncthreads();
+  for (int w = SA_SLICES / 2; w > 0; w >>= 1) {
+    if (ts < w) red[ts][tc] += red[ts + w][tc];
+    __syncthreads();
+  }
+  if (ts == 0 && c < Ck) dsa[c] = float(red[0][tc] / double(sa[c]));
 }
 
 // ------------------------------------------------------------------ SiLU gating
@@ -320,30 +345,40 @@ hipError_t rmsnorm_bwd(const void* h, bool h_bf16, const float* g, const float* 
   return hipGetLastError();
 }
 
+hipError_t rope_table(int S, int dh, float base, float* tab, hipStream_t st) {
+  const int64_t n = int64_t(S) * (dh / 2);
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_table_kernel, dim3(blocks_for(n)), dim3(BT), 0, st, S, dh, base,
+                     reinterpret_cast<float2*>(tab));
+  return hipGetLastError();
+}
+
 hipError_t qkv_post(const float* qkv, const float* b, int64_t T, int S, int H, int Hkv, int dh,
-                    float base, const float* sa, float* Qt, float* Kt, float* V, hipStream_t st) {
+                    const float* tab, const float* sa, float* Qt, float* Kt, float* V,
+                    hipStream_t st) {
   const int64_t n = T * int64_t(H + 2 * Hkv) * (dh / 2);
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(qkv_post_kernel, dim3(blocks_for(n)), dim3(BT), 0, st, qkv, b, T, S, H, Hkv,
-                     dh, base, sa, Qt, Kt, V);
+                     dh, sa, reinterpret_cast<const float2*>(tab), Qt, Kt, V);
   return hipGetLastError();
 }
 
 hipError_t qkv_post_bwd(const float* dQt, const float* dKt, const float* dV, int64_t T, int S,
-                        int H, int Hkv, int dh, float base, const float* sa, void* dqkv,
+                        int H, int Hkv, int dh, const float* tab, const float* sa, void* dqkv,
                         hipStream_t st) {
   const int64_t n = T * int64_t(H + 2 * Hkv) * (dh / 2);
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(qkv_post_bwd_kernel, dim3(blocks_for(n)), dim3(BT), 0, st, dQt, dKt, dV, T,
-                     S, H, Hkv, dh, base, sa, static_cast<uint16_t*>(dqkv));
+                     S, H, Hkv, dh, sa, reinterpret_cast<const float2*>(tab),
+                     static_cast<uint16_t*>(dqkv));
   return hipGetLastError();
 }
 
 hipError_t sa_grad_finish(const float* pq, int64_t nq, const float* pk, int64_t nk, int H, int Hkv,
                           int dh, const float* sa, float* dsa, hipStream_t st) {
   const int64_t n = int64_t(Hkv) * dh;
-  hipLaunchKernelGGL(sa_grad_finish_kernel, dim3(blocks_for(n)), dim3(BT), 0, st, pq, nq, pk, nk,
-                     H, Hkv, dh, sa, dsa);
+  hipLaunchKernelGGL(sa_grad_finish_kernel, dim3(unsigned((n + SA_COLS - 1) / SA_COLS)),
+                     dim3(SA_COLS * SA_SLICES), 0, st, pq, nq, pk, nk, H, Hkv, dh, sa, dsa);
   return hipGetLastError();
 }
 

@@ -219,10 +219,13 @@ hipError_t rmsnorm_fwd(const void* h, bool h_bf16, const float* g, int64_t T, in
 hipError_t rmsnorm_bwd(const void* h, bool h_bf16, const float* g, const float* rstd,
                        const float* dxt, const float* s, const float* dres, int64_t T, int64_t D,
                        float* dh, hipStream_t st);
+// RoPE angle table of one sample: tab [S, dh/2] float2 (cos, sin).
+hipError_t rope_table(int S, int dh, float base, float* tab, hipStream_t st);
 hipError_t qkv_post(const float* qkv, const float* b, int64_t T, int S, int H, int Hkv, int dh,
-                    float base, const float* sa, float* Qt, float* Kt, float* V, hipStream_t st);
+                    const float* tab, const float* sa, float* Qt, float* Kt, float* V,
+                    hipStream_t st);
 hipError_t qkv_post_bwd(const float* dQt, const float* dKt, const float* dV, int64_t T, int S,
-                        int H, int Hkv, int dh, float base, const float* sa, void* dqkv,
+                        int H, int Hkv, int dh, const float* tab, const float* sa, void* dqkv,
                         hipStream_t st);
 hipError_t sa_grad_finish(const float* pq, int64_t nq, const float* pk, int64_t nk, int H, int Hkv,
                           int dh, const float* sa, float* dsa, hipStream_t st);

@@ -226,8 +226,9 @@ def grad_items(g):
 def compare_step(desc, h0, target, p, act_bits):
     """One block step on the GPU against the oracle's (with its bf16 operand
     reading): the loss, and every gradient tensor in max-norm (max |g - r| /
-    max |r|) and in L2 (||g - r|| / ||r||), within TOL.  Measured errors are
-    1e-3 to 5e-3 at LLaMA-7B width and below 1e-3 on the small blocks."""
+    max |r|) and in L2 (||g - r|| / ||r||), within TOL (with quantised
+    activations, see below).  Measured errors without activation quantisation
+    are 1e-3 to 5e-3 at LLaMA-7B width and below 1e-3 on the small blocks."""
     T = h0.shape[0]
     blk = gpu_block(desc, T, act_bits)
     q = dev_params(p)
@@ -238,6 +239,16 @@ def compare_step(desc, h0, target, p, act_bits):
     print(f"  [llama] oracle step T={T}", flush=True)
     ref_loss, ref = lb.block_step(desc, h0, target, p)
     refs = dict(grad_items(ref))
+    bars = {n: (TOL, TOL) for n in refs}
+    if desc["act_bits"] < 16:
+        # quantised activations: a code flips wherever the two sides' inputs
+        # straddle a code boundary (a whole step of the per-token grid), and
+        # grouped clipping gradients sum such flips with cancellation; the bar
+        # is then the distance the oracle's own gradients move between its bf16
+        # operand reading and unrounded operands, where that exceeds TOL
+        _, g64 = lb.block_step(dict(desc, bf16=False), h0, target, p)
+        for n, a in grad_items(g64):
+            bars[n] = (max(TOL, normwise(a, refs[n])), max(TOL, l2rel(a, refs[n])))
     e_loss = abs(loss - ref_loss) / abs(ref_loss)
     bad = {} if e_loss <= TOL else {"loss": e_loss}
     line = [f"loss {e_loss:.1e}"]
@@ -257,9 +268,9 @@ def compare_step(desc, h0, target, p, act_bits):
             e2 = float(np.linalg.norm(err) / max(np.linalg.norm(refs[n]), np.linalg.norm(sa_terms)))
         else:
             en, e2 = normwise(a, refs[n]), l2rel(a, refs[n])
-        line.append(f"{n} {en:.1e} {e2:.1e}")
-        if en > TOL or e2 > TOL:
-            bad[n] = (en, e2)
+        line.append(f"{n} {en:.1e} {e2:.1e}" + (f" /{bars[n][0]:.0e}" if bars[n][0] > TOL else ""))
+        if en > bars[n][0] or e2 > bars[n][1]:
+            bad[n] = (en, e2, bars[n])
     print("  " + "  ".join(line), flush=True)
     assert not bad, bad
     return blk, q
