@@ -1576,6 +1576,7 @@ struct LlamaWs {
   void *dh2_16, *dh1_16, *dgu16, *datt16, *dqkv16;
   double* rows;
   float* rope;                        // RoPE table [S, dh/2] (cos, sin)
+  float* part;                        // K-split partial products
   float *bt_qkv, *bt_o, *bt_gu;       // folded biases B~ of the LET sites
   float *dbt, *psx, *ps1, *psxq, *psxk, *pw, *pb, *amax;
   double* csum;
@@ -1655,8 +1656,34 @@ size_t llama_carve(const LlamaDims& m, char* base, LlamaWs* w) {
   const int64_t nc = colstat_nparts(T);
   t.amax = cv.take<float>(nc * maxM);
   t.csum = cv.take<double>(nc * maxM);
+  // partial products of the K-split forward and input-gradient products
+  // (llama_mm takes the same decisions)
+  int64_t part = 0;
+  const int64_t fwd[4][2] = {{m.Mqkv, D}, {D, m.Hd}, {2 * F, D}, {D, F}};   // (N = c_out, K = c_in)
+  for (const auto& f : fwd) {
+    const int sf = gemm_mn_splits(false, false, T, f[0], f[1], f[1], f[1]);
+    if (sf > 1) part = std::max(part, sf * T * f[0]);
+    const int sd = gemm_mn_splits(false, true, T, f[1], f[0], f[0], f[1]);
+    if (sd > 1) part = std::max(part, sd * T * f[1]);
+  }
+  t.part = cv.take<float>(part);
   if (w) *w = t;
   return cv.off + 256;
+}
+
+// C [M, N] fp32 = A B with the K split gemm_mn_splits models fastest: the
+// parts go to w.part and are summed into C in fixed order (deterministic).
+oq_status llama_mm(const LlamaWs& w, const void* A, bool a_mn, const void* B, bool b_mn,
+                   int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, float* C,
+                   hipStream_t st, const char* what) {
+  const int sp = gemm_mn_splits(a_mn, b_mn, M, N, K, lda, ldb);
+  if (sp > 1) {
+    OQ_HIP(gemm_f32out_mn(A, a_mn, B, b_mn, M, N, K, lda, ldb, w.part, N, st, sp, M * N), what);
+    OQ_HIP(sum_partials_to(w.part, C, M * N, sp, M * N, st), what);
+  } else {
+    OQ_HIP(gemm_f32out_mn(A, a_mn, B, b_mn, M, N, K, lda, ldb, C, N, st), what);
+  }
+  return OQ_OK;
 }
 
 }  // namespace
@@ -1720,8 +1747,7 @@ oq_status llama_forward(const LlamaDims& m, const oq_llama_desc* d, const void* 
   };
   auto product = [&](const void* x, const void* wt, int64_t M, int64_t K, float* out) -> oq_status {
     ProfScope ps(PK_GEMM_FWD, st, 2.0 * double(T) * M * K);
-    OQ_HIP(gemm_f32out_mn(x, false, wt, false, T, M, K, K, K, out, M, st), "forward product");
-    return OQ_OK;
+    return llama_mm(w, x, false, wt, false, T, M, K, K, K, out, st, "forward product");
   };
   oq_status e;
   // ---- attention half
@@ -1921,7 +1947,8 @@ oq_status oq_llama_block_step(const oq_llama_desc* d, const void* h0, const void
     const bool let_site = let && k < 3;
     {
       ProfScope ps(PK_GEMM_DGRAD, st, 2.0 * double(T) * M * C);
-      OQ_HIP(gemm_f32out_mn(dy16, false, wst, true, T, C, M, M, C, dxh, C, st), "input gradient");
+      oq_status e2 = llama_mm(w, dy16, false, wst, true, T, C, M, M, C, dxh, st, "input gradient");
+      if (e2 != OQ_OK) return e2;
     }
     {
       ProfScope ps(PK_GEMM_WGRAD, st, 2.0 * double(T) * M * C);

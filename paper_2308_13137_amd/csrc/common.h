@@ -261,17 +261,17 @@ OQ_DEV QParams make_group_qparams(int quant, float mx, float mn, float p1, float
 // codes saturated above qmax and below 0.
 OQ_DEV void group_terms(int quant, float g, const QElem& qe, const QParams& p, float qmax,
                         float& s1, float& s2) {
+  // (selects rather than a branch between the two sums: a reference chosen
+  // at run time would put them in scratch memory)
   if (quant == WQ_PACT) {
-    if (!qe.m) {
-      if (qe.q == qmax) s1 += g;
-      else s2 += g;
-    }
+    s1 += (!qe.m && qe.q == qmax) ? g : 0.0f;
+    s2 += (!qe.m && qe.q != qmax) ? g : 0.0f;
     return;
   }
   const float t = qe.q - p.z;
   const float th = qe.m ? t - qe.u : t;
   s1 += g * th;
-  if (!qe.m) s2 += g;
+  s2 += qe.m ? 0.0f : g;
 }
 
 // A group's parameter gradients from its two sums, and the max/min

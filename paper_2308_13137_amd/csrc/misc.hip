@@ -332,12 +332,13 @@ __global__ __launch_bounds__(256) void adamw_multi_kernel(AdamList L, AdamCoef c
 }
 
 // ------------------------------------------------------------------ K-split partial sums
-// c[i] = ((c[i] + c[i + stride]) + c[i + 2 stride]) + ...  (fixed order), in
-// place over the first partial; grid stride, four elements per thread when
-// the layout allows.
-__global__ __launch_bounds__(256) void sum_partials4_kernel(float* c, int64_t n4, int parts,
-                                                            int64_t stride4) {
-  float4* c4 = reinterpret_cast<float4*>(c);
+// d[i] = ((c[i] + c[i + stride]) + c[i + 2 stride]) + ...  (fixed order); d
+// may be c (in place over the first partial); grid stride, four elements per
+// thread when the layout allows.
+__global__ __launch_bounds__(256) void sum_partials4_kernel(const float* c, float* d, int64_t n4,
+                                                            int parts, int64_t stride4) {
+  const float4* c4 = reinterpret_cast<const float4*>(c);
+  float4* d4 = reinterpret_cast<float4*>(d);
   for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n4;
        i += int64_t(gridDim.x) * 256) {
     float4 a = c4[i];
@@ -348,17 +349,17 @@ __global__ __launch_bounds__(256) void sum_partials4_kernel(float* c, int64_t n4
       a.z += b.z;
       a.w += b.w;
     }
-    c4[i] = a;
+    d4[i] = a;
   }
 }
 
-__global__ __launch_bounds__(256) void sum_partials1_kernel(float* c, int64_t n, int parts,
-                                                            int64_t stride) {
+__global__ __launch_bounds__(256) void sum_partials1_kernel(const float* c, float* d, int64_t n,
+                                                            int parts, int64_t stride) {
   for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n;
        i += int64_t(gridDim.x) * 256) {
     float a = c[i];
     for (int s = 1; s < parts; ++s) a += c[i + s * stride];
-    c[i] = a;
+    d[i] = a;
   }
 }
 
@@ -517,18 +518,26 @@ hipError_t adamw_multi(const AdamList& L, AdamCoef c0, AdamCoef c1, hipStream_t 
   return hipGetLastError();
 }
 
-hipError_t sum_partials(float* c, int64_t n, int parts, int64_t stride, hipStream_t st) {
-  if (n <= 0 || parts <= 1) return hipSuccess;
-  if (stride < n) return hipErrorInvalidValue;
-  const bool v4 = n % 4 == 0 && stride % 4 == 0 && (reinterpret_cast<uintptr_t>(c) & 15) == 0;
+hipError_t sum_partials_to(const float* c, float* d, int64_t n, int parts, int64_t stride,
+                           hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  if (parts < 1 || (parts > 1 && stride < n)) return hipErrorInvalidValue;
+  if (parts == 1 && c == d) return hipSuccess;
+  const bool v4 = n % 4 == 0 && stride % 4 == 0 && (reinterpret_cast<uintptr_t>(c) & 15) == 0 &&
+                  (reinterpret_cast<uintptr_t>(d) & 15) == 0;
   const int64_t work = v4 ? n / 4 : n;
   const unsigned grid = unsigned(std::min<int64_t>((work + 255) / 256, 8192));
   if (v4)
-    hipLaunchKernelGGL(sum_partials4_kernel, dim3(grid), dim3(256), 0, st, c, n / 4, parts,
+    hipLaunchKernelGGL(sum_partials4_kernel, dim3(grid), dim3(256), 0, st, c, d, n / 4, parts,
                        stride / 4);
   else
-    hipLaunchKernelGGL(sum_partials1_kernel, dim3(grid), dim3(256), 0, st, c, n, parts, stride);
+    hipLaunchKernelGGL(sum_partials1_kernel, dim3(grid), dim3(256), 0, st, c, d, n, parts, stride);
   return hipGetLastError();
+}
+
+hipError_t sum_partials(float* c, int64_t n, int parts, int64_t stride, hipStream_t st) {
+  if (parts <= 1) return hipSuccess;
+  return sum_partials_to(c, c, n, parts, stride, st);
 }
 
 hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, AdamCoef c,

@@ -195,6 +195,9 @@ hipError_t adamw_multi(const AdamList& L, AdamCoef c0, AdamCoef c1, hipStream_t 
 // In place over the first of `parts` fp32 partials spaced `stride` apart:
 // c[i] = ((c[i] + c[i + stride]) + ...) in that order, i < n.
 hipError_t sum_partials(float* c, int64_t n, int parts, int64_t stride, hipStream_t st);
+// d = the sum of the parts c, c + stride, ... (fixed order); d may be c.
+hipError_t sum_partials_to(const float* c, float* d, int64_t n, int parts, int64_t stride,
+                           hipStream_t st);
 hipError_t adamw(float* p, const float* g, float* m, float* v, int64_t n, AdamCoef c,
                  hipStream_t st);
 // LET initialisation pieces
