@@ -143,19 +143,25 @@ def summarize_traffic(fetch_dir, write_dir, workload, cmd_fetch, cmd_write, kind
 
 def summarize_trace(db_path, steps, title, cmd):
     """Markdown summary of a rocprofv3 kernel trace (its rocpd database),
-    restricted to the timed steps: every step launches the same kernel
-    sequence, so the step's length is the period of the sequence at the end of
-    the trace, and the last ``steps`` periods are the timed steps."""
+    restricted to the timed steps: every step launches the same kernels, so
+    the step's length is the smallest window whose kernel multiset repeats
+    over the last ``steps`` windows of the trace, and those windows are the
+    timed steps."""
     import sqlite3
     con = sqlite3.connect(db_path)
     rows = con.execute("select name, start, end from kernels order by start").fetchall()
     period, drop = None, 0
     # trailing dispatches after the steps (the runtime's copy of the loss to
     # the host) are not part of the period
+    from collections import Counter
     for drop in range(0, 16):
         names = [r[0] for r in rows[:len(rows) - drop]]
         for L in range(1, len(names) // (steps + 1) + 1):
-            if all(names[-i] == names[-i - L] for i in range(1, (steps - 1) * L + 1)):
+            # the same kernels in each of the last `steps` windows (their order
+            # may differ where a step forks work onto side streams)
+            last = Counter(names[len(names) - L:])
+            if all(Counter(names[len(names) - (i + 1) * L:len(names) - i * L]) == last
+                   for i in range(1, steps)):
                 period = L
                 break
         if period:
