@@ -476,10 +476,14 @@ oq_status oq_pack_codes(const uint8_t* codes, int64_t c_out, int64_t c_in, int b
  *   Y      : [n_tok, c_out] in y_dt (fp32 or bf16), overwritten
  * Supported: bits 2..7 and c_in <= 65536 (else OQ_ERR_UNSUPPORTED); c_in % 32
  * == 0; group % 32 == 0 dividing c_in; every pointer 16-byte aligned (else
- * OQ_ERR_INVALID_ARG).  Any n_tok >= 0: the kernel is sized for decoding, one
- * launch per 8 tokens, each reading the packed weights once; n_tok == 0 or
- * c_out == 0 is a no-op that accepts NULL pointers.  Products and sums are
- * fp32 in a fixed order, so results are reproducible.
+ * OQ_ERR_INVALID_ARG).  Any n_tok >= 0: below 8 tokens (or for groups other
+ * than 128) the vector kernel, sized for decoding, one launch per 8 tokens;
+ * from 8 tokens with groups of 128 the matrix-core kernel, one launch per 64
+ * tokens; each launch reads the packed weights once.  n_tok == 0 or c_out == 0
+ * is a no-op that accepts NULL pointers.  Products of codes and activations
+ * are exact in fp32 and the sums run in a fixed order, so results are
+ * reproducible (on matrix cores a token's outputs do not depend on the other
+ * tokens of its batch).
  */
 oq_status oq_packed_linear(const void* X, oq_dtype x_dt, int64_t n_tok, int64_t c_in,
                            const uint8_t* packed, int bits, int64_t group, const float* h,

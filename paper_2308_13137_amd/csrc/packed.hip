@@ -32,6 +32,7 @@ constexpr int PL_ROWS = 2;                    // output rows a wave works on tog
 constexpr int PL_U = 2;                       // runs per lane loaded together
 constexpr uint32_t BF16_128_PAIR = 0x43004300u;
 constexpr size_t PL_LDS_MAX = 160 * 1024;
+constexpr int64_t PM_MIN_TOKENS = 8;          // batches from this size run on matrix cores
 
 typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
 
@@ -339,6 +340,153 @@ int resident(const void* kernel, size_t lds) {
   return n;
 }
 
+// ------------------------------------------------------------------ the linear on matrix cores
+// For batches of 8 or more tokens and groups of 128 codes.  A workgroup owns
+// 16 output rows; its eight waves take the row's groups g = wave, wave + 8, ...
+// For group g a lane (f, i) (f = lane / 16, i = lane % 16) loads run 4 g + f
+// of row i (BITS dwords); matrix instruction m (0..3) of the group multiplies
+// codes 8 m .. 8 m + 7 of each lane's run, widened to 128 + q in bf16 (exact),
+// with the activations of the same columns, 32 (4 g + f) + 8 m + e, as its B
+// operand: the group's p = sum x (128 + q) for 16 rows x 16 tokens, fp32.  The
+// lanes also sum those activations (xs = sum x), and the group contributes
+// h (p - (128 + z) xs) to each output, in fp32, as in the VALU kernel.  The
+// eight waves' partial outputs are added in fixed order through LDS.
+constexpr int PM_THREADS = 512;                // 8 waves share a tile's groups
+constexpr int PM_GROUP = 128;
+template <int BITS, int NTB>
+__global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
+    const uint16_t* __restrict__ X, int n_tok, int64_t c_in, const uint32_t* __restrict__ packed,
+    const float* __restrict__ h, const float* __restrict__ z, const float* __restrict__ bias,
+    int64_t c_out, void* __restrict__ Y, bool y_bf16) {
+  __shared__ float red[PM_THREADS / 64][NTB * 16][17];
+  // h and z of the workgroup's 16 rows (one contiguous block of each)
+  extern __shared__ float hz[];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int f = lane >> 4, i = lane & 15;
+  const int64_t o0 = int64_t(blockIdx.x) * 16;
+  const int ng = int(c_in / PM_GROUP);
+  const int64_t runs_row = c_in / 32;
+  {
+    const int64_t nrow = min<int64_t>(16, c_out - o0);
+    for (int e = tid; e < 16 * ng; e += PM_THREADS) {
+      const int64_t src = (o0 + min<int64_t>(e / ng, nrow - 1)) * ng + e % ng;
+      hz[e] = h[src];
+      hz[16 * ng + e] = 128.0f + z[src];
+    }
+  }
+  __syncthreads();
+  // this lane's A row (rows past c_out re-read the last row and store nothing)
+  const int64_t arow = min(o0 + i, c_out - 1);
+  const uint32_t* prow = packed + arow * runs_row * BITS;
+  // the token of this lane's B operand and accumulator column, per 16-token block
+  const uint16_t* xrow[NTB];
+  bool tok_ok[NTB];
+#pragma unroll
+  for (int tb = 0; tb < NTB; ++tb) {
+    const int t = 16 * tb + i;
+    tok_ok[tb] = t < n_tok;
+    xrow[tb] = X + int64_t(tok_ok[tb] ? t : 0) * c_in;
+  }
+  f32x4_t y[NTB];
+#pragma unroll
+  for (int tb = 0; tb < NTB; ++tb) y[tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // the next group's codes and activations are loaded while this one computes
+  uint32_t wn[BITS];
+  uint4 xn[4][NTB];
+  auto fetch = [&](int g) {
+    load_run<BITS>(prow + (4 * int64_t(g) + f) * BITS, wn);
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb)
+        xn[m][tb] = *reinterpret_cast<const uint4*>(xrow[tb] + 32 * (4 * int64_t(g) + f) + 8 * m);
+  };
+  if (wave < ng) fetch(wave);
+  for (int g = wave; g < ng; g += PM_THREADS / 64) {
+    uint32_t w[BITS];
+    uint4 xg[4][NTB];
+#pragma unroll
+    for (int k = 0; k < BITS; ++k) w[k] = wn[k];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb) xg[m][tb] = xn[m][tb];
+    if (g + PM_THREADS / 64 < ng) fetch(g + PM_THREADS / 64);
+    float hr[4], zr[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      hr[r] = hz[(4 * f + r) * ng + g];
+      zr[r] = hz[16 * ng + (4 * f + r) * ng + g];
+    }
+    f32x4_t acc[NTB];
+    float xs[NTB];
+#pragma unroll
+    for (int tb = 0; tb < NTB; ++tb) {
+      acc[tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      xs[tb] = 0.f;
+    }
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      uint32_t a[4];
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+        a[p] = field<BITS>(w, (8 * m + 2 * p) * BITS) |
+               (field<BITS>(w, (8 * m + 2 * p + 1) * BITS) << 16) | BF16_128_PAIR;
+      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, make_uint4(a[0], a[1], a[2], a[3]));
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb) {
+        uint4 xv = xg[m][tb];
+        if (!tok_ok[tb]) xv = make_uint4(0u, 0u, 0u, 0u);
+        acc[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8_t, xv),
+                                                          acc[tb], 0, 0, 0);
+        xs[tb] = dot2_bf16(xv.x, 0x3f803f80u, xs[tb]);
+        xs[tb] = dot2_bf16(xv.y, 0x3f803f80u, xs[tb]);
+        xs[tb] = dot2_bf16(xv.z, 0x3f803f80u, xs[tb]);
+        xs[tb] = dot2_bf16(xv.w, 0x3f803f80u, xs[tb]);
+      }
+    }
+#pragma unroll
+    for (int tb = 0; tb < NTB; ++tb) {
+      // xs of token 16 tb + i over the whole group: the four lanes f of column i
+      float s = xs[tb];
+      s += __shfl_xor(s, 16);
+      s += __shfl_xor(s, 32);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) y[tb][r] += hr[r] * (acc[tb][r] - zr[r] * s);
+    }
+  }
+  // lane (f, i) holds rows 4 f + r of the tile for token 16 tb + i
+#pragma unroll
+  for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[wave][16 * tb + i][4 * f + r] = y[tb][r];
+  __syncthreads();
+  for (int e = tid; e < NTB * 16 * 16; e += PM_THREADS) {
+    const int t = e / 16, rr = e % 16;
+    const int64_t o = o0 + rr;
+    if (t < n_tok && o < c_out) {
+      float v = red[0][t][rr];
+#pragma unroll
+      for (int w8 = 1; w8 < PM_THREADS / 64; ++w8) v += red[w8][t][rr];
+      if (bias) v += bias[o];
+      if (y_bf16) static_cast<uint16_t*>(Y)[int64_t(t) * c_out + o] = f2bf(v);
+      else static_cast<float*>(Y)[int64_t(t) * c_out + o] = v;
+    }
+  }
+}
+
+template <int BITS, int NTB>
+hipError_t launch_mfma(const uint16_t* X, int n_tok, int64_t c_in, const uint8_t* packed,
+                       const float* h, const float* z, const float* bias, int64_t c_out, void* Y,
+                       bool y_bf16, hipStream_t stream) {
+  const size_t lds = size_t(2 * 16) * size_t(c_in / PM_GROUP) * sizeof(float);
+  hipLaunchKernelGGL((packed_mfma_kernel<BITS, NTB>), dim3(unsigned((c_out + 15) / 16)),
+                     dim3(PM_THREADS), lds, stream, X, n_tok, c_in,
+                     reinterpret_cast<const uint32_t*>(packed), h, z, bias, c_out, Y, y_bf16);
+  return hipGetLastError();
+}
+
 template <int BITS, int NT>
 hipError_t launch_linear(const uint16_t* X, int n_tok, int64_t c_in, const uint8_t* packed,
                          int64_t group, const float* h, const float* z, const float* bias,
@@ -359,6 +507,22 @@ hipError_t linear_bits(const uint16_t* X, int64_t n_tok, int64_t c_in, const uin
                        int64_t group, const float* h, const float* z, const float* bias,
                        int64_t c_out, void* Y, bool y_bf16, hipStream_t stream) {
   const size_t es = y_bf16 ? 2 : 4;
+  if (n_tok >= PM_MIN_TOKENS && group == PM_GROUP) {
+    // matrix cores: launches of up to 16, 32 or 64 tokens
+    for (int64_t t0 = 0; t0 < n_tok;) {
+      const int64_t rem = n_tok - t0;
+      const int take = int(std::min<int64_t>(rem, 64));
+      const uint16_t* x = X + t0 * c_in;
+      void* y = static_cast<char*>(Y) + size_t(t0) * size_t(c_out) * es;
+      hipError_t e;
+      if (take <= 16) e = launch_mfma<BITS, 1>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
+      else if (take <= 32) e = launch_mfma<BITS, 2>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
+      else e = launch_mfma<BITS, 4>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
+      if (e != hipSuccess) return e;
+      t0 += take;
+    }
+    return hipSuccess;
+  }
   for (int64_t t0 = 0; t0 < n_tok;) {
     const int64_t rem = n_tok - t0;
     int nt = rem >= 8 ? 8 : rem >= 4 ? (rem == 4 ? 4 : 8) : rem >= 2 ? (rem == 2 ? 2 : 4) : 1;

@@ -8,7 +8,12 @@ h * (p - (128 + z) * xs) with xs = sum x, and sums runs and lanes in fp32.  Each
 of the at most ~40 roundings on the way contributes at most 2^-24 times a
 partial sum bounded by sum_c |x_c| (256 + q_c + |z_g|) h_g, so
 |Y - Y_oracle| <= 4e-6 * sum_c |x_c| (256 + q_c + |z_g|) h_g, plus half a bf16
-ulp of |Y| when Y is stored in bf16."""
+ulp of |Y| when Y is stored in bf16.
+
+Batches of 8 or more tokens with groups of 128 run on matrix cores: each
+group's p is a chain of four 32-term matrix products, up to 128 fp32
+roundings of a partial sum bounded by the same magnitude, plus the ~40 of the
+rest: (128 + 40) 2^-24 ~ 1.0e-5 times the same sum."""
 import numpy as np
 import pytest
 import torch
@@ -36,9 +41,15 @@ def make_linear(seed, bits, n_tok, c_out, c_in, group, bias, z_spread=0):
     return q, h, z, X, B
 
 
+def mfma_path(n_tok, group):
+    """The dispatch rule of oq_packed_linear: matrix cores from 8 tokens, groups of 128."""
+    return n_tok >= 8 and group == 128
+
+
 def bound(q, h, z, X, group):
     mag = (256.0 + q.astype(np.float64) + np.repeat(np.abs(z), group, axis=1)) * np.repeat(h, group, axis=1)
-    return 4e-6 * (np.abs(X).astype(np.float64) @ mag.T)
+    eps = (128 + 40) * 2.0 ** -24 if mfma_path(X.shape[0], group) else 4e-6
+    return eps * (np.abs(X).astype(np.float64) @ mag.T)
 
 
 def to_dev(a, dtype=None):
@@ -77,6 +88,15 @@ LINEAR = [
     (3, 1, 33, 11008, 11008, False, torch.float32, 0),
     # the widest input: one token per launch fits LDS, so 3 tokens are 3 launches
     (4, 3, 7, 65536, 128, False, torch.float32, 0),
+    # matrix cores (8+ tokens, groups of 128): 16-, 32- and 64-token launches,
+    # 70 = 64 + 6 tokens, ragged rows, the 7B shapes, every code width
+    (4, 16, 4096, 4096, 128, True, torch.float32, 0),
+    (4, 64, 1000, 11008, 128, False, torch.float32, 0),
+    (3, 33, 129, 11008, 128, True, torch.bfloat16, 1),
+    (2, 70, 300, 4096, 128, False, torch.float32, 0),
+    (5, 20, 17, 256, 128, True, torch.float32, 2),
+    (6, 9, 40, 384, 128, False, torch.float32, 0),
+    (7, 24, 33, 128, 128, True, torch.float32, 0),
 ]
 
 
@@ -108,6 +128,20 @@ def test_packed_linear_empty_and_reproducible():
     # one token at a time gives the same bits as the batch (fixed sum order)
     for t in range(5):
         assert torch.equal(oq.packed_linear(Xd[t:t + 1], Pd, 4, 128, hd, zd)[0], a[t])
+
+
+def test_matrix_core_batches_give_each_token_the_same_bits():
+    """On matrix cores a token's outputs depend only on its own column: a
+    token gives the same bits in batches of 8, 20 and 64."""
+    q, h, z, X, B = make_linear(12, 4, 64, 260, 4096, 128, True)
+    Xd, Pd, hd, zd, Bd = (to_dev(X, torch.bfloat16), to_dev(o_pack(q, 4)), to_dev(h), to_dev(z),
+                          to_dev(B))
+    full = oq.packed_linear(Xd, Pd, 4, 128, hd, zd, Bd)
+    a = oq.packed_linear(Xd[:8], Pd, 4, 128, hd, zd, Bd)
+    b = oq.packed_linear(Xd[30:50], Pd, 4, 128, hd, zd, Bd)
+    torch.cuda.synchronize()
+    assert torch.equal(a, full[:8])
+    assert torch.equal(b, full[30:50])
 
 
 def test_gate_up_stack_full_size_sampled_rows():
