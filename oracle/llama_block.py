@@ -22,7 +22,10 @@ Readings (the paper writes the equations, not the block's code):
     shared by the query heads of its group (grouped-query attention), so
     softmax((Q/s_a)(s_a K)^T) = softmax(Q K^T) exactly without quantisation;
   * Q_a applies per token to Q~, K~ and V (all heads of a token together) as
-    it does to the linears' inputs; the softmax output stays unquantised;
+    it does to the linears' inputs; the softmax output stays unquantised
+    unless ``desc["softmax_bits"]`` < 16 (the ablation on softmax
+    quantisation: Q_a on every query row of probabilities, see
+    :func:`attention`);
   * the residual stream, norms, RoPE, softmax and SiLU are evaluated in fp64;
     the quantisers in fp32 in Eq. 2's fixed order (the functions of
     ``oracle.quant``); the operands the kernels feed to matrix cores
@@ -95,17 +98,26 @@ def rope(x, n_heads, d, cos, sin, inverse=False):
     return out.reshape(T, n_heads * d)
 
 
-def attention(q, k, v, H, Hkv, d, seq_len, bf16=False):
+def attention(q, k, v, H, Hkv, d, seq_len, bf16=False, p_bits=16, rec=None, frozen=None,
+              ft=np.float32):
     """Causal softmax(q k^T / sqrt(d)) v per sample and query head; query
-    head h reads key/value head h // (H / Hkv).  Returns (out, probs), probs
-    the exact softmax.
+    head h reads key/value head h // (H / Hkv).  Returns (out, probs, phat):
+    probs the exact softmax, phat the probabilities that multiply v (None
+    without softmax quantisation).
 
     ``bf16``: the weights enter the product with v as bf16 matrix-core
     operands.  Reading: a row's weights are 2^(t - M) with t the logit in
     base 2 (s log2(e)) and M = ceil(max t) (an integral reference, so that
     the rounded weights do not depend on how the maximum was found), each
     rounded to bf16, and the output is divided by the sum of those rounded
-    weights (a weighted mean of v rows)."""
+    weights (a weighted mean of v rows).
+
+    ``p_bits`` < 16 (the softmax-quantisation ablation): each query row of
+    probabilities (its S entries, the causally masked zeros included) goes
+    through Q_a -- per-row asymmetric MinMax, in ``ft`` (the quantiser's fp32
+    order), its state kept in ``rec`` under "pq<b>_<h>" -- or, with
+    ``frozen``, the frozen surrogate; the quantised row multiplies v as it
+    is (bf16 operands with ``bf16``, no renormalisation)."""
     T = q.shape[0]
     ns = T // seq_len
     grp = H // Hkv
@@ -114,13 +126,14 @@ def attention(q, k, v, H, Hkv, d, seq_len, bf16=False):
     v = v.reshape(ns, seq_len, Hkv, d)
     out = np.zeros((ns, seq_len, H, d))
     P = np.zeros((ns, H, seq_len, seq_len))
+    PH = np.zeros_like(P) if p_bits < 16 else None
     mask = np.triu(np.ones((seq_len, seq_len), bool), 1)
     for b in range(ns):
         for h in range(H):
             kv = h // grp
             s = q[b, :, h, :] @ k[b, :, kv, :].T / np.sqrt(d)
             s[mask] = -np.inf
-            if bf16:
+            if bf16 and p_bits >= 16:
                 t = s * np.log2(np.e)
                 w = _op(np.exp2(t - np.ceil(np.max(t, axis=1, keepdims=True))), True)
                 out[b, :, h, :] = (w @ v[b, :, kv, :]) / np.sum(w, axis=1, keepdims=True)
@@ -128,14 +141,29 @@ def attention(q, k, v, H, Hkv, d, seq_len, bf16=False):
             p = np.exp(s)
             p /= np.sum(p, axis=1, keepdims=True)
             P[b, h] = p
-            if not bf16:
+            if p_bits < 16:
+                key = f"pq{b}_{h}"
+                if frozen is not None:
+                    ones = np.ones(seq_len)
+                    ph = _quant_frozen(p, ones, ones, frozen[key])
+                else:
+                    st = act_fwd(np.asarray(p, ft), p_bits, ft=ft)
+                    if rec is not None:
+                        rec[key] = st
+                    ph = st["X_dq"].astype(np.float64)
+                PH[b, h] = ph
+                out[b, :, h, :] = _op(ph, bf16) @ v[b, :, kv, :]
+            elif not bf16:
                 out[b, :, h, :] = p @ v[b, :, kv, :]
-    return out.reshape(T, H * d), P
+    return out.reshape(T, H * d), P, PH
 
 
-def attention_bwd(q, k, v, P, dout, H, Hkv, d, seq_len, bf16=False):
+def attention_bwd(q, k, v, P, dout, H, Hkv, d, seq_len, bf16=False, PH=None, rec=None):
     """Gradients of :func:`attention` with respect to q, k, v (from the exact
-    softmax ``P``).  ``bf16``: P enters the dV product as a bf16 operand."""
+    softmax ``P``).  ``bf16``: P enters the dV product as a bf16 operand.
+    With softmax quantisation (``PH`` the quantised probabilities, ``rec``
+    the quantiser states): dV from PH, and dP through Q_a's straight-through
+    backward before the softmax backward."""
     T = q.shape[0]
     ns = T // seq_len
     grp = H // Hkv
@@ -150,8 +178,11 @@ def attention_bwd(q, k, v, P, dout, H, Hkv, d, seq_len, bf16=False):
         for h in range(H):
             kv = h // grp
             p = P[b, h]
-            dv[b, :, kv, :] += _op(p, bf16).T @ do[b, :, h, :]
+            pv = p if PH is None else PH[b, h]
+            dv[b, :, kv, :] += _op(pv, bf16).T @ do[b, :, h, :]
             dp = do[b, :, h, :] @ v[b, :, kv, :].T
+            if PH is not None:
+                dp = act_bwd(rec[f"pq{b}_{h}"], dp)
             ds = p * (dp - np.sum(dp * p, axis=1, keepdims=True)) / np.sqrt(d)
             dq[b, :, h, :] = ds @ k[b, :, kv, :]
             dk[b, :, kv, :] += ds.T @ q[b, :, h, :]
@@ -276,8 +307,10 @@ def block_forward(desc, h0, target, params, frozen=None, ft=np.float32):
     qh = _op(_act(qt, ab, frozen, "actq", rec, ft, sym), bf16)
     kh = _op(_act(kt, ab, frozen, "actk", rec, ft, sym), bf16)
     vh = _op(_act(v, ab, frozen, "actv", rec, ft, sym), bf16)
-    att, probs = attention(qh, kh, vh, H, Hkv, d, S, bf16)
-    c.update(qt=qt, kt=kt, v=v, qh=qh, kh=kh, vh=vh, probs=probs, sa=sa, sa_q=sa_q)
+    pb = desc.get("softmax_bits", 16)
+    att, probs, ph = attention(qh, kh, vh, H, Hkv, d, S, bf16, p_bits=pb, rec=rec, frozen=frozen,
+                               ft=ft)
+    c.update(qt=qt, kt=kt, v=v, qh=qh, kh=kh, vh=vh, probs=probs, ph=ph, sa=sa, sa_q=sa_q)
     x2op = site_input(att, 1)
     c.update(x2=att, xop1=x2op)
     h1 = h0 + linear(3, x2op)
@@ -355,7 +388,7 @@ def block_step(desc, h0, target, params, ft=np.float32):
     datt = site_bwd(1, linear_bwd(3, dh1))
     # dO enters the attention backward's products (dP = dO V^T, dV = P^T dO)
     dqh, dkh, dvh = attention_bwd(c["qh"], c["kh"], c["vh"], c["probs"], _op(datt, bf16), H, Hkv,
-                                  d, S, bf16)
+                                  d, S, bf16, PH=c["ph"], rec=rec)
     dqt = _act_bwd(dqh, ab, "actq", rec)
     dkt = _act_bwd(dkh, ab, "actk", rec)
     dv = _act_bwd(dvh, ab, "actv", rec)
@@ -406,7 +439,7 @@ def fp_block(desc, h0, params):
     q = rope(x1 @ W[0].T, H, d, cos, sin)
     k = rope(x1 @ W[1].T, Hkv, d, cos, sin)
     v = x1 @ W[2].T
-    att, _ = attention(q, k, v, H, Hkv, d, S)
+    att, _, _ = attention(q, k, v, H, Hkv, d, S)
     h1 = h0 + att @ W[3].T
     x3, _ = rmsnorm(h1, params["g2"], d2["norm_eps"])
     x4 = silu(x3 @ W[4].T) * (x3 @ W[5].T)

@@ -131,7 +131,7 @@ def test_attention_kernels(c):
         k = 0.2 * k + rng.standard_normal(Hkv * d) * 3.0
         v = 0.1 * v + rng.standard_normal(Hkv * d) * 2.0
     q, k, v = bf16_exact(q), bf16_exact(k), bf16_exact(v)
-    out, P = lb.attention(q, k, v, H, Hkv, d, S, bf16=True)
+    out, P, _ = lb.attention(q, k, v, H, Hkv, d, S, bf16=True)
     O, lse = oq.attention_fwd(dev(q, torch.bfloat16), dev(k, torch.bfloat16), dev(v, torch.bfloat16),
                               S, H, Hkv)
     # the statistic in natural log: ln sum_k exp(q.k / sqrt(d))

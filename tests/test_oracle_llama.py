@@ -16,10 +16,10 @@ from oracle import llama_block as lb
 
 
 def tiny_desc(act_bits=4, let=True, H=2, Hkv=1, D=16, F=24, S=6, bits=(3, 4, 4, 3, 4, 3, 4),
-              act_sym=False):
+              act_sym=False, softmax_bits=16):
     return dict(hidden=D, heads=H, kv_heads=Hkv, ffn=F, seq_len=S, norm_eps=1e-6,
                 rope_base=10000.0, w_bits=list(bits), w_group=[8, 8, 16, 8, 8, 16, 8],
-                act_bits=act_bits, let=let, act_sym=act_sym)
+                act_bits=act_bits, let=let, act_sym=act_sym, softmax_bits=softmax_bits)
 
 
 def tiny_params(desc, rng, T):
@@ -101,7 +101,7 @@ def test_attention_matches_library_sdpa(H, Hkv):
     q = rng.standard_normal((ns * S, H * d))
     k = rng.standard_normal((ns * S, Hkv * d))
     v = rng.standard_normal((ns * S, Hkv * d))
-    out, P = lb.attention(q, k, v, H, Hkv, d, S)
+    out, P, _ = lb.attention(q, k, v, H, Hkv, d, S)
     tq = torch.from_numpy(q).reshape(ns, S, H, d).transpose(1, 2)
     tk = torch.from_numpy(k).reshape(ns, S, Hkv, d).transpose(1, 2).repeat_interleave(H // Hkv, 1)
     tv = torch.from_numpy(v).reshape(ns, S, Hkv, d).transpose(1, 2).repeat_interleave(H // Hkv, 1)
@@ -139,7 +139,7 @@ def test_attention_bf16_weights_brute_force():
     q = rng.standard_normal((S, H * d)) * 2
     k = rng.standard_normal((S, Hkv * d))
     v = rng.standard_normal((S, Hkv * d))
-    out, _ = lb.attention(q, k, v, H, Hkv, d, S, bf16=True)
+    out, _, _ = lb.attention(q, k, v, H, Hkv, d, S, bf16=True)
     for h in range(H):
         for i in range(S):
             t = [sum(q[i, h * d + e] * k[j, e] for e in range(d)) / math.sqrt(d) / math.log(2)
@@ -160,11 +160,11 @@ def test_attention_bf16_weights_properties():
     q = rng.standard_normal((2 * S, H * d)) * 2
     k = rng.standard_normal((2 * S, Hkv * d))
     u = rng.standard_normal(Hkv * d) * 50
-    out_u, _ = lb.attention(q, k, np.tile(u, (2 * S, 1)), H, Hkv, d, S, bf16=True)
+    out_u, _, _ = lb.attention(q, k, np.tile(u, (2 * S, 1)), H, Hkv, d, S, bf16=True)
     np.testing.assert_allclose(out_u, np.tile(u, (2 * S, H // Hkv)), rtol=1e-13)
     v = rng.standard_normal((2 * S, Hkv * d)) + u
-    out_b, P = lb.attention(q, k, v, H, Hkv, d, S, bf16=True)
-    out_x, _ = lb.attention(q, k, v, H, Hkv, d, S)
+    out_b, P, _ = lb.attention(q, k, v, H, Hkv, d, S, bf16=True)
+    out_x, _, _ = lb.attention(q, k, v, H, Hkv, d, S)
     spread = np.max(np.abs(v - v.mean(axis=0)))
     assert np.max(np.abs(out_b - out_x)) <= 2.0 ** -8 * spread
     do = rng.standard_normal(out_b.shape)
@@ -177,6 +177,36 @@ def test_attention_bf16_weights_properties():
             bound[b * S:(b + 1) * S, h * d:(h + 1) * d] = 2.0 ** -8 * Pb[b, h] @ np.abs(
                 do[b * S:(b + 1) * S, h * d:(h + 1) * d])
     assert np.all(np.abs(dv_b - dv_x) <= bound + 1e-15)
+
+
+def test_softmax_quantisation_properties():
+    """Q_a on each query row of probabilities: codes in range, within h/2 of
+    the row, the causally masked zeros (row minimum 0, so z = 0) stay exactly
+    zero, the row's largest probability lands on the top code, and the
+    output is the quantised rows times V; at 15 bits the output approaches
+    exact attention within 2^-14 of the spread of V."""
+    rng = np.random.default_rng(13)
+    H, Hkv, d, S = 2, 1, 8, 12
+    q = rng.standard_normal((2 * S, H * d)) * 2
+    k = rng.standard_normal((2 * S, Hkv * d))
+    v = rng.standard_normal((2 * S, Hkv * d))
+    rec = {}
+    out, P, PH = lb.attention(q, k, v, H, Hkv, d, S, p_bits=4, rec=rec)
+    mask = np.triu(np.ones((S, S), bool), 1)
+    for b in range(2):
+        for h in range(H):
+            st = rec[f"pq{b}_{h}"]
+            ph, p = PH[b, h], P[b, h]
+            assert np.all((st["q"] >= 0) & (st["q"] <= 15))
+            hq = st["h"].astype(np.float64)[:, None]
+            assert np.all(np.abs(ph - p) <= 0.5 * hq * (1 + 1e-6) + 1e-12)
+            assert np.all(ph[:-1][mask[:-1]] == 0.0)
+            assert np.all(st["q"][np.arange(S), np.argmax(p, axis=1)] == 15)
+            np.testing.assert_allclose(out.reshape(2, S, H, d)[b, :, h, :], ph @ v.reshape(2, S, Hkv, d)[b, :, 0, :],
+                                       rtol=1e-12, atol=1e-12)
+    out15, _, _ = lb.attention(q, k, v, H, Hkv, d, S, p_bits=15, rec={})
+    out_x, _, _ = lb.attention(q, k, v, H, Hkv, d, S)
+    assert np.max(np.abs(out15 - out_x)) <= 2.0 ** -14 * np.max(np.abs(v)) * S
 
 
 def test_fp_block_matches_a_torch_llama_block():
@@ -238,7 +268,8 @@ def test_let_is_an_equivalence_through_the_whole_block():
 
 # ---------------------------------------------------------------- finite differences
 FD_CASES = [dict(act_bits=4, let=True), dict(act_bits=16, let=True), dict(act_bits=16, let=False),
-            dict(act_bits=3, let=True, H=4, Hkv=2), dict(act_bits=4, let=True, act_sym=True)]
+            dict(act_bits=3, let=True, H=4, Hkv=2), dict(act_bits=4, let=True, act_sym=True),
+            dict(act_bits=4, let=True, softmax_bits=4), dict(act_bits=16, let=True, softmax_bits=6)]
 
 
 @pytest.mark.parametrize("case", FD_CASES, ids=[str(c) for c in FD_CASES])
@@ -297,8 +328,8 @@ def test_fd_detects_a_planted_error_in_the_attention_backward():
     _, g_ok = lb.block_step(desc, h0, target, p, ft=np.float64)
     good = lb.attention_bwd
     try:
-        def bad(*a):
-            dq, dk, dv = good(*a)
+        def bad(*a, **kw):
+            dq, dk, dv = good(*a, **kw)
             return dq * 1.01, dk, dv
         lb.attention_bwd = bad
         _, g_bad = lb.block_step(desc, h0, target, p, ft=np.float64)
