@@ -524,7 +524,8 @@ BLOCK_MODELS = {
 def block_name(args):
     g = "ch" if args.block_group == 0 else str(args.block_group)
     name = (f"{args.block_model}_block_w{args.block_bits}a{args.block_act_bits}_g{g}"
-            f"{'_let' if args.block_let else ''}")
+            f"{'_let' if args.block_let else ''}"
+            f"{f'_p{args.block_softmax_bits}' if args.block_softmax_bits < 16 else ''}")
     return name if args.block_tokens == args.block_seq else f"{name}_t{args.block_tokens}"
 
 
@@ -558,7 +559,8 @@ def block_inputs(args, device="cuda"):
                    delta=[torch.zeros(n, device=device) for n in sw],
                    s_a=torch.ones(Hkv * d, device=device))
     blk = oq.LlamaBlock(T, args.block_seq, D, H, Hkv, F, [args.block_bits] * 7, groups,
-                        act_bits=args.block_act_bits, let=args.block_let)
+                        act_bits=args.block_act_bits, let=args.block_let,
+                        softmax_bits=args.block_softmax_bits)
     target = blk.forward(h0, W, g1, g2, quantised=False)
     return blk, h0, target, W, g1, g2, gl, bl, let, groups
 
@@ -582,7 +584,7 @@ def block_cpu_baseline(args, groups):
     W = [bf(inputs.weights(rng, a, b, 0.02, 0.001)) for a, b in shapes]
     desc = dict(hidden=D, heads=H, kv_heads=Hkv, ffn=F, seq_len=T, norm_eps=1e-6, rope_base=10000.0,
                 w_bits=[args.block_bits] * 7, w_group=groups, act_bits=args.block_act_bits,
-                let=args.block_let)
+                let=args.block_let, softmax_bits=args.block_softmax_bits)
     gl = [np.full((a, b // g), 4.0, np.float32) for (a, b), g in zip(shapes, groups)]
     p = dict(W=W, gamma_logit=gl, beta_logit=[g.copy() for g in gl],
              g1=np.ones(D, np.float32), g2=np.ones(D, np.float32),
@@ -670,6 +672,7 @@ def bench_block(args):
                    "seq_len": args.block_seq, "hidden": D, "heads": H, "kv_heads": Hkv, "ffn": F,
                    "w_bits": args.block_bits, "group": args.block_group or "per-channel",
                    "act_bits": args.block_act_bits, "let": args.block_let,
+                   "softmax_bits": args.block_softmax_bits,
                    "parallelism": "single GPU"},
         "loss": loss,
         "block_seconds_at_20_epochs_128_samples": round(20 * 128 * args.block_seq / args.block_tokens
@@ -723,6 +726,8 @@ def main():
     ap.add_argument("--block-group", type=int, default=0, help="0: per output channel")
     ap.add_argument("--block-act-bits", type=int, default=4)
     ap.add_argument("--block-let", type=int, default=1)
+    ap.add_argument("--block-softmax-bits", type=int, default=16,
+                    help="2..8: quantise the softmax output too (16: not)")
     ap.add_argument("--block-seq", type=int, default=2048)
     ap.add_argument("--block-tokens", type=int, default=2048)
     ap.add_argument("--summarize-trace", nargs=3, metavar=("DB", "TITLE", "CMD"),

@@ -498,24 +498,35 @@ oq_status oq_packed_linear(const void* X, oq_dtype x_dt, int64_t n_tok, int64_t 
  *   head h / (H / Hkv).  O [T, H d] fp32 = softmax(Q K^T / sqrt(d) + causal
  *   mask) V per sample and head.  LSE [H, T] fp32: per query the log-sum-exp
  *   of its logits in base 2 of t = q.k log2(e)/sqrt(d) (kept for the backward).
- * The probabilities enter the product with V as bf16 weights 2^(t - ceil(max t))
- * and O is divided by the sum of those rounded weights (an exact weighted mean
- * of V rows).
+ * softmax_bits = 16: the probabilities enter the product with V as bf16
+ * weights 2^(t - ceil(max t)) and O is divided by the sum of those rounded
+ * weights (an exact weighted mean of V rows); pstat may be NULL.
+ * softmax_bits in 2..8 (the ablation on quantising the softmax output,
+ * Table tab:ablation_softmax): each query row of probabilities P = 2^(t - LSE),
+ * its S entries with the causally masked zeros, goes through the activation
+ * quantiser (per-row asymmetric MinMax, Eq. 2 with gamma = beta = 1) and the
+ * dequantised row multiplies V as bf16 operands, not renormalised.  pstat
+ * [H, T, 4] fp32 (16-byte aligned) receives per row (max P, min P, and the
+ * lowest key index holding each, as int32 bit patterns) for the backward.
  * Backward: dO [T, H d] bf16 -> dQ [T, H d], dK, dV [T, Hkv d] fp32 (dK and dV
  * summed over the query heads of each group), from the probabilities
  * recomputed with LSE; D = sum_j P_ij dP_ij is formed from those same
- * probabilities; P enters the dV product as bf16, dS the dQ and dK products
- * as a pair of bf16 terms (hi + lo); deterministic (no atomics).  Workspace:
- * [H, T] fp32 (D).
+ * probabilities; P (or its quantised row) enters the dV product as bf16, dS
+ * the dQ and dK products as a pair of bf16 terms (hi + lo); with a quantised
+ * softmax dP passes the quantiser's straight-through backward first (the
+ * row's max / min gradients to the keys in pstat).  Deterministic (no
+ * atomics).  Workspace: [H, T] fp32 (D), three times that with a quantised
+ * softmax.
  * Supported: d in {64, 128}, S a multiple of 64, T a multiple of S.
  */
 oq_status oq_attention_fwd(const void* Q, const void* K, const void* V, int64_t T, int64_t S,
-                           int H, int Hkv, int head_dim, float* O, float* LSE, hipStream_t stream);
-oq_status oq_attention_bwd_workspace_size(int64_t T, int H, size_t* bytes);
+                           int H, int Hkv, int head_dim, int softmax_bits, float* O, float* LSE,
+                           float* pstat, hipStream_t stream);
+oq_status oq_attention_bwd_workspace_size(int64_t T, int H, int softmax_bits, size_t* bytes);
 oq_status oq_attention_bwd(const void* Q, const void* K, const void* V, const void* dO,
-                           const float* LSE, int64_t T, int64_t S, int H, int Hkv, int head_dim,
-                           float* dQ, float* dK, float* dV, void* ws, size_t ws_bytes,
-                           hipStream_t stream);
+                           const float* LSE, const float* pstat, int64_t T, int64_t S, int H,
+                           int Hkv, int head_dim, int softmax_bits, float* dQ, float* dK, float* dV,
+                           void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * One calibration step over a whole LLaMA transformer block (Eq. 1 with F
@@ -548,6 +559,8 @@ typedef struct {
   int act_bits;                       /* 2..8 (| OQ_ACT_SYM): Q_a on the four linear
                                          inputs and on Q~, K~, V; 16 = none       */
   int let;                            /* 1: LET on the q/k/v, o, gate/up inputs and s_a */
+  int softmax_bits;                   /* 2..8: Q_a on each query row of the softmax
+                                         output (as oq_attention_fwd); 16 = none */
 } oq_llama_desc;
 
 typedef struct {                      /* device pointers                            */

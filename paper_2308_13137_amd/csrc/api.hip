@@ -1523,6 +1523,7 @@ struct LlamaDims {
   int64_t T, S, D, F, H, Hkv, dh, Hd, Kd, Mqkv;
   int64_t c_out[NL], c_in[NL];
   int ab;     // activation bits without the symmetric flag
+  int pb;     // softmax-output bits (16 = unquantised)
   bool sym, let;
 };
 
@@ -1552,6 +1553,9 @@ oq_status llama_dims(const oq_llama_desc* d, LlamaDims* o) {
   if (!(m.ab == 16 || (m.ab >= 2 && m.ab <= 8)) || (m.sym && m.ab == 16))
     return fail(OQ_ERR_UNSUPPORTED, "activation bits %d", d->act_bits);
   m.let = d->let != 0;
+  m.pb = d->softmax_bits;
+  if (!(m.pb == 16 || (m.pb >= 2 && m.pb <= 8)))
+    return fail(OQ_ERR_UNSUPPORTED, "softmax bits %d", d->softmax_bits);
   const int64_t co[NL] = {m.Hd, m.Kd, m.Kd, m.D, m.F, m.F, m.D};
   const int64_t ci[NL] = {m.D, m.D, m.D, m.Hd, m.D, m.D, m.F};
   for (int l = 0; l < NL; ++l) {
@@ -1570,7 +1574,7 @@ oq_status llama_dims(const oq_llama_desc* d, LlamaDims* o) {
 }
 
 struct LlamaWs {
-  float *x1, *rstd1, *qkv, *qt, *kt, *vv, *att, *lse, *o, *h1, *x3, *rstd2, *gu, *x4, *dn, *h2;
+  float *x1, *rstd1, *qkv, *qt, *kt, *vv, *att, *lse, *pstat, *o, *h1, *x3, *rstd2, *gu, *x4, *dn, *h2;
   void *xh1, *wqkv, *qh, *kh, *vh, *xh2, *wo, *xh3, *wgu, *xh4, *wd;
   float *dh2, *dW, *dxh, *dxt, *dh1, *Dl, *dQ, *dK, *dV, *dqt, *dkt, *dvt;
   void *dh2_16, *dh1_16, *dgu16, *datt16, *dqkv16;
@@ -1604,6 +1608,7 @@ size_t llama_carve(const LlamaDims& m, char* base, LlamaWs* w) {
   t.vh = cv.take<uint16_t>(T * m.Kd);
   t.att = cv.take<float>(T * m.Hd);
   t.lse = cv.take<float>(m.H * T);
+  t.pstat = cv.take<float>(m.pb < 16 ? 4 * m.H * T : 0);
   t.xh2 = cv.take<uint16_t>(T * m.Hd);
   t.wo = cv.take<uint16_t>(D * m.Hd);
   t.o = cv.take<float>(T * D);
@@ -1632,7 +1637,7 @@ size_t llama_carve(const LlamaDims& m, char* base, LlamaWs* w) {
   t.dh1_16 = cv.take<uint16_t>(T * D);
   t.dgu16 = cv.take<uint16_t>(T * 2 * F);
   t.datt16 = cv.take<uint16_t>(T * m.Hd);
-  t.Dl = cv.take<float>(m.H * T);
+  t.Dl = cv.take<float>(int64_t(attn_bwd_ws_floats(T, int(m.H), m.pb)));
   t.dQ = cv.take<float>(T * m.Hd);
   t.dK = cv.take<float>(T * m.Kd);
   t.dV = cv.take<float>(T * m.Kd);
@@ -1778,7 +1783,8 @@ oq_status llama_forward(const LlamaDims& m, const oq_llama_desc* d, const void* 
   }
   {
     ProfScope ps(PK_ATTN_FWD, st, 2.0 * double(T) * m.S * m.Hd);   // causal: QK^T and PV, half each
-    OQ_HIP(attn_fwd(w.qh, w.kh, w.vh, T, int(m.S), int(m.H), int(m.Hkv), int(m.dh), w.att, w.lse, st),
+    OQ_HIP(attn_fwd(w.qh, w.kh, w.vh, T, int(m.S), int(m.H), int(m.Hkv), int(m.dh),
+                    quant ? m.pb : 16, w.att, w.lse, w.pstat, st),
            "attention");
   }
   {
@@ -1836,39 +1842,50 @@ oq_status llama_check(const LlamaDims& m, const oq_llama_params* p, bool quant) 
 extern "C" {
 
 oq_status oq_attention_fwd(const void* Q, const void* K, const void* V, int64_t T, int64_t S,
-                           int H, int Hkv, int head_dim, float* O, float* LSE, hipStream_t st) {
+                           int H, int Hkv, int head_dim, int softmax_bits, float* O, float* LSE,
+                           float* pstat, hipStream_t st) {
   OQ_REQ(Q && K && V && O && LSE, "Q, K, V, O and LSE are required");
   OQ_REQ(aligned16(Q) && aligned16(K) && aligned16(V) && aligned16(O), "pointers must be 16-byte aligned");
+  OQ_REQ(softmax_bits == 16 || (softmax_bits >= 2 && softmax_bits <= 8), "softmax bits %d",
+         softmax_bits);
+  OQ_REQ(softmax_bits == 16 || (pstat && aligned16(pstat)),
+         "pstat (16-byte aligned) is required with softmax quantisation");
   if (!attn_supported(T, int(S), H, Hkv, head_dim) || S > INT32_MAX)
     return fail(OQ_ERR_UNSUPPORTED, "attention shape T=%lld S=%lld H=%d Hkv=%d d=%d", (long long)T,
                 (long long)S, H, Hkv, head_dim);
+  // causal: QK^T and PV, half each (a quantised softmax recomputes QK^T once more)
   ProfScope ps(PK_ATTN_FWD, st, 2.0 * double(T) * S * H * head_dim);
-  OQ_HIP(attn_fwd(Q, K, V, T, int(S), H, Hkv, head_dim, O, LSE, st), "attention");
+  OQ_HIP(attn_fwd(Q, K, V, T, int(S), H, Hkv, head_dim, softmax_bits, O, LSE, pstat, st), "attention");
   return OQ_OK;
 }
 
-oq_status oq_attention_bwd_workspace_size(int64_t T, int H, size_t* bytes) {
+oq_status oq_attention_bwd_workspace_size(int64_t T, int H, int softmax_bits, size_t* bytes) {
   OQ_REQ(bytes && T >= 0 && H > 0, "bad arguments");
-  *bytes = size_t(T) * size_t(H) * 4 + 256;
+  *bytes = attn_bwd_ws_floats(T, H, softmax_bits) * 4 + 256;
   return OQ_OK;
 }
 
 oq_status oq_attention_bwd(const void* Q, const void* K, const void* V, const void* dO,
-                           const float* LSE, int64_t T, int64_t S, int H, int Hkv, int head_dim,
-                           float* dQ, float* dK, float* dV, void* ws, size_t ws_bytes,
-                           hipStream_t st) {
+                           const float* LSE, const float* pstat, int64_t T, int64_t S, int H,
+                           int Hkv, int head_dim, int softmax_bits, float* dQ, float* dK, float* dV,
+                           void* ws, size_t ws_bytes, hipStream_t st) {
   OQ_REQ(Q && K && V && dO && LSE && dQ && dK && dV, "every tensor is required");
   OQ_REQ(aligned16(Q) && aligned16(K) && aligned16(V) && aligned16(dO),
          "pointers must be 16-byte aligned");
+  OQ_REQ(softmax_bits == 16 || (softmax_bits >= 2 && softmax_bits <= 8), "softmax bits %d",
+         softmax_bits);
+  OQ_REQ(softmax_bits == 16 || (pstat && aligned16(pstat)),
+         "pstat (16-byte aligned) is required with softmax quantisation");
+  OQ_REQ(!ws || aligned16(ws), "workspace must be 16-byte aligned");
   if (!attn_supported(T, int(S), H, Hkv, head_dim) || S > INT32_MAX)
     return fail(OQ_ERR_UNSUPPORTED, "attention shape T=%lld S=%lld H=%d Hkv=%d d=%d", (long long)T,
                 (long long)S, H, Hkv, head_dim);
   size_t need = 0;
-  oq_attention_bwd_workspace_size(T, H, &need);
+  oq_attention_bwd_workspace_size(T, H, softmax_bits, &need);
   if (!ws || ws_bytes < need) return fail(OQ_ERR_WORKSPACE, "workspace of %zu bytes needed", need);
   ProfScope ps(PK_ATTN_BWD, st, 4.0 * double(T) * S * H * head_dim);   // dV, dP, dQ, dK (causal halves)
-  OQ_HIP(attn_bwd(Q, K, V, dO, LSE, T, int(S), H, Hkv, head_dim, static_cast<float*>(ws), dQ, dK, dV,
-                  st),
+  OQ_HIP(attn_bwd(Q, K, V, dO, LSE, pstat, T, int(S), H, Hkv, head_dim, softmax_bits,
+                  static_cast<float*>(ws), dQ, dK, dV, st),
          "attention backward");
   return OQ_OK;
 }
@@ -2013,8 +2030,8 @@ oq_status oq_llama_block_step(const oq_llama_desc* d, const void* h0, const void
   OQ_HIP(scale_to_bf16(w.dxt, let ? p->s[1] : nullptr, T, m.Hd, w.datt16, st), "dO");
   {
     ProfScope ps(PK_ATTN_BWD, st, 4.0 * double(T) * m.S * m.Hd);   // dV, dP, dQ, dK (causal halves)
-    OQ_HIP(attn_bwd(w.qh, w.kh, w.vh, w.datt16, w.lse, T, int(m.S), int(m.H), int(m.Hkv),
-                    int(m.dh), w.Dl, w.dQ, w.dK, w.dV, st),
+    OQ_HIP(attn_bwd(w.qh, w.kh, w.vh, w.datt16, w.lse, w.pstat, T, int(m.S), int(m.H),
+                    int(m.Hkv), int(m.dh), m.pb, w.Dl, w.dQ, w.dK, w.dV, st),
            "attention backward");
   }
   {

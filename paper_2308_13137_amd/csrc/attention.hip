@@ -243,6 +243,164 @@ __global__ __launch_bounds__(ANT) void attn_fwd_kernel(const bf16raw* __restrict
   if (fk == 0) LSE[int64_t(h) * T + row0 + qrow] = m + log2f(l);
 }
 
+// ------------------------------------------------------------------ forward, quantised softmax
+// The ablation on softmax quantisation: every query row of probabilities
+// goes through Q_a (per-row asymmetric MinMax, the activation quantiser's
+// fp32 order) before the product with V.  A row's range must be known before
+// any of its values is quantised, so the kernel sweeps the key tiles twice:
+// the first forms LSE (integral running maximum, as the forward above) and
+// the extreme logits, the second recomputes P = 2^(t - LSE), quantises it
+// with the row's (max, min) and accumulates O = sum P^ V (no renormalisation:
+// P^ approximates the normalised row).  Row record pstat [H, T, 4]:
+// (max P, min P, lowest index holding each) -- the masked entries of a row
+// are zeros, so every row but a sample's last has min 0.
+template <int DH>
+__global__ __launch_bounds__(ANT) void attn_fwd_q_kernel(const bf16raw* __restrict__ Q,
+                                                         const bf16raw* __restrict__ K,
+                                                         const bf16raw* __restrict__ V, int S,
+                                                         int H, int Hkv, int p_bits,
+                                                         float* __restrict__ O,
+                                                         float* __restrict__ LSE,
+                                                         float4* __restrict__ pstat, int64_t T) {
+  constexpr int KS = DH / 32, JD = DH / 16, NR = AT * DH / 8 / ANT;
+  __shared__ uint4 sK[AT * DH / 8];
+  __shared__ uint4 sV[AT * DH / 8];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int fr = lane & 15, fk = lane >> 4;
+  const int ntile = S / AT;
+  const int qt = ntile - 1 - int(blockIdx.x);
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int g = h / (H / Hkv);
+  const int64_t ldq = int64_t(H) * DH, ldk = int64_t(Hkv) * DH;
+  const int64_t row0 = int64_t(b) * S;
+  const int qrow = qt * AT + 16 * wave + fr;
+  const float sc = 1.4426950408889634f / sqrtf(float(DH));
+  const float qmax = float((1 << p_bits) - 1);
+
+  bf16x8_t qf[KS];
+  {
+    const bf16raw* qp = Q + (row0 + qrow) * ldq + int64_t(h) * DH;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qf[ks] = bits_as_bf16x8(*reinterpret_cast<const uint4*>(qp + 32 * ks + 8 * fk));
+  }
+  f32x4_t acc[JD];
+#pragma unroll
+  for (int j = 0; j < JD; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m = -INFINITY, l = 0.f, smax = -INFINITY, smin = INFINITY, lse = 0.f;
+  QParams prm{};
+  float pmx = 0.f, pmn = 0.f;
+  int amax = INT_MAX, amin = INT_MAX;
+  u32x4_t kr[NR], vr[NR];
+  const int nk = qt + 1;
+  auto fetch = [&](int t) {
+    const int64_t krow = row0 + int64_t(t) * AT;
+    tile_to_regs<DH>(kr, K + krow * ldk + int64_t(g) * DH, ldk, tid);
+    tile_to_regs<DH>(vr, V + krow * ldk + int64_t(g) * DH, ldk, tid);
+  };
+  fetch(0);
+  for (int it = 0; it < 2 * nk; ++it) {
+    const int kt = it < nk ? it : it - nk;
+    __syncthreads();
+    regs_to_k<DH>(sK, kr, tid);
+    regs_to_v<DH>(sV, vr, tid);
+    __syncthreads();
+    fetch(kt + 1 < nk ? kt + 1 : 0);
+    f32x4_t st[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      st[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        st[i] = mfma(read_rm<DH>(sK, 16 * i + fr, 4 * ks + fk), qf[ks], st[i]);
+    }
+    if (kt == qt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (kt * AT + 16 * i + 4 * fk + r > qrow) st[i][r] = -INFINITY;
+    }
+    if (it < nk) {
+      // sweep 1: LSE as the forward forms it, and the row's extreme logits
+      float mt = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          mt = fmaxf(mt, st[i][r]);
+          if (st[i][r] != -INFINITY) smin = fminf(smin, st[i][r]);
+        }
+      smax = fmaxf(smax, mt);
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float mn_ = fmaxf(m, ceilf(mt * sc));
+      float ls = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ls += __builtin_amdgcn_exp2f(fmaf(st[i][r], sc, -mn_));
+      ls += __shfl_xor(ls, 16);
+      ls += __shfl_xor(ls, 32);
+      l = (m == -INFINITY ? 0.0f : l * ldexpf(1.0f, int(m - mn_))) + ls;
+      m = mn_;
+      if (it == nk - 1) {
+        smax = fmaxf(smax, __shfl_xor(smax, 16));
+        smax = fmaxf(smax, __shfl_xor(smax, 32));
+        smin = fminf(smin, __shfl_xor(smin, 16));
+        smin = fminf(smin, __shfl_xor(smin, 32));
+        lse = m + log2f(l);
+        // the row's extreme probabilities, computed as each element's is
+        pmx = __builtin_amdgcn_exp2f(fmaf(smax, sc, -lse));
+        pmn = qrow < S - 1 ? 0.0f : __builtin_amdgcn_exp2f(fmaf(smin, sc, -lse));
+        prm = make_qparams(pmx, pmn, 1.0f, 1.0f, qmax);
+      }
+      continue;
+    }
+    // sweep 2: P, its quantisation, and O += P^ V
+    bf16x8_t pb[2];
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = 2 * k2 + (e >> 1), r0 = 2 * (e & 1);
+        float pq[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(st[i][r0 + c], sc, -lse));
+          const int key = kt * AT + 16 * i + 4 * fk + r0 + c;
+          if (p == pmx) amax = min(amax, key);
+          if (p == pmn) amin = min(amin, key);
+          pq[c] = dequant(quant_elem(p, prm, qmax).q, prm);
+        }
+        w[e] = pack2(pq[0], pq[1]);
+      }
+      pb[k2] = bits_as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+    }
+#pragma unroll
+    for (int j = 0; j < JD; ++j)
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) acc[j] = mfma(v_frag<DH>(sV, j, k2, lane), pb[k2], acc[j]);
+  }
+  amax = min(amax, __shfl_xor(amax, 16));
+  amax = min(amax, __shfl_xor(amax, 32));
+  amin = min(amin, __shfl_xor(amin, 16));
+  amin = min(amin, __shfl_xor(amin, 32));
+  // a masked key past the visited tiles is the first zero if none came before
+  if (amin == INT_MAX) amin = qrow + 1;
+  float* op = O + (row0 + qrow) * ldq + int64_t(h) * DH;
+#pragma unroll
+  for (int j = 0; j < JD; ++j)
+    *reinterpret_cast<float4*>(op + 16 * j + 4 * fk) =
+        make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+  if (fk == 0) {
+    LSE[int64_t(h) * T + row0 + qrow] = lse;
+    pstat[int64_t(h) * T + row0 + qrow] =
+        make_float4(pmx, pmn, __int_as_float(amax), __int_as_float(amin));
+  }
+}
+
 // ------------------------------------------------------------------ backward
 // Operands the backward needs transposed are read from the row-major tiles
 // with ds_read_b64_tr_b16: lane i of a 16-lane group receives rows
@@ -287,11 +445,15 @@ OQ_DEV bf16x8_t t16_frag(const bf16raw* t, int kb, int lane) {
 // and accumulates over every query tile and query head of its group (S^T and
 // dP^T recomputed from LSE and D).  P^T and dS^T pass through the wave's
 // staging tiles, query-major, to become A operands.
-template <int DH>
-__global__ __launch_bounds__(ANT, 2) void attn_bwd_dkv_kernel(
+// QP (softmax quantisation): P^ (the quantised row) enters dV, and dP goes
+// through Q_a's straight-through rule: dP = m dP^ plus the routed gradients of
+// the row's max and min (from the dQ kernel's first sweep).
+template <int DH, bool QP>
+__global__ __launch_bounds__(ANT, QP ? 1 : 2) void attn_bwd_dkv_kernel(
     const bf16raw* __restrict__ Q, const bf16raw* __restrict__ K, const bf16raw* __restrict__ V,
     const bf16raw* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ Dl,
-    int S, int H, int Hkv, int64_t T, float* __restrict__ dK, float* __restrict__ dV) {
+    int S, int H, int Hkv, int64_t T, float* __restrict__ dK, float* __restrict__ dV,
+    int p_bits, const float4* __restrict__ pstat, const float2* __restrict__ dmm) {
   constexpr int KS = DH / 32, JD = DH / 16, NR = AT * DH / 8 / ANT;
   __shared__ uint4 sQ[AT * DH / 8];
   __shared__ uint4 sdO[AT * DH / 8];
@@ -299,6 +461,12 @@ __global__ __launch_bounds__(ANT, 2) void attn_bwd_dkv_kernel(
   __shared__ __attribute__((aligned(16))) bf16raw sH[4][AT * TS];
   __shared__ __attribute__((aligned(16))) bf16raw sLo[4][AT * TS];
   __shared__ float sL[AT], sD[AT];
+  // QP: per query row h, 1/h, z of Q_a, the routed max / min gradients and
+  // the indices that take them
+  __shared__ float sQh[QP ? AT : 1], sQr[QP ? AT : 1], sQz[QP ? AT : 1];
+  __shared__ float sDmx[QP ? AT : 1], sDmn[QP ? AT : 1];
+  __shared__ int sAmx[QP ? AT : 1], sAmn[QP ? AT : 1];
+  const float qmax = QP ? float((1 << p_bits) - 1) : 0.0f;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int fr = lane & 15, fk = lane >> 4;
   const int ntile = S / AT;
@@ -329,6 +497,8 @@ __global__ __launch_bounds__(ANT, 2) void attn_bwd_dkv_kernel(
   // registers holding the next (query head, query tile)'s Q, dO, LSE and D
   u32x4_t qr[NR], dr[NR];
   float lr = 0.f, dlr = 0.f;
+  float4 psr{};
+  float2 dmr{};
   auto fetch = [&](int it) {
     const int hq = g * grp + it / nq, qt = kt + it % nq;
     const int64_t qrow0 = row0 + int64_t(qt) * AT;
@@ -337,6 +507,10 @@ __global__ __launch_bounds__(ANT, 2) void attn_bwd_dkv_kernel(
     if (tid < AT) {
       lr = LSE[int64_t(hq) * T + qrow0 + tid];
       dlr = Dl[int64_t(hq) * T + qrow0 + tid];
+      if constexpr (QP) {
+        psr = pstat[int64_t(hq) * T + qrow0 + tid];
+        dmr = dmm[int64_t(hq) * T + qrow0 + tid];
+      }
     }
   };
   fetch(0);
@@ -351,6 +525,16 @@ __global__ __launch_bounds__(ANT, 2) void attn_bwd_dkv_kernel(
     if (tid < AT) {
       sL[tid] = lr;
       sD[tid] = dlr;
+      if constexpr (QP) {
+        const QParams prm = make_qparams(psr.x, psr.y, 1.0f, 1.0f, qmax);
+        sQh[tid] = prm.h;
+        sQr[tid] = prm.r;
+        sQz[tid] = prm.z;
+        sDmx[tid] = dmr.x;
+        sDmn[tid] = dmr.y;
+        sAmx[tid] = __float_as_int(psr.z);
+        sAmn[tid] = __float_as_int(psr.w);
+      }
     }
     __syncthreads();
     fetch(it + 1 < n_it ? it + 1 : it);                 // in flight meanwhile
@@ -374,8 +558,22 @@ __global__ __launch_bounds__(ANT, 2) void attn_bwd_dkv_kernel(
       for (int r = 0; r < 4; ++r) {
         float p = __builtin_amdgcn_exp2f(fmaf(st[jn][r], sc, -L));
         if (diag && 16 * wave + 4 * fk + r > ql) p = 0.0f;
-        st[jn][r] = p;
-        dp[jn][r] = p * (dp[jn][r] - D) * rs;           // dS^T (with the 1/sqrt(d) of the logits)
+        if constexpr (QP) {
+          QParams prm{};
+          prm.h = sQh[ql];
+          prm.r = sQr[ql];
+          prm.z = sQz[ql];
+          const QElem qe = quant_elem(p, prm, qmax);
+          const int key = key_w + 4 * fk + r;
+          float g = qe.m ? dp[jn][r] : 0.0f;
+          if (key == sAmx[ql]) g += sDmx[ql];
+          if (key == sAmn[ql]) g += sDmn[ql];
+          st[jn][r] = dequant(qe.q, prm);               // P^ enters dV
+          dp[jn][r] = p * (g - D) * rs;
+        } else {
+          st[jn][r] = p;
+          dp[jn][r] = p * (dp[jn][r] - D) * rs;         // dS^T (with the 1/sqrt(d) of the logits)
+        }
       }
       // P^T query-major: row = query, four consecutive keys
       t16_put4(tp, ql, 4 * fk, st[jn][0], st[jn][1], st[jn][2], st[jn][3]);
@@ -419,11 +617,17 @@ __global__ __launch_bounds__(ANT, 2) void attn_bwd_dkv_kernel(
 // probabilities the gradients use (so every row of dS sums to zero to fp32
 // rounding) and writes it for the dK/dV kernel; the second sweep accumulates
 // dQ = dS K, dS staged key-major as two bf16 terms.
-template <int DH>
-__global__ __launch_bounds__(ANT, 2) void attn_bwd_dq_kernel(
+// QP (softmax quantisation): the first sweep also forms Q_a's row sums
+// S_h = sum dP^ ((q - z) - m u), S_z = sum dP^ (1 - m) and E = sum P m dP^,
+// hence the row's max / min gradients (written to dmm for the dK/dV kernel)
+// and D = E + max dmax + min dmin; the second sweep's dP follows Q_a's
+// straight-through rule.
+template <int DH, bool QP>
+__global__ __launch_bounds__(ANT, QP ? 1 : 2) void attn_bwd_dq_kernel(
     const bf16raw* __restrict__ Q, const bf16raw* __restrict__ K, const bf16raw* __restrict__ V,
     const bf16raw* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ Dl,
-    int S, int H, int Hkv, int64_t T, float* __restrict__ dQ) {
+    int S, int H, int Hkv, int64_t T, float* __restrict__ dQ, int p_bits,
+    const float4* __restrict__ pstat, float2* __restrict__ dmm) {
   constexpr int KS = DH / 32, JD = DH / 16, NR = AT * DH / 8 / ANT;
   __shared__ uint4 sK[AT * DH / 8];
   __shared__ uint4 sV[AT * DH / 8];
@@ -457,6 +661,21 @@ __global__ __launch_bounds__(ANT, 2) void attn_bwd_dq_kernel(
   for (int r = 0; r < 4; ++r) {
     lse[r] = LSE[int64_t(h) * T + row0 + q_w + 4 * fk + r];
     dl[r] = 0.f;
+  }
+  // QP: per row of this wave, (1/h, z, index of the max, index of the min)
+  // and the max / min gradients once sweep 1 has them, in LDS (not registers)
+  __shared__ float4 sRq[QP ? 4 : 1][16];
+  __shared__ float2 sRg[QP ? 4 : 1][16];
+  const float qmax = QP ? float((1 << p_bits) - 1) : 0.0f;
+  float sh[QP ? 4 : 1], sz[QP ? 4 : 1];
+  if constexpr (QP) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sh[r] = sz[r] = 0.f;
+    if (lane < 16) {
+      const float4 p4 = pstat[int64_t(h) * T + row0 + q_w + lane];
+      const QParams pr = make_qparams(p4.x, p4.y, 1.0f, 1.0f, qmax);
+      sRq[wave][lane] = make_float4(pr.r, pr.z, p4.z, p4.w);
+    }
   }
   f32x4_t adq[JD];
 #pragma unroll
@@ -499,16 +718,46 @@ __global__ __launch_bounds__(ANT, 2) void attn_bwd_dq_kernel(
         st[jn][r] = p;
       }
     if (it < nk) {
-      // sweep 1: D
+      // sweep 1: D (with QP, Q_a's row sums first)
 #pragma unroll
       for (int jn = 0; jn < 4; ++jn)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) dl[r] += st[jn][r] * dp[jn][r];
+        for (int r = 0; r < 4; ++r) {
+          if constexpr (QP) {
+            const float4 rq = sRq[wave][4 * fk + r];
+            QParams pr{};
+            pr.r = rq.x;
+            pr.z = rq.y;
+            const QElem qe = quant_elem(st[jn][r], pr, qmax);
+            const float t = qe.q - pr.z;
+            sh[r] += dp[jn][r] * (qe.m ? t - qe.u : t);
+            sz[r] += qe.m ? 0.0f : dp[jn][r];
+            dl[r] += qe.m ? st[jn][r] * dp[jn][r] : 0.0f;
+          } else {
+            dl[r] += st[jn][r] * dp[jn][r];
+          }
+        }
       if (it == nk - 1) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
 #pragma unroll
           for (int o = 1; o < 16; o <<= 1) dl[r] += __shfl_xor(dl[r], o);
+          if constexpr (QP) {
+#pragma unroll
+            for (int o = 1; o < 16; o <<= 1) {
+              sh[r] += __shfl_xor(sh[r], o);
+              sz[r] += __shfl_xor(sz[r], o);
+            }
+            const int64_t ri = int64_t(h) * T + row0 + q_w + 4 * fk + r;
+            const float4 p4 = pstat[ri];
+            const QParams pr = make_qparams(p4.x, p4.y, 1.0f, 1.0f, qmax);
+            const QGrad qg = quant_group_grad(sh[r], sz[r], p4.x, p4.y, pr, qmax);
+            dl[r] += p4.x * qg.dmx + p4.y * qg.dmn;
+            if (fr == 0) {
+              sRg[wave][4 * fk + r] = make_float2(qg.dmx, qg.dmn);
+              dmm[ri] = make_float2(qg.dmx, qg.dmn);
+            }
+          }
         }
         if (fr == 0) {
 #pragma unroll
@@ -525,7 +774,20 @@ __global__ __launch_bounds__(ANT, 2) void attn_bwd_dq_kernel(
       float v[4], hi[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        v[r] = st[jn][r] * (dp[jn][r] - dl[r]) * rs;
+        float gp = dp[jn][r];
+        if constexpr (QP) {
+          const float4 rq = sRq[wave][4 * fk + r];
+          const float2 rg = sRg[wave][4 * fk + r];
+          QParams pr{};
+          pr.r = rq.x;
+          pr.z = rq.y;
+          const QElem qe = quant_elem(st[jn][r], pr, qmax);
+          const int key = kt * AT + 16 * jn + fr;
+          gp = qe.m ? gp : 0.0f;
+          if (key == __float_as_int(rq.z)) gp += rg.x;
+          if (key == __float_as_int(rq.w)) gp += rg.y;
+        }
+        v[r] = st[jn][r] * (gp - dl[r]) * rs;
         hi[r] = bf2f(f2bf(v[r]));
       }
       t16_put4(th, 16 * jn + fr, 4 * fk, hi[0], hi[1], hi[2], hi[3]);
@@ -552,27 +814,47 @@ __global__ __launch_bounds__(ANT, 2) void attn_bwd_dq_kernel(
 
 template <int DH>
 hipError_t attn_fwd_t(const void* Q, const void* K, const void* V, int64_t T, int S, int H,
-                      int Hkv, float* O, float* LSE, hipStream_t st) {
+                      int Hkv, int p_bits, float* O, float* LSE, float4* pstat, hipStream_t st) {
   const dim3 grid(unsigned(S / AT), unsigned(H), unsigned(T / S));
-  hipLaunchKernelGGL(attn_fwd_kernel<DH>, grid, dim3(ANT), 0, st, static_cast<const bf16raw*>(Q),
-                     static_cast<const bf16raw*>(K), static_cast<const bf16raw*>(V), S, H, Hkv, O,
-                     LSE, T);
+  const auto q = static_cast<const bf16raw*>(Q);
+  const auto k = static_cast<const bf16raw*>(K);
+  const auto v = static_cast<const bf16raw*>(V);
+  if (p_bits < 16)
+    hipLaunchKernelGGL(attn_fwd_q_kernel<DH>, grid, dim3(ANT), 0, st, q, k, v, S, H, Hkv, p_bits,
+                       O, LSE, pstat, T);
+  else
+    hipLaunchKernelGGL(attn_fwd_kernel<DH>, grid, dim3(ANT), 0, st, q, k, v, S, H, Hkv, O, LSE, T);
   return hipGetLastError();
+}
+
+template <int DH, bool QP>
+void attn_bwd_launch(const void* Q, const void* K, const void* V, const void* dO,
+                     const float* LSE, const float4* pstat, int64_t T, int S, int H, int Hkv,
+                     int p_bits, float* Dl, float2* dmm, float* dQ, float* dK, float* dV,
+                     hipStream_t st) {
+  const auto q = static_cast<const bf16raw*>(Q);
+  const auto k = static_cast<const bf16raw*>(K);
+  const auto v = static_cast<const bf16raw*>(V);
+  const auto o = static_cast<const bf16raw*>(dO);
+  // dQ first: it also writes D (and, quantised, the max / min gradients),
+  // which the dK/dV kernel reads
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<DH, QP>), dim3(unsigned(S / AT), unsigned(H), unsigned(T / S)),
+                     dim3(ANT), 0, st, q, k, v, o, LSE, Dl, S, H, Hkv, T, dQ, p_bits, pstat, dmm);
+  hipLaunchKernelGGL((attn_bwd_dkv_kernel<DH, QP>), dim3(unsigned(S / AT), unsigned(Hkv), unsigned(T / S)),
+                     dim3(ANT), 0, st, q, k, v, o, LSE, Dl, S, H, Hkv, T, dK, dV, p_bits, pstat,
+                     dmm);
 }
 
 template <int DH>
 hipError_t attn_bwd_t(const void* Q, const void* K, const void* V, const void* dO,
-                      const float* LSE, int64_t T, int S, int H, int Hkv, float* Dl, float* dQ,
-                      float* dK, float* dV, hipStream_t st) {
-  // dQ first: it also writes D, which the dK/dV kernel reads
-  hipLaunchKernelGGL(attn_bwd_dq_kernel<DH>, dim3(unsigned(S / AT), unsigned(H), unsigned(T / S)),
-                     dim3(ANT), 0, st, static_cast<const bf16raw*>(Q), static_cast<const bf16raw*>(K),
-                     static_cast<const bf16raw*>(V), static_cast<const bf16raw*>(dO), LSE, Dl, S, H,
-                     Hkv, T, dQ);
-  hipLaunchKernelGGL(attn_bwd_dkv_kernel<DH>, dim3(unsigned(S / AT), unsigned(Hkv), unsigned(T / S)),
-                     dim3(ANT), 0, st, static_cast<const bf16raw*>(Q), static_cast<const bf16raw*>(K),
-                     static_cast<const bf16raw*>(V), static_cast<const bf16raw*>(dO), LSE, Dl, S, H,
-                     Hkv, T, dK, dV);
+                      const float* LSE, const float4* pstat, int64_t T, int S, int H, int Hkv,
+                      int p_bits, float* ws, float* dQ, float* dK, float* dV, hipStream_t st) {
+  float2* dmm = reinterpret_cast<float2*>(ws + T * H);
+  if (p_bits < 16)
+    attn_bwd_launch<DH, true>(Q, K, V, dO, LSE, pstat, T, S, H, Hkv, p_bits, ws, dmm, dQ, dK, dV, st);
+  else
+    attn_bwd_launch<DH, false>(Q, K, V, dO, LSE, nullptr, T, S, H, Hkv, 16, ws, nullptr, dQ, dK, dV,
+                               st);
   return hipGetLastError();
 }
 
@@ -583,19 +865,25 @@ bool attn_supported(int64_t T, int S, int H, int Hkv, int dh) {
          Hkv > 0 && H % Hkv == 0 && T / S <= 65535 && H <= 65535;
 }
 
+size_t attn_bwd_ws_floats(int64_t T, int H, int p_bits) {
+  return size_t(T) * size_t(H) * (p_bits < 16 ? 3 : 1);
+}
+
 hipError_t attn_fwd(const void* Q, const void* K, const void* V, int64_t T, int S, int H, int Hkv,
-                    int dh, float* O, float* LSE, hipStream_t st) {
+                    int dh, int p_bits, float* O, float* LSE, float* pstat, hipStream_t st) {
   if (!attn_supported(T, S, H, Hkv, dh)) return hipErrorInvalidValue;
-  return dh == 128 ? attn_fwd_t<128>(Q, K, V, T, S, H, Hkv, O, LSE, st)
-                   : attn_fwd_t<64>(Q, K, V, T, S, H, Hkv, O, LSE, st);
+  float4* ps = reinterpret_cast<float4*>(pstat);
+  return dh == 128 ? attn_fwd_t<128>(Q, K, V, T, S, H, Hkv, p_bits, O, LSE, ps, st)
+                   : attn_fwd_t<64>(Q, K, V, T, S, H, Hkv, p_bits, O, LSE, ps, st);
 }
 
 hipError_t attn_bwd(const void* Q, const void* K, const void* V, const void* dO, const float* LSE,
-                    int64_t T, int S, int H, int Hkv, int dh, float* Dl, float* dQ, float* dK,
-                    float* dV, hipStream_t st) {
+                    const float* pstat, int64_t T, int S, int H, int Hkv, int dh, int p_bits,
+                    float* ws, float* dQ, float* dK, float* dV, hipStream_t st) {
   if (!attn_supported(T, S, H, Hkv, dh)) return hipErrorInvalidValue;
-  return dh == 128 ? attn_bwd_t<128>(Q, K, V, dO, LSE, T, S, H, Hkv, Dl, dQ, dK, dV, st)
-                   : attn_bwd_t<64>(Q, K, V, dO, LSE, T, S, H, Hkv, Dl, dQ, dK, dV, st);
+  const float4* ps = reinterpret_cast<const float4*>(pstat);
+  return dh == 128 ? attn_bwd_t<128>(Q, K, V, dO, LSE, ps, T, S, H, Hkv, p_bits, ws, dQ, dK, dV, st)
+                   : attn_bwd_t<64>(Q, K, V, dO, LSE, ps, T, S, H, Hkv, p_bits, ws, dQ, dK, dV, st);
 }
 
 }  // namespace oq

@@ -211,12 +211,18 @@ hipError_t let_init_finish(int64_t C, int64_t T, const float* ax_parts, int64_t 
 // ---------------------------------------------------------------- whole-block pieces
 // Causal attention (bf16 matrix cores), head_dim 64 or 128, S a multiple of 64.
 bool attn_supported(int64_t T, int S, int H, int Hkv, int dh);
+// p_bits < 16: each query row of probabilities goes through Q_a before the
+// product with V; pstat [H, T] float4 = (max P, min P, their lowest indices as
+// int bits) is written by the forward and read by the backward.
 hipError_t attn_fwd(const void* Q, const void* K, const void* V, int64_t T, int S, int H, int Hkv,
-                    int dh, float* O, float* LSE, hipStream_t st);
-// Dl [H, T] scratch (D = sum_j P_ij dP_ij); dQ [T, H dh], dK, dV [T, Hkv dh] fp32 outputs.
+                    int dh, int p_bits, float* O, float* LSE, float* pstat, hipStream_t st);
+// ws: attn_bwd_ws_floats fp32 scratch (D = sum_j P_ij dP_ij per query row, and
+// with p_bits < 16 the row's max / min gradients); dQ [T, H dh], dK, dV
+// [T, Hkv dh] fp32 outputs.
+size_t attn_bwd_ws_floats(int64_t T, int H, int p_bits);
 hipError_t attn_bwd(const void* Q, const void* K, const void* V, const void* dO, const float* LSE,
-                    int64_t T, int S, int H, int Hkv, int dh, float* Dl, float* dQ, float* dK,
-                    float* dV, hipStream_t st);
+                    const float* pstat, int64_t T, int S, int H, int Hkv, int dh, int p_bits,
+                    float* ws, float* dQ, float* dK, float* dV, hipStream_t st);
 hipError_t rmsnorm_fwd(const void* h, bool h_bf16, const float* g, int64_t T, int64_t D, float eps,
                        float* x, float* rstd, hipStream_t st);
 hipError_t rmsnorm_bwd(const void* h, bool h_bf16, const float* g, const float* rstd,

@@ -1144,7 +1144,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
             const float t = qe.q - p.z;
             const float th = qe.m ? t - qe.u : t;
             sums.x += g[k][e] * th;
-            if (!qe.m) sums.y += g[k][e];
+            sums.y += qe.m ? 0.0f : g[k][e];
           }
         }
       }

@@ -614,9 +614,10 @@ def profile_read():
 
 # ------------------------------------------------------------------ whole LLaMA block
 _SIGS_LLAMA = {
-    "oq_attention_fwd": (_I, [_P, _P, _P, _I64, _I64, _I, _I, _I, _P, _P, _P]),
-    "oq_attention_bwd_workspace_size": (_I, [_I64, _I, _PSZ]),
-    "oq_attention_bwd": (_I, [_P, _P, _P, _P, _P, _I64, _I64, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]),
+    "oq_attention_fwd": (_I, [_P, _P, _P, _I64, _I64, _I, _I, _I, _I, _P, _P, _P, _P]),
+    "oq_attention_bwd_workspace_size": (_I, [_I64, _I, _I, _PSZ]),
+    "oq_attention_bwd": (_I, [_P, _P, _P, _P, _P, _P, _I64, _I64, _I, _I, _I, _I, _P, _P, _P, _P, _SZ,
+                              _P]),
     "oq_llama_workspace_size": (_I, [_P, _PSZ]),
     "oq_llama_block_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "oq_llama_block_forward": (_I, [_P, _P, _P, _I, _P, _P, _SZ, _P]),
@@ -629,7 +630,8 @@ class LlamaDesc(C.Structure):
     _fields_ = [("tokens", C.c_int64), ("seq_len", C.c_int64), ("hidden", C.c_int64),
                 ("ffn", C.c_int64), ("heads", C.c_int), ("kv_heads", C.c_int),
                 ("norm_eps", C.c_float), ("rope_base", C.c_float), ("w_bits", C.c_int * NL),
-                ("w_group", C.c_int64 * NL), ("act_bits", C.c_int), ("let", C.c_int)]
+                ("w_group", C.c_int64 * NL), ("act_bits", C.c_int), ("let", C.c_int),
+                ("softmax_bits", C.c_int)]
 
 
 class LlamaParams(C.Structure):
@@ -653,20 +655,24 @@ class LlamaOptim(C.Structure):
                 ("wd", C.c_double)]
 
 
-def attention_fwd(Q, K, V, S, H, Hkv, stream=None):
-    """Causal attention over bf16 Q [T, H d], K, V [T, Hkv d].  Returns (O, LSE)."""
+def attention_fwd(Q, K, V, S, H, Hkv, softmax_bits=16, stream=None):
+    """Causal attention over bf16 Q [T, H d], K, V [T, Hkv d].  Returns
+    (O, LSE, pstat); pstat [H, T, 4] (the quantised rows' max / min and their
+    indices) only with softmax_bits < 16, else None."""
     T = Q.shape[0]
     d = Q.shape[1] // H
     O = torch.empty((T, H * d), dtype=torch.float32, device=Q.device)
     lse = torch.empty((H, T), dtype=torch.float32, device=Q.device)
-    _check(lib().oq_attention_fwd(_ptr(Q), _ptr(K), _ptr(V), T, S, H, Hkv, d, _ptr(O), _ptr(lse),
-                                  _stream(stream)))
-    return O, lse
+    pstat = (torch.empty((H, T, 4), dtype=torch.float32, device=Q.device)
+             if softmax_bits < 16 else None)
+    _check(lib().oq_attention_fwd(_ptr(Q), _ptr(K), _ptr(V), T, S, H, Hkv, d, softmax_bits,
+                                  _ptr(O), _ptr(lse), _ptr(pstat), _stream(stream)))
+    return O, lse, pstat
 
 
-def attention_bwd(Q, K, V, dO, lse, S, H, Hkv, stream=None):
-    """Gradients of :func:`attention_fwd` for bf16 dO [T, H d], from its LSE.
-    Returns (dQ, dK, dV) fp32."""
+def attention_bwd(Q, K, V, dO, lse, S, H, Hkv, softmax_bits=16, pstat=None, stream=None):
+    """Gradients of :func:`attention_fwd` for bf16 dO [T, H d], from its LSE
+    (and pstat with softmax_bits < 16).  Returns (dQ, dK, dV) fp32."""
     T = Q.shape[0]
     d = Q.shape[1] // H
     f32 = dict(dtype=torch.float32, device=Q.device)
@@ -674,11 +680,11 @@ def attention_bwd(Q, K, V, dO, lse, S, H, Hkv, stream=None):
     dK = torch.empty((T, Hkv * d), **f32)
     dV = torch.empty((T, Hkv * d), **f32)
     n = C.c_size_t(0)
-    _check(lib().oq_attention_bwd_workspace_size(T, H, C.byref(n)))
+    _check(lib().oq_attention_bwd_workspace_size(T, H, softmax_bits, C.byref(n)))
     ws = torch.empty(n.value, dtype=torch.uint8, device=Q.device)
-    _check(lib().oq_attention_bwd(_ptr(Q), _ptr(K), _ptr(V), _ptr(dO), _ptr(lse), T, S, H, Hkv, d,
-                                  _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), n.value,
-                                  _stream(stream)))
+    _check(lib().oq_attention_bwd(_ptr(Q), _ptr(K), _ptr(V), _ptr(dO), _ptr(lse), _ptr(pstat), T,
+                                  S, H, Hkv, d, softmax_bits, _ptr(dQ), _ptr(dK), _ptr(dV),
+                                  _ptr(ws), n.value, _stream(stream)))
     return dQ, dK, dV
 
 
@@ -688,7 +694,7 @@ class LlamaBlock:
     Linears in the order q, k, v, o, gate, up, down."""
 
     def __init__(self, T, seq_len, hidden, heads, kv_heads, ffn, w_bits, w_group, act_bits=16,
-                 let=False, norm_eps=1e-6, rope_base=10000.0, device="cuda"):
+                 let=False, norm_eps=1e-6, rope_base=10000.0, softmax_bits=16, device="cuda"):
         d = LlamaDesc()
         d.tokens, d.seq_len, d.hidden, d.ffn = T, seq_len, hidden, ffn
         d.heads, d.kv_heads = heads, kv_heads
@@ -696,6 +702,7 @@ class LlamaBlock:
         for l in range(NL):
             d.w_bits[l], d.w_group[l] = w_bits[l], w_group[l]
         d.act_bits, d.let = act_bits, int(bool(let))
+        d.softmax_bits = softmax_bits
         self.desc, self.device, self.let = d, device, bool(let)
         self.T, self.D, self.H, self.Hkv, self.F = T, hidden, heads, kv_heads, ffn
         dh = hidden // heads

@@ -44,6 +44,25 @@ def may_round_apart(x, eps):
     return (x > 0) & (np.abs(lo - 0x8000) <= eps * 2.0 ** 24 + 1)
 
 
+def logit_error(Q, K, d, S):
+    """Base-2 logits t of one head and sample, the bound dt on their fp32
+    error, and the bound eps_p on the relative error of P = 2^(t - LSE) as
+    the backward recomputes it (see attention_bounds)."""
+    l2e, ln2, rs = np.log2(np.e), np.log(2.0), 1.0 / np.sqrt(d)
+    gd, gS = (d + 4) * U, (S + 4) * U
+    mask = np.triu(np.ones((S, S), bool), 1)
+    t = np.where(mask, -np.inf, Q @ K.T * (l2e * rs))
+    t0 = np.where(mask, 0, t)
+    dt = np.where(mask, 0.0, gd * (np.abs(Q) @ np.abs(K).T) * l2e * rs + 2 * U * np.abs(t0))
+    eps_w = ln2 * dt + 4 * U
+    m0 = np.max(t, axis=1, keepdims=True)
+    l0 = np.sum(np.exp2(t - m0), axis=1, keepdims=True)
+    lse = m0 + np.log2(l0)
+    dlse = (gS + np.max(eps_w, axis=1, keepdims=True)) / ln2 + 2 * U * (np.abs(lse) + 1)
+    eps_p = ln2 * (dt + dlse + U * (np.abs(t0) + np.abs(lse))) + 4 * U
+    return t, dt, lse, eps_p
+
+
 def attention_bounds(q, k, v, do, H, Hkv, d, S):
     """Per-element bounds on |GPU - oracle| for the attention forward (O) and
     backward (dQ, dK, dV), derived from the kernels' arithmetic:
@@ -62,9 +81,8 @@ def attention_bounds(q, k, v, do, H, Hkv, d, S):
     Second-order terms are left to the factor 2 the test applies."""
     T = q.shape[0]
     ns, grp = T // S, H // Hkv
-    l2e, ln2, rs = np.log2(np.e), np.log(2.0), 1.0 / np.sqrt(d)
+    ln2, rs = np.log(2.0), 1.0 / np.sqrt(d)
     gd, gS, gG = (d + 4) * U, (S + 4) * U, (2 * grp * S + 4) * U
-    mask = np.triu(np.ones((S, S), bool), 1)
     bO, bdQ = np.zeros((T, H * d)), np.zeros((T, H * d))
     bdK, bdV = np.zeros((T, Hkv * d)), np.zeros((T, Hkv * d))
     for b in range(ns):
@@ -74,8 +92,7 @@ def attention_bounds(q, k, v, do, H, Hkv, d, S):
             cq, ck = slice(h * d, (h + 1) * d), slice(g * d, (g + 1) * d)
             Q, K, V, dO = q[r, cq], k[r, ck], v[r, ck], do[r, cq]
             aq, ak, av, ado = np.abs(Q), np.abs(K), np.abs(V), np.abs(dO)
-            t = np.where(mask, -np.inf, Q @ K.T * (l2e * rs))
-            dt = np.where(mask, 0.0, gd * (aq @ ak.T) * l2e * rs + 2 * U * np.abs(np.where(mask, 0, t)))
+            t, dt, lse, eps_p = logit_error(Q, K, d, S)
             M = np.ceil(np.max(t, axis=1, keepdims=True))
             w = np.exp2(t - M)
             eps_w = ln2 * dt + 4 * U
@@ -86,12 +103,7 @@ def attention_bounds(q, k, v, do, H, Hkv, d, S):
             bO[r, cq] = (gS * (wb @ av) + np.abs(O) * gS * Lw + fw @ av + np.sum(fw, 1, keepdims=True)
                          * np.abs(O)) / Lw + 2 * U * np.abs(O)
             # backward
-            m0 = np.max(t, axis=1, keepdims=True)
-            l0 = np.sum(np.exp2(t - m0), axis=1, keepdims=True)
-            lse = m0 + np.log2(l0)
             P = np.exp2(t - lse)
-            dlse = (gS + np.max(eps_w, axis=1, keepdims=True)) / ln2 + 2 * U * (np.abs(lse) + 1)
-            eps_p = ln2 * (dt + dlse + U * (np.abs(np.where(mask, 0, t)) + np.abs(lse))) + 4 * U
             dP = dO @ V.T
             ddP = gd * (ado @ av.T)
             D = np.sum(P * dP, axis=1, keepdims=True)
@@ -132,8 +144,8 @@ def test_attention_kernels(c):
         v = 0.1 * v + rng.standard_normal(Hkv * d) * 2.0
     q, k, v = bf16_exact(q), bf16_exact(k), bf16_exact(v)
     out, P, _ = lb.attention(q, k, v, H, Hkv, d, S, bf16=True)
-    O, lse = oq.attention_fwd(dev(q, torch.bfloat16), dev(k, torch.bfloat16), dev(v, torch.bfloat16),
-                              S, H, Hkv)
+    O, lse, _ = oq.attention_fwd(dev(q, torch.bfloat16), dev(k, torch.bfloat16),
+                                 dev(v, torch.bfloat16), S, H, Hkv)
     # the statistic in natural log: ln sum_k exp(q.k / sqrt(d))
     ns = T // S
     s = np.einsum("bqhd,bkhd->bhqk", q.reshape(ns, S, H, d),
@@ -159,14 +171,117 @@ def test_attention_kernels(c):
     assert all(ratios[n] <= 1.0 for n in ("O", "dQ", "dK", "dV")), ratios
 
 
+QATT_CASES = [dict(S=128, ns=2, H=2, Hkv=1, d=128, bits=4), dict(S=64, ns=2, H=4, Hkv=2, d=64, bits=6),
+              dict(S=256, ns=1, H=2, Hkv=2, d=128, bits=8), dict(S=192, ns=1, H=2, Hkv=1, d=64, bits=2)]
+P_EPS = 1e-5    # decision margin: relative difference of the two sides' probabilities
+
+
+def decision_margins(st, qmax, eps=P_EPS):
+    """Where two sides whose probabilities (and so each row's max and min)
+    agree within relative eps may quantise differently: ``near`` [rows, S]
+    marks elements whose u = P / h lies within 2 eps u of a rounding midpoint
+    (their codes may differ by one step), ``zrow`` rows whose zero point
+    b / h does, ``lvl`` [rows, S] the bf16 ulp of each element's dequantised
+    level k h where that level lies within 2 eps of a bf16 rounding midpoint
+    (both sides round P^ to bf16 for the matrix cores), else 0."""
+    u = np.asarray(st["u"], np.float64)
+    near = np.abs(u - np.floor(u) - 0.5) <= 2 * eps * u + 1e-6
+    bz = np.asarray(st["b"], np.float64) / np.asarray(st["h"], np.float64)
+    zrow = np.abs(bz - np.floor(bz) - 0.5) <= 2 * eps * np.abs(bz) + 1e-6
+    h = np.asarray(st["h"], np.float64)[:, None]
+    lv = (np.asarray(st["q"], np.float64) - np.asarray(st["z"], np.float64)[:, None]) * h
+    lvl = may_round_apart(lv, 2 * eps) * bf16_ulp(lv)
+    return near, zrow, lvl
+
+
+@pytest.mark.parametrize("c", QATT_CASES, ids=[str(c) for c in QATT_CASES])
+def test_attention_softmax_quantised(c):
+    """The softmax-quantisation ablation: every query row of probabilities
+    through Q_a before the product with V.  Codes are decisions taken in fp32
+    on both sides from probabilities that agree to a few ulps (the recorded
+    row max is held to P_EPS), so an element whose decision lies within that
+    margin of a rounding midpoint (decision_margins) may differ by one
+    quantisation step, or its bf16 level by one ulp.  O is held element by
+    element to the fp32 sums' bound plus those possible differences; dQ rows
+    normwise to 1e-3 (floored at 1e-3 of the head's largest) except in rows
+    holding such an element (at most 10% of
+    rows: the straight-through terms there move with the codes); the
+    per-row record exactly (indices, min 0 of rows with masked keys); dK and
+    dV sum over all query rows and are held normwise (1e-2)."""
+    print(f"quantised attention {c}", flush=True)
+    rng = np.random.default_rng(1000 + c["S"] + 3 * c["bits"])
+    T = c["S"] * c["ns"]
+    H, Hkv, d, S, bits = c["H"], c["Hkv"], c["d"], c["S"], c["bits"]
+    q = bf16_exact(rng.standard_normal((T, H * d)) * 1.5)
+    k = bf16_exact(rng.standard_normal((T, Hkv * d)))
+    v = bf16_exact(rng.standard_normal((T, Hkv * d)))
+    do = bf16_exact(rng.standard_normal((T, H * d)))
+    rec = {}
+    out, P, PH = lb.attention(q, k, v, H, Hkv, d, S, bf16=True, p_bits=bits, rec=rec)
+    dq, dk, dv = lb.attention_bwd(q, k, v, P, do, H, Hkv, d, S, bf16=True, PH=PH, rec=rec)
+    b16 = torch.bfloat16
+    Qd, Kd, Vd = dev(q, b16), dev(k, b16), dev(v, b16)
+    O, lse, pstat = oq.attention_fwd(Qd, Kd, Vd, S, H, Hkv, softmax_bits=bits)
+    gq, gk, gv = oq.attention_bwd(Qd, Kd, Vd, dev(do, b16), lse, S, H, Hkv, softmax_bits=bits,
+                                  pstat=pstat)
+    O, gq, gk, gv = host(O), host(gq), host(gk), host(gv)
+    ps = pstat.cpu()
+    pmax, pmin = ps[..., 0].numpy(), ps[..., 1].numpy()
+    imax = ps[..., 2].contiguous().view(torch.int32).numpy()
+    imin = ps[..., 3].contiguous().view(torch.int32).numpy()
+    qmax = 2 ** bits - 1
+    ns = T // S
+    n_amb = 0
+    worst = dict(O=0.0, dQ=0.0, mx=0.0)
+    for b in range(ns):
+        r = slice(b * S, (b + 1) * S)
+        for h in range(H):
+            st = rec[f"pq{b}_{h}"]
+            cq = slice(h * d, (h + 1) * d)
+            g = h // (H // Hkv)
+            ck = slice(g * d, (g + 1) * d)
+            near, zrow, lvl = decision_margins(st, qmax)
+            amb = np.any(near, axis=1) | zrow
+            n_amb += int(np.sum(amb))
+            ok = ~amb
+            # record: indices of the extremes (lowest on ties) and their values
+            assert np.array_equal(imax[h, r][ok], st["i_mx"][ok])
+            last = S - 1
+            if ok[last]:
+                assert imin[h, b * S + last] == st["i_mn"][last]
+            # rows with masked entries have min 0 (its index is any zero: the
+            # gradient routed there meets P = 0)
+            assert np.all(pmin[h, r][:-1] == 0.0)
+            worst["mx"] = max(worst["mx"], float(np.max(np.abs(pmax[h, r] / st["mx"] - 1))))
+            ph = bf16_exact(PH[b, h]).astype(np.float64)
+            av = np.abs(v[r, ck])
+            hs = np.asarray(st["h"], np.float64)[:, None]
+            flips = (near * (hs + bf16_ulp(ph + hs)) + np.where(zrow[:, None], hs, 0.0) + lvl) @ av
+            bound = 2 * ((S + 4) * U * (np.abs(ph) @ av)) + flips + 1e-7
+            err = np.abs(O[r, cq] - out[r, cq])
+            worst["O"] = max(worst["O"], float(np.max(err / bound)))
+            dqr, gqr = dq[r, cq][ok], gq[r, cq][ok]
+            # (a sample's first query attends to one key: its dQ is 0 exactly)
+            den = np.maximum(np.max(np.abs(dqr), axis=1), 1e-3 * np.max(np.abs(dq[r, cq])))
+            worst["dQ"] = max(worst["dQ"], float(np.max(np.max(np.abs(gqr - dqr), axis=1) / den))
+                              if ok.any() else 0.0)
+    nk, nv = normwise(gk, dk), normwise(gv, dv)
+    print(f"  ambiguous rows {n_amb}/{ns * H * S}  O {worst['O']:.2e}  dQ.row {worst['dQ']:.2e}  "
+          f"max.rel {worst['mx']:.1e}  dK.n {nk:.2e}  dV.n {nv:.2e}", flush=True)
+    assert n_amb <= 0.1 * ns * H * S
+    assert worst["O"] <= 1.0 and worst["dQ"] <= 1e-3 and worst["mx"] <= P_EPS
+    assert nk <= 1e-2 and nv <= 1e-2
+
+
 # ---------------------------------------------------------------- the whole block
-def llama_problem(D, H, Hkv, F, S, ns, bits, groups, act_bits, let, seed):
+def llama_problem(D, H, Hkv, F, S, ns, bits, groups, act_bits, let, seed, softmax_bits=16):
     rng = inputs.rng_for(61, seed, D, F, S)
     T = S * ns
     d = D // H
     desc = dict(hidden=D, heads=H, kv_heads=Hkv, ffn=F, seq_len=S, norm_eps=1e-6,
                 rope_base=10000.0, w_bits=list(bits), w_group=list(groups),
-                act_bits=act_bits & 0xFF, act_sym=bool(act_bits & oq.ACT_SYM), let=let)
+                act_bits=act_bits & 0xFF, act_sym=bool(act_bits & oq.ACT_SYM), let=let,
+                softmax_bits=softmax_bits)
     shapes = [(H * d, D), (Hkv * d, D), (Hkv * d, D), (D, H * d), (F, D), (F, D), (D, F)]
     W = [bf16_exact(inputs.weights(rng, a, b, 0.02, 0.001)) for a, b in shapes]
     gl = [rng.uniform(2.0, 6.0, (a, b // g)).astype(np.float32) for (a, b), g in zip(shapes, groups)]
@@ -184,7 +299,7 @@ def llama_problem(D, H, Hkv, F, S, ns, bits, groups, act_bits, let, seed):
 def gpu_block(desc, T, act_bits):
     return oq.LlamaBlock(T, desc["seq_len"], desc["hidden"], desc["heads"], desc["kv_heads"],
                          desc["ffn"], desc["w_bits"], desc["w_group"], act_bits=act_bits,
-                         let=desc["let"])
+                         let=desc["let"], softmax_bits=desc.get("softmax_bits", 16))
 
 
 def dev_params(p):
@@ -240,8 +355,8 @@ def compare_step(desc, h0, target, p, act_bits):
     ref_loss, ref = lb.block_step(desc, h0, target, p)
     refs = dict(grad_items(ref))
     bars = {n: (TOL, TOL) for n in refs}
-    if desc["act_bits"] < 16:
-        # quantised activations: a code flips wherever the two sides' inputs
+    if desc["act_bits"] < 16 or desc.get("softmax_bits", 16) < 16:
+        # quantised activations (or softmax output): a code flips wherever the two sides' inputs
         # straddle a code boundary (a whole step of the per-token grid), and
         # grouped clipping gradients sum such flips with cancellation; the bar
         # is then the distance the oracle's own gradients move between its bf16
@@ -285,15 +400,21 @@ BLOCK_CASES = [
          act_bits=4, let=True),
     dict(D=256, H=4, Hkv=4, F=512, S=128, ns=1, bits=(4,) * 7, groups=(64,) * 7,
          act_bits=8 | oq.ACT_SYM, let=True),
+    # the softmax-quantisation ablation
+    dict(D=256, H=2, Hkv=1, F=512, S=128, ns=2, bits=(4,) * 7, groups=(128,) * 7, act_bits=4,
+         let=True, softmax_bits=4),
+    dict(D=256, H=4, Hkv=2, F=512, S=64, ns=2, bits=(4,) * 7, groups=(64,) * 7, act_bits=16,
+         let=True, softmax_bits=6),
 ]
 
 
 @pytest.mark.parametrize("c", BLOCK_CASES, ids=[f"{c['D']}_{c['H']}_{c['Hkv']}_a{c['act_bits']}_let{int(c['let'])}"
-                                                for c in BLOCK_CASES])
+                                                f"_p{c.get('softmax_bits', 16)}" for c in BLOCK_CASES])
 def test_llama_block_step(c):
     print(f"llama block {c}", flush=True)
     desc, h0, target, p = llama_problem(c["D"], c["H"], c["Hkv"], c["F"], c["S"], c["ns"], c["bits"],
-                                        c["groups"], c["act_bits"], c["let"], seed=1)
+                                        c["groups"], c["act_bits"], c["let"], seed=1,
+                                        softmax_bits=c.get("softmax_bits", 16))
     compare_step(desc, h0, target, p, c["act_bits"])
 
 
