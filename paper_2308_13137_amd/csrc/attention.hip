@@ -449,7 +449,7 @@ OQ_DEV bf16x8_t t16_frag(const bf16raw* t, int kb, int lane) {
 // through Q_a's straight-through rule: dP = m dP^ plus the routed gradients of
 // the row's max and min (from the dQ kernel's first sweep).
 template <int DH, bool QP>
-__global__ __launch_bounds__(ANT, QP ? 1 : 2) void attn_bwd_dkv_kernel(
+__global__ __launch_bounds__(ANT, 2) void attn_bwd_dkv_kernel(
     const bf16raw* __restrict__ Q, const bf16raw* __restrict__ K, const bf16raw* __restrict__ V,
     const bf16raw* __restrict__ dO, const float* __restrict__ LSE, const float* __restrict__ Dl,
     int S, int H, int Hkv, int64_t T, float* __restrict__ dK, float* __restrict__ dV,
@@ -623,7 +623,7 @@ __global__ __launch_bounds__(ANT, QP ? 1 : 2) void attn_bwd_dkv_kernel(
 // and D = E + max dmax + min dmin; the second sweep's dP follows Q_a's
 // straight-through rule.
 template <int DH, bool QP>
-__global__ __launch_bounds__(ANT, QP ? 1 : 2) void attn_bwd_dq_kernel(
+__global__ __launch_bounds__(ANT, 2) void attn_bwd_dq_kernel(
     const bf16raw* __restrict__ Q, const bf16raw* __restrict__ K, const bf16raw* __restrict__ V,
     const bf16raw* __restrict__ dO, const float* __restrict__ LSE, float* __restrict__ Dl,
     int S, int H, int Hkv, int64_t T, float* __restrict__ dQ, int p_bits,
