@@ -46,6 +46,7 @@ struct EpiF32 {
   bool vec;
   int64_t split_stride;              // elements between the K-split partial outputs
   static constexpr bool kRows = false;
+  static constexpr bool kPre = false;
   OQ_DEV void split(int s) { C += s * split_stride; }
   struct Row { float* c; };
   OQ_DEV Row row(int64_t m) const { return Row{C + m * ldc}; }
@@ -69,6 +70,7 @@ struct EpiStore {
   const float* bias;
   bool vec;
   static constexpr bool kRows = false;
+  static constexpr bool kPre = false;
   OQ_DEV void split(int) {}
   struct Row { TC* c; float b; };
   OQ_DEV Row row(int64_t m) const { return Row{C + m * ldc, bias ? bias[m] : 0.0f}; }
@@ -89,11 +91,15 @@ struct EpiStore {
 };
 
 // y = acc + B~[m]; r = y - y_fp; dY = r * 2/(T*c_out) stored in T;  row sums of r^2, dY.
+// With a bf16 target the 8-wave kernel loads every chunk of y_fp a lane
+// needs (pre) before it stages the accumulators, so the epilogue waits on
+// one round of global loads instead of one per pass (apply8_pre).
 template <typename T>
 struct EpiResid {
   ResidArgs a;
   bool vec;
   static constexpr bool kRows = true;
+  static constexpr bool kPre = sizeof(T) == 2;
   OQ_DEV void split(int) {}
   struct Row { const T* yfp; T* dy; float scale; float b; };
   OQ_DEV Row row(int64_t m) const {
@@ -117,14 +123,37 @@ struct EpiResid {
     return r;
   }
   OQ_DEV float2 apply8(const Row& r, int64_t n, const float* v, int cnt) const {
-    float yf[8], d[8];
-    const bool full = vec && cnt == 8;
-    if (full) {
+    float yf[8];
+    if (vec && cnt == 8) {
       load8(r.yfp + n, yf);
     } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) yf[e] = e < cnt ? load1(r.yfp + n + e) : 0.0f;
     }
+    return resid8(r, n, v, cnt, yf);
+  }
+  // bf16 target only: the raw chunk, then the chunk's arithmetic from it
+  OQ_DEV uint4 pre(const Row& r, int64_t n, int cnt) const {
+    if (vec && cnt == 8) return *reinterpret_cast<const uint4*>(r.yfp + n);
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (e < cnt) w[e >> 1] |= uint32_t(reinterpret_cast<const uint16_t*>(r.yfp)[n + e]) << (16 * (e & 1));
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  OQ_DEV float2 apply8_pre(const Row& r, int64_t n, const float* v, int cnt, uint4 q) const {
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    float yf[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      yf[2 * e] = __uint_as_float(w[e] << 16);
+      yf[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+    }
+    return resid8(r, n, v, cnt, yf);
+  }
+  OQ_DEV float2 resid8(const Row& r, int64_t n, const float* v, int cnt, const float* yf) const {
+    float d[8];
+    const bool full = vec && cnt == 8;
     float sq = 0.f, sdy = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -512,7 +541,8 @@ OQ_DEV void mfma_half(f32x4_t (&acc)[8][4], const bf16x8_t (&af)[8], const bf16x
 // partials: 8 lanes per row, then the four column waves in a fixed order.
 template <int P, class Epi>
 OQ_DEV void epi8_pass(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, int64_t M, int wm,
-                      int wn, int lane, int64_t nb, int cnt, float* reg, float2 (*rowbuf)[BM]) {
+                      int wn, int lane, int64_t nb, int cnt, float* reg, float2 (*rowbuf)[BM],
+                      const uint4 (&pre)[4][4]) {
   constexpr int PITCH = EPI8_PITCH;
   const int fr = lane & 15, fk = lane >> 4;
   const int cl = lane & 7, rl = lane >> 3;
@@ -523,6 +553,7 @@ OQ_DEV void epi8_pass(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, in
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         reg[(16 * ii + 4 * fk + r) * PITCH + 16 * j + fr] = acc[2 * P + ii][j][r];
+#pragma unroll
   for (int it = 0; it < 4; ++it) {
     const int rloc = rl + 8 * it;
     const int trow = wm * 128 + 32 * P + rloc;
@@ -533,7 +564,10 @@ OQ_DEV void epi8_pass(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, in
     v[0] = a_.x; v[1] = a_.y; v[2] = a_.z; v[3] = a_.w;
     v[4] = b_.x; v[5] = b_.y; v[6] = b_.z; v[7] = b_.w;
     float2 c = make_float2(0.f, 0.f);
-    if (m < M && cnt > 0) c = epi.apply8(epi.row(m), nb, v, cnt);
+    if (m < M && cnt > 0) {
+      if constexpr (Epi::kPre) c = epi.apply8_pre(epi.row(m), nb, v, cnt, pre[P][it]);
+      else c = epi.apply8(epi.row(m), nb, v, cnt);
+    }
     if constexpr (Epi::kRows) {
       c.x = group_sum<8>(c.x);
       c.y = group_sum<8>(c.y);
@@ -550,10 +584,21 @@ OQ_DEV void epilogue8(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, in
   float* reg = scratch + wave * (32 * EPI8_PITCH);
   const int64_t nb = n0 + wn * 64 + 8 * (lane & 7);
   const int cnt = int(max<int64_t>(0, min<int64_t>(8, N - nb)));
-  epi8_pass<0>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf);
-  epi8_pass<1>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf);
-  epi8_pass<2>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf);
-  epi8_pass<3>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf);
+  // the chunks of every pass in flight at once (row m0 + wm 128 + 32 P + lane/8 + 8 it)
+  uint4 pre[4][4];
+  if constexpr (Epi::kPre) {
+#pragma unroll
+    for (int P = 0; P < 4; ++P)
+#pragma unroll
+      for (int it = 0; it < 4; ++it) {
+        const int64_t m = m0 + wm * 128 + 32 * P + (lane >> 3) + 8 * it;
+        pre[P][it] = (m < M && cnt > 0) ? epi.pre(epi.row(m), nb, cnt) : make_uint4(0u, 0u, 0u, 0u);
+      }
+  }
+  epi8_pass<0>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf, pre);
+  epi8_pass<1>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf, pre);
+  epi8_pass<2>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf, pre);
+  epi8_pass<3>(acc, epi, m0, M, wm, wn, lane, nb, cnt, reg, rowbuf, pre);
   if constexpr (Epi::kRows) {
     __syncthreads();
     const int tid = threadIdx.x;
