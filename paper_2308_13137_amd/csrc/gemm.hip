@@ -617,6 +617,97 @@ OQ_DEV void epilogue8(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, in
   }
 }
 
+// Residual epilogue, fast form, for a tile inside M and N whose rows all
+// belong to one stacked linear, with 16-byte access: the linear is looked up
+// once per tile, a lane's 16 rows are its first row plus constant strides,
+// their bias and target chunks are loaded before the accumulators are
+// staged, and the 8-lane row sums run on DPP (quad xor 1, quad xor 2, then
+// the half-row mirror: the same pairings as the butterfly, so the sums are
+// bit-identical to the general form's).
+OQ_DEV float group8_sum(float v) {
+  v += dpp_f(v, 0);
+  v += dpp_f(v, 1);
+  v += dpp_f(v, 2);
+  return v;
+}
+
+OQ_DEV int resid_seg(const ResidArgs& a, int64_t m) {
+  int s = 0;
+#pragma unroll
+  for (int k = 1; k < MAX_SEG; ++k)
+    if (k < a.nseg && m >= a.seg_begin[k]) s = k;
+  return s;
+}
+
+OQ_DEV void epilogue8_resid(const f32x4_t (&acc)[8][4], const EpiResid<uint16_t>& ep, int seg,
+                            int64_t m0, int64_t n0, int tn, int wave, int lane, float* scratch,
+                            float2 (*rowbuf)[BM]) {
+  constexpr int PITCH = EPI8_PITCH;
+  const ResidArgs& a = ep.a;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int fr = lane & 15, fk = lane >> 4;
+  const int cl = lane & 7, rl = lane >> 3;
+  float* reg = scratch + wave * (32 * PITCH);
+  // this lane's first row m0 + wm 128 + rl; the others follow at 32 P + 8 it
+  const int64_t mr = m0 + wm * 128 + rl;
+  const int64_t nb = n0 + wn * 64 + 8 * cl;
+  const float scale = a.scale[seg];
+  const uint16_t* yl = static_cast<const uint16_t*>(a.yfp[seg]) + (mr - a.seg_begin[seg]) * a.ld_yfp + nb;
+  uint16_t* dl = static_cast<uint16_t*>(a.dy) + mr * a.ld_dy + nb;
+  uint4 yv[4][4];
+  float bv[4][4];
+#pragma unroll
+  for (int P = 0; P < 4; ++P)
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int64_t o = 32 * P + 8 * it;
+      yv[P][it] = *reinterpret_cast<const uint4*>(yl + o * a.ld_yfp);
+      bv[P][it] = a.bias ? a.bias[mr + o] : 0.0f;
+    }
+#pragma unroll
+  for (int P = 0; P < 4; ++P) {
+#pragma unroll
+    for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          reg[(16 * ii + 4 * fk + r) * PITCH + 16 * j + fr] = acc[2 * P + ii][j][r];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int rloc = rl + 8 * it;
+      const float4 lo = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl);
+      const float4 hi = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl + 4);
+      const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      const uint32_t w[4] = {yv[P][it].x, yv[P][it].y, yv[P][it].z, yv[P][it].w};
+      float d[8], sq = 0.f, sdy = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float yf = __uint_as_float(e & 1 ? w[e >> 1] & 0xffff0000u : w[e >> 1] << 16);
+        const float res = (v[e] + bv[P][it]) - yf;
+        d[e] = res * scale;
+        sq += res * res;
+        sdy += bf2f(f2bf(d[e]));
+      }
+      store8(dl + int64_t(32 * P + 8 * it) * a.ld_dy, d);
+      sq = group8_sum(sq);
+      sdy = group8_sum(sdy);
+      if (cl == 0) rowbuf[wn][wm * 128 + 32 * P + rloc] = make_float2(sq, sdy);
+    }
+  }
+  __syncthreads();
+  const int tid = threadIdx.x;
+  if (tid < BM) {
+    float2 t = rowbuf[0][tid];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      t.x += rowbuf[w][tid].x;
+      t.y += rowbuf[w][tid].y;
+    }
+    ep.finish(m0 + tid, tn, t.x, t.y);
+  }
+}
+
 // Weight gradient with the LWC straight-through backward fused (no LET):
 // the accumulators are dW^ for rows m (output channels of the stacked
 // linears) and columns n (input channels).  G = group / 8 lanes of a row
@@ -885,9 +976,19 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
   if constexpr (IsLwc<Epi>::value)
     epilogue8_lwc(acc, epi, m0, n0, M, N, wave, lane, reinterpret_cast<float*>(&lds[0]),
                   reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304));
-  else
-    epilogue8(acc, epi, m0, n0, M, N, tn, wave, lane, reinterpret_cast<float*>(&lds[0]),
-              reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304));
+  else {
+    float* stg = reinterpret_cast<float*>(&lds[0]);
+    auto rows = reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304);
+    if constexpr (std::is_same<Epi, EpiResid<uint16_t>>::value) {
+      // the fast form when the tile is whole and within one linear (uniform)
+      const int seg = resid_seg(epi.a, m0);
+      if (epi.vec && m0 + BM <= M && n0 + BN <= N && resid_seg(epi.a, m0 + BM - 1) == seg) {
+        epilogue8_resid(acc, epi, seg, m0, n0, tn, wave, lane, stg, rows);
+        return;
+      }
+    }
+    epilogue8(acc, epi, m0, n0, M, N, tn, wave, lane, stg, rows);
+  }
 }
 
 // ------------------------------------------------------------------ split forward's residual
