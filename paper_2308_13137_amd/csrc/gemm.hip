@@ -639,6 +639,9 @@ OQ_DEV int resid_seg(const ResidArgs& a, int64_t m) {
   return s;
 }
 
+// BIAS: the tile's linear has a bias; DY: the row sums of dY are wanted
+// (the LET bias path).  Without them their per-element work is not done.
+template <bool BIAS, bool DY>
 OQ_DEV void epilogue8_resid(const f32x4_t (&acc)[8][4], const EpiResid<uint16_t>& ep, int seg,
                             int64_t m0, int64_t n0, int tn, int wave, int lane, float* scratch,
                             float2 (*rowbuf)[BM]) {
@@ -662,7 +665,7 @@ OQ_DEV void epilogue8_resid(const f32x4_t (&acc)[8][4], const EpiResid<uint16_t>
     for (int it = 0; it < 4; ++it) {
       const int64_t o = 32 * P + 8 * it;
       yv[P][it] = *reinterpret_cast<const uint4*>(yl + o * a.ld_yfp);
-      bv[P][it] = a.bias ? a.bias[mr + o] : 0.0f;
+      bv[P][it] = BIAS ? a.bias[mr + o] : 0.0f;
     }
 #pragma unroll
   for (int P = 0; P < 4; ++P) {
@@ -684,14 +687,14 @@ OQ_DEV void epilogue8_resid(const f32x4_t (&acc)[8][4], const EpiResid<uint16_t>
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float yf = __uint_as_float(e & 1 ? w[e >> 1] & 0xffff0000u : w[e >> 1] << 16);
-        const float res = (v[e] + bv[P][it]) - yf;
+        const float res = (BIAS ? v[e] + bv[P][it] : v[e]) - yf;
         d[e] = res * scale;
         sq += res * res;
-        sdy += bf2f(f2bf(d[e]));
+        if (DY) sdy += bf2f(f2bf(d[e]));
       }
       store8(dl + int64_t(32 * P + 8 * it) * a.ld_dy, d);
       sq = group8_sum(sq);
-      sdy = group8_sum(sdy);
+      if (DY) sdy = group8_sum(sdy);
       if (cl == 0) rowbuf[wn][wm * 128 + 32 * P + rloc] = make_float2(sq, sdy);
     }
   }
@@ -983,7 +986,13 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
       // the fast form when the tile is whole and within one linear (uniform)
       const int seg = resid_seg(epi.a, m0);
       if (epi.vec && m0 + BM <= M && n0 + BN <= N && resid_seg(epi.a, m0 + BM - 1) == seg) {
-        epilogue8_resid(acc, epi, seg, m0, n0, tn, wave, lane, stg, rows);
+        if (epi.a.bias) {
+          if (epi.a.part_dy) epilogue8_resid<true, true>(acc, epi, seg, m0, n0, tn, wave, lane, stg, rows);
+          else epilogue8_resid<true, false>(acc, epi, seg, m0, n0, tn, wave, lane, stg, rows);
+        } else {
+          if (epi.a.part_dy) epilogue8_resid<false, true>(acc, epi, seg, m0, n0, tn, wave, lane, stg, rows);
+          else epilogue8_resid<false, false>(acc, epi, seg, m0, n0, tn, wave, lane, stg, rows);
+        }
         return;
       }
     }
