@@ -444,3 +444,63 @@ def fp_block(desc, h0, params):
     x3, _ = rmsnorm(h1, params["g2"], d2["norm_eps"])
     x4 = silu(x3 @ W[4].T) * (x3 @ W[5].T)
     return h1 + x4 @ W[6].T
+
+
+# ---------------------------------------------------------------- Algorithm 1 over a stack
+def _adam_update(params, grads, mom, step, lr_lwc, lr_let):
+    """One AdamW step (oracle.adamw, fp64, stored back as fp32) on every
+    trained tensor: the clipping logits at lr_lwc, s, delta and s_a at
+    lr_let."""
+    from .adamw import adamw
+    pairs = [("gamma_logit", "d_gamma_logit", lr_lwc), ("beta_logit", "d_beta_logit", lr_lwc),
+             ("s", "d_s", lr_let), ("delta", "d_delta", lr_let)]
+    for pk, gk, lr in pairs:
+        for i, g in enumerate(grads[gk]):
+            if g is None:
+                continue
+            key = (pk, i)
+            m, v = mom.get(key, (0.0, 0.0))
+            p, m, v = adamw(params[pk][i], g, m, v, step, lr)
+            params[pk][i] = p.astype(np.float32)
+            mom[key] = (m, v)
+    if grads["d_s_a"] is not None:
+        m, v = mom.get("s_a", (0.0, 0.0))
+        p, m, v = adamw(params["s_a"], grads["d_s_a"], m, v, step, lr_let)
+        params["s_a"] = p.astype(np.float32)
+        mom["s_a"] = (m, v)
+
+
+def algorithm1(desc, blocks, samples, epochs, lr_lwc=5e-3, lr_let=1e-2):
+    """Algorithm 1 over a stack of blocks, calibrated one after another.
+
+    ``blocks``: per block a params dict as block_step takes (W, g1, g2 and the
+    initial clipping logits, s, delta, s_a); ``samples``: the calibration
+    inputs, one [seq_len, D] array per sample (batch size 1).  Block i is
+    trained against its full-precision output on the full-precision stream
+    (the targets, rounded to bf16 as the kernels store them), from the
+    quantised stream as input, for ``epochs`` passes over the samples in
+    order with one AdamW step per sample (a fresh AdamW state per block);
+    then both streams move on: the full-precision stream through the block
+    unquantised (the targets), the quantised one through the block with its
+    learned parameters (bf16).
+    Returns (losses [blocks][epochs * samples], trained params per block,
+    final quantised stream)."""
+    x_fp = [np.asarray(x, np.float64) for x in samples]
+    x_q = [np.asarray(x, np.float64) for x in samples]
+    losses, trained = [], []
+    for params in blocks:
+        P = {k: (list(v) if isinstance(v, list) else v) for k, v in params.items()}
+        targets = [bf16_round(fp_block(desc, x, P)) for x in x_fp]
+        mom, step = {}, 0              # a fresh optimizer for every block
+        block_losses = []
+        for _ in range(epochs):
+            for j in range(len(samples)):
+                step += 1
+                loss, g = block_step(desc, x_q[j], targets[j], P)
+                block_losses.append(loss)
+                _adam_update(P, g, mom, step, lr_lwc, lr_let)
+        x_q = [bf16_round(block_forward(desc, x, t, P)[1]["h2"]) for x, t in zip(x_q, targets)]
+        x_fp = targets
+        losses.append(block_losses)
+        trained.append(P)
+    return losses, trained, x_q

@@ -13,6 +13,7 @@ import pytest
 import torch
 
 from oracle import llama_block as lb
+from oracle.quant import bf16_round
 
 
 def tiny_desc(act_bits=4, let=True, H=2, Hkv=1, D=16, F=24, S=6, bits=(3, 4, 4, 3, 4, 3, 4),
@@ -337,3 +338,78 @@ def test_fd_detects_a_planted_error_in_the_attention_backward():
         lb.attention_bwd = good
     assert abs(g_ok["d_s_a"][j] - fd) <= 1e-6 * abs(fd)
     assert abs(g_bad["d_s_a"][j] - fd) > 1e-4 * abs(fd)
+
+
+# ---------------------------------------------------------------- Algorithm 1 over a stack
+def _stack(desc, rng, n_blocks, T):
+    blocks = []
+    for _ in range(n_blocks):
+        _, _, p = tiny_params(desc, rng, T)
+        # the trained tensors are fp32, as the kernels keep them
+        for k in ("gamma_logit", "beta_logit", "s", "delta"):
+            p[k] = [np.asarray(a, np.float32) for a in p[k]]
+        p["s_a"] = np.asarray(p["s_a"], np.float32)
+        blocks.append(p)
+    return blocks
+
+
+def test_algorithm1_without_learning_composes_the_blocks():
+    """With both learning rates 0 nothing moves: every loss of block i is
+    one step's loss at its initial parameters, against targets that are the
+    full-precision blocks composed (each output rounded to bf16), from the
+    quantised blocks composed at their initial parameters."""
+    desc = tiny_desc()
+    rng = np.random.default_rng(41)
+    S = desc["seq_len"]
+    blocks = _stack(desc, rng, 2, S)
+    samples = [rng.standard_normal((S, desc["hidden"])) for _ in range(2)]
+    losses, trained, xq = lb.algorithm1(desc, blocks, samples, epochs=2, lr_lwc=0.0, lr_let=0.0)
+    fp1 = [bf16_round(lb.fp_block(desc, x, blocks[0])) for x in samples]
+    fp2 = [bf16_round(lb.fp_block(desc, x, blocks[1])) for x in fp1]
+    q1 = [bf16_round(lb.block_forward(desc, x, t, blocks[0])[1]["h2"]) for x, t in zip(samples, fp1)]
+    want0 = [lb.block_step(desc, x, t, blocks[0])[0] for x, t in zip(samples, fp1)]
+    want1 = [lb.block_step(desc, x, t, blocks[1])[0] for x, t in zip(q1, fp2)]
+    np.testing.assert_allclose(losses[0], want0 * 2, rtol=1e-12)
+    np.testing.assert_allclose(losses[1], want1 * 2, rtol=1e-12)
+    q2 = [bf16_round(lb.block_forward(desc, x, t, blocks[1])[1]["h2"]) for x, t in zip(q1, fp2)]
+    for a, b in zip(xq, q2):
+        np.testing.assert_array_equal(a, b)
+    for P, P0 in zip(trained, blocks):
+        for a, b in zip(P["gamma_logit"], P0["gamma_logit"]):
+            np.testing.assert_allclose(a, b, rtol=1e-7)
+
+
+def test_algorithm1_first_step_of_every_block_is_a_fresh_adam_step():
+    """Each block gets a fresh AdamW state: its first update moves every
+    parameter with a nonzero gradient by its learning rate (Adam's first
+    bias-corrected step is lr g / (|g| + eps)), the clipping logits by 5e-3
+    and s, delta, s_a by 1e-2, in the second block as in the first."""
+    desc = tiny_desc()
+    rng = np.random.default_rng(42)
+    S = desc["seq_len"]
+    blocks = _stack(desc, rng, 2, S)
+    samples = [rng.standard_normal((S, desc["hidden"]))]
+    _, trained, _ = lb.algorithm1(desc, blocks, samples, epochs=1)
+    def check(moved, lr, key):
+        # no element moves further than lr (up to the fp32 storage of p);
+        # the typical one (|g| >> eps) moves lr
+        assert np.max(moved) <= lr * (1 + 1e-4) + 1e-6, key
+        assert abs(np.median(moved) / lr - 1) < 2e-3, (key, np.median(moved))
+    for P, P0 in zip(trained, blocks):
+        for key, lr in (("gamma_logit", 5e-3), ("beta_logit", 5e-3), ("s", 1e-2), ("delta", 1e-2)):
+            moved = np.concatenate([np.abs(np.asarray(a, np.float64) - np.asarray(b, np.float32)).ravel()
+                                    for a, b in zip(P[key], P0[key])])
+            check(moved, lr, key)
+        check(np.abs(np.asarray(P["s_a"], np.float64) - np.asarray(P0["s_a"], np.float32)), 1e-2, "s_a")
+
+
+def test_algorithm1_training_lowers_the_loss():
+    """Twenty epochs over two samples lower every block's loss."""
+    desc = tiny_desc(act_bits=16)
+    rng = np.random.default_rng(43)
+    S = desc["seq_len"]
+    blocks = _stack(desc, rng, 2, S)
+    samples = [rng.standard_normal((S, desc["hidden"])) for _ in range(2)]
+    losses, _, _ = lb.algorithm1(desc, blocks, samples, epochs=20)
+    for bl_ in losses:
+        assert sum(bl_[-2:]) < 0.9 * sum(bl_[:2]), bl_
