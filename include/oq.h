@@ -597,6 +597,22 @@ oq_status oq_llama_block_step(const oq_llama_desc* desc, const void* h0, const v
                               const oq_llama_optim* optim, float* loss, void* ws,
                               size_t ws_bytes, hipStream_t stream);
 
+/* Algorithm 1's training loop for one block: `epochs` passes over the
+ * samples in order, one oq_llama_block_step with the AdamW update per sample
+ * (batch size 1, Sec. 4.1).  h0[j], target[j]: sample j's block input X_q and
+ * its full-precision block output, bf16 [tokens, hidden] device, 16-byte
+ * aligned, each desc->tokens tokens.  The AdamW steps count from optim->step
+ * (>= 1) on; losses: device fp32 [epochs * n_samples], step i = epoch *
+ * n_samples + j.  Parameters are updated in place; grads hold the last step's
+ * gradients.  Pointers are checked before the first launch; a failing step
+ * returns its status with the earlier steps applied.  Same workspace as the
+ * step. */
+oq_status oq_llama_calibrate(const oq_llama_desc* desc, int n_samples, int epochs,
+                             const void* const* h0, const void* const* target,
+                             const oq_llama_params* params, const oq_llama_grads* grads,
+                             const oq_llama_optim* optim, float* losses, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
+
 /* The block's forward alone, for Algorithm 1's propagation from block to
  * block: quantised = 0 gives the full-precision block (W as given, no LET,
  * no quantiser: X_fp <- B(X_fp)); quantised = 1 the quantised block with the

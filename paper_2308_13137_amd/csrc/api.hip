@@ -2082,4 +2082,31 @@ oq_status oq_llama_block_step(const oq_llama_desc* d, const void* h0, const void
   return OQ_OK;
 }
 
+oq_status oq_llama_calibrate(const oq_llama_desc* d, int n_samples, int epochs,
+                             const void* const* h0, const void* const* target,
+                             const oq_llama_params* p, const oq_llama_grads* g,
+                             const oq_llama_optim* opt, float* losses, void* ws, size_t ws_bytes,
+                             hipStream_t st) {
+  OQ_REQ(d && h0 && target && p && g && opt && losses,
+         "desc, h0, target, params, grads, optim and losses are required");
+  OQ_REQ(n_samples >= 1 && epochs >= 1, "need n_samples >= 1 and epochs >= 1 (got %d, %d)",
+         n_samples, epochs);
+  OQ_REQ(opt->step >= 1 && int64_t(opt->step) + int64_t(epochs) * n_samples - 1 <= INT32_MAX,
+         "optim step %d out of range for %d steps", opt->step, epochs * n_samples);
+  // every sample's pointers before the first launch; the first step checks the rest
+  for (int j = 0; j < n_samples; ++j)
+    OQ_REQ(h0[j] && target[j] && aligned16(h0[j]) && aligned16(target[j]),
+           "sample %d: h0 or target missing or misaligned", j);
+  oq_llama_optim o = *opt;
+  for (int ep = 0; ep < epochs; ++ep)
+    for (int j = 0; j < n_samples; ++j) {
+      const int64_t i = int64_t(ep) * n_samples + j;
+      o.step = int(opt->step + i);
+      const oq_status e = oq_llama_block_step(d, h0[j], target[j], p, g, &o, losses + i, ws,
+                                              ws_bytes, st);
+      if (e != OQ_OK) return e;
+    }
+  return OQ_OK;
+}
+
 }  // extern "C"

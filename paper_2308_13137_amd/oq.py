@@ -620,6 +620,7 @@ _SIGS_LLAMA = {
                               _P]),
     "oq_llama_workspace_size": (_I, [_P, _PSZ]),
     "oq_llama_block_step": (_I, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "oq_llama_calibrate": (_I, [_P, _I, _I, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "oq_llama_block_forward": (_I, [_P, _P, _P, _I, _P, _P, _SZ, _P]),
 }
 SIGNATURES.update(_SIGS_LLAMA)
@@ -746,6 +747,7 @@ class LlamaBlock:
             z(self.d_s_a, "v_s_a")
         o.lr_lwc, o.lr_let, o.beta1, o.beta2, o.eps, o.wd = lr_lwc, lr_let, beta1, beta2, eps, wd
         self.opt = o
+        self.step_count = 0
 
     def _params(self, W, norm1, norm2, gl=None, bl=None, s=None, delta=None, s_a=None):
         p = LlamaParams()
@@ -761,6 +763,41 @@ class LlamaBlock:
                 p.delta[k] = _ptr(delta[k]).value
             p.s_a = _ptr(s_a).value
         return p
+
+    def _grads(self):
+        g = LlamaGrads()
+        for l in range(NL):
+            g.d_gamma_logit[l] = self.d_gamma[l].data_ptr()
+            g.d_beta_logit[l] = self.d_beta[l].data_ptr()
+        if self.let:
+            for k in range(3):
+                g.d_s[k] = self.d_s[k].data_ptr()
+                g.d_delta[k] = self.d_delta[k].data_ptr()
+            g.d_s_a = self.d_s_a.data_ptr()
+        return g
+
+    def calibrate(self, h0s, targets, W, norm1, norm2, gl, bl, s=None, delta=None, s_a=None,
+                  epochs=1, stream=None):
+        """Algorithm 1's loop for this block (oq_llama_calibrate): ``epochs``
+        passes over the samples (bf16 [T, D] each, inputs and full-precision
+        outputs), one AdamW step per sample, parameters updated in place.
+        Returns the losses, fp32 [epochs * len(h0s)]."""
+        if self.opt is None:
+            raise OQError("call init_optimizer() before calibrate")
+        n = len(h0s)
+        if len(targets) != n or n == 0:
+            raise OQError("one target per sample is needed")
+        p = self._params(W, norm1, norm2, gl, bl, s, delta, s_a)
+        g = self._grads()
+        hp = (C.c_void_p * n)(*[_ptr(x).value for x in h0s])
+        tp = (C.c_void_p * n)(*[_ptr(x).value for x in targets])
+        losses = torch.empty(epochs * n, dtype=torch.float32, device=self.device)
+        self.opt.step = self.step_count + 1
+        _check(lib().oq_llama_calibrate(C.byref(self.desc), n, epochs, hp, tp, C.byref(p),
+                                        C.byref(g), C.byref(self.opt), _ptr(losses), _ptr(self.ws),
+                                        self.ws_bytes, _stream(stream)))
+        self.step_count += epochs * n
+        return losses
 
     def step(self, h0, target, W, norm1, norm2, gl, bl, s=None, delta=None, s_a=None,
              update=False, stream=None):
@@ -796,3 +833,29 @@ class LlamaBlock:
                                             int(bool(quantised)), _ptr(out), _ptr(self.ws),
                                             self.ws_bytes, _stream(stream)))
         return out
+
+
+def llama_algorithm1(blk, blocks, samples, epochs, lr_lwc=5e-3, lr_let=1e-2, stream=None):
+    """Algorithm 1 over a stack of LLaMA blocks of one shape (``blk``'s
+    descriptor), one block after another.  ``blocks``: per block a dict of
+    device tensors W (7), norm1, norm2, gl, bl and, with LET, s, delta, s_a
+    (the trainable ones updated in place); ``samples``: the calibration
+    inputs, bf16 [T, D] each (batch size 1).  Block i's targets are its
+    full-precision outputs on the full-precision stream; it trains from the
+    quantised stream with a fresh AdamW state; then the full-precision
+    stream moves on through the block unquantised and the quantised stream
+    through the block with its learned parameters.  Returns (the losses of
+    each block, the final quantised stream)."""
+    x_fp, x_q = list(samples), list(samples)
+    losses = []
+    for b in blocks:
+        W, n1, n2 = b["W"], b["norm1"], b["norm2"]
+        let = dict(s=b.get("s"), delta=b.get("delta"), s_a=b.get("s_a"))
+        targets = [blk.forward(x, W, n1, n2, quantised=False, stream=stream) for x in x_fp]
+        blk.init_optimizer(lr_lwc, lr_let)
+        losses.append(blk.calibrate(x_q, targets, W, n1, n2, b["gl"], b["bl"], epochs=epochs,
+                                    stream=stream, **let))
+        x_q = [blk.forward(x, W, n1, n2, b["gl"], b["bl"], quantised=True, stream=stream, **let)
+               for x in x_q]
+        x_fp = targets
+    return losses, x_q

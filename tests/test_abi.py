@@ -342,3 +342,61 @@ def test_checkpoint_load_validation(tmp_path):
     assert L.oq_block_state_load(C.byref(d), C.byref(prm), None, C.byref(done),
                                  str(tmp_path / "missing.bin").encode(), None) == INVALID
     assert done.value == -1                      # nothing reported on failure
+
+
+def _llama_desc(softmax_bits=16):
+    d = oq.LlamaDesc()
+    d.tokens, d.seq_len, d.hidden, d.ffn, d.heads, d.kv_heads = 128, 128, 256, 512, 2, 1
+    d.norm_eps, d.rope_base = 1e-6, 10000.0
+    for l in range(7):
+        d.w_bits[l], d.w_group[l] = 4, 128
+    d.act_bits, d.let, d.softmax_bits = 16, 0, softmax_bits
+    return d
+
+
+def test_llama_softmax_bits_and_attention_validation():
+    L = oq.lib()
+    n = C.c_size_t(0)
+    assert L.oq_llama_workspace_size(C.byref(_llama_desc(4)), C.byref(n)) == OK
+    n16 = C.c_size_t(0)
+    assert L.oq_llama_workspace_size(C.byref(_llama_desc(16)), C.byref(n16)) == OK
+    assert n.value > n16.value                      # the per-row record and the larger scratch
+    for bad in (1, 9, 15):
+        assert L.oq_llama_workspace_size(C.byref(_llama_desc(bad)), C.byref(n)) == UNSUPPORTED
+    ws = C.c_size_t(0)
+    assert L.oq_attention_bwd_workspace_size(128, 2, 4, C.byref(ws)) == OK
+    assert ws.value == 3 * 128 * 2 * 4 + 256
+    assert L.oq_attention_bwd_workspace_size(128, 2, 16, C.byref(ws)) == OK
+    assert ws.value == 128 * 2 * 4 + 256
+
+    def fwd(bits, pstat):
+        return L.oq_attention_fwd(FAKE, FAKE, FAKE, 128, 64, 2, 1, 64, bits, FAKE, FAKE, pstat, None)
+    assert fwd(4, None) == INVALID and fwd(4, MISALIGNED) == INVALID
+    assert fwd(9, FAKE) == INVALID and fwd(1, FAKE) == INVALID
+
+    def bwd(bits, pstat, nbytes):
+        return L.oq_attention_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, pstat, 128, 64, 2, 1, 64, bits, FAKE,
+                                  FAKE, FAKE, FAKE, nbytes, None)
+    assert bwd(4, None, 1 << 20) == INVALID
+    assert bwd(4, FAKE, 3 * 128 * 2 * 4) == WORKSPACE     # one fp32 [H, T] short of the three
+
+
+def test_llama_calibrate_validation():
+    L = oq.lib()
+    d = _llama_desc()
+    n = C.c_size_t(0)
+    assert L.oq_llama_workspace_size(C.byref(d), C.byref(n)) == OK
+    prm, grd, opt = oq.LlamaParams(), oq.LlamaGrads(), oq.LlamaOptim()
+    opt.step = 1
+    hp = (C.c_void_p * 2)(0x10000, 0x10000)
+    tp = (C.c_void_p * 2)(0x10000, None)           # sample 1's target missing
+
+    def call(ns=2, ep=2, h=hp, t=tp, losses=FAKE):
+        return L.oq_llama_calibrate(C.byref(d), ns, ep, h, t, C.byref(prm), C.byref(grd),
+                                    C.byref(opt), losses, FAKE, n.value, None)
+    assert call() == INVALID                        # found before any launch
+    assert call(ns=0) == INVALID and call(ep=0) == INVALID
+    assert call(losses=None) == INVALID
+    assert call(t=(C.c_void_p * 2)(0x10000, 0x10004)) == INVALID     # misaligned
+    opt.step = 0
+    assert call(t=(C.c_void_p * 2)(0x10000, 0x10000)) == INVALID
