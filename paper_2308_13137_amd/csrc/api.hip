@@ -780,7 +780,7 @@ SiteSizes site_sizes(const oq_block_desc* d, const SitePlan& p) {
   // a split forward's parts live there too (the weight gradient comes later)
   const int sf = fwd_splits(d, p);
   if (sf > 1) z.dW = std::max(z.dW, size_t(p.M * T) * size_t(sf));
-  if (fused_lwc(d, p)) z.gs = size_t(p.M * (p.C / d->lin_group[p.l0]));
+  if (fused_lwc(d, p)) z.gs = size_t(2 * p.M * (p.C / d->lin_group[p.l0]));
   z.parts = size_t(p.M * ntn);
   z.rows = size_t(p.M);
   if (p.let || p.act) z.xhat = size_t(T * p.C);
@@ -966,7 +966,7 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
       ProfScope ps(PK_LWC_FWD, st, double(co) * C * 2 * es);
       OQ_HIP(lwc_fwd(prm->W[l], bf, co, C, s, prm->gamma_logit[l], prm->beta_logit[l],
                      d->lin_bits[l], d->lin_group[l], static_cast<char*>(w.what) + off * C * es, bf,
-                     nullptr, nullptr, nullptr, st, fused ? w.gstat + off * ngs : nullptr,
+                     nullptr, nullptr, nullptr, st, fused ? w.gstat + 2 * off * ngs : nullptr,
                      d->lin_quant[l]),
              "lwc_fwd");
       la.row_begin[l] = row_base + off;
@@ -1059,8 +1059,6 @@ oq_status oq_block_calib_step(const oq_block_desc* d, const void* const* Y_fp_T,
           b += d->lin_c_out[l];
           la.seg_end[i] = b;
           la.W[i] = static_cast<const uint16_t*>(prm->W[l]);
-          la.gl[i] = prm->gamma_logit[l];
-          la.bl[i] = prm->beta_logit[l];
           la.dgl[i] = gr->d_gamma_logit[l];
           la.dbl[i] = gr->d_beta_logit[l];
         }

@@ -723,13 +723,14 @@ struct EpiLwc {
   OQ_DEV void split(int) {}
   // linear of stacked row m: constant indices only, so the argument block
   // stays in scalar registers
-  struct Seg { const uint16_t* w; const float* gl; const float* bl; float* dgl; float* dbl; int64_t o; };
+  // (o: m's row within its linear, b: the linear's first stacked row)
+  struct Seg { const uint16_t* w; float* dgl; float* dbl; int64_t o, b; };
   OQ_DEV Seg seg(int64_t m) const {
-    Seg s{a.W[0], a.gl[0], a.bl[0], a.dgl[0], a.dbl[0], m - a.seg_begin[0]};
+    Seg s{a.W[0], a.dgl[0], a.dbl[0], m - a.seg_begin[0], a.seg_begin[0]};
 #pragma unroll
     for (int i = 1; i < MAX_SEG; ++i) {
       if (i < a.nseg && m >= a.seg_begin[i]) {
-        s = Seg{a.W[i], a.gl[i], a.bl[i], a.dgl[i], a.dbl[i], m - a.seg_begin[i]};
+        s = Seg{a.W[i], a.dgl[i], a.dbl[i], m - a.seg_begin[i], a.seg_begin[i]};
       }
     }
     return s;
@@ -739,9 +740,12 @@ struct EpiLwc {
     const Seg s = seg(m);
     float w[8];
     load8(s.w + s.o * a.C + n, w);
-    const float4 st = a.gstat[m * a.ng + n / a.group];
-    const float r = div_rn(1.0f, st.z);
-    const float lo = -st.w, hi = a.qmax - st.w;
+    const int64_t gi = m * a.ng + n / a.group;
+    return chunk_terms(w, g, a.gstat[2 * gi].w, a.gstat[2 * gi + 1].z);
+  }
+  // the same from the chunk's weights, the group's z and 1/h
+  OQ_DEV float2 chunk_terms(const float* w, const float* g, float z, float r) const {
+    const float lo = -z, hi = a.qmax - z;
     float2 c = make_float2(0.f, 0.f);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -756,13 +760,14 @@ struct EpiLwc {
     }
     return c;
   }
-  // Eq. 2's parameters again from the group's max / min and the logits, then
-  // the logit gradients
-  OQ_DEV void finish(int64_t m, int gi, float sh, float sz) const {
-    const Seg s = seg(m);
-    const float4 st = a.gstat[m * a.ng + gi];
-    const int64_t k = s.o * a.ng + gi;
-    const QParams p = make_qparams(st.x, st.y, clip_strength(s.gl[k]), clip_strength(s.bl[k]), a.qmax);
+  // Eq. 2's parameters again from the group's max / min and the clip
+  // strengths the forward recorded, then the logit gradients
+  OQ_DEV void finish(int64_t m, int gi, float sh, float sz) const { finish_in(seg(m), m, gi, sh, sz); }
+  OQ_DEV void finish_in(const Seg& s, int64_t m, int gi, float sh, float sz) const {
+    const float4 st = a.gstat[2 * (m * a.ng + gi)];
+    const float4 gb = a.gstat[2 * (m * a.ng + gi) + 1];
+    const int64_t k = (m - s.b) * a.ng + gi;
+    const QParams p = make_qparams(st.x, st.y, gb.x, gb.y, a.qmax);
     const QGrad qg = quant_group_grad(sh, sz, st.x, st.y, p, a.qmax);
     s.dgl[k] = qg.dgamma * p.gamma * (1.0f - p.gamma);
     s.dbl[k] = qg.dbeta * p.beta * (1.0f - p.beta);
@@ -834,6 +839,88 @@ OQ_DEV void epilogue8_lwc(const f32x4_t (&acc)[8][4], const EpiLwc<G>& ep, int64
         }
         ep.finish(m, int(ng0 / ep.a.group), s.x, s.y);
       }
+    }
+  }
+}
+
+// Fused LWC epilogue, fast form, for a tile inside M and N whose rows all
+// belong to one linear: the linear is looked up once, and every weight chunk
+// and group record a lane needs (its 16 rows at constant strides) is loaded
+// before the accumulators are staged, so the epilogue waits on one round of
+// loads instead of one per pass.
+template <int G>
+OQ_DEV void epilogue8_lwc_fast(const f32x4_t (&acc)[8][4], const EpiLwc<G>& ep,
+                               const typename EpiLwc<G>::Seg& sg, int64_t m0, int64_t n0, int wave,
+                               int lane, float* scratch, float2 (*rowbuf)[BM]) {
+  constexpr int PITCH = EPI8_PITCH;
+  const LwcArgs& a = ep.a;
+  const int wm = wave >> 2, wn = wave & 3;
+  float* reg = scratch + wave * (32 * EPI8_PITCH);
+  const int fr = lane & 15, fk = lane >> 4;
+  const int cl = lane & 7, rl = lane >> 3;
+  const int64_t mr = m0 + wm * 128 + rl;     // this lane's first row; the others at 32 P + 8 it
+  const int64_t nb = n0 + wn * 64 + 8 * cl;
+  const int gi = int(nb / a.group);
+  const uint16_t* wl = sg.w + (mr - sg.b) * a.C + nb;
+  const float* rec = reinterpret_cast<const float*>(a.gstat) + 8 * (mr * a.ng + gi);
+  uint4 wv[4][4];
+  float zv[4][4], rv[4][4];
+#pragma unroll
+  for (int P = 0; P < 4; ++P)
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int64_t o = 32 * P + 8 * it;
+      wv[P][it] = *reinterpret_cast<const uint4*>(wl + o * a.C);
+      zv[P][it] = rec[8 * o * a.ng + 3];
+      rv[P][it] = rec[8 * o * a.ng + 6];
+    }
+#pragma unroll
+  for (int P = 0; P < 4; ++P) {
+#pragma unroll
+    for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          reg[(16 * ii + 4 * fk + r) * PITCH + 16 * j + fr] = acc[2 * P + ii][j][r];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int rloc = rl + 8 * it;
+      const int trow = wm * 128 + 32 * P + rloc;
+      const float4 lo = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl);
+      const float4 hi = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 8 * cl + 4);
+      const float g[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      const uint32_t ww[4] = {wv[P][it].x, wv[P][it].y, wv[P][it].z, wv[P][it].w};
+      float w[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        w[2 * e] = __uint_as_float(ww[e] << 16);
+        w[2 * e + 1] = __uint_as_float(ww[e] & 0xffff0000u);
+      }
+      float2 c = ep.chunk_terms(w, g, zv[P][it], rv[P][it]);
+      if constexpr (G <= 8) {
+        c.x = group_sum<G>(c.x);
+        c.y = group_sum<G>(c.y);
+        if (cl % G == 0) ep.finish_in(sg, m0 + trow, gi, c.x, c.y);
+      } else {
+        c.x = group_sum<8>(c.x);
+        c.y = group_sum<8>(c.y);
+        if (cl == 0) rowbuf[wn][trow] = c;
+      }
+    }
+  }
+  if constexpr (G > 8) {
+    constexpr int WPG = G / 8, GPR = 4 / WPG;
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < BM * GPR; idx += NTHR8) {
+      const int trow = idx / GPR, gq = idx % GPR;
+      float2 t = rowbuf[gq * WPG][trow];
+#pragma unroll
+      for (int w = 1; w < WPG; ++w) {
+        t.x += rowbuf[gq * WPG + w][trow].x;
+        t.y += rowbuf[gq * WPG + w][trow].y;
+      }
+      ep.finish_in(sg, m0 + trow, int((n0 + int64_t(gq) * WPG * 64) / a.group), t.x, t.y);
     }
   }
 }
@@ -976,10 +1063,16 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
   }
   __syncthreads();
   // epilogue staging (68 KiB) and row partials (8 KiB at 96 KiB) reuse the stages
-  if constexpr (IsLwc<Epi>::value)
-    epilogue8_lwc(acc, epi, m0, n0, M, N, wave, lane, reinterpret_cast<float*>(&lds[0]),
-                  reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304));
-  else {
+  if constexpr (IsLwc<Epi>::value) {
+    float* stg = reinterpret_cast<float*>(&lds[0]);
+    auto rows = reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304);
+    // the fast form when the tile is whole and within one linear (uniform)
+    const auto sg = epi.seg(m0);
+    if (m0 + BM <= M && n0 + BN <= N && epi.seg(m0 + BM - 1).b == sg.b)
+      epilogue8_lwc_fast(acc, epi, sg, m0, n0, wave, lane, stg, rows);
+    else
+      epilogue8_lwc(acc, epi, m0, n0, M, N, wave, lane, stg, rows);
+  } else {
     float* stg = reinterpret_cast<float*>(&lds[0]);
     auto rows = reinterpret_cast<float2 (*)[BM]>(reinterpret_cast<char*>(&lds[0]) + 98304);
     if constexpr (std::is_same<Epi, EpiResid<uint16_t>>::value) {

@@ -90,11 +90,9 @@ struct LwcArgs {
   int nseg;
   int64_t seg_begin[MAX_SEG], seg_end[MAX_SEG];
   const uint16_t* W[MAX_SEG];      // bf16 [rows_l, C]
-  const float* gl[MAX_SEG];        // [rows_l, ng] clip-strength logits
-  const float* bl[MAX_SEG];
   float* dgl[MAX_SEG];             // [rows_l, ng] outputs
   float* dbl[MAX_SEG];
-  const float4* gstat;             // [M, ng] {max, min, h, z} of each group
+  const float4* gstat;             // [M, ng] pairs {max, min, h, z}, {gamma, beta, 1/h, 0}
   int64_t C;
   int group, ng;
   float qmax;
@@ -107,7 +105,8 @@ hipError_t gemm_wgrad_lwc(const void* dyT, const void* x, int64_t M, int64_t C, 
 // ---------------------------------------------------------------- quantisers
 // LWC forward on rows [0, c_out) of one weight.  Returns hipErrorInvalidValue
 // when (c_in, group) is outside the supported set.
-// gstat (power-of-two groups without s only) receives {max, min, h, z} per group.
+// gstat (power-of-two groups without s only) receives two float4 per group:
+// {max, min, h, z} and {gamma, beta, 1/h, 0}.
 // quant: WQ_LWC (gl, bl = clip-strength logits), WQ_PACT (gl, bl = upper and
 // lower thresholds), WQ_LSQ (gl, bl = step and zero point); see common.h.
 hipError_t lwc_fwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, const float* s,

@@ -569,7 +569,10 @@ __global__ __launch_bounds__(NT) void lwc_fwd_coal_kernel(
       if (step * (U * NGW) + lane < ngroup) {
         if (hout) hout[g] = p.h;
         if (zout) zout[g] = p.z;
-        if (gstat) gstat[g] = make_float4(gmx, gmn, p.h, p.z);
+        if (gstat) {
+          gstat[2 * g] = make_float4(gmx, gmn, p.h, p.z);
+          gstat[2 * g + 1] = make_float4(p.gamma, p.beta, p.r, 0.0f);
+        }
       }
     }
 #pragma unroll
