@@ -624,12 +624,15 @@ OQ_DEV void epilogue8(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, in
 // staged, and the 8-lane row sums run on DPP (quad xor 1, quad xor 2, then
 // the half-row mirror: the same pairings as the butterfly, so the sums are
 // bit-identical to the general form's).
-OQ_DEV float group8_sum(float v) {
-  v += dpp_f(v, 0);
-  v += dpp_f(v, 1);
-  v += dpp_f(v, 2);
+template <int L>
+OQ_DEV float group_sum_dpp(float v) {
+  static_assert(L == 1 || L == 2 || L == 4 || L == 8, "groups of up to 8 lanes");
+  if constexpr (L >= 2) v += dpp_f(v, 0);
+  if constexpr (L >= 4) v += dpp_f(v, 1);
+  if constexpr (L >= 8) v += dpp_f(v, 2);
   return v;
 }
+OQ_DEV float group8_sum(float v) { return group_sum_dpp<8>(v); }
 
 OQ_DEV int resid_seg(const ResidArgs& a, int64_t m) {
   int s = 0;
@@ -898,13 +901,14 @@ OQ_DEV void epilogue8_lwc_fast(const f32x4_t (&acc)[8][4], const EpiLwc<G>& ep,
         w[2 * e + 1] = __uint_as_float(ww[e] & 0xffff0000u);
       }
       float2 c = ep.chunk_terms(w, g, zv[P][it], rv[P][it]);
+      // DPP sums with the butterfly's pairings (bit-identical)
       if constexpr (G <= 8) {
-        c.x = group_sum<G>(c.x);
-        c.y = group_sum<G>(c.y);
+        c.x = group_sum_dpp<G>(c.x);
+        c.y = group_sum_dpp<G>(c.y);
         if (cl % G == 0) ep.finish_in(sg, m0 + trow, gi, c.x, c.y);
       } else {
-        c.x = group_sum<8>(c.x);
-        c.y = group_sum<8>(c.y);
+        c.x = group_sum_dpp<8>(c.x);
+        c.y = group_sum_dpp<8>(c.y);
         if (cl == 0) rowbuf[wn][trow] = c;
       }
     }
