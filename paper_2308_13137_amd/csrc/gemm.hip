@@ -576,6 +576,42 @@ OQ_DEV void epi8_pass(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, in
   }
 }
 
+// fp32 store epilogue, fast form (a tile inside N, 16-byte access): a lane
+// stores columns 4 c .. 4 c + 3 and 32 + 4 c .. 32 + 4 c + 3 of its row, so
+// each store instruction writes 128 contiguous bytes per row (the general
+// form's 8 consecutive columns per lane make every instruction cover half of
+// each 32-byte piece).
+OQ_DEV void epilogue8_f32(const f32x4_t (&acc)[8][4], const EpiF32& epi, int64_t m0, int64_t n0,
+                          int64_t M, int wave, int lane, float* scratch) {
+  constexpr int PITCH = EPI8_PITCH;
+  const int wm = wave >> 2, wn = wave & 3;
+  float* reg = scratch + wave * (32 * PITCH);
+  const int fr = lane & 15, fk = lane >> 4;
+  const int cl = lane & 7, rl = lane >> 3;
+  float* cb = epi.C + (m0 + wm * 128 + rl) * epi.ldc + n0 + wn * 64 + 4 * cl;
+#pragma unroll
+  for (int P = 0; P < 4; ++P) {
+#pragma unroll
+    for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          reg[(16 * ii + 4 * fk + r) * PITCH + 16 * j + fr] = acc[2 * P + ii][j][r];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int rloc = rl + 8 * it;
+      if (m0 + wm * 128 + 32 * P + rloc < M) {
+        const float4 lo = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 4 * cl);
+        const float4 hi = *reinterpret_cast<const float4*>(reg + rloc * PITCH + 32 + 4 * cl);
+        float* c = cb + int64_t(32 * P + 8 * it) * epi.ldc;
+        *reinterpret_cast<float4*>(c) = lo;
+        *reinterpret_cast<float4*>(c + 32) = hi;
+      }
+    }
+  }
+}
+
 template <class Epi>
 OQ_DEV void epilogue8(const f32x4_t (&acc)[8][4], const Epi& epi, int64_t m0, int64_t n0,
                       int64_t M, int64_t N, int tn, int wave, int lane, float* scratch,
@@ -1090,6 +1126,12 @@ __global__ __launch_bounds__(NTHR8, 1) void gemm_bf16_w8_kernel(
           if (epi.a.part_dy) epilogue8_resid<false, true>(acc, epi, seg, m0, n0, tn, wave, lane, stg, rows);
           else epilogue8_resid<false, false>(acc, epi, seg, m0, n0, tn, wave, lane, stg, rows);
         }
+        return;
+      }
+    }
+    if constexpr (std::is_same<Epi, EpiF32>::value) {
+      if (epi.vec && n0 + BN <= N) {
+        epilogue8_f32(acc, epi, m0, n0, M, wave, lane, stg);
         return;
       }
     }
