@@ -206,14 +206,14 @@ __global__ __launch_bounds__(NT) void lwc_fwd_kernel(
 // Per group:  S_h = sum g*((q - z) - m*u),  S_z = sum g*(1 - m)  ->  dgamma, dbeta
 // per element: dW~ = g*m + [i = argmax] dmax + [i = argmin] dmin
 // per column (optional): partial sum over this block's rows of dW~ * W.
-template <typename TW, int KC, bool WHOLE_ROW, bool LETW>
-__global__ __launch_bounds__(NT) void lwc_bwd_kernel(
+template <typename TW, int KC, bool WHOLE_ROW, bool LETW, int NTB = NT>
+__global__ __launch_bounds__(NTB) void lwc_bwd_kernel(
     const TW* __restrict__ W, int64_t c_out, int64_t c_in, const float* __restrict__ s,
     const float* __restrict__ gl, const float* __restrict__ bl, int bits, int group, int R,
     const float* __restrict__ dW, float* __restrict__ dgl, float* __restrict__ dbl,
     float* __restrict__ dWt, float* __restrict__ ds_parts, int quant, float gs) {
-  __shared__ MinMax shm[NT / 64];
-  __shared__ float2 shs[NT / 64];
+  __shared__ MinMax shm[NTB / 64];
+  __shared__ float2 shs[NTB / 64];
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
   const int cpr = int(c_in / 8);
@@ -227,7 +227,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
   float sv[KS][8], dsacc[KS][8];
 #pragma unroll
   for (int k = 0; k < KS; ++k) {
-    const int j = tid + NT * k;
+    const int j = tid + NTB * k;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       sv[k][e] = 1.0f;
@@ -240,13 +240,13 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
   const int64_t r1 = min(c_out, r0 + R);
   // whole rows of up to two chunks per thread: the next row's W and dW^ are
   // loaded while this row is reduced (wider rows would spill)
-  constexpr bool PF = WHOLE_ROW && KC <= 2;
+  constexpr bool PF = WHOLE_ROW && KC <= (NTB >= 512 ? 4 : 2);
   Chunk8<TW> wn[KC];
   float gn[KC][8];
   auto issue = [&](int64_t row) {
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
-      const int j = tid + NT * k;
+      const int j = tid + NTB * k;
       if (j < cpr) {
         wn[k].load(W + row * c_in + 8 * j);
         load8(dW + row * c_in + 8 * j, gn[k]);
@@ -275,7 +275,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
       } else {
 #pragma unroll
         for (int k = 0; k < KC; ++k) {
-          const int j = tid + NT * k;
+          const int j = tid + NTB * k;
           if (j < cpr) {
             wc[k].load(wrow + 8 * j);
             load8(grow + 8 * j, g[k]);
@@ -289,7 +289,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
       };
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
-        const int j = tid + NT * k;
+        const int j = tid + NTB * k;
         if (j < cpr) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) minmax_add(st, wt_at(k, e), 8 * j + e);
@@ -300,7 +300,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
       lds_barrier();
       st = shm[0];
 #pragma unroll
-      for (int w8 = 1; w8 < NT / 64; ++w8) {
+      for (int w8 = 1; w8 < NTB / 64; ++w8) {
         sel_max(st.mx, st.imx, shm[w8].mx, shm[w8].imx);
         sel_min(st.mn, st.imn, shm[w8].mn, shm[w8].imn);
       }
@@ -308,7 +308,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
       float2 sums = make_float2(0.f, 0.f);
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
-        const int j = tid + NT * k;
+        const int j = tid + NTB * k;
         if (j < cpr) {
 #pragma unroll
           for (int e = 0; e < 8; ++e)
@@ -321,7 +321,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
       lds_barrier();
       sums = shs[0];
 #pragma unroll
-      for (int w8 = 1; w8 < NT / 64; ++w8) {
+      for (int w8 = 1; w8 < NTB / 64; ++w8) {
         sums.x += shs[w8].x;
         sums.y += shs[w8].y;
       }
@@ -333,7 +333,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
       if (LETW || dWt) {
 #pragma unroll
         for (int k = 0; k < KC; ++k) {
-          const int j = tid + NT * k;
+          const int j = tid + NTB * k;
           if (j < cpr) {
             // without LET only dW~ needs this pass: dW^ is read again rather
             // than kept live through the reductions
@@ -362,7 +362,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
     } else {
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
-        const int j = tid + NT * k;
+        const int j = tid + NTB * k;
         const bool valid = j < cpr;
         float w[8], wt[8], g[8];
         MinMax st = minmax_init();
@@ -418,7 +418,7 @@ __global__ __launch_bounds__(NT) void lwc_bwd_kernel(
   if (LETW && ds_parts) {
 #pragma unroll
     for (int k = 0; k < KS; ++k) {
-      const int j = tid + NT * k;
+      const int j = tid + NTB * k;
       if (j < cpr) store8(ds_parts + int64_t(blockIdx.x) * c_in + 8 * j, dsacc[k]);
     }
   }
@@ -1257,10 +1257,10 @@ int kc_for(int64_t cols) {
   return 0;
 }
 
-// Blocks of NT threads (with lds bytes of dynamic LDS each) that the current
+// Blocks of `threads` threads (with lds bytes of dynamic LDS each) that the current
 // device keeps resident at once: compute units times the kernel's occupancy,
 // cached per (kernel, LDS bytes, device).
-int resident_blocks(const void* kernel, size_t lds = 0) {
+int resident_blocks(const void* kernel, size_t lds = 0, int threads = NT) {
   struct Entry { const void* k; size_t lds; int dev, n; };
   static std::mutex mu;
   static std::vector<Entry> cache;
@@ -1273,7 +1273,7 @@ int resident_blocks(const void* kernel, size_t lds = 0) {
   }
   int cus = 0, per = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, NT, lds) != hipSuccess)
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, lds) != hipSuccess)
     return 1024;
   const int n = std::max(1, cus * per);
   std::lock_guard<std::mutex> g(mu);
@@ -1486,21 +1486,27 @@ hipError_t lwc_bwd(const void* W, bool w_bf16, int64_t c_out, int64_t c_in, cons
   const int kc = kc_for(c_in);
   auto go = [&](auto tw, auto kcc, auto wr) {
     using TW = decltype(tw);
-    constexpr int KCc = decltype(kcc)::value;
+    constexpr int KC0 = decltype(kcc)::value;
     constexpr bool WR = decltype(wr)::value;
+    // whole rows of more than two chunks per thread (wider than 4,096):
+    // 512-thread blocks, half the chunks per thread (11,008-wide rows
+    // measured 247 -> 173 us; 4,096-wide ones are faster at 256 threads)
+    constexpr int NTc = WR && KC0 >= 4 ? 512 : NT;
+    constexpr int KCc = NTc == 512 ? KC0 / 2 : KC0;
     if (s || ds_parts) {
       // the ds partials are one row per block: the block count is the fixed
       // lwc_bwd_nparts(c_out) the workspace was sized for
       const int R = rows_per_block(c_out, LWC_BLOCKS);
-      hipLaunchKernelGGL((lwc_bwd_kernel<TW, KCc, WR, true>), dim3(unsigned((c_out + R - 1) / R)),
-                         dim3(NT), 0, st, static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits,
+      hipLaunchKernelGGL((lwc_bwd_kernel<TW, KCc, WR, true, NTc>), dim3(unsigned((c_out + R - 1) / R)),
+                         dim3(NTc), 0, st, static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits,
                          int(group), R, dW, dgl, dbl, dW_tilde, ds_parts, quant, gs);
     } else {
       // no partials: one round of resident blocks
       const int R = rows_per_block(
-          c_out, resident_blocks(reinterpret_cast<const void*>(lwc_bwd_kernel<TW, KCc, WR, false>)));
-      hipLaunchKernelGGL((lwc_bwd_kernel<TW, KCc, WR, false>), dim3(unsigned((c_out + R - 1) / R)),
-                         dim3(NT), 0, st, static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits,
+          c_out, resident_blocks(reinterpret_cast<const void*>(lwc_bwd_kernel<TW, KCc, WR, false, NTc>),
+                                 0, NTc));
+      hipLaunchKernelGGL((lwc_bwd_kernel<TW, KCc, WR, false, NTc>), dim3(unsigned((c_out + R - 1) / R)),
+                         dim3(NTc), 0, st, static_cast<const TW*>(W), c_out, c_in, s, gl, bl, bits,
                          int(group), R, dW, dgl, dbl, dW_tilde, ds_parts, quant, gs);
     }
   };
