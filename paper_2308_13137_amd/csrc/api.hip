@@ -738,6 +738,33 @@ hipError_t site_streams(SiteStreams** out) {
   return hipSuccess;
 }
 
+// The whole-block step's weight side (weight gradients, LWC backward, LET
+// weight and bias paths) runs on a side stream of its own beside the input
+// gradients: one per device and host thread, kept for the life of the
+// process, with its fork and join events.
+struct BlockSide {
+  hipStream_t s;
+  hipEvent_t fork, join;
+  bool ok;
+};
+
+hipError_t block_side(BlockSide** out) {
+  thread_local BlockSide cache[16] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 16) return hipErrorInvalidDevice;
+  BlockSide& c = cache[dev];
+  if (!c.ok) {
+    if ((e = hipStreamCreateWithFlags(&c.s, hipStreamNonBlocking)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&c.fork, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&c.join, hipEventDisableTiming)) != hipSuccess) return e;
+    c.ok = true;
+  }
+  *out = &c;
+  return hipSuccess;
+}
+
 // Sites run concurrently (one stream each) at small token counts, where a
 // site's products leave CUs idle in their last wave of tiles; each site then
 // has its own buffers.  At large token counts the sites share one set.
@@ -1949,9 +1976,18 @@ oq_status oq_llama_block_step(const oq_llama_desc* d, const void* h0, const void
     OQ_HIP(block_loss(w.h2, target, T, D, w.dh2, w.dh2_16, w.rows, loss, st), "loss");
   }
   const int64_t npa = act_bwd_nparts(T);
-  // dX^ = dY W^ and dW^ = dY^T X^ of the linears [l0, l1) stacked on one
-  // site, then their LWC backward (with LET: the weight-path ds partials and
-  // the bias-path partials of ddelta); dy16 bf16 [T, M], xh bf16 [T, C].
+  // The weight side of each site runs on a side stream sw, forked from st
+  // once the site's dY is ready and joined back where its outputs are read
+  // (the LET finish, and before AdamW).  Its buffers (dW, the ds and bias
+  // partials, the column sums) are its own; the next site's weight side is
+  // forked after this site's LET finish, which reads them.
+  BlockSide* sd = nullptr;
+  OQ_HIP(block_side(&sd), "side stream");
+  const hipStream_t sw = sd->s;
+  // dX^ = dY W^ (on st) and dW^ = dY^T X^ (on sw) of the linears [l0, l1)
+  // stacked on one site, then their LWC backward (with LET: the weight-path
+  // ds partials and the bias-path partials of ddelta); dy16 bf16 [T, M],
+  // xh bf16 [T, C].
   int64_t npw = 0, npb = 0;
   auto linears_bwd = [&](int l0, int l1, const void* dy16, const void* wst, const void* xh,
                          float* dxh) -> oq_status {
@@ -1960,39 +1996,42 @@ oq_status oq_llama_block_step(const oq_llama_desc* d, const void* h0, const void
     int64_t M = 0;
     for (int l = l0; l < l1; ++l) M += m.c_out[l];
     const bool let_site = let && k < 3;
+    OQ_HIP(hipEventRecord(sd->fork, st), "fork");
+    OQ_HIP(hipStreamWaitEvent(sw, sd->fork, 0), "fork");
     {
       ProfScope ps(PK_GEMM_DGRAD, st, 2.0 * double(T) * M * C);
       oq_status e2 = llama_mm(w, dy16, false, wst, true, T, C, M, M, C, dxh, st, "input gradient");
       if (e2 != OQ_OK) return e2;
     }
     {
-      ProfScope ps(PK_GEMM_WGRAD, st, 2.0 * double(T) * M * C);
-      OQ_HIP(gemm_f32out_mn(dy16, true, xh, true, M, C, T, M, C, w.dW, C, st), "weight gradient");
+      ProfScope ps(PK_GEMM_WGRAD, sw, 2.0 * double(T) * M * C);
+      OQ_HIP(gemm_f32out_mn(dy16, true, xh, true, M, C, T, M, C, w.dW, C, sw), "weight gradient");
     }
     npw = npb = 0;
     int64_t off = 0;
     for (int l = l0; l < l1; ++l) {
-      ProfScope ps(PK_LWC_BWD, st, double(m.c_out[l]) * C * 6);
+      ProfScope ps(PK_LWC_BWD, sw, double(m.c_out[l]) * C * 6);
       OQ_HIP(lwc_bwd(p->W[l], true, m.c_out[l], C, let_site ? p->s[k] : nullptr, p->gamma_logit[l],
                      p->beta_logit[l], d->w_bits[l], d->w_group[l], w.dW + off * C,
                      g->d_gamma_logit[l], g->d_beta_logit[l], nullptr,
-                     let_site ? w.pw + npw * C : nullptr, st),
+                     let_site ? w.pw + npw * C : nullptr, sw),
              "lwc_bwd");
       if (let_site) npw += lwc_bwd_nparts(m.c_out[l]);
       off += m.c_out[l];
     }
     if (let_site) {
-      ProfScope ps(PK_OTHER, st, double(T) * M * 2 + double(M) * C * 2);
+      ProfScope ps(PK_OTHER, sw, double(T) * M * 2 + double(M) * C * 2);
       const int64_t nc = colstat_nparts(T);
-      OQ_HIP(colstat(dy16, true, T, M, w.amax, w.csum, st), "bias-path column sums");
-      OQ_HIP(colsum_finish(w.csum, nc, M, w.dbt, st), "bias-path finish");
+      OQ_HIP(colstat(dy16, true, T, M, w.amax, w.csum, sw), "bias-path column sums");
+      OQ_HIP(colsum_finish(w.csum, nc, M, w.dbt, sw), "bias-path finish");
       off = 0;
       for (int l = l0; l < l1; ++l) {
-        OQ_HIP(wcolsum(p->W[l], true, m.c_out[l], C, w.dbt + off, w.pb + npb * C, st), "bias path");
+        OQ_HIP(wcolsum(p->W[l], true, m.c_out[l], C, w.dbt + off, w.pb + npb * C, sw), "bias path");
         npb += wcolsum_nparts(m.c_out[l]);
         off += m.c_out[l];
       }
     }
+    OQ_HIP(hipEventRecord(sd->join, sw), "join");
     return OQ_OK;
   };
   // through Q_a and the LET transform of site k: dxt = dL/dX~ (and the LET
@@ -2006,10 +2045,12 @@ oq_status oq_llama_block_step(const oq_llama_desc* d, const void* h0, const void
                      let_site ? w.ps1 : nullptr, st, sym),
              "act_bwd");
     }
-    if (let_site)
+    if (let_site) {
+      OQ_HIP(hipStreamWaitEvent(st, sd->join, 0), "join");
       OQ_HIP(let_grad_finish(C, p->s[k], w.pw, npw, w.psx, w.ps1, npa, w.pb, npb, g->d_s[k],
                              g->d_delta[k], st),
              "LET finish");
+    }
     return OQ_OK;
   };
   // ---- feed-forward half
@@ -2052,6 +2093,8 @@ oq_status oq_llama_block_step(const oq_llama_desc* d, const void* h0, const void
          "qkv epilogue backward");
   if ((e = linears_bwd(0, 3, w.dqkv16, w.wqkv, w.xh1, w.dxh)) != OQ_OK) return e;
   if ((e = site_bwd(0, w.x1, D, w.dxh, w.dxt)) != OQ_OK) return e;
+  // the last weight side (the clipping-logit gradients of q, k, v) back on st
+  OQ_HIP(hipStreamWaitEvent(st, sd->join, 0), "join");
   // ---- AdamW over every trained tensor
   if (opt) {
     const AdamCoef cl = adam_coef(opt->lr_lwc, opt->beta1, opt->beta2, opt->eps, opt->wd, opt->step);
