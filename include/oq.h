@@ -547,6 +547,11 @@ oq_status oq_attention_bwd(const void* Q, const void* K, const void* V, const vo
  * Supported: head_dim D/H in {64, 128}; S a multiple of 64; T a multiple of
  * S; H a multiple of Hkv; every linear's c_in a multiple of 64; bits 2..8,
  * groups as oq_lwc_fakequant_fwd.  Workspace: oq_llama_workspace_size.
+ * The step's backward runs each site's weight side (weight gradient, LWC
+ * backward, LET weight and bias paths) on a side stream (non-blocking,
+ * default priority, created once per device and host thread) forked from
+ * `stream` and joined back to it before the step returns, so the step
+ * orders on `stream` like one launch.
  */
 #define OQ_LLAMA_LINEARS 7   /* q, k, v, o, gate, up, down */
 typedef struct {
