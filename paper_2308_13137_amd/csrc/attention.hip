@@ -243,6 +243,150 @@ __global__ __launch_bounds__(ANT) void attn_fwd_kernel(const bf16raw* __restrict
   if (fk == 0) LSE[int64_t(h) * T + row0 + qrow] = m + log2f(l);
 }
 
+// The same forward with 32 queries per wave (128 per workgroup, S a multiple
+// of 128): every K and V fragment read from LDS feeds two matrix
+// instructions, one per 16-query half, which halves the LDS traffic per
+// instruction.  Arithmetic per query is the kernel's above, unchanged.
+template <int DH>
+__global__ __launch_bounds__(ANT) void attn_fwd2_kernel(const bf16raw* __restrict__ Q,
+                                                        const bf16raw* __restrict__ K,
+                                                        const bf16raw* __restrict__ V, int S,
+                                                        int H, int Hkv, float* __restrict__ O,
+                                                        float* __restrict__ LSE, int64_t T) {
+  constexpr int KS = DH / 32;
+  constexpr int JD = DH / 16;
+  constexpr int NR = AT * DH / 8 / ANT;
+  constexpr int QW = 2 * AT;                           // queries per workgroup
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  __shared__ uint4 sK[AT * DH / 8];
+  __shared__ uint4 sV[AT * DH / 8];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int fr = lane & 15, fk = lane >> 4;
+  const int nq = S / QW;
+  const int qt = nq - 1 - int(blockIdx.x);             // longest tiles first
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int g = h / (H / Hkv);
+  const int64_t ldq = int64_t(H) * DH, ldk = int64_t(Hkv) * DH;
+  const int64_t row0 = int64_t(b) * S;
+  int qrow[2];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) qrow[hh] = qt * QW + 32 * wave + 16 * hh + fr;
+  const float sc = 1.4426950408889634f / sqrtf(float(DH));
+  const bf16x2_t ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+  bf16x8_t qf[2][KS];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const bf16raw* qp = Q + (row0 + qrow[hh]) * ldq + int64_t(h) * DH;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qf[hh][ks] = bits_as_bf16x8(*reinterpret_cast<const uint4*>(qp + 32 * ks + 8 * fk));
+  }
+  f32x4_t acc[2][JD];
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+    for (int j = 0; j < JD; ++j) acc[hh][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f}, l_b[2] = {0.f, 0.f};
+  u32x4_t kr[NR], vr[NR];
+  tile_to_regs<DH>(kr, K + row0 * ldk + int64_t(g) * DH, ldk, tid);
+  tile_to_regs<DH>(vr, V + row0 * ldk + int64_t(g) * DH, ldk, tid);
+  const int nk = 2 * qt + 2;                           // key tiles up to the diagonal
+  for (int kt = 0; kt < nk; ++kt) {
+    __syncthreads();
+    regs_to_k<DH>(sK, kr, tid);
+    regs_to_v<DH>(sV, vr, tid);
+    __syncthreads();
+    {
+      const int64_t krow = row0 + int64_t(kt + 1 < nk ? kt + 1 : kt) * AT;
+      tile_to_regs<DH>(kr, K + krow * ldk + int64_t(g) * DH, ldk, tid);
+      tile_to_regs<DH>(vr, V + krow * ldk + int64_t(g) * DH, ldk, tid);
+    }
+    // S^T [64 keys x 16 queries] per half: lane holds key 16 i + 4 fk + r, query fr
+    f32x4_t st[2][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      st[0][i] = st[1][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8_t kf = read_rm<DH>(sK, 16 * i + fr, 4 * ks + fk);
+        st[0][i] = mfma(kf, qf[0][ks], st[0][i]);
+        st[1][i] = mfma(kf, qf[1][ks], st[1][i]);
+      }
+    }
+    if (kt >= 2 * qt) {                                // the tiles the diagonal crosses
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (kt * AT + 16 * i + 4 * fk + r > qrow[hh]) st[hh][i][r] = -INFINITY;
+    }
+    bf16x8_t pb[2][2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      float mt = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        mt = fmaxf(fmaxf(mt, fmaxf(st[hh][i][0], st[hh][i][1])), fmaxf(st[hh][i][2], st[hh][i][3]));
+      mt = fmaxf(mt, __shfl_xor(mt, 16));
+      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      const float mn = fmaxf(m[hh], ceilf(mt * sc));
+      float ls = 0.f, lr = 0.f;
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int i = 2 * k2 + (e >> 1), r0 = 2 * (e & 1);
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(st[hh][i][r0], sc, -mn));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(st[hh][i][r0 + 1], sc, -mn));
+          ls += p0 + p1;
+          w[e] = pack2(p0, p1);
+          lr = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w[e]), ones, lr, false);
+        }
+        pb[hh][k2] = bits_as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+      }
+      ls += __shfl_xor(ls, 16);
+      ls += __shfl_xor(ls, 32);
+      lr += __shfl_xor(lr, 16);
+      lr += __shfl_xor(lr, 32);
+      if (__any(mn != m[hh])) {
+        // a row whose first tile is wholly masked keeps m = -inf until its
+        // first key arrives: alpha 0 leaves its (zero) sums as they are
+        const float alpha = m[hh] == -INFINITY ? 0.0f : ldexpf(1.0f, int(m[hh] - mn));
+        l[hh] *= alpha;
+        l_b[hh] *= alpha;
+#pragma unroll
+        for (int j = 0; j < JD; ++j) acc[hh][j] = acc[hh][j] * alpha;
+      }
+      l[hh] += ls;
+      l_b[hh] += lr;
+      m[hh] = mn;
+    }
+#pragma unroll
+    for (int j = 0; j < JD; ++j)
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        const bf16x8_t vf = v_frag<DH>(sV, j, k2, lane);
+        acc[0][j] = mfma(vf, pb[0][k2], acc[0][j]);
+        acc[1][j] = mfma(vf, pb[1][k2], acc[1][j]);
+      }
+  }
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh) {
+    const float inv = 1.0f / l_b[hh];
+    float* op = O + (row0 + qrow[hh]) * ldq + int64_t(h) * DH;
+#pragma unroll
+    for (int j = 0; j < JD; ++j)
+      *reinterpret_cast<float4*>(op + 16 * j + 4 * fk) =
+          make_float4(acc[hh][j][0] * inv, acc[hh][j][1] * inv, acc[hh][j][2] * inv,
+                      acc[hh][j][3] * inv);
+    if (fk == 0) LSE[int64_t(h) * T + row0 + qrow[hh]] = m[hh] + log2f(l[hh]);
+  }
+}
+
 // ------------------------------------------------------------------ forward, quantised softmax
 // The ablation on softmax quantisation: every query row of probabilities
 // goes through Q_a (per-row asymmetric MinMax, the activation quantiser's
@@ -822,6 +966,9 @@ hipError_t attn_fwd_t(const void* Q, const void* K, const void* V, int64_t T, in
   if (p_bits < 16)
     hipLaunchKernelGGL(attn_fwd_q_kernel<DH>, grid, dim3(ANT), 0, st, q, k, v, S, H, Hkv, p_bits,
                        O, LSE, pstat, T);
+  else if (S % (2 * AT) == 0)
+    hipLaunchKernelGGL(attn_fwd2_kernel<DH>, dim3(unsigned(S / (2 * AT)), unsigned(H), unsigned(T / S)),
+                       dim3(ANT), 0, st, q, k, v, S, H, Hkv, O, LSE, T);
   else
     hipLaunchKernelGGL(attn_fwd_kernel<DH>, grid, dim3(ANT), 0, st, q, k, v, S, H, Hkv, O, LSE, T);
   return hipGetLastError();
