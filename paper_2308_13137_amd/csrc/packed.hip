@@ -340,6 +340,23 @@ int resident(const void* kernel, size_t lds) {
   return n;
 }
 
+// Lets the kernel take up to PL_LDS_MAX bytes of dynamic LDS on the current
+// device (once per kernel and device).
+hipError_t allow_lds(const void* kernel) {
+  struct Entry { const void* k; int dev; };
+  static std::mutex mu;
+  static std::vector<Entry> done;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> g(mu);
+  for (const Entry& d : done)
+    if (d.k == kernel && d.dev == dev) return hipSuccess;
+  e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, int(PL_LDS_MAX));
+  if (e == hipSuccess) done.push_back(Entry{kernel, dev});
+  return e;
+}
+
 // ------------------------------------------------------------------ the linear on matrix cores
 // For batches of 8 or more tokens and groups of 128 codes.  A workgroup owns
 // 16 output rows; its eight waves take the row's groups g = wave, wave + 8, ...
@@ -348,24 +365,96 @@ int resident(const void* kernel, size_t lds) {
 // codes 8 m .. 8 m + 7 of each lane's run, widened to 128 + q in bf16 (exact),
 // with the activations of the same columns, 32 (4 g + f) + 8 m + e, as its B
 // operand: the group's p = sum x (128 + q) for 16 rows x 16 tokens, fp32.  The
-// lanes also sum those activations (xs = sum x), and the group contributes
+// lanes also sum those activations (xs = sum x), and the group adds
 // h (p - (128 + z) xs) to each output, in fp32, as in the VALU kernel.  The
 // eight waves' partial outputs are added in fixed order through LDS.
+//
+// Activations reach the B operand through LDS: each wave copies a group's
+// 16-token x 128-channel block (4 KiB) with four global_load_lds_dwordx4, one
+// instruction per four tokens, so every instruction reads four whole 256-byte
+// token rows (a 16-lane B operand read straight from global memory would touch
+// sixteen rows 8 KiB apart).  In LDS token t's 16-byte chunk c sits in slot
+// c ^ t of the token's 256 bytes, so the lanes of one fragment read hit
+// distinct banks.  Each wave double-buffers its blocks: the copies of group
+// g + 8 are in flight while group g computes.
 constexpr int PM_THREADS = 512;                // 8 waves share a tile's groups
+constexpr int PM_WAVES = PM_THREADS / 64;
 constexpr int PM_GROUP = 128;
+constexpr int PM_XBLOCK = 16 * PM_GROUP * 2;   // bytes of one group's 16-token block
+
+// 16 bytes per lane, global -> LDS (lane l's bytes land at LDS byte address
+// lds + 16 l); inline assembly, so the kernel waits for it (vmcnt) itself.
+// m0 (the copy's LDS base) is saved and restored around it, with one wait
+// state between its write and the copy that reads it.
+OQ_DEV void copy16_lds(const void* g, uint32_t lds) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %2, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(m0v), "v"(g)
+      : "memory");
+}
+OQ_DEV void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+OQ_DEV uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
+      (__attribute__((address_space(3))) const char*)(p)));
+}
+
+// dynamic LDS of the kernel: h and z of 16 rows, then two activation blocks
+// per wave and 16-token block (the partial-output exchange reuses them)
+size_t mfma_lds(int ntb, int64_t c_in) {
+  return size_t(2 * 16) * size_t(c_in / PM_GROUP) * sizeof(float) +
+         size_t(PM_WAVES) * 2 * size_t(ntb) * PM_XBLOCK;
+}
+
 template <int BITS, int NTB>
 __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
     const uint16_t* __restrict__ X, int n_tok, int64_t c_in, const uint32_t* __restrict__ packed,
     const float* __restrict__ h, const float* __restrict__ z, const float* __restrict__ bias,
     int64_t c_out, void* __restrict__ Y, bool y_bf16) {
-  __shared__ float red[PM_THREADS / 64][NTB * 16][17];
-  // h and z of the workgroup's 16 rows (one contiguous block of each)
-  extern __shared__ float hz[];
+  constexpr int XB = NTB * PM_XBLOCK;          // one wave's buffer: a group's NTB blocks
+  extern __shared__ float lds[];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int f = lane >> 4, i = lane & 15;
   const int64_t o0 = int64_t(blockIdx.x) * 16;
   const int ng = int(c_in / PM_GROUP);
   const int64_t runs_row = c_in / 32;
+  float* hz = lds;                             // [2][16][ng]: h, then 128 + z
+  char* xbuf = reinterpret_cast<char*>(lds + 32 * ng) + size_t(wave) * 2 * XB;
+  // this lane's A row (rows past c_out re-read the last row and store nothing)
+  const int64_t arow = min(o0 + i, c_out - 1);
+  const uint32_t* prow = packed + arow * runs_row * BITS;
+
+  // copies of group g's activations into buffer b: instruction j of block tb
+  // carries tokens 16 tb + 4 j .. + 3 (lane l: token 4 j + l / 16 of the
+  // block, slot l % 16 holding chunk (l % 16) ^ token).  Instructions whose
+  // tokens all lie past n_tok are skipped; single tokens past it read the
+  // last token: they only feed accumulator columns that are never stored.
+  auto stage = [&](int g, int b) {
+#pragma unroll
+    for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t0 = 16 * tb + 4 * j;
+        if (t0 < n_tok) {
+          const int tt = 4 * j + (lane >> 4);
+          const int t = min(16 * tb + tt, n_tok - 1);
+          const int c = (lane & 15) ^ tt;
+          copy16_lds(X + int64_t(t) * c_in + PM_GROUP * int64_t(g) + 8 * c,
+                     lds_addr(xbuf + b * XB + tb * PM_XBLOCK + j * 1024));
+        }
+      }
+  };
+  uint32_t wn[BITS];
+  if (wave < ng) {
+    stage(wave, 0);
+    load_run<BITS>(prow + (4 * int64_t(wave) + f) * BITS, wn);
+  }
   {
     const int64_t nrow = min<int64_t>(16, c_out - o0);
     for (int e = tid; e < 16 * ng; e += PM_THREADS) {
@@ -375,44 +464,21 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
     }
   }
   __syncthreads();
-  // this lane's A row (rows past c_out re-read the last row and store nothing)
-  const int64_t arow = min(o0 + i, c_out - 1);
-  const uint32_t* prow = packed + arow * runs_row * BITS;
-  // the token of this lane's B operand and accumulator column, per 16-token block
-  const uint16_t* xrow[NTB];
-  bool tok_ok[NTB];
-#pragma unroll
-  for (int tb = 0; tb < NTB; ++tb) {
-    const int t = 16 * tb + i;
-    tok_ok[tb] = t < n_tok;
-    xrow[tb] = X + int64_t(tok_ok[tb] ? t : 0) * c_in;
-  }
   f32x4_t y[NTB];
 #pragma unroll
   for (int tb = 0; tb < NTB; ++tb) y[tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // the next group's codes and activations are loaded while this one computes
-  uint32_t wn[BITS];
-  uint4 xn[4][NTB];
-  auto fetch = [&](int g) {
-    load_run<BITS>(prow + (4 * int64_t(g) + f) * BITS, wn);
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-      for (int tb = 0; tb < NTB; ++tb)
-        xn[m][tb] = *reinterpret_cast<const uint4*>(xrow[tb] + 32 * (4 * int64_t(g) + f) + 8 * m);
-  };
-  if (wave < ng) fetch(wave);
-  for (int g = wave; g < ng; g += PM_THREADS / 64) {
+  int b = 0;
+  for (int g = wave; g < ng; g += PM_WAVES, b ^= 1) {
+    // group g's copies and codes, issued one turn ago, have landed
+    wait_vm0();
     uint32_t w[BITS];
-    uint4 xg[4][NTB];
 #pragma unroll
     for (int k = 0; k < BITS; ++k) w[k] = wn[k];
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-      for (int tb = 0; tb < NTB; ++tb) xg[m][tb] = xn[m][tb];
-    if (g + PM_THREADS / 64 < ng) fetch(g + PM_THREADS / 64);
+    if (g + PM_WAVES < ng) {
+      stage(g + PM_WAVES, b ^ 1);
+      load_run<BITS>(prow + (4 * int64_t(g + PM_WAVES) + f) * BITS, wn);
+    }
     float hr[4], zr[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -426,6 +492,7 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
       acc[tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       xs[tb] = 0.f;
     }
+    const char* xb = xbuf + b * XB + i * 256;
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       uint32_t a[4];
@@ -436,8 +503,8 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
       const bf16x8_t av = __builtin_bit_cast(bf16x8_t, make_uint4(a[0], a[1], a[2], a[3]));
 #pragma unroll
       for (int tb = 0; tb < NTB; ++tb) {
-        uint4 xv = xg[m][tb];
-        if (!tok_ok[tb]) xv = make_uint4(0u, 0u, 0u, 0u);
+        const uint4 xv =
+            *reinterpret_cast<const uint4*>(xb + tb * PM_XBLOCK + 16 * ((4 * f + m) ^ i));
         acc[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8_t, xv),
                                                           acc[tb], 0, 0, 0);
         xs[tb] = dot2_bf16(xv.x, 0x3f803f80u, xs[tb]);
@@ -456,19 +523,23 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
       for (int r = 0; r < 4; ++r) y[tb][r] += hr[r] * (acc[tb][r] - zr[r] * s);
     }
   }
-  // lane (f, i) holds rows 4 f + r of the tile for token 16 tb + i
+  // every wave's copies have landed (each waited before its last group), so
+  // the activation buffers can hold the partial outputs: lane (f, i) holds
+  // rows 4 f + r of the tile for token 16 tb + i
+  __syncthreads();
+  float* red = lds + 32 * ng;                  // [PM_WAVES][NTB * 16][17]
 #pragma unroll
   for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) red[wave][16 * tb + i][4 * f + r] = y[tb][r];
+    for (int r = 0; r < 4; ++r) red[(wave * NTB * 16 + 16 * tb + i) * 17 + 4 * f + r] = y[tb][r];
   __syncthreads();
   for (int e = tid; e < NTB * 16 * 16; e += PM_THREADS) {
     const int t = e / 16, rr = e % 16;
     const int64_t o = o0 + rr;
     if (t < n_tok && o < c_out) {
-      float v = red[0][t][rr];
+      float v = red[t * 17 + rr];
 #pragma unroll
-      for (int w8 = 1; w8 < PM_THREADS / 64; ++w8) v += red[w8][t][rr];
+      for (int w8 = 1; w8 < PM_WAVES; ++w8) v += red[(w8 * NTB * 16 + t) * 17 + rr];
       if (bias) v += bias[o];
       if (y_bf16) static_cast<uint16_t*>(Y)[int64_t(t) * c_out + o] = f2bf(v);
       else static_cast<float*>(Y)[int64_t(t) * c_out + o] = v;
@@ -480,10 +551,14 @@ template <int BITS, int NTB>
 hipError_t launch_mfma(const uint16_t* X, int n_tok, int64_t c_in, const uint8_t* packed,
                        const float* h, const float* z, const float* bias, int64_t c_out, void* Y,
                        bool y_bf16, hipStream_t stream) {
-  const size_t lds = size_t(2 * 16) * size_t(c_in / PM_GROUP) * sizeof(float);
-  hipLaunchKernelGGL((packed_mfma_kernel<BITS, NTB>), dim3(unsigned((c_out + 15) / 16)),
-                     dim3(PM_THREADS), lds, stream, X, n_tok, c_in,
-                     reinterpret_cast<const uint32_t*>(packed), h, z, bias, c_out, Y, y_bf16);
+  auto k = packed_mfma_kernel<BITS, NTB>;
+  const size_t lds = mfma_lds(NTB, c_in);
+  if (lds > 64 * 1024) {
+    const hipError_t e = allow_lds(reinterpret_cast<const void*>(k));
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k, dim3(unsigned((c_out + 15) / 16)), dim3(PM_THREADS), lds, stream, X, n_tok,
+                     c_in, reinterpret_cast<const uint32_t*>(packed), h, z, bias, c_out, Y, y_bf16);
   return hipGetLastError();
 }
 
@@ -508,16 +583,16 @@ hipError_t linear_bits(const uint16_t* X, int64_t n_tok, int64_t c_in, const uin
                        int64_t c_out, void* Y, bool y_bf16, hipStream_t stream) {
   const size_t es = y_bf16 ? 2 : 4;
   if (n_tok >= PM_MIN_TOKENS && group == PM_GROUP) {
-    // matrix cores: launches of up to 16, 32 or 64 tokens
+    // matrix cores: launches of up to 32 tokens, or 16 where two blocks
+    // of 32 tokens exceed LDS
+    const int most = mfma_lds(2, c_in) <= PL_LDS_MAX ? 32 : 16;
     for (int64_t t0 = 0; t0 < n_tok;) {
-      const int64_t rem = n_tok - t0;
-      const int take = int(std::min<int64_t>(rem, 64));
+      const int take = int(std::min<int64_t>(n_tok - t0, most));
       const uint16_t* x = X + t0 * c_in;
       void* y = static_cast<char*>(Y) + size_t(t0) * size_t(c_out) * es;
-      hipError_t e;
-      if (take <= 16) e = launch_mfma<BITS, 1>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
-      else if (take <= 32) e = launch_mfma<BITS, 2>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
-      else e = launch_mfma<BITS, 4>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
+      const hipError_t e =
+          take <= 16 ? launch_mfma<BITS, 1>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream)
+                     : launch_mfma<BITS, 2>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
       if (e != hipSuccess) return e;
       t0 += take;
     }

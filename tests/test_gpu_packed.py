@@ -88,7 +88,7 @@ LINEAR = [
     (3, 1, 33, 11008, 11008, False, torch.float32, 0),
     # the widest input: one token per launch fits LDS, so 3 tokens are 3 launches
     (4, 3, 7, 65536, 128, False, torch.float32, 0),
-    # matrix cores (8+ tokens, groups of 128): 16-, 32- and 64-token launches,
+    # matrix cores (8+ tokens, groups of 128): 16- and 32-token launches,
     # 70 = 64 + 6 tokens, ragged rows, the 7B shapes, every code width
     (4, 16, 4096, 4096, 128, True, torch.float32, 0),
     (4, 64, 1000, 11008, 128, False, torch.float32, 0),
@@ -97,6 +97,10 @@ LINEAR = [
     (5, 20, 17, 256, 128, True, torch.float32, 2),
     (6, 9, 40, 384, 128, False, torch.float32, 0),
     (7, 24, 33, 128, 128, True, torch.float32, 0),
+    # the widest inputs on matrix cores: 32-token launches fill LDS exactly at
+    # 32768 channels (40 = 32 + 8); at 65536 launches take 16 tokens (20 = 16 + 4)
+    (4, 40, 7, 32768, 128, True, torch.float32, 0),
+    (3, 20, 5, 65536, 128, False, torch.bfloat16, 0),
 ]
 
 
