@@ -380,7 +380,6 @@ hipError_t allow_lds(const void* kernel) {
 constexpr int PM_THREADS = 512;                // 8 waves share a tile's groups
 constexpr int PM_WAVES = PM_THREADS / 64;
 constexpr int PM_GROUP = 128;
-constexpr int PM_XBLOCK = 16 * PM_GROUP * 2;   // bytes of one group's 16-token block
 
 // 16 bytes per lane, global -> LDS (lane l's bytes land at LDS byte address
 // lds + 16 l); inline assembly, so the kernel waits for it (vmcnt) itself.
@@ -406,18 +405,23 @@ OQ_DEV uint32_t lds_addr(const void* p) {
 }
 
 // dynamic LDS of the kernel: h and z of 16 rows, then two activation blocks
-// per wave and 16-token block (the partial-output exchange reuses them)
-size_t mfma_lds(int ntb, int64_t c_in) {
+// per wave and 16-token block, of tpb staged tokens each (the partial-output
+// exchange reuses them)
+size_t mfma_lds(int ntb, int tpb, int64_t c_in) {
   return size_t(2 * 16) * size_t(c_in / PM_GROUP) * sizeof(float) +
-         size_t(PM_WAVES) * 2 * size_t(ntb) * PM_XBLOCK;
+         size_t(PM_WAVES) * 2 * size_t(ntb) * size_t(tpb) * PM_GROUP * 2;
 }
 
-template <int BITS, int NTB>
+// NTB blocks of 16 tokens; TPB = 8 stages only the first 8 tokens of the
+// block (batches of at most 8: half the LDS, so more workgroups per CU)
+template <int BITS, int NTB, int TPB>
 __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
     const uint16_t* __restrict__ X, int n_tok, int64_t c_in, const uint32_t* __restrict__ packed,
     const float* __restrict__ h, const float* __restrict__ z, const float* __restrict__ bias,
     int64_t c_out, void* __restrict__ Y, bool y_bf16) {
-  constexpr int XB = NTB * PM_XBLOCK;          // one wave's buffer: a group's NTB blocks
+  static_assert(TPB == 16 || (TPB == 8 && NTB == 1), "staged tokens per block");
+  constexpr int XBLK = TPB * PM_GROUP * 2;     // bytes of one group's block
+  constexpr int XB = NTB * XBLK;               // one wave's buffer: a group's NTB blocks
   extern __shared__ float lds[];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int f = lane >> 4, i = lane & 15;
@@ -439,14 +443,14 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < TPB / 4; ++j) {
         const int t0 = 16 * tb + 4 * j;
         if (t0 < n_tok) {
           const int tt = 4 * j + (lane >> 4);
           const int t = min(16 * tb + tt, n_tok - 1);
           const int c = (lane & 15) ^ tt;
           copy16_lds(X + int64_t(t) * c_in + PM_GROUP * int64_t(g) + 8 * c,
-                     lds_addr(xbuf + b * XB + tb * PM_XBLOCK + j * 1024));
+                     lds_addr(xbuf + b * XB + tb * XBLK + j * 1024));
         }
       }
   };
@@ -492,7 +496,9 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
       acc[tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       xs[tb] = 0.f;
     }
-    const char* xb = xbuf + b * XB + i * 256;
+    // columns past the staged tokens (TPB = 8) re-read tokens 0..7: never stored
+    const int ti = i & (TPB - 1);
+    const char* xb = xbuf + b * XB + ti * 256;
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       uint32_t a[4];
@@ -504,7 +510,7 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
 #pragma unroll
       for (int tb = 0; tb < NTB; ++tb) {
         const uint4 xv =
-            *reinterpret_cast<const uint4*>(xb + tb * PM_XBLOCK + 16 * ((4 * f + m) ^ i));
+            *reinterpret_cast<const uint4*>(xb + tb * XBLK + 16 * ((4 * f + m) ^ ti));
         acc[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8_t, xv),
                                                           acc[tb], 0, 0, 0);
         xs[tb] = dot2_bf16(xv.x, 0x3f803f80u, xs[tb]);
@@ -547,12 +553,12 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
   }
 }
 
-template <int BITS, int NTB>
+template <int BITS, int NTB, int TPB>
 hipError_t launch_mfma(const uint16_t* X, int n_tok, int64_t c_in, const uint8_t* packed,
                        const float* h, const float* z, const float* bias, int64_t c_out, void* Y,
                        bool y_bf16, hipStream_t stream) {
-  auto k = packed_mfma_kernel<BITS, NTB>;
-  const size_t lds = mfma_lds(NTB, c_in);
+  auto k = packed_mfma_kernel<BITS, NTB, TPB>;
+  const size_t lds = mfma_lds(NTB, TPB, c_in);
   if (lds > 64 * 1024) {
     const hipError_t e = allow_lds(reinterpret_cast<const void*>(k));
     if (e != hipSuccess) return e;
@@ -584,15 +590,16 @@ hipError_t linear_bits(const uint16_t* X, int64_t n_tok, int64_t c_in, const uin
   const size_t es = y_bf16 ? 2 : 4;
   if (n_tok >= PM_MIN_TOKENS && group == PM_GROUP) {
     // matrix cores: launches of up to 32 tokens, or 16 where two blocks
-    // of 32 tokens exceed LDS
-    const int most = mfma_lds(2, c_in) <= PL_LDS_MAX ? 32 : 16;
+    // of 32 tokens exceed LDS; batches of at most 8 stage 8 tokens per group
+    const int most = mfma_lds(2, 16, c_in) <= PL_LDS_MAX ? 32 : 16;
     for (int64_t t0 = 0; t0 < n_tok;) {
       const int take = int(std::min<int64_t>(n_tok - t0, most));
       const uint16_t* x = X + t0 * c_in;
       void* y = static_cast<char*>(Y) + size_t(t0) * size_t(c_out) * es;
       const hipError_t e =
-          take <= 16 ? launch_mfma<BITS, 1>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream)
-                     : launch_mfma<BITS, 2>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
+          take <= 8    ? launch_mfma<BITS, 1, 8>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream)
+          : take <= 16 ? launch_mfma<BITS, 1, 16>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream)
+                       : launch_mfma<BITS, 2, 16>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
       if (e != hipSuccess) return e;
       t0 += take;
     }

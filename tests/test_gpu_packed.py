@@ -101,6 +101,10 @@ LINEAR = [
     # 32768 channels (40 = 32 + 8); at 65536 launches take 16 tokens (20 = 16 + 4)
     (4, 40, 7, 32768, 128, True, torch.float32, 0),
     (3, 20, 5, 65536, 128, False, torch.bfloat16, 0),
+    # more 16-row workgroups than CUs (8, 12 and 40 tokens)
+    (4, 8, 4200, 1024, 128, False, torch.float32, 0),
+    (5, 12, 4113, 512, 128, True, torch.bfloat16, 1),
+    (4, 40, 4352, 640, 128, True, torch.float32, 0),
 ]
 
 
