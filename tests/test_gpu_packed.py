@@ -73,6 +73,7 @@ LINEAR = [
     # bits, n_tok, c_out, c_in, group, bias, out dtype, z outside [0, qmax]
     (4, 1, 4096, 4096, 128, False, torch.float32, 0),     # 7B q/k/v/o shape
     (4, 1, 1000, 11008, 128, True, torch.float32, 0),     # down_proj width, ragged rows
+    (4, 2, 12289, 1024, 128, True, torch.float32, 0),     # more row pairs than resident waves
     (3, 1, 333, 4096, 128, False, torch.float32, 0),
     (2, 1, 257, 4096, 64, False, torch.float32, 0),
     (4, 3, 129, 512, 32, True, torch.bfloat16, 2),
