@@ -478,8 +478,9 @@ oq_status oq_pack_codes(const uint8_t* codes, int64_t c_out, int64_t c_in, int b
  * == 0; group % 32 == 0 dividing c_in; every pointer 16-byte aligned (else
  * OQ_ERR_INVALID_ARG).  Any n_tok >= 0: below 8 tokens (or for groups other
  * than 128) the vector kernel, sized for decoding, one launch per 8 tokens;
- * from 8 tokens with groups of 128 the matrix-core kernel, one launch per 64
- * tokens; each launch reads the packed weights once.  n_tok == 0 or c_out == 0
+ * from 8 tokens with groups of 128 the matrix-core kernel, one launch per 32
+ * tokens (16 past 32768 input channels); each launch reads the packed weights
+ * once.  n_tok == 0 or c_out == 0
  * is a no-op that accepts NULL pointers.  Products of codes and activations
  * are exact in fp32 and the sums run in a fixed order, so results are
  * reproducible (on matrix cores a token's outputs do not depend on the other
