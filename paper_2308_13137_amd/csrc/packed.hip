@@ -380,6 +380,7 @@ hipError_t allow_lds(const void* kernel) {
 constexpr int PM_THREADS = 512;                // 8 waves share a tile's groups
 constexpr int PM_WAVES = PM_THREADS / 64;
 constexpr int PM_GROUP = 128;
+constexpr int64_t PM_RT2_ROWS = 16384;         // output rows from which a workgroup takes 32
 
 // 16 bytes per lane, global -> LDS (lane l's bytes land at LDS byte address
 // lds + 16 l); inline assembly, so the kernel waits for it (vmcnt) itself.
@@ -407,14 +408,16 @@ OQ_DEV uint32_t lds_addr(const void* p) {
 // dynamic LDS of the kernel: h and z of 16 rows, then two activation blocks
 // per wave and 16-token block, of tpb staged tokens each (the partial-output
 // exchange reuses them)
-size_t mfma_lds(int ntb, int tpb, int64_t c_in) {
-  return size_t(2 * 16) * size_t(c_in / PM_GROUP) * sizeof(float) +
+size_t mfma_lds(int rt, int ntb, int tpb, int64_t c_in) {
+  return size_t(2 * 16 * rt) * size_t(c_in / PM_GROUP) * sizeof(float) +
          size_t(PM_WAVES) * 2 * size_t(ntb) * size_t(tpb) * PM_GROUP * 2;
 }
 
 // NTB blocks of 16 tokens; TPB = 8 stages only the first 8 tokens of the
-// block (batches of at most 8: half the LDS, so more workgroups per CU)
-template <int BITS, int NTB, int TPB>
+// block (batches of at most 8: half the LDS, so more workgroups per CU).  RT
+// tiles of 16 rows per workgroup: each activation fragment read from LDS
+// feeds RT matrix instructions.  A row's arithmetic does not depend on RT.
+template <int BITS, int NTB, int TPB, int RT>
 __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
     const uint16_t* __restrict__ X, int n_tok, int64_t c_in, const uint32_t* __restrict__ packed,
     const float* __restrict__ h, const float* __restrict__ z, const float* __restrict__ bias,
@@ -425,14 +428,16 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
   extern __shared__ float lds[];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int f = lane >> 4, i = lane & 15;
-  const int64_t o0 = int64_t(blockIdx.x) * 16;
+  const int64_t o0 = int64_t(blockIdx.x) * 16 * RT;
   const int ng = int(c_in / PM_GROUP);
   const int64_t runs_row = c_in / 32;
-  float* hz = lds;                             // [2][16][ng]: h, then 128 + z
-  char* xbuf = reinterpret_cast<char*>(lds + 32 * ng) + size_t(wave) * 2 * XB;
-  // this lane's A row (rows past c_out re-read the last row and store nothing)
-  const int64_t arow = min(o0 + i, c_out - 1);
-  const uint32_t* prow = packed + arow * runs_row * BITS;
+  float* hz = lds;                             // [2][16 RT][ng]: h, then 128 + z
+  char* xbuf = reinterpret_cast<char*>(lds + 32 * RT * ng) + size_t(wave) * 2 * XB;
+  // this lane's A rows (rows past c_out re-read the last row and store nothing)
+  const uint32_t* prow[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+    prow[rt] = packed + min(o0 + 16 * rt + i, c_out - 1) * runs_row * BITS;
 
   // copies of group g's activations into buffer b: instruction j of block tb
   // carries tokens 16 tb + 4 j .. + 3 (lane l: token 4 j + l / 16 of the
@@ -454,46 +459,56 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
         }
       }
   };
-  uint32_t wn[BITS];
+  uint32_t wn[RT][BITS];
   if (wave < ng) {
     stage(wave, 0);
-    load_run<BITS>(prow + (4 * int64_t(wave) + f) * BITS, wn);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) load_run<BITS>(prow[rt] + (4 * int64_t(wave) + f) * BITS, wn[rt]);
   }
   {
-    const int64_t nrow = min<int64_t>(16, c_out - o0);
-    for (int e = tid; e < 16 * ng; e += PM_THREADS) {
+    const int64_t nrow = min<int64_t>(16 * RT, c_out - o0);
+    for (int e = tid; e < 16 * RT * ng; e += PM_THREADS) {
       const int64_t src = (o0 + min<int64_t>(e / ng, nrow - 1)) * ng + e % ng;
       hz[e] = h[src];
-      hz[16 * ng + e] = 128.0f + z[src];
+      hz[16 * RT * ng + e] = 128.0f + z[src];
     }
   }
   __syncthreads();
-  f32x4_t y[NTB];
+  f32x4_t y[RT][NTB];
 #pragma unroll
-  for (int tb = 0; tb < NTB; ++tb) y[tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int tb = 0; tb < NTB; ++tb) y[rt][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   int b = 0;
   for (int g = wave; g < ng; g += PM_WAVES, b ^= 1) {
     // group g's copies and codes, issued one turn ago, have landed
     wait_vm0();
-    uint32_t w[BITS];
+    uint32_t w[RT][BITS];
 #pragma unroll
-    for (int k = 0; k < BITS; ++k) w[k] = wn[k];
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int k = 0; k < BITS; ++k) w[rt][k] = wn[rt][k];
     if (g + PM_WAVES < ng) {
       stage(g + PM_WAVES, b ^ 1);
-      load_run<BITS>(prow + (4 * int64_t(g + PM_WAVES) + f) * BITS, wn);
-    }
-    float hr[4], zr[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      hr[r] = hz[(4 * f + r) * ng + g];
-      zr[r] = hz[16 * ng + (4 * f + r) * ng + g];
+      for (int rt = 0; rt < RT; ++rt)
+        load_run<BITS>(prow[rt] + (4 * int64_t(g + PM_WAVES) + f) * BITS, wn[rt]);
     }
-    f32x4_t acc[NTB];
+    float hr[RT][4], zr[RT][4];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        hr[rt][r] = hz[(16 * rt + 4 * f + r) * ng + g];
+        zr[rt][r] = hz[16 * RT * ng + (16 * rt + 4 * f + r) * ng + g];
+      }
+    f32x4_t acc[RT][NTB];
     float xs[NTB];
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
-      acc[tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) acc[rt][tb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       xs[tb] = 0.f;
     }
     // columns past the staged tokens (TPB = 8) re-read tokens 0..7: never stored
@@ -501,18 +516,24 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
     const char* xb = xbuf + b * XB + ti * 256;
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
-      uint32_t a[4];
+      bf16x8_t av[RT];
 #pragma unroll
-      for (int p = 0; p < 4; ++p)
-        a[p] = field<BITS>(w, (8 * m + 2 * p) * BITS) |
-               (field<BITS>(w, (8 * m + 2 * p + 1) * BITS) << 16) | BF16_128_PAIR;
-      const bf16x8_t av = __builtin_bit_cast(bf16x8_t, make_uint4(a[0], a[1], a[2], a[3]));
+      for (int rt = 0; rt < RT; ++rt) {
+        uint32_t a[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p)
+          a[p] = field<BITS>(w[rt], (8 * m + 2 * p) * BITS) |
+                 (field<BITS>(w[rt], (8 * m + 2 * p + 1) * BITS) << 16) | BF16_128_PAIR;
+        av[rt] = __builtin_bit_cast(bf16x8_t, make_uint4(a[0], a[1], a[2], a[3]));
+      }
 #pragma unroll
       for (int tb = 0; tb < NTB; ++tb) {
         const uint4 xv =
             *reinterpret_cast<const uint4*>(xb + tb * XBLK + 16 * ((4 * f + m) ^ ti));
-        acc[tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8_t, xv),
-                                                          acc[tb], 0, 0, 0);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+          acc[rt][tb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              av[rt], __builtin_bit_cast(bf16x8_t, xv), acc[rt][tb], 0, 0, 0);
         xs[tb] = dot2_bf16(xv.x, 0x3f803f80u, xs[tb]);
         xs[tb] = dot2_bf16(xv.y, 0x3f803f80u, xs[tb]);
         xs[tb] = dot2_bf16(xv.z, 0x3f803f80u, xs[tb]);
@@ -526,26 +547,31 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
       s += __shfl_xor(s, 16);
       s += __shfl_xor(s, 32);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) y[tb][r] += hr[r] * (acc[tb][r] - zr[r] * s);
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[rt][tb][r] += hr[rt][r] * (acc[rt][tb][r] - zr[rt][r] * s);
     }
   }
   // every wave's copies have landed (each waited before its last group), so
   // the activation buffers can hold the partial outputs: lane (f, i) holds
-  // rows 4 f + r of the tile for token 16 tb + i
+  // rows 16 rt + 4 f + r of the workgroup for token 16 tb + i
   __syncthreads();
-  float* red = lds + 32 * ng;                  // [PM_WAVES][NTB * 16][17]
+  float* red = lds + 32 * RT * ng;             // [PM_WAVES][RT][NTB * 16][17]
 #pragma unroll
-  for (int tb = 0; tb < NTB; ++tb)
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) red[(wave * NTB * 16 + 16 * tb + i) * 17 + 4 * f + r] = y[tb][r];
+    for (int tb = 0; tb < NTB; ++tb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        red[((wave * RT + rt) * NTB * 16 + 16 * tb + i) * 17 + 4 * f + r] = y[rt][tb][r];
   __syncthreads();
-  for (int e = tid; e < NTB * 16 * 16; e += PM_THREADS) {
-    const int t = e / 16, rr = e % 16;
-    const int64_t o = o0 + rr;
+  for (int e = tid; e < RT * NTB * 16 * 16; e += PM_THREADS) {
+    const int rr = e % 16, t = (e / 16) % (NTB * 16), rt = e / (16 * NTB * 16);
+    const int64_t o = o0 + 16 * rt + rr;
     if (t < n_tok && o < c_out) {
-      float v = red[t * 17 + rr];
+      float v = red[(rt * NTB * 16 + t) * 17 + rr];
 #pragma unroll
-      for (int w8 = 1; w8 < PM_WAVES; ++w8) v += red[(w8 * NTB * 16 + t) * 17 + rr];
+      for (int w8 = 1; w8 < PM_WAVES; ++w8) v += red[((w8 * RT + rt) * NTB * 16 + t) * 17 + rr];
       if (bias) v += bias[o];
       if (y_bf16) static_cast<uint16_t*>(Y)[int64_t(t) * c_out + o] = f2bf(v);
       else static_cast<float*>(Y)[int64_t(t) * c_out + o] = v;
@@ -553,19 +579,29 @@ __global__ __launch_bounds__(PM_THREADS) void packed_mfma_kernel(
   }
 }
 
-template <int BITS, int NTB, int TPB>
-hipError_t launch_mfma(const uint16_t* X, int n_tok, int64_t c_in, const uint8_t* packed,
-                       const float* h, const float* z, const float* bias, int64_t c_out, void* Y,
-                       bool y_bf16, hipStream_t stream) {
-  auto k = packed_mfma_kernel<BITS, NTB, TPB>;
-  const size_t lds = mfma_lds(NTB, TPB, c_in);
+template <int BITS, int NTB, int TPB, int RT>
+hipError_t launch_mfma_rt(const uint16_t* X, int n_tok, int64_t c_in, const uint8_t* packed,
+                          const float* h, const float* z, const float* bias, int64_t c_out, void* Y,
+                          bool y_bf16, hipStream_t stream) {
+  auto k = packed_mfma_kernel<BITS, NTB, TPB, RT>;
+  const size_t lds = mfma_lds(RT, NTB, TPB, c_in);
   if (lds > 64 * 1024) {
     const hipError_t e = allow_lds(reinterpret_cast<const void*>(k));
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(k, dim3(unsigned((c_out + 15) / 16)), dim3(PM_THREADS), lds, stream, X, n_tok,
-                     c_in, reinterpret_cast<const uint32_t*>(packed), h, z, bias, c_out, Y, y_bf16);
+  hipLaunchKernelGGL(k, dim3(unsigned((c_out + 16 * RT - 1) / (16 * RT))), dim3(PM_THREADS), lds,
+                     stream, X, n_tok, c_in, reinterpret_cast<const uint32_t*>(packed), h, z, bias,
+                     c_out, Y, y_bf16);
   return hipGetLastError();
+}
+
+template <int BITS, int NTB, int TPB>
+hipError_t launch_mfma(int rt, const uint16_t* X, int n_tok, int64_t c_in, const uint8_t* packed,
+                       const float* h, const float* z, const float* bias, int64_t c_out, void* Y,
+                       bool y_bf16, hipStream_t stream) {
+  if (rt == 2)
+    return launch_mfma_rt<BITS, NTB, TPB, 2>(X, n_tok, c_in, packed, h, z, bias, c_out, Y, y_bf16, stream);
+  return launch_mfma_rt<BITS, NTB, TPB, 1>(X, n_tok, c_in, packed, h, z, bias, c_out, Y, y_bf16, stream);
 }
 
 template <int BITS, int NT>
@@ -591,15 +627,18 @@ hipError_t linear_bits(const uint16_t* X, int64_t n_tok, int64_t c_in, const uin
   if (n_tok >= PM_MIN_TOKENS && group == PM_GROUP) {
     // matrix cores: launches of up to 32 tokens, or 16 where two blocks
     // of 32 tokens exceed LDS; batches of at most 8 stage 8 tokens per group
-    const int most = mfma_lds(2, 16, c_in) <= PL_LDS_MAX ? 32 : 16;
+    // two row tiles per workgroup where that still leaves two workgroups or
+    // more per CU (the shape alone decides, so every batch size sums alike)
+    const int rt = c_out >= PM_RT2_ROWS && mfma_lds(2, 1, 16, c_in) <= PL_LDS_MAX ? 2 : 1;
+    const int most = mfma_lds(rt, 2, 16, c_in) <= PL_LDS_MAX ? 32 : 16;
     for (int64_t t0 = 0; t0 < n_tok;) {
       const int take = int(std::min<int64_t>(n_tok - t0, most));
       const uint16_t* x = X + t0 * c_in;
       void* y = static_cast<char*>(Y) + size_t(t0) * size_t(c_out) * es;
       const hipError_t e =
-          take <= 8    ? launch_mfma<BITS, 1, 8>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream)
-          : take <= 16 ? launch_mfma<BITS, 1, 16>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream)
-                       : launch_mfma<BITS, 2, 16>(x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
+          take <= 8    ? launch_mfma<BITS, 1, 8>(rt, x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream)
+          : take <= 16 ? launch_mfma<BITS, 1, 16>(rt, x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream)
+                       : launch_mfma<BITS, 2, 16>(rt, x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream);
       if (e != hipSuccess) return e;
       t0 += take;
     }

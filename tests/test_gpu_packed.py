@@ -106,6 +106,10 @@ LINEAR = [
     (4, 8, 4200, 1024, 128, False, torch.float32, 0),
     (5, 12, 4113, 512, 128, True, torch.bfloat16, 1),
     (4, 40, 4352, 640, 128, True, torch.float32, 0),
+    # 16,384 rows or more: two 16-row tiles per workgroup (ragged last one)
+    (4, 12, 16400, 512, 128, True, torch.bfloat16, 0),
+    (3, 40, 16384, 1024, 128, False, torch.float32, 1),
+    (5, 8, 16424, 384, 128, True, torch.float32, 0),
 ]
 
 
@@ -139,10 +143,13 @@ def test_packed_linear_empty_and_reproducible():
         assert torch.equal(oq.packed_linear(Xd[t:t + 1], Pd, 4, 128, hd, zd)[0], a[t])
 
 
-def test_matrix_core_batches_give_each_token_the_same_bits():
+@pytest.mark.parametrize("c_out", [260, 16400])
+def test_matrix_core_batches_give_each_token_the_same_bits(c_out):
     """On matrix cores a token's outputs depend only on its own column: a
-    token gives the same bits in batches of 8, 20 and 64."""
-    q, h, z, X, B = make_linear(12, 4, 64, 260, 4096, 128, True)
+    token gives the same bits in batches of 8, 20 and 64.  From 16,384 rows a
+    workgroup takes two 16-row tiles; its rows give the same bits as the same
+    rows in a launch of one tile per workgroup."""
+    q, h, z, X, B = make_linear(12, 4, 64, c_out, 4096, 128, True)
     Xd, Pd, hd, zd, Bd = (to_dev(X, torch.bfloat16), to_dev(o_pack(q, 4)), to_dev(h), to_dev(z),
                           to_dev(B))
     full = oq.packed_linear(Xd, Pd, 4, 128, hd, zd, Bd)
@@ -151,6 +158,10 @@ def test_matrix_core_batches_give_each_token_the_same_bits():
     torch.cuda.synchronize()
     assert torch.equal(a, full[:8])
     assert torch.equal(b, full[30:50])
+    if c_out > 260:
+        head = oq.packed_linear(Xd, Pd[:260], 4, 128, hd[:260], zd[:260], Bd[:260])
+        torch.cuda.synchronize()
+        assert torch.equal(head, full[:, :260])
 
 
 def test_gate_up_stack_full_size_sampled_rows():
