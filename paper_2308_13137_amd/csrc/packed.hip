@@ -359,7 +359,8 @@ hipError_t allow_lds(const void* kernel) {
 
 // ------------------------------------------------------------------ the linear on matrix cores
 // For batches of 8 or more tokens and groups of 128 codes.  A workgroup owns
-// 16 output rows; its eight waves take the row's groups g = wave, wave + 8, ...
+// 16 output rows (or two tiles of 16, RT = 2); its eight waves take the rows'
+// groups g = wave, wave + 8, ...
 // For group g a lane (f, i) (f = lane / 16, i = lane % 16) loads run 4 g + f
 // of row i (BITS dwords); matrix instruction m (0..3) of the group multiplies
 // codes 8 m .. 8 m + 7 of each lane's run, widened to 128 + q in bf16 (exact),
