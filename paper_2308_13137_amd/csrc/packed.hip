@@ -628,14 +628,16 @@ hipError_t linear_bits(const uint16_t* X, int64_t n_tok, int64_t c_in, const uin
   if (n_tok >= PM_MIN_TOKENS && group == PM_GROUP) {
     // matrix cores: launches of up to 32 tokens, or 16 where two blocks
     // of 32 tokens exceed LDS; batches of at most 8 stage 8 tokens per group
-    // two row tiles per workgroup where that still leaves two workgroups or
-    // more per CU (the shape alone decides, so every batch size sums alike)
-    const int rt = c_out >= PM_RT2_ROWS && mfma_lds(2, 1, 16, c_in) <= PL_LDS_MAX ? 2 : 1;
-    const int most = mfma_lds(rt, 2, 16, c_in) <= PL_LDS_MAX ? 32 : 16;
+    const int most = mfma_lds(1, 2, 16, c_in) <= PL_LDS_MAX ? 32 : 16;
     for (int64_t t0 = 0; t0 < n_tok;) {
       const int take = int(std::min<int64_t>(n_tok - t0, most));
       const uint16_t* x = X + t0 * c_in;
       void* y = static_cast<char*>(Y) + size_t(t0) * size_t(c_out) * es;
+      // two row tiles per workgroup from 16384 rows, and from 8192 rows for
+      // two token blocks, where LDS allows (a row's sums do not depend on it)
+      const int ntb = take > 16 ? 2 : 1, tpb = take > 8 ? 16 : 8;
+      const bool two = c_out >= PM_RT2_ROWS || (c_out >= PM_RT2_ROWS / 2 && ntb == 2);
+      const int rt = two && mfma_lds(2, ntb, tpb, c_in) <= PL_LDS_MAX ? 2 : 1;
       const hipError_t e =
           take <= 8    ? launch_mfma<BITS, 1, 8>(rt, x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream)
           : take <= 16 ? launch_mfma<BITS, 1, 16>(rt, x, take, c_in, packed, h, z, bias, c_out, y, y_bf16, stream)

@@ -89,7 +89,7 @@ LINEAR = [
     (3, 1, 33, 11008, 11008, False, torch.float32, 0),
     # the widest input: one token per launch fits LDS, so 3 tokens are 3 launches
     (4, 3, 7, 65536, 128, False, torch.float32, 0),
-    # matrix cores (8+ tokens, groups of 128): 16- and 32-token launches,
+    # matrix cores (8+ tokens, groups of 128): 8-, 16- and 32-token launches,
     # 70 = 64 + 6 tokens, ragged rows, the 7B shapes, every code width
     (4, 16, 4096, 4096, 128, True, torch.float32, 0),
     (4, 64, 1000, 11008, 128, False, torch.float32, 0),
@@ -110,6 +110,7 @@ LINEAR = [
     (4, 12, 16400, 512, 128, True, torch.bfloat16, 0),
     (3, 40, 16384, 1024, 128, False, torch.float32, 1),
     (5, 8, 16424, 384, 128, True, torch.float32, 0),
+    (4, 24, 9000, 256, 128, True, torch.float32, 0),      # from 8,192 rows at 17-32 tokens
 ]
 
 
@@ -143,12 +144,13 @@ def test_packed_linear_empty_and_reproducible():
         assert torch.equal(oq.packed_linear(Xd[t:t + 1], Pd, 4, 128, hd, zd)[0], a[t])
 
 
-@pytest.mark.parametrize("c_out", [260, 16400])
+@pytest.mark.parametrize("c_out", [260, 9000, 16400])
 def test_matrix_core_batches_give_each_token_the_same_bits(c_out):
     """On matrix cores a token's outputs depend only on its own column: a
-    token gives the same bits in batches of 8, 20 and 64.  From 16,384 rows a
-    workgroup takes two 16-row tiles; its rows give the same bits as the same
-    rows in a launch of one tile per workgroup."""
+    token gives the same bits in batches of 8, 20 and 64.  From 16,384 rows
+    (from 8,192 in launches of 17-32 tokens) a workgroup takes two 16-row
+    tiles; its rows give the same bits as the same rows in a launch of one
+    tile per workgroup."""
     q, h, z, X, B = make_linear(12, 4, 64, c_out, 4096, 128, True)
     Xd, Pd, hd, zd, Bd = (to_dev(X, torch.bfloat16), to_dev(o_pack(q, 4)), to_dev(h), to_dev(z),
                           to_dev(B))
