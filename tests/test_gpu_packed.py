@@ -199,13 +199,15 @@ def test_pack_and_linear_agree_with_lwc_dequantised_weight():
     assert torch.all((Y.double() - ref).abs() <= 4e-6 * scale)
 
 
-def test_packed_linear_graph_replays_match_eager():
+@pytest.mark.parametrize("n_tok", [2, 12, 24])
+def test_packed_linear_graph_replays_match_eager(n_tok):
     # a decode loop replays the same launches from a HIP graph: every replay,
     # with eager work and new activations between replays, matches eager runs
-    q, h, z, X, B = make_linear(31, 4, 2, 700, 4096, 128, True)
+    # (2 tokens: the vector kernel; 12 and 24: the matrix-core kernel)
+    q, h, z, X, B = make_linear(31, 4, n_tok, 700, 4096, 128, True)
     Xd, Pd, hd, zd, Bd = (to_dev(X, torch.bfloat16), to_dev(o_pack(q, 4)), to_dev(h), to_dev(z),
                           to_dev(B))
-    Y = torch.empty((2, 700), device=DEV)
+    Y = torch.empty((n_tok, 700), device=DEV)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -218,7 +220,7 @@ def test_packed_linear_graph_replays_match_eager():
     rng = np.random.default_rng(32)
     for i in range(4):
         if i:
-            Xd.copy_(to_dev(bf16_round(rng.standard_normal((2, 4096)).astype(np.float32)),
+            Xd.copy_(to_dev(bf16_round(rng.standard_normal((n_tok, 4096)).astype(np.float32)),
                             torch.bfloat16))
         want = oq.packed_linear(Xd, Pd, 4, 128, hd, zd, Bd)
         Y.zero_()
