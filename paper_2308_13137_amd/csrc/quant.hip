@@ -1032,13 +1032,13 @@ __global__ __launch_bounds__(NT) void act_fwd_kernel(
 // One barrier per block reduction (lds_barrier): the LDS slots of the two
 // reductions alternate, and a wave reads each slot before it arrives at the
 // other reduction's barrier, so no second barrier guards the rewrite.
-template <typename TX, int KC>
-__global__ __launch_bounds__(NT) void act_bwd_kernel(
+template <typename TX, int KC, int NTB = NT>
+__global__ __launch_bounds__(NTB) void act_bwd_kernel(
     const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
     const float* __restrict__ delta, int R, const float* __restrict__ dXdq,
     float* __restrict__ dXt, float* __restrict__ p_sx, float* __restrict__ p_s1, bool sym) {
-  __shared__ MinMax shm[NT / 64];
-  __shared__ float2 shs[NT / 64];
+  __shared__ MinMax shm[NTB / 64];
+  __shared__ float2 shs[NTB / 64];
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
   const int cpr = int(C / 8);
@@ -1048,7 +1048,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
   float rs[KC][8], dl[KC][8], asx[KC][8], as1[KC][8];
 #pragma unroll
   for (int k = 0; k < KC; ++k) {
-    const int j = tid + NT * k;
+    const int j = tid + NTB * k;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       rs[k][e] = 1.0f;
@@ -1076,7 +1076,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
   auto issue = [&](int64_t row) {
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
-      const int j = tid + NT * k;
+      const int j = tid + NTB * k;
       if (j < cpr) {
         xn[k].load(X + row * C + 8 * j);
         load8(dXdq + row * C + 8 * j, gn[k]);
@@ -1102,7 +1102,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
     } else {
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
-        const int j = tid + NT * k;
+        const int j = tid + NTB * k;
         if (j < cpr) {
           load8(X + row * C + 8 * j, v[k]);
           load8(dXdq + row * C + 8 * j, g[k]);
@@ -1111,7 +1111,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
     }
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
-      const int j = tid + NT * k;
+      const int j = tid + NTB * k;
       if (j < cpr) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -1126,7 +1126,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
       lds_barrier();
       st = shm[0];
 #pragma unroll
-      for (int w = 1; w < NT / 64; ++w) {
+      for (int w = 1; w < NTB / 64; ++w) {
         sel_max(st.mx, st.imx, shm[w].mx, shm[w].imx);
         sel_min(st.mn, st.imn, shm[w].mn, shm[w].imn);
       }
@@ -1138,7 +1138,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
       bool mk[KC][8];
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
-        const int j = tid + NT * k;
+        const int j = tid + NTB * k;
         if (j < cpr) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -1157,7 +1157,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
       lds_barrier();
       sums = shs[0];
 #pragma unroll
-      for (int w = 1; w < NT / 64; ++w) {
+      for (int w = 1; w < NTB / 64; ++w) {
         sums.x += shs[w].x;
         sums.y += shs[w].y;
       }
@@ -1167,7 +1167,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
       const float dab = sym ? (p.hclamp ? 0.0f : sgn * div_rn(sums.x, qs)) : 0.0f;
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
-        const int j = tid + NT * k;
+        const int j = tid + NTB * k;
         if (j < cpr) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -1186,7 +1186,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
     }
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
-      const int j = tid + NT * k;
+      const int j = tid + NTB * k;
       if (j < cpr) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -1199,7 +1199,7 @@ __global__ __launch_bounds__(NT) void act_bwd_kernel(
   }
 #pragma unroll
   for (int k = 0; k < KC; ++k) {
-    const int j = tid + NT * k;
+    const int j = tid + NTB * k;
     if (j < cpr) {
       if (p_sx) store8(p_sx + int64_t(blockIdx.x) * C + 8 * j, asx[k]);
       if (p_s1) store8(p_s1 + int64_t(blockIdx.x) * C + 8 * j, as1[k]);
@@ -1597,9 +1597,17 @@ hipError_t act_bwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, c
   auto go = [&](auto tx, auto kcc) {
     using TX = decltype(tx);
     constexpr int KCc = decltype(kcc)::value;
-    hipLaunchKernelGGL((act_bwd_kernel<TX, KCc>), grid, dim3(NT), 0, st,
-                       static_cast<const TX*>(X), T, C, bits, s, delta, R, dXdq, dXt, p_sx, p_s1,
-                       sym && bits < 16);
+    if constexpr (KCc >= 8) {
+      // wide rows: twice the threads per row, half the chunks per thread
+      // (256 threads with 8 chunks each leave one wave per SIMD)
+      hipLaunchKernelGGL((act_bwd_kernel<TX, KCc / 2, 2 * NT>), grid, dim3(2 * NT), 0, st,
+                         static_cast<const TX*>(X), T, C, bits, s, delta, R, dXdq, dXt, p_sx, p_s1,
+                         sym && bits < 16);
+    } else {
+      hipLaunchKernelGGL((act_bwd_kernel<TX, KCc>), grid, dim3(NT), 0, st,
+                         static_cast<const TX*>(X), T, C, bits, s, delta, R, dXdq, dXt, p_sx, p_s1,
+                         sym && bits < 16);
+    }
   };
   auto by_kc = [&](auto tx) -> hipError_t {
     OQ_KC_SWITCH(kc, go(tx, std::integral_constant<int, KC>{}))

@@ -196,6 +196,8 @@ ACT_CASES = [
     # several rows per workgroup (T > 2048), so the backward's row pipeline
     # runs; a ragged 257-chunk row and a plain 4096-channel one
     dict(T=4100, C=2056, bits=4, let=True), dict(T=3000, C=4096, bits=3, let=False),
+    # rows wider than 8,192 channels: the backward runs 512 threads per row
+    dict(T=1600, C=11008, bits=4, let=False, bf16=False), dict(T=12, C=20480, bits=6, let=True),
 ]
 
 
