@@ -40,6 +40,7 @@ OQ_DEV void minmax_add(MinMax& s, float v, int idx) {
 }
 
 // Whole-workgroup (max, argmax, min, argmin); every thread gets the result.
+template <int NTB = NT>
 OQ_DEV MinMax block_minmax(MinMax v, MinMax* sh) {
   group_minmax<64>(v.mx, v.imx, v.mn, v.imn);
   const int wave = threadIdx.x >> 6;
@@ -48,7 +49,7 @@ OQ_DEV MinMax block_minmax(MinMax v, MinMax* sh) {
   __syncthreads();
   MinMax r = sh[0];
 #pragma unroll
-  for (int w = 1; w < NT / 64; ++w) {
+  for (int w = 1; w < NTB / 64; ++w) {
     sel_max(r.mx, r.imx, sh[w].mx, sh[w].imx);
     sel_min(r.mn, r.imn, sh[w].mn, sh[w].imn);
   }
@@ -945,12 +946,12 @@ __global__ __launch_bounds__(NT) void lwc_fwd_row_kernel(
 
 // ------------------------------------------------------------------ activation forward
 // x~ = (x - delta) * (1/s); per token row Eq. 2 with gamma = beta = 1.
-template <typename TX, typename TQ, int KC>
-__global__ __launch_bounds__(NT) void act_fwd_kernel(
+template <typename TX, typename TQ, int KC, int NTB = NT>
+__global__ __launch_bounds__(NTB) void act_fwd_kernel(
     const TX* __restrict__ X, int64_t T, int64_t C, int bits, const float* __restrict__ s,
     const float* __restrict__ delta, int R, TQ* __restrict__ xdq, uint8_t* __restrict__ codes,
     float* __restrict__ hout, float* __restrict__ zout, bool sym) {
-  __shared__ MinMax shm[NT / 64];
+  __shared__ MinMax shm[NTB / 64];
   const int tid = threadIdx.x;
   const int cpr = int(C / 8);
   const bool quant = bits < 16;
@@ -959,7 +960,7 @@ __global__ __launch_bounds__(NT) void act_fwd_kernel(
   float rs[KC][8], dl[KC][8];
 #pragma unroll
   for (int k = 0; k < KC; ++k) {
-    const int j = tid + NT * k;
+    const int j = tid + NTB * k;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       rs[k][e] = 1.0f;
@@ -982,7 +983,7 @@ __global__ __launch_bounds__(NT) void act_fwd_kernel(
     MinMax st = minmax_init();
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
-      const int j = tid + NT * k;
+      const int j = tid + NTB * k;
       if (j < cpr) {
         load8(X + row * C + 8 * j, v[k]);
 #pragma unroll
@@ -995,19 +996,19 @@ __global__ __launch_bounds__(NT) void act_fwd_kernel(
     if (!quant) {
 #pragma unroll
       for (int k = 0; k < KC; ++k) {
-        const int j = tid + NT * k;
+        const int j = tid + NTB * k;
         if (j < cpr && xdq) store8(xdq + row * C + 8 * j, v[k]);
       }
       continue;
     }
-    st = block_minmax(st, shm);
+    st = block_minmax<NTB>(st, shm);
     int iab;
     float sgn;
     const QParams p = sym ? make_sym_qparams(st.mx, st.imx, st.mn, st.imn, qs, iab, sgn)
                           : make_qparams(st.mx, st.mn, 1.0f, 1.0f, qmax);
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
-      const int j = tid + NT * k;
+      const int j = tid + NTB * k;
       if (j < cpr) {
         float q[8], d[8];
 #pragma unroll
@@ -1565,9 +1566,16 @@ hipError_t act_fwd(const void* X, bool x_bf16, int64_t T, int64_t C, int bits, c
     using TX = decltype(tx);
     using TQ = decltype(tq);
     constexpr int KCc = decltype(kcc)::value;
-    hipLaunchKernelGGL((act_fwd_kernel<TX, TQ, KCc>), grid, dim3(NT), 0, st,
-                       static_cast<const TX*>(X), T, C, bits, s, delta, R, static_cast<TQ*>(X_dq),
-                       codes, h, z, sym);
+    if constexpr (KCc >= 8) {
+      // wide rows: twice the threads per row, half the chunks per thread
+      hipLaunchKernelGGL((act_fwd_kernel<TX, TQ, KCc / 2, 2 * NT>), grid, dim3(2 * NT), 0, st,
+                         static_cast<const TX*>(X), T, C, bits, s, delta, R, static_cast<TQ*>(X_dq),
+                         codes, h, z, sym);
+    } else {
+      hipLaunchKernelGGL((act_fwd_kernel<TX, TQ, KCc>), grid, dim3(NT), 0, st,
+                         static_cast<const TX*>(X), T, C, bits, s, delta, R, static_cast<TQ*>(X_dq),
+                         codes, h, z, sym);
+    }
   };
   auto by_kc = [&](auto tx, auto tq) -> hipError_t {
     OQ_KC_SWITCH(kc, go(tx, tq, std::integral_constant<int, KC>{}))
