@@ -406,9 +406,9 @@ OQ_DEV uint32_t lds_addr(const void* p) {
       (__attribute__((address_space(3))) const char*)(p)));
 }
 
-// dynamic LDS of the kernel: h and z of 16 rows, then two activation blocks
-// per wave and 16-token block, of tpb staged tokens each (the partial-output
-// exchange reuses them)
+// dynamic LDS of the kernel: h and z of the workgroup's 16 rt rows, then two
+// activation blocks per wave and 16-token block, of tpb staged tokens each
+// (the partial-output exchange reuses them)
 size_t mfma_lds(int rt, int ntb, int tpb, int64_t c_in) {
   return size_t(2 * 16 * rt) * size_t(c_in / PM_GROUP) * sizeof(float) +
          size_t(PM_WAVES) * 2 * size_t(ntb) * size_t(tpb) * PM_GROUP * 2;
