@@ -111,6 +111,9 @@ LINEAR = [
     (3, 40, 16384, 1024, 128, False, torch.float32, 1),
     (5, 8, 16424, 384, 128, True, torch.float32, 0),
     (4, 24, 9000, 256, 128, True, torch.float32, 0),      # from 8,192 rows at 17-32 tokens
+    (2, 20, 16400, 256, 128, False, torch.bfloat16, 1),
+    (6, 8, 16390, 128, 128, True, torch.float32, 0),
+    (7, 33, 16384, 384, 128, False, torch.float32, 0),
 ]
 
 
